@@ -1,0 +1,421 @@
+"""Plain fp64 CPU oracle for the Gaunt Tensor Product (Luo et al., ICLR 2024,
+"Enabling efficient equivariant operations in the Fourier basis via Gaunt
+Tensor Products").
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path may import, call or
+execute this module: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` use it.  It shares no code, table or
+constant generator with the HIP library; the only thing both sides consume is
+the seeded input generator in ``paper_2401_10216_amd/inputs.py`` (which does no
+arithmetic of the method).
+
+Everything is numpy float64 and written to be checked against the paper by eye:
+
+* real spherical harmonics (Appendix "Spherical Harmonics"), z polar axis, no
+  Condon-Shortley phase, index ``i = l*l + l + m``;
+* real Gaunt coefficients (Sec. 3.1, eq. ``equivalence-wigner-eckart``) by
+  Gauss-Legendre (in cos theta) x uniform-phi quadrature, which is exact for the
+  polynomial degree of a triple product;
+* the Gaunt tensor product itself (Sec. 3.1, eq. ``tp-eq-mul``) as a dense
+  contraction of the Gaunt tensor ("mode A"), and as the pointwise product of
+  the two spherical functions on an exact quadrature grid ("mode B");
+* the three stages of Sec. 3.2 individually: SH -> 2D Fourier (eq. ``sh-fs``),
+  the 2D convolution (eq. ``2D-conv``) and Fourier -> SH (eq. ``fs-sh``), each
+  from its plain definition;
+* the many-body self product (Sec. 3.3 and Appendix "Implementation
+  Details", generalized Gaunt coefficients), stepwise and fused;
+* real Wigner-D matrices by quadrature, for the equivariance pin (Appendix D).
+
+Every function is pinned by ``tests/test_oracle.py`` against closed forms,
+library routines (scipy spherical harmonics, sympy real Gaunt, numpy
+Gauss-Legendre, scipy convolve2d), the Racah formula, brute force and
+equivariance.  Nothing here is "parity unpinned".
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+FOUR_PI = 4.0 * math.pi
+
+
+def nsh(L: int) -> int:
+    """Number of real SH coefficients up to degree L: (L+1)^2 (Sec. 2)."""
+    return (L + 1) * (L + 1)
+
+
+# ---------------------------------------------------------------------------
+# Quadrature
+# ---------------------------------------------------------------------------
+
+def gauss_legendre(n: int):
+    """Gauss-Legendre nodes/weights on [-1, 1] by Newton iteration on P_n.
+
+    Textbook construction (Golub & Welsch give the same rule); exact for
+    polynomials of degree <= 2n-1.
+    """
+    if n < 1:
+        raise ValueError("n >= 1")
+    k = np.arange(1, n + 1, dtype=np.float64)
+    x = np.cos(math.pi * (k - 0.25) / (n + 0.5))  # Tricomi initial guess
+    for _ in range(100):
+        p0 = np.ones_like(x)
+        p1 = x.copy()
+        for j in range(2, n + 1):
+            p0, p1 = p1, ((2 * j - 1) * x * p1 - (j - 1) * p0) / j
+        if n == 1:
+            p0, p1 = np.ones_like(x), x.copy()
+        # derivative of P_n from P_n and P_{n-1}
+        dp = n * (x * p1 - p0) / (x * x - 1.0)
+        dx = p1 / dp
+        x = x - dx
+        if np.max(np.abs(dx)) < 1e-16:
+            break
+    p0 = np.ones_like(x)
+    p1 = x.copy()
+    for j in range(2, n + 1):
+        p0, p1 = p1, ((2 * j - 1) * x * p1 - (j - 1) * p0) / j
+    if n == 1:
+        p0 = np.ones_like(x)
+    dp = n * (x * p1 - p0) / (x * x - 1.0)
+    w = 2.0 / ((1.0 - x * x) * dp * dp)
+    order = np.argsort(x)
+    return x[order], w[order]
+
+
+def sphere_quadrature(degree: int):
+    """Product rule on S^2 exact for every polynomial of total degree <= degree.
+
+    Gauss-Legendre in t = cos(theta) with ceil((degree+1)/2) nodes and a
+    uniform phi grid with degree+1 points.  Returns flat (theta, phi, weight)
+    arrays whose weights sum to 4*pi.
+    """
+    nt = max(1, (degree + 2) // 2)
+    npf = degree + 1
+    t, wt = gauss_legendre(nt)
+    phi = 2.0 * math.pi * np.arange(npf) / npf
+    th = np.arccos(t)
+    TH, PH = np.meshgrid(th, phi, indexing="ij")
+    W = np.outer(wt, np.full(npf, 2.0 * math.pi / npf))
+    return TH.ravel(), PH.ravel(), W.ravel()
+
+
+# ---------------------------------------------------------------------------
+# Real spherical harmonics
+# ---------------------------------------------------------------------------
+
+def real_sh(lmax: int, theta, phi) -> np.ndarray:
+    """Orthonormal real spherical harmonics Y_l^m(theta, phi), l <= lmax.
+
+    Convention (the paper leaves it open, Appendix "Spherical Harmonics"):
+    z is the polar axis, no Condon-Shortley phase,
+      Y_l^0  = Q_l^0(cos th),
+      Y_l^m  = sqrt(2) Q_l^m(cos th) cos(m phi),  m > 0,
+      Y_l^-m = sqrt(2) Q_l^m(cos th) sin(m phi),  m > 0,
+    with Q_l^m = sqrt((2l+1)/(4 pi) (l-m)!/(l+m)!) P_l^m the normalised
+    associated Legendre function.  So Y_1 = sqrt(3/(4 pi)) (y, z, x).
+    Output index i = l*l + l + m (m = -l..l), last axis.
+    """
+    theta = np.asarray(theta, dtype=np.float64)
+    phi = np.asarray(phi, dtype=np.float64)
+    shape = np.broadcast(theta, phi).shape
+    theta = np.broadcast_to(theta, shape)
+    phi = np.broadcast_to(phi, shape)
+    t = np.cos(theta)
+    s = np.sin(theta)
+    out = np.zeros(shape + (nsh(lmax),), dtype=np.float64)
+    sqrt2 = math.sqrt(2.0)
+
+    def store(l, m, q):
+        if m == 0:
+            out[..., l * l + l] = q
+        else:
+            out[..., l * l + l + m] = sqrt2 * q * np.cos(m * phi)
+            out[..., l * l + l - m] = sqrt2 * q * np.sin(m * phi)
+
+    qmm = np.full(shape, math.sqrt(1.0 / FOUR_PI))
+    for m in range(lmax + 1):
+        if m > 0:
+            qmm = qmm * math.sqrt((2.0 * m + 1.0) / (2.0 * m)) * s
+        store(m, m, qmm)
+        if m + 1 > lmax:
+            continue
+        q_prev2 = qmm
+        q_prev1 = math.sqrt(2.0 * m + 3.0) * t * qmm
+        store(m + 1, m, q_prev1)
+        for l in range(m + 2, lmax + 1):
+            a = math.sqrt((4.0 * l * l - 1.0) / (l * l - m * m))
+            b = math.sqrt(((l - 1.0) ** 2 - m * m) / (4.0 * (l - 1.0) ** 2 - 1.0))
+            q = a * (t * q_prev1 - b * q_prev2)
+            store(l, m, q)
+            q_prev2, q_prev1 = q_prev1, q
+    return out
+
+
+def real_sh_xyz(lmax: int, r) -> np.ndarray:
+    """Real SH of unit vectors r[..., 3] (x, y, z) in the convention above."""
+    r = np.asarray(r, dtype=np.float64)
+    n = np.linalg.norm(r, axis=-1)
+    z = np.clip(r[..., 2] / n, -1.0, 1.0)
+    theta = np.arccos(z)
+    phi = np.arctan2(r[..., 1], r[..., 0])
+    return real_sh(lmax, theta, phi)
+
+
+# ---------------------------------------------------------------------------
+# Gaunt coefficients and the Gaunt tensor product (Sec. 3.1)
+# ---------------------------------------------------------------------------
+
+def gaunt_tensor(L1: int, L2: int, L3: int) -> np.ndarray:
+    """Dense real Gaunt tensor G[i, j, k] = int Y_i Y_j Y_k dOmega.
+
+    i runs over degree <= L1, j over <= L2, k over <= L3.  The quadrature of
+    ``sphere_quadrature(L1+L2+L3)`` is exact: a triple product of real SH with
+    a non-vanishing phi integral is a polynomial of degree l1+l2+l3 in (x,y,z).
+    """
+    th, ph, w = sphere_quadrature(L1 + L2 + L3)
+    Y = real_sh(max(L1, L2, L3), th, ph)
+    Y1 = Y[:, : nsh(L1)]
+    Y2 = Y[:, : nsh(L2)]
+    Y3w = Y[:, : nsh(L3)] * w[:, None]
+    G = np.empty((nsh(L1), nsh(L2), nsh(L3)), dtype=np.float64)
+    for i in range(nsh(L1)):
+        G[i] = (Y1[:, i : i + 1] * Y2).T @ Y3w
+    return G
+
+
+_GAUNT_CACHE: dict = {}
+
+
+def _gaunt_cached(L1, L2, L3):
+    key = (L1, L2, L3)
+    if key not in _GAUNT_CACHE:
+        _GAUNT_CACHE[key] = gaunt_tensor(L1, L2, L3)
+    return _GAUNT_CACHE[key]
+
+
+def gtp(x1, x2, L1: int, L2: int, Lout: int, chunk: int = 2048) -> np.ndarray:
+    """Gaunt tensor product, mode A (eq. tp-eq-mul, second line).
+
+    y[n, k] = sum_{i,j} G[i, j, k] x1[n, i] x2[n, j], contracted densely over
+    every (i, j, k) of the Gaunt tensor.  x1[..., (L1+1)^2], x2[..., (L2+1)^2]
+    with identical leading shape; returns y[..., (Lout+1)^2] in float64.
+    Output degrees above L1+L2 come out as (quadrature-exact) zeros.
+    """
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    lead = x1.shape[:-1]
+    assert x1.shape[-1] == nsh(L1) and x2.shape[-1] == nsh(L2)
+    assert x2.shape[:-1] == lead
+    a = x1.reshape(-1, nsh(L1))
+    b = x2.reshape(-1, nsh(L2))
+    G = _gaunt_cached(L1, L2, Lout)
+    Gm = G.reshape(nsh(L1), nsh(L2) * nsh(Lout))
+    y = np.empty((a.shape[0], nsh(Lout)), dtype=np.float64)
+    for s in range(0, a.shape[0], chunk):
+        T = (a[s : s + chunk] @ Gm).reshape(-1, nsh(L2), nsh(Lout))
+        y[s : s + chunk] = np.einsum("nj,njk->nk", b[s : s + chunk], T)
+    return y.reshape(lead + (nsh(Lout),))
+
+
+def gtp_grid(x1, x2, L1: int, L2: int, Lout: int, chunk: int = 4096) -> np.ndarray:
+    """Gaunt tensor product, mode B (eq. tp-eq-mul, last line).
+
+    Evaluates F1 = sum x1 Y and F2 = sum x2 Y on a quadrature grid exact for
+    degree L1+L2+Lout, multiplies them pointwise and projects onto Y_l^m,
+    l <= Lout.  Exact (up to rounding) and cheaper than mode A at large L.
+    """
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    lead = x1.shape[:-1]
+    a = x1.reshape(-1, nsh(L1))
+    b = x2.reshape(-1, nsh(L2))
+    th, ph, w = sphere_quadrature(L1 + L2 + Lout)
+    Y = real_sh(max(L1, L2, Lout), th, ph)
+    Y1 = Y[:, : nsh(L1)]
+    Y2 = Y[:, : nsh(L2)]
+    Y3w = Y[:, : nsh(Lout)] * w[:, None]
+    y = np.empty((a.shape[0], nsh(Lout)), dtype=np.float64)
+    for s in range(0, a.shape[0], chunk):
+        F = (a[s : s + chunk] @ Y1.T) * (b[s : s + chunk] @ Y2.T)
+        y[s : s + chunk] = F @ Y3w
+    return y.reshape(lead + (nsh(Lout),))
+
+
+# ---------------------------------------------------------------------------
+# The three stages of Sec. 3.2, each from its plain definition
+# ---------------------------------------------------------------------------
+
+def sh2fourier(x, L: int) -> np.ndarray:
+    """SH coefficients -> 2D Fourier coefficients x*_{u,v} (eq. sh-fs).
+
+    The function F = sum x Y is extended from theta in [0, pi] to the torus
+    theta in [-pi, pi) by F(-theta, phi) := F(theta, phi + pi) (the double
+    Fourier sphere; the paper leaves the theta range open).  The extension is a
+    trigonometric polynomial with |u|, |v| <= L, so the 2D DFT of its samples on
+    a (2L+2) x (2L+2) torus grid returns its Fourier coefficients exactly.
+
+    x[..., (L+1)^2] -> complex grid[..., 2L+1, 2L+1], grid[..., u+L, v+L].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    lead = x.shape[:-1]
+    a = x.reshape(-1, nsh(L))
+    N = 2 * L + 2
+    th = -math.pi + 2.0 * math.pi * np.arange(N) / N
+    ph = 2.0 * math.pi * np.arange(N) / N
+    TH, PH = np.meshgrid(th, ph, indexing="ij")
+    neg = TH < 0
+    Y = real_sh(L, np.abs(TH), np.where(neg, PH + math.pi, PH))  # [N, N, K]
+    F = np.einsum("nk,abk->nab", a, Y)  # samples on the torus
+    u = np.arange(-L, L + 1)
+    Eth = np.exp(-1j * np.outer(u, th)) / N  # [2L+1, N]
+    Eph = np.exp(-1j * np.outer(ph, u)) / N  # [N, 2L+1]
+    g = np.einsum("ua,nab,bv->nuv", Eth, F, Eph)
+    return g.reshape(lead + (2 * L + 1, 2 * L + 1))
+
+
+def fourier_conv(g1, g2) -> np.ndarray:
+    """2D convolution of Fourier grids (eq. 2D-conv), written out literally:
+    f3[u1+u2, v1+v2] += f1[u1, v1] * f2[u2, v2].
+
+    g1[..., 2A+1, 2A+1], g2[..., 2B+1, 2B+1] -> g3[..., 2(A+B)+1, 2(A+B)+1],
+    all indexed with the centre at the middle.
+    """
+    g1 = np.asarray(g1, dtype=np.complex128)
+    g2 = np.asarray(g2, dtype=np.complex128)
+    n1 = g1.shape[-1]
+    n2 = g2.shape[-1]
+    n3 = n1 + n2 - 1
+    g3 = np.zeros(np.broadcast_shapes(g1.shape[:-2], g2.shape[:-2]) + (n3, n3), dtype=np.complex128)
+    for a in range(n1):
+        for b in range(n1):
+            g3[..., a : a + n2, b : b + n2] += g1[..., a, b, None, None] * g2
+    return g3
+
+
+def fourier2sh(g3, L3: int, Lout: int, n_theta: int | None = None) -> np.ndarray:
+    """2D Fourier coefficients -> SH coefficients (eq. fs-sh).
+
+    The printed equation claims each Fourier basis function is a finite SH sum,
+    which it is not; the reading used here is the projection
+        y_l^m = int_{S^2} F(theta, phi) Y_l^m dOmega,
+        F = sum_{u,v} g3[u, v] exp(i (u theta + v phi)),  theta in [0, pi].
+    The phi integral uses a uniform rule with L3+Lout+1 points (exact for the
+    trigonometric polynomial in phi); the theta integral uses Gauss-Legendre in
+    theta itself on [0, pi], which converges geometrically for these entire
+    integrands (the default node count is far past convergence, see tests).
+
+    g3[..., 2*L3+1, 2*L3+1] -> complex y[..., (Lout+1)^2].  For grids of real
+    functions (e.g. made by sh2fourier and fourier_conv) the imaginary part is
+    zero up to rounding.
+    """
+    g3 = np.asarray(g3, dtype=np.complex128)
+    lead = g3.shape[:-2]
+    a = g3.reshape(-1, 2 * L3 + 1, 2 * L3 + 1)
+    if n_theta is None:
+        n_theta = 2 * (L3 + Lout) + 48
+    xg, wg = gauss_legendre(n_theta)
+    th = 0.5 * math.pi * (xg + 1.0)
+    wth = 0.5 * math.pi * wg * np.sin(th)  # includes the sin(theta) measure
+    npf = L3 + Lout + 1
+    ph = 2.0 * math.pi * np.arange(npf) / npf
+    wph = 2.0 * math.pi / npf
+    u = np.arange(-L3, L3 + 1)
+    Eth = np.exp(1j * np.outer(th, u))  # [T, 2L3+1]
+    Eph = np.exp(1j * np.outer(u, ph))  # [2L3+1, P]
+    F = np.einsum("tu,nuv,vp->ntp", Eth, a, Eph)  # samples of F on the grid
+    TH, PH = np.meshgrid(th, ph, indexing="ij")
+    Y = real_sh(Lout, TH, PH)  # [T, P, K]
+    W = wth[:, None] * wph
+    y = np.einsum("ntp,tpk->nk", F * W[None], Y)
+    return y.reshape(lead + (nsh(Lout),))
+
+
+# ---------------------------------------------------------------------------
+# Many-body self product (Sec. 3.3; Appendix "Implementation Details")
+# ---------------------------------------------------------------------------
+
+def selfproduct(x, L: int, nu: int, Lout: int, mode: str = "stepwise") -> np.ndarray:
+    """nu-fold Gaunt product of A = x with itself.
+
+    mode "stepwise": B_1 = P_Lout(A); B_{k+1} = P_Lout(B_k * A), i.e. each of
+      the nu-1 products is truncated to degree Lout before the next one.
+    mode "fused": P_Lout(F_A^nu), the generalized Gaunt coefficients of the
+      appendix with no intermediate truncation; evaluated exactly on a
+      quadrature grid of degree nu*L + Lout.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    if nu < 1:
+        raise ValueError("nu >= 1")
+    lead = x.shape[:-1]
+    a = x.reshape(-1, nsh(L))
+    if mode == "stepwise":
+        if nu == 1:
+            y = np.zeros((a.shape[0], nsh(Lout)))
+            k = min(nsh(L), nsh(Lout))
+            y[:, :k] = a[:, :k]
+            return y.reshape(lead + (nsh(Lout),))
+        B, LB = a, L
+        for _ in range(nu - 1):
+            B = gtp(B, a, LB, L, Lout) if max(LB, L, Lout) <= 8 else gtp_grid(B, a, LB, L, Lout)
+            LB = Lout
+        return B.reshape(lead + (nsh(Lout),))
+    if mode == "fused":
+        th, ph, w = sphere_quadrature(nu * L + Lout)
+        Y = real_sh(max(L, Lout), th, ph)
+        F = a @ Y[:, : nsh(L)].T
+        y = (F ** nu) @ (Y[:, : nsh(Lout)] * w[:, None])
+        return y.reshape(lead + (nsh(Lout),))
+    raise ValueError(mode)
+
+
+# ---------------------------------------------------------------------------
+# Rotations (Appendix D, equivariance)
+# ---------------------------------------------------------------------------
+
+def random_rotation(rng: np.random.Generator) -> np.ndarray:
+    """Uniformly random rotation matrix from a normalised Gaussian quaternion."""
+    q = rng.standard_normal(4)
+    q /= np.linalg.norm(q)
+    w, x, y, z = q
+    return np.array([
+        [1 - 2 * (y * y + z * z), 2 * (x * y - z * w), 2 * (x * z + y * w)],
+        [2 * (x * y + z * w), 1 - 2 * (x * x + z * z), 2 * (y * z - x * w)],
+        [2 * (x * z - y * w), 2 * (y * z + x * w), 1 - 2 * (x * x + y * y)],
+    ])
+
+
+def wigner_d_real(L: int, R: np.ndarray) -> np.ndarray:
+    """Block-diagonal real Wigner-D for degrees 0..L, by exact quadrature.
+
+    D[i, j] = int Y_i(R r) Y_j(r) dOmega (same-degree blocks only), so that
+    Y(R r) = D Y(r), and coefficients of F(R^-1 r) are D x.
+    """
+    th, ph, w = sphere_quadrature(2 * L)
+    r = np.stack([np.sin(th) * np.cos(ph), np.sin(th) * np.sin(ph), np.cos(th)], axis=-1)
+    Y = real_sh(L, th, ph)
+    YR = real_sh_xyz(L, r @ R.T)
+    D = (YR * w[:, None]).T @ Y
+    mask = np.zeros_like(D, dtype=bool)
+    for l in range(L + 1):
+        mask[l * l : (l + 1) ** 2, l * l : (l + 1) ** 2] = True
+    return np.where(mask, D, 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Error metric
+# ---------------------------------------------------------------------------
+
+def max_rel_err(y, yref) -> float:
+    """max over products of max_i |y - yref| / ||yref||_2 (per product).
+
+    Products whose reference norm is below 1e-30 are measured in absolute
+    error.  The last axis is the coefficient axis.
+    """
+    y = np.asarray(y, dtype=np.float64)
+    yref = np.asarray(yref, dtype=np.float64)
+    d = np.abs(y - yref).reshape(-1, y.shape[-1]).max(axis=1)
+    nrm = np.linalg.norm(yref.reshape(-1, yref.shape[-1]), axis=1)
+    nrm = np.where(nrm < 1e-30, 1.0, nrm)
+    return float((d / nrm).max()) if d.size else 0.0
