@@ -1,0 +1,234 @@
+"""Benchmark of the Gaunt tensor product hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg] [--L L]
+                    [--no-cpu-baseline] [--gpus 1]
+
+Default: the edge workload (B=65536 edges x C=128 channels, L1=L2=Lout=6,
+x2 = radial weights x real SH of the edge direction), fp32.  One step is one
+gtp_full over the whole batch.  Prints one JSON line with the throughput in
+(b,c)-products/s, the roofline of the kernel (its launch duration measured
+with HIP events on the stream it runs on) and the fp64 oracle timed on the
+host cores on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "Gaunt TP (b,c)-products/sec at L=6 fp32; % HBM/MFMA roofline on 1 MI355X"
+PEAK_FP32_TFLOPS = 157.3  # MI355X published fp32 vector / matrix peak
+PEAK_HBM_GBS = 8000.0     # MI355X HBM3E
+
+# Algorithmic flops per (b,c)-product of the paper's Fourier method in real
+# form (sparse change of basis, min(direct, FFT) convolution, projection to
+# Lout), the per-unit figures the roofline is priced with.
+ALG_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
+# Stepwise nu = 3, L = 2, Lout = 3 many-body chain (two products).
+ALG_FLOPS_MANYBODY = 2200
+
+
+def nsh(L):
+    return (L + 1) * (L + 1)
+
+
+def kernel_sources_sha() -> str:
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2401_10216_amd", "csrc"))):
+        with open(os.path.join(ROOT, "paper_2401_10216_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload: str):
+    """HBM bytes per launch from committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    counters, if they were taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path)).get(workload)
+    except Exception:
+        return None
+    if not d or d.get("kernel_sha") != kernel_sources_sha():
+        return None
+    return d.get("bytes_per_launch")
+
+
+def make_workload(args, torch, gtp, inputs):
+    """Returns (step callable, products per step, description dict, alg flops, alg bytes, oracle sample fn)."""
+    dev = torch.device("cuda:0")
+    w = args.workload
+    if w == "edge":
+        B, C, L = 65536, 128, 6
+        x1, r, h = inputs.edge_inputs(B, C, L)
+        t1 = torch.from_numpy(x1).to(dev)
+        tr = torch.from_numpy(r.astype("float32")).to(dev)
+        th = torch.from_numpy(h).to(dev)
+        t2 = gtp.gtp_sh_filter(L, tr, th)
+        del th
+        plan = gtp.Plan(L, L, L)
+        y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
+
+        def step():
+            gtp.gtp_full(plan, t1, t2, y)
+
+        def oracle_sample(O, idx):
+            deg = inputs.degree_of_index(L)
+            bi, ci = idx // C, idx % C
+            a = x1[bi, ci].astype("float64")
+            bref = h[bi, ci][:, deg] * O.real_sh_xyz(L, r[bi])
+            return (lambda: O.gtp(a, bref, L, L, L)), y.view(B * C, -1)
+
+        desc = {"workload": "edge: B=65536 edges x C=128 channels, L1=L2=Lout=6, x1~N(0,1), "
+                            "x2 = h[b,c,l] * Y_lm(r_b), r_b uniform on S^2, h~N(0,1)",
+                "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
+        return step, B * C, desc, ALG_FLOPS[6], 4 * (2 * nsh(L) + nsh(L)), oracle_sample, 2
+    if w in ("tiny", "sweep", "highdeg"):
+        if w == "tiny":
+            B, C, L, idx_cfg = 1024, 1, 2, 1
+            x1, x2 = inputs.pair_inputs(1, B, C, L, L)
+        elif w == "sweep":
+            L = args.L
+            B, C, idx_cfg = 2048, 128, 4
+            x1, x2 = inputs.sweep_inputs(L)
+        else:
+            B, C, L, idx_cfg = 32768, 64, 16, 5
+            b1, b2, x1, x2 = inputs.highdeg_inputs(B, C, L)
+        if w == "highdeg":
+            t1 = torch.from_numpy(b1.view("int16")).to(dev).view(torch.bfloat16)
+            t2 = torch.from_numpy(b2.view("int16")).to(dev).view(torch.bfloat16)
+            in_bytes = 2
+        else:
+            t1 = torch.from_numpy(x1).to(dev)
+            t2 = torch.from_numpy(x2).to(dev)
+            in_bytes = 4
+        plan = gtp.Plan(L, L, L)
+        y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
+
+        def step():
+            gtp.gtp_full(plan, t1, t2, y)
+
+        def oracle_sample(O, idx):
+            a = x1.reshape(B * C, -1)[idx].astype("float64")
+            b = x2.reshape(B * C, -1)[idx].astype("float64")
+            fn = (lambda: O.gtp(a, b, L, L, L)) if L <= 8 else (lambda: O.gtp_grid(a, b, L, L, L))
+            return fn, y.view(B * C, -1)
+
+        desc = {"workload": f"{w}: B={B} x C={C}, L1=L2=Lout={L}, iid N(0,1)" + (" rounded to bf16" if w == "highdeg" else ""),
+                "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "bf16" if w == "highdeg" else "f32"}
+        return step, B * C, desc, ALG_FLOPS.get(L), in_bytes * 2 * nsh(L) + 4 * nsh(L), oracle_sample, idx_cfg
+    if w == "manybody":
+        N, C, L, nu, Lout = 1728, 256, 2, 3, 3
+        x = inputs.manybody_inputs(N, C, L)
+        tx = torch.from_numpy(x).to(dev)
+        y = torch.empty((N, C, nsh(Lout)), dtype=torch.float32, device=dev)
+
+        def step():
+            gtp.gtp_selfproduct(tx, L, nu, Lout, gtp.GTP_SELF_STEPWISE, y)
+
+        def oracle_sample(O, idx):
+            a = x.reshape(N * C, -1)[idx].astype("float64")
+            return (lambda: O.selfproduct(a, L, nu, Lout, "stepwise")), y.view(N * C, -1)
+
+        desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
+                            "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
+        return step, N * C, desc, ALG_FLOPS_MANYBODY, 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
+    raise SystemExit(f"unknown workload {w}")
+
+
+def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=12.0):
+    """Time the oracle on a seeded subsample sized to roughly budget_s seconds."""
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    n = min(1024, total)
+    while True:
+        idx = inputs.sample_indices(idx_cfg, total, n)
+        fn, ydev = oracle_sample(O, idx)
+        t0 = time.perf_counter()
+        ref = fn()
+        dt = time.perf_counter() - t0
+        if dt >= budget_s / 4 or n >= total:
+            break
+        n = int(min(total, max(2 * n, n * budget_s / max(dt, 1e-3))))
+    import torch
+    got = ydev[torch.from_numpy(idx).to(ydev.device)].cpu().numpy()
+    err = O.max_rel_err(got, ref)
+    return {"value": n / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
+                      f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="edge")
+    ap.add_argument("--L", type=int, default=32)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the Gaunt tensor product shards over (b,c) with no exchange, "
+              "and this build runs on a single MI355X (--gpus 1).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2401_10216_amd import gtp, inputs
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    gtp.lib()  # fails loudly if the HIP library is not built
+    step, products, desc, alg_flops, alg_bytes, oracle_sample, idx_cfg = make_workload(args, torch, gtp, inputs)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    kernel_ms = ev0.elapsed_time(ev1) / args.steps  # average launch duration on the launch stream
+    value = products * args.steps / wall
+
+    roof = None
+    if alg_flops:
+        achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
+        tb = load_traffic(args.workload)
+        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb,
+                "kernel_ms": round(kernel_ms, 5), "alg_flops_per_product": alg_flops,
+                "hbm": {"achieved": round(alg_bytes * products / (kernel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                        "unit": "GB/s", "alg_bytes_per_product": alg_bytes}}
+        roof["hbm"]["frac"] = round(roof["hbm"]["achieved"] / PEAK_HBM_GBS, 4)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        from oracle import gtp_oracle as O
+        cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
+
+    line = {"metric": METRIC, "value": value, "unit": "products/s", "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
+            "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": desc,
+            "roofline": roof, "cpu_baseline": cpu}
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

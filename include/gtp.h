@@ -1,0 +1,172 @@
+/*
+ * gtp.h -- C ABI of the MI355X (gfx950) Gaunt Tensor Product library.
+ *
+ * The Gaunt Tensor Product (Luo, Chen, He, "Enabling efficient equivariant
+ * operations in the Fourier basis via Gaunt Tensor Products", ICLR 2024) of
+ * two real spherical-harmonic (SH) coefficient vectors x1 (degrees <= L1) and
+ * x2 (degrees <= L2) is the SH expansion, truncated to degree Lout, of the
+ * product of the two spherical functions they define (Sec. 3.1, eq.
+ * tp-eq-mul):
+ *
+ *   y_l^m = sum G^{(l,m)}_{(l1,m1)(l2,m2)} x1_{l1}^{m1} x2_{l2}^{m2},
+ *   G     = int_{S^2} Y_{l1}^{m1} Y_{l2}^{m2} Y_l^m dOmega   (real Gaunt coefficients).
+ *
+ * The library computes it the paper's way (Sec. 3.2): change of basis SH ->
+ * 2D Fourier, product of the two functions as a 2D convolution of their Fourier
+ * grids, projection back to SH.
+ *
+ * Conventions shared by every entry point
+ *   - Real SH, z polar axis, no Condon-Shortley phase:
+ *       Y_l^0 = Q_l^0(cos t), Y_l^{+m} = sqrt2 Q_l^m(cos t) cos(m p),
+ *       Y_l^{-m} = sqrt2 Q_l^m(cos t) sin(m p),  Q_l^m = N_lm P_l^m,
+ *     so Y_1 = sqrt(3/(4 pi)) (y, z, x).
+ *   - Coefficient vectors are contiguous, index i = l*l + l + m, (L+1)^2 long.
+ *     Batched tensors are row-major [B, C, (L+1)^2] (channel-wise products:
+ *     product (b,c) uses channel c of both inputs, Appendix "Implementation
+ *     Details", channel-wise combination).
+ *   - Every data pointer is a DEVICE pointer on the current HIP device, owned
+ *     by the caller; the library only reads inputs and writes outputs, never
+ *     allocates or frees caller memory.  Pointers must be 4-byte aligned
+ *     (2-byte for bf16 inputs).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls are
+ *     asynchronous on that stream; a launch failure returns GTP_ERR_HIP.
+ *   - Every argument is validated on the host BEFORE any HIP call; invalid
+ *     arguments return GTP_ERR_INVALID_ARG and touch nothing.
+ *   - Functions never throw.  gtp_last_error() gives a thread-local message.
+ *   - Floating point: tables are built in fp64 on the host and rounded once to
+ *     fp32; arithmetic and outputs are fp32; bf16 applies to inputs only.
+ *   - Limits: 0 <= L1, L2, Lout <= 64.  Output degrees above L1 + L2 are
+ *     written as zeros.
+ */
+#ifndef GTP_H
+#define GTP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GTP_OK = 0,
+  GTP_ERR_INVALID_ARG = 1, /* bad sizes, null pointers, overlap, bad enum */
+  GTP_ERR_UNSUPPORTED = 2, /* valid request the library does not implement  */
+  GTP_ERR_NO_DEVICE = 3,   /* no HIP device visible                          */
+  GTP_ERR_HIP = 4,         /* a HIP runtime call or kernel launch failed      */
+  GTP_ERR_ALLOC = 5        /* host or device allocation failed                */
+} gtp_status;
+
+typedef enum { GTP_F32 = 0, GTP_BF16 = 1 } gtp_dtype;
+
+/* Plan flags (bitwise or). */
+#define GTP_CONV_AUTO 0u      /* pick the 2D-convolution algorithm by measured crossover */
+#define GTP_CONV_DIRECT 1u    /* direct 2D convolution of the Fourier grids (eq. 2D-conv) */
+#define GTP_CONV_FFT 2u       /* convolution theorem: transform, pointwise product, transform back */
+#define GTP_PLAN_HOST_ONLY 16u /* build the fp64 tables only; no HIP call (host-side checks) */
+
+/* Many-body modes for gtp_selfproduct. */
+#define GTP_SELF_STEPWISE 0u /* B_1 = A, B_{k+1} = P_Lout(B_k * A): truncate after every product */
+#define GTP_SELF_FUSED 1u    /* P_Lout(A^nu): one multi-convolution, projected once */
+
+/* Opaque plan: the SH <-> Fourier change-of-basis tables for one
+ * (L1, L2, Lout), built in fp64 and uploaded once to the device that is
+ * current at creation.  Use a plan only while that device is current. */
+typedef struct gtp_plan_ *gtp_plan;
+
+/* Create a plan (Sec. 3.2: the coefficients y^{l,m,*}_{u,v} of eq. sh-fs and
+ * z^{l,m,*}_{u,v} of eq. fs-sh, plus the grids of the convolution).
+ * out: receives the plan.  Returns GTP_ERR_NO_DEVICE without a device unless
+ * GTP_PLAN_HOST_ONLY is set.  The plan owns its host and device tables. */
+gtp_status gtp_plan_create(gtp_plan *out, int L1, int L2, int Lout, unsigned flags);
+
+/* Destroy a plan and free its tables (NULL is a no-op).  Not stream-ordered:
+ * the caller must make sure no launch using the plan is still pending. */
+gtp_status gtp_plan_destroy(gtp_plan p);
+
+/* Fused Gaunt tensor product (Sec. 3.1 eq. tp-eq-mul computed by Sec. 3.2):
+ *   y[b,c,:] = GTP(x1[b,c,:], x2[b,c,:]) truncated to degree Lout.
+ * x1: [B, C, (L1+1)^2], x2: [B, C, (L2+1)^2] of type in_dtype;
+ * y: [B, C, (Lout+1)^2] fp32.  B*C == 0 is a successful no-op.  y must not
+ * overlap x1 or x2.  The Fourier grids never leave the chip. */
+gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
+                    int64_t B, int64_t C, float *y, void *stream);
+
+/* Step 1 (Sec. 3.2, eq. sh-fs): SH coefficients -> 2D Fourier coefficients
+ * x*_{u,v}, |u|,|v| <= L, for L = L1 (which = 1) or L2 (which = 2).
+ * The function is extended to theta in [-pi, pi) by F(-t, p) = F(t, p + pi).
+ * x: [n, (L+1)^2] (in_dtype); grid: [n, 2L+1, 2L+1] complex64 interleaved
+ * (re, im), element (u, v) at [(u+L)*(2L+1) + (v+L)]. */
+gtp_status gtp_sh2fourier(gtp_plan p, int which, const void *x, gtp_dtype in_dtype, int64_t n,
+                          float *grid, void *stream);
+
+/* Step 2 (Sec. 3.2, eq. 2D-conv): f3_{u,v} = sum_{u1+u2=u, v1+v2=v} f1_{u1,v1} f2_{u2,v2}.
+ * g1: [n, 2L1+1, 2L1+1], g2: [n, 2L2+1, 2L2+1], g3: [n, 2U+1, 2U+1] with
+ * U = L1 + L2, all complex64 interleaved and centred as above.  Computed as a
+ * direct convolution (the grids are the public, paper-layout grids). */
+gtp_status gtp_fourier_conv(gtp_plan p, const float *g1, const float *g2, int64_t n, float *g3,
+                            void *stream);
+
+/* Step 3 (Sec. 3.2, eq. fs-sh): y_l^m = Re sum_{u,v} g3_{u,v} z^{l,m}_{u,v},
+ * z^{l,m}_{u,v} = int_{S^2} exp(i(u t + v p)) Y_l^m dOmega (the projection of
+ * the grid's function onto the SH basis), l <= Lout.
+ * g3: [n, 2U+1, 2U+1] complex64; y: [n, (Lout+1)^2] fp32.  For grids of real
+ * functions (anything made by gtp_sh2fourier and gtp_fourier_conv) the
+ * discarded imaginary part is zero. */
+gtp_status gtp_fourier2sh(gtp_plan p, const float *g3, int64_t n, float *y, void *stream);
+
+/* Many-body self product (Sec. 3.3 "Equivariant Many-body Interactions";
+ * Appendix "Implementation Details", generalized Gaunt coefficients and the
+ * divide-and-conquer multi-convolution): the nu-fold product of A = x with
+ * itself, nu >= 1.
+ *   mode GTP_SELF_STEPWISE: B_1 = P_Lout(A), B_{k+1} = P_Lout(B_k * A).
+ *   mode GTP_SELF_FUSED   : P_Lout(A^nu) with no intermediate truncation.
+ * x: [B, C, (L+1)^2] (in_dtype); y: [B, C, (Lout+1)^2] fp32.  Plans for the
+ * needed degrees are built and cached internally (per device).  The fused
+ * mode needs nu * L <= 64 (GTP_ERR_UNSUPPORTED otherwise).  The stepwise
+ * mode may take a stream-ordered device workspace (hipMallocAsync) when no
+ * single-kernel path exists for (L, nu, Lout). */
+gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void *x,
+                           gtp_dtype in_dtype, int64_t B, int64_t C, float *y, void *stream);
+
+/* Spherical-harmonic filter of an equivariant convolution (Sec. 3.3
+ * "Equivariant Convolutions"): out[b,c,(l,m)] = h[b,c,l] * Y_l^m(r_b / |r_b|).
+ * r: [B, 3] fp32 edge vectors (need not be unit; zero vectors give the
+ * direction (0,0,1)); h: [B, C, L+1] fp32 per-degree radial weights, or NULL
+ * for h = 1 (then C must be 1); out: [B, C, (L+1)^2] fp32.  0 <= L <= 64. */
+gtp_status gtp_sh_filter(int L, const float *r, const float *h, int64_t B, int64_t C, float *out,
+                         void *stream);
+
+/* Number of floats of one per-product public grid: which = 1 or 2 gives the
+ * input grids (2 * (2L+1)^2), which = 3 the product grid (2 * (2U+1)^2).
+ * Returns -1 on a bad argument. */
+int64_t gtp_grid_floats(gtp_plan p, int which);
+
+/* Plan geometry: out[0..7] = {L1, L2, Lout, U = L1+L2, Le = min(Lout, U),
+ * NT (theta intervals of the sampling grid on [0, pi]), NP (phi samples),
+ * conv algorithm actually used by gtp_full (GTP_CONV_DIRECT or GTP_CONV_FFT)}. */
+gtp_status gtp_plan_info(gtp_plan p, int64_t *out8);
+
+/* Copy one of the plan's fp64 host tables (test aid, host memory):
+ *   which 0: T1   [tri(l,m)][u], u in [0, Lin]      theta-Fourier series of Q_l^m (step 1)
+ *   which 1: Zc   [tri(l,m)][u], u in [0, U]        int cos(u t) Q sin t dt (step 3)
+ *   which 2: Zs   [tri(l,m)][u], u in [0, U]        int sin(u t) Q sin t dt (step 3)
+ *   which 3: S    [tri(l,m)][j], j in [0, NT]       synthesis at the theta nodes
+ *   which 4: W    [tri(l,m)][j], j in [0, NT]       analysis weights at the theta nodes
+ * with tri(l,m) = l(l+1)/2 + m, m >= 0.  Pass buf = NULL to get the length in
+ * *count; otherwise *count is the capacity in doubles. */
+gtp_status gtp_plan_table(gtp_plan p, int which, double *buf, int64_t *count);
+
+/* fp64 host evaluation of the plan's three-step transform pipeline on host
+ * arrays (x1[n,(L1+1)^2], x2[n,(L2+1)^2] -> y[n,(Lout+1)^2]).  A CPU check of
+ * the tables only; gtp_full never calls it and it is not a fallback. */
+gtp_status gtp_debug_host_pipeline(gtp_plan p, const double *x1, const double *x2, int64_t n,
+                                   double *y);
+
+const char *gtp_status_str(gtp_status s);
+const char *gtp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GTP_H */

@@ -1,0 +1,77 @@
+"""Build libgtp.so (HIP kernels for gfx950 + fp64 host table builder + C ABI).
+
+    python -m paper_2401_10216_amd.build [-v]
+
+Objects go to ``_build/`` at the repository root; the library is written
+in-tree as ``paper_2401_10216_amd/libgtp.so`` so it travels with the source
+tree.  Always recompiles.
+"""
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import time
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+BUILD = os.path.join(ROOT, "_build")
+LIB = os.path.join(PKG, "libgtp.so")
+
+HIP_SOURCES = ["gtp_api.hip", "gtp_small.hip", "gtp_generic.hip"]
+CPP_SOURCES = ["gtp_tables.cpp"]
+ARCH = "gfx950"
+# Packed fp32 VALU forms stay off: plain fp32 FMAs only.
+HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",
+             "-packed-fp32-ops", "-Wno-unused-command-line-argument", f"-I{os.path.join(ROOT, 'include')}"]
+CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall"]
+
+
+def _hipcc() -> str:
+    for c in (os.environ.get("HIPCC"), "/opt/rocm/bin/hipcc", shutil.which("hipcc")):
+        if c and os.path.exists(c):
+            return c
+    raise RuntimeError("hipcc not found")
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    hipcc = _hipcc()
+    jobs = []
+    for s in HIP_SOURCES:
+        obj = os.path.join(BUILD, s.replace(".hip", ".o"))
+        jobs.append(([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj))
+    for s in CPP_SOURCES:
+        obj = os.path.join(BUILD, s.replace(".cpp", ".o"))
+        jobs.append((["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj))
+    t0 = time.time()
+    procs = [(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True), cmd, obj)
+             for cmd, obj in jobs]
+    failed = []
+    for p, cmd, obj in procs:
+        out, _ = p.communicate()
+        if verbose or p.returncode:
+            print(" ".join(cmd))
+            if out:
+                print(out)
+        if p.returncode:
+            failed.append(obj)
+    if failed:
+        raise RuntimeError(f"compilation failed: {failed}")
+    tmp = LIB + ".tmp"
+    link = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *[o for _, o in jobs]]
+    r = subprocess.run(link, capture_output=True, text=True)
+    if r.returncode:
+        print(" ".join(link))
+        print(r.stdout, r.stderr)
+        raise RuntimeError("link failed")
+    os.replace(tmp, LIB)
+    if verbose:
+        print(f"built {LIB} in {time.time() - t0:.1f}s")
+    return LIB
+
+
+if __name__ == "__main__":
+    build(verbose="-v" in sys.argv)

@@ -1,0 +1,436 @@
+// C ABI of the Gaunt Tensor Product library: plans, argument validation (all
+// of it before the first HIP call), table upload and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <new>
+#include <stdexcept>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "../../include/gtp.h"
+#include "gtp_device.hpp"
+#include "gtp_tables.hpp"
+
+struct gtp_plan_ {
+  int L1 = 0, L2 = 0, Lout = 0;
+  unsigned flags = 0;
+  bool host_only = true;
+  int device = -1;
+  int conv = GTP_CONV_FFT;
+  bool force_generic = false;
+  gtp::Tables tab;
+  std::vector<float*> dbufs;
+  gtp::DevTables dev{};
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+gtp_status fail(gtp_status s, const std::string& msg) {
+  g_last_error = msg;
+  return s;
+}
+
+gtp_status hip_fail(hipError_t e, const char* what) {
+  return fail(GTP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+constexpr int kMaxL = 64;
+constexpr int kMaxLout = 64;
+// Internal flag: force the workgroup-per-product kernel (tests compare paths).
+constexpr unsigned kForceGeneric = 32u;
+
+bool ranges_overlap(const void* a, size_t na, const void* b, size_t nb) {
+  const char* pa = static_cast<const char*>(a);
+  const char* pb = static_cast<const char*>(b);
+  return pa < pb + nb && pb < pa + na;
+}
+
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+size_t dtype_size(gtp_dtype d) { return d == GTP_BF16 ? 2 : 4; }
+bool dtype_ok(gtp_dtype d) { return d == GTP_F32 || d == GTP_BF16; }
+
+gtp_status upload(gtp_plan_* p) {
+  using gtp::ntri;
+  const gtp::Tables& t = p->tab;
+  const int nmp = 2 * t.Mphi + 1;
+  const int ntE = ntri(t.Le);
+  std::vector<float> WT(size_t(t.NJ) * ntE), PhiT(size_t(t.NP) * nmp);
+  for (int r = 0; r < ntE; ++r)
+    for (int j = 0; j < t.NJ; ++j) WT[size_t(j) * ntE + r] = float(t.W[size_t(r) * t.NJ + j]);
+  for (int mp = 0; mp < nmp; ++mp)
+    for (int k = 0; k < t.NP; ++k) PhiT[size_t(k) * nmp + mp] = float(t.Phi[size_t(mp) * t.NP + k]);
+  auto up = [&](const std::vector<double>* src64, const std::vector<float>* src32, const float** dst) -> gtp_status {
+    const size_t cnt = src64 ? src64->size() : src32->size();
+    std::vector<float> h(cnt ? cnt : 1, 0.0f);
+    for (size_t i = 0; i < cnt; ++i) h[i] = src64 ? float((*src64)[i]) : (*src32)[i];
+    float* d = nullptr;
+    hipError_t e = hipMalloc(&d, h.size() * sizeof(float));
+    if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMalloc: ") + hipGetErrorString(e));
+    p->dbufs.push_back(d);
+    e = hipMemcpy(d, h.data(), h.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+    *dst = d;
+    return GTP_OK;
+  };
+  gtp_status s;
+  gtp::DevTables& d = p->dev;
+  d.L1 = t.L1; d.L2 = t.L2; d.Lout = t.Lout; d.U = t.U; d.Le = t.Le; d.Lin = t.Lin;
+  d.NT = t.NT; d.NJ = t.NJ; d.NP = t.NP; d.Mphi = t.Mphi; d.ldT1 = t.ldT1; d.ldZ = t.ldZ;
+  if ((s = up(&t.S, nullptr, &d.S)) != GTP_OK) return s;
+  if ((s = up(&t.W, nullptr, &d.W)) != GTP_OK) return s;
+  if ((s = up(nullptr, &WT, &d.WT)) != GTP_OK) return s;
+  if ((s = up(&t.Phi, nullptr, &d.Phi)) != GTP_OK) return s;
+  if ((s = up(nullptr, &PhiT, &d.PhiT)) != GTP_OK) return s;
+  if ((s = up(&t.T1, nullptr, &d.T1)) != GTP_OK) return s;
+  if ((s = up(&t.Zc, nullptr, &d.Zc)) != GTP_OK) return s;
+  if ((s = up(&t.Zs, nullptr, &d.Zs)) != GTP_OK) return s;
+  return GTP_OK;
+}
+
+void release(gtp_plan_* p) {
+  for (float* b : p->dbufs) (void)hipFree(b);
+  p->dbufs.clear();
+}
+
+gtp_status check_device() {
+  int n = 0;
+  hipError_t e = hipGetDeviceCount(&n);
+  if (e != hipSuccess || n <= 0) return fail(GTP_ERR_NO_DEVICE, "no HIP device visible");
+  return GTP_OK;
+}
+
+gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, int maxL) {
+  if (!out) return fail(GTP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (L1 < 0 || L2 < 0 || Lout < 0 || L1 > maxL || L2 > maxL || Lout > kMaxLout)
+    return fail(GTP_ERR_INVALID_ARG, "degrees must satisfy 0 <= L1, L2, Lout <= 64");
+  const unsigned conv = flags & 3u;
+  if (conv == 3u) return fail(GTP_ERR_INVALID_ARG, "GTP_CONV_DIRECT and GTP_CONV_FFT are exclusive");
+  if (flags & ~(3u | GTP_PLAN_HOST_ONLY | kForceGeneric)) return fail(GTP_ERR_INVALID_ARG, "unknown flag bits");
+  std::unique_ptr<gtp_plan_> p(new (std::nothrow) gtp_plan_);
+  if (!p) return fail(GTP_ERR_ALLOC, "host allocation failed");
+  p->L1 = L1;
+  p->L2 = L2;
+  p->Lout = Lout;
+  p->flags = flags;
+  p->host_only = (flags & GTP_PLAN_HOST_ONLY) != 0;
+  p->force_generic = (flags & kForceGeneric) != 0;
+  // The convolution-theorem path is used at every degree: its flop count is
+  // below the direct real-form convolution's from L = 2 on.
+  p->conv = conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : GTP_CONV_FFT;
+  try {
+    p->tab = gtp::build_tables(L1, L2, Lout);
+  } catch (const std::bad_alloc&) {
+    return fail(GTP_ERR_ALLOC, "table allocation failed");
+  } catch (const std::exception& e) {
+    return fail(GTP_ERR_INVALID_ARG, e.what());
+  }
+  if (!p->host_only) {
+    gtp_status s = check_device();
+    if (s != GTP_OK) return s;
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    s = upload(p.get());
+    if (s != GTP_OK) {
+      release(p.get());
+      return s;
+    }
+  }
+  *out = p.release();
+  return GTP_OK;
+}
+
+// Internal plan cache for the many-body entry point, keyed by device and degrees.
+std::mutex g_cache_mu;
+std::map<std::tuple<int, int, int, int>, gtp_plan> g_cache;
+
+gtp_status cached_plan(int L1, int L2, int Lout, gtp_plan* out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  auto key = std::make_tuple(dev, L1, L2, Lout);
+  auto it = g_cache.find(key);
+  if (it != g_cache.end()) {
+    *out = it->second;
+    return GTP_OK;
+  }
+  gtp_plan p = nullptr;
+  gtp_status s = make_plan(&p, L1, L2, Lout, 0u, kMaxL);
+  if (s != GTP_OK) return s;
+  g_cache[key] = p;
+  *out = p;
+  return GTP_OK;
+}
+
+gtp_status plan_check(gtp_plan p) {
+  if (!p) return fail(GTP_ERR_INVALID_ARG, "plan is NULL");
+  return GTP_OK;
+}
+
+// Last step of validation, after every argument check: a plan built with
+// GTP_PLAN_HOST_ONLY has no device tables.
+gtp_status device_ready(gtp_plan p) {
+  if (p->host_only) return fail(GTP_ERR_INVALID_ARG, "plan was created with GTP_PLAN_HOST_ONLY");
+  return GTP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gtp_status gtp_plan_create(gtp_plan* out, int L1, int L2, int Lout, unsigned flags) {
+  return make_plan(out, L1, L2, Lout, flags, kMaxL);
+}
+
+gtp_status gtp_plan_destroy(gtp_plan p) {
+  if (!p) return GTP_OK;
+  release(p);
+  delete p;
+  return GTP_OK;
+}
+
+gtp_status gtp_full(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, int64_t B, int64_t C, float* y,
+                    void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  int64_t n = 0, e1 = 0, e2 = 0, eo = 0;
+  if (!mul_ok(B, C, &n)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit in int64");
+  if (!mul_ok(n, gtp::nsh(p->L1), &e1) || !mul_ok(n, gtp::nsh(p->L2), &e2) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      e1 > INT64_MAX / 4 || e2 > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  if (n == 0) return GTP_OK;
+  if (!x1 || !x2 || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype);
+  if (ranges_overlap(y, size_t(eo) * 4, x1, size_t(e1) * es) || ranges_overlap(y, size_t(eo) * 4, x2, size_t(e2) * es))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps x1 or x2");
+  if ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % es || reinterpret_cast<uintptr_t>(y) % 4)
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  hipError_t e = hipSuccess;
+  if (p->conv == GTP_CONV_DIRECT) {
+    e = gtp::launch_full_direct(p->dev, x1, x2, it, n, y, st);
+    if (e == hipErrorNotSupported) return fail(GTP_ERR_UNSUPPORTED, "direct convolution path not built");
+    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+  }
+  bool done = false;
+  if (!p->force_generic) {
+    e = gtp::launch_full_small(p->dev, x1, x2, it, n, y, 0, st, &done);
+    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+  }
+  e = gtp::launch_full_generic(p->dev, x1, it, x2, it, n, y, 0, st);
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+}
+
+gtp_status gtp_sh2fourier(gtp_plan p, int which, const void* x, gtp_dtype in_dtype, int64_t n, float* grid,
+                          void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (which != 1 && which != 2) return fail(GTP_ERR_INVALID_ARG, "which must be 1 or 2");
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "bad in_dtype");
+  const int L = which == 1 ? p->L1 : p->L2;
+  int64_t ex = 0, eg = 0;
+  if (!mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, int64_t(2) * (2 * L + 1) * (2 * L + 1), &eg) || eg > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "n must be >= 0 and n * grid size must fit");
+  if (n == 0) return GTP_OK;
+  if (!x || !grid) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (ranges_overlap(grid, size_t(eg) * 4, x, size_t(ex) * dtype_size(in_dtype)))
+    return fail(GTP_ERR_INVALID_ARG, "grid overlaps x");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  hipError_t e = gtp::launch_sh2fourier(p->dev, L, x, in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32, n, grid,
+                                        static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_sh2fourier launch");
+}
+
+gtp_status gtp_fourier_conv(gtp_plan p, const float* g1, const float* g2, int64_t n, float* g3, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  const int64_t D1 = 2 * p->L1 + 1, D2 = 2 * p->L2 + 1, D3 = 2 * (p->L1 + p->L2) + 1;
+  int64_t e1 = 0, e2 = 0, e3 = 0;
+  if (!mul_ok(n, 2 * D1 * D1, &e1) || !mul_ok(n, 2 * D2 * D2, &e2) || !mul_ok(n, 2 * D3 * D3, &e3) ||
+      e3 > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "n must be >= 0 and n * grid size must fit");
+  if (n == 0) return GTP_OK;
+  if (!g1 || !g2 || !g3) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (ranges_overlap(g3, size_t(e3) * 4, g1, size_t(e1) * 4) || ranges_overlap(g3, size_t(e3) * 4, g2, size_t(e2) * 4))
+    return fail(GTP_ERR_INVALID_ARG, "g3 overlaps g1 or g2");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  hipError_t e = gtp::launch_fourier_conv(p->L1, p->L2, g1, g2, n, g3, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_fourier_conv launch");
+}
+
+gtp_status gtp_fourier2sh(gtp_plan p, const float* g3, int64_t n, float* y, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  const int64_t D3 = 2 * (p->L1 + p->L2) + 1;
+  int64_t e3 = 0, eo = 0;
+  if (!mul_ok(n, 2 * D3 * D3, &e3) || !mul_ok(n, gtp::nsh(p->Lout), &eo) || e3 > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "n must be >= 0 and n * grid size must fit");
+  if (n == 0) return GTP_OK;
+  if (!g3 || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (ranges_overlap(y, size_t(eo) * 4, g3, size_t(e3) * 4)) return fail(GTP_ERR_INVALID_ARG, "y overlaps g3");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  hipError_t e = gtp::launch_fourier2sh(p->dev, g3, n, y, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_fourier2sh launch");
+}
+
+gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void* x, gtp_dtype in_dtype, int64_t B,
+                           int64_t C, float* y, void* stream) {
+  if (L < 0 || L > kMaxL || Lout < 0 || Lout > kMaxLout) return fail(GTP_ERR_INVALID_ARG, "degree out of range");
+  if (nu < 1) return fail(GTP_ERR_INVALID_ARG, "nu must be >= 1");
+  if (mode != GTP_SELF_STEPWISE && mode != GTP_SELF_FUSED) return fail(GTP_ERR_INVALID_ARG, "bad mode");
+  if (mode == GTP_SELF_FUSED && int64_t(nu) * L > kMaxL)
+    return fail(GTP_ERR_UNSUPPORTED, "fused mode needs nu * L <= 64");
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "bad in_dtype");
+  int64_t n = 0, ex = 0, eo = 0;
+  if (!mul_ok(B, C, &n) || !mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, gtp::nsh(Lout), &eo) || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and sizes must fit");
+  if (n == 0) return GTP_OK;
+  if (!x || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (ranges_overlap(y, size_t(eo) * 4, x, size_t(ex) * dtype_size(in_dtype)))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps x");
+  gtp_status s = check_device();
+  if (s != GTP_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  hipError_t e = hipSuccess;
+  if (nu == 1) {
+    // B_1 = P_Lout(A): truncate or zero-pad the input
+    e = gtp::launch_pad_copy(x, it, L, n, y, Lout, st);
+    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
+  }
+  if (mode == GTP_SELF_STEPWISE && nu == 2) {
+    gtp_plan p = nullptr;
+    if ((s = cached_plan(L, L, Lout, &p)) != GTP_OK) return s;
+    bool done = false;
+    e = gtp::launch_full_small(p->dev, x, x, it, n, y, 0, st, &done);
+    if (!done) e = gtp::launch_full_generic(p->dev, x, it, x, it, n, y, 0, st);
+    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
+  }
+  if (mode == GTP_SELF_FUSED) {
+    gtp_plan p = nullptr;
+    if ((s = cached_plan(L, (nu - 1) * L, Lout, &p)) != GTP_OK) return s;
+    bool done = false;
+    e = gtp::launch_full_small(p->dev, x, x, it, n, y, nu, st, &done);
+    if (!done) e = gtp::launch_full_generic(p->dev, x, it, nullptr, it, n, y, nu, st);
+    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
+  }
+  // stepwise, nu >= 3
+  gtp_plan p1 = nullptr, p2 = nullptr;
+  if ((s = cached_plan(L, L, Lout, &p1)) != GTP_OK) return s;
+  if ((s = cached_plan(Lout, L, Lout, &p2)) != GTP_OK) return s;
+  bool done = false;
+  e = gtp::launch_self_stepwise_small(p1->dev, p2->dev, nu, x, it, n, y, st, &done);
+  if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
+  // generic chain through a stream-ordered workspace
+  float* work = nullptr;
+  e = hipMallocAsync(reinterpret_cast<void**>(&work), size_t(eo) * sizeof(float), st);
+  if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+  float* cur = (nu % 2 == 1) ? work : y;  // the last product lands in y
+  float* nxt = (nu % 2 == 1) ? y : work;
+  e = gtp::launch_full_generic(p1->dev, x, it, x, it, n, cur, 0, st);
+  for (int step = 3; e == hipSuccess && step <= nu; ++step) {
+    // B_k (fp32, degree Lout) times A
+    e = gtp::launch_full_generic(p2->dev, cur, gtp::IN_F32, x, it, n, nxt, 0, st);
+    std::swap(cur, nxt);
+  }
+  hipError_t e2 = hipFreeAsync(work, st);
+  if (e != hipSuccess) return hip_fail(e, "gtp_selfproduct launch");
+  return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
+}
+
+gtp_status gtp_sh_filter(int L, const float* r, const float* h, int64_t B, int64_t C, float* out, void* stream) {
+  if (L < 0 || L > kMaxL) return fail(GTP_ERR_INVALID_ARG, "degree out of range");
+  int64_t n = 0, eo = 0;
+  if (!mul_ok(B, C, &n) || !mul_ok(n, gtp::nsh(L), &eo) || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and sizes must fit");
+  if (!h && C != 1) return fail(GTP_ERR_INVALID_ARG, "h == NULL requires C == 1");
+  if (n == 0) return GTP_OK;
+  if (!r || !out) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (ranges_overlap(out, size_t(eo) * 4, r, size_t(B) * 12) ||
+      (h && ranges_overlap(out, size_t(eo) * 4, h, size_t(n) * (L + 1) * 4)))
+    return fail(GTP_ERR_INVALID_ARG, "out overlaps an input");
+  gtp_status s = check_device();
+  if (s != GTP_OK) return s;
+  hipError_t e = gtp::launch_sh_filter(L, r, h, B, C, out, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_sh_filter launch");
+}
+
+int64_t gtp_grid_floats(gtp_plan p, int which) {
+  if (!p || which < 1 || which > 3) return -1;
+  const int64_t L = which == 1 ? p->L1 : (which == 2 ? p->L2 : p->L1 + p->L2);
+  return 2 * (2 * L + 1) * (2 * L + 1);
+}
+
+gtp_status gtp_plan_info(gtp_plan p, int64_t* out8) {
+  if (!p || !out8) return fail(GTP_ERR_INVALID_ARG, "NULL argument");
+  const gtp::Tables& t = p->tab;
+  const int64_t v[8] = {t.L1, t.L2, t.Lout, t.U, t.Le, t.NT, t.NP, p->conv};
+  std::memcpy(out8, v, sizeof(v));
+  return GTP_OK;
+}
+
+gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
+  if (!p || !count) return fail(GTP_ERR_INVALID_ARG, "NULL argument");
+  const std::vector<double>* src = nullptr;
+  switch (which) {
+    case 0: src = &p->tab.T1; break;
+    case 1: src = &p->tab.Zc; break;
+    case 2: src = &p->tab.Zs; break;
+    case 3: src = &p->tab.S; break;
+    case 4: src = &p->tab.W; break;
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..4");
+  }
+  if (!buf) {
+    *count = int64_t(src->size());
+    return GTP_OK;
+  }
+  if (*count < int64_t(src->size())) return fail(GTP_ERR_INVALID_ARG, "buffer too small");
+  std::memcpy(buf, src->data(), src->size() * sizeof(double));
+  *count = int64_t(src->size());
+  return GTP_OK;
+}
+
+gtp_status gtp_debug_host_pipeline(gtp_plan p, const double* x1, const double* x2, int64_t n, double* y) {
+  if (!p || n < 0 || (n > 0 && (!x1 || !x2 || !y))) return fail(GTP_ERR_INVALID_ARG, "bad argument");
+  try {
+    gtp::host_pipeline(p->tab, x1, x2, n, y);
+  } catch (const std::bad_alloc&) {
+    return fail(GTP_ERR_ALLOC, "host allocation failed");
+  }
+  return GTP_OK;
+}
+
+const char* gtp_status_str(gtp_status s) {
+  switch (s) {
+    case GTP_OK: return "GTP_OK";
+    case GTP_ERR_INVALID_ARG: return "GTP_ERR_INVALID_ARG";
+    case GTP_ERR_UNSUPPORTED: return "GTP_ERR_UNSUPPORTED";
+    case GTP_ERR_NO_DEVICE: return "GTP_ERR_NO_DEVICE";
+    case GTP_ERR_HIP: return "GTP_ERR_HIP";
+    case GTP_ERR_ALLOC: return "GTP_ERR_ALLOC";
+  }
+  return "GTP_ERR_UNKNOWN";
+}
+
+const char* gtp_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// Device-side declarations shared by the HIP kernels and the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace gtp {
+
+// fp32 copies of a plan's tables on one device (see gtp_tables.hpp for the
+// definitions).  Row index tri(l, m) = l(l+1)/2 + m.
+struct DevTables {
+  int L1, L2, Lout, U, Le, Lin, NT, NJ, NP, Mphi, ldT1, ldZ;
+  const float* S;     // [tri(l<=Lin)][NJ]   Theta_lm at theta nodes
+  const float* W;     // [tri(l<=Le)][NJ]    analysis weights
+  const float* WT;    // [NJ][tri(l<=Le)]    transposed W
+  const float* Phi;   // [2 Mphi + 1][NP]    trig(mp, k)
+  const float* PhiT;  // [NP][2 Mphi + 1]
+  const float* T1;    // [tri(l<=Lt)][ldT1]  theta-Fourier series of Theta_lm
+  const float* Zc;    // [tri(l<=Le)][ldZ]
+  const float* Zs;    // [tri(l<=Le)][ldZ]
+};
+
+enum InType : int { IN_F32 = 0, IN_BF16 = 1 };
+
+// Launchers (return the launch's hipError_t).  n = number of products.
+// Thread-per-product fused kernel for the degree triples it is instantiated
+// for; *supported = false when (L1, L2, Lout, nu) has no instantiation.
+hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+                             float* y, int nu, hipStream_t s, bool* supported);
+// Stepwise many-body chain in one kernel (thread per product) for the
+// instantiated (L, nu, Lout); t1 = tables of (L, L, Lout), t2 = (Lout, L, Lout).
+hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x,
+                                      int in_type, int64_t n, float* y, hipStream_t s, bool* supported);
+// Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
+// nu >= 2: x1^nu with the plan built for U = nu * L).
+hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,
+                               int64_t n, float* y, int nu, hipStream_t s);
+// y[p, :(Lout+1)^2] = x[p, :(L+1)^2] truncated or zero-padded.
+hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
+// Direct 2D convolution of the real-form Fourier grids (the paper's eq.
+// 2D-conv without the convolution theorem), workgroup per product.
+hipError_t launch_full_direct(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+                              float* y, hipStream_t s);
+// Unfused stages with the paper's complex grids.
+hipError_t launch_sh2fourier(const DevTables& t, int L, const void* x, int in_type, int64_t n, float* grid,
+                             hipStream_t s);
+hipError_t launch_fourier_conv(int L1, int L2, const float* g1, const float* g2, int64_t n, float* g3,
+                               hipStream_t s);
+hipError_t launch_fourier2sh(const DevTables& t, const float* g3, int64_t n, float* y, hipStream_t s);
+// SH filter out[b,c,lm] = h[b,c,l] Y_lm(r_b).
+hipError_t launch_sh_filter(int L, const float* r, const float* h, int64_t B, int64_t C, float* out,
+                            hipStream_t s);
+
+}  // namespace gtp

@@ -1,0 +1,481 @@
+// Thread-per-product fused Gaunt tensor product for small degrees (gfx950).
+//
+// One lane owns one (b, c) product.  The three steps of Sec. 3.2 run with the
+// convolution theorem: the 2D Fourier series of each input is sampled on a
+// uniform (theta, phi) torus grid (the inverse transforms, with step 1 folded
+// into the theta part: table S), the samples are multiplied pointwise, and the
+// forward transforms followed by step 3 (table W) give the SH coefficients.
+// The theta transforms use the grid's mirror symmetry t <-> pi - t (Theta_lm
+// has parity (-1)^(l+m)), the phi transforms use p <-> -p and are unrolled
+// direct DFTs with compile-time twiddles.  Nothing but x and y touches HBM.
+#include <type_traits>
+#include <utility>
+
+#include "gtp_device.hpp"
+
+namespace gtp {
+namespace {
+
+constexpr double kPiD = 3.14159265358979323846264338327950288;
+
+// cos / sin of 2 pi k / N by exact integer reduction and a Taylor series,
+// evaluated at compile time (fp64, rounded once to fp32 where used).
+constexpr double ct_angle(long long k, long long N) {
+  long long r = k % N;
+  if (r < 0) r += N;
+  double x = 2.0 * kPiD * double(r) / double(N);
+  if (x > kPiD) x -= 2.0 * kPiD;
+  return x;
+}
+constexpr double ct_cos2pi(long long k, long long N) {
+  const double x = ct_angle(k, N);
+  double term = 1.0, sum = 1.0;
+  for (int i = 1; i < 40; ++i) {
+    term *= -x * x / double((2 * i - 1) * (2 * i));
+    sum += term;
+  }
+  return sum;
+}
+constexpr double ct_sin2pi(long long k, long long N) {
+  const double x = ct_angle(k, N);
+  double term = x, sum = x;
+  for (int i = 1; i < 40; ++i) {
+    term *= -x * x / double((2 * i) * (2 * i + 1));
+    sum += term;
+  }
+  return sum;
+}
+constexpr float ct_round(double v) {
+  // exact zeros and units stay exact; everything else rounds to fp32
+  return (v > -1e-15 && v < 1e-15) ? 0.0f : float(v);
+}
+
+template <int B, int... Is, typename F>
+__device__ __forceinline__ void sfor_impl(std::integer_sequence<int, Is...>, F& f) {
+  (f(std::integral_constant<int, B + Is>{}), ...);
+}
+// Compile-time loop over [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void sfor(F&& f) {
+  if constexpr (E > B) sfor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
+}
+
+constexpr int ctri(int l, int m) { return l * (l + 1) / 2 + m; }
+constexpr int csh(int L) { return (L + 1) * (L + 1); }
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+
+__device__ __forceinline__ float ld_in(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_in(const uint16_t* p, int64_t i) {
+  return __uint_as_float(uint32_t(p[i]) << 16);
+}
+
+// F[k] = A0 + sum_m A[2m-1] cos(m p_k) + A[2m] sin(m p_k), k < NP.
+template <int M, int NP>
+__device__ __forceinline__ void phi_synth(const float (&A)[2 * M + 1], float (&F)[NP]) {
+  sfor<0, NP / 2 + 1>([&](auto KK) {
+    constexpr int k = decltype(KK)::value;
+    constexpr bool mirror = (k > 0) && (2 * k != NP);
+    float e = A[0];
+    sfor<1, M + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value;
+      constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
+      if constexpr (c != 0.0f) e = fmaf(A[2 * m - 1], c, e);
+    });
+    if constexpr (mirror) {
+      float o = 0.0f;
+      sfor<1, M + 1>([&](auto MM) {
+        constexpr int m = decltype(MM)::value;
+        constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
+        if constexpr (sn != 0.0f) o = fmaf(A[2 * m], sn, o);
+      });
+      F[k] = e + o;
+      F[NP - k] = e - o;
+    } else {
+      F[k] = e;
+    }
+  });
+}
+
+// C[0] = sum_k F_k, C[2m-1] = sum_k F_k cos(m p_k), C[2m] = sum_k F_k sin(m p_k), m <= MO.
+template <int MO, int NP>
+__device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 * MO + 1]) {
+  constexpr int H = NP / 2;
+  float P[H + 1], D[H + 1];
+  P[0] = F[0];
+  D[0] = 0.0f;
+  sfor<1, H + 1>([&](auto KK) {
+    constexpr int k = decltype(KK)::value;
+    if constexpr (2 * k == NP) {
+      P[k] = F[k];
+      D[k] = 0.0f;
+    } else {
+      P[k] = F[k] + F[NP - k];
+      D[k] = F[k] - F[NP - k];
+    }
+  });
+  sfor<0, MO + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    float cs = 0.0f;
+    sfor<0, H + 1>([&](auto KK) {
+      constexpr int k = decltype(KK)::value;
+      constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
+      if constexpr (c != 0.0f) cs = fmaf(P[k], c, cs);
+    });
+    if constexpr (m == 0) {
+      C[0] = cs;
+    } else {
+      float sn = 0.0f;
+      sfor<1, H + 1>([&](auto KK) {
+        constexpr int k = decltype(KK)::value;
+        if constexpr (2 * k != NP) {
+          constexpr float s = ct_round(ct_sin2pi((long long)m * k, NP));
+          if constexpr (s != 0.0f) sn = fmaf(D[k], s, sn);
+        }
+      });
+      C[2 * m - 1] = cs;
+      C[2 * m] = sn;
+    }
+  });
+}
+
+// Theta synthesis at the mirror pair (t_j, t_{NT-j}) of one input of degree
+// L: even-parity and odd-parity (l + m) partial sums give both nodes.
+template <int L, int NJ>
+__device__ __forceinline__ void theta_synth_pair(const float (&x)[csh(L)], const float* __restrict__ S, int j,
+                                                 float (&Aj)[2 * L + 1], float (&Ajp)[2 * L + 1]) {
+  sfor<0, L + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    float ec = 0.0f, oc = 0.0f, es = 0.0f, os = 0.0f;
+    sfor<m, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float sv = S[ctri(l, m) * NJ + j];
+      if constexpr ((l + m) % 2 == 0) {
+        ec = fmaf(sv, x[l * l + l + m], ec);
+        if constexpr (m > 0) es = fmaf(sv, x[l * l + l - m], es);
+      } else {
+        oc = fmaf(sv, x[l * l + l + m], oc);
+        if constexpr (m > 0) os = fmaf(sv, x[l * l + l - m], os);
+      }
+    });
+    if constexpr (m == 0) {
+      Aj[0] = ec + oc;
+      Ajp[0] = ec - oc;
+    } else {
+      Aj[2 * m - 1] = ec + oc;
+      Ajp[2 * m - 1] = ec - oc;
+      Aj[2 * m] = es + os;
+      Ajp[2 * m] = es - os;
+    }
+  });
+}
+
+// Theta synthesis at the equator (only even l + m survive).
+template <int L, int NJ>
+__device__ __forceinline__ void theta_synth_eq(const float (&x)[csh(L)], const float* __restrict__ S, int j,
+                                               float (&A)[2 * L + 1]) {
+  sfor<0, L + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    float ec = 0.0f, es = 0.0f;
+    sfor<m, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      if constexpr ((l + m) % 2 == 0) {
+        const float sv = S[ctri(l, m) * NJ + j];
+        ec = fmaf(sv, x[l * l + l + m], ec);
+        if constexpr (m > 0) es = fmaf(sv, x[l * l + l - m], es);
+      }
+    });
+    if constexpr (m == 0) {
+      A[0] = ec;
+    } else {
+      A[2 * m - 1] = ec;
+      A[2 * m] = es;
+    }
+  });
+}
+
+template <int NU>
+__device__ __forceinline__ float ipow(float v) {
+  if constexpr (NU == 1) {
+    return v;
+  } else if constexpr (NU % 2 == 0) {
+    const float h = ipow<NU / 2>(v);
+    return h * h;
+  } else {
+    return v * ipow<NU - 1>(v);
+  }
+}
+
+// One node: phi synthesis of both functions, pointwise product (or power),
+// phi analysis of the product's moments m <= LE.
+template <int L1, int L2, int LE, int NP, int NU>
+__device__ __forceinline__ void node_product(const float (&A)[2 * L1 + 1], const float (&B)[2 * L2 + 1],
+                                             float (&C)[2 * LE + 1]) {
+  float F[NP];
+  phi_synth<L1, NP>(A, F);
+  if constexpr (NU == 0) {
+    float G[NP];
+    phi_synth<L2, NP>(B, G);
+    sfor<0, NP>([&](auto KK) { F[decltype(KK)::value] *= G[decltype(KK)::value]; });
+  } else {
+    sfor<0, NP>([&](auto KK) { F[decltype(KK)::value] = ipow<NU>(F[decltype(KK)::value]); });
+  }
+  phi_analysis<LE, NP>(F, C);
+}
+
+// Degree bookkeeping of one product stage.  NU = 0: x1 (deg L1) times x2
+// (deg L2); NU >= 2: x1^NU (L2 unused).
+template <int L1, int L2, int LO, int NU>
+struct Geo {
+  static constexpr int U = NU == 0 ? L1 + L2 : NU * L1;
+  static constexpr int LE = cmin(LO, U);
+  static constexpr int NT = U + 1;
+  static constexpr int NJ = NT + 1;
+  static constexpr int NP = U + LE + 1;
+  static constexpr int KE = csh(LE);
+};
+
+// acc (degree <= LE) = product of xa and xb (or xa^NU) for one lane.
+template <int L1, int L2, int LO, int NU>
+__device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float (&xb)[csh(L2)],
+                                         float (&acc)[Geo<L1, L2, LO, NU>::KE], const float* __restrict__ S,
+                                         const float* __restrict__ W) {
+  using G = Geo<L1, L2, LO, NU>;
+  constexpr int LE = G::LE, NT = G::NT, NJ = G::NJ, NP = G::NP;
+  sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+
+  // Poles (t = 0 and t = pi): only m = 0 is non-zero; the phi samples are all
+  // equal, so the m = 0 moment is NP times the product value.
+  {
+    float ae = 0.0f, ao = 0.0f, be = 0.0f, bo = 0.0f;
+    sfor<0, L1 + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float sv = S[ctri(l, 0) * NJ];
+      if constexpr (l % 2 == 0) ae = fmaf(sv, xa[l * l + l], ae);
+      else ao = fmaf(sv, xa[l * l + l], ao);
+    });
+    float fn, fs;
+    if constexpr (NU == 0) {
+      sfor<0, L2 + 1>([&](auto LL) {
+        constexpr int l = decltype(LL)::value;
+        const float sv = S[ctri(l, 0) * NJ];
+        if constexpr (l % 2 == 0) be = fmaf(sv, xb[l * l + l], be);
+        else bo = fmaf(sv, xb[l * l + l], bo);
+      });
+      fn = (ae + ao) * (be + bo);
+      fs = (ae - ao) * (be - bo);
+    } else {
+      fn = ipow<NU>(ae + ao);
+      fs = ipow<NU>(ae - ao);
+    }
+    const float ce = float(NP) * (fn + fs), co = float(NP) * (fn - fs);
+    sfor<0, LE + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float w = W[ctri(l, 0) * NJ];
+      acc[l * l + l] = fmaf(w, (l % 2 == 0) ? ce : co, acc[l * l + l]);
+    });
+  }
+
+  // Interior mirror pairs (j, NT - j), 1 <= j < NT / 2.
+  for (int j = 1; 2 * j < NT; ++j) {
+    float Aj[2 * L1 + 1], Ajp[2 * L1 + 1];
+    float Bj[2 * L2 + 1], Bjp[2 * L2 + 1];
+    theta_synth_pair<L1, NJ>(xa, S, j, Aj, Ajp);
+    if constexpr (NU == 0) theta_synth_pair<L2, NJ>(xb, S, j, Bj, Bjp);
+    float Cj[2 * LE + 1], Cjp[2 * LE + 1];
+    node_product<L1, L2, LE, NP, NU>(Aj, Bj, Cj);
+    node_product<L1, L2, LE, NP, NU>(Ajp, Bjp, Cjp);
+    sfor<0, LE + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value;
+      constexpr int mc = m == 0 ? 0 : 2 * m - 1;
+      const float ecs = Cj[mc] + Cjp[mc], ocs = Cj[mc] - Cjp[mc];
+      float ess = 0.0f, oss = 0.0f;
+      if constexpr (m > 0) {
+        ess = Cj[2 * m] + Cjp[2 * m];
+        oss = Cj[2 * m] - Cjp[2 * m];
+      }
+      sfor<m, LE + 1>([&](auto LL) {
+        constexpr int l = decltype(LL)::value;
+        const float w = W[ctri(l, m) * NJ + j];
+        constexpr bool even = (l + m) % 2 == 0;
+        acc[l * l + l + m] = fmaf(w, even ? ecs : ocs, acc[l * l + l + m]);
+        if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, even ? ess : oss, acc[l * l + l - m]);
+      });
+    });
+  }
+
+  // Equator node when NT is even.
+  if constexpr (NT % 2 == 0) {
+    constexpr int j = NT / 2;
+    float A[2 * L1 + 1], B[2 * L2 + 1];
+    theta_synth_eq<L1, NJ>(xa, S, j, A);
+    if constexpr (NU == 0) theta_synth_eq<L2, NJ>(xb, S, j, B);
+    float Cq[2 * LE + 1];
+    node_product<L1, L2, LE, NP, NU>(A, B, Cq);
+    sfor<0, LE + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value;
+      sfor<m, LE + 1>([&](auto LL) {
+        constexpr int l = decltype(LL)::value;
+        if constexpr ((l + m) % 2 == 0) {
+          const float w = W[ctri(l, m) * NJ + j];
+          acc[l * l + l + m] = fmaf(w, Cq[m == 0 ? 0 : 2 * m - 1], acc[l * l + l + m]);
+          if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, Cq[2 * m], acc[l * l + l - m]);
+        }
+      });
+    });
+  }
+}
+
+constexpr int kTile = 64;  // products per workgroup (one wave)
+
+// Coalesced load of a [kTile, K] slab through LDS into per-lane registers.
+template <int K, typename TIn>
+__device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0, int cnt, float* tile,
+                                          float (&r)[K]) {
+  const int tid = threadIdx.x;
+  const int64_t base = p0 * K;
+  for (int i = tid; i < kTile * K; i += kTile) tile[i] = (i < cnt * K) ? ld_in(x, base + i) : 0.0f;
+  __syncthreads();
+  sfor<0, K>([&](auto I) { r[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
+  __syncthreads();
+}
+
+template <int KO, int KE>
+__device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, int cnt, float* tile,
+                                           const float (&acc)[KE]) {
+  const int tid = threadIdx.x;
+  sfor<0, KO>([&](auto I) {
+    constexpr int i = decltype(I)::value;
+    tile[tid * KO + i] = (i < KE) ? acc[i < KE ? i : 0] : 0.0f;
+  });
+  __syncthreads();
+  float* out = y + p0 * KO;
+  for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
+}
+
+template <int L1, int L2, int LO, int NU, typename TIn>
+__global__ __launch_bounds__(kTile) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
+                                                      float* __restrict__ y, int64_t n,
+                                                      const float* __restrict__ S, const float* __restrict__ W) {
+  using G = Geo<L1, L2, LO, NU>;
+  constexpr int K1 = csh(L1), K2 = NU == 0 ? csh(L2) : 1, KO = csh(LO);
+  constexpr int KT = cmax(cmax(K1, K2), KO);
+  __shared__ float tile[kTile * KT];
+  const int64_t p0 = int64_t(blockIdx.x) * kTile;
+  const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
+  float xa[K1];
+  load_rows<K1>(x1, p0, cnt, tile, xa);
+  float xb[csh(L2)];
+  if constexpr (NU == 0) {
+    load_rows<K2>(x2, p0, cnt, tile, xb);
+  } else {
+    sfor<0, csh(L2)>([&](auto I) { xb[decltype(I)::value] = 0.0f; });
+  }
+  float acc[G::KE];
+  gtp_core<L1, L2, LO, NU>(xa, xb, acc, S, W);
+  store_rows<KO, G::KE>(y, p0, cnt, tile, acc);
+}
+
+// Stepwise many-body chain: B_2 = P_LO(A A), B_{k+1} = P_LO(B_k A).
+template <int L, int LO, typename TIn>
+__global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __restrict__ x, float* __restrict__ y,
+                                                               int64_t n, int nu, const float* __restrict__ S1,
+                                                               const float* __restrict__ W1,
+                                                               const float* __restrict__ S2,
+                                                               const float* __restrict__ W2) {
+  constexpr int K = csh(L), KO = csh(LO);
+  using G1 = Geo<L, L, LO, 0>;
+  using G2 = Geo<LO, L, LO, 0>;
+  constexpr int KT = cmax(K, KO);
+  __shared__ float tile[kTile * KT];
+  const int64_t p0 = int64_t(blockIdx.x) * kTile;
+  const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
+  float a[K];
+  load_rows<K>(x, p0, cnt, tile, a);
+  float b[KO];
+  {
+    float acc[G1::KE];
+    gtp_core<L, L, LO, 0>(a, a, acc, S1, W1);
+    sfor<0, KO>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      b[i] = i < G1::KE ? acc[i < G1::KE ? i : 0] : 0.0f;
+    });
+  }
+  for (int step = 2; step < nu; ++step) {
+    float acc[G2::KE];
+    gtp_core<LO, L, LO, 0>(b, a, acc, S2, W2);
+    sfor<0, KO>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      b[i] = i < G2::KE ? acc[i < G2::KE ? i : 0] : 0.0f;
+    });
+  }
+  store_rows<KO, KO>(y, p0, cnt, tile, b);
+}
+
+template <int L1, int L2, int LO, int NU>
+hipError_t launch_one(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                      hipStream_t s) {
+  const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
+  if (in_type == IN_BF16)
+    hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, uint16_t>), grid, block, 0, s,
+                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n, t.S, t.W);
+  else
+    hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, float>), grid, block, 0, s, static_cast<const float*>(x1),
+                       static_cast<const float*>(x2), y, n, t.S, t.W);
+  return hipGetLastError();
+}
+
+template <int L, int LO>
+hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const void* x, int in_type, int64_t n,
+                        float* y, hipStream_t s) {
+  const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
+  if (in_type == IN_BF16)
+    hipLaunchKernelGGL((k_self_stepwise_small<L, LO, uint16_t>), grid, block, 0, s,
+                       static_cast<const uint16_t*>(x), y, n, nu, t1.S, t1.W, t2.S, t2.W);
+  else
+    hipLaunchKernelGGL((k_self_stepwise_small<L, LO, float>), grid, block, 0, s, static_cast<const float*>(x), y,
+                       n, nu, t1.S, t1.W, t2.S, t2.W);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// (L1, L2, Lout) pair products and (L, nu, Lout) fused powers with a
+// thread-per-product instantiation.  Everything else takes the generic path.
+#define GTP_SMALL_PAIRS(X) \
+  X(1, 1, 1) X(2, 2, 2) X(3, 3, 3) X(4, 4, 4) X(5, 5, 5) X(6, 6, 6) X(2, 2, 3) X(3, 2, 3) X(1, 2, 2) X(2, 1, 3)
+#define GTP_SMALL_POWERS(X) X(2, 2, 3) X(2, 3, 3) X(2, 4, 3) X(1, 3, 2) X(3, 3, 3)
+#define GTP_SMALL_CHAINS(X) X(2, 3) X(1, 2) X(3, 3) X(2, 2)
+
+hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                             int nu, hipStream_t s, bool* supported) {
+  *supported = true;
+  if (nu == 0) {
+#define GTP_CASE(a, b, c) \
+  if (t.L1 == a && t.L2 == b && t.Lout == c) return launch_one<a, b, c, 0>(t, x1, x2, in_type, n, y, s);
+    GTP_SMALL_PAIRS(GTP_CASE)
+#undef GTP_CASE
+  } else {
+    // power plans are built as (L, (nu - 1) L, Lout)
+#define GTP_CASE(a, v, c) \
+  if (nu == v && t.L1 == a && t.L2 == (v - 1) * a && t.Lout == c) return launch_one<a, 0, c, v>(t, x1, x1, in_type, n, y, s);
+    GTP_SMALL_POWERS(GTP_CASE)
+#undef GTP_CASE
+  }
+  *supported = false;
+  return hipSuccess;
+}
+
+hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x, int in_type,
+                                      int64_t n, float* y, hipStream_t s, bool* supported) {
+  *supported = true;
+#define GTP_CASE(a, c) \
+  if (t1.L1 == a && t1.L2 == a && t1.Lout == c && t2.L1 == c && t2.L2 == a && t2.Lout == c) \
+    return launch_chain<a, c>(t1, t2, nu, x, in_type, n, y, s);
+  GTP_SMALL_CHAINS(GTP_CASE)
+#undef GTP_CASE
+  *supported = false;
+  return hipSuccess;
+}
+
+}  // namespace gtp

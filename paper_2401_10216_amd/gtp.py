@@ -1,0 +1,227 @@
+"""Thin ctypes binding of libgtp.so (the C ABI in include/gtp.h).
+
+Only argument marshalling happens here: every step of the Gaunt tensor
+product runs in the library's HIP kernels.  Tensors are torch CUDA (HIP)
+tensors; the current torch stream is passed to the library.  If the library
+is not built the import of any entry point raises -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libgtp.so")
+
+GTP_OK, GTP_ERR_INVALID_ARG, GTP_ERR_UNSUPPORTED, GTP_ERR_NO_DEVICE, GTP_ERR_HIP, GTP_ERR_ALLOC = range(6)
+GTP_F32, GTP_BF16 = 0, 1
+GTP_CONV_AUTO, GTP_CONV_DIRECT, GTP_CONV_FFT = 0, 1, 2
+GTP_PLAN_HOST_ONLY = 16
+GTP_FORCE_GENERIC = 32  # internal: use the workgroup-per-product kernel
+GTP_SELF_STEPWISE, GTP_SELF_FUSED = 0, 1
+
+_lib = None
+_lock = threading.Lock()
+
+
+class GTPError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{_STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_STATUS = {0: "GTP_OK", 1: "GTP_ERR_INVALID_ARG", 2: "GTP_ERR_UNSUPPORTED", 3: "GTP_ERR_NO_DEVICE",
+           4: "GTP_ERR_HIP", 5: "GTP_ERR_ALLOC"}
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I = ctypes.c_int
+_U = ctypes.c_uint
+_DP = ctypes.POINTER(ctypes.c_double)
+
+_SIGS = {
+    "gtp_plan_create": (_I, [ctypes.POINTER(_P), _I, _I, _I, _U]),
+    "gtp_plan_destroy": (_I, [_P]),
+    "gtp_full": (_I, [_P, _P, _P, _I, _I64, _I64, _P, _P]),
+    "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
+    "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
+    "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
+    "gtp_selfproduct": (_I, [_I, _I, _I, _U, _P, _I, _I64, _I64, _P, _P]),
+    "gtp_sh_filter": (_I, [_I, _P, _P, _I64, _I64, _P, _P]),
+    "gtp_grid_floats": (_I64, [_P, _I]),
+    "gtp_plan_info": (_I, [_P, ctypes.POINTER(_I64)]),
+    "gtp_plan_table": (_I, [_P, _I, _DP, ctypes.POINTER(_I64)]),
+    "gtp_debug_host_pipeline": (_I, [_P, _DP, _DP, _I64, _DP]),
+    "gtp_status_str": (ctypes.c_char_p, [_I]),
+    "gtp_last_error": (ctypes.c_char_p, []),
+}
+
+
+def lib():
+    """Load libgtp.so once (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2401_10216_amd.build`")
+            L = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in _SIGS.items():
+                f = getattr(L, name)
+                f.restype = res
+                f.argtypes = args
+            _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != GTP_OK:
+        raise GTPError(status, lib().gtp_last_error().decode())
+
+
+def _stream(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(t):
+    import torch
+    if t.dtype == torch.float32:
+        return GTP_F32
+    if t.dtype == torch.bfloat16:
+        return GTP_BF16
+    raise TypeError(f"unsupported input dtype {t.dtype} (float32 or bfloat16)")
+
+
+def _dev(t, name):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def nsh(L: int) -> int:
+    return (L + 1) * (L + 1)
+
+
+class Plan:
+    """gtp_plan_create / gtp_plan_destroy."""
+
+    def __init__(self, L1: int, L2: int, Lout: int, flags: int = 0):
+        self.L1, self.L2, self.Lout, self.flags = L1, L2, Lout, flags
+        h = _P()
+        _check(lib().gtp_plan_create(ctypes.byref(h), L1, L2, Lout, flags))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None) is not None and self.handle.value:
+            lib().gtp_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def info(self) -> dict:
+        out = (_I64 * 8)()
+        _check(lib().gtp_plan_info(self.handle, out))
+        keys = ["L1", "L2", "Lout", "U", "Le", "NT", "NP", "conv"]
+        return dict(zip(keys, [int(v) for v in out]))
+
+    def table(self, which: int):
+        import numpy as np
+        cnt = _I64(0)
+        _check(lib().gtp_plan_table(self.handle, which, None, ctypes.byref(cnt)))
+        buf = np.zeros(cnt.value, dtype=np.float64)
+        _check(lib().gtp_plan_table(self.handle, which, buf.ctypes.data_as(_DP), ctypes.byref(cnt)))
+        return buf
+
+    def grid_floats(self, which: int) -> int:
+        return int(lib().gtp_grid_floats(self.handle, which))
+
+
+def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
+    """y[B,C,(Lout+1)^2] = Gaunt tensor product of x1[B,C,(L1+1)^2] and x2[B,C,(L2+1)^2]."""
+    import torch
+    if x1.dtype != x2.dtype:
+        raise TypeError("x1 and x2 must have the same dtype")
+    if x1.dim() != 3 or x2.dim() != 3 or x1.shape[:2] != x2.shape[:2]:
+        raise ValueError("x1, x2 must be [B, C, K] with equal B, C")
+    if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2):
+        raise ValueError("coefficient dimension does not match the plan")
+    B, C = int(x1.shape[0]), int(x1.shape[1])
+    if y is None:
+        y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
+    _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
+                          _stream(stream)))
+    return y
+
+
+def gtp_sh2fourier(plan: Plan, which: int, x, grid=None, stream=None):
+    """Complex grids [n, 2L+1, 2L+1] (as torch.complex64) of x[n, (L+1)^2]."""
+    import torch
+    L = plan.L1 if which == 1 else plan.L2
+    n = int(x.shape[0])
+    if grid is None:
+        grid = torch.empty((n, 2 * L + 1, 2 * L + 1), dtype=torch.complex64, device=x.device)
+    _check(lib().gtp_sh2fourier(plan.handle, which, _dev(x, "x"), _dtype_code(x), n, _dev(grid, "grid"),
+                                _stream(stream)))
+    return grid
+
+
+def gtp_fourier_conv(plan: Plan, g1, g2, g3=None, stream=None):
+    import torch
+    n = int(g1.shape[0])
+    D3 = 2 * (plan.L1 + plan.L2) + 1
+    if g3 is None:
+        g3 = torch.empty((n, D3, D3), dtype=torch.complex64, device=g1.device)
+    _check(lib().gtp_fourier_conv(plan.handle, _dev(g1, "g1"), _dev(g2, "g2"), n, _dev(g3, "g3"), _stream(stream)))
+    return g3
+
+
+def gtp_fourier2sh(plan: Plan, g3, y=None, stream=None):
+    import torch
+    n = int(g3.shape[0])
+    if y is None:
+        y = torch.empty((n, nsh(plan.Lout)), dtype=torch.float32, device=g3.device)
+    _check(lib().gtp_fourier2sh(plan.handle, _dev(g3, "g3"), n, _dev(y, "y"), _stream(stream)))
+    return y
+
+
+def gtp_selfproduct(x, L: int, nu: int, Lout: int, mode: int = GTP_SELF_STEPWISE, y=None, stream=None):
+    import torch
+    if x.dim() != 3 or x.shape[2] != nsh(L):
+        raise ValueError("x must be [B, C, (L+1)^2]")
+    B, C = int(x.shape[0]), int(x.shape[1])
+    if y is None:
+        y = torch.empty((B, C, nsh(Lout)), dtype=torch.float32, device=x.device)
+    _check(lib().gtp_selfproduct(L, nu, Lout, mode, _dev(x, "x"), _dtype_code(x), B, C, _dev(y, "y"),
+                                 _stream(stream)))
+    return y
+
+
+def gtp_sh_filter(L: int, r, h=None, out=None, stream=None):
+    """out[B,C,(L+1)^2] = h[B,C,L+1] * Y(r_b); h=None gives Y(r) with C = 1."""
+    import torch
+    B = int(r.shape[0])
+    C = 1 if h is None else int(h.shape[1])
+    if out is None:
+        out = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=r.device)
+    hp = ctypes.c_void_p(None) if h is None else _dev(h, "h")
+    _check(lib().gtp_sh_filter(L, _dev(r, "r"), hp, B, C, _dev(out, "out"), _stream(stream)))
+    return out
+
+
+def gtp_debug_host_pipeline(plan: Plan, x1, x2):
+    """fp64 host evaluation of the plan's sampled pipeline (table check only)."""
+    import numpy as np
+    a = np.ascontiguousarray(x1, dtype=np.float64).reshape(-1, nsh(plan.L1))
+    b = np.ascontiguousarray(x2, dtype=np.float64).reshape(-1, nsh(plan.L2))
+    y = np.zeros((a.shape[0], nsh(plan.Lout)), dtype=np.float64)
+    _check(lib().gtp_debug_host_pipeline(plan.handle, a.ctypes.data_as(_DP), b.ctypes.data_as(_DP), a.shape[0],
+                                         y.ctypes.data_as(_DP)))
+    return y

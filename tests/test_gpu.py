@@ -1,0 +1,290 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Bar (per product): max_i |y_gpu - y_ref| / ||y_ref||_2 <= 1e-5 for fp32 inputs
+and <= 2e-2 for the bf16-input workload (oracle fed the same bf16-rounded
+values).  Small sizes compare every output; full-size workloads compare a
+seeded subsample of products that the oracle computes one by one."""
+import math
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import gtp_oracle as O
+from paper_2401_10216_amd import gtp, inputs
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+torch = pytest.importorskip("torch")
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    gtp.lib()
+    return torch.device("cuda:0")
+
+
+def dev(a, dtype=torch.float32):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device="cuda:0", dtype=dtype)
+
+
+def oracle_pair(a, b, L1, L2, Lout):
+    if max(L1, L2, Lout) <= 8:
+        return O.gtp(a, b, L1, L2, Lout)
+    return O.gtp_grid(a, b, L1, L2, Lout)
+
+
+def run_full(plan, a, b):
+    y = gtp.gtp_full(plan, dev(a), dev(b))
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+# ------------------------------------------------------------------ small workloads, every output
+
+def test_tiny_workload_every_output():
+    cfg = inputs.WORKLOADS["tiny"]
+    x1, x2 = inputs.pair_inputs(cfg["index"], cfg["B"], cfg["C"], 2, 2)
+    ref = O.gtp(x1, x2, 2, 2, 2)
+    for flags in (0, gtp.GTP_FORCE_GENERIC):
+        _say(f"tiny B=1024 C=1 L=2 flags={flags}")
+        y = run_full(gtp.Plan(2, 2, 2, flags), x1, x2)
+        assert y.shape == (1024, 1, 9)
+        err = O.max_rel_err(y, ref)
+        assert err <= TOL, err
+
+
+PAIRS = [(0, 0, 0), (1, 1, 1), (2, 2, 2), (3, 3, 3), (4, 4, 4), (5, 5, 5), (6, 6, 6), (2, 2, 3), (3, 2, 3),
+         (1, 2, 2), (2, 1, 3), (1, 0, 1), (0, 3, 2), (2, 3, 9), (6, 6, 2), (7, 7, 7), (8, 8, 8), (4, 6, 5),
+         (10, 3, 7), (12, 12, 12)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout", PAIRS)
+@pytest.mark.parametrize("generic", [False, True])
+def test_pair_products_ragged(L1, L2, Lout, generic):
+    n = 64 * 17 + 37  # several tiles and a ragged tail
+    rng = np.random.default_rng(7 + L1 + 17 * L2 + 289 * Lout)
+    a = rng.standard_normal((n, 1, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L2))).astype(np.float32)
+    _say(f"pair L1={L1} L2={L2} Lout={Lout} generic={generic} n={n}")
+    plan = gtp.Plan(L1, L2, Lout, gtp.GTP_FORCE_GENERIC if generic else 0)
+    y = run_full(plan, a, b)
+    ref = oracle_pair(a.astype(np.float64), b.astype(np.float64), L1, L2, Lout)
+    err = O.max_rel_err(y, ref)
+    assert err <= TOL, err
+    if Lout > L1 + L2:
+        assert np.all(y[..., O.nsh(L1 + L2):] == 0)
+
+
+def test_bf16_inputs():
+    L = 6
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal((2, 3000, 1, O.nsh(L))).astype(np.float32)
+    bits1, v1 = inputs.round_to_bf16(x[0])
+    bits2, v2 = inputs.round_to_bf16(x[1])
+    _say("bf16 L=6")
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    for flags in (0, gtp.GTP_FORCE_GENERIC):
+        y = gtp.gtp_full(gtp.Plan(L, L, L, flags), t1, t2)
+        torch.cuda.synchronize()
+        ref = O.gtp(v1.astype(np.float64), v2.astype(np.float64), L, L, L)
+        err = O.max_rel_err(y.cpu().numpy(), ref)
+        _say(f"  bf16 flags={flags} err={err:.3e}")
+        assert err <= 2e-2
+        assert err <= 1e-4  # bf16 values are exact in fp32: only fp32 arithmetic error remains
+
+
+def test_empty_and_single():
+    plan = gtp.Plan(3, 3, 3)
+    a = torch.zeros((0, 4, 16), device="cuda:0")
+    y = gtp.gtp_full(plan, a, a)
+    assert y.shape == (0, 4, 16)
+    rng = np.random.default_rng(3)
+    a = rng.standard_normal((1, 1, 16)).astype(np.float32)
+    b = rng.standard_normal((1, 1, 16)).astype(np.float32)
+    y = run_full(plan, a, b)
+    assert O.max_rel_err(y, O.gtp(a, b, 3, 3, 3)) <= TOL
+
+
+def test_deterministic_and_streams():
+    L = 6
+    rng = np.random.default_rng(5)
+    a = dev(rng.standard_normal((4096, 1, 49)))
+    b = dev(rng.standard_normal((4096, 1, 49)))
+    plan = gtp.Plan(L, L, L)
+    y1 = gtp.gtp_full(plan, a, b)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        y2 = gtp.gtp_full(plan, a, b)
+    torch.cuda.synchronize()
+    assert torch.equal(y1, y2)
+
+
+# ------------------------------------------------------------------ the three stages
+
+@pytest.mark.parametrize("L1,L2,Lout", [(2, 2, 2), (1, 3, 4), (3, 2, 1), (0, 2, 2), (5, 5, 5), (4, 2, 9)])
+def test_stages_match_oracle(L1, L2, Lout):
+    rng = np.random.default_rng(21 + L1 + 7 * L2 + 49 * Lout)
+    n = 300
+    a = rng.standard_normal((n, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((n, O.nsh(L2))).astype(np.float32)
+    _say(f"stages L1={L1} L2={L2} Lout={Lout}")
+    plan = gtp.Plan(L1, L2, Lout)
+    g1 = gtp.gtp_sh2fourier(plan, 1, dev(a))
+    g2 = gtp.gtp_sh2fourier(plan, 2, dev(b))
+    g3 = gtp.gtp_fourier_conv(plan, g1, g2)
+    y = gtp.gtp_fourier2sh(plan, g3)
+    yf = gtp.gtp_full(plan, dev(a)[:, None], dev(b)[:, None])
+    torch.cuda.synchronize()
+    r1 = O.sh2fourier(a.astype(np.float64), L1)
+    r2 = O.sh2fourier(b.astype(np.float64), L2)
+    e1 = (np.abs(g1.cpu().numpy() - r1) / np.linalg.norm(r1.reshape(n, -1), axis=1)[:, None, None]).max()
+    e2 = (np.abs(g2.cpu().numpy() - r2) / np.linalg.norm(r2.reshape(n, -1), axis=1)[:, None, None]).max()
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+    # conv stage on the oracle's own grids (rounded to complex64 like the device input)
+    r3 = O.fourier_conv(r1.astype(np.complex64).astype(np.complex128), r2.astype(np.complex64).astype(np.complex128))
+    g3b = gtp.gtp_fourier_conv(plan, dev(r1.astype(np.complex64), torch.complex64),
+                               dev(r2.astype(np.complex64), torch.complex64))
+    torch.cuda.synchronize()
+    e3 = (np.abs(g3b.cpu().numpy() - r3) / np.linalg.norm(r3.reshape(n, -1), axis=1)[:, None, None]).max()
+    assert e3 <= TOL, e3
+    # projection stage on the oracle's product grid
+    yref = O.fourier2sh(r3, L1 + L2, Lout).real
+    yb = gtp.gtp_fourier2sh(plan, dev(r3.astype(np.complex64), torch.complex64))
+    torch.cuda.synchronize()
+    assert O.max_rel_err(yb.cpu().numpy(), yref) <= TOL
+    # the unfused chain and the fused kernel both give the Gaunt product
+    ref = O.gtp(a.astype(np.float64), b.astype(np.float64), L1, L2, Lout)
+    assert O.max_rel_err(y.cpu().numpy(), ref) <= TOL
+    assert O.max_rel_err(yf.cpu().numpy()[:, 0], ref) <= TOL
+
+
+def test_fourier2sh_of_arbitrary_grid_takes_real_part():
+    """A grid that is not of a real function: the result is Re of the projection."""
+    L1, L2, Lout = 1, 1, 2
+    rng = np.random.default_rng(31)
+    g = (rng.standard_normal((50, 5, 5)) + 1j * rng.standard_normal((50, 5, 5))).astype(np.complex64)
+    plan = gtp.Plan(L1, L2, Lout)
+    y = gtp.gtp_fourier2sh(plan, dev(g, torch.complex64))
+    torch.cuda.synchronize()
+    ref = O.fourier2sh(g.astype(np.complex128), 2, Lout).real
+    assert O.max_rel_err(y.cpu().numpy(), ref) <= TOL
+
+
+# ------------------------------------------------------------------ SH filter
+
+def test_sh_filter_matches_oracle():
+    L = 6
+    rng = np.random.default_rng(41)
+    r = rng.standard_normal((500, 3)).astype(np.float32)
+    h = rng.standard_normal((500, 3, L + 1)).astype(np.float32)
+    out = gtp.gtp_sh_filter(L, dev(r), dev(h))
+    Y = gtp.gtp_sh_filter(L, dev(r))
+    torch.cuda.synchronize()
+    Yref = O.real_sh_xyz(L, r.astype(np.float64))
+    deg = inputs.degree_of_index(L)
+    ref = h[..., deg] * Yref[:, None, :]
+    assert np.abs(Y.cpu().numpy()[:, 0] - Yref).max() < 1e-6
+    assert np.abs(out.cpu().numpy() - ref).max() < 1e-5
+
+
+# ------------------------------------------------------------------ full-size workloads (sampled)
+
+def test_edge_workload_full_size_sampled():
+    cfg = inputs.WORKLOADS["edge"]
+    B, C, L = cfg["B"], cfg["C"], cfg["L1"]
+    _say("edge workload: generating inputs")
+    x1, r, h = inputs.edge_inputs(B, C, L)
+    t1 = dev(x1)
+    tr = dev(r.astype(np.float32))
+    th = dev(h)
+    x2 = gtp.gtp_sh_filter(L, tr, th)
+    del th
+    plan = gtp.Plan(L, L, L)
+    _say("edge workload: gtp_full B=65536 C=128 L=6")
+    y = gtp.gtp_full(plan, t1, x2)
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(cfg["index"], B * C, 4096)
+    bi, ci = idx // C, idx % C
+    yf = y.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    x2s = x2.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    deg = inputs.degree_of_index(L)
+    x2ref = h[bi, ci][:, deg] * O.real_sh_xyz(L, r[bi])
+    assert np.abs(x2s - x2ref).max() < 1e-5
+    ref = O.gtp(x1[bi, ci].astype(np.float64), x2ref, L, L, L)
+    err = O.max_rel_err(yf, ref)
+    _say(f"edge workload sampled err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("mode", [gtp.GTP_SELF_STEPWISE, gtp.GTP_SELF_FUSED])
+def test_manybody_workload_full(mode):
+    cfg = inputs.WORKLOADS["manybody"]
+    x = inputs.manybody_inputs(cfg["B"], cfg["C"], cfg["L"])
+    _say(f"manybody mode={mode}")
+    y = gtp.gtp_selfproduct(dev(x), cfg["L"], cfg["nu"], cfg["Lout"], mode)
+    torch.cuda.synchronize()
+    ref = O.selfproduct(x.astype(np.float64), cfg["L"], cfg["nu"], cfg["Lout"],
+                        "stepwise" if mode == gtp.GTP_SELF_STEPWISE else "fused")
+    err = O.max_rel_err(y.cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("L,nu,Lout,mode", [(1, 3, 2, 0), (3, 3, 3, 0), (2, 2, 2, 0), (2, 4, 3, 0), (4, 3, 4, 0),
+                                            (2, 1, 3, 0), (2, 3, 3, 1), (1, 3, 2, 1), (3, 3, 3, 1), (4, 3, 4, 1),
+                                            (2, 5, 3, 1), (3, 2, 4, 1)])
+def test_selfproduct_variants(L, nu, Lout, mode):
+    rng = np.random.default_rng(51 + L + 10 * nu + 100 * Lout + 1000 * mode)
+    x = rng.standard_normal((700, 1, O.nsh(L))).astype(np.float32)
+    _say(f"selfproduct L={L} nu={nu} Lout={Lout} mode={mode}")
+    y = gtp.gtp_selfproduct(dev(x), L, nu, Lout, mode)
+    torch.cuda.synchronize()
+    ref = O.selfproduct(x.astype(np.float64), L, nu, Lout, "stepwise" if mode == 0 else "fused")
+    err = O.max_rel_err(y.cpu().numpy(), ref)
+    assert err <= TOL, err
+
+
+@pytest.mark.parametrize("L,n", [(4, 262144), (8, 262144), (16, 262144), (32, 16384), (64, 1024)])
+def test_sweep_sampled(L, n):
+    x1, x2 = inputs.sweep_inputs(L)
+    x1 = x1.reshape(-1, O.nsh(L))[:n]
+    x2 = x2.reshape(-1, O.nsh(L))[:n]
+    _say(f"sweep L={L} n={n}")
+    plan = gtp.Plan(L, L, L)
+    y = gtp.gtp_full(plan, dev(x1)[:, None], dev(x2)[:, None])
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(4, n, 256 if L >= 32 else 1024)
+    yf = y[torch.from_numpy(idx).cuda(), 0].cpu().numpy()
+    ref = oracle_pair(x1[idx].astype(np.float64), x2[idx].astype(np.float64), L, L, L)
+    err = O.max_rel_err(yf, ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL
+
+
+def test_highdeg_bf16_sampled():
+    cfg = inputs.WORKLOADS["highdeg"]
+    B, C, L = 4096, cfg["C"], cfg["L1"]  # a slice of the B=32768 workload
+    b1, b2, v1, v2 = inputs.highdeg_inputs(cfg["B"], C, L)
+    b1, b2, v1, v2 = b1[:B], b2[:B], v1[:B], v2[:B]
+    _say("highdeg bf16 L=16")
+    t1 = torch.from_numpy(b1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(b2.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_full(gtp.Plan(L, L, L), t1, t2)
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(cfg["index"], B * C, 512)
+    yf = y.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    ref = O.gtp_grid(v1.reshape(B * C, -1)[idx].astype(np.float64), v2.reshape(B * C, -1)[idx].astype(np.float64),
+                     L, L, L)
+    err = O.max_rel_err(yf, ref)
+    _say(f"  err={err:.3e}")
+    assert err <= 2e-2
