@@ -140,10 +140,21 @@ def make_workload(args, torch, gtp, inputs):
         desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
         return step, N * C, desc, ALG_FLOPS_MANYBODY, 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
+    if w == "copy":
+        # plain device copy of a known size: calibrates the HBM byte counters
+        nbytes = 1 << 30
+        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+
+        def step():
+            dst.copy_(src)
+
+        desc = {"workload": "copy: 1 GiB fp32 device-to-device copy (HBM counter calibration)", "bytes": nbytes}
+        return step, nbytes, desc, None, 2, None, 0
     raise SystemExit(f"unknown workload {w}")
 
 
-def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=12.0):
+def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     """Time the oracle on a seeded subsample sized to roughly budget_s seconds."""
     try:
         from threadpoolctl import threadpool_info
@@ -157,7 +168,7 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=12.0):
         t0 = time.perf_counter()
         ref = fn()
         dt = time.perf_counter() - t0
-        if dt >= budget_s / 4 or n >= total:
+        if dt >= 0.6 * budget_s or n >= total:
             break
         n = int(min(total, max(2 * n, n * budget_s / max(dt, 1e-3))))
     import torch
@@ -218,6 +229,10 @@ def main():
                         "unit": "GB/s", "alg_bytes_per_product": alg_bytes}}
         roof["hbm"]["frac"] = round(roof["hbm"]["achieved"] / PEAK_HBM_GBS, 4)
 
+    if args.workload == "copy":
+        print(json.dumps({"workload": "copy", "bytes_per_step": products, "ms_per_step": kernel_ms,
+                          "GBps_read_plus_write": 2 * products / (kernel_ms * 1e-3) / 1e9}), flush=True)
+        return
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import gtp_oracle as O

@@ -69,9 +69,12 @@ gtp_status upload(gtp_plan_* p) {
   const gtp::Tables& t = p->tab;
   const int nmp = 2 * t.Mphi + 1;
   const int ntE = ntri(t.Le);
-  std::vector<float> WT(size_t(t.NJ) * ntE), PhiT(size_t(t.NP) * nmp);
+  const int ntS = ntri(t.Lin);
+  std::vector<float> WT(size_t(t.NJ) * ntE), ST(size_t(t.NJ) * ntS), PhiT(size_t(t.NP) * nmp);
   for (int r = 0; r < ntE; ++r)
     for (int j = 0; j < t.NJ; ++j) WT[size_t(j) * ntE + r] = float(t.W[size_t(r) * t.NJ + j]);
+  for (int r = 0; r < ntS; ++r)
+    for (int j = 0; j < t.NJ; ++j) ST[size_t(j) * ntS + r] = float(t.S[size_t(r) * t.NJ + j]);
   for (int mp = 0; mp < nmp; ++mp)
     for (int k = 0; k < t.NP; ++k) PhiT[size_t(k) * nmp + mp] = float(t.Phi[size_t(mp) * t.NP + k]);
   auto up = [&](const std::vector<double>* src64, const std::vector<float>* src32, const float** dst) -> gtp_status {
@@ -94,6 +97,9 @@ gtp_status upload(gtp_plan_* p) {
   if ((s = up(&t.S, nullptr, &d.S)) != GTP_OK) return s;
   if ((s = up(&t.W, nullptr, &d.W)) != GTP_OK) return s;
   if ((s = up(nullptr, &WT, &d.WT)) != GTP_OK) return s;
+  if ((s = up(nullptr, &ST, &d.ST)) != GTP_OK) return s;
+  d.ntS = ntS;
+  d.ntW = ntE;
   if ((s = up(&t.Phi, nullptr, &d.Phi)) != GTP_OK) return s;
   if ((s = up(nullptr, &PhiT, &d.PhiT)) != GTP_OK) return s;
   if ((s = up(&t.T1, nullptr, &d.T1)) != GTP_OK) return s;

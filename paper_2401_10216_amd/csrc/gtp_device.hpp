@@ -13,7 +13,9 @@ struct DevTables {
   int L1, L2, Lout, U, Le, Lin, NT, NJ, NP, Mphi, ldT1, ldZ;
   const float* S;     // [tri(l<=Lin)][NJ]   Theta_lm at theta nodes
   const float* W;     // [tri(l<=Le)][NJ]    analysis weights
-  const float* WT;    // [NJ][tri(l<=Le)]    transposed W
+  const float* WT;    // [NJ][tri(l<=Le)]    transposed W (node-major)
+  const float* ST;    // [NJ][tri(l<=Lin)]   transposed S (node-major)
+  int ntS, ntW;       // row lengths of ST and WT
   const float* Phi;   // [2 Mphi + 1][NP]    trig(mp, k)
   const float* PhiT;  // [NP][2 Mphi + 1]
   const float* T1;    // [tri(l<=Lt)][ldT1]  theta-Fourier series of Theta_lm

@@ -13,6 +13,11 @@
 
 #include "gtp_device.hpp"
 
+// Scheduling fence between the per-node stages: keeps the two mirror nodes
+// from being interleaved (which costs registers) and keeps the table
+// prefetch behind the LDS reads it would otherwise make wait.
+#define GTP_SCHED_FENCE() __builtin_amdgcn_sched_barrier(0)
+
 namespace gtp {
 namespace {
 
@@ -65,34 +70,67 @@ constexpr int csh(int L) { return (L + 1) * (L + 1); }
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
 
+// Coefficient accessors of one lane's input vector: in registers, or a row of
+// the workgroup's LDS tile.  touch() makes the LDS row offset opaque so the
+// reads stay inside the node loop instead of being hoisted into registers.
+template <int K>
+struct RegX {
+  float (&a)[K];
+  template <class I>
+  __device__ __forceinline__ float operator()(I) const { return a[I::value]; }
+  __device__ __forceinline__ void touch() {}
+};
+struct LdsX {
+  const float* tile;
+  int off;
+  template <class I>
+  __device__ __forceinline__ float operator()(I) const { return tile[off + I::value]; }
+  __device__ __forceinline__ void touch() { asm volatile("" : "+v"(off)); }
+};
+
 __device__ __forceinline__ float ld_in(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld_in(const uint16_t* p, int64_t i) {
   return __uint_as_float(uint32_t(p[i]) << 16);
 }
 
-// F[k] = A0 + sum_m A[2m-1] cos(m p_k) + A[2m] sin(m p_k), k < NP.
+// phi grid p_k = 2 pi k / NP with NP = 4Q.  The points k, -k, 2Q + k, 2Q - k
+// share |cos(m p)| and |sin(m p)|, with signs set by the parity of m, so both
+// transforms work on the quarter 0 <= k <= Q and fan out.
+
+// F[k] = A0 + sum_m A[2m-1] cos(m p_k) + A[2m] sin(m p_k), k < NP, for a
+// function of phi-degree <= M.
 template <int M, int NP>
 __device__ __forceinline__ void phi_synth(const float (&A)[2 * M + 1], float (&F)[NP]) {
-  sfor<0, NP / 2 + 1>([&](auto KK) {
+  static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
+  constexpr int Q = NP / 4;
+  sfor<0, Q + 1>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
-    constexpr bool mirror = (k > 0) && (2 * k != NP);
-    float e = A[0];
+    // partial sums over even / odd m of the cos and sin parts
+    float pe = A[0], po = 0.0f, qe = 0.0f, qo = 0.0f;
     sfor<1, M + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
-      if constexpr (c != 0.0f) e = fmaf(A[2 * m - 1], c, e);
+      constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
+      if constexpr (m % 2 == 0) {
+        if constexpr (c != 0.0f) pe = fmaf(A[2 * m - 1], c, pe);
+        if constexpr (sn != 0.0f) qe = fmaf(A[2 * m], sn, qe);
+      } else {
+        if constexpr (c != 0.0f) po = fmaf(A[2 * m - 1], c, po);
+        if constexpr (sn != 0.0f) qo = fmaf(A[2 * m], sn, qo);
+      }
     });
-    if constexpr (mirror) {
-      float o = 0.0f;
-      sfor<1, M + 1>([&](auto MM) {
-        constexpr int m = decltype(MM)::value;
-        constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
-        if constexpr (sn != 0.0f) o = fmaf(A[2 * m], sn, o);
-      });
-      F[k] = e + o;
-      F[NP - k] = e - o;
+    if constexpr (k == 0) {
+      F[0] = pe + po;
+      F[2 * Q] = pe - po;
+    } else if constexpr (k == Q) {
+      F[Q] = pe + qo;  // cos(odd m pi/2) = sin(even m pi/2) = 0
+      F[3 * Q] = pe - qo;
     } else {
-      F[k] = e;
+      const float s1 = pe + po, d1 = pe - po, s2 = qe + qo, d2 = qe - qo;
+      F[k] = s1 + s2;
+      F[NP - k] = s1 - s2;
+      F[2 * Q + k] = d1 + d2;
+      F[2 * Q - k] = d1 - d2;
     }
   });
 }
@@ -100,62 +138,57 @@ __device__ __forceinline__ void phi_synth(const float (&A)[2 * M + 1], float (&F
 // C[0] = sum_k F_k, C[2m-1] = sum_k F_k cos(m p_k), C[2m] = sum_k F_k sin(m p_k), m <= MO.
 template <int MO, int NP>
 __device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 * MO + 1]) {
-  constexpr int H = NP / 2;
-  float P[H + 1], D[H + 1];
-  P[0] = F[0];
-  D[0] = 0.0f;
-  sfor<1, H + 1>([&](auto KK) {
+  static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
+  constexpr int Q = NP / 4;
+  sfor<0, 2 * MO + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
+  sfor<0, Q + 1>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
-    if constexpr (2 * k == NP) {
-      P[k] = F[k];
-      D[k] = 0.0f;
+    // even-m / odd-m folds of the four points sharing this quarter angle
+    float ce, co, se = 0.0f, so = 0.0f;
+    if constexpr (k == 0) {
+      ce = F[0] + F[2 * Q];
+      co = F[0] - F[2 * Q];
+    } else if constexpr (k == Q) {
+      ce = F[Q] + F[3 * Q];
+      co = 0.0f;
+      so = F[Q] - F[3 * Q];
     } else {
-      P[k] = F[k] + F[NP - k];
-      D[k] = F[k] - F[NP - k];
+      const float a = F[k] + F[NP - k], b = F[2 * Q + k] + F[2 * Q - k];
+      const float d = F[k] - F[NP - k], e = F[2 * Q + k] - F[2 * Q - k];
+      ce = a + b;
+      co = a - b;
+      se = d + e;
+      so = d - e;
     }
-  });
-  sfor<0, MO + 1>([&](auto MM) {
-    constexpr int m = decltype(MM)::value;
-    float cs = 0.0f;
-    sfor<0, H + 1>([&](auto KK) {
-      constexpr int k = decltype(KK)::value;
+    sfor<0, MO + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value;
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
-      if constexpr (c != 0.0f) cs = fmaf(P[k], c, cs);
+      constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
+      constexpr int ic = m == 0 ? 0 : 2 * m - 1;
+      if constexpr (c != 0.0f) C[ic] = fmaf((m % 2 == 0) ? ce : co, c, C[ic]);
+      if constexpr (m > 0 && sn != 0.0f) C[2 * m] = fmaf((m % 2 == 0) ? se : so, sn, C[2 * m]);
     });
-    if constexpr (m == 0) {
-      C[0] = cs;
-    } else {
-      float sn = 0.0f;
-      sfor<1, H + 1>([&](auto KK) {
-        constexpr int k = decltype(KK)::value;
-        if constexpr (2 * k != NP) {
-          constexpr float s = ct_round(ct_sin2pi((long long)m * k, NP));
-          if constexpr (s != 0.0f) sn = fmaf(D[k], s, sn);
-        }
-      });
-      C[2 * m - 1] = cs;
-      C[2 * m] = sn;
-    }
   });
 }
 
 // Theta synthesis at the mirror pair (t_j, t_{NT-j}) of one input of degree
-// L: even-parity and odd-parity (l + m) partial sums give both nodes.
-template <int L, int NJ>
-__device__ __forceinline__ void theta_synth_pair(const float (&x)[csh(L)], const float* __restrict__ S, int j,
-                                                 float (&Aj)[2 * L + 1], float (&Ajp)[2 * L + 1]) {
+// L: even-parity and odd-parity (l + m) partial sums give both nodes.  x(I)
+// returns coefficient I; ST row j holds Theta_lm(t_j) for all (l, m).
+template <int L, typename X, typename T>
+__device__ __forceinline__ void theta_synth_pair(X x, const T& Sj, float (&Aj)[2 * L + 1],
+                                                 float (&Ajp)[2 * L + 1]) {
   sfor<0, L + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     float ec = 0.0f, oc = 0.0f, es = 0.0f, os = 0.0f;
     sfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
-      const float sv = S[ctri(l, m) * NJ + j];
+      const float sv = Sj[ctri(l, m)];
       if constexpr ((l + m) % 2 == 0) {
-        ec = fmaf(sv, x[l * l + l + m], ec);
-        if constexpr (m > 0) es = fmaf(sv, x[l * l + l - m], es);
+        ec = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), ec);
+        if constexpr (m > 0) es = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), es);
       } else {
-        oc = fmaf(sv, x[l * l + l + m], oc);
-        if constexpr (m > 0) os = fmaf(sv, x[l * l + l - m], os);
+        oc = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), oc);
+        if constexpr (m > 0) os = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), os);
       }
     });
     if constexpr (m == 0) {
@@ -170,19 +203,56 @@ __device__ __forceinline__ void theta_synth_pair(const float (&x)[csh(L)], const
   });
 }
 
+// Theta synthesis at one node of the mirror pair: MIRROR = false gives t_j,
+// MIRROR = true gives t_{NT-j} (Theta_lm picks up (-1)^(l+m)).
+template <int L, bool MIRROR, typename X, typename T>
+__device__ __forceinline__ void theta_synth_node(X x, const T& Sj, float (&A)[2 * L + 1]) {
+  sfor<0, L + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    float ec = 0.0f, es = 0.0f;
+    sfor<m, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float sv = (MIRROR && (l + m) % 2) ? -Sj[ctri(l, m)] : Sj[ctri(l, m)];
+      ec = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), ec);
+      if constexpr (m > 0) es = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), es);
+    });
+    if constexpr (m == 0) {
+      A[0] = ec;
+    } else {
+      A[2 * m - 1] = ec;
+      A[2 * m] = es;
+    }
+  });
+}
+
+// acc += W(t_j) * C for the moments C of one node; MIRROR uses the weights of
+// t_{NT-j}, which are (-1)^(l+m) times those of t_j.
+template <int LE, bool MIRROR, typename T>
+__device__ __forceinline__ void theta_analysis_node(const T& Wj, const float (&C)[2 * LE + 1],
+                                                    float (&acc)[(LE + 1) * (LE + 1)]) {
+  sfor<0, LE + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    sfor<m, LE + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float w = (MIRROR && (l + m) % 2) ? -Wj[ctri(l, m)] : Wj[ctri(l, m)];
+      acc[l * l + l + m] = fmaf(w, C[m == 0 ? 0 : 2 * m - 1], acc[l * l + l + m]);
+      if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, C[2 * m], acc[l * l + l - m]);
+    });
+  });
+}
+
 // Theta synthesis at the equator (only even l + m survive).
-template <int L, int NJ>
-__device__ __forceinline__ void theta_synth_eq(const float (&x)[csh(L)], const float* __restrict__ S, int j,
-                                               float (&A)[2 * L + 1]) {
+template <int L, typename X>
+__device__ __forceinline__ void theta_synth_eq(X x, const float* __restrict__ Sj, float (&A)[2 * L + 1]) {
   sfor<0, L + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     float ec = 0.0f, es = 0.0f;
     sfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       if constexpr ((l + m) % 2 == 0) {
-        const float sv = S[ctri(l, m) * NJ + j];
-        ec = fmaf(sv, x[l * l + l + m], ec);
-        if constexpr (m > 0) es = fmaf(sv, x[l * l + l - m], es);
+        const float sv = Sj[ctri(l, m)];
+        ec = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), ec);
+        if constexpr (m > 0) es = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), es);
       }
     });
     if constexpr (m == 0) {
@@ -231,17 +301,19 @@ struct Geo {
   static constexpr int LE = cmin(LO, U);
   static constexpr int NT = U + 1;
   static constexpr int NJ = NT + 1;
-  static constexpr int NP = U + LE + 1;
+  static constexpr int NP = (U + LE + 1 + 3) / 4 * 4;  // same rule as the host tables
   static constexpr int KE = csh(LE);
 };
 
 // acc (degree <= LE) = product of xa and xb (or xa^NU) for one lane.
-template <int L1, int L2, int LO, int NU>
-__device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float (&xb)[csh(L2)],
-                                         float (&acc)[Geo<L1, L2, LO, NU>::KE], const float* __restrict__ S,
-                                         const float* __restrict__ W) {
+// xa(I), xb(I) return input coefficient I; ST / WT are the node-major
+// synthesis and analysis tables with row lengths ntS / ntW.
+template <int L1, int L2, int LO, int NU, typename XA, typename XB>
+__device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, LO, NU>::KE],
+                                         const float* __restrict__ ST, int ntS, const float* __restrict__ WT,
+                                         int ntW) {
   using G = Geo<L1, L2, LO, NU>;
-  constexpr int LE = G::LE, NT = G::NT, NJ = G::NJ, NP = G::NP;
+  constexpr int LE = G::LE, NT = G::NT, NP = G::NP;
   sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
 
   // Poles (t = 0 and t = pi): only m = 0 is non-zero; the phi samples are all
@@ -250,17 +322,17 @@ __device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float
     float ae = 0.0f, ao = 0.0f, be = 0.0f, bo = 0.0f;
     sfor<0, L1 + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
-      const float sv = S[ctri(l, 0) * NJ];
-      if constexpr (l % 2 == 0) ae = fmaf(sv, xa[l * l + l], ae);
-      else ao = fmaf(sv, xa[l * l + l], ao);
+      const float sv = ST[ctri(l, 0)];
+      if constexpr (l % 2 == 0) ae = fmaf(sv, xa(std::integral_constant<int, l * l + l>{}), ae);
+      else ao = fmaf(sv, xa(std::integral_constant<int, l * l + l>{}), ao);
     });
     float fn, fs;
     if constexpr (NU == 0) {
       sfor<0, L2 + 1>([&](auto LL) {
         constexpr int l = decltype(LL)::value;
-        const float sv = S[ctri(l, 0) * NJ];
-        if constexpr (l % 2 == 0) be = fmaf(sv, xb[l * l + l], be);
-        else bo = fmaf(sv, xb[l * l + l], bo);
+        const float sv = ST[ctri(l, 0)];
+        if constexpr (l % 2 == 0) be = fmaf(sv, xb(std::integral_constant<int, l * l + l>{}), be);
+        else bo = fmaf(sv, xb(std::integral_constant<int, l * l + l>{}), bo);
       });
       fn = (ae + ao) * (be + bo);
       fs = (ae - ao) * (be - bo);
@@ -271,45 +343,62 @@ __device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float
     const float ce = float(NP) * (fn + fs), co = float(NP) * (fn - fs);
     sfor<0, LE + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
-      const float w = W[ctri(l, 0) * NJ];
+      const float w = WT[ctri(l, 0)];
       acc[l * l + l] = fmaf(w, (l % 2 == 0) ? ce : co, acc[l * l + l]);
     });
   }
 
   // Interior mirror pairs (j, NT - j), 1 <= j < NT / 2.
+  // The node-pair tables are software-pipelined through scalar registers:
+  // S of pair j + 1 and W of pair j are requested after the first LDS reads
+  // of pair j (LDS reads share the scalar loads' wait counter) and arrive
+  // while the phi transforms of pair j run.
+  constexpr int NS = ctri(cmax(L1, L2), cmax(L1, L2)) + 1;
+  constexpr int NW = ctri(LE, LE) + 1;
+  float scur[NS];
+  sfor<0, NS>([&](auto I) { scur[decltype(I)::value] = ST[ntS + decltype(I)::value]; });
   for (int j = 1; 2 * j < NT; ++j) {
+    xa.touch();
+    xb.touch();
+    // x1 at both mirror nodes from shared even / odd partial sums; x2 node by
+    // node (fewer live registers), its first node before the table prefetch
     float Aj[2 * L1 + 1], Ajp[2 * L1 + 1];
-    float Bj[2 * L2 + 1], Bjp[2 * L2 + 1];
-    theta_synth_pair<L1, NJ>(xa, S, j, Aj, Ajp);
-    if constexpr (NU == 0) theta_synth_pair<L2, NJ>(xb, S, j, Bj, Bjp);
-    float Cj[2 * LE + 1], Cjp[2 * LE + 1];
-    node_product<L1, L2, LE, NP, NU>(Aj, Bj, Cj);
-    node_product<L1, L2, LE, NP, NU>(Ajp, Bjp, Cjp);
-    sfor<0, LE + 1>([&](auto MM) {
-      constexpr int m = decltype(MM)::value;
-      constexpr int mc = m == 0 ? 0 : 2 * m - 1;
-      const float ecs = Cj[mc] + Cjp[mc], ocs = Cj[mc] - Cjp[mc];
-      float ess = 0.0f, oss = 0.0f;
-      if constexpr (m > 0) {
-        ess = Cj[2 * m] + Cjp[2 * m];
-        oss = Cj[2 * m] - Cjp[2 * m];
-      }
-      sfor<m, LE + 1>([&](auto LL) {
-        constexpr int l = decltype(LL)::value;
-        const float w = W[ctri(l, m) * NJ + j];
-        constexpr bool even = (l + m) % 2 == 0;
-        acc[l * l + l + m] = fmaf(w, even ? ecs : ocs, acc[l * l + l + m]);
-        if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, even ? ess : oss, acc[l * l + l - m]);
-      });
-    });
+    float Bj[2 * L2 + 1];
+    theta_synth_pair<L1>(xa, scur, Aj, Ajp);
+    if constexpr (NU == 0) theta_synth_node<L2, false>(xb, scur, Bj);
+    GTP_SCHED_FENCE();
+    float sb[NS];
+    sfor<0, NS>([&](auto I) { sb[decltype(I)::value] = scur[decltype(I)::value]; });
+    // row j + 1 always exists (j + 1 <= NT), even when it is not used
+    const float* Sn = ST + (j + 1) * ntS;
+    sfor<0, NS>([&](auto I) { scur[decltype(I)::value] = Sn[decltype(I)::value]; });
+    const float* Wj = WT + j * ntW;
+    float wcur[NW];
+    sfor<0, NW>([&](auto I) { wcur[decltype(I)::value] = Wj[decltype(I)::value]; });
+    GTP_SCHED_FENCE();
+    {
+      float C[2 * LE + 1];
+      node_product<L1, L2, LE, NP, NU>(Aj, Bj, C);
+      theta_analysis_node<LE, false>(wcur, C, acc);
+    }
+    GTP_SCHED_FENCE();
+    {
+      if constexpr (NU == 0) theta_synth_node<L2, true>(xb, sb, Bj);
+      float C[2 * LE + 1];
+      node_product<L1, L2, LE, NP, NU>(Ajp, Bj, C);
+      theta_analysis_node<LE, true>(wcur, C, acc);
+    }
+    GTP_SCHED_FENCE();
   }
 
   // Equator node when NT is even.
   if constexpr (NT % 2 == 0) {
     constexpr int j = NT / 2;
+    const float* Sj = ST + j * ntS;
+    const float* Wj = WT + j * ntW;
     float A[2 * L1 + 1], B[2 * L2 + 1];
-    theta_synth_eq<L1, NJ>(xa, S, j, A);
-    if constexpr (NU == 0) theta_synth_eq<L2, NJ>(xb, S, j, B);
+    theta_synth_eq<L1>(xa, Sj, A);
+    if constexpr (NU == 0) theta_synth_eq<L2>(xb, Sj, B);
     float Cq[2 * LE + 1];
     node_product<L1, L2, LE, NP, NU>(A, B, Cq);
     sfor<0, LE + 1>([&](auto MM) {
@@ -317,7 +406,7 @@ __device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float
       sfor<m, LE + 1>([&](auto LL) {
         constexpr int l = decltype(LL)::value;
         if constexpr ((l + m) % 2 == 0) {
-          const float w = W[ctri(l, m) * NJ + j];
+          const float w = Wj[ctri(l, m)];
           acc[l * l + l + m] = fmaf(w, Cq[m == 0 ? 0 : 2 * m - 1], acc[l * l + l + m]);
           if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, Cq[2 * m], acc[l * l + l - m]);
         }
@@ -327,6 +416,9 @@ __device__ __forceinline__ void gtp_core(const float (&xa)[csh(L1)], const float
 }
 
 constexpr int kTile = 64;  // products per workgroup (one wave)
+#ifndef GTP_SMALL_WAVES
+#define GTP_SMALL_WAVES 3  // waves per SIMD the register budget is sized for
+#endif
 
 // Coalesced load of a [kTile, K] slab through LDS into per-lane registers.
 template <int K, typename TIn>
@@ -354,35 +446,39 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
 }
 
 template <int L1, int L2, int LO, int NU, typename TIn>
-__global__ __launch_bounds__(kTile) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
+__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(GTP_SMALL_WAVES))) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
-                                                      const float* __restrict__ S, const float* __restrict__ W) {
+                                                      const float* __restrict__ ST, int ntS,
+                                                      const float* __restrict__ WT, int ntW) {
   using G = Geo<L1, L2, LO, NU>;
   constexpr int K1 = csh(L1), K2 = NU == 0 ? csh(L2) : 1, KO = csh(LO);
   constexpr int KT = cmax(cmax(K1, K2), KO);
   __shared__ float tile[kTile * KT];
+  const int tid = threadIdx.x;
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float xa[K1];
   load_rows<K1>(x1, p0, cnt, tile, xa);
-  float xb[csh(L2)];
-  if constexpr (NU == 0) {
-    load_rows<K2>(x2, p0, cnt, tile, xb);
-  } else {
-    sfor<0, csh(L2)>([&](auto I) { xb[decltype(I)::value] = 0.0f; });
-  }
+  RegX<K1> A{xa};
   float acc[G::KE];
-  gtp_core<L1, L2, LO, NU>(xa, xb, acc, S, W);
+  if constexpr (NU == 0) {
+    // x2 stays in LDS, row-major with an odd row length (conflict-free reads)
+    const int64_t base = p0 * K2;
+    for (int i = tid; i < kTile * K2; i += kTile) tile[i] = (i < cnt * K2) ? ld_in(x2, base + i) : 0.0f;
+    __syncthreads();
+    LdsX B{tile, tid * K2};
+    gtp_core<L1, L2, LO, NU>(A, B, acc, ST, ntS, WT, ntW);
+    __syncthreads();
+  } else {
+    gtp_core<L1, L2, LO, NU>(A, A, acc, ST, ntS, WT, ntW);
+  }
   store_rows<KO, G::KE>(y, p0, cnt, tile, acc);
 }
 
 // Stepwise many-body chain: B_2 = P_LO(A A), B_{k+1} = P_LO(B_k A).
 template <int L, int LO, typename TIn>
 __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __restrict__ x, float* __restrict__ y,
-                                                               int64_t n, int nu, const float* __restrict__ S1,
-                                                               const float* __restrict__ W1,
-                                                               const float* __restrict__ S2,
-                                                               const float* __restrict__ W2) {
+                                                               int64_t n, int nu, DevTables t1, DevTables t2) {
   constexpr int K = csh(L), KO = csh(LO);
   using G1 = Geo<L, L, LO, 0>;
   using G2 = Geo<LO, L, LO, 0>;
@@ -395,7 +491,8 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   float b[KO];
   {
     float acc[G1::KE];
-    gtp_core<L, L, LO, 0>(a, a, acc, S1, W1);
+    RegX<K> A{a};
+    gtp_core<L, L, LO, 0>(A, A, acc, t1.ST, t1.ntS, t1.WT, t1.ntW);
     sfor<0, KO>([&](auto I) {
       constexpr int i = decltype(I)::value;
       b[i] = i < G1::KE ? acc[i < G1::KE ? i : 0] : 0.0f;
@@ -403,7 +500,9 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   }
   for (int step = 2; step < nu; ++step) {
     float acc[G2::KE];
-    gtp_core<LO, L, LO, 0>(b, a, acc, S2, W2);
+    RegX<K> A{a};
+    RegX<KO> Bv{b};
+    gtp_core<LO, L, LO, 0>(Bv, A, acc, t2.ST, t2.ntS, t2.WT, t2.ntW);
     sfor<0, KO>([&](auto I) {
       constexpr int i = decltype(I)::value;
       b[i] = i < G2::KE ? acc[i < G2::KE ? i : 0] : 0.0f;
@@ -418,10 +517,11 @@ hipError_t launch_one(const DevTables& t, const void* x1, const void* x2, int in
   const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
   if (in_type == IN_BF16)
     hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, uint16_t>), grid, block, 0, s,
-                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n, t.S, t.W);
+                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n, t.ST, t.ntS, t.WT,
+                       t.ntW);
   else
     hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, float>), grid, block, 0, s, static_cast<const float*>(x1),
-                       static_cast<const float*>(x2), y, n, t.S, t.W);
+                       static_cast<const float*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW);
   return hipGetLastError();
 }
 
@@ -431,10 +531,10 @@ hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const 
   const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
   if (in_type == IN_BF16)
     hipLaunchKernelGGL((k_self_stepwise_small<L, LO, uint16_t>), grid, block, 0, s,
-                       static_cast<const uint16_t*>(x), y, n, nu, t1.S, t1.W, t2.S, t2.W);
+                       static_cast<const uint16_t*>(x), y, n, nu, t1, t2);
   else
     hipLaunchKernelGGL((k_self_stepwise_small<L, LO, float>), grid, block, 0, s, static_cast<const float*>(x), y,
-                       n, nu, t1.S, t1.W, t2.S, t2.W);
+                       n, nu, t1, t2);
   return hipGetLastError();
 }
 

@@ -64,8 +64,9 @@ Tables build_tables(int L1, int L2, int Lout) {
   t.NT = t.U + 1;
   t.NJ = t.NT + 1;
   // The product has phi frequencies <= U; reading moments m <= Le from NP
-  // uniform samples is alias-free when NP > U + Le.
-  t.NP = t.U + t.Le + 1;
+  // uniform samples is alias-free when NP > U + Le.  NP is rounded up to a
+  // multiple of 4 so that the phi grid is closed under p -> -p, p -> pi +- p.
+  t.NP = (t.U + t.Le + 1 + 3) / 4 * 4;
   t.ldT1 = t.Lt + 1;
   t.ldZ = t.NT + 1;
 

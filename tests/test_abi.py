@@ -107,10 +107,10 @@ def test_host_pipeline_equals_oracle(L1, L2, Lout):
 def test_plan_info_geometry():
     p = host_plan(6, 6, 6)
     i = p.info()
-    assert (i["U"], i["Le"], i["NT"], i["NP"]) == (12, 6, 13, 19)
+    assert (i["U"], i["Le"], i["NT"], i["NP"]) == (12, 6, 13, 20)
     p = host_plan(2, 1, 7)
     i = p.info()
-    assert (i["U"], i["Le"], i["NT"], i["NP"]) == (3, 3, 4, 7)
+    assert (i["U"], i["Le"], i["NT"], i["NP"]) == (3, 3, 4, 8)
     assert p.grid_floats(1) == 2 * 25 and p.grid_floats(2) == 2 * 9 and p.grid_floats(3) == 2 * 49
     assert p.grid_floats(4) == -1
 
