@@ -241,6 +241,8 @@ gtp_status gtp_full(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dty
   if (!p->force_generic) {
     e = gtp::launch_full_small(p->dev, x1, x2, it, n, y, 0, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+    e = gtp::launch_full_large(p->dev, x1, x2, it, n, y, st, &done);
+    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
   }
   e = gtp::launch_full_generic(p->dev, x1, it, x2, it, n, y, 0, st);
   return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");

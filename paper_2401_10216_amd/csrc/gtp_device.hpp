@@ -34,6 +34,10 @@ hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2,
 // instantiated (L, nu, Lout); t1 = tables of (L, L, Lout), t2 = (Lout, L, Lout).
 hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x,
                                       int in_type, int64_t n, float* y, hipStream_t s, bool* supported);
+// Wave-per-product fused kernel for L1 = L2 = Lout = L in {16, 32};
+// *supported = false otherwise.
+hipError_t launch_full_large(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                             hipStream_t s, bool* supported);
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,

@@ -416,9 +416,9 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
 }
 
 constexpr int kTile = 64;  // products per workgroup (one wave)
-#ifndef GTP_SMALL_WAVES
-#define GTP_SMALL_WAVES 3  // waves per SIMD the register budget is sized for
-#endif
+// Waves per SIMD the register budget is sized for: x1 and the accumulators
+// stay in registers, so the budget shrinks with the degree.
+constexpr int small_waves(int L1, int L2, int LO) { return (L1 > 6 || L2 > 6 || LO > 6) ? 2 : 3; }
 
 // Coalesced load of a [kTile, K] slab through LDS into per-lane registers.
 template <int K, typename TIn>
@@ -446,7 +446,7 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
 }
 
 template <int L1, int L2, int LO, int NU, typename TIn>
-__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(GTP_SMALL_WAVES))) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
+__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
                                                       const float* __restrict__ ST, int ntS,
                                                       const float* __restrict__ WT, int ntW) {
@@ -543,7 +543,8 @@ hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const 
 // (L1, L2, Lout) pair products and (L, nu, Lout) fused powers with a
 // thread-per-product instantiation.  Everything else takes the generic path.
 #define GTP_SMALL_PAIRS(X) \
-  X(1, 1, 1) X(2, 2, 2) X(3, 3, 3) X(4, 4, 4) X(5, 5, 5) X(6, 6, 6) X(2, 2, 3) X(3, 2, 3) X(1, 2, 2) X(2, 1, 3)
+  X(1, 1, 1) X(2, 2, 2) X(3, 3, 3) X(4, 4, 4) X(5, 5, 5) X(6, 6, 6) X(7, 7, 7) X(8, 8, 8) X(2, 2, 3) X(3, 2, 3) X(1, 2, 2) \
+      X(2, 1, 3)
 #define GTP_SMALL_POWERS(X) X(2, 2, 3) X(2, 3, 3) X(2, 4, 3) X(1, 3, 2) X(3, 3, 3)
 #define GTP_SMALL_CHAINS(X) X(2, 3) X(1, 2) X(3, 3) X(2, 2)
 

@@ -84,6 +84,24 @@ def test_pair_products_ragged(L1, L2, Lout, generic):
         assert np.all(y[..., O.nsh(L1 + L2):] == 0)
 
 
+@pytest.mark.parametrize("L,n", [(16, 2 * 300 + 1), (32, 257)])
+@pytest.mark.parametrize("generic", [False, True])
+def test_large_degree_ragged(L, n, generic):
+    """Wave-per-product kernel (several products per wave at L = 16, an odd
+    count leaves a partly filled last wave) against the oracle, and the
+    workgroup-per-product kernel on the same inputs."""
+    rng = np.random.default_rng(70 + L)
+    a = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    _say(f"large L={L} n={n} generic={generic}")
+    y = run_full(gtp.Plan(L, L, L, gtp.GTP_FORCE_GENERIC if generic else 0), a, b)
+    idx = np.arange(0, n, 7)
+    ref = O.gtp_grid(a[idx].astype(np.float64), b[idx].astype(np.float64), L, L, L)
+    err = O.max_rel_err(y[idx], ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
 def test_bf16_inputs():
     L = 6
     rng = np.random.default_rng(11)
