@@ -105,6 +105,25 @@ gtp_status upload(gtp_plan_* p) {
   if ((s = up(&t.T1, nullptr, &d.T1)) != GTP_OK) return s;
   if ((s = up(&t.Zc, nullptr, &d.Zc)) != GTP_OK) return s;
   if ((s = up(&t.Zs, nullptr, &d.Zs)) != GTP_OK) return s;
+  d.waveL = t.waveL;
+  d.SM = d.TWS = d.TWA = d.SMP = d.SM0P = d.WP = nullptr;
+  d.XMAP = nullptr;
+  d.XQUADS = t.XQUADS;
+  if (t.waveL) {
+    if ((s = up(&t.SM, nullptr, &d.SM)) != GTP_OK) return s;
+    if ((s = up(&t.TWS, nullptr, &d.TWS)) != GTP_OK) return s;
+    if ((s = up(&t.TWA, nullptr, &d.TWA)) != GTP_OK) return s;
+    if ((s = up(&t.SMP, nullptr, &d.SMP)) != GTP_OK) return s;
+    if ((s = up(&t.SM0P, nullptr, &d.SM0P)) != GTP_OK) return s;
+    if ((s = up(&t.WP, nullptr, &d.WP)) != GTP_OK) return s;
+    int* dm = nullptr;
+    hipError_t e = hipMalloc(&dm, t.XMAPP.size() * sizeof(int));
+    if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMalloc: ") + hipGetErrorString(e));
+    p->dbufs.push_back(reinterpret_cast<float*>(dm));
+    e = hipMemcpy(dm, t.XMAPP.data(), t.XMAPP.size() * sizeof(int), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy");
+    d.XMAP = dm;
+  }
   return GTP_OK;
 }
 
@@ -405,7 +424,10 @@ gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
     case 2: src = &p->tab.Zs; break;
     case 3: src = &p->tab.S; break;
     case 4: src = &p->tab.W; break;
-    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..4");
+    case 5: src = &p->tab.SM; break;
+    case 6: src = &p->tab.TWS; break;
+    case 7: src = &p->tab.TWA; break;
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..7");
   }
   if (!buf) {
     *count = int64_t(src->size());

@@ -21,6 +21,17 @@ struct DevTables {
   const float* T1;    // [tri(l<=Lt)][ldT1]  theta-Fourier series of Theta_lm
   const float* Zc;    // [tri(l<=Le)][ldZ]
   const float* Zs;    // [tri(l<=Le)][ldZ]
+  // Operand tables of the matrix-core wave kernel (L1 = L2 = Lout = waveL in
+  // {16, 32}; null and waveL = 0 otherwise).
+  int waveL;
+  const float* SM;    // [m][idx][jp]          Theta_{m+d,m} at nodes 0..L
+  const float* TWS;   // [lane][type][mb][s]   phi synthesis operands
+  const float* TWA;   // [lane][type][mb][r]   phi analysis operands (+ m = 0 weights)
+  const float* SMP;   // [pass][s][u2][lane][4] lane-permuted theta synthesis values
+  const float* SM0P;  // [pass][lane][v]       lane-permuted m = 0 values (+ pole)
+  const float* WP;    // [pass][it][lane][8]   lane-permuted analysis weights
+  const int* XMAP;    // [lane][k]             LDS slot of input coefficient lane + 64 k
+  int XQUADS;
 };
 
 enum InType : int { IN_F32 = 0, IN_BF16 = 1 };

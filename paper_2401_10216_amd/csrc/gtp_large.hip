@@ -44,6 +44,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t table_rsrc(const float* p, int
 __device__ __forceinline__ float tload(__amdgpu_buffer_rsrc_t r, int byte_off) {
   return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));  // raw bits -> float
 }
+// same with a wave-uniform part of the offset in a scalar register
+__device__ __forceinline__ float tload_s(__amdgpu_buffer_rsrc_t r, int byte_off, int uniform_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, uniform_off, 0));
+}
+// 16-byte table read (byte_off a multiple of 16)
+__device__ __forceinline__ float4 tload4_s(__amdgpu_buffer_rsrc_t r, int byte_off, int uniform_off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, uniform_off, 0);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
 
 __device__ __forceinline__ float ld_in_any(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
@@ -317,11 +326,378 @@ hipError_t launch_large_one(const DevTables& t, const void* x1, const void* x2, 
   return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// Matrix-core variant (L in {16, 32}).  One 64-lane wave per product, lane =
+// 16 g + i, i = 8 h + pi.  The phi stage at every theta node is a set of small
+// dense contractions whose operands are shared by all nodes and products, so
+// it runs on the fp32 MFMA units (16x16x4: A = phi operand table, B = theta
+// synthesis values; the 16 columns are the 8 mirror pairs of a pass, column
+// pi = node jp, column 8 + pi = node NT - jp):
+//   synthesis  pe/po/qe/qo[k][node] = sum over the even/odd-m cos/sin parts
+//              of trig(m phi_k) * value[m][node], k = 0..Q (4-fold phi
+//              symmetry as in the direct kernel: points k, -k, 2Q - k, 2Q + k);
+//   product    the four sample products folded into ce/co/se/so[k][node];
+//   analysis   C[m][node] = sum_k w_k trig(m phi_k) * {ce, co, se, so}[k][node]
+//              (w_k = 1/2 at k = 0, Q, where the 4-point sets repeat points).
+// The accumulator layout of one contraction is the B layout of the next
+// (register r of lane (g, i) holds row 4 g + r, column i), so nothing moves
+// between them.  Theta synthesis (VALU) produces the B operands in place: in
+// K-step s lane (g, 8h + pi) sums the m-parts m = 8s + 2g + 1 and + 2 at node
+// jp over the l with l - m = h (mod 2); one exchange between lanes i and i ^ 8
+// then gives node jp (even + odd) and its mirror (even - odd).  Theta analysis
+// (VALU) accumulates per pass.
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int L>
+struct WGeo {
+  static constexpr int NT = 2 * L + 1;
+  static constexpr int NJ = NT + 1;
+  static constexpr int NP = (3 * L + 1 + 3) / 4 * 4;  // host rule with U = 2L, Le = L
+  static constexpr int Q = NP / 4;
+  static constexpr int PASSES = L / 8;               // 8 mirror pairs per pass
+  static constexpr int NKS = L / 8;                  // K-steps per class of m-parts
+  static constexpr int NMB = (Q + 1 + 15) / 16;      // 16-sample blocks of k = 0..Q
+  static constexpr int RS = L + 2;                   // SM row length
+  static constexpr int NC = L + 1;                   // SM columns (nodes 0..L)
+  static constexpr int NMP = 2 * L + 1;
+  static constexpr int K = (L + 1) * (L + 1);
+  static constexpr int EOP = 2 * 8 * NMP;            // floats of one pass's combined moments
+  static constexpr int NROW = (L + 1) * (L + 2) / 2 - (L + 1);  // output rows with m > 0
+  static constexpr int NIT = (NROW + 63) / 64;
+  // u-steps (two degrees each) of K-step s
+  __host__ __device__ static constexpr int nu(int s) { return L / 2 - 4 * s; }
+  // quad offset of the x block of m-pair c = 4 s + g (m = 2c + 1, 2c + 2): the
+  // m = 0 block (L + 1 quads) first, then 4 nu(s) quads + 1 pad per pair
+  __host__ __device__ static constexpr int xb(int c) {
+    return (L + 1) + c + 4 * (4 * ((c / 4) * (L / 2) - 2 * (c / 4) * (c / 4 - 1)) + (c % 4) * nu(c / 4));
+  }
+  static constexpr int XQ = xb(L / 2);
+  // u-step pairs before K-step s, and in all K-steps
+  __host__ __device__ static constexpr int u2off(int s) { return s * (L / 4) - s * (s - 1); }
+  static constexpr int TU2 = u2off(NKS);
+  static constexpr int NV0 = (L + 1 + 7) / 8;          // m = 0 steps of 8 degrees
+  static constexpr int NV0P = (NV0 + 3) / 4 * 4;
+};
+
+// m = 0 theta synthesis reduction: lane (g, 8h + pi) holds the partial sum
+// over l = g + 4h (mod 8); returns the value at the lane's column node (the
+// node itself for h = 0, its mirror, odd l negated, for h = 1).
+__device__ __forceinline__ float m0_reduce(float a, int g, int h) {
+  a += __shfl_xor(a, 8);
+  const float t = __shfl_xor(a, 16);
+  const float sum = a + t, dif = (g & 1) ? t - a : a - t;
+  const float node = sum + __shfl_xor(sum, 32), mirror = dif + __shfl_xor(dif, 32);
+  return h ? mirror : node;
+}
+
+template <int L, typename TIn>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_full_wave(
+    const TIn* __restrict__ x1, const TIn* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+  using G = WGeo<L>;
+  static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
+  constexpr int NJ = G::NJ, NP = G::NP, NMB = G::NMB, NKS = G::NKS, RS = G::RS, NC = G::NC;
+  constexpr int NMP = G::NMP, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
+  __shared__ __align__(16) float xs[G::XQ * 4];
+  __shared__ __align__(16) float eo[G::EOP];
+  const float4* const xq = reinterpret_cast<const float4*>(xs);
+
+  const int lane = threadIdx.x, g = lane >> 4, i = lane & 15, h = i >> 3, pi = i & 7;
+  const int64_t P = blockIdx.x;
+  if (P >= n) return;  // whole-wave exit (one product per workgroup)
+
+  // ---- 0. x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin): every
+  // load is issued before the first wait
+  {
+    constexpr int NXK = (K + 63) / 64, NXKP = (NXK + 3) / 4 * 4;
+    int slot[NXKP];
+    lfor<0, NXKP / 4>([&](auto K4) {
+      constexpr int k4 = decltype(K4)::value;
+      const int4 v = reinterpret_cast<const int4*>(t.XMAP + lane * NXKP)[k4];
+      slot[4 * k4] = v.x;
+      slot[4 * k4 + 1] = v.y;
+      slot[4 * k4 + 2] = v.z;
+      slot[4 * k4 + 3] = v.w;
+    });
+    float v1[NXK], v2[NXK];
+    lfor<0, NXK>([&](auto KK) {
+      constexpr int k = decltype(KK)::value;
+      const int e = lane + 64 * k;
+      if (64 * k + 63 < K || e < K) {
+        v1[k] = ld_in_any(x1, P * K + e);
+        v2[k] = ld_in_any(x2, P * K + e);
+      }
+    });
+    lfor<0, G::XQ / 64>([&](auto Z) {
+      reinterpret_cast<float4*>(xs)[lane + 64 * decltype(Z)::value] = make_float4(0.f, 0.f, 0.f, 0.f);
+    });
+    if (lane < G::XQ % 64) reinterpret_cast<float4*>(xs)[lane + 64 * (G::XQ / 64)] = make_float4(0.f, 0.f, 0.f, 0.f);
+    __syncthreads();
+    lfor<0, NXK>([&](auto KK) {
+      constexpr int k = decltype(KK)::value;
+      if (64 * k + 63 < K || lane + 64 * k < K) {
+        xs[slot[k]] = v1[k];
+        xs[slot[k] + 2] = v2[k];
+      }
+    });
+  }
+  __syncthreads();
+
+  const __amdgpu_buffer_rsrc_t SPr = table_rsrc(t.SMP, PASSES * G::TU2 * 64 * 4);
+  const __amdgpu_buffer_rsrc_t S0r = table_rsrc(t.SM0P, (PASSES + 1) * 64 * G::NV0P);
+  const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
+  const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
+  // m = 0 theta synthesis at the lane's column node (x1 and x2 cos parts);
+  // pass = PASSES gives the poles
+  auto m0_synth = [&](int pass, float& a1, float& a2) {
+    float sv[G::NV0P];
+    lfor<0, G::NV0P / 4>([&](auto V4) {
+      constexpr int v4 = decltype(V4)::value;
+      const float4 w = tload4_s(S0r, lane * G::NV0P * 4 + 16 * v4, pass * 64 * G::NV0P * 4);
+      sv[4 * v4] = w.x;
+      sv[4 * v4 + 1] = w.y;
+      sv[4 * v4 + 2] = w.z;
+      sv[4 * v4 + 3] = w.w;
+    });
+    float s1 = 0.0f, s2 = 0.0f;
+    lfor<0, G::NV0>([&](auto V) {
+      constexpr int v = decltype(V)::value;
+      const int l = 8 * v + g + 4 * h;
+      if (8 * v + 7 <= L || l <= L) {
+        const float4 q = xq[l];
+        s1 = fmaf(sv[v], q.x, s1);
+        s2 = fmaf(sv[v], q.z, s2);
+      }
+    });
+    a1 = m0_reduce(s1, g, h);
+    a2 = m0_reduce(s2, g, h);
+  };
+
+  // theta-analysis rows: tri(l, 0) with l = lane (l <= L), and the rows with
+  // m > 0 numbered q = lane + 64 it; per row the byte offset of its weight
+  // column and the LDS offset of its moment (parity of l + m, m-part)
+  float y0 = 0.0f, yc[NIT], ys[NIT];
+  int er[NIT];
+  const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP;
+  lfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    yc[it] = 0.0f;
+    ys[it] = 0.0f;
+    const int q = lane + 64 * it;
+    int l = int((sqrtf(8.0f * float(q) + 1.0f) + 1.0f) * 0.5f);
+    l -= (l * (l - 1) / 2 > q) ? 1 : 0;
+    l += ((l + 1) * l / 2 <= q) ? 1 : 0;
+    const int m = q - l * (l - 1) / 2 + 1;
+    er[it] = ((l + m) & 1) * 8 * NMP + 2 * m - 1;
+  });
+
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
+    float c1, c2;
+    m0_synth(pu, c1, c2);
+
+    // ---- 1 + 2a. theta synthesis feeding the phi-synthesis contractions
+    f4 acc[2][NMB][4];  // [input][k block][type]
+    lfor<0, NMB>([&](auto MB) {
+      constexpr int mb = decltype(MB)::value;
+      acc[0][mb][0] = f4{c1, c1, c1, c1};  // m = 0 enters every pe sample
+      acc[1][mb][0] = f4{c2, c2, c2, c2};
+      lfor<1, 4>([&](auto TY) {
+        acc[0][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        acc[1][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+      });
+    });
+    lfor<0, NKS>([&](auto SS) {
+      constexpr int s = decltype(SS)::value;
+      const int c = 4 * s + g;
+      // this lane's parity: h = 0 takes (mo, l_a) and (mo+1, l_b), h = 1 (mo, l_b) and (mo+1, l_a)
+      const float4* xa = xq + G::xb(c) + h;
+      const float4* xe = xq + G::xb(c) + 3 - h;
+      float tw[4][NMB];
+      {
+        const f4* src = reinterpret_cast<const f4*>(t.TWS + (lane * NKS + s) * 4 * NMB);
+        lfor<0, NMB>([&](auto Q4) {
+          constexpr int q4 = decltype(Q4)::value;
+          const f4 v = src[q4];
+          tw[(4 * q4 + 0) / NMB][(4 * q4 + 0) % NMB] = v.x;
+          tw[(4 * q4 + 1) / NMB][(4 * q4 + 1) % NMB] = v.y;
+          tw[(4 * q4 + 2) / NMB][(4 * q4 + 2) % NMB] = v.z;
+          tw[(4 * q4 + 3) / NMB][(4 * q4 + 3) % NMB] = v.w;
+        });
+      }
+      f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
+      const int sbase = (pu * G::TU2 + G::u2off(s)) * 64 * 16;
+      lfor<0, G::nu(s) / 2>([&](auto U2) {
+        constexpr int u2 = decltype(U2)::value;
+        const float4 sv = tload4_s(SPr, lane * 16, sbase + u2 * 64 * 16);
+        lfor<0, 2>([&](auto E) {
+          constexpr int u = 2 * u2 + decltype(E)::value;
+          const float so = E == 0 ? sv.x : sv.z, se = E == 0 ? sv.y : sv.w;
+          const float4 qa = xa[4 * u], qe = xe[4 * u];
+          Vo += so * f4{qa.x, qa.y, qa.z, qa.w};
+          Ve += se * f4{qe.x, qe.y, qe.z, qe.w};
+        });
+        if constexpr (u2 % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+      });
+      // column value: node jp (h = 0: own even + partner odd) or its mirror (h = 1: partner even - own odd)
+      f4 Bo, Be;
+      lfor<0, 4>([&](auto C) {
+        constexpr int cc = decltype(C)::value;
+        const float po = __shfl_xor(Vo[cc], 8), pe = __shfl_xor(Ve[cc], 8);
+        Bo[cc] = h ? po - Vo[cc] : po + Vo[cc];
+        Be[cc] = h ? pe - Ve[cc] : pe + Ve[cc];
+      });
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        lfor<0, 2>([&](auto TI) {
+          constexpr int ti = decltype(TI)::value;
+          acc[ti][mb][0] = mfma4(tw[0][mb], Be[2 * ti], acc[ti][mb][0]);
+          acc[ti][mb][1] = mfma4(tw[1][mb], Bo[2 * ti], acc[ti][mb][1]);
+          acc[ti][mb][2] = mfma4(tw[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
+          acc[ti][mb][3] = mfma4(tw[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
+        });
+      });
+    });
+
+    // ---- 2b. sample products, folded over the 4-point sets
+    lfor<0, NMB>([&](auto MB) {
+      constexpr int mb = decltype(MB)::value;
+      const f4 pe1 = acc[0][mb][0], po1 = acc[0][mb][1], qe1 = acc[0][mb][2], qo1 = acc[0][mb][3];
+      const f4 pe2 = acc[1][mb][0], po2 = acc[1][mb][1], qe2 = acc[1][mb][2], qo2 = acc[1][mb][3];
+      const f4 s1 = pe1 + po1, d1 = pe1 - po1, s2 = qe1 + qo1, d2 = qe1 - qo1;
+      const f4 t1 = pe2 + po2, u1 = pe2 - po2, t2 = qe2 + qo2, u2 = qe2 - qo2;
+      const f4 hk = (s1 + s2) * (t1 + t2), hmk = (s1 - s2) * (t1 - t2);
+      const f4 hpk = (d1 + d2) * (u1 + u2), hpmk = (d1 - d2) * (u1 - u2);
+      const f4 a = hk + hmk, b = hpk + hpmk, dd = hk - hmk, ee = hpk - hpmk;
+      acc[0][mb][0] = a + b;
+      acc[0][mb][1] = a - b;
+      acc[0][mb][2] = dd + ee;
+      acc[0][mb][3] = dd - ee;
+    });
+
+    // ---- 2c. phi analysis contractions, then 3. mirror combination into LDS
+    // eo[parity][pi][m-part]: parity 0 = C(jp) + C(NT - jp), 1 = C(jp) - C(NT - jp)
+    float* const eoh = eo + (h * 8 + pi) * NMP;
+    lfor<0, 4>([&](auto TY) {
+      constexpr int ty = decltype(TY)::value;
+      float tw[NMB][4];
+      {
+        const f4* src = reinterpret_cast<const f4*>(t.TWA + (lane * 5 + ty) * NMB * 4);
+        lfor<0, NMB>([&](auto MB) {
+          const f4 v = src[decltype(MB)::value];
+          lfor<0, 4>([&](auto R) { tw[decltype(MB)::value][decltype(R)::value] = v[decltype(R)::value]; });
+        });
+      }
+      f4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        lfor<0, 4>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          o = mfma4(tw[mb][r], acc[0][mb][ty][r], o);
+        });
+      });
+      lfor<0, 4>([&](auto R) {
+        constexpr int r = decltype(R)::value;
+        const int m = 2 * (4 * g + r) + ((ty & 1) ? 1 : 2);
+        const float pv = __shfl_xor(o[r], 8);
+        const float v = h ? pv - o[r] : pv + o[r];
+        if (L == 32 || m <= L) eoh[ty < 2 ? 2 * m - 1 : 2 * m] = v;
+      });
+    });
+    {
+      const f4* src = reinterpret_cast<const f4*>(t.TWA + (lane * 5 + 4) * NMB * 4);
+      float zz = 0.0f;
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        const f4 w = src[mb];
+        lfor<0, 4>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          zz = fmaf(w[r], acc[0][mb][0][r], zz);
+        });
+      });
+      zz += __shfl_xor(zz, 16);
+      zz += __shfl_xor(zz, 32);
+      const float pz = __shfl_xor(zz, 8);
+      if (g == 0) eoh[0] = h ? pz - zz : pz + zz;
+    }
+    __syncthreads();
+
+    // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
+    const int wbase = pu * (NIT + 1) * 64 * 32;
+    if (lane <= L) {
+      const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
+      const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
+      const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      lfor<0, 8>([&](auto JJ) {
+        constexpr int jj = decltype(JJ)::value;
+        y0 = fmaf(w[jj], eo[er0 + jj * NMP], y0);
+      });
+    }
+    lfor<0, NIT>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      if (lane + 64 * it < NROW) {
+        const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
+        const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
+        const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        lfor<0, 8>([&](auto JJ) {
+          constexpr int jj = decltype(JJ)::value;
+          yc[it] = fmaf(w[jj], eo[er[it] + jj * NMP], yc[it]);
+          ys[it] = fmaf(w[jj], eo[er[it] + jj * NMP + 1], ys[it]);
+        });
+      }
+      if constexpr (it % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+    });
+    __syncthreads();  // eo is rewritten by the next pass
+  }
+
+  // poles (only the m = 0 parts are non-zero there) and the stores
+  float p1, p2;
+  m0_synth(PASSES, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  const float f = p1 * p2 * float(NP);
+  const float fN = __shfl(f, 0), fS = __shfl(f, 8);
+  if (lane <= L) {
+    const int l = lane;
+    y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
+    y[P * K + l * l + l] = y0;
+  }
+  lfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    const int q = lane + 64 * it;
+    if (q < NROW) {
+      int l = int((sqrtf(8.0f * float(q) + 1.0f) + 1.0f) * 0.5f);
+      l -= (l * (l - 1) / 2 > q) ? 1 : 0;
+      l += ((l + 1) * l / 2 <= q) ? 1 : 0;
+      const int m = q - l * (l - 1) / 2 + 1;
+      y[P * K + l * l + l + m] = yc[it];
+      y[P * K + l * l + l - m] = ys[it];
+    }
+  });
+}
+
+template <int L>
+hipError_t launch_wave_one(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                           hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (in_type == IN_BF16)
+    hipLaunchKernelGGL((k_full_wave<L, uint16_t>), dim3(unsigned(n)), dim3(64), 0, s,
+                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n, t);
+  else
+    hipLaunchKernelGGL((k_full_wave<L, float>), dim3(unsigned(n)), dim3(64), 0, s, static_cast<const float*>(x1),
+                       static_cast<const float*>(x2), y, n, t);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_full_large(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
                              hipStream_t s, bool* supported) {
   *supported = true;
+  if (t.waveL == 16 && t.SM) return launch_wave_one<16>(t, x1, x2, in_type, n, y, s);
+  if (t.waveL == 32 && t.SM) return launch_wave_one<32>(t, x1, x2, in_type, n, y, s);
   if (t.L1 == t.L2 && t.L1 == t.Lout) {
     if (t.L1 == 16) return launch_large_one<16>(t, x1, x2, in_type, n, y, s);
     if (t.L1 == 32) return launch_large_one<32>(t, x1, x2, in_type, n, y, s);

@@ -174,7 +174,165 @@ Tables build_tables(int L1, int L2, int Lout) {
       if (mp > 0) v = (mp % 2 == 1) ? std::cos(ang) : std::sin(ang);
       t.Phi[size_t(mp) * t.NP + k] = v;
     }
+  if (L1 == L2 && L1 == Lout && (L1 == 16 || L1 == 32)) build_wave_tables(t);
   return t;
+}
+
+// Wave kernel geometry (L = L1 = L2 = Lout): lane = 16 g + i (g = 0..3,
+// i = 0..15); mirror pairs of theta nodes (jp, NT - jp), jp = 1..L, 8 per
+// pass; phi samples k = 0..Q (Q = NP / 4) in NMB blocks of 16; the m-parts
+// m = 1..L split into 4 classes {cos, sin} x {even m, odd m} of L / 2 values
+// each, taken 4 at a time (one per lane group g) in NKS = L / 8 K-steps.
+//
+//   SM [m][idx][jp]  m = 0..L, idx = 0..L+1, jp = 0..L:  Theta_{m+d, m}(t_jp)
+//                    with d = idx for odd m, d = idx - 1 for even m (so idx 0
+//                    of an even-m row is 0), zero for d outside 0..L-m.
+//   TWS[lane][s][type][mb]  synthesis operand: trig(m phi_k), k = 16 mb + i,
+//                    m = 8 s + 2 g + 2 (even types) or 8 s + 2 g + 1 (odd
+//                    types), zero for k > Q.
+//   TWA[lane][type][mb][r]  analysis operand: w_k trig(m phi_k), m = 2 i + 2
+//                    (even types) or 2 i + 1 (odd types), k = 16 mb + 4 g + r,
+//                    w_k = 1/2 at k = 0 and k = Q (those sample sets hold each
+//                    point twice), 1 inside, 0 for k > Q; type 4 holds w_k
+//                    alone (the m = 0 moment).
+//   SMP[pass][s][u2][lane][4]  the SM entries lane (g, 8h + pi) reads in
+//                    pass p (pair jp = 8p + pi + 1), K-step s, u-steps 2u2 and
+//                    2u2 + 1: Theta_{mo+2u+h, mo}(t_jp), Theta_{me+2u-h, me}(t_jp)
+//                    for u = 2u2 then 2u2 + 1 (mo = 8s + 2g + 1, me = mo + 1;
+//                    zero outside m <= l <= L), so each read is one coalesced
+//                    16-byte load per lane.
+//   SM0P[pass][lane][v]  m = 0 parts: Theta_{l,0}(t_jp), l = 8v + g + 4h
+//                    (v < NV0 = ceil((L+1)/8), padded to 4 | NV0); pass = L/8
+//                    holds the north pole (jp = 0).
+//   WP[pass][it][lane][jj]  analysis weights W[row][8 pass + jj + 1] of the
+//                    rows lane owns: it < NIT: the (lane + 64 it)-th row with
+//                    m > 0 in tri order, it = NIT: row tri(lane, 0); zero
+//                    where the row does not exist.
+//   XMAPP[lane][k]   XMAP[lane + 64 k] (k < NXK = ceil((L+1)^2 / 64), padded
+//                    to 4 | NXK with -1): the slots a lane fills when it
+//                    stages coefficients lane, lane + 64, ...
+//   XMAP[idx]        where coefficient idx = l^2 + l + m' of an input goes in
+//                    the kernel's LDS image: 4 * quad + (m' < 0), quads being
+//                    the m = 0 block (quad l), then for each m-pair c
+//                    (m = 2c + 1, 2c + 2) 4 quads per u-step
+//                    (2c+1, l_a), (2c+1, l_b), (2c+2, l_a), (2c+2, l_b) with
+//                    l_a = 2c + 1 + 2u, l_b = l_a + 1, and one pad quad.
+// Types: 0 cos/even m, 1 cos/odd m, 2 sin/even m, 3 sin/odd m.
+void build_wave_tables(Tables& t) {
+  const int L = t.L1;
+  if (t.L2 != L || t.Lout != L || (L != 16 && L != 32)) throw std::invalid_argument("wave tables: bad degree");
+  const int NP = t.NP, Q = NP / 4, NMB = (Q + 1 + 15) / 16, NKS = L / 8, RS = L + 2, NC = L + 1;
+  auto trig = [&](bool is_sin, int m, int k) {
+    const double ang = 2.0 * kPi * double((int64_t(m) * k) % NP) / NP;
+    return is_sin ? std::sin(ang) : std::cos(ang);
+  };
+  t.waveL = L;
+  t.SM.assign(size_t(L + 1) * RS * NC, 0.0);
+  for (int m = 0; m <= L; ++m)
+    for (int idx = 0; idx < RS; ++idx) {
+      const int d = (m % 2 == 1) ? idx : idx - 1;
+      if (d < 0 || d > L - m) continue;
+      for (int jp = 0; jp <= L; ++jp)
+        t.SM[(size_t(m) * RS + idx) * NC + jp] = t.S[size_t(tri(m + d, m)) * t.NJ + jp];
+    }
+  t.TWS.assign(size_t(64) * 4 * NMB * NKS, 0.0);
+  t.TWA.assign(size_t(64) * 5 * NMB * 4, 0.0);
+  for (int lane = 0; lane < 64; ++lane) {
+    const int g = lane / 16, i = lane % 16;
+    for (int type = 0; type < 4; ++type) {
+      const bool even = (type % 2 == 0), is_sin = type >= 2;
+      for (int mb = 0; mb < NMB; ++mb) {
+        for (int s = 0; s < NKS; ++s) {
+          const int k = 16 * mb + i, m = 8 * s + 2 * g + (even ? 2 : 1);
+          t.TWS[((size_t(lane) * NKS + s) * 4 + type) * NMB + mb] = k <= Q ? trig(is_sin, m, k) : 0.0;
+        }
+        for (int r = 0; r < 4; ++r) {
+          const int k = 16 * mb + 4 * g + r, m = 2 * i + (even ? 2 : 1);
+          const double w = k > Q ? 0.0 : (k == 0 || k == Q) ? 0.5 : 1.0;
+          t.TWA[((size_t(lane) * 5 + type) * NMB + mb) * 4 + r] = m <= L ? w * trig(is_sin, m, k) : 0.0;
+        }
+      }
+    }
+    for (int mb = 0; mb < NMB; ++mb)
+      for (int r = 0; r < 4; ++r) {
+        const int k = 16 * mb + 4 * g + r;
+        t.TWA[((size_t(lane) * 5 + 4) * NMB + mb) * 4 + r] = k > Q ? 0.0 : (k == 0 || k == Q) ? 0.5 : 1.0;
+      }
+  }
+  // x scatter map; pair blocks hold nu(s) = L/2 - 4s u-steps (s = c / 4)
+  std::vector<int> xb(L / 2 + 1);
+  xb[0] = L + 1;
+  for (int c = 0; c < L / 2; ++c) xb[c + 1] = xb[c] + 4 * (L / 2 - 4 * (c / 4)) + 1;
+  t.XMAP.assign(size_t(L + 1) * (L + 1), 0);
+  for (int l = 0; l <= L; ++l)
+    for (int ms = -l; ms <= l; ++ms) {
+      const int m = ms < 0 ? -ms : ms;
+      int quad = l;
+      if (m > 0) {
+        const int c = (m - 1) / 2, dl = l - (2 * c + 1);
+        quad = xb[c] + 4 * (dl / 2) + (m % 2 == 1 ? 0 : 2) + (dl % 2);
+      }
+      t.XMAP[size_t(l) * l + l + ms] = 4 * quad + (ms < 0 ? 1 : 0);
+    }
+  t.XQUADS = xb[L / 2];
+  const int K = (L + 1) * (L + 1), NXK = (K + 63) / 64, NXKP = (NXK + 3) / 4 * 4;
+  t.XMAPP.assign(size_t(64) * NXKP, -1);
+  for (int lane = 0; lane < 64; ++lane)
+    for (int k = 0; k < NXK; ++k)
+      if (lane + 64 * k < K) t.XMAPP[size_t(lane) * NXKP + k] = t.XMAP[lane + 64 * k];
+
+  // lane-permuted copies for 16-byte loads
+  auto S = [&](int l, int m, int j) { return (m <= l && l <= L) ? t.S[size_t(tri(l, m)) * t.NJ + j] : 0.0; };
+  const int PASSES = L / 8;
+  int TU2 = 0;
+  for (int s = 0; s < NKS; ++s) TU2 += (L / 2 - 4 * s) / 2;
+  t.SMP.assign(size_t(PASSES) * TU2 * 64 * 4, 0.0);
+  for (int pass = 0; pass < PASSES; ++pass) {
+    int u2base = 0;
+    for (int s = 0; s < NKS; ++s) {
+      const int nu = L / 2 - 4 * s;
+      for (int u2 = 0; u2 < nu / 2; ++u2)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int g = lane / 16, h = (lane / 8) % 2, pi = lane % 8;
+          const int mo = 2 * (4 * s + g) + 1, me = mo + 1, jp = 8 * pass + pi + 1;
+          double* o = &t.SMP[((size_t(pass) * TU2 + u2base + u2) * 64 + lane) * 4];
+          for (int e = 0; e < 2; ++e) {
+            const int u = 2 * u2 + e;
+            o[2 * e] = S(mo + 2 * u + h, mo, jp);
+            o[2 * e + 1] = S(me + 2 * u - h, me, jp);
+          }
+        }
+      u2base += nu / 2;
+    }
+  }
+  const int NV0 = (L + 1 + 7) / 8, NV0P = (NV0 + 3) / 4 * 4;
+  t.SM0P.assign(size_t(PASSES + 1) * 64 * NV0P, 0.0);
+  for (int pass = 0; pass <= PASSES; ++pass)
+    for (int lane = 0; lane < 64; ++lane) {
+      const int g = lane / 16, h = (lane / 8) % 2, pi = lane % 8;
+      const int jp = pass < PASSES ? 8 * pass + pi + 1 : 0;
+      for (int v = 0; v < NV0; ++v) t.SM0P[(size_t(pass) * 64 + lane) * NV0P + v] = S(8 * v + g + 4 * h, 0, jp);
+    }
+  const int NROW = ntri(L) - (L + 1), NIT = (NROW + 63) / 64;
+  t.WP.assign(size_t(PASSES) * (NIT + 1) * 64 * 8, 0.0);
+  for (int pass = 0; pass < PASSES; ++pass)
+    for (int it = 0; it <= NIT; ++it)
+      for (int lane = 0; lane < 64; ++lane) {
+        int row = -1;
+        if (it < NIT) {
+          const int q = lane + 64 * it;
+          if (q < NROW) {
+            int l = 1;
+            while ((l + 1) * l / 2 <= q) ++l;  // rows with m > 0: l rows of degree l
+            row = tri(l, q - l * (l - 1) / 2 + 1);
+          }
+        } else if (lane <= L) {
+          row = tri(lane, 0);
+        }
+        if (row < 0) continue;
+        for (int jj = 0; jj < 8; ++jj)
+          t.WP[((size_t(pass) * (NIT + 1) + it) * 64 + lane) * 8 + jj] = t.W[size_t(row) * t.NJ + 8 * pass + jj + 1];
+      }
 }
 
 void host_pipeline(const Tables& t, const double* x1, const double* x2, int64_t n, double* y) {
