@@ -106,13 +106,14 @@ gtp_status upload(gtp_plan_* p) {
   if ((s = up(&t.Zc, nullptr, &d.Zc)) != GTP_OK) return s;
   if ((s = up(&t.Zs, nullptr, &d.Zs)) != GTP_OK) return s;
   d.waveL = t.waveL;
-  d.SM = d.TWS = d.TWA = d.SMP = d.SM0P = d.WP = nullptr;
+  d.SM = d.TWS = d.TWA = d.TWR = d.SMP = d.SM0P = d.WP = nullptr;
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
   if (t.waveL) {
     if ((s = up(&t.SM, nullptr, &d.SM)) != GTP_OK) return s;
     if ((s = up(&t.TWS, nullptr, &d.TWS)) != GTP_OK) return s;
     if ((s = up(&t.TWA, nullptr, &d.TWA)) != GTP_OK) return s;
+    if ((s = up(&t.TWR, nullptr, &d.TWR)) != GTP_OK) return s;
     if ((s = up(&t.SMP, nullptr, &d.SMP)) != GTP_OK) return s;
     if ((s = up(&t.SM0P, nullptr, &d.SM0P)) != GTP_OK) return s;
     if ((s = up(&t.WP, nullptr, &d.WP)) != GTP_OK) return s;

@@ -27,6 +27,7 @@ struct DevTables {
   const float* SM;    // [m][idx][jp]          Theta_{m+d,m} at nodes 0..L
   const float* TWS;   // [lane][type][mb][s]   phi synthesis operands
   const float* TWA;   // [lane][type][mb][r]   phi analysis operands (+ m = 0 weights)
+  const float* TWR;   // [lane][24]            seeds of the phi operands (rotation recurrences)
   const float* SMP;   // [pass][s][u2][lane][4] lane-permuted theta synthesis values
   const float* SM0P;  // [pass][lane][v]       lane-permuted m = 0 values (+ pole)
   const float* WP;    // [pass][it][lane][8]   lane-permuted analysis weights

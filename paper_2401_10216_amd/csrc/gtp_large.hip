@@ -366,7 +366,8 @@ struct WGeo {
   static constexpr int NC = L + 1;                   // SM columns (nodes 0..L)
   static constexpr int NMP = 2 * L + 1;
   static constexpr int K = (L + 1) * (L + 1);
-  static constexpr int EOP = 2 * 8 * NMP;            // floats of one pass's combined moments
+  static constexpr int NMP2 = 2 * L + 2;             // moment row: [m=0, -, cos 1, sin 1, .., cos L, sin L]
+  static constexpr int EOP = 2 * 8 * NMP2;           // floats of one pass's combined moments
   static constexpr int NROW = (L + 1) * (L + 2) / 2 - (L + 1);  // output rows with m > 0
   static constexpr int NIT = (NROW + 63) / 64;
   // u-steps (two degrees each) of K-step s
@@ -401,7 +402,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   using G = WGeo<L>;
   static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
   constexpr int NJ = G::NJ, NP = G::NP, NMB = G::NMB, NKS = G::NKS, RS = G::RS, NC = G::NC;
-  constexpr int NMP = G::NMP, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
+  constexpr int NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
   __shared__ __align__(16) float xs[G::XQ * 4];
   __shared__ __align__(16) float eo[G::EOP];
   const float4* const xq = reinterpret_cast<const float4*>(xs);
@@ -452,9 +453,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
   const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
   // m = 0 theta synthesis at the lane's column node (x1 and x2 cos parts);
-  // pass = PASSES gives the poles
-  auto m0_synth = [&](int pass, float& a1, float& a2) {
-    float sv[G::NV0P];
+  // pass = PASSES gives the poles.  Split into the table read and the sums so
+  // that other loads can be issued in between.
+  auto m0_load = [&](int pass, float (&sv)[G::NV0P]) {
     lfor<0, G::NV0P / 4>([&](auto V4) {
       constexpr int v4 = decltype(V4)::value;
       const float4 w = tload4_s(S0r, lane * G::NV0P * 4 + 16 * v4, pass * 64 * G::NV0P * 4);
@@ -463,6 +464,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
       sv[4 * v4 + 2] = w.z;
       sv[4 * v4 + 3] = w.w;
     });
+  };
+  auto m0_finish = [&](const float (&sv)[G::NV0P], float& a1, float& a2) {
     float s1 = 0.0f, s2 = 0.0f;
     lfor<0, G::NV0>([&](auto V) {
       constexpr int v = decltype(V)::value;
@@ -476,13 +479,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     a1 = m0_reduce(s1, g, h);
     a2 = m0_reduce(s2, g, h);
   };
+  // phi-stage operands from per-lane seeds: cos/sin of m phi advance by
+  // rotations (angle addition) instead of table reads
+  auto rot = [](float& c, float& s, float cr, float sr) {
+    const float cn = c * cr - s * sr;
+    s = fmaf(s, cr, c * sr);
+    c = cn;
+  };
 
   // theta-analysis rows: tri(l, 0) with l = lane (l <= L), and the rows with
   // m > 0 numbered q = lane + 64 it; per row the byte offset of its weight
   // column and the LDS offset of its moment (parity of l + m, m-part)
   float y0 = 0.0f, yc[NIT], ys[NIT];
   int er[NIT];
-  const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP;
+  const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP2;
   lfor<0, NIT>([&](auto IT) {
     constexpr int it = decltype(IT)::value;
     yc[it] = 0.0f;
@@ -492,13 +502,40 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     l -= (l * (l - 1) / 2 > q) ? 1 : 0;
     l += ((l + 1) * l / 2 <= q) ? 1 : 0;
     const int m = q - l * (l - 1) / 2 + 1;
-    er[it] = ((l + m) & 1) * 8 * NMP + 2 * m - 1;
+    er[it] = ((l + m) & 1) * 8 * NMP2 + 2 * m;
   });
 
   for (int pass = 0; pass < PASSES; ++pass) {
     const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
+    // loads first (m = 0 part, the first theta-table steps, the first phi
+    // operands), then the m = 0 sums
+    constexpr int D = 5;  // theta-table steps in flight
+    const int sbase = pu * G::TU2 * 64 * 16;
+    float s0v[G::NV0P];
+    m0_load(pu, s0v);
+    float4 sring[D];
+    lfor<0, D>([&](auto T) {
+      constexpr int tt = decltype(T)::value;
+      if constexpr (tt < G::TU2) sring[tt] = tload4_s(SPr, lane * 16, sbase + tt * 64 * 16);
+    });
+    // synthesis operands twc[type][mb] of K-step 0 and the rotation by 8 phi_k
+    float twc[4][NMB], r8c[NMB], r8s[NMB];
+    {
+      const f4* src = reinterpret_cast<const f4*>(t.TWR + lane * 24);
+      const f4 a = src[0], b = src[1], c = src[2];
+      const float sd[12] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w, c.x, c.y, c.z, c.w};
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        twc[0][mb] = sd[6 * mb + 0];  // cos, even m
+        twc[2][mb] = sd[6 * mb + 1];  // sin, even m
+        twc[1][mb] = sd[6 * mb + 2];  // cos, odd m
+        twc[3][mb] = sd[6 * mb + 3];  // sin, odd m
+        r8c[mb] = sd[6 * mb + 4];
+        r8s[mb] = sd[6 * mb + 5];
+      });
+    }
     float c1, c2;
-    m0_synth(pu, c1, c2);
+    m0_finish(s0v, c1, c2);
 
     // ---- 1 + 2a. theta synthesis feeding the phi-synthesis contractions
     f4 acc[2][NMB][4];  // [input][k block][type]
@@ -511,29 +548,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         acc[1][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
       });
     });
+    float twa[5][NMB][4];
     lfor<0, NKS>([&](auto SS) {
       constexpr int s = decltype(SS)::value;
       const int c = 4 * s + g;
       // this lane's parity: h = 0 takes (mo, l_a) and (mo+1, l_b), h = 1 (mo, l_b) and (mo+1, l_a)
       const float4* xa = xq + G::xb(c) + h;
       const float4* xe = xq + G::xb(c) + 3 - h;
-      float tw[4][NMB];
-      {
-        const f4* src = reinterpret_cast<const f4*>(t.TWS + (lane * NKS + s) * 4 * NMB);
-        lfor<0, NMB>([&](auto Q4) {
-          constexpr int q4 = decltype(Q4)::value;
-          const f4 v = src[q4];
-          tw[(4 * q4 + 0) / NMB][(4 * q4 + 0) % NMB] = v.x;
-          tw[(4 * q4 + 1) / NMB][(4 * q4 + 1) % NMB] = v.y;
-          tw[(4 * q4 + 2) / NMB][(4 * q4 + 2) % NMB] = v.z;
-          tw[(4 * q4 + 3) / NMB][(4 * q4 + 3) % NMB] = v.w;
-        });
-      }
       f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
-      const int sbase = (pu * G::TU2 + G::u2off(s)) * 64 * 16;
       lfor<0, G::nu(s) / 2>([&](auto U2) {
-        constexpr int u2 = decltype(U2)::value;
-        const float4 sv = tload4_s(SPr, lane * 16, sbase + u2 * 64 * 16);
+        constexpr int u2 = decltype(U2)::value, tt = G::u2off(s) + u2;
+        const float4 sv = sring[tt % D];
+        if constexpr (tt + D < G::TU2) sring[tt % D] = tload4_s(SPr, lane * 16, sbase + (tt + D) * 64 * 16);
         lfor<0, 2>([&](auto E) {
           constexpr int u = 2 * u2 + decltype(E)::value;
           const float so = E == 0 ? sv.x : sv.z, se = E == 0 ? sv.y : sv.w;
@@ -541,8 +567,33 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
           Vo += so * f4{qa.x, qa.y, qa.z, qa.w};
           Ve += se * f4{qe.x, qe.y, qe.z, qe.w};
         });
-        if constexpr (u2 % 2 == 1) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch distance
       });
+      if constexpr (s == NKS - 1) {
+        // phi-analysis operands twa[type][mb][r] = w_k trig(m phi_k), k = 16 mb + 4 g + r,
+        // m = 2i + 2 (even types) or 2i + 1 (odd types); type 4 = w_k
+        const f4* src = reinterpret_cast<const f4*>(t.TWR + lane * 24);
+        const f4 a = src[3], b = src[4], st = src[5];
+        const float sd[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        lfor<0, NMB>([&](auto MB) {
+          constexpr int mb = decltype(MB)::value;
+          float ce = sd[4 * mb + 0], se = sd[4 * mb + 1], co = sd[4 * mb + 2], so = sd[4 * mb + 3];
+          lfor<0, 4>([&](auto R) {
+            constexpr int r = decltype(R)::value;
+            if constexpr (r > 0) {
+              rot(ce, se, st.x, st.y);
+              rot(co, so, st.z, st.w);
+            }
+            const int k = 16 * mb + 4 * g + r;
+            const float w = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f : 1.0f;
+            twa[0][mb][r] = w * ce;
+            twa[1][mb][r] = w * co;
+            twa[2][mb][r] = w * se;
+            twa[3][mb][r] = w * so;
+            twa[4][mb][r] = w;
+          });
+        });
+      }
       // column value: node jp (h = 0: own even + partner odd) or its mirror (h = 1: partner even - own odd)
       f4 Bo, Be;
       lfor<0, 4>([&](auto C) {
@@ -555,12 +606,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         constexpr int mb = decltype(MB)::value;
         lfor<0, 2>([&](auto TI) {
           constexpr int ti = decltype(TI)::value;
-          acc[ti][mb][0] = mfma4(tw[0][mb], Be[2 * ti], acc[ti][mb][0]);
-          acc[ti][mb][1] = mfma4(tw[1][mb], Bo[2 * ti], acc[ti][mb][1]);
-          acc[ti][mb][2] = mfma4(tw[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
-          acc[ti][mb][3] = mfma4(tw[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
+          acc[ti][mb][0] = mfma4(twc[0][mb], Be[2 * ti], acc[ti][mb][0]);
+          acc[ti][mb][1] = mfma4(twc[1][mb], Bo[2 * ti], acc[ti][mb][1]);
+          acc[ti][mb][2] = mfma4(twc[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
+          acc[ti][mb][3] = mfma4(twc[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
         });
       });
+      if constexpr (s + 1 < NKS) {
+        // next K-step: m -> m + 8
+        lfor<0, NMB>([&](auto MB) {
+          constexpr int mb = decltype(MB)::value;
+          rot(twc[0][mb], twc[2][mb], r8c[mb], r8s[mb]);
+          rot(twc[1][mb], twc[3][mb], r8c[mb], r8s[mb]);
+        });
+      }
     });
 
     // ---- 2b. sample products, folded over the 4-point sets
@@ -580,43 +639,40 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     });
 
     // ---- 2c. phi analysis contractions, then 3. mirror combination into LDS
-    // eo[parity][pi][m-part]: parity 0 = C(jp) + C(NT - jp), 1 = C(jp) - C(NT - jp)
-    float* const eoh = eo + (h * 8 + pi) * NMP;
+    // eo[parity][pi][slot]: parity 0 = C(jp) + C(NT - jp), 1 = C(jp) - C(NT - jp);
+    // slot 0 = m 0, 2m = cos m, 2m + 1 = sin m
+    float* const eoh = eo + (h * 8 + pi) * NMP2;
+    f4 o[4];
     lfor<0, 4>([&](auto TY) {
       constexpr int ty = decltype(TY)::value;
-      float tw[NMB][4];
-      {
-        const f4* src = reinterpret_cast<const f4*>(t.TWA + (lane * 5 + ty) * NMB * 4);
-        lfor<0, NMB>([&](auto MB) {
-          const f4 v = src[decltype(MB)::value];
-          lfor<0, 4>([&](auto R) { tw[decltype(MB)::value][decltype(R)::value] = v[decltype(R)::value]; });
-        });
-      }
-      f4 o = {0.0f, 0.0f, 0.0f, 0.0f};
+      f4 a = {0.0f, 0.0f, 0.0f, 0.0f};
       lfor<0, NMB>([&](auto MB) {
         constexpr int mb = decltype(MB)::value;
         lfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
-          o = mfma4(tw[mb][r], acc[0][mb][ty][r], o);
+          a = mfma4(twa[ty][mb][r], acc[0][mb][ty][r], a);
         });
       });
+      o[ty] = a;
+    });
+    lfor<0, 2>([&](auto PAR) {
+      constexpr int odd = decltype(PAR)::value;  // types odd (cos), odd + 2 (sin)
       lfor<0, 4>([&](auto R) {
         constexpr int r = decltype(R)::value;
-        const int m = 2 * (4 * g + r) + ((ty & 1) ? 1 : 2);
-        const float pv = __shfl_xor(o[r], 8);
-        const float v = h ? pv - o[r] : pv + o[r];
-        if (L == 32 || m <= L) eoh[ty < 2 ? 2 * m - 1 : 2 * m] = v;
+        const int m = 2 * (4 * g + r) + (odd ? 1 : 2);
+        const float pc = __shfl_xor(o[odd][r], 8), ps = __shfl_xor(o[odd + 2][r], 8);
+        const float vc = h ? pc - o[odd][r] : pc + o[odd][r];
+        const float vs = h ? ps - o[odd + 2][r] : ps + o[odd + 2][r];
+        if (L == 32 || m <= L) *reinterpret_cast<float2*>(eoh + 2 * m) = make_float2(vc, vs);
       });
     });
     {
-      const f4* src = reinterpret_cast<const f4*>(t.TWA + (lane * 5 + 4) * NMB * 4);
       float zz = 0.0f;
       lfor<0, NMB>([&](auto MB) {
         constexpr int mb = decltype(MB)::value;
-        const f4 w = src[mb];
         lfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
-          zz = fmaf(w[r], acc[0][mb][0][r], zz);
+          zz = fmaf(twa[4][mb][r], acc[0][mb][0][r], zz);
         });
       });
       zz += __shfl_xor(zz, 16);
@@ -634,7 +690,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
       const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
       lfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
-        y0 = fmaf(w[jj], eo[er0 + jj * NMP], y0);
+        y0 = fmaf(w[jj], eo[er0 + jj * NMP2], y0);
       });
     }
     lfor<0, NIT>([&](auto IT) {
@@ -645,8 +701,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         const float w[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
         lfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
-          yc[it] = fmaf(w[jj], eo[er[it] + jj * NMP], yc[it]);
-          ys[it] = fmaf(w[jj], eo[er[it] + jj * NMP + 1], ys[it]);
+          const float2 cs = *reinterpret_cast<const float2*>(eo + er[it] + jj * NMP2);
+          yc[it] = fmaf(w[jj], cs.x, yc[it]);
+          ys[it] = fmaf(w[jj], cs.y, ys[it]);
         });
       }
       if constexpr (it % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
@@ -656,7 +713,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
 
   // poles (only the m = 0 parts are non-zero there) and the stores
   float p1, p2;
-  m0_synth(PASSES, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  {
+    float sv[G::NV0P];
+    m0_load(PASSES, sv);
+    m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  }
   const float f = p1 * p2 * float(NP);
   const float fN = __shfl(f, 0), fS = __shfl(f, 8);
   if (lane <= L) {

@@ -195,6 +195,13 @@ Tables build_tables(int L1, int L2, int Lout) {
 //                    w_k = 1/2 at k = 0 and k = Q (those sample sets hold each
 //                    point twice), 1 inside, 0 for k > Q; type 4 holds w_k
 //                    alone (the m = 0 moment).
+//   TWR[lane][24]    seeds of TWS and TWA for rotation recurrences: per mb
+//                    (k = 16 mb + i, zero for k > Q) cos/sin of (2g+2) phi_k,
+//                    cos/sin of (2g+1) phi_k, cos/sin of 8 phi_k (entries
+//                    6 mb .. 6 mb + 5); then per mb (k0 = 16 mb + 4 g)
+//                    cos/sin of (2i+2) phi_k0 and of (2i+1) phi_k0 (entries
+//                    12 + 4 mb ..); then cos/sin of (2i+2) phi_1 and of
+//                    (2i+1) phi_1 (entries 20..23); zero where m > L.
 //   SMP[pass][s][u2][lane][4]  the SM entries lane (g, 8h + pi) reads in
 //                    pass p (pair jp = 8p + pi + 1), K-step s, u-steps 2u2 and
 //                    2u2 + 1: Theta_{mo+2u+h, mo}(t_jp), Theta_{me+2u-h, me}(t_jp)
@@ -280,6 +287,42 @@ void build_wave_tables(Tables& t) {
   for (int lane = 0; lane < 64; ++lane)
     for (int k = 0; k < NXK; ++k)
       if (lane + 64 * k < K) t.XMAPP[size_t(lane) * NXKP + k] = t.XMAP[lane + 64 * k];
+
+  t.TWR.assign(size_t(64) * 24, 0.0);
+  if (NMB > 2) throw std::invalid_argument("wave tables: more than two phi blocks");
+  for (int lane = 0; lane < 64; ++lane) {
+    const int g = lane / 16, i = lane % 16;
+    double* o = &t.TWR[size_t(lane) * 24];
+    for (int mb = 0; mb < NMB; ++mb) {
+      const int k = 16 * mb + i;
+      if (k <= Q) {
+        o[6 * mb + 0] = trig(false, 2 * g + 2, k);
+        o[6 * mb + 1] = trig(true, 2 * g + 2, k);
+        o[6 * mb + 2] = trig(false, 2 * g + 1, k);
+        o[6 * mb + 3] = trig(true, 2 * g + 1, k);
+        o[6 * mb + 4] = trig(false, 8, k);
+        o[6 * mb + 5] = trig(true, 8, k);
+      }
+      const int k0 = 16 * mb + 4 * g, me = 2 * i + 2, mo = 2 * i + 1;
+      if (me <= L) {
+        o[12 + 4 * mb + 0] = trig(false, me, k0);
+        o[12 + 4 * mb + 1] = trig(true, me, k0);
+      }
+      if (mo <= L) {
+        o[12 + 4 * mb + 2] = trig(false, mo, k0);
+        o[12 + 4 * mb + 3] = trig(true, mo, k0);
+      }
+    }
+    const int me = 2 * i + 2, mo = 2 * i + 1;
+    if (me <= L) {
+      o[20] = trig(false, me, 1);
+      o[21] = trig(true, me, 1);
+    }
+    if (mo <= L) {
+      o[22] = trig(false, mo, 1);
+      o[23] = trig(true, mo, 1);
+    }
+  }
 
   // lane-permuted copies for 16-byte loads
   auto S = [&](int l, int m, int j) { return (m <= l && l <= L) ? t.S[size_t(tri(l, m)) * t.NJ + j] : 0.0; };

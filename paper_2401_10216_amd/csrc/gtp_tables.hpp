@@ -50,7 +50,7 @@ struct Tables {
   // the matrix cores; built when L1 = L2 = Lout = L with L in {16, 32}
   // (waveL = L), empty otherwise.  Layouts are given in build_wave_tables.
   int waveL = 0;
-  std::vector<double> SM, TWS, TWA, SMP, SM0P, WP;
+  std::vector<double> SM, TWS, TWA, TWR, SMP, SM0P, WP;
   std::vector<int> XMAP, XMAPP;
   int XQUADS = 0;  // quads of the kernel's LDS image of one input pair
 };
