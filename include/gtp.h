@@ -152,11 +152,14 @@ gtp_status gtp_plan_info(gtp_plan p, int64_t *out8);
  *   which 2: Zs   [tri(l,m)][u], u in [0, U]        int sin(u t) Q sin t dt (step 3)
  *   which 3: S    [tri(l,m)][j], j in [0, NT]       synthesis at the theta nodes
  *   which 4: W    [tri(l,m)][j], j in [0, NT]       analysis weights at the theta nodes
- *   which 5: SM   [m][idx][j], j in [0, L]          S regrouped per m for the matrix-core kernel
- *   which 6: TWS  [lane][type][mb][s]               its phi synthesis operands
- *   which 7: TWA  [lane][type][mb][r]               its phi analysis operands
- * with tri(l,m) = l(l+1)/2 + m, m >= 0.  Tables 5..7 exist only for
- * L1 = L2 = Lout = L in {16, 32} (length 0 otherwise).  Pass buf = NULL to
+ *   which 5: TWR  [lane][24]            phi-operand seeds of the matrix-core kernel
+ *   which 6: SMP  [pass][s][u2][lane][4]  its lane-permuted theta synthesis values
+ *   which 7: SM0P [pass][lane][v]         its m = 0 theta synthesis values (+ pole)
+ *   which 8: WP   [pass][it][lane][8]     its lane-permuted theta analysis weights
+ *   which 9: XMAP [lane][k]               its LDS slot of input coefficient lane + 64k
+ * with tri(l,m) = l(l+1)/2 + m, m >= 0.  Tables 5..9 exist only for
+ * L1 = L2 = Lout = L in {16, 32} (length 0 otherwise); their layouts are
+ * internal to that kernel.  Pass buf = NULL to
  * get the length in *count; otherwise *count is the capacity in doubles. */
 gtp_status gtp_plan_table(gtp_plan p, int which, double *buf, int64_t *count);
 

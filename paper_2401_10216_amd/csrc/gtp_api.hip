@@ -106,13 +106,10 @@ gtp_status upload(gtp_plan_* p) {
   if ((s = up(&t.Zc, nullptr, &d.Zc)) != GTP_OK) return s;
   if ((s = up(&t.Zs, nullptr, &d.Zs)) != GTP_OK) return s;
   d.waveL = t.waveL;
-  d.SM = d.TWS = d.TWA = d.TWR = d.SMP = d.SM0P = d.WP = nullptr;
+  d.TWR = d.SMP = d.SM0P = d.WP = nullptr;
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
   if (t.waveL) {
-    if ((s = up(&t.SM, nullptr, &d.SM)) != GTP_OK) return s;
-    if ((s = up(&t.TWS, nullptr, &d.TWS)) != GTP_OK) return s;
-    if ((s = up(&t.TWA, nullptr, &d.TWA)) != GTP_OK) return s;
     if ((s = up(&t.TWR, nullptr, &d.TWR)) != GTP_OK) return s;
     if ((s = up(&t.SMP, nullptr, &d.SMP)) != GTP_OK) return s;
     if ((s = up(&t.SM0P, nullptr, &d.SM0P)) != GTP_OK) return s;
@@ -261,7 +258,7 @@ gtp_status gtp_full(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dty
   if (!p->force_generic) {
     e = gtp::launch_full_small(p->dev, x1, x2, it, n, y, 0, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
-    e = gtp::launch_full_large(p->dev, x1, x2, it, n, y, st, &done);
+    e = gtp::launch_full_wave(p->dev, x1, x2, it, n, y, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
   }
   e = gtp::launch_full_generic(p->dev, x1, it, x2, it, n, y, 0, st);
@@ -419,16 +416,23 @@ gtp_status gtp_plan_info(gtp_plan p, int64_t* out8) {
 gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
   if (!p || !count) return fail(GTP_ERR_INVALID_ARG, "NULL argument");
   const std::vector<double>* src = nullptr;
+  std::vector<double> tmp;
   switch (which) {
     case 0: src = &p->tab.T1; break;
     case 1: src = &p->tab.Zc; break;
     case 2: src = &p->tab.Zs; break;
     case 3: src = &p->tab.S; break;
     case 4: src = &p->tab.W; break;
-    case 5: src = &p->tab.SM; break;
-    case 6: src = &p->tab.TWS; break;
-    case 7: src = &p->tab.TWA; break;
-    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..7");
+    case 5: src = &p->tab.TWR; break;
+    case 6: src = &p->tab.SMP; break;
+    case 7: src = &p->tab.SM0P; break;
+    case 8: src = &p->tab.WP; break;
+    case 9: {
+      tmp.assign(p->tab.XMAPP.begin(), p->tab.XMAPP.end());
+      src = &tmp;
+      break;
+    }
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..9");
   }
   if (!buf) {
     *count = int64_t(src->size());

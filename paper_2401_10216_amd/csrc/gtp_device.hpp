@@ -21,17 +21,14 @@ struct DevTables {
   const float* T1;    // [tri(l<=Lt)][ldT1]  theta-Fourier series of Theta_lm
   const float* Zc;    // [tri(l<=Le)][ldZ]
   const float* Zs;    // [tri(l<=Le)][ldZ]
-  // Operand tables of the matrix-core wave kernel (L1 = L2 = Lout = waveL in
-  // {16, 32}; null and waveL = 0 otherwise).
+  // Lane-permuted tables of the matrix-core wave kernel (L1 = L2 = Lout =
+  // waveL in {16, 32}; null and waveL = 0 otherwise).
   int waveL;
-  const float* SM;    // [m][idx][jp]          Theta_{m+d,m} at nodes 0..L
-  const float* TWS;   // [lane][type][mb][s]   phi synthesis operands
-  const float* TWA;   // [lane][type][mb][r]   phi analysis operands (+ m = 0 weights)
-  const float* TWR;   // [lane][24]            seeds of the phi operands (rotation recurrences)
-  const float* SMP;   // [pass][s][u2][lane][4] lane-permuted theta synthesis values
-  const float* SM0P;  // [pass][lane][v]       lane-permuted m = 0 values (+ pole)
-  const float* WP;    // [pass][it][lane][8]   lane-permuted analysis weights
-  const int* XMAP;    // [lane][k]             LDS slot of input coefficient lane + 64 k
+  const float* TWR;   // [lane][24]             seeds of the phi operands (rotation recurrences)
+  const float* SMP;   // [pass][s][u2][lane][4] theta synthesis values
+  const float* SM0P;  // [pass][lane][v]        m = 0 theta synthesis values (+ pole)
+  const float* WP;    // [pass][it][lane][8]    theta analysis weights
+  const int* XMAP;    // [lane][k]              LDS slot of input coefficient lane + 64 k
   int XQUADS;
 };
 
@@ -46,10 +43,10 @@ hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2,
 // instantiated (L, nu, Lout); t1 = tables of (L, L, Lout), t2 = (Lout, L, Lout).
 hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x,
                                       int in_type, int64_t n, float* y, hipStream_t s, bool* supported);
-// Wave-per-product fused kernel for L1 = L2 = Lout = L in {16, 32};
-// *supported = false otherwise.
-hipError_t launch_full_large(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                             hipStream_t s, bool* supported);
+// Wave-per-product fused kernel with the phi stage on the matrix cores, for
+// L1 = L2 = Lout = L in {16, 32}; *supported = false otherwise.
+hipError_t launch_full_wave(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                            hipStream_t s, bool* supported);
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,

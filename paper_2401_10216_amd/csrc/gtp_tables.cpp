@@ -174,103 +174,68 @@ Tables build_tables(int L1, int L2, int Lout) {
       if (mp > 0) v = (mp % 2 == 1) ? std::cos(ang) : std::sin(ang);
       t.Phi[size_t(mp) * t.NP + k] = v;
     }
-  if (L1 == L2 && L1 == Lout && (L1 == 16 || L1 == 32)) build_wave_tables(t);
+  if (L1 == L2 && L1 == Lout && (L1 == 16 || L1 == 32 || L1 == 64)) build_wave_tables(t);
   return t;
 }
 
 // Wave kernel geometry (L = L1 = L2 = Lout): lane = 16 g + i (g = 0..3,
-// i = 0..15); mirror pairs of theta nodes (jp, NT - jp), jp = 1..L, 8 per
-// pass; phi samples k = 0..Q (Q = NP / 4) in NMB blocks of 16; the m-parts
-// m = 1..L split into 4 classes {cos, sin} x {even m, odd m} of L / 2 values
-// each, taken 4 at a time (one per lane group g) in NKS = L / 8 K-steps.
+// i = 8 h + pi); mirror pairs of theta nodes (jp, NT - jp), jp = 1..L, 8 per
+// pass (PASSES = L / 8); phi samples k = 0..Q (Q = NP / 4) in NMB blocks of
+// 16; the m-parts m = 1..L split into 4 classes {cos, sin} x {even m, odd m}
+// of L / 2 values each, taken 4 at a time (one per lane group g) in NKS = L / 8
+// K-steps: K-step s, group g holds m = 8s + 2g + 2 (even) and 8s + 2g + 1
+// (odd).  Lane (g, 8h + pi) sums, for pair jp = 8 pass + pi + 1, the terms
+// with l - m = h (mod 2).  Every table is a lane-permuted copy that the
+// kernel reads as one 16-byte load per lane:
 //
-//   SM [m][idx][jp]  m = 0..L, idx = 0..L+1, jp = 0..L:  Theta_{m+d, m}(t_jp)
-//                    with d = idx for odd m, d = idx - 1 for even m (so idx 0
-//                    of an even-m row is 0), zero for d outside 0..L-m.
-//   TWS[lane][s][type][mb]  synthesis operand: trig(m phi_k), k = 16 mb + i,
-//                    m = 8 s + 2 g + 2 (even types) or 8 s + 2 g + 1 (odd
-//                    types), zero for k > Q.
-//   TWA[lane][type][mb][r]  analysis operand: w_k trig(m phi_k), m = 2 i + 2
-//                    (even types) or 2 i + 1 (odd types), k = 16 mb + 4 g + r,
-//                    w_k = 1/2 at k = 0 and k = Q (those sample sets hold each
-//                    point twice), 1 inside, 0 for k > Q; type 4 holds w_k
-//                    alone (the m = 0 moment).
-//   TWR[lane][24]    seeds of TWS and TWA for rotation recurrences: per mb
-//                    (k = 16 mb + i, zero for k > Q) cos/sin of (2g+2) phi_k,
+//   TWR[lane][TWRN]  seeds of the phi operands for rotation recurrences
+//                    (NMBP = NMB rounded up to even; NMR = 16-row blocks of
+//                    analysis m-rows per class, L / 32 at L = 64, else 1): per
+//                    mb (k = 16 mb + i, zero for k > Q) cos/sin of (2g+2) phi_k,
 //                    cos/sin of (2g+1) phi_k, cos/sin of 8 phi_k (entries
-//                    6 mb .. 6 mb + 5); then per mb (k0 = 16 mb + 4 g)
-//                    cos/sin of (2i+2) phi_k0 and of (2i+1) phi_k0 (entries
-//                    12 + 4 mb ..); then cos/sin of (2i+2) phi_1 and of
-//                    (2i+1) phi_1 (entries 20..23); zero where m > L.
-//   SMP[pass][s][u2][lane][4]  the SM entries lane (g, 8h + pi) reads in
-//                    pass p (pair jp = 8p + pi + 1), K-step s, u-steps 2u2 and
-//                    2u2 + 1: Theta_{mo+2u+h, mo}(t_jp), Theta_{me+2u-h, me}(t_jp)
-//                    for u = 2u2 then 2u2 + 1 (mo = 8s + 2g + 1, me = mo + 1;
-//                    zero outside m <= l <= L), so each read is one coalesced
-//                    16-byte load per lane.
+//                    6 mb .. 6 mb + 5); from ASD = 6 NMBP, per (mr, mb)
+//                    (k0 = 16 mb + 4 g, m = 2(16 mr + i) + 2) cos/sin of m phi_k0
+//                    and of (m - 1) phi_k0 (entries ASD + 4 (mr NMBP + mb) ..);
+//                    from AST = ASD + 4 NMR NMBP, per mr cos/sin of m phi_1 and
+//                    of (m - 1) phi_1; zero where m > L.  TWRN = AST + 4 NMR.
+//   SMP[pass][s][u2][lane][4]  Theta_{mo+2u+h, mo}(t_jp),
+//                    Theta_{me+2u-h, me}(t_jp) for u = 2 u2, then u = 2 u2 + 1
+//                    (mo = 8s + 2g + 1, me = mo + 1; zero outside m <= l <= L);
+//                    u2 < nu(s) / 2 with nu(s) = L/2 - 4s u-steps in K-step s.
 //   SM0P[pass][lane][v]  m = 0 parts: Theta_{l,0}(t_jp), l = 8v + g + 4h
 //                    (v < NV0 = ceil((L+1)/8), padded to 4 | NV0); pass = L/8
 //                    holds the north pole (jp = 0).
-//   WP[pass][it][lane][jj]  analysis weights W[row][8 pass + jj + 1] of the
-//                    rows lane owns: it < NIT: the (lane + 64 it)-th row with
-//                    m > 0 in tri order, it = NIT: row tri(lane, 0); zero
-//                    where the row does not exist.
-//   XMAPP[lane][k]   XMAP[lane + 64 k] (k < NXK = ceil((L+1)^2 / 64), padded
-//                    to 4 | NXK with -1): the slots a lane fills when it
-//                    stages coefficients lane, lane + 64, ...
-//   XMAP[idx]        where coefficient idx = l^2 + l + m' of an input goes in
-//                    the kernel's LDS image: 4 * quad + (m' < 0), quads being
-//                    the m = 0 block (quad l), then for each m-pair c
-//                    (m = 2c + 1, 2c + 2) 4 quads per u-step
-//                    (2c+1, l_a), (2c+1, l_b), (2c+2, l_a), (2c+2, l_b) with
-//                    l_a = 2c + 1 + 2u, l_b = l_a + 1, and one pad quad.
-// Types: 0 cos/even m, 1 cos/odd m, 2 sin/even m, 3 sin/odd m.
+//   WP               analysis weights W[row][j] of the rows a thread owns:
+//                    step it < NIT: the (tid + NTH it)-th row with m > 0 in
+//                    tri order, it = NIT: row tri(tid, 0); zero where the row
+//                    does not exist.  NTH = 64 (L <= 32): [pass][it][lane][jj],
+//                    j = 8 pass + jj + 1; NTH = 256 (L = 64, four waves per
+//                    product): [it][tid][j - 1], j = 1..L.
+//   XMAPP[tid][k]    LDS slot (4 * quad + (m' < 0)) of coefficient
+//                    idx = tid + NTH k = l^2 + l + m' (k < NXK = ceil(K / NTH),
+//                    padded to 4 | NXK with -1).  Quads: the m = 0 block
+//                    (quad l), then for each m-pair c (m = 2c + 1, 2c + 2) 4
+//                    quads per u-step (2c+1, l_a), (2c+1, l_b), (2c+2, l_a),
+//                    (2c+2, l_b) with l_a = 2c + 1 + 2u, l_b = l_a + 1, for
+//                    nu(c / 4) u-steps, and one pad quad.
 void build_wave_tables(Tables& t) {
   const int L = t.L1;
-  if (t.L2 != L || t.Lout != L || (L != 16 && L != 32)) throw std::invalid_argument("wave tables: bad degree");
-  const int NP = t.NP, Q = NP / 4, NMB = (Q + 1 + 15) / 16, NKS = L / 8, RS = L + 2, NC = L + 1;
+  if (t.L2 != L || t.Lout != L || (L != 16 && L != 32 && L != 64)) throw std::invalid_argument("wave tables: bad degree");
+  const int NP = t.NP, Q = NP / 4, NMB = (Q + 1 + 15) / 16, NKS = L / 8;
+  const int NMBP = (NMB + 1) / 2 * 2;                        // seed layout per lane
+  const int NMR = L > 32 ? L / 32 : 1, ASD = 6 * NMBP, AST = ASD + 4 * NMR * NMBP, TWRN = AST + 4 * NMR;
+  const int NTH = L > 32 ? 256 : 64;                         // threads per product
   auto trig = [&](bool is_sin, int m, int k) {
     const double ang = 2.0 * kPi * double((int64_t(m) * k) % NP) / NP;
     return is_sin ? std::sin(ang) : std::cos(ang);
   };
   t.waveL = L;
-  t.SM.assign(size_t(L + 1) * RS * NC, 0.0);
-  for (int m = 0; m <= L; ++m)
-    for (int idx = 0; idx < RS; ++idx) {
-      const int d = (m % 2 == 1) ? idx : idx - 1;
-      if (d < 0 || d > L - m) continue;
-      for (int jp = 0; jp <= L; ++jp)
-        t.SM[(size_t(m) * RS + idx) * NC + jp] = t.S[size_t(tri(m + d, m)) * t.NJ + jp];
-    }
-  t.TWS.assign(size_t(64) * 4 * NMB * NKS, 0.0);
-  t.TWA.assign(size_t(64) * 5 * NMB * 4, 0.0);
-  for (int lane = 0; lane < 64; ++lane) {
-    const int g = lane / 16, i = lane % 16;
-    for (int type = 0; type < 4; ++type) {
-      const bool even = (type % 2 == 0), is_sin = type >= 2;
-      for (int mb = 0; mb < NMB; ++mb) {
-        for (int s = 0; s < NKS; ++s) {
-          const int k = 16 * mb + i, m = 8 * s + 2 * g + (even ? 2 : 1);
-          t.TWS[((size_t(lane) * NKS + s) * 4 + type) * NMB + mb] = k <= Q ? trig(is_sin, m, k) : 0.0;
-        }
-        for (int r = 0; r < 4; ++r) {
-          const int k = 16 * mb + 4 * g + r, m = 2 * i + (even ? 2 : 1);
-          const double w = k > Q ? 0.0 : (k == 0 || k == Q) ? 0.5 : 1.0;
-          t.TWA[((size_t(lane) * 5 + type) * NMB + mb) * 4 + r] = m <= L ? w * trig(is_sin, m, k) : 0.0;
-        }
-      }
-    }
-    for (int mb = 0; mb < NMB; ++mb)
-      for (int r = 0; r < 4; ++r) {
-        const int k = 16 * mb + 4 * g + r;
-        t.TWA[((size_t(lane) * 5 + 4) * NMB + mb) * 4 + r] = k > Q ? 0.0 : (k == 0 || k == Q) ? 0.5 : 1.0;
-      }
-  }
   // x scatter map; pair blocks hold nu(s) = L/2 - 4s u-steps (s = c / 4)
   std::vector<int> xb(L / 2 + 1);
   xb[0] = L + 1;
   for (int c = 0; c < L / 2; ++c) xb[c + 1] = xb[c] + 4 * (L / 2 - 4 * (c / 4)) + 1;
-  t.XMAP.assign(size_t(L + 1) * (L + 1), 0);
+  const int K = (L + 1) * (L + 1);
+  std::vector<int> xmap(K, 0);
   for (int l = 0; l <= L; ++l)
     for (int ms = -l; ms <= l; ++ms) {
       const int m = ms < 0 ? -ms : ms;
@@ -279,20 +244,19 @@ void build_wave_tables(Tables& t) {
         const int c = (m - 1) / 2, dl = l - (2 * c + 1);
         quad = xb[c] + 4 * (dl / 2) + (m % 2 == 1 ? 0 : 2) + (dl % 2);
       }
-      t.XMAP[size_t(l) * l + l + ms] = 4 * quad + (ms < 0 ? 1 : 0);
+      xmap[size_t(l) * l + l + ms] = 4 * quad + (ms < 0 ? 1 : 0);
     }
   t.XQUADS = xb[L / 2];
-  const int K = (L + 1) * (L + 1), NXK = (K + 63) / 64, NXKP = (NXK + 3) / 4 * 4;
-  t.XMAPP.assign(size_t(64) * NXKP, -1);
-  for (int lane = 0; lane < 64; ++lane)
+  const int NXK = (K + NTH - 1) / NTH, NXKP = (NXK + 3) / 4 * 4;
+  t.XMAPP.assign(size_t(NTH) * NXKP, -1);
+  for (int tid = 0; tid < NTH; ++tid)
     for (int k = 0; k < NXK; ++k)
-      if (lane + 64 * k < K) t.XMAPP[size_t(lane) * NXKP + k] = t.XMAP[lane + 64 * k];
+      if (tid + NTH * k < K) t.XMAPP[size_t(tid) * NXKP + k] = xmap[tid + NTH * k];
 
-  t.TWR.assign(size_t(64) * 24, 0.0);
-  if (NMB > 2) throw std::invalid_argument("wave tables: more than two phi blocks");
+  t.TWR.assign(size_t(64) * TWRN, 0.0);
   for (int lane = 0; lane < 64; ++lane) {
     const int g = lane / 16, i = lane % 16;
-    double* o = &t.TWR[size_t(lane) * 24];
+    double* o = &t.TWR[size_t(lane) * TWRN];
     for (int mb = 0; mb < NMB; ++mb) {
       const int k = 16 * mb + i;
       if (k <= Q) {
@@ -303,24 +267,30 @@ void build_wave_tables(Tables& t) {
         o[6 * mb + 4] = trig(false, 8, k);
         o[6 * mb + 5] = trig(true, 8, k);
       }
-      const int k0 = 16 * mb + 4 * g, me = 2 * i + 2, mo = 2 * i + 1;
+      const int k0 = 16 * mb + 4 * g;
+      for (int mr = 0; mr < NMR; ++mr) {
+        const int me = 2 * (16 * mr + i) + 2, mo = me - 1;
+        double* a = &o[ASD + 4 * (mr * NMBP + mb)];
+        if (me <= L) {
+          a[0] = trig(false, me, k0);
+          a[1] = trig(true, me, k0);
+        }
+        if (mo <= L) {
+          a[2] = trig(false, mo, k0);
+          a[3] = trig(true, mo, k0);
+        }
+      }
+    }
+    for (int mr = 0; mr < NMR; ++mr) {
+      const int me = 2 * (16 * mr + i) + 2, mo = me - 1;
       if (me <= L) {
-        o[12 + 4 * mb + 0] = trig(false, me, k0);
-        o[12 + 4 * mb + 1] = trig(true, me, k0);
+        o[AST + 4 * mr + 0] = trig(false, me, 1);
+        o[AST + 4 * mr + 1] = trig(true, me, 1);
       }
       if (mo <= L) {
-        o[12 + 4 * mb + 2] = trig(false, mo, k0);
-        o[12 + 4 * mb + 3] = trig(true, mo, k0);
+        o[AST + 4 * mr + 2] = trig(false, mo, 1);
+        o[AST + 4 * mr + 3] = trig(true, mo, 1);
       }
-    }
-    const int me = 2 * i + 2, mo = 2 * i + 1;
-    if (me <= L) {
-      o[20] = trig(false, me, 1);
-      o[21] = trig(true, me, 1);
-    }
-    if (mo <= L) {
-      o[22] = trig(false, mo, 1);
-      o[23] = trig(true, mo, 1);
     }
   }
 
@@ -356,26 +326,35 @@ void build_wave_tables(Tables& t) {
       const int jp = pass < PASSES ? 8 * pass + pi + 1 : 0;
       for (int v = 0; v < NV0; ++v) t.SM0P[(size_t(pass) * 64 + lane) * NV0P + v] = S(8 * v + g + 4 * h, 0, jp);
     }
-  const int NROW = ntri(L) - (L + 1), NIT = (NROW + 63) / 64;
-  t.WP.assign(size_t(PASSES) * (NIT + 1) * 64 * 8, 0.0);
-  for (int pass = 0; pass < PASSES; ++pass)
-    for (int it = 0; it <= NIT; ++it)
-      for (int lane = 0; lane < 64; ++lane) {
-        int row = -1;
-        if (it < NIT) {
-          const int q = lane + 64 * it;
-          if (q < NROW) {
-            int l = 1;
-            while ((l + 1) * l / 2 <= q) ++l;  // rows with m > 0: l rows of degree l
-            row = tri(l, q - l * (l - 1) / 2 + 1);
-          }
-        } else if (lane <= L) {
-          row = tri(lane, 0);
+  const int NROW = ntri(L) - (L + 1), NIT = (NROW + NTH - 1) / NTH;
+  // row owned by thread tid in row step it (it = NIT: the m = 0 row), or -1
+  auto owned_row = [&](int it, int tid) {
+    if (it == NIT) return tid <= L ? tri(tid, 0) : -1;
+    const int q = tid + NTH * it;
+    if (q >= NROW) return -1;
+    int l = 1;
+    while ((l + 1) * l / 2 <= q) ++l;  // rows with m > 0: l rows of degree l
+    return tri(l, q - l * (l - 1) / 2 + 1);
+  };
+  if (NTH == 64) {
+    t.WP.assign(size_t(PASSES) * (NIT + 1) * 64 * 8, 0.0);
+    for (int pass = 0; pass < PASSES; ++pass)
+      for (int it = 0; it <= NIT; ++it)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int row = owned_row(it, lane);
+          if (row < 0) continue;
+          for (int jj = 0; jj < 8; ++jj)
+            t.WP[((size_t(pass) * (NIT + 1) + it) * 64 + lane) * 8 + jj] = t.W[size_t(row) * t.NJ + 8 * pass + jj + 1];
         }
+  } else {
+    t.WP.assign(size_t(NIT + 1) * NTH * L, 0.0);
+    for (int it = 0; it <= NIT; ++it)
+      for (int tid = 0; tid < NTH; ++tid) {
+        const int row = owned_row(it, tid);
         if (row < 0) continue;
-        for (int jj = 0; jj < 8; ++jj)
-          t.WP[((size_t(pass) * (NIT + 1) + it) * 64 + lane) * 8 + jj] = t.W[size_t(row) * t.NJ + 8 * pass + jj + 1];
+        for (int j = 1; j <= L; ++j) t.WP[(size_t(it) * NTH + tid) * L + j - 1] = t.W[size_t(row) * t.NJ + j];
       }
+  }
 }
 
 void host_pipeline(const Tables& t, const double* x1, const double* x2, int64_t n, double* y) {

@@ -46,17 +46,17 @@ struct Tables {
   int Mphi = 0;
   std::vector<double> Phi;
 
-  // Operand tables of the wave-per-product kernel whose phi transforms run on
-  // the matrix cores; built when L1 = L2 = Lout = L with L in {16, 32}
+  // Lane-permuted tables of the wave-per-product kernel whose phi transforms
+  // run on the matrix cores; built when L1 = L2 = Lout = L with L in {16, 32}
   // (waveL = L), empty otherwise.  Layouts are given in build_wave_tables.
   int waveL = 0;
-  std::vector<double> SM, TWS, TWA, TWR, SMP, SM0P, WP;
-  std::vector<int> XMAP, XMAPP;
+  std::vector<double> TWR, SMP, SM0P, WP;
+  std::vector<int> XMAPP;
   int XQUADS = 0;  // quads of the kernel's LDS image of one input pair
 };
 
-// Fills t.SM, t.TWS, t.TWA (and t.waveL) from t.S and the phi grid; t must
-// have L1 = L2 = Lout = L in {16, 32}.
+// Fills the wave-kernel tables (and t.waveL) from t.S, t.W and the phi grid;
+// t must have L1 = L2 = Lout = L in {16, 32}.
 void build_wave_tables(Tables& t);
 
 // Builds every table for (L1, L2, Lout) in fp64.  Throws std::invalid_argument

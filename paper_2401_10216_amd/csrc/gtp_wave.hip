@@ -1,0 +1,630 @@
+// Wave-per-product fused Gaunt tensor product on the matrix cores, for
+// L1 = L2 = Lout = L in {16, 32} (gfx950).
+//
+// Same sampled pipeline as the small-degree kernel (Sec. 3.2 with the
+// convolution theorem): theta nodes t_j = j pi / (2L+1), taken as mirror
+// pairs (j, 2L+1-j), j = 1..L, plus the two poles; phi samples
+// p_k = 2 pi k / NP.
+#include <type_traits>
+#include <utility>
+
+#include "gtp_device.hpp"
+
+namespace gtp {
+namespace {
+
+template <int B, int... Is, typename F>
+__device__ __forceinline__ void lfor_impl(std::integer_sequence<int, Is...>, F& f) {
+  (f(std::integral_constant<int, B + Is>{}), ...);
+}
+template <int B, int E, typename F>
+__device__ __forceinline__ void lfor(F&& f) {
+  if constexpr (E > B) lfor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
+}
+
+// Table reads go through buffer resources: 32-bit offsets (the wave-uniform
+// part in a scalar register), and reads past the table return zero.
+constexpr int kBufDword3 = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t table_rsrc(const float* p, int nfloats) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, nfloats * 4, kBufDword3);
+}
+__device__ __forceinline__ float tload(__amdgpu_buffer_rsrc_t r, int byte_off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));  // raw bits -> float
+}
+// 16-byte table read (byte_off a multiple of 16)
+__device__ __forceinline__ float4 tload4_s(__amdgpu_buffer_rsrc_t r, int byte_off, int uniform_off) {
+  const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, uniform_off, 0);
+  return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]), __uint_as_float(v[3]));
+}
+
+__device__ __forceinline__ float ld_in_any(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
+  return __uint_as_float(uint32_t(p[i]) << 16);
+}
+
+// One 64-lane wave per product, lane = 16 g + i, i = 8 h + pi.  The phi stage
+// at every theta node is a set of small dense contractions whose operands are
+// shared by all nodes and products, so it runs on the fp32 MFMA units
+// (16x16x4; A = phi operands, B = theta-synthesis values; the 16 columns are
+// the 8 mirror pairs of a pass: column pi = node jp, column 8 + pi = node
+// NT - jp):
+//   synthesis  pe/po/qe/qo[k][node] = sum over the even/odd-m cos/sin parts of
+//              trig(m phi_k) * value[m][node], k = 0..Q, Q = NP / 4 (the 4-fold
+//              phi symmetry of the small-degree kernel: the sample sets
+//              {k, -k, 2Q - k, 2Q + k} share these four sums);
+//   product    the four sample products folded into ce/co/se/so[k][node];
+//   analysis   C[m][node] = sum_k w_k trig(m phi_k) * {ce, co, se, so}[k][node]
+//              (w_k = 1/2 at k = 0, Q, where a 4-point set repeats points).
+// The accumulator layout of one contraction is the B layout of the next
+// (register r of lane (g, i) holds row 4 g + r, column i), so nothing moves
+// between them.  The A operands are generated in registers from per-lane
+// seeds by angle-addition rotations.  Theta synthesis (VALU) produces the B
+// operands in place: in K-step s lane (g, 8h + pi) sums the m-parts
+// m = 8s + 2g + 1 and + 2 at node jp over the l with l - m = h (mod 2); one
+// exchange between lanes i and i ^ 8 then gives node jp (even + odd) and its
+// mirror (even - odd).  Theta analysis (VALU) accumulates over the passes.
+// All table reads are lane-permuted copies read as one 16-byte load per lane
+// (the texture-address unit, not the bytes, bounds the table traffic).
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+template <int L>
+struct WGeo {
+  static constexpr int NT = 2 * L + 1;
+  static constexpr int NJ = NT + 1;
+  static constexpr int NP = (3 * L + 1 + 3) / 4 * 4;  // host rule with U = 2L, Le = L
+  static constexpr int Q = NP / 4;
+  static constexpr int PASSES = L / 8;               // 8 mirror pairs per pass
+  static constexpr int NKS = L / 8;                  // K-steps per class of m-parts
+  static constexpr int NMB = (Q + 1 + 15) / 16;      // 16-sample blocks of k = 0..Q
+  static constexpr int NW = L > 32 ? 4 : 1;          // waves per product
+  static constexpr int NTH = 64 * NW;
+  static constexpr int K = (L + 1) * (L + 1);
+  static constexpr int NMP2 = 2 * L + 2;             // moment row: [m=0, -, cos 1, sin 1, .., cos L, sin L]
+  static constexpr int EOP = 2 * 8 * NMP2;           // floats of one pass's combined moments
+  static constexpr int NROW = (L + 1) * (L + 2) / 2 - (L + 1);  // output rows with m > 0
+  static constexpr int NIT = (NROW + NTH - 1) / NTH;
+  static constexpr int NMBP = (NMB + 1) / 2 * 2;     // phi blocks in the seed layout (even)
+  static constexpr int NMR = L > 32 ? L / 32 : 1;    // 16-row blocks of analysis m-rows per class
+  static constexpr int ASD = 6 * NMBP;               // seed offsets: analysis seeds,
+  static constexpr int AST = ASD + 4 * NMR * NMBP;   //   analysis rotation steps,
+  static constexpr int TWRN = AST + 4 * NMR;         //   total per lane
+  // u-steps (two degrees each) of K-step s
+  __host__ __device__ static constexpr int nu(int s) { return L / 2 - 4 * s; }
+  // quad offset of the x block of m-pair c = 4 s + g (m = 2c + 1, 2c + 2): the
+  // m = 0 block (L + 1 quads) first, then 4 nu(s) quads + 1 pad per pair
+  __host__ __device__ static constexpr int xb(int c) {
+    return (L + 1) + c + 4 * (4 * ((c / 4) * (L / 2) - 2 * (c / 4) * (c / 4 - 1)) + (c % 4) * nu(c / 4));
+  }
+  static constexpr int XQ = xb(L / 2);
+  // u-step pairs before K-step s, and in all K-steps
+  __host__ __device__ static constexpr int u2off(int s) { return s * (L / 4) - s * (s - 1); }
+  static constexpr int TU2 = u2off(NKS);
+  static constexpr int NV0 = (L + 1 + 7) / 8;          // m = 0 steps of 8 degrees
+  static constexpr int NV0P = (NV0 + 3) / 4 * 4;
+  static constexpr int NXK = (K + NTH - 1) / NTH;      // staged coefficients per thread
+  static constexpr int NXKP = (NXK + 3) / 4 * 4;
+};
+
+// m = 0 theta synthesis reduction: lane (g, 8h + pi) holds the partial sum
+// over l = g + 4h (mod 8); returns the value at the lane's column node (the
+// node itself for h = 0, its mirror, odd l negated, for h = 1).
+__device__ __forceinline__ float m0_reduce(float a, int g, int h) {
+  a += __shfl_xor(a, 8);
+  const float t = __shfl_xor(a, 16);
+  const float sum = a + t, dif = (g & 1) ? t - a : a - t;
+  const float node = sum + __shfl_xor(sum, 32), mirror = dif + __shfl_xor(dif, 32);
+  return h ? mirror : node;
+}
+
+// cos/sin of m phi advanced by angle addition
+__device__ __forceinline__ void rot(float& c, float& s, float cr, float sr) {
+  const float cn = c * cr - s * sr;
+  s = fmaf(s, cr, c * sr);
+  c = cn;
+}
+
+// The per-wave view of one product: lane roles, the x image in LDS, the
+// theta tables.
+template <int L>
+struct WaveCtx {
+  using G = WGeo<L>;
+  int lane, g, h, pi;
+  const float4* xq;
+  __amdgpu_buffer_rsrc_t SPr, S0r;
+  const float* TWR;
+
+  __device__ __forceinline__ WaveCtx(int lane_, const float4* xq_, const DevTables& t)
+      : lane(lane_), g(lane_ >> 4), h((lane_ >> 3) & 1), pi(lane_ & 7), xq(xq_), TWR(t.TWR) {
+    SPr = table_rsrc(t.SMP, G::PASSES * G::TU2 * 64 * 4);
+    S0r = table_rsrc(t.SM0P, (G::PASSES + 1) * 64 * G::NV0P);
+  }
+
+  // m = 0 theta synthesis at the lane's column node (x1 and x2 cos parts);
+  // pass = PASSES gives the poles.  Split into the table read and the sums so
+  // that other loads can be issued in between.
+  __device__ __forceinline__ void m0_load(int pass, float (&sv)[G::NV0P]) const {
+    lfor<0, G::NV0P / 4>([&](auto V4) {
+      constexpr int v4 = decltype(V4)::value;
+      const float4 w = tload4_s(S0r, lane * G::NV0P * 4 + 16 * v4, pass * 64 * G::NV0P * 4);
+      sv[4 * v4] = w.x;
+      sv[4 * v4 + 1] = w.y;
+      sv[4 * v4 + 2] = w.z;
+      sv[4 * v4 + 3] = w.w;
+    });
+  }
+  __device__ __forceinline__ void m0_finish(const float (&sv)[G::NV0P], float& a1, float& a2) const {
+    float s1 = 0.0f, s2 = 0.0f;
+    lfor<0, G::NV0>([&](auto V) {
+      constexpr int v = decltype(V)::value;
+      const int l = 8 * v + g + 4 * h;
+      if (8 * v + 7 <= L || l <= L) {
+        const float4 q = xq[l];
+        s1 = fmaf(sv[v], q.x, s1);
+        s2 = fmaf(sv[v], q.z, s2);
+      }
+    });
+    a1 = m0_reduce(s1, g, h);
+    a2 = m0_reduce(s2, g, h);
+  }
+
+  // One pass (8 mirror pairs, jp = 8 pu + pi + 1): theta synthesis, phi
+  // synthesis contractions, sample products, phi analysis contractions.
+  // Returns the analysis accumulators o[mr][type] (row 4g + r of m-row block
+  // mr, column i) and zz, the m = 0 moment of the lane's column node.
+  __device__ __forceinline__ void pass(int pu, f4 (&o)[G::NMR][4], float& zz) const {
+    constexpr int NMB = G::NMB, NMBP = G::NMBP, NKS = G::NKS, TWRN = G::TWRN, NMR = G::NMR;
+    // loads first (m = 0 part, the first theta-table steps, the first phi
+    // operands), then the m = 0 sums
+    constexpr int D = 5;  // theta-table steps in flight
+    const int sbase = pu * G::TU2 * 64 * 16;
+    float s0v[G::NV0P];
+    m0_load(pu, s0v);
+    float4 sring[D];
+    lfor<0, D>([&](auto T) {
+      constexpr int tt = decltype(T)::value;
+      if constexpr (tt < G::TU2) sring[tt] = tload4_s(SPr, lane * 16, sbase + tt * 64 * 16);
+    });
+    // synthesis operands twc[type][mb] of K-step 0 and the rotation by 8 phi_k
+    const f4* seeds = reinterpret_cast<const f4*>(TWR + lane * TWRN);
+    float twc[4][NMB], r8c[NMB], r8s[NMB];
+    {
+      float sd[6 * NMBP];
+      lfor<0, 6 * NMBP / 4>([&](auto Q4) {
+        constexpr int q4 = decltype(Q4)::value;
+        const f4 v = seeds[q4];
+        lfor<0, 4>([&](auto E) { sd[4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
+      });
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        twc[0][mb] = sd[6 * mb + 0];  // cos, even m
+        twc[2][mb] = sd[6 * mb + 1];  // sin, even m
+        twc[1][mb] = sd[6 * mb + 2];  // cos, odd m
+        twc[3][mb] = sd[6 * mb + 3];  // sin, odd m
+        r8c[mb] = sd[6 * mb + 4];
+        r8s[mb] = sd[6 * mb + 5];
+      });
+    }
+    float c1, c2;
+    m0_finish(s0v, c1, c2);
+
+    // ---- 1 + 2a. theta synthesis feeding the phi-synthesis contractions
+    f4 acc[2][NMB][4];  // [input][k block][type]
+    lfor<0, NMB>([&](auto MB) {
+      constexpr int mb = decltype(MB)::value;
+      acc[0][mb][0] = f4{c1, c1, c1, c1};  // m = 0 enters every pe sample
+      acc[1][mb][0] = f4{c2, c2, c2, c2};
+      lfor<1, 4>([&](auto TY) {
+        acc[0][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        acc[1][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+      });
+    });
+    float asd[NMR][4 * NMB];  // analysis seeds, read during the last K-step
+    f4 ast[NMR];
+    lfor<0, NKS>([&](auto SS) {
+      constexpr int s = decltype(SS)::value;
+      const int c = 4 * s + g;
+      // this lane's parity: h = 0 takes (mo, l_a) and (mo+1, l_b), h = 1 (mo, l_b) and (mo+1, l_a)
+      const float4* xa = xq + G::xb(c) + h;
+      const float4* xe = xq + G::xb(c) + 3 - h;
+      f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
+      lfor<0, G::nu(s) / 2>([&](auto U2) {
+        constexpr int u2 = decltype(U2)::value, tt = G::u2off(s) + u2;
+        const float4 sv = sring[tt % D];
+        if constexpr (tt + D < G::TU2) sring[tt % D] = tload4_s(SPr, lane * 16, sbase + (tt + D) * 64 * 16);
+        lfor<0, 2>([&](auto E) {
+          constexpr int u = 2 * u2 + decltype(E)::value;
+          const float so = E == 0 ? sv.x : sv.z, se = E == 0 ? sv.y : sv.w;
+          const float4 qa = xa[4 * u], qe = xe[4 * u];
+          Vo += so * f4{qa.x, qa.y, qa.z, qa.w};
+          Ve += se * f4{qe.x, qe.y, qe.z, qe.w};
+        });
+        __builtin_amdgcn_sched_barrier(0);  // keep the prefetch distance
+      });
+      if constexpr (s == NKS - 1) {
+        lfor<0, NMR>([&](auto MR) {
+          constexpr int mr = decltype(MR)::value;
+          lfor<0, NMB>([&](auto Q4) {
+            constexpr int q4 = decltype(Q4)::value;
+            const f4 v = seeds[(G::ASD + 4 * (mr * NMBP + q4)) / 4];
+            lfor<0, 4>([&](auto E) { asd[mr][4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
+          });
+          ast[mr] = seeds[(G::AST + 4 * mr) / 4];
+        });
+      }
+      // column value: node jp (h = 0: own even + partner odd) or its mirror (h = 1: partner even - own odd)
+      f4 Bo, Be;
+      lfor<0, 4>([&](auto C) {
+        constexpr int cc = decltype(C)::value;
+        const float po = __shfl_xor(Vo[cc], 8), pe = __shfl_xor(Ve[cc], 8);
+        Bo[cc] = h ? po - Vo[cc] : po + Vo[cc];
+        Be[cc] = h ? pe - Ve[cc] : pe + Ve[cc];
+      });
+      lfor<0, NMB>([&](auto MB) {
+        constexpr int mb = decltype(MB)::value;
+        lfor<0, 2>([&](auto TI) {
+          constexpr int ti = decltype(TI)::value;
+          acc[ti][mb][0] = mfma4(twc[0][mb], Be[2 * ti], acc[ti][mb][0]);
+          acc[ti][mb][1] = mfma4(twc[1][mb], Bo[2 * ti], acc[ti][mb][1]);
+          acc[ti][mb][2] = mfma4(twc[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
+          acc[ti][mb][3] = mfma4(twc[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
+        });
+      });
+      if constexpr (s + 1 < NKS) {
+        // next K-step: m -> m + 8
+        lfor<0, NMB>([&](auto MB) {
+          constexpr int mb = decltype(MB)::value;
+          rot(twc[0][mb], twc[2][mb], r8c[mb], r8s[mb]);
+          rot(twc[1][mb], twc[3][mb], r8c[mb], r8s[mb]);
+        });
+      }
+    });
+
+    // ---- 2b. sample products, folded over the 4-point sets
+    lfor<0, NMB>([&](auto MB) {
+      constexpr int mb = decltype(MB)::value;
+      const f4 pe1 = acc[0][mb][0], po1 = acc[0][mb][1], qe1 = acc[0][mb][2], qo1 = acc[0][mb][3];
+      const f4 pe2 = acc[1][mb][0], po2 = acc[1][mb][1], qe2 = acc[1][mb][2], qo2 = acc[1][mb][3];
+      const f4 s1 = pe1 + po1, d1 = pe1 - po1, s2 = qe1 + qo1, d2 = qe1 - qo1;
+      const f4 t1 = pe2 + po2, u1 = pe2 - po2, t2 = qe2 + qo2, u2 = qe2 - qo2;
+      const f4 hk = (s1 + s2) * (t1 + t2), hmk = (s1 - s2) * (t1 - t2);
+      const f4 hpk = (d1 + d2) * (u1 + u2), hpmk = (d1 - d2) * (u1 - u2);
+      const f4 a = hk + hmk, b = hpk + hpmk, dd = hk - hmk, ee = hpk - hpmk;
+      acc[0][mb][0] = a + b;
+      acc[0][mb][1] = a - b;
+      acc[0][mb][2] = dd + ee;
+      acc[0][mb][3] = dd - ee;
+    });
+
+    // ---- 2c. phi analysis contractions; operands per k block from the seeds:
+    // w_k trig(m phi_k), k = 16 mb + 4 g + r, m = 2(16 mr + i) + 2 (even
+    // types) or + 1 (odd types)
+    lfor<0, NMR>([&](auto MR) {
+      lfor<0, 4>([&](auto TY) { o[decltype(MR)::value][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
+    });
+    zz = 0.0f;
+    lfor<0, NMB>([&](auto MB) {
+      constexpr int mb = decltype(MB)::value;
+      lfor<0, NMR>([&](auto MR) {
+        constexpr int mr = decltype(MR)::value;
+        float ce = asd[mr][4 * mb + 0], se = asd[mr][4 * mb + 1], co = asd[mr][4 * mb + 2], so = asd[mr][4 * mb + 3];
+        lfor<0, 4>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          if constexpr (r > 0) {
+            rot(ce, se, ast[mr].x, ast[mr].y);
+            rot(co, so, ast[mr].z, ast[mr].w);
+          }
+          const int k = 16 * mb + 4 * g + r;
+          const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f : 1.0f;
+          o[mr][0] = mfma4(wk * ce, acc[0][mb][0][r], o[mr][0]);
+          o[mr][1] = mfma4(wk * co, acc[0][mb][1][r], o[mr][1]);
+          o[mr][2] = mfma4(wk * se, acc[0][mb][2][r], o[mr][2]);
+          o[mr][3] = mfma4(wk * so, acc[0][mb][3][r], o[mr][3]);
+          if constexpr (mr == 0) zz = fmaf(wk, acc[0][mb][0][r], zz);
+        });
+      });
+    });
+    zz += __shfl_xor(zz, 16);
+    zz += __shfl_xor(zz, 32);
+  }
+
+  // ---- 3. mirror combination into LDS, eo[parity][pi][slot]: parity 0 =
+  // C(jp) + C(NT - jp), 1 = C(jp) - C(NT - jp); slot 0 = m 0, 2m = cos m,
+  // 2m + 1 = sin m
+  __device__ __forceinline__ void store_moments(float* eo, const f4 (&o)[G::NMR][4], float zz) const {
+    float* const eoh = eo + (h * 8 + pi) * G::NMP2;
+    lfor<0, G::NMR>([&](auto MR) {
+      constexpr int mr = decltype(MR)::value;
+      lfor<0, 2>([&](auto PAR) {
+        constexpr int odd = decltype(PAR)::value;  // types odd (cos), odd + 2 (sin)
+        lfor<0, 4>([&](auto R) {
+          constexpr int r = decltype(R)::value;
+          const int m = 2 * (16 * mr + 4 * g + r) + (odd ? 1 : 2);
+          const float pc = __shfl_xor(o[mr][odd][r], 8), ps = __shfl_xor(o[mr][odd + 2][r], 8);
+          const float vc = h ? pc - o[mr][odd][r] : pc + o[mr][odd][r];
+          const float vs = h ? ps - o[mr][odd + 2][r] : ps + o[mr][odd + 2][r];
+          // m-rows past L exist only at L = 16 (16 rows per class)
+          if (L != 16 || m <= L) *reinterpret_cast<float2*>(eoh + 2 * m) = make_float2(vc, vs);
+        });
+      });
+    });
+    const float pz = __shfl_xor(zz, 8);
+    if (g == 0) eoh[0] = h ? pz - zz : pz + zz;
+  }
+};
+
+// x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
+// threads of the workgroup: every load is issued before the first wait
+template <int L, typename TIn>
+__device__ __forceinline__ void stage_x(float* xs, const TIn* x1, const TIn* x2, int64_t P, int tid,
+                                        const int* xmap) {
+  using G = WGeo<L>;
+  constexpr int K = G::K, NTH = G::NTH, NXK = G::NXK, NXKP = G::NXKP;
+  int slot[NXKP];
+  lfor<0, NXKP / 4>([&](auto K4) {
+    constexpr int k4 = decltype(K4)::value;
+    const int4 v = reinterpret_cast<const int4*>(xmap + tid * NXKP)[k4];
+    slot[4 * k4] = v.x;
+    slot[4 * k4 + 1] = v.y;
+    slot[4 * k4 + 2] = v.z;
+    slot[4 * k4 + 3] = v.w;
+  });
+  float v1[NXK], v2[NXK];
+  lfor<0, NXK>([&](auto KK) {
+    constexpr int k = decltype(KK)::value;
+    const int e = tid + NTH * k;
+    if (NTH * k + NTH - 1 < K || e < K) {
+      v1[k] = ld_in_any(x1, P * K + e);
+      v2[k] = ld_in_any(x2, P * K + e);
+    }
+  });
+  lfor<0, G::XQ / NTH>([&](auto Z) {
+    reinterpret_cast<float4*>(xs)[tid + NTH * decltype(Z)::value] = make_float4(0.f, 0.f, 0.f, 0.f);
+  });
+  if (tid < G::XQ % NTH) reinterpret_cast<float4*>(xs)[tid + NTH * (G::XQ / NTH)] = make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+  lfor<0, NXK>([&](auto KK) {
+    constexpr int k = decltype(KK)::value;
+    if (NTH * k + NTH - 1 < K || tid + NTH * k < K) {
+      xs[slot[k]] = v1[k];
+      xs[slot[k] + 2] = v2[k];
+    }
+  });
+  __syncthreads();
+}
+
+// degree l and order m > 0 of the q-th output row with m > 0 in tri order
+__device__ __forceinline__ void row_lm(int q, int& l, int& m) {
+  l = int((sqrtf(8.0f * float(q) + 1.0f) + 1.0f) * 0.5f);
+  l -= (l * (l - 1) / 2 > q) ? 1 : 0;
+  l += ((l + 1) * l / 2 <= q) ? 1 : 0;
+  m = q - l * (l - 1) / 2 + 1;
+}
+
+// L in {16, 32}: one wave per product; theta analysis accumulates in
+// registers after every pass.
+template <int L, typename TIn>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_full_wave(
+    const TIn* __restrict__ x1, const TIn* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+  using G = WGeo<L>;
+  static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
+  constexpr int NJ = G::NJ, NP = G::NP;
+  constexpr int NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
+  __shared__ __align__(16) float xs[G::XQ * 4];
+  __shared__ __align__(16) float eo[G::EOP];
+
+  const int lane = threadIdx.x;
+  const int64_t P = blockIdx.x;
+  if (P >= n) return;  // whole-wave exit (one product per workgroup)
+  stage_x<L>(xs, x1, x2, P, lane, t.XMAP);
+  const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(xs), t);
+
+  const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
+  const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
+  // theta-analysis rows: tri(l, 0) with l = lane (l <= L), and the rows with
+  // m > 0 numbered q = lane + 64 it; per row the LDS offset of its moment
+  // (parity of l + m, m-part)
+  float y0 = 0.0f, yc[NIT], ys[NIT];
+  int er[NIT];
+  const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP2;
+  lfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    yc[it] = 0.0f;
+    ys[it] = 0.0f;
+    int l, m;
+    row_lm(lane + 64 * it, l, m);
+    er[it] = ((l + m) & 1) * 8 * NMP2 + 2 * m;
+  });
+
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
+    f4 o[1][4];
+    float zz;
+    w.pass(pu, o, zz);
+    w.store_moments(eo, o, zz);
+    __syncthreads();
+
+    // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
+    const int wbase = pu * (NIT + 1) * 64 * 32;
+    if (lane <= L) {
+      const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
+      const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      lfor<0, 8>([&](auto JJ) {
+        constexpr int jj = decltype(JJ)::value;
+        y0 = fmaf(wv[jj], eo[er0 + jj * NMP2], y0);
+      });
+    }
+    lfor<0, NIT>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      if (lane + 64 * it < NROW) {
+        const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
+        const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
+        const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        lfor<0, 8>([&](auto JJ) {
+          constexpr int jj = decltype(JJ)::value;
+          const float2 cs = *reinterpret_cast<const float2*>(eo + er[it] + jj * NMP2);
+          yc[it] = fmaf(wv[jj], cs.x, yc[it]);
+          ys[it] = fmaf(wv[jj], cs.y, ys[it]);
+        });
+      }
+      if constexpr (it % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+    });
+    __syncthreads();  // eo is rewritten by the next pass
+  }
+
+  // poles (only the m = 0 parts are non-zero there) and the stores
+  float p1, p2;
+  {
+    float sv[G::NV0P];
+    w.m0_load(PASSES, sv);
+    w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  }
+  const float f = p1 * p2 * float(NP);
+  const float fN = __shfl(f, 0), fS = __shfl(f, 8);
+  if (lane <= L) {
+    const int l = lane;
+    y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
+    y[P * K + l * l + l] = y0;
+  }
+  lfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    const int q = lane + 64 * it;
+    if (q < NROW) {
+      int l, m;
+      row_lm(q, l, m);
+      y[P * K + l * l + l + m] = yc[it];
+      y[P * K + l * l + l - m] = ys[it];
+    }
+  });
+}
+
+// L = 64: four waves per product (256 threads), wave v runs passes 2v and
+// 2v + 1.  The moments of the first pass go to LDS at once; those of the
+// second stay in registers until every wave is done with the x image, then
+// go into its place.  The 256 threads then do the theta analysis, each over
+// all 64 mirror pairs of its output rows.
+template <int L, typename TIn>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_full_wave4(
+    const TIn* __restrict__ x1, const TIn* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+  using G = WGeo<L>;
+  static_assert(G::NW == 4 && G::PASSES == 8, "four waves, two passes each");
+  constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
+                NIT = G::NIT, EOP = G::EOP, NTH = G::NTH;
+  constexpr int XF = (G::XQ * 4 > 4 * EOP) ? G::XQ * 4 : 4 * EOP;  // x image, later the odd passes' moments
+  __shared__ __align__(16) float lds[XF + 4 * EOP];               // + the even passes' moments
+  float* const eo_odd = lds;
+  float* const eo_even = lds + XF;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t P = blockIdx.x;
+  if (P >= n) return;  // whole-workgroup exit (one product per workgroup)
+  stage_x<L>(lds, x1, x2, P, tid, t.XMAP);
+  const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(lds), t);
+
+  f4 o[G::NMR][4];
+  float zz;
+  w.pass(__builtin_amdgcn_readfirstlane(2 * wave), o, zz);
+  w.store_moments(eo_even + wave * EOP, o, zz);
+  w.pass(__builtin_amdgcn_readfirstlane(2 * wave + 1), o, zz);
+  // poles (only the m = 0 parts are non-zero there), before the x image goes
+  float p1, p2;
+  {
+    float sv[G::NV0P];
+    w.m0_load(PASSES, sv);
+    w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  }
+  const float f = p1 * p2 * float(NP);
+  const float fN = __shfl(f, 0), fS = __shfl(f, 8);
+  __syncthreads();  // the x image is dead
+  w.store_moments(eo_odd + wave * EOP, o, zz);
+  __syncthreads();
+
+  // ---- 4. theta analysis: thread tid owns row tri(tid, 0) (tid <= L) and
+  // the m > 0 rows q = tid + 256 it; weights WP[it][tid][j - 1], j = 1..L
+  const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, (NIT + 1) * NTH * L);
+  auto row_sum = [&](int it, int er, float& ac, float& as, bool with_sin) {
+    lfor<0, PASSES>([&](auto PP) {
+      constexpr int pp = decltype(PP)::value;  // pass: pairs 8 pp + 1 .. 8 pp + 8
+      const float* eop = (pp % 2 == 0 ? eo_even : eo_odd) + (pp / 2) * EOP;
+      const float4 w0 = tload4_s(WPr, tid * L * 4 + pp * 32, it * NTH * L * 4);
+      const float4 w1 = tload4_s(WPr, tid * L * 4 + pp * 32 + 16, it * NTH * L * 4);
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      lfor<0, 8>([&](auto JJ) {
+        constexpr int jj = decltype(JJ)::value;
+        const float2 cs = *reinterpret_cast<const float2*>(eop + er + jj * NMP2);
+        ac = fmaf(wv[jj], cs.x, ac);
+        if (with_sin) as = fmaf(wv[jj], cs.y, as);
+      });
+      if constexpr (pp % 4 == 3) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+    });
+  };
+  if (tid <= L) {
+    const int l = tid;
+    float a0 = 0.0f, unused = 0.0f;
+    row_sum(NIT, (l & 1) * 8 * NMP2, a0, unused, false);
+    const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
+    a0 = fmaf(tload(Wr, (l * (l + 1) / 2) * 4), fN + ((l & 1) ? -fS : fS), a0);
+    y[P * K + l * l + l] = a0;
+  }
+  for (int it = 0; it < NIT; ++it) {
+    const int q = tid + NTH * it;
+    if (q < NROW) {
+      int l, m;
+      row_lm(q, l, m);
+      float ac = 0.0f, as = 0.0f;
+      row_sum(it, ((l + m) & 1) * 8 * NMP2 + 2 * m, ac, as, true);
+      y[P * K + l * l + l + m] = ac;
+      y[P * K + l * l + l - m] = as;
+    }
+  }
+}
+
+template <int L>
+hipError_t launch_wave_one(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                           hipStream_t s) {
+  using G = WGeo<L>;
+  // at most 2^30 workgroups per launch
+  for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
+    const int64_t nn = n - p0 < (int64_t(1) << 30) ? n - p0 : (int64_t(1) << 30);
+    const size_t es = in_type == IN_BF16 ? 2 : 4;
+    const char* a = static_cast<const char*>(x1) + size_t(p0) * G::K * es;
+    const char* b = static_cast<const char*>(x2) + size_t(p0) * G::K * es;
+    float* yy = y + size_t(p0) * G::K;
+    if constexpr (G::NW == 1) {
+      if (in_type == IN_BF16)
+        hipLaunchKernelGGL((k_full_wave<L, uint16_t>), dim3(unsigned(nn)), dim3(64), 0, s,
+                           reinterpret_cast<const uint16_t*>(a), reinterpret_cast<const uint16_t*>(b), yy, nn, t);
+      else
+        hipLaunchKernelGGL((k_full_wave<L, float>), dim3(unsigned(nn)), dim3(64), 0, s,
+                           reinterpret_cast<const float*>(a), reinterpret_cast<const float*>(b), yy, nn, t);
+    } else {
+      if (in_type == IN_BF16)
+        hipLaunchKernelGGL((k_full_wave4<L, uint16_t>), dim3(unsigned(nn)), dim3(G::NTH), 0, s,
+                           reinterpret_cast<const uint16_t*>(a), reinterpret_cast<const uint16_t*>(b), yy, nn, t);
+      else
+        hipLaunchKernelGGL((k_full_wave4<L, float>), dim3(unsigned(nn)), dim3(G::NTH), 0, s,
+                           reinterpret_cast<const float*>(a), reinterpret_cast<const float*>(b), yy, nn, t);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+hipError_t launch_full_wave(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
+                            hipStream_t s, bool* supported) {
+  *supported = true;
+  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, x2, in_type, n, y, s);
+  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, x2, in_type, n, y, s);
+  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, x2, in_type, n, y, s);
+  *supported = false;
+  return hipSuccess;
+}
+
+}  // namespace gtp
