@@ -38,25 +38,42 @@ def nsh(L):
     return (L + 1) * (L + 1)
 
 
-def kernel_sources_sha() -> str:
+SHARED_SOURCES = ["gtp_api.hip", "gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
+
+
+def dominant_kernel(workload: str, L: int):
+    """(kernel, roofline bound, source file) of the kernel that dominates a workload."""
+    if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
+        return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
+    if workload == "manybody":
+        return "k_self_stepwise_small", "alu", "gtp_small.hip"
+    return "k_full_small", "alu", "gtp_small.hip"
+
+
+def kernel_sources_sha(kernel_source: str) -> str:
+    """Hash of the sources that make up one kernel's launch path."""
     h = hashlib.sha256()
-    for f in sorted(os.listdir(os.path.join(ROOT, "paper_2401_10216_amd", "csrc"))):
+    for f in sorted(SHARED_SOURCES + [kernel_source]):
         with open(os.path.join(ROOT, "paper_2401_10216_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def load_traffic(workload: str):
+def traffic_key(workload: str, L: int) -> str:
+    return f"sweep_L{L}" if workload == "sweep" else workload
+
+
+def load_traffic(key: str, kernel_source: str):
     """HBM bytes per launch from committed rocprofv3 FETCH_SIZE / WRITE_SIZE
-    counters, if they were taken on the current kernel sources."""
+    counters, if they were taken on the current sources of the kernel."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     try:
-        d = json.load(open(path)).get(workload)
+        d = json.load(open(path)).get(key)
     except Exception:
         return None
-    if not d or d.get("kernel_sha") != kernel_sources_sha():
+    if not d or d.get("kernel_sha") != kernel_sources_sha(kernel_source):
         return None
     return d.get("bytes_per_launch")
 
@@ -221,9 +238,11 @@ def main():
     roof = None
     if alg_flops:
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
-        tb = load_traffic(args.workload)
-        roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb,
+        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)))
+        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)), ksrc)
+        # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
+        roof = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb, "kernel": kname,
                 "kernel_ms": round(kernel_ms, 5), "alg_flops_per_product": alg_flops,
                 "hbm": {"achieved": round(alg_bytes * products / (kernel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
                         "unit": "GB/s", "alg_bytes_per_product": alg_bytes}}

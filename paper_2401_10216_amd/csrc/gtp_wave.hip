@@ -425,19 +425,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
   const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
   // theta-analysis rows: tri(l, 0) with l = lane (l <= L), and the rows with
-  // m > 0 numbered q = lane + 64 it; per row the LDS offset of its moment
-  // (parity of l + m, m-part)
+  // m > 0 numbered q = lane + 64 it
   float y0 = 0.0f, yc[NIT], ys[NIT];
-  int er[NIT];
   const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP2;
   lfor<0, NIT>([&](auto IT) {
-    constexpr int it = decltype(IT)::value;
-    yc[it] = 0.0f;
-    ys[it] = 0.0f;
-    int l, m;
-    row_lm(lane + 64 * it, l, m);
-    er[it] = ((l + m) & 1) * 8 * NMP2 + 2 * m;
+    yc[decltype(IT)::value] = 0.0f;
+    ys[decltype(IT)::value] = 0.0f;
   });
+  // LDS offset of row q's moment (parity of l + m, m-part), recomputed in
+  // every pass from an opaque copy of the lane id (hoisting these offsets out
+  // of the pass loop would keep a dozen registers live and spill them)
+  auto row_er = [&](int q) {
+    int l, m;
+    row_lm(q, l, m);
+    return ((l + m) & 1) * 8 * NMP2 + 2 * m;
+  };
 
   for (int pass = 0; pass < PASSES; ++pass) {
     const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
@@ -449,6 +451,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
 
     // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
     const int wbase = pu * (NIT + 1) * 64 * 32;
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
     if (lane <= L) {
       const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
       const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
@@ -464,9 +468,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
         const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        const int er = row_er(ln + 64 * it);
         lfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
-          const float2 cs = *reinterpret_cast<const float2*>(eo + er[it] + jj * NMP2);
+          const float2 cs = *reinterpret_cast<const float2*>(eo + er + jj * NMP2);
           yc[it] = fmaf(wv[jj], cs.x, yc[it]);
           ys[it] = fmaf(wv[jj], cs.y, ys[it]);
         });
@@ -490,9 +495,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
     y[P * K + l * l + l] = y0;
   }
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
   lfor<0, NIT>([&](auto IT) {
     constexpr int it = decltype(IT)::value;
-    const int q = lane + 64 * it;
+    const int q = ln + 64 * it;
     if (q < NROW) {
       int l, m;
       row_lm(q, l, m);
