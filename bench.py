@@ -126,7 +126,16 @@ def make_workload(args, torch, gtp, inputs):
             t1 = torch.from_numpy(x1).to(dev)
             t2 = torch.from_numpy(x2).to(dev)
             in_bytes = 4
-        plan = gtp.Plan(L, L, L)
+        flags = {"auto": 0, "direct": gtp.GTP_CONV_DIRECT, "generic": gtp.GTP_FORCE_GENERIC}[args.conv]
+        plan = gtp.Plan(L, L, L, flags)
+        if args.products:
+            # crossover runs: the first N products, as [N, 1, K]
+            C = 1
+            B = min(args.products, t1.shape[0] * t1.shape[1])
+            t1 = t1.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
+            t2 = t2.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
+            x1 = x1.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
+            x2 = x2.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
         y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
 
         def step():
@@ -140,6 +149,8 @@ def make_workload(args, torch, gtp, inputs):
 
         desc = {"workload": f"{w}: B={B} x C={C}, L1=L2=Lout={L}, iid N(0,1)" + (" rounded to bf16" if w == "highdeg" else ""),
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "bf16" if w == "highdeg" else "f32"}
+        if args.conv != "auto":
+            desc["conv"] = args.conv
         return step, B * C, desc, ALG_FLOPS.get(L), in_bytes * 2 * nsh(L) + 4 * nsh(L), oracle_sample, idx_cfg
     if w == "manybody":
         N, C, L, nu, Lout = 1728, 256, 2, 3, 3
@@ -204,6 +215,12 @@ def main():
     ap.add_argument("--workload", default="edge")
     ap.add_argument("--L", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--conv", choices=["auto", "direct", "generic"], default="auto",
+                    help="step-2 algorithm for the convolution crossover: auto (the shipped kernels), direct "
+                         "(fused direct real-form convolution), generic (workgroup-per-product convolution "
+                         "theorem, the direct kernel's structural twin)")
+    ap.add_argument("--products", type=int, default=0,
+                    help="use only the first N products of a pair workload (crossover runs of slow variants)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the Gaunt tensor product shards over (b,c) with no exchange, "

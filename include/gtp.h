@@ -87,7 +87,11 @@ gtp_status gtp_plan_destroy(gtp_plan p);
  *   y[b,c,:] = GTP(x1[b,c,:], x2[b,c,:]) truncated to degree Lout.
  * x1: [B, C, (L1+1)^2], x2: [B, C, (L2+1)^2] of type in_dtype;
  * y: [B, C, (Lout+1)^2] fp32.  B*C == 0 is a successful no-op.  y must not
- * overlap x1 or x2.  The Fourier grids never leave the chip. */
+ * overlap x1 or x2.  The Fourier grids never leave the chip.  The plan's
+ * GTP_CONV_* flag picks step 2 (eq. 2D-conv): the convolution theorem
+ * (GTP_CONV_FFT, and GTP_CONV_AUTO, which measured faster at every degree)
+ * or the direct real-form convolution (GTP_CONV_DIRECT; GTP_ERR_UNSUPPORTED
+ * when its per-product working set exceeds 64 KB of LDS, about L1 = L2 = 40). */
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 

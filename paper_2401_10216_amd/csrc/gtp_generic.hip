@@ -324,6 +324,136 @@ __global__ __launch_bounds__(kBlock) void k_sh_filter(int L, const float* __rest
   }
 }
 
+// Fused product with the 2D convolution done directly (Sec. 3.2, eq.
+// 2D-conv, without the convolution theorem), in the real form of the
+// Fourier basis, one product per workgroup:
+//   (1) g_t[m][u] = sum_l T1[tri(l, m)][u] (x_t[l, +m] - i x_t[l, -m]): F_t =
+//       sum_{m >= 0, u} Re(g_t[m][u] e^{i m phi}) T_m(u theta), T_m = cos for
+//       even m, sin for odd m (the theta series of eq. sh-fs, real form);
+//   (2) c[m3][u3]: product of the two series; in phi
+//       Re(a e^{i m1 phi}) Re(b e^{i m2 phi}) = 1/2 Re(a b e^{i (m1+m2) phi})
+//       + 1/2 Re(a conj(b) e^{i (m1-m2) phi}), in theta the product-to-sum
+//       identities of cos / sin, each output cell gathering its terms;
+//   (3) y[l, +m] = n_m sum_u Z[tri(l, m)][u] Re c[m][u], y[l, -m] = n_m sum_u
+//       Z[tri(l, m)][u] (-Im c[m][u]), Z = Zc (even m) or Zs (odd m),
+//       n_0 = 2 pi, n_m = pi (eq. fs-sh: the phi integral of cos^2, sin^2).
+// LDS: x1, x2, then g1, g2 (complex), c (complex).
+struct DirectLayout {
+  int K1, K2, G1, G2, C3, off_g1, off_g2, off_c, total;
+};
+__host__ __device__ inline DirectLayout direct_layout(const DevTables& t) {
+  DirectLayout d;
+  d.K1 = (t.L1 + 1) * (t.L1 + 1);
+  d.K2 = (t.L2 + 1) * (t.L2 + 1);
+  d.G1 = (t.L1 + 1) * (t.L1 + 1);  // [m][u], m, u <= L1
+  d.G2 = (t.L2 + 1) * (t.L2 + 1);
+  d.C3 = (t.Le + 1) * (t.U + 1);   // [m3][u3], m3 <= Le, u3 <= U
+  d.off_g1 = d.K1 + d.K2;
+  d.off_g2 = d.off_g1 + 2 * d.G1;
+  d.off_c = d.off_g2 + 2 * d.G2;
+  d.total = d.off_c + 2 * d.C3;
+  return d;
+}
+
+// theta product-to-sum coefficient of T_{m1}(u1 t) T_{m2}(u2 t) on the output
+// term T_{m1+m2}(u3 t): sum = 1 for u1 + u2 = u3, else the difference term
+__device__ __forceinline__ float theta_coef(bool odd1, bool odd2, bool is_sum, int u1, int u2) {
+  if (!odd1 && !odd2) return 0.5f;                       // cos cos = (cos(u1-u2) + cos(u1+u2)) / 2
+  if (odd1 && odd2) return is_sum ? -0.5f : 0.5f;        // sin sin = (cos(u1-u2) - cos(u1+u2)) / 2
+  if (is_sum) return 0.5f;                               // sin cos, cos sin: sin(u1+u2) / 2 ...
+  const int d = odd1 ? u1 - u2 : u2 - u1;                // ... + sin(u1-u2) / 2, resp. + sin(u2-u1) / 2
+  return d > 0 ? 0.5f : (d < 0 ? -0.5f : 0.0f);
+}
+
+template <typename T1, typename T2>
+__global__ __launch_bounds__(kBlock) void k_full_direct(DevTables t, const T1* __restrict__ x1,
+                                                        const T2* __restrict__ x2, float* __restrict__ y, int64_t n) {
+  extern __shared__ float smem[];
+  const DirectLayout d = direct_layout(t);
+  const int tid = threadIdx.x;
+  const int L1 = t.L1, L2 = t.L2, Le = t.Le, U = t.U;
+  const int KO = (t.Lout + 1) * (t.Lout + 1);
+  float* xs1 = smem;
+  float* xs2 = smem + d.K1;
+  float2* g1 = reinterpret_cast<float2*>(smem + d.off_g1);
+  float2* g2 = reinterpret_cast<float2*>(smem + d.off_g2);
+  float2* c3 = reinterpret_cast<float2*>(smem + d.off_c);
+  const float kPiF = 3.14159265358979323846f;
+
+  for (int64_t p = blockIdx.x; p < n; p += gridDim.x) {
+    for (int i = tid; i < d.K1; i += kBlock) xs1[i] = ld_in(x1, p * d.K1 + i);
+    for (int i = tid; i < d.K2; i += kBlock) xs2[i] = ld_in(x2, p * d.K2 + i);
+    __syncthreads();
+    // (1) theta series of every phi part
+    for (int e = tid; e < d.G1 + d.G2; e += kBlock) {
+      const bool second = e >= d.G1;
+      const int L = second ? L2 : L1;
+      const int ee = second ? e - d.G1 : e;
+      const int m = ee / (L + 1), u = ee % (L + 1);
+      const float* xs = second ? xs2 : xs1;
+      float re = 0.0f, im = 0.0f;
+      for (int l = (m > u ? m : u); l <= L; ++l) {
+        if ((l - u) & 1) continue;  // Theta_lm has only u = l (mod 2)
+        const float c = t.T1[dtri(l, m) * t.ldT1 + u];
+        re = fmaf(c, xs[l * l + l + m], re);
+        if (m > 0) im = fmaf(-c, xs[l * l + l - m], im);
+      }
+      (second ? g2 : g1)[ee] = make_float2(re, im);
+    }
+    __syncthreads();
+    // (2) direct convolution, gathered per output cell (m3, u3)
+    for (int e = tid; e < d.C3; e += kBlock) {
+      const int m3 = e / (U + 1), u3 = e % (U + 1);
+      float cr = 0.0f, ci = 0.0f;
+      for (int m1 = 0; m1 <= L1; ++m1) {
+        // the (m2, phi factor) partners of m1: 0 = a b (m1 + m2 = m3),
+        // 1 = a conj(b) (m1 - m2 = m3), 2 = conj(a) b (m2 - m1 = m3 > 0)
+        for (int kind = 0; kind < 3; ++kind) {
+          const int m2 = kind == 0 ? m3 - m1 : (kind == 1 ? m1 - m3 : m1 + m3);
+          if (m2 < 0 || m2 > L2 || (kind == 2 && m3 == 0)) continue;
+          const bool odd1 = m1 & 1, odd2 = m2 & 1;
+          const float2* a = g1 + m1 * (L1 + 1);
+          const float2* b = g2 + m2 * (L2 + 1);
+          float sr = 0.0f, si = 0.0f;
+          for (int u1 = 0; u1 <= L1; ++u1) {
+            // theta partners: u1 + u2 = u3, u1 - u2 = u3, u2 - u1 = u3 (> 0)
+            for (int tk = 0; tk < 3; ++tk) {
+              const int u2 = tk == 0 ? u3 - u1 : (tk == 1 ? u1 - u3 : u1 + u3);
+              if (u2 < 0 || u2 > L2 || (tk == 2 && u3 == 0)) continue;
+              const float w = theta_coef(odd1, odd2, tk == 0, u1, u2);
+              if (w == 0.0f) continue;
+              const float2 av = a[u1], bv = b[u2];
+              // a b, a conj(b) or conj(a) b
+              const float bi = kind == 1 ? -bv.y : bv.y, ai = kind == 2 ? -av.y : av.y;
+              sr = fmaf(w, av.x * bv.x - ai * bi, sr);
+              si = fmaf(w, av.x * bi + ai * bv.x, si);
+            }
+          }
+          cr = fmaf(0.5f, sr, cr);
+          ci = fmaf(0.5f, si, ci);
+        }
+      }
+      c3[e] = make_float2(cr, ci);
+    }
+    __syncthreads();
+    // (3) projection onto the output SH
+    for (int o = tid; o < KO; o += kBlock) {
+      int l = 0;
+      while ((l + 1) * (l + 1) <= o) ++l;
+      const int ms = o - l * l - l, m = ms < 0 ? -ms : ms;
+      float acc = 0.0f;
+      if (l <= Le) {
+        const float* Z = ((m & 1) ? t.Zs : t.Zc) + dtri(l, m) * t.ldZ;
+        const float2* c = c3 + m * (U + 1);
+        for (int u = 0; u <= U; ++u) acc = fmaf(Z[u], ms < 0 ? -c[u].y : c[u].x, acc);
+        acc *= m == 0 ? 2.0f * kPiF : kPiF;
+      }
+      y[p * KO + o] = acc;
+    }
+    __syncthreads();
+  }
+}
+
 unsigned grid_for(int64_t work_items, int per_block) {
   int64_t g = (work_items + per_block - 1) / per_block;
   if (g < 1) g = 1;
@@ -384,8 +514,19 @@ hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* 
   return hipGetLastError();
 }
 
-hipError_t launch_full_direct(const DevTables&, const void*, const void*, int, int64_t, float*, hipStream_t) {
-  return hipErrorNotSupported;
+hipError_t launch_full_direct(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+                              float* y, hipStream_t s) {
+  const size_t lds = size_t(direct_layout(t).total) * sizeof(float);
+  if (lds > 64 * 1024) return hipErrorNotSupported;  // the default LDS limit of one workgroup
+  if (n <= 0) return hipSuccess;
+  const dim3 grid(grid_for(n, 1)), block(kBlock);
+  if (in_type == IN_BF16)
+    hipLaunchKernelGGL((k_full_direct<uint16_t, uint16_t>), grid, block, lds, s, t,
+                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n);
+  else
+    hipLaunchKernelGGL((k_full_direct<float, float>), grid, block, lds, s, t, static_cast<const float*>(x1),
+                       static_cast<const float*>(x2), y, n);
+  return hipGetLastError();
 }
 
 hipError_t launch_sh2fourier(const DevTables& t, int L, const void* x, int in_type, int64_t n, float* grid,

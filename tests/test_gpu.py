@@ -102,6 +102,49 @@ def test_large_degree_ragged(L, n, generic):
     assert err <= TOL, err
 
 
+@pytest.mark.parametrize("L1,L2,Lout,n", [(1, 1, 2, 300), (2, 2, 2, 1024), (3, 2, 4, 257), (6, 6, 6, 513),
+                                          (8, 8, 8, 129), (16, 16, 16, 64), (4, 4, 9, 100)])
+def test_direct_convolution(L1, L2, Lout, n):
+    """Fused direct-convolution path (GTP_CONV_DIRECT) against the oracle."""
+    rng = np.random.default_rng(40 + L1 + 3 * L2 + 7 * Lout)
+    a = rng.standard_normal((n, 1, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L2))).astype(np.float32)
+    _say(f"direct L1={L1} L2={L2} Lout={Lout} n={n}")
+    plan = gtp.Plan(L1, L2, Lout, gtp.GTP_CONV_DIRECT)
+    assert plan.info()["conv"] == gtp.GTP_CONV_DIRECT
+    y = run_full(plan, a, b)
+    idx = np.arange(0, n, max(1, n // 64))
+    ref = oracle_pair(a[idx].astype(np.float64), b[idx].astype(np.float64), L1, L2, Lout)
+    err = O.max_rel_err(y[idx], ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_direct_convolution_bf16_and_empty():
+    L = 4
+    rng = np.random.default_rng(44)
+    x = rng.standard_normal((2, 200, 1, O.nsh(L))).astype(np.float32)
+    bits1, v1 = inputs.round_to_bf16(x[0])
+    bits2, v2 = inputs.round_to_bf16(x[1])
+    plan = gtp.Plan(L, L, L, gtp.GTP_CONV_DIRECT)
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_full(plan, t1, t2)
+    torch.cuda.synchronize()
+    ref = O.gtp(v1[:, 0].astype(np.float64), v2[:, 0].astype(np.float64), L, L, L)
+    assert O.max_rel_err(y[:, 0].cpu().numpy().astype(np.float64), ref) <= TOL
+    e = gtp.gtp_full(plan, t1[:0], t2[:0])
+    assert e.shape[0] == 0
+
+
+def test_direct_convolution_too_large_is_unsupported():
+    plan = gtp.Plan(48, 48, 48, gtp.GTP_CONV_DIRECT)
+    a = torch.zeros((2, 1, O.nsh(48)), device="cuda")
+    with pytest.raises(gtp.GTPError) as ei:
+        gtp.gtp_full(plan, a, a)
+    assert ei.value.status == gtp.GTP_ERR_UNSUPPORTED
+
+
 def test_bf16_inputs():
     L = 6
     rng = np.random.default_rng(11)
