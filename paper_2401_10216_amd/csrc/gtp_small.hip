@@ -420,13 +420,31 @@ constexpr int kTile = 64;  // products per workgroup (one wave)
 // stay in registers, so the budget shrinks with the degree.
 constexpr int small_waves(int L1, int L2, int LO) { return (L1 > 6 || L2 > 6 || LO > 6) ? 2 : 3; }
 
-// Coalesced load of a [kTile, K] slab through LDS into per-lane registers.
+// Coalesced read of a workgroup's kTile x K slab (lane-contiguous), every
+// load issued before the first wait.
+template <int K, typename TIn>
+__device__ __forceinline__ void fetch_slab(const TIn* __restrict__ x, int64_t p0, int cnt, float (&v)[K]) {
+  const int tid = threadIdx.x;
+  const int64_t base = p0 * K;
+  sfor<0, K>([&](auto I) {
+    constexpr int k = decltype(I)::value;
+    const int i = tid + k * kTile;
+    v[k] = (i < cnt * K) ? ld_in(x, base + i) : 0.0f;
+  });
+}
+template <int K>
+__device__ __forceinline__ void slab_to_tile(const float (&v)[K], float* tile) {
+  sfor<0, K>([&](auto I) { tile[threadIdx.x + decltype(I)::value * kTile] = v[decltype(I)::value]; });
+}
+
+// The slab into per-lane rows (row tid = product p0 + tid) through the LDS tile.
 template <int K, typename TIn>
 __device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0, int cnt, float* tile,
                                           float (&r)[K]) {
   const int tid = threadIdx.x;
-  const int64_t base = p0 * K;
-  for (int i = tid; i < kTile * K; i += kTile) tile[i] = (i < cnt * K) ? ld_in(x, base + i) : 0.0f;
+  float v[K];
+  fetch_slab<K>(x, p0, cnt, v);
+  slab_to_tile<K>(v, tile);
   __syncthreads();
   sfor<0, K>([&](auto I) { r[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
   __syncthreads();
@@ -458,18 +476,27 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float xa[K1];
-  load_rows<K1>(x1, p0, cnt, tile, xa);
-  RegX<K1> A{xa};
   float acc[G::KE];
   if constexpr (NU == 0) {
-    // x2 stays in LDS, row-major with an odd row length (conflict-free reads)
-    const int64_t base = p0 * K2;
-    for (int i = tid; i < kTile * K2; i += kTile) tile[i] = (i < cnt * K2) ? ld_in(x2, base + i) : 0.0f;
+    // both slabs requested before the first wait; x1 into registers through
+    // the tile, then x2 stays in LDS, row-major with an odd row length
+    // (conflict-free reads)
+    float v1[K1], v2[K2];
+    fetch_slab<K1>(x1, p0, cnt, v1);
+    fetch_slab<K2>(x2, p0, cnt, v2);
+    slab_to_tile<K1>(v1, tile);
     __syncthreads();
+    sfor<0, K1>([&](auto I) { xa[decltype(I)::value] = tile[tid * K1 + decltype(I)::value]; });
+    __syncthreads();
+    slab_to_tile<K2>(v2, tile);
+    __syncthreads();
+    RegX<K1> A{xa};
     LdsX B{tile, tid * K2};
     gtp_core<L1, L2, LO, NU>(A, B, acc, ST, ntS, WT, ntW);
     __syncthreads();
   } else {
+    load_rows<K1>(x1, p0, cnt, tile, xa);
+    RegX<K1> A{xa};
     gtp_core<L1, L2, LO, NU>(A, A, acc, ST, ntS, WT, ntW);
   }
   store_rows<KO, G::KE>(y, p0, cnt, tile, acc);
