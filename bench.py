@@ -26,12 +26,42 @@ METRIC = "Gaunt TP (b,c)-products/sec at L=6 fp32; % HBM/MFMA roofline on 1 MI35
 PEAK_FP32_TFLOPS = 157.3  # MI355X published fp32 vector / matrix peak
 PEAK_HBM_GBS = 8000.0     # MI355X HBM3E
 
-# Algorithmic flops per (b,c)-product of the paper's Fourier method in real
-# form (sparse change of basis, min(direct, FFT) convolution, projection to
-# Lout), the per-unit figures the roofline is priced with.
-ALG_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
-# Stepwise nu = 3, L = 2, Lout = 3 many-body chain (two products).
-ALG_FLOPS_MANYBODY = 2200
+# Flops per (b,c)-product of the paper's Fourier method counted for an
+# FFT-based real-form convolution (sparse change of basis, min(direct, FFT)
+# convolution, projection to Lout): the reference figures the 50 % targets
+# were set with.
+SURVEY_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
+SURVEY_FLOPS_MANYBODY = 2200
+
+
+def formulation_flops(L1: int, L2: int, Lout: int) -> int:
+    """Flops per product of the formulation the kernels implement (Sec. 3.2
+    with the convolution theorem on a real-form sampling grid): theta nodes
+    t_j = j pi / (U + 1), interior nodes in U / 2 mirror pairs plus two poles;
+    phi samples NP = 4 Q with the 4-fold sample symmetry; an FMA counts 2.
+      theta synthesis, per input t: K_t FMA per mirror pair (even/odd partial
+        sums), 2 adds per m-part and pair (node and mirror), 2 FMA per degree
+        at the poles;
+      phi synthesis, per input and interior node: 2 L_t FMA per sample set;
+      sample products and folds: 28 flops per node and sample set;
+      phi analysis: (2 Le + 1) FMA per node and sample set;
+      mirror combination: 2 adds per moment and pair;
+      theta analysis: (Le + 1)^2 FMA per pair, 2 FMA per degree at the poles."""
+    U = L1 + L2
+    Le = min(Lout, U)
+    NP = (U + Le + 1 + 3) // 4 * 4
+    sets = NP // 4 + 1
+    pairs = U / 2
+    f = 0.0
+    for Lt in (L1, L2):
+        K = (Lt + 1) ** 2
+        f += 2 * K * pairs + 2 * (2 * Lt + 1) * pairs + 4 * (Lt + 1)
+        f += 4 * Lt * sets * U
+    f += 28 * U * sets
+    f += 2 * (2 * Le + 1) * sets * U
+    f += 2 * (2 * Le + 1) * pairs
+    f += 2 * (Le + 1) ** 2 * pairs + 4 * (Le + 1)
+    return int(round(f))
 
 
 def nsh(L):
@@ -106,7 +136,8 @@ def make_workload(args, torch, gtp, inputs):
         desc = {"workload": "edge: B=65536 edges x C=128 channels, L1=L2=Lout=6, x1~N(0,1), "
                             "x2 = h[b,c,l] * Y_lm(r_b), r_b uniform on S^2, h~N(0,1)",
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
-        return step, B * C, desc, ALG_FLOPS[6], 4 * (2 * nsh(L) + nsh(L)), oracle_sample, 2
+        return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
+            oracle_sample, 2
     if w in ("tiny", "sweep", "highdeg"):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1
@@ -151,7 +182,8 @@ def make_workload(args, torch, gtp, inputs):
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "bf16" if w == "highdeg" else "f32"}
         if args.conv != "auto":
             desc["conv"] = args.conv
-        return step, B * C, desc, ALG_FLOPS.get(L), in_bytes * 2 * nsh(L) + 4 * nsh(L), oracle_sample, idx_cfg
+        return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS.get(L)), \
+            in_bytes * 2 * nsh(L) + 4 * nsh(L), oracle_sample, idx_cfg
     if w == "manybody":
         N, C, L, nu, Lout = 1728, 256, 2, 3, 3
         x = inputs.manybody_inputs(N, C, L)
@@ -167,7 +199,8 @@ def make_workload(args, torch, gtp, inputs):
 
         desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
-        return step, N * C, desc, ALG_FLOPS_MANYBODY, 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
+        return step, N * C, desc, (formulation_flops(L, L, Lout) + formulation_flops(Lout, L, Lout),
+                                   SURVEY_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
     if w == "copy":
         # plain device copy of a known size: calibrates the HBM byte counters
         nbytes = 1 << 30
@@ -254,6 +287,7 @@ def main():
 
     roof = None
     if alg_flops:
+        alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
         kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)))
         tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)), ksrc)
@@ -261,6 +295,9 @@ def main():
         roof = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb, "kernel": kname,
                 "kernel_ms": round(kernel_ms, 5), "alg_flops_per_product": alg_flops,
+                "survey_flops_per_product": survey_flops,
+                "frac_at_survey_flops": (round(survey_flops * products / (kernel_ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4)
+                                         if survey_flops else None),
                 "hbm": {"achieved": round(alg_bytes * products / (kernel_ms * 1e-3) / 1e9, 1), "peak": PEAK_HBM_GBS,
                         "unit": "GB/s", "alg_bytes_per_product": alg_bytes}}
         roof["hbm"]["frac"] = round(roof["hbm"]["achieved"] / PEAK_HBM_GBS, 4)

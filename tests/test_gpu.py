@@ -332,6 +332,26 @@ def test_sweep_sampled(L, n):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("L,n", [(32, 300), (64, 40)])
+def test_wave_kernels_bf16(L, n):
+    """Matrix-core kernels with bf16 inputs (fp32 arithmetic): against the
+    oracle fed the same bf16-rounded values, to the fp32 bar."""
+    rng = np.random.default_rng(60 + L)
+    x = rng.standard_normal((2, n, 1, O.nsh(L))).astype(np.float32)
+    bits1, v1 = inputs.round_to_bf16(x[0])
+    bits2, v2 = inputs.round_to_bf16(x[1])
+    _say(f"wave bf16 L={L} n={n}")
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_full(gtp.Plan(L, L, L), t1, t2)
+    torch.cuda.synchronize()
+    idx = np.arange(0, n, max(1, n // 32))
+    ref = O.gtp_grid(v1[idx, 0].astype(np.float64), v2[idx, 0].astype(np.float64), L, L, L)
+    err = O.max_rel_err(y[torch.from_numpy(idx).cuda(), 0].cpu().numpy().astype(np.float64), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
 def test_highdeg_bf16_sampled():
     cfg = inputs.WORKLOADS["highdeg"]
     B, C, L = 4096, cfg["C"], cfg["L1"]  # a slice of the B=32768 workload
