@@ -1,14 +1,15 @@
 """Benchmark of the Gaunt tensor product hot path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg] [--L L]
-                    [--no-cpu-baseline] [--gpus 1]
+                    [--backward] [--no-cpu-baseline] [--gpus 1]
 
 Default: the edge workload (B=65536 edges x C=128 channels, L1=L2=Lout=6,
 x2 = radial weights x real SH of the edge direction), fp32.  One step is one
 gtp_full over the whole batch.  Prints one JSON line with the throughput in
 (b,c)-products/s, the roofline of the kernel (its launch duration measured
 with HIP events on the stream it runs on) and the fp64 oracle timed on the
-host cores on a bounded sample of the same workload.
+host cores on a bounded sample of the same workload.  --backward times
+gtp_full_backward (both input gradients) on the same inputs instead.
 """
 from __future__ import annotations
 
@@ -18,6 +19,8 @@ import json
 import os
 import sys
 import time
+
+import numpy as np
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -108,6 +111,41 @@ def load_traffic(key: str, kernel_source: str):
     return d.get("bytes_per_launch")
 
 
+def pair_step(args, torch, gtp, inputs, plan, t1, t2, y, idx_cfg):
+    """The timed step of a pair workload: gtp_full, or with --backward the
+    gradients of <dy, gtp_full(x1, x2)> in both inputs for a seeded dy.
+    Returns (step, rows(idx) -> the device result rows of products idx,
+    oracle_of(O, idx, a, b) -> fn computing the same rows on the host, the
+    output tensors the step writes)."""
+    L1, L2, Lout = plan.L1, plan.L2, plan.Lout
+    if not args.backward:
+        def step():
+            gtp.gtp_full(plan, t1, t2, y)
+
+        def oracle_of(O, idx, a, b):
+            if max(L1, L2, Lout) <= 8:
+                return lambda: O.gtp(a, b, L1, L2, Lout)
+            return lambda: O.gtp_grid(a, b, L1, L2, Lout)
+        return step, (lambda idx: y.view(-1, y.shape[-1])[torch.from_numpy(idx).to(y.device)]), oracle_of, (y,)
+    B, C = int(t1.shape[0]), int(t1.shape[1])
+    d = inputs.output_gradient(idx_cfg, (B, C, nsh(Lout)))
+    dy = torch.from_numpy(d).to(y.device)
+    dx1 = torch.empty((B, C, nsh(L1)), dtype=torch.float32, device=y.device)
+    dx2 = torch.empty((B, C, nsh(L2)), dtype=torch.float32, device=y.device)
+
+    def step():
+        gtp.gtp_full_backward(plan, t1, t2, dy, dx1=dx1, dx2=dx2)
+
+    def result(idx):
+        ti = torch.from_numpy(idx).to(y.device)
+        return torch.cat([dx1.view(B * C, -1)[ti], dx2.view(B * C, -1)[ti]], dim=1)
+
+    def oracle_of(O, idx, a, b):
+        dd = d.reshape(B * C, -1)[idx].astype("float64")
+        return lambda: np.concatenate(O.gtp_vjp(a, b, dd, L1, L2, Lout), axis=1)
+    return step, result, oracle_of, (dx1, dx2)
+
+
 def make_workload(args, torch, gtp, inputs):
     """Returns (step callable, products per step, description dict, alg flops, alg bytes, oracle sample fn)."""
     dev = torch.device("cuda:0")
@@ -122,22 +160,22 @@ def make_workload(args, torch, gtp, inputs):
         del th
         plan = gtp.Plan(L, L, L)
         y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
-
-        def step():
-            gtp.gtp_full(plan, t1, t2, y)
+        step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, 2)
 
         def oracle_sample(O, idx):
             deg = inputs.degree_of_index(L)
             bi, ci = idx // C, idx % C
             a = x1[bi, ci].astype("float64")
             bref = h[bi, ci][:, deg] * O.real_sh_xyz(L, r[bi])
-            return (lambda: O.gtp(a, bref, L, L, L)), y.view(B * C, -1)
+            return oracle_of(O, idx, a, bref), result
 
         desc = {"workload": "edge: B=65536 edges x C=128 channels, L1=L2=Lout=6, x1~N(0,1), "
                             "x2 = h[b,c,l] * Y_lm(r_b), r_b uniform on S^2, h~N(0,1)",
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
         return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2
+    if args.backward and w not in ("edge", "tiny", "sweep", "highdeg"):
+        raise SystemExit("--backward applies to the pair workloads (edge, tiny, sweep, highdeg)")
     if w in ("tiny", "sweep", "highdeg"):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1
@@ -168,15 +206,12 @@ def make_workload(args, torch, gtp, inputs):
             x1 = x1.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
             x2 = x2.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
         y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
-
-        def step():
-            gtp.gtp_full(plan, t1, t2, y)
+        step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, idx_cfg)
 
         def oracle_sample(O, idx):
             a = x1.reshape(B * C, -1)[idx].astype("float64")
             b = x2.reshape(B * C, -1)[idx].astype("float64")
-            fn = (lambda: O.gtp(a, b, L, L, L)) if L <= 8 else (lambda: O.gtp_grid(a, b, L, L, L))
-            return fn, y.view(B * C, -1)
+            return oracle_of(O, idx, a, b), result
 
         desc = {"workload": f"{w}: B={B} x C={C}, L1=L2=Lout={L}, iid N(0,1)" + (" rounded to bf16" if w == "highdeg" else ""),
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "bf16" if w == "highdeg" else "f32"}
@@ -195,7 +230,8 @@ def make_workload(args, torch, gtp, inputs):
 
         def oracle_sample(O, idx):
             a = x.reshape(N * C, -1)[idx].astype("float64")
-            return (lambda: O.selfproduct(a, L, nu, Lout, "stepwise")), y.view(N * C, -1)
+            return (lambda: O.selfproduct(a, L, nu, Lout, "stepwise")), \
+                (lambda ix: y.view(N * C, -1)[torch.from_numpy(ix).to(y.device)])
 
         desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
@@ -225,15 +261,17 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     n = min(1024, total)
     while True:
         idx = inputs.sample_indices(idx_cfg, total, n)
-        fn, ydev = oracle_sample(O, idx)
+        fn, rows = oracle_sample(O, idx)
         t0 = time.perf_counter()
         ref = fn()
         dt = time.perf_counter() - t0
         if dt >= 0.6 * budget_s or n >= total:
             break
         n = int(min(total, max(2 * n, n * budget_s / max(dt, 1e-3))))
-    import torch
-    got = ydev[torch.from_numpy(idx).to(ydev.device)].cpu().numpy()
+    # rows(idx) gathers the device results of exactly these products (each
+    # index < total, checked on the host first)
+    assert idx.size and 0 <= idx.min() and idx.max() < total
+    got = rows(idx).cpu().numpy()
     err = O.max_rel_err(got, ref)
     return {"value": n / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{n} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
@@ -252,6 +290,9 @@ def main():
                     help="step-2 algorithm for the convolution crossover: auto (the shipped kernels), direct "
                          "(fused direct real-form convolution), generic (workgroup-per-product convolution "
                          "theorem, the direct kernel's structural twin)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time the backward pass (gtp_full_backward: both input gradients for a seeded dy) "
+                         "of a pair workload instead of gtp_full")
     ap.add_argument("--products", type=int, default=0,
                     help="use only the first N products of a pair workload (crossover runs of slow variants)")
     args = ap.parse_args()
@@ -282,7 +323,14 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    kernel_ms = ev0.elapsed_time(ev1) / args.steps  # average launch duration on the launch stream
+    # average launch duration on the launch stream (a backward step is two
+    # launches of the same kernel, one per input gradient)
+    launches = 2 if args.backward else 1
+    if args.backward and alg_flops:
+        # per launch: dy (fp32) and one input in, one gradient out (equal degrees)
+        K = nsh(desc["L1"])
+        alg_bytes = (4 + (2 if desc.get("in_dtype") == "bf16" else 4) + 4) * K
+    kernel_ms = ev0.elapsed_time(ev1) / args.steps / launches
     value = products * args.steps / wall
 
     roof = None
@@ -290,7 +338,7 @@ def main():
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
         kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)))
-        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)), ksrc)
+        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + ("_backward" if args.backward else ""), ksrc)
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         roof = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb, "kernel": kname,
@@ -311,7 +359,12 @@ def main():
         from oracle import gtp_oracle as O
         cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
 
-    line = {"metric": METRIC, "value": value, "unit": "products/s", "n_gpus": 1, "steps": args.steps,
+    metric = METRIC
+    if args.backward:
+        metric = "Gaunt TP backward (dx1 and dx2) (b,c)-products/sec; % MFMA/ALU roofline per launch on 1 MI355X"
+        desc["workload"] = "backward of " + desc["workload"] + "; dy ~ N(0,1)"
+        desc["launches_per_step"] = 2
+    line = {"metric": metric, "value": value, "unit": "products/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": desc,
             "roofline": roof, "cpu_baseline": cpu}

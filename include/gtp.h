@@ -95,6 +95,25 @@ gtp_status gtp_plan_destroy(gtp_plan p);
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 
+/* Backward pass (vector-Jacobian product) of gtp_full: given the gradient dy
+ * of a scalar loss with respect to y = gtp_full(x1, x2), the gradients
+ *   dx1[b,c,i] = sum_{j,k} G_{i j k} x2[b,c,j] dy[b,c,k]   (i over degrees <= L1),
+ *   dx2[b,c,j] = sum_{i,k} G_{i j k} x1[b,c,i] dy[b,c,k]   (j over degrees <= L2),
+ * with G the real Gaunt coefficients of Sec. 3.1 (eq. tp-eq-mul).  G is the
+ * integral of a product of three real SH, symmetric in its three (l, m)
+ * pairs, so dx1 is the Gaunt tensor product of dy and x2 truncated to degree
+ * L1 (and dx2 that of dy and x1 truncated to L2); both are computed that way
+ * (Sec. 3.2), with the plan's GTP_CONV_* choice.
+ * x1, x2: the forward inputs (in_dtype); dy: [B, C, (Lout+1)^2] fp32;
+ * dx1: [B, C, (L1+1)^2] fp32 or NULL (not computed); dx2: [B, C, (L2+1)^2]
+ * fp32 or NULL.  x1 may be NULL when dx2 is, x2 when dx1 is.  The gradients
+ * are written, not accumulated.  Neither may overlap an input or the other.
+ * B*C == 0, or dx1 == dx2 == NULL, is a successful no-op.  Tables for
+ * (Lout, L2, L1) and (Lout, L1, L2) are built on first use and cached per
+ * device (that first call is synchronous); equal degrees reuse the plan's. */
+gtp_status gtp_full_backward(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype, const float *dy,
+                             int64_t B, int64_t C, float *dx1, float *dx2, void *stream);
+
 /* Step 1 (Sec. 3.2, eq. sh-fs): SH coefficients -> 2D Fourier coefficients
  * x*_{u,v}, |u|,|v| <= L, for L = L1 (which = 1) or L2 (which = 2).
  * The function is extended to theta in [-pi, pi) by F(-t, p) = F(t, p + pi).

@@ -19,6 +19,8 @@ Everything is numpy float64 and written to be checked against the paper by eye:
 * the Gaunt tensor product itself (Sec. 3.1, eq. ``tp-eq-mul``) as a dense
   contraction of the Gaunt tensor ("mode A"), and as the pointwise product of
   the two spherical functions on an exact quadrature grid ("mode B");
+* its gradients (the vector-Jacobian product of the bilinear map), from the
+  same Gaunt tensor or the same quadrature;
 * the three stages of Sec. 3.2 individually: SH -> 2D Fourier (eq. ``sh-fs``),
   the 2D convolution (eq. ``2D-conv``) and Fourier -> SH (eq. ``fs-sh``), each
   from its plain definition;
@@ -241,6 +243,53 @@ def gtp_grid(x1, x2, L1: int, L2: int, Lout: int, chunk: int = 4096) -> np.ndarr
         F = (a[s : s + chunk] @ Y1.T) * (b[s : s + chunk] @ Y2.T)
         y[s : s + chunk] = F @ Y3w
     return y.reshape(lead + (nsh(Lout),))
+
+
+def gtp_vjp(x1, x2, dy, L1: int, L2: int, Lout: int, chunk: int = 2048, mode: str = "auto"):
+    """Gradients of s = sum_k dy[k] y[k], y = gtp(x1, x2, L1, L2, Lout).
+
+    y is bilinear in (x1, x2) with coefficients G[i, j, k] (eq. tp-eq-mul), so
+      dx1[n, i] = sum_{j,k} G[i, j, k] x2[n, j] dy[n, k],
+      dx2[n, j] = sum_{i,k} G[i, j, k] x1[n, i] dy[n, k].
+    For max degree <= 8 this contracts the dense Gaunt tensor; above, the same
+    sums are the integrals  int Y_i F2 F_dy dOmega  and  int Y_j F1 F_dy dOmega
+    (G is an integral of three real SH), taken on a quadrature grid exact for
+    degree L1 + L2 + Lout (mode "gaunt" / "grid" forces one).  Returns
+    (dx1, dx2) in float64.
+    """
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    lead = x1.shape[:-1]
+    a = x1.reshape(-1, nsh(L1))
+    b = x2.reshape(-1, nsh(L2))
+    d = dy.reshape(-1, nsh(Lout))
+    assert a.shape[0] == b.shape[0] == d.shape[0]
+    dx1 = np.empty_like(a)
+    dx2 = np.empty_like(b)
+    if mode == "auto":
+        mode = "gaunt" if max(L1, L2, Lout) <= 8 else "grid"
+    if mode == "gaunt":
+        G = _gaunt_cached(L1, L2, Lout)
+        for s in range(0, a.shape[0], chunk):
+            e = slice(s, s + chunk)
+            Gd = np.einsum("ijk,nk->nij", G, d[e])
+            dx1[e] = np.einsum("nij,nj->ni", Gd, b[e])
+            dx2[e] = np.einsum("nij,ni->nj", Gd, a[e])
+    elif mode == "grid":
+        th, ph, w = sphere_quadrature(L1 + L2 + Lout)
+        Y = real_sh(max(L1, L2, Lout), th, ph)
+        Y1 = Y[:, : nsh(L1)]
+        Y2 = Y[:, : nsh(L2)]
+        Y3 = Y[:, : nsh(Lout)]
+        for s in range(0, a.shape[0], chunk):
+            e = slice(s, s + chunk)
+            Fd = (d[e] @ Y3.T) * w
+            dx1[e] = ((b[e] @ Y2.T) * Fd) @ Y1
+            dx2[e] = ((a[e] @ Y1.T) * Fd) @ Y2
+    else:
+        raise ValueError(mode)
+    return dx1.reshape(lead + (nsh(L1),)), dx2.reshape(lead + (nsh(L2),))
 
 
 # ---------------------------------------------------------------------------

@@ -178,23 +178,24 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
   return GTP_OK;
 }
 
-// Internal plan cache for the many-body entry point, keyed by device and degrees.
+// Internal plan cache of the many-body and backward entry points, keyed by
+// device, degrees and plan flags.
 std::mutex g_cache_mu;
-std::map<std::tuple<int, int, int, int>, gtp_plan> g_cache;
+std::map<std::tuple<int, int, int, int, unsigned>, gtp_plan> g_cache;
 
-gtp_status cached_plan(int L1, int L2, int Lout, gtp_plan* out) {
+gtp_status cached_plan(int L1, int L2, int Lout, unsigned flags, gtp_plan* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
   std::lock_guard<std::mutex> lk(g_cache_mu);
-  auto key = std::make_tuple(dev, L1, L2, Lout);
+  auto key = std::make_tuple(dev, L1, L2, Lout, flags);
   auto it = g_cache.find(key);
   if (it != g_cache.end()) {
     *out = it->second;
     return GTP_OK;
   }
   gtp_plan p = nullptr;
-  gtp_status s = make_plan(&p, L1, L2, Lout, 0u, kMaxL);
+  gtp_status s = make_plan(&p, L1, L2, Lout, flags, kMaxL);
   if (s != GTP_OK) return s;
   g_cache[key] = p;
   *out = p;
@@ -211,6 +212,29 @@ gtp_status plan_check(gtp_plan p) {
 gtp_status device_ready(gtp_plan p) {
   if (p->host_only) return fail(GTP_ERR_INVALID_ARG, "plan was created with GTP_PLAN_HOST_ONLY");
   return GTP_OK;
+}
+
+// One fused product y = P_Lout(x1 * x2) with the plan's tables: the direct
+// convolution when the plan asks for it, else the thread-per-product kernel,
+// the matrix-core wave kernel or the workgroup kernel, the first that has an
+// instantiation for the degrees and input types.
+gtp_status run_product(gtp_plan p, const void* x1, int it1, const void* x2, int it2, int64_t n, float* y,
+                       hipStream_t st, const char* what) {
+  hipError_t e = hipSuccess;
+  if (p->conv == GTP_CONV_DIRECT) {
+    e = gtp::launch_full_direct(p->dev, x1, it1, x2, it2, n, y, st);
+    if (e == hipErrorNotSupported) return fail(GTP_ERR_UNSUPPORTED, "direct convolution path not built");
+    return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+  }
+  bool done = false;
+  if (!p->force_generic) {
+    e = gtp::launch_full_small(p->dev, x1, it1, x2, it2, n, y, 0, st, &done);
+    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+    e = gtp::launch_full_wave(p->dev, x1, it1, x2, it2, n, y, st, &done);
+    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+  }
+  e = gtp::launch_full_generic(p->dev, x1, it1, x2, it2, n, y, 0, st);
+  return e == hipSuccess ? GTP_OK : hip_fail(e, what);
 }
 
 }  // namespace
@@ -246,23 +270,54 @@ gtp_status gtp_full(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dty
   if ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % es || reinterpret_cast<uintptr_t>(y) % 4)
     return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   if ((s = device_ready(p)) != GTP_OK) return s;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
-  hipError_t e = hipSuccess;
-  if (p->conv == GTP_CONV_DIRECT) {
-    e = gtp::launch_full_direct(p->dev, x1, x2, it, n, y, st);
-    if (e == hipErrorNotSupported) return fail(GTP_ERR_UNSUPPORTED, "direct convolution path not built");
-    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+  return run_product(p, x1, it, x2, it, n, y, static_cast<hipStream_t>(stream), "gtp_full launch");
+}
+
+gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* dy,
+                             int64_t B, int64_t C, float* dx1, float* dx2, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  int64_t n = 0, e1 = 0, e2 = 0, eo = 0;
+  if (!mul_ok(B, C, &n)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit in int64");
+  if (!mul_ok(n, gtp::nsh(p->L1), &e1) || !mul_ok(n, gtp::nsh(p->L2), &e2) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      e1 > INT64_MAX / 4 || e2 > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  if (n == 0 || (!dx1 && !dx2)) return GTP_OK;
+  if (!dy || (dx1 && !x2) || (dx2 && !x1)) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype);
+  const size_t b1 = size_t(e1) * 4, b2 = size_t(e2) * 4;
+  // every output against every input it could alias, and the outputs against each other
+  auto hits_inputs = [&](const void* out, size_t nb) {
+    return (x1 && ranges_overlap(out, nb, x1, size_t(e1) * es)) || (x2 && ranges_overlap(out, nb, x2, size_t(e2) * es)) ||
+           ranges_overlap(out, nb, dy, size_t(eo) * 4);
+  };
+  if ((dx1 && hits_inputs(dx1, b1)) || (dx2 && hits_inputs(dx2, b2)) || (dx1 && dx2 && ranges_overlap(dx1, b1, dx2, b2)))
+    return fail(GTP_ERR_INVALID_ARG, "a gradient overlaps an input or the other gradient");
+  if ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % es ||
+      (reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(dx1) | reinterpret_cast<uintptr_t>(dx2)) % 4)
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  // dx1 = P_L1(GTP(dy, x2)) and dx2 = P_L2(GTP(dy, x1)): the real Gaunt
+  // coefficient is symmetric in its three (l, m) pairs, so the gradient of
+  // <dy, GTP(x1, x2)> in x1 is the product of the functions of dy and x2
+  // projected to degree L1 (and likewise for x2).
+  const unsigned conv = p->conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : 0u;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  if (dx1) {
+    gtp_plan q = p;  // the plan's own tables when (Lout, L2, L1) = (L1, L2, Lout)
+    if (p->Lout != p->L1 && (s = cached_plan(p->Lout, p->L2, p->L1, conv, &q)) != GTP_OK) return s;
+    if ((s = run_product(q, dy, gtp::IN_F32, x2, it, n, dx1, st, "gtp_full_backward launch")) != GTP_OK) return s;
   }
-  bool done = false;
-  if (!p->force_generic) {
-    e = gtp::launch_full_small(p->dev, x1, x2, it, n, y, 0, st, &done);
-    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
-    e = gtp::launch_full_wave(p->dev, x1, x2, it, n, y, st, &done);
-    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+  if (dx2) {
+    gtp_plan q = p;
+    if ((p->Lout != p->L1 || p->L1 != p->L2) && (s = cached_plan(p->Lout, p->L1, p->L2, conv, &q)) != GTP_OK)
+      return s;
+    if ((s = run_product(q, dy, gtp::IN_F32, x1, it, n, dx2, st, "gtp_full_backward launch")) != GTP_OK) return s;
   }
-  e = gtp::launch_full_generic(p->dev, x1, it, x2, it, n, y, 0, st);
-  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full launch");
+  return GTP_OK;
 }
 
 gtp_status gtp_sh2fourier(gtp_plan p, int which, const void* x, gtp_dtype in_dtype, int64_t n, float* grid,
@@ -344,24 +399,24 @@ gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void* x
   }
   if (mode == GTP_SELF_STEPWISE && nu == 2) {
     gtp_plan p = nullptr;
-    if ((s = cached_plan(L, L, Lout, &p)) != GTP_OK) return s;
+    if ((s = cached_plan(L, L, Lout, 0u, &p)) != GTP_OK) return s;
     bool done = false;
-    e = gtp::launch_full_small(p->dev, x, x, it, n, y, 0, st, &done);
+    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, 0, st, &done);
     if (!done) e = gtp::launch_full_generic(p->dev, x, it, x, it, n, y, 0, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
   }
   if (mode == GTP_SELF_FUSED) {
     gtp_plan p = nullptr;
-    if ((s = cached_plan(L, (nu - 1) * L, Lout, &p)) != GTP_OK) return s;
+    if ((s = cached_plan(L, (nu - 1) * L, Lout, 0u, &p)) != GTP_OK) return s;
     bool done = false;
-    e = gtp::launch_full_small(p->dev, x, x, it, n, y, nu, st, &done);
+    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, nu, st, &done);
     if (!done) e = gtp::launch_full_generic(p->dev, x, it, nullptr, it, n, y, nu, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
   }
   // stepwise, nu >= 3
   gtp_plan p1 = nullptr, p2 = nullptr;
-  if ((s = cached_plan(L, L, Lout, &p1)) != GTP_OK) return s;
-  if ((s = cached_plan(Lout, L, Lout, &p2)) != GTP_OK) return s;
+  if ((s = cached_plan(L, L, Lout, 0u, &p1)) != GTP_OK) return s;
+  if ((s = cached_plan(Lout, L, Lout, 0u, &p2)) != GTP_OK) return s;
   bool done = false;
   e = gtp::launch_self_stepwise_small(p1->dev, p2->dev, nu, x, it, n, y, st, &done);
   if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");

@@ -36,17 +36,19 @@ enum InType : int { IN_F32 = 0, IN_BF16 = 1 };
 
 // Launchers (return the launch's hipError_t).  n = number of products.
 // Thread-per-product fused kernel for the degree triples it is instantiated
-// for; *supported = false when (L1, L2, Lout, nu) has no instantiation.
-hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+// for; *supported = false when (L1, L2, Lout, nu) or the pair of input types
+// (it1, it2) has no instantiation.
+hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                              float* y, int nu, hipStream_t s, bool* supported);
 // Stepwise many-body chain in one kernel (thread per product) for the
 // instantiated (L, nu, Lout); t1 = tables of (L, L, Lout), t2 = (Lout, L, Lout).
 hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x,
                                       int in_type, int64_t n, float* y, hipStream_t s, bool* supported);
 // Wave-per-product fused kernel with the phi stage on the matrix cores, for
-// L1 = L2 = Lout = L in {16, 32}; *supported = false otherwise.
-hipError_t launch_full_wave(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                            hipStream_t s, bool* supported);
+// L1 = L2 = Lout = L in {16, 32, 64}; *supported = false otherwise, or for a
+// bf16 x1 with an fp32 x2.
+hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                            float* y, hipStream_t s, bool* supported);
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,
@@ -55,7 +57,7 @@ hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, co
 hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
 // Direct 2D convolution of the real-form Fourier grids (the paper's eq.
 // 2D-conv without the convolution theorem), workgroup per product.
-hipError_t launch_full_direct(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+hipError_t launch_full_direct(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                               float* y, hipStream_t s);
 // Unfused stages with the paper's complex grids.
 hipError_t launch_sh2fourier(const DevTables& t, int L, const void* x, int in_type, int64_t n, float* grid,

@@ -514,18 +514,24 @@ hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* 
   return hipGetLastError();
 }
 
-hipError_t launch_full_direct(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n,
+hipError_t launch_full_direct(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                               float* y, hipStream_t s) {
   const size_t lds = size_t(direct_layout(t).total) * sizeof(float);
   if (lds > 64 * 1024) return hipErrorNotSupported;  // the default LDS limit of one workgroup
   if (n <= 0) return hipSuccess;
   const dim3 grid(grid_for(n, 1)), block(kBlock);
-  if (in_type == IN_BF16)
-    hipLaunchKernelGGL((k_full_direct<uint16_t, uint16_t>), grid, block, lds, s, t,
-                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n);
+  const float* f1 = static_cast<const float*>(x1);
+  const float* f2 = static_cast<const float*>(x2);
+  const uint16_t* h1 = static_cast<const uint16_t*>(x1);
+  const uint16_t* h2 = static_cast<const uint16_t*>(x2);
+  if (it1 == IN_BF16 && it2 == IN_BF16)
+    hipLaunchKernelGGL((k_full_direct<uint16_t, uint16_t>), grid, block, lds, s, t, h1, h2, y, n);
+  else if (it1 == IN_BF16)
+    hipLaunchKernelGGL((k_full_direct<uint16_t, float>), grid, block, lds, s, t, h1, f2, y, n);
+  else if (it2 == IN_BF16)
+    hipLaunchKernelGGL((k_full_direct<float, uint16_t>), grid, block, lds, s, t, f1, h2, y, n);
   else
-    hipLaunchKernelGGL((k_full_direct<float, float>), grid, block, lds, s, t, static_cast<const float*>(x1),
-                       static_cast<const float*>(x2), y, n);
+    hipLaunchKernelGGL((k_full_direct<float, float>), grid, block, lds, s, t, f1, f2, y, n);
   return hipGetLastError();
 }
 

@@ -463,8 +463,8 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
   for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
 }
 
-template <int L1, int L2, int LO, int NU, typename TIn>
-__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const TIn* __restrict__ x1, const TIn* __restrict__ x2,
+template <int L1, int L2, int LO, int NU, typename T1, typename T2>
+__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const T1* __restrict__ x1, const T2* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
                                                       const float* __restrict__ ST, int ntS,
                                                       const float* __restrict__ WT, int ntW) {
@@ -538,18 +538,27 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   store_rows<KO, KO>(y, p0, cnt, tile, b);
 }
 
-template <int L1, int L2, int LO, int NU>
-hipError_t launch_one(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                      hipStream_t s) {
+template <int L1, int L2, int LO, int NU, typename T1, typename T2>
+hipError_t launch_typed(const DevTables& t, const void* x1, const void* x2, int64_t n, float* y, hipStream_t s) {
   const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
-  if (in_type == IN_BF16)
-    hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, uint16_t>), grid, block, 0, s,
-                       static_cast<const uint16_t*>(x1), static_cast<const uint16_t*>(x2), y, n, t.ST, t.ntS, t.WT,
-                       t.ntW);
-  else
-    hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, float>), grid, block, 0, s, static_cast<const float*>(x1),
-                       static_cast<const float*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW);
+  hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, T1, T2>), grid, block, 0, s, static_cast<const T1*>(x1),
+                     static_cast<const T2*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW);
   return hipGetLastError();
+}
+
+// Input types: both fp32, both bf16, or (equal degrees only) fp32 x1 with
+// bf16 x2, the pairing of a backward pass (fp32 output gradient times a bf16
+// input).  Other pairings are not instantiated (*supported = false).
+template <int L1, int L2, int LO, int NU>
+hipError_t launch_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n, float* y,
+                      hipStream_t s, bool* supported) {
+  if (it1 == IN_BF16 && it2 == IN_BF16) return launch_typed<L1, L2, LO, NU, uint16_t, uint16_t>(t, x1, x2, n, y, s);
+  if (it1 == IN_F32 && it2 == IN_F32) return launch_typed<L1, L2, LO, NU, float, float>(t, x1, x2, n, y, s);
+  if constexpr (L1 == L2 && L2 == LO && NU == 0) {
+    if (it1 == IN_F32 && it2 == IN_BF16) return launch_typed<L1, L2, LO, NU, float, uint16_t>(t, x1, x2, n, y, s);
+  }
+  *supported = false;
+  return hipSuccess;
 }
 
 template <int L, int LO>
@@ -575,18 +584,19 @@ hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const 
 #define GTP_SMALL_POWERS(X) X(2, 2, 3) X(2, 3, 3) X(2, 4, 3) X(1, 3, 2) X(3, 3, 3)
 #define GTP_SMALL_CHAINS(X) X(2, 3) X(1, 2) X(3, 3) X(2, 2)
 
-hipError_t launch_full_small(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                             int nu, hipStream_t s, bool* supported) {
+hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                             float* y, int nu, hipStream_t s, bool* supported) {
   *supported = true;
   if (nu == 0) {
 #define GTP_CASE(a, b, c) \
-  if (t.L1 == a && t.L2 == b && t.Lout == c) return launch_one<a, b, c, 0>(t, x1, x2, in_type, n, y, s);
+  if (t.L1 == a && t.L2 == b && t.Lout == c) return launch_one<a, b, c, 0>(t, x1, it1, x2, it2, n, y, s, supported);
     GTP_SMALL_PAIRS(GTP_CASE)
 #undef GTP_CASE
   } else {
     // power plans are built as (L, (nu - 1) L, Lout)
 #define GTP_CASE(a, v, c) \
-  if (nu == v && t.L1 == a && t.L2 == (v - 1) * a && t.Lout == c) return launch_one<a, 0, c, v>(t, x1, x1, in_type, n, y, s);
+  if (nu == v && t.L1 == a && t.L2 == (v - 1) * a && t.Lout == c) \
+    return launch_one<a, 0, c, v>(t, x1, it1, x1, it1, n, y, s, supported);
     GTP_SMALL_POWERS(GTP_CASE)
 #undef GTP_CASE
   }

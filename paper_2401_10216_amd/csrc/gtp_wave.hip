@@ -358,8 +358,8 @@ struct WaveCtx {
 
 // x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
 // threads of the workgroup: every load is issued before the first wait
-template <int L, typename TIn>
-__device__ __forceinline__ void stage_x(float* xs, const TIn* x1, const TIn* x2, int64_t P, int tid,
+template <int L, typename T1, typename T2>
+__device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, int64_t P, int tid,
                                         const int* xmap) {
   using G = WGeo<L>;
   constexpr int K = G::K, NTH = G::NTH, NXK = G::NXK, NXKP = G::NXKP;
@@ -406,9 +406,9 @@ __device__ __forceinline__ void row_lm(int q, int& l, int& m) {
 
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.
-template <int L, typename TIn>
+template <int L, typename T1, typename T2>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_full_wave(
-    const TIn* __restrict__ x1, const TIn* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
   using G = WGeo<L>;
   static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
   constexpr int NJ = G::NJ, NP = G::NP;
@@ -514,9 +514,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
 // second stay in registers until every wave is done with the x image, then
 // go into its place.  The 256 threads then do the theta analysis, each over
 // all 64 mirror pairs of its output rows.
-template <int L, typename TIn>
+template <int L, typename T1, typename T2>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_full_wave4(
-    const TIn* __restrict__ x1, const TIn* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
   using G = WGeo<L>;
   static_assert(G::NW == 4 && G::PASSES == 8, "four waves, two passes each");
   constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
@@ -590,46 +590,46 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   }
 }
 
-template <int L>
-hipError_t launch_wave_one(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                           hipStream_t s) {
+template <int L, typename T1, typename T2>
+hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t, hipStream_t s) {
   using G = WGeo<L>;
   // at most 2^30 workgroups per launch
   for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
     const int64_t nn = n - p0 < (int64_t(1) << 30) ? n - p0 : (int64_t(1) << 30);
-    const size_t es = in_type == IN_BF16 ? 2 : 4;
-    const char* a = static_cast<const char*>(x1) + size_t(p0) * G::K * es;
-    const char* b = static_cast<const char*>(x2) + size_t(p0) * G::K * es;
+    const T1* a = static_cast<const T1*>(x1) + size_t(p0) * G::K;
+    const T2* b = static_cast<const T2*>(x2) + size_t(p0) * G::K;
     float* yy = y + size_t(p0) * G::K;
-    if constexpr (G::NW == 1) {
-      if (in_type == IN_BF16)
-        hipLaunchKernelGGL((k_full_wave<L, uint16_t>), dim3(unsigned(nn)), dim3(64), 0, s,
-                           reinterpret_cast<const uint16_t*>(a), reinterpret_cast<const uint16_t*>(b), yy, nn, t);
-      else
-        hipLaunchKernelGGL((k_full_wave<L, float>), dim3(unsigned(nn)), dim3(64), 0, s,
-                           reinterpret_cast<const float*>(a), reinterpret_cast<const float*>(b), yy, nn, t);
-    } else {
-      if (in_type == IN_BF16)
-        hipLaunchKernelGGL((k_full_wave4<L, uint16_t>), dim3(unsigned(nn)), dim3(G::NTH), 0, s,
-                           reinterpret_cast<const uint16_t*>(a), reinterpret_cast<const uint16_t*>(b), yy, nn, t);
-      else
-        hipLaunchKernelGGL((k_full_wave4<L, float>), dim3(unsigned(nn)), dim3(G::NTH), 0, s,
-                           reinterpret_cast<const float*>(a), reinterpret_cast<const float*>(b), yy, nn, t);
-    }
+    if constexpr (G::NW == 1)
+      hipLaunchKernelGGL((k_full_wave<L, T1, T2>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t);
+    else
+      hipLaunchKernelGGL((k_full_wave4<L, T1, T2>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
+// Input types: both fp32, both bf16, or fp32 x1 with bf16 x2 (a backward
+// pass: fp32 output gradient times a bf16 input); *supported = false for
+// bf16 x1 with fp32 x2.
+template <int L>
+hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                           float* y, hipStream_t s, bool* supported) {
+  if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float>(x1, x2, n, y, t, s);
+  if (it1 == IN_BF16 && it2 == IN_BF16) return launch_wave_typed<L, uint16_t, uint16_t>(x1, x2, n, y, t, s);
+  if (it1 == IN_F32 && it2 == IN_BF16) return launch_wave_typed<L, float, uint16_t>(x1, x2, n, y, t, s);
+  *supported = false;
+  return hipSuccess;
+}
+
 }  // namespace
 
-hipError_t launch_full_wave(const DevTables& t, const void* x1, const void* x2, int in_type, int64_t n, float* y,
-                            hipStream_t s, bool* supported) {
+hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                            float* y, hipStream_t s, bool* supported) {
   *supported = true;
-  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, x2, in_type, n, y, s);
-  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, x2, in_type, n, y, s);
-  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, x2, in_type, n, y, s);
+  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, it1, x2, it2, n, y, s, supported);
+  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, it1, x2, it2, n, y, s, supported);
+  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, it1, x2, it2, n, y, s, supported);
   *supported = false;
   return hipSuccess;
 }

@@ -44,6 +44,7 @@ _SIGS = {
     "gtp_plan_create": (_I, [ctypes.POINTER(_P), _I, _I, _I, _U]),
     "gtp_plan_destroy": (_I, [_P]),
     "gtp_full": (_I, [_P, _P, _P, _I, _I64, _I64, _P, _P]),
+    "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
     "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
     "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
     "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
@@ -159,6 +160,30 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
     _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
                           _stream(stream)))
     return y
+
+
+def gtp_full_backward(plan: Plan, x1, x2, dy, need_dx1: bool = True, need_dx2: bool = True, dx1=None, dx2=None,
+                      stream=None):
+    """(dx1, dx2): gradients of <dy, gtp_full(x1, x2)> in x1 and x2 (fp32; None when not requested)."""
+    import torch
+    if x1.dtype != x2.dtype:
+        raise TypeError("x1 and x2 must have the same dtype")
+    if x1.dim() != 3 or x2.dim() != 3 or dy.dim() != 3 or x1.shape[:2] != x2.shape[:2] or dy.shape[:2] != x1.shape[:2]:
+        raise ValueError("x1, x2, dy must be [B, C, K] with equal B, C")
+    if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2) or dy.shape[2] != nsh(plan.Lout):
+        raise ValueError("coefficient dimension does not match the plan")
+    if dy.dtype != torch.float32:
+        raise TypeError("dy must be float32")
+    B, C = int(x1.shape[0]), int(x1.shape[1])
+    if need_dx1 and dx1 is None:
+        dx1 = torch.empty((B, C, nsh(plan.L1)), dtype=torch.float32, device=x1.device)
+    if need_dx2 and dx2 is None:
+        dx2 = torch.empty((B, C, nsh(plan.L2)), dtype=torch.float32, device=x1.device)
+    p1 = _dev(dx1, "dx1") if need_dx1 else ctypes.c_void_p(None)
+    p2 = _dev(dx2, "dx2") if need_dx2 else ctypes.c_void_p(None)
+    _check(lib().gtp_full_backward(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), _dev(dy, "dy"), B, C,
+                                   p1, p2, _stream(stream)))
+    return (dx1 if need_dx1 else None), (dx2 if need_dx2 else None)
 
 
 def gtp_sh2fourier(plan: Plan, which: int, x, grid=None, stream=None):

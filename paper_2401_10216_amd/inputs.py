@@ -114,6 +114,11 @@ def highdeg_inputs(B: int = 32768, C: int = 64, L: int = 16, index: int = 5):
     return b1, b2, v1, v2
 
 
+def output_gradient(index: int, shape) -> np.ndarray:
+    """Seeded N(0,1) output gradient dy of a workload (for its backward pass)."""
+    return normal(rng_for(index, 200), shape)
+
+
 def sample_indices(index: int, total: int, count: int) -> np.ndarray:
     """Sorted distinct product indices for subsampled checks."""
     rng = rng_for(index, 100)

@@ -169,6 +169,30 @@ def test_full_validation(L):
     assert b"HOST_ONLY" in L.gtp_last_error()
 
 
+def test_backward_validation(L):
+    p = host_plan(2, 3, 4)
+    H = p.handle
+    x1, x2, dy, d1, d2 = fake(0x100000), fake(0x200000), fake(0x300000), fake(0x400000), fake(0x500000)
+    S = ctypes.c_void_p(0)
+    INV, OK = gtp.GTP_ERR_INVALID_ARG, gtp.GTP_OK
+    f = L.gtp_full_backward
+    assert f(None, x1, x2, 0, dy, 4, 4, d1, d2, S) == INV
+    assert f(H, x1, x2, 3, dy, 4, 4, d1, d2, S) == INV  # bad dtype
+    assert f(H, x1, x2, 0, dy, -1, 4, d1, d2, S) == INV
+    assert f(H, x1, x2, 0, dy, 1 << 30, 1 << 30, d1, d2, S) == INV  # size overflow
+    assert f(H, x1, x2, 0, None, 4, 4, d1, d2, S) == INV  # dy NULL
+    assert f(H, x1, None, 0, dy, 4, 4, d1, None, S) == INV  # dx1 needs x2
+    assert f(H, None, x2, 0, dy, 4, 4, None, d2, S) == INV  # dx2 needs x1
+    assert f(H, x1, x2, 0, dy, 4, 4, fake(0x300000 + 8), d2, S) == INV  # dx1 overlaps dy
+    assert f(H, x1, x2, 0, dy, 4, 4, d1, fake(0x200000 + 4), S) == INV  # dx2 overlaps x2
+    assert f(H, x1, x2, 0, dy, 4, 4, d1, fake(0x400000 + 4 * 16 * 9 - 4), S) == INV  # dx1 overlaps dx2
+    assert f(H, x1, x2, 0, dy, 4, 4, fake(0x400002), d2, S) == INV  # misaligned
+    assert f(H, x1, x2, 0, dy, 0, 4, d1, d2, S) == OK  # empty batch
+    assert f(H, x1, x2, 0, dy, 4, 4, None, None, S) == OK  # nothing requested
+    assert f(H, None, x2, 0, dy, 4, 4, d1, None, S) == INV  # valid, but the plan is host-only
+    assert b"HOST_ONLY" in L.gtp_last_error()
+
+
 def test_stage_validation(L):
     p = host_plan(2, 3, 2)
     H = p.handle

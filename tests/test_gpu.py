@@ -369,3 +369,113 @@ def test_highdeg_bf16_sampled():
     err = O.max_rel_err(yf, ref)
     _say(f"  err={err:.3e}")
     assert err <= 2e-2
+
+
+# ------------------------------------------------------------------ backward pass (vector-Jacobian product)
+
+def oracle_vjp(a, b, d, L1, L2, Lout):
+    return O.gtp_vjp(a.astype(np.float64), b.astype(np.float64), d.astype(np.float64), L1, L2, Lout)
+
+
+BWD = [(2, 2, 2), (4, 4, 4), (6, 6, 6), (8, 8, 8), (2, 2, 3), (3, 5, 4), (6, 6, 2), (1, 0, 1), (16, 16, 16)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout", BWD)
+def test_backward_ragged(L1, L2, Lout):
+    n = 64 * 9 + 21 if max(L1, L2, Lout) <= 8 else 301
+    rng = np.random.default_rng(80 + L1 + 11 * L2 + 121 * Lout)
+    a = rng.standard_normal((n, 1, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L2))).astype(np.float32)
+    d = rng.standard_normal((n, 1, O.nsh(Lout))).astype(np.float32)
+    _say(f"backward L1={L1} L2={L2} Lout={Lout} n={n}")
+    dx1, dx2 = gtp.gtp_full_backward(gtp.Plan(L1, L2, Lout), dev(a), dev(b), dev(d))
+    torch.cuda.synchronize()
+    r1, r2 = oracle_vjp(a, b, d, L1, L2, Lout)
+    e1 = O.max_rel_err(dx1.cpu().numpy(), r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy(), r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
+@pytest.mark.parametrize("L,n", [(32, 129), (64, 17)])
+def test_backward_matrix_core_sampled(L, n):
+    rng = np.random.default_rng(90 + L)
+    a, b, d = (rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32) for _ in range(3))
+    _say(f"backward wave L={L} n={n}")
+    dx1, dx2 = gtp.gtp_full_backward(gtp.Plan(L, L, L), dev(a), dev(b), dev(d))
+    torch.cuda.synchronize()
+    idx = np.arange(0, n, 8)
+    r1, r2 = oracle_vjp(a[idx], b[idx], d[idx], L, L, L)
+    e1 = O.max_rel_err(dx1.cpu().numpy()[idx], r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy()[idx], r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
+@pytest.mark.parametrize("L1,L2,Lout", [(6, 6, 6), (16, 16, 16), (2, 2, 3)])
+def test_backward_bf16_inputs(L1, L2, Lout):
+    """bf16 forward inputs, fp32 output gradient: mixed-type kernels, against
+    the oracle fed the same bf16-rounded inputs."""
+    n = 300
+    rng = np.random.default_rng(95 + L1 + Lout)
+    bits1, v1 = inputs.round_to_bf16(rng.standard_normal((n, 1, O.nsh(L1))).astype(np.float32))
+    bits2, v2 = inputs.round_to_bf16(rng.standard_normal((n, 1, O.nsh(L2))).astype(np.float32))
+    d = rng.standard_normal((n, 1, O.nsh(Lout))).astype(np.float32)
+    _say(f"backward bf16 L1={L1} L2={L2} Lout={Lout}")
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    dx1, dx2 = gtp.gtp_full_backward(gtp.Plan(L1, L2, Lout), t1, t2, dev(d))
+    torch.cuda.synchronize()
+    r1, r2 = oracle_vjp(v1, v2, d, L1, L2, Lout)
+    e1 = O.max_rel_err(dx1.cpu().numpy(), r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy(), r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
+def test_backward_options_and_paths():
+    """One gradient at a time, the generic and direct plans, and an empty batch."""
+    L = 4
+    n = 200
+    rng = np.random.default_rng(97)
+    a, b, d = (rng.standard_normal((n, 2, O.nsh(L))).astype(np.float32) for _ in range(3))
+    r1, r2 = oracle_vjp(a, b, d, L, L, L)
+    for flags in (0, gtp.GTP_FORCE_GENERIC, gtp.GTP_CONV_DIRECT):
+        _say(f"backward options flags={flags}")
+        plan = gtp.Plan(L, L, L, flags)
+        dx1, none = gtp.gtp_full_backward(plan, dev(a), dev(b), dev(d), need_dx2=False)
+        assert none is None
+        none, dx2 = gtp.gtp_full_backward(plan, dev(a), dev(b), dev(d), need_dx1=False)
+        assert none is None
+        torch.cuda.synchronize()
+        assert O.max_rel_err(dx1.cpu().numpy(), r1) <= TOL
+        assert O.max_rel_err(dx2.cpu().numpy(), r2) <= TOL
+    z = torch.empty((0, 2, O.nsh(L)), device="cuda:0")
+    e1, e2 = gtp.gtp_full_backward(gtp.Plan(L, L, L), z, z, z)
+    assert e1.shape == (0, 2, O.nsh(L)) and e2.shape == (0, 2, O.nsh(L))
+
+
+def test_backward_edge_workload_sampled():
+    """Edge-shaped gradients at full size (B=65536, C=128, L=6): a seeded
+    subsample of products checked one by one."""
+    cfg = inputs.WORKLOADS["edge"]
+    B, C, L = cfg["B"], cfg["C"], 6
+    x1, r, h = inputs.edge_inputs(B, C, L)
+    t1 = torch.from_numpy(x1).cuda()
+    t2 = gtp.gtp_sh_filter(L, torch.from_numpy(r.astype(np.float32)).cuda(), torch.from_numpy(h).cuda())
+    d = inputs.output_gradient(2, (B, C, O.nsh(L)))
+    dy = torch.from_numpy(d).cuda()
+    _say("backward edge full size")
+    dx1, dx2 = gtp.gtp_full_backward(gtp.Plan(L, L, L), t1, t2, dy)
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(2, B * C, 4096)
+    ti = torch.from_numpy(idx).cuda()
+    bi, ci = idx // C, idx % C
+    a = x1[bi, ci].astype(np.float64)
+    # the oracle builds the filter from the raw ingredients with its own SH
+    b = h[bi, ci][:, inputs.degree_of_index(L)] * O.real_sh_xyz(L, r[bi])
+    r1, r2 = oracle_vjp(a, b, d[bi, ci], L, L, L)
+    e1 = O.max_rel_err(dx1.view(B * C, -1)[ti].cpu().numpy(), r1)
+    e2 = O.max_rel_err(dx2.view(B * C, -1)[ti].cpu().numpy(), r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)

@@ -447,6 +447,101 @@ def test_selfproduct_modes():
     assert np.abs(O.selfproduct(x, L, 1, Lout, "stepwise")[:, :9] - x).max() == 0
 
 
+# --------------------------------------------------------------------------- gradients (VJP)
+
+@pytest.mark.parametrize("L1,L2,Lout", [(2, 2, 2), (1, 2, 3), (3, 1, 2), (2, 2, 1)])
+def test_vjp_brute_force_basis(L1, L2, Lout):
+    """y is linear in x1: dx1[i] = <dy, gtp(e_i, x2)> for every basis vector e_i (and likewise for x2)."""
+    rng = np.random.default_rng(40 + L1 + 5 * L2 + 25 * Lout)
+    x1 = rng.standard_normal((3, O.nsh(L1)))
+    x2 = rng.standard_normal((3, O.nsh(L2)))
+    dy = rng.standard_normal((3, O.nsh(Lout)))
+    dx1, dx2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    for i in range(O.nsh(L1)):
+        e = np.zeros_like(x1)
+        e[:, i] = 1.0
+        assert np.abs(dx1[:, i] - np.einsum("nk,nk->n", dy, O.gtp(e, x2, L1, L2, Lout))).max() < 1e-13
+    for j in range(O.nsh(L2)):
+        e = np.zeros_like(x2)
+        e[:, j] = 1.0
+        assert np.abs(dx2[:, j] - np.einsum("nk,nk->n", dy, O.gtp(x1, e, L1, L2, Lout))).max() < 1e-13
+
+
+@pytest.mark.parametrize("L1,L2,Lout", [(6, 6, 6), (3, 5, 4), (4, 2, 9), (16, 16, 16)])
+def test_vjp_adjoint_identity(L1, L2, Lout):
+    """Euler's identity for a bilinear form: <dx1, x1> = <dy, y> = <dx2, x2>."""
+    rng = np.random.default_rng(50 + L1)
+    x1 = rng.standard_normal((4, O.nsh(L1)))
+    x2 = rng.standard_normal((4, O.nsh(L2)))
+    dy = rng.standard_normal((4, O.nsh(Lout)))
+    dx1, dx2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    s = np.einsum("nk,nk->n", dy, O.gtp_grid(x1, x2, L1, L2, Lout))
+    assert np.abs(np.einsum("ni,ni->n", dx1, x1) - s).max() < 1e-11 * (1 + np.abs(s).max())
+    assert np.abs(np.einsum("nj,nj->n", dx2, x2) - s).max() < 1e-11 * (1 + np.abs(s).max())
+
+
+def test_vjp_gaunt_and_grid_modes_agree():
+    rng = np.random.default_rng(52)
+    L1, L2, Lout = 5, 4, 6
+    x1 = rng.standard_normal((5, O.nsh(L1)))
+    x2 = rng.standard_normal((5, O.nsh(L2)))
+    dy = rng.standard_normal((5, O.nsh(Lout)))
+    a1, a2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout, mode="gaunt")
+    b1, b2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout, mode="grid")
+    assert np.abs(a1 - b1).max() < 1e-12 and np.abs(a2 - b2).max() < 1e-12
+
+
+def test_vjp_closed_forms():
+    """Gradients that follow from Legendre algebra by hand.
+
+    F2 = z (x2 = sqrt(4 pi / 3) e_(1,0)) and dy = e_(2,0): dx1 = P_L1(z Y_2^0),
+    and z P_2 = (3/5) P_3 + (2/5) P_1 gives dx1 = (2/sqrt 15) Y_1^0 + (3/sqrt 35) Y_3^0.
+    dy = e_(0,0): dx1 = x2 / sqrt(4 pi) (the gradient of y_00 = <x1, x2> / sqrt(4 pi)).
+    A constant F2 = 1 (x2 = sqrt(4 pi) e_0) makes y = P_Lout(x1): dx1 = P_L1(dy), and
+    dx2[0] = <x1, dy> / sqrt(4 pi) over the common degrees."""
+    L1, L2, Lout = 4, 1, 2
+    x2 = np.zeros(O.nsh(L2))
+    x2[idx(1, 0)] = math.sqrt(4 * math.pi / 3)
+    x1 = np.random.default_rng(53).standard_normal(O.nsh(L1))
+    dy = np.zeros(O.nsh(Lout))
+    dy[idx(2, 0)] = 1.0
+    dx1, _ = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    want = np.zeros(O.nsh(L1))
+    want[idx(1, 0)] = 2 / math.sqrt(15)
+    want[idx(3, 0)] = 3 / math.sqrt(35)
+    assert np.abs(dx1 - want).max() < 1e-14
+    dy = np.zeros(O.nsh(Lout))
+    dy[0] = 1.0
+    dx1, _ = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    want = np.zeros(O.nsh(L1))
+    want[: O.nsh(L2)] = x2 / math.sqrt(4 * math.pi)
+    assert np.abs(dx1 - want).max() < 1e-14
+    rng = np.random.default_rng(54)
+    for (L1, L2, Lout) in [(3, 0, 5), (5, 2, 3)]:
+        x1 = rng.standard_normal(O.nsh(L1))
+        x2 = np.zeros(O.nsh(L2))
+        x2[0] = math.sqrt(4 * math.pi)
+        dy = rng.standard_normal(O.nsh(Lout))
+        dx1, dx2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+        k = min(O.nsh(L1), O.nsh(Lout))
+        want = np.zeros(O.nsh(L1))
+        want[:k] = dy[:k]
+        assert np.abs(dx1 - want).max() < 1e-13
+        assert abs(dx2[0] - x1[:k] @ dy[:k] / math.sqrt(4 * math.pi)) < 1e-13
+
+
+def test_vjp_is_a_truncated_product():
+    """G is symmetric in its three (l, m) pairs: dx1 = P_L1(gtp(dy, x2)), dx2 = P_L2(gtp(dy, x1))."""
+    rng = np.random.default_rng(55)
+    L1, L2, Lout = 3, 5, 4
+    x1 = rng.standard_normal((6, O.nsh(L1)))
+    x2 = rng.standard_normal((6, O.nsh(L2)))
+    dy = rng.standard_normal((6, O.nsh(Lout)))
+    dx1, dx2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    assert np.abs(dx1 - O.gtp(dy, x2, Lout, L2, L1)).max() < 1e-13
+    assert np.abs(dx2 - O.gtp(dy, x1, Lout, L1, L2)).max() < 1e-13
+
+
 def test_max_rel_err():
     y = np.array([[3.0, 4.0], [0.0, 0.0]])
     assert O.max_rel_err(y, y) == 0
