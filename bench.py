@@ -1,7 +1,7 @@
 """Benchmark of the Gaunt tensor product hot path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg] [--L L]
-                    [--backward] [--no-cpu-baseline] [--gpus 1]
+                    [--backward | --weighted] [--no-cpu-baseline] [--gpus 1]
 
 Default: the edge workload (B=65536 edges x C=128 channels, L1=L2=Lout=6,
 x2 = radial weights x real SH of the edge direction), fp32.  One step is one
@@ -9,7 +9,8 @@ gtp_full over the whole batch.  Prints one JSON line with the throughput in
 (b,c)-products/s, the roofline of the kernel (its launch duration measured
 with HIP events on the stream it runs on) and the fp64 oracle timed on the
 host cores on a bounded sample of the same workload.  --backward times
-gtp_full_backward (both input gradients) on the same inputs instead.
+gtp_full_backward (both input gradients) on the same inputs instead,
+--weighted gtp_full_weighted with per-degree weights.
 """
 from __future__ import annotations
 
@@ -118,6 +119,18 @@ def pair_step(args, torch, gtp, inputs, plan, t1, t2, y, idx_cfg):
     oracle_of(O, idx, a, b) -> fn computing the same rows on the host, the
     output tensors the step writes)."""
     L1, L2, Lout = plan.L1, plan.L2, plan.Lout
+    if getattr(args, "weighted", False):
+        # one row of per-degree weights shared by every channel (w_l1 w_l2 w_l)
+        rng = inputs.rng_for(idx_cfg, 300)
+        w = [rng.standard_normal((1, L + 1)).astype("float32") for L in (L1, L2, Lout)]
+        tw = [torch.from_numpy(v).to(y.device) for v in w]
+
+        def step():
+            gtp.gtp_full_weighted(plan, t1, t2, tw[0], tw[1], tw[2], False, y=y)
+
+        def oracle_of(O, idx, a, b):
+            return lambda: O.gtp_weighted(a, b, w[0][0], w[1][0], w[2][0], L1, L2, Lout)
+        return step, (lambda idx: y.view(-1, y.shape[-1])[torch.from_numpy(idx).to(y.device)]), oracle_of, (y,)
     if not args.backward:
         def step():
             gtp.gtp_full(plan, t1, t2, y)
@@ -174,8 +187,10 @@ def make_workload(args, torch, gtp, inputs):
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
         return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2
-    if args.backward and w not in ("edge", "tiny", "sweep", "highdeg"):
-        raise SystemExit("--backward applies to the pair workloads (edge, tiny, sweep, highdeg)")
+    if (args.backward or args.weighted) and w not in ("edge", "tiny", "sweep", "highdeg"):
+        raise SystemExit("--backward / --weighted apply to the pair workloads (edge, tiny, sweep, highdeg)")
+    if args.backward and args.weighted:
+        raise SystemExit("--backward and --weighted are separate benchmarks")
     if w in ("tiny", "sweep", "highdeg"):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1
@@ -293,6 +308,9 @@ def main():
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass (gtp_full_backward: both input gradients for a seeded dy) "
                          "of a pair workload instead of gtp_full")
+    ap.add_argument("--weighted", action="store_true",
+                    help="time gtp_full_weighted (per-degree weights w_l1 w_l2 w_l shared by all channels) of a "
+                         "pair workload instead of gtp_full")
     ap.add_argument("--products", type=int, default=0,
                     help="use only the first N products of a pair workload (crossover runs of slow variants)")
     args = ap.parse_args()
@@ -326,6 +344,9 @@ def main():
     # average launch duration on the launch stream (a backward step is two
     # launches of the same kernel, one per input gradient)
     launches = 2 if args.backward else 1
+    if args.weighted and alg_flops:
+        # one multiply per input and output coefficient on top of the product
+        alg_flops = (alg_flops[0] + 3 * nsh(desc["L1"]), alg_flops[1])
     if args.backward and alg_flops:
         # per launch: dy (fp32) and one input in, one gradient out (equal degrees)
         K = nsh(desc["L1"])
@@ -338,7 +359,8 @@ def main():
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
         kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)))
-        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + ("_backward" if args.backward else ""), ksrc)
+        suffix = "_backward" if args.backward else ("_weighted" if args.weighted else "")
+        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + suffix, ksrc)
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         roof = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "traffic": tb, "kernel": kname,
@@ -360,6 +382,9 @@ def main():
         cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
 
     metric = METRIC
+    if args.weighted:
+        metric = "weighted Gaunt TP (per-degree w_l1 w_l2 w_l) (b,c)-products/sec; % MFMA/ALU roofline on 1 MI355X"
+        desc["workload"] = "weighted " + desc["workload"] + "; weights ~ N(0,1), one row for all channels"
     if args.backward:
         metric = "Gaunt TP backward (dx1 and dx2) (b,c)-products/sec; % MFMA/ALU roofline per launch on 1 MI355X"
         desc["workload"] = "backward of " + desc["workload"] + "; dy ~ N(0,1)"

@@ -95,6 +95,23 @@ gtp_status gtp_plan_destroy(gtp_plan p);
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 
+/* Weighted Gaunt tensor product (Sec. 3.1, eq. tp-eq-mul-weight; Appendix
+ * "Feature Interaction" weights w^l_{l1,l2} reparameterized as
+ * w_{l1} w_{l2} w_l):
+ *   y[b,c,(l,m)] = wout[r,l] * sum_{l1,l2} w1[r,l1] w2[r,l2] (x1^(l1) (x) x2^(l2))^(l)_m,
+ * computed as gtp_full of the degree-scaled inputs, scaled per output degree
+ * (the weights are applied as the inputs are loaded and the output stored).
+ * A degree mask (weights 0 / 1) gives the partial products x^(l1) (x) x^(l2).
+ * r = c when per_channel = 1 (one weight row per channel), r = 0 when
+ * per_channel = 0 (one row shared by every channel).
+ * w1: [R, L1+1], w2: [R, L2+1], wout: [R, Lout+1] fp32 device arrays with
+ * R = C or 1; any of them may be NULL (all ones).  Other arguments as in
+ * gtp_full; y must not overlap the inputs or the weights.  Plans built with
+ * GTP_CONV_DIRECT return GTP_ERR_UNSUPPORTED. */
+gtp_status gtp_full_weighted(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype, const float *w1,
+                             const float *w2, const float *wout, int per_channel, int64_t B, int64_t C, float *y,
+                             void *stream);
+
 /* Backward pass (vector-Jacobian product) of gtp_full: given the gradient dy
  * of a scalar loss with respect to y = gtp_full(x1, x2), the gradients
  *   dx1[b,c,i] = sum_{j,k} G_{i j k} x2[b,c,j] dy[b,c,k]   (i over degrees <= L1),

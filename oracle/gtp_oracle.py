@@ -21,6 +21,8 @@ Everything is numpy float64 and written to be checked against the paper by eye:
   the two spherical functions on an exact quadrature grid ("mode B");
 * its gradients (the vector-Jacobian product of the bilinear map), from the
   same Gaunt tensor or the same quadrature;
+* the weighted product with per-degree weights (Sec. 3.1, eq.
+  ``tp-eq-mul-weight``) as the double sum over degree pairs;
 * the three stages of Sec. 3.2 individually: SH -> 2D Fourier (eq. ``sh-fs``),
   the 2D convolution (eq. ``2D-conv``) and Fourier -> SH (eq. ``fs-sh``), each
   from its plain definition;
@@ -243,6 +245,45 @@ def gtp_grid(x1, x2, L1: int, L2: int, Lout: int, chunk: int = 4096) -> np.ndarr
         F = (a[s : s + chunk] @ Y1.T) * (b[s : s + chunk] @ Y2.T)
         y[s : s + chunk] = F @ Y3w
     return y.reshape(lead + (nsh(Lout),))
+
+
+def gtp_weighted(x1, x2, w1, w2, wo, L1: int, L2: int, Lout: int, mode: str = "auto") -> np.ndarray:
+    """Weighted Gaunt tensor product (Sec. 3.1, eq. tp-eq-mul-weight):
+
+        y^(l) = sum_{l1 <= L1} sum_{l2 <= L2} w1[l1] w2[l2] wo[l] (x1^(l1) (x) x2^(l2))^(l),
+
+    the learnable weights w^l_{l1,l2} of the feature-interaction layer in the
+    reparameterized form w_{l1} w_{l2} w_l.  x1[n, (L1+1)^2], x2[n, (L2+1)^2];
+    w1[n, L1+1], w2[n, L2+1], wo[n, Lout+1] hold the weights of each product
+    (rows broadcast).  Mode "sum" (default for max degree <= 8) evaluates the
+    double sum over degree pairs with the (l1, l2) blocks of the Gaunt tensor;
+    mode "scaled" evaluates the paper's equivalent route (Appendix, weighted
+    combinations): the product of the functions of w1 x1 and w2 x2, projected
+    and scaled by wo.
+    """
+    x1 = np.asarray(x1, dtype=np.float64).reshape(-1, nsh(L1))
+    x2 = np.asarray(x2, dtype=np.float64).reshape(-1, nsh(L2))
+    n = x1.shape[0]
+    w1 = np.broadcast_to(np.asarray(w1, dtype=np.float64), (n, L1 + 1))
+    w2 = np.broadcast_to(np.asarray(w2, dtype=np.float64), (n, L2 + 1))
+    wo = np.broadcast_to(np.asarray(wo, dtype=np.float64), (n, Lout + 1))
+    deg = lambda L: np.concatenate([np.full(2 * l + 1, l) for l in range(L + 1)])
+    if mode == "auto":
+        mode = "sum" if max(L1, L2, Lout) <= 8 else "scaled"
+    if mode == "sum":
+        G = _gaunt_cached(L1, L2, Lout)
+        y = np.zeros((n, nsh(Lout)))
+        for l1 in range(L1 + 1):
+            b1 = slice(l1 * l1, (l1 + 1) ** 2)
+            for l2 in range(L2 + 1):
+                b2 = slice(l2 * l2, (l2 + 1) ** 2)
+                part = np.einsum("ni,nj,ijk->nk", x1[:, b1], x2[:, b2], G[b1, b2, :])
+                y += (w1[:, l1] * w2[:, l2])[:, None] * part
+        return y * wo[:, deg(Lout)]
+    if mode == "scaled":
+        y = gtp_grid(x1 * w1[:, deg(L1)], x2 * w2[:, deg(L2)], L1, L2, Lout)
+        return y * wo[:, deg(Lout)]
+    raise ValueError(mode)
 
 
 def gtp_vjp(x1, x2, dy, L1: int, L2: int, Lout: int, chunk: int = 2048, mode: str = "auto"):

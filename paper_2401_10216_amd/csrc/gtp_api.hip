@@ -218,22 +218,25 @@ gtp_status device_ready(gtp_plan p) {
 // convolution when the plan asks for it, else the thread-per-product kernel,
 // the matrix-core wave kernel or the workgroup kernel, the first that has an
 // instantiation for the degrees and input types.
+constexpr gtp::DegWeights kNoWeights{nullptr, nullptr, nullptr, 1, 0, 0, false};
+
 gtp_status run_product(gtp_plan p, const void* x1, int it1, const void* x2, int it2, int64_t n, float* y,
-                       hipStream_t st, const char* what) {
+                       hipStream_t st, const char* what, const gtp::DegWeights& wt = kNoWeights) {
   hipError_t e = hipSuccess;
   if (p->conv == GTP_CONV_DIRECT) {
+    if (wt.on) return fail(GTP_ERR_UNSUPPORTED, "per-degree weights are not built for the direct convolution path");
     e = gtp::launch_full_direct(p->dev, x1, it1, x2, it2, n, y, st);
     if (e == hipErrorNotSupported) return fail(GTP_ERR_UNSUPPORTED, "direct convolution path not built");
     return e == hipSuccess ? GTP_OK : hip_fail(e, what);
   }
   bool done = false;
   if (!p->force_generic) {
-    e = gtp::launch_full_small(p->dev, x1, it1, x2, it2, n, y, 0, st, &done);
+    e = gtp::launch_full_small(p->dev, x1, it1, x2, it2, n, y, 0, wt, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
-    e = gtp::launch_full_wave(p->dev, x1, it1, x2, it2, n, y, st, &done);
+    e = gtp::launch_full_wave(p->dev, x1, it1, x2, it2, n, y, wt, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
   }
-  e = gtp::launch_full_generic(p->dev, x1, it1, x2, it2, n, y, 0, st);
+  e = gtp::launch_full_generic(p->dev, x1, it1, x2, it2, n, y, 0, wt, st);
   return e == hipSuccess ? GTP_OK : hip_fail(e, what);
 }
 
@@ -272,6 +275,38 @@ gtp_status gtp_full(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dty
   if ((s = device_ready(p)) != GTP_OK) return s;
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
   return run_product(p, x1, it, x2, it, n, y, static_cast<hipStream_t>(stream), "gtp_full launch");
+}
+
+gtp_status gtp_full_weighted(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* w1,
+                             const float* w2, const float* wout, int per_channel, int64_t B, int64_t C, float* y,
+                             void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  if (per_channel != 0 && per_channel != 1) return fail(GTP_ERR_INVALID_ARG, "per_channel must be 0 or 1");
+  int64_t n = 0, e1 = 0, e2 = 0, eo = 0;
+  if (!mul_ok(B, C, &n)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit in int64");
+  if (!mul_ok(n, gtp::nsh(p->L1), &e1) || !mul_ok(n, gtp::nsh(p->L2), &e2) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      e1 > INT64_MAX / 4 || e2 > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  if (n == 0) return GTP_OK;
+  if (!x1 || !x2 || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype);
+  const size_t rows = per_channel ? size_t(C) : 1;
+  const size_t nw1 = rows * (p->L1 + 1) * 4, nw2 = rows * (p->L2 + 1) * 4, nwo = rows * (p->Lout + 1) * 4;
+  const size_t ny = size_t(eo) * 4;
+  if (ranges_overlap(y, ny, x1, size_t(e1) * es) || ranges_overlap(y, ny, x2, size_t(e2) * es) ||
+      (w1 && ranges_overlap(y, ny, w1, nw1)) || (w2 && ranges_overlap(y, ny, w2, nw2)) ||
+      (wout && ranges_overlap(y, ny, wout, nwo)))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps an input or a weight array");
+  if ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % es ||
+      (reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(w1) | reinterpret_cast<uintptr_t>(w2) |
+       reinterpret_cast<uintptr_t>(wout)) % 4)
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  const gtp::DegWeights wt{w1, w2, wout, C, 0, per_channel, w1 || w2 || wout};
+  return run_product(p, x1, it, x2, it, n, y, static_cast<hipStream_t>(stream), "gtp_full_weighted launch", wt);
 }
 
 gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* dy,
@@ -401,16 +436,16 @@ gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void* x
     gtp_plan p = nullptr;
     if ((s = cached_plan(L, L, Lout, 0u, &p)) != GTP_OK) return s;
     bool done = false;
-    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, 0, st, &done);
-    if (!done) e = gtp::launch_full_generic(p->dev, x, it, x, it, n, y, 0, st);
+    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, 0, kNoWeights, st, &done);
+    if (!done) e = gtp::launch_full_generic(p->dev, x, it, x, it, n, y, 0, kNoWeights, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
   }
   if (mode == GTP_SELF_FUSED) {
     gtp_plan p = nullptr;
     if ((s = cached_plan(L, (nu - 1) * L, Lout, 0u, &p)) != GTP_OK) return s;
     bool done = false;
-    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, nu, st, &done);
-    if (!done) e = gtp::launch_full_generic(p->dev, x, it, nullptr, it, n, y, nu, st);
+    e = gtp::launch_full_small(p->dev, x, it, x, it, n, y, nu, kNoWeights, st, &done);
+    if (!done) e = gtp::launch_full_generic(p->dev, x, it, nullptr, it, n, y, nu, kNoWeights, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_selfproduct launch");
   }
   // stepwise, nu >= 3
@@ -426,10 +461,10 @@ gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void* x
   if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
   float* cur = (nu % 2 == 1) ? work : y;  // the last product lands in y
   float* nxt = (nu % 2 == 1) ? y : work;
-  e = gtp::launch_full_generic(p1->dev, x, it, x, it, n, cur, 0, st);
+  e = gtp::launch_full_generic(p1->dev, x, it, x, it, n, cur, 0, kNoWeights, st);
   for (int step = 3; e == hipSuccess && step <= nu; ++step) {
     // B_k (fp32, degree Lout) times A
-    e = gtp::launch_full_generic(p2->dev, cur, gtp::IN_F32, x, it, n, nxt, 0, st);
+    e = gtp::launch_full_generic(p2->dev, cur, gtp::IN_F32, x, it, n, nxt, 0, kNoWeights, st);
     std::swap(cur, nxt);
   }
   hipError_t e2 = hipFreeAsync(work, st);

@@ -34,12 +34,40 @@ struct DevTables {
 
 enum InType : int { IN_F32 = 0, IN_BF16 = 1 };
 
+// Per-degree weights folded into one product's input loads and output store
+// (Sec. 3.1, the weights w_{l1} w_{l2} w_l of a weighted combination): the
+// degree-l block of x1 is scaled by w1[row][l], of x2 by w2[row][l], of y by
+// wo[row][l], with row = (pbase + p) % C when per_channel, else 0, for the
+// launch's product p (pbase: the launch's first product in the caller's
+// batch).  A null pointer means all ones; on = false when all three are null.
+struct DegWeights {
+  const float* w1;
+  const float* w2;
+  const float* wo;
+  int64_t C;
+  int64_t pbase;
+  int per_channel;
+  bool on;
+};
+
+__device__ __forceinline__ int64_t weight_row(const DegWeights& w, int64_t p) {
+  return w.per_channel ? (w.pbase + p) % w.C : 0;
+}
+
+// degree l of SH coefficient index i = l*l + l + m
+__device__ __forceinline__ int degree_of(int i) {
+  int l = int(sqrtf(float(i)));
+  l += ((l + 1) * (l + 1) <= i) ? 1 : 0;
+  l -= (l * l > i) ? 1 : 0;
+  return l;
+}
+
 // Launchers (return the launch's hipError_t).  n = number of products.
 // Thread-per-product fused kernel for the degree triples it is instantiated
 // for; *supported = false when (L1, L2, Lout, nu) or the pair of input types
 // (it1, it2) has no instantiation.
 hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                             float* y, int nu, hipStream_t s, bool* supported);
+                             float* y, int nu, const DegWeights& wt, hipStream_t s, bool* supported);
 // Stepwise many-body chain in one kernel (thread per product) for the
 // instantiated (L, nu, Lout); t1 = tables of (L, L, Lout), t2 = (Lout, L, Lout).
 hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, int nu, const void* x,
@@ -48,11 +76,11 @@ hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, 
 // L1 = L2 = Lout = L in {16, 32, 64}; *supported = false otherwise, or for a
 // bf16 x1 with an fp32 x2.
 hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                            float* y, hipStream_t s, bool* supported);
+                            float* y, const DegWeights& wt, hipStream_t s, bool* supported);
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,
-                               int64_t n, float* y, int nu, hipStream_t s);
+                               int64_t n, float* y, int nu, const DegWeights& wt, hipStream_t s);
 // y[p, :(Lout+1)^2] = x[p, :(L+1)^2] truncated or zero-padded.
 hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
 // Direct 2D convolution of the real-form Fourier grids (the paper's eq.

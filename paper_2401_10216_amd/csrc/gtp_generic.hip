@@ -58,7 +58,7 @@ __host__ __device__ inline GenericLayout generic_layout(const DevTables& t, int 
 template <typename T1, typename T2>
 __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* __restrict__ x1,
                                                          const T2* __restrict__ x2, float* __restrict__ y,
-                                                         int64_t n, int nu, int JC) {
+                                                         int64_t n, int nu, int JC, DegWeights wt) {
   extern __shared__ float smem[];
   const GenericLayout g = generic_layout(t, nu, JC);
   const int tid = threadIdx.x;
@@ -74,8 +74,11 @@ __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* 
   float* Cm = smem + g.off_C;
 
   for (int64_t p = blockIdx.x; p < n; p += gridDim.x) {
-    for (int i = tid; i < g.K1; i += kBlock) xs1[i] = ld_in(x1, p * g.K1 + i);
-    for (int i = tid; i < g.K2; i += kBlock) xs2[i] = ld_in(x2, p * g.K2 + i);
+    const int64_t wrow = weight_row(wt, p);
+    for (int i = tid; i < g.K1; i += kBlock)
+      xs1[i] = ld_in(x1, p * g.K1 + i) * (wt.w1 ? wt.w1[wrow * (t.L1 + 1) + degree_of(i)] : 1.0f);
+    for (int i = tid; i < g.K2; i += kBlock)
+      xs2[i] = ld_in(x2, p * g.K2 + i) * (wt.w2 ? wt.w2[wrow * (t.L2 + 1) + degree_of(i)] : 1.0f);
     float acc[kMaxOut];
 #pragma unroll
     for (int q = 0; q < kMaxOut; ++q) acc[q] = 0.0f;
@@ -139,7 +142,8 @@ __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* 
 #pragma unroll
     for (int q = 0; q < kMaxOut; ++q) {
       const int o = tid + q * kBlock;
-      if (o < KO) y[p * KO + o] = (o < KE) ? acc[q] : 0.0f;
+      if (o < KO)
+        y[p * KO + o] = (o < KE) ? acc[q] * (wt.wo ? wt.wo[wrow * (t.Lout + 1) + degree_of(o)] : 1.0f) : 0.0f;
     }
   }
 }
@@ -472,7 +476,7 @@ int generic_chunk(const DevTables& t, int nu, size_t* lds_bytes) {
 }
 
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2, int64_t n,
-                               float* y, int nu, hipStream_t s) {
+                               float* y, int nu, const DegWeights& wt, hipStream_t s) {
   size_t lds = 0;
   const int JC = generic_chunk(t, nu, &lds);
   const dim3 grid(grid_for(n, 1)), block(kBlock);
@@ -480,16 +484,16 @@ hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, co
   using u16 = uint16_t;
   if (b1 && b2)
     hipLaunchKernelGGL((k_full_generic<u16, u16>), grid, block, lds, s, t, static_cast<const u16*>(x1),
-                       static_cast<const u16*>(x2), y, n, nu, JC);
+                       static_cast<const u16*>(x2), y, n, nu, JC, wt);
   else if (b1)
     hipLaunchKernelGGL((k_full_generic<u16, float>), grid, block, lds, s, t, static_cast<const u16*>(x1),
-                       static_cast<const float*>(x2), y, n, nu, JC);
+                       static_cast<const float*>(x2), y, n, nu, JC, wt);
   else if (b2)
     hipLaunchKernelGGL((k_full_generic<float, u16>), grid, block, lds, s, t, static_cast<const float*>(x1),
-                       static_cast<const u16*>(x2), y, n, nu, JC);
+                       static_cast<const u16*>(x2), y, n, nu, JC, wt);
   else
     hipLaunchKernelGGL((k_full_generic<float, float>), grid, block, lds, s, t, static_cast<const float*>(x1),
-                       static_cast<const float*>(x2), y, n, nu, JC);
+                       static_cast<const float*>(x2), y, n, nu, JC, wt);
   return hipGetLastError();
 }
 

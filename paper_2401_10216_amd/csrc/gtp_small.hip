@@ -66,6 +66,12 @@ __device__ __forceinline__ void sfor(F&& f) {
 }
 
 constexpr int ctri(int l, int m) { return l * (l + 1) / 2 + m; }
+// degree of coefficient index i = l*l + l + m
+constexpr int cdeg(int i) {
+  int l = 0;
+  while ((l + 1) * (l + 1) <= i) ++l;
+  return l;
+}
 constexpr int csh(int L) { return (L + 1) * (L + 1); }
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
@@ -463,11 +469,20 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
   for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
 }
 
-template <int L1, int L2, int LO, int NU, typename T1, typename T2>
+// Per-degree weights of one lane's product (WGT = true): scale the K values
+// at(I) (degrees <= L) by wrow[degree].
+template <int L, int K, typename V>
+__device__ __forceinline__ void scale_by_degree(const float* __restrict__ wrow, V&& at) {
+  float wl[L + 1];
+  sfor<0, L + 1>([&](auto LL) { wl[decltype(LL)::value] = wrow[decltype(LL)::value]; });
+  sfor<0, K>([&](auto I) { at(I) *= wl[cdeg(decltype(I)::value)]; });
+}
+
+template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT>
 __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const T1* __restrict__ x1, const T2* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
                                                       const float* __restrict__ ST, int ntS,
-                                                      const float* __restrict__ WT, int ntW) {
+                                                      const float* __restrict__ WT, int ntW, DegWeights wt) {
   using G = Geo<L1, L2, LO, NU>;
   constexpr int K1 = csh(L1), K2 = NU == 0 ? csh(L2) : 1, KO = csh(LO);
   constexpr int KT = cmax(cmax(K1, K2), KO);
@@ -490,9 +505,24 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     __syncthreads();
     slab_to_tile<K2>(v2, tile);
     __syncthreads();
+    if constexpr (WGT) {
+      // each lane scales its own product: x1 in registers, x2 in its tile row
+      const int64_t row = weight_row(wt, p0 + tid);
+      if (wt.w1)
+        scale_by_degree<L1, K1>(wt.w1 + row * (L1 + 1), [&](auto I) -> float& { return xa[decltype(I)::value]; });
+      if (wt.w2)
+        scale_by_degree<L2, K2>(wt.w2 + row * (L2 + 1),
+                                [&](auto I) -> float& { return tile[tid * K2 + decltype(I)::value]; });
+    }
     RegX<K1> A{xa};
     LdsX B{tile, tid * K2};
     gtp_core<L1, L2, LO, NU>(A, B, acc, ST, ntS, WT, ntW);
+    if constexpr (WGT) {
+      // outputs above degree LE are zeros and stay zeros
+      if (wt.wo)
+        scale_by_degree<G::LE, G::KE>(wt.wo + weight_row(wt, p0 + tid) * (LO + 1),
+                                      [&](auto I) -> float& { return acc[decltype(I)::value]; });
+    }
     __syncthreads();
   } else {
     load_rows<K1>(x1, p0, cnt, tile, xa);
@@ -538,24 +568,38 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   store_rows<KO, KO>(y, p0, cnt, tile, b);
 }
 
-template <int L1, int L2, int LO, int NU, typename T1, typename T2>
-hipError_t launch_typed(const DevTables& t, const void* x1, const void* x2, int64_t n, float* y, hipStream_t s) {
+template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT>
+hipError_t launch_typed(const DevTables& t, const void* x1, const void* x2, int64_t n, float* y,
+                        const DegWeights& wt, hipStream_t s) {
   const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
-  hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, T1, T2>), grid, block, 0, s, static_cast<const T1*>(x1),
-                     static_cast<const T2*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW);
+  hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, T1, T2, WGT>), grid, block, 0, s, static_cast<const T1*>(x1),
+                     static_cast<const T2*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW, wt);
   return hipGetLastError();
 }
 
 // Input types: both fp32, both bf16, or (equal degrees only) fp32 x1 with
 // bf16 x2, the pairing of a backward pass (fp32 output gradient times a bf16
-// input).  Other pairings are not instantiated (*supported = false).
+// input).  Per-degree weights: equal degrees, equal input types.  Other
+// combinations are not instantiated (*supported = false).
 template <int L1, int L2, int LO, int NU>
 hipError_t launch_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n, float* y,
-                      hipStream_t s, bool* supported) {
-  if (it1 == IN_BF16 && it2 == IN_BF16) return launch_typed<L1, L2, LO, NU, uint16_t, uint16_t>(t, x1, x2, n, y, s);
-  if (it1 == IN_F32 && it2 == IN_F32) return launch_typed<L1, L2, LO, NU, float, float>(t, x1, x2, n, y, s);
-  if constexpr (L1 == L2 && L2 == LO && NU == 0) {
-    if (it1 == IN_F32 && it2 == IN_BF16) return launch_typed<L1, L2, LO, NU, float, uint16_t>(t, x1, x2, n, y, s);
+                      const DegWeights& wt, hipStream_t s, bool* supported) {
+  constexpr bool equal = L1 == L2 && L2 == LO && NU == 0;
+  if (wt.on) {
+    if constexpr (equal) {
+      if (it1 == IN_BF16 && it2 == IN_BF16)
+        return launch_typed<L1, L2, LO, NU, uint16_t, uint16_t, true>(t, x1, x2, n, y, wt, s);
+      if (it1 == IN_F32 && it2 == IN_F32) return launch_typed<L1, L2, LO, NU, float, float, true>(t, x1, x2, n, y, wt, s);
+    }
+    *supported = false;
+    return hipSuccess;
+  }
+  if (it1 == IN_BF16 && it2 == IN_BF16)
+    return launch_typed<L1, L2, LO, NU, uint16_t, uint16_t, false>(t, x1, x2, n, y, wt, s);
+  if (it1 == IN_F32 && it2 == IN_F32) return launch_typed<L1, L2, LO, NU, float, float, false>(t, x1, x2, n, y, wt, s);
+  if constexpr (equal) {
+    if (it1 == IN_F32 && it2 == IN_BF16)
+      return launch_typed<L1, L2, LO, NU, float, uint16_t, false>(t, x1, x2, n, y, wt, s);
   }
   *supported = false;
   return hipSuccess;
@@ -585,18 +629,18 @@ hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const 
 #define GTP_SMALL_CHAINS(X) X(2, 3) X(1, 2) X(3, 3) X(2, 2)
 
 hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                             float* y, int nu, hipStream_t s, bool* supported) {
+                             float* y, int nu, const DegWeights& wt, hipStream_t s, bool* supported) {
   *supported = true;
   if (nu == 0) {
 #define GTP_CASE(a, b, c) \
-  if (t.L1 == a && t.L2 == b && t.Lout == c) return launch_one<a, b, c, 0>(t, x1, it1, x2, it2, n, y, s, supported);
+  if (t.L1 == a && t.L2 == b && t.Lout == c) return launch_one<a, b, c, 0>(t, x1, it1, x2, it2, n, y, wt, s, supported);
     GTP_SMALL_PAIRS(GTP_CASE)
 #undef GTP_CASE
   } else {
     // power plans are built as (L, (nu - 1) L, Lout)
 #define GTP_CASE(a, v, c) \
   if (nu == v && t.L1 == a && t.L2 == (v - 1) * a && t.Lout == c) \
-    return launch_one<a, 0, c, v>(t, x1, it1, x1, it1, n, y, s, supported);
+    return launch_one<a, 0, c, v>(t, x1, it1, x1, it1, n, y, wt, s, supported);
     GTP_SMALL_POWERS(GTP_CASE)
 #undef GTP_CASE
   }

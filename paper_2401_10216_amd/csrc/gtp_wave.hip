@@ -358,9 +358,9 @@ struct WaveCtx {
 
 // x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
 // threads of the workgroup: every load is issued before the first wait
-template <int L, typename T1, typename T2>
+template <int L, bool WGT, typename T1, typename T2>
 __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, int64_t P, int tid,
-                                        const int* xmap) {
+                                        const int* xmap, const DegWeights& wt) {
   using G = WGeo<L>;
   constexpr int K = G::K, NTH = G::NTH, NXK = G::NXK, NXKP = G::NXKP;
   int slot[NXKP];
@@ -381,6 +381,19 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
       v2[k] = ld_in_any(x2, P * K + e);
     }
   });
+  if constexpr (WGT) {
+    // per-degree weights of this product (Sec. 3.1), gathered per coefficient
+    const int64_t row = weight_row(wt, P) * (L + 1);
+    lfor<0, NXK>([&](auto KK) {
+      constexpr int k = decltype(KK)::value;
+      const int e = tid + NTH * k;
+      if (NTH * k + NTH - 1 < K || e < K) {
+        const int l = degree_of(e);
+        if (wt.w1) v1[k] *= wt.w1[row + l];
+        if (wt.w2) v2[k] *= wt.w2[row + l];
+      }
+    });
+  }
   lfor<0, G::XQ / NTH>([&](auto Z) {
     reinterpret_cast<float4*>(xs)[tid + NTH * decltype(Z)::value] = make_float4(0.f, 0.f, 0.f, 0.f);
   });
@@ -406,9 +419,10 @@ __device__ __forceinline__ void row_lm(int q, int& l, int& m) {
 
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.
-template <int L, typename T1, typename T2>
+template <int L, typename T1, typename T2, bool WGT>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_full_wave(
-    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
+    DegWeights wt) {
   using G = WGeo<L>;
   static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
   constexpr int NJ = G::NJ, NP = G::NP;
@@ -419,7 +433,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   const int lane = threadIdx.x;
   const int64_t P = blockIdx.x;
   if (P >= n) return;  // whole-wave exit (one product per workgroup)
-  stage_x<L>(xs, x1, x2, P, lane, t.XMAP);
+  stage_x<L, WGT>(xs, x1, x2, P, lane, t.XMAP, wt);
   const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(xs), t);
 
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
@@ -493,6 +507,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   if (lane <= L) {
     const int l = lane;
     y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
+    if constexpr (WGT) {
+      if (wt.wo) y0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
+    }
     y[P * K + l * l + l] = y0;
   }
   int ln = lane;
@@ -503,8 +520,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     if (q < NROW) {
       int l, m;
       row_lm(q, l, m);
-      y[P * K + l * l + l + m] = yc[it];
-      y[P * K + l * l + l - m] = ys[it];
+      float wl = 1.0f;
+      if constexpr (WGT) {
+        if (wt.wo) wl = wt.wo[weight_row(wt, P) * (L + 1) + l];
+      }
+      y[P * K + l * l + l + m] = yc[it] * wl;
+      y[P * K + l * l + l - m] = ys[it] * wl;
     }
   });
 }
@@ -514,9 +535,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
 // second stay in registers until every wave is done with the x image, then
 // go into its place.  The 256 threads then do the theta analysis, each over
 // all 64 mirror pairs of its output rows.
-template <int L, typename T1, typename T2>
+template <int L, typename T1, typename T2, bool WGT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_full_wave4(
-    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t) {
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
+    DegWeights wt) {
   using G = WGeo<L>;
   static_assert(G::NW == 4 && G::PASSES == 8, "four waves, two passes each");
   constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
@@ -529,7 +551,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t P = blockIdx.x;
   if (P >= n) return;  // whole-workgroup exit (one product per workgroup)
-  stage_x<L>(lds, x1, x2, P, tid, t.XMAP);
+  stage_x<L, WGT>(lds, x1, x2, P, tid, t.XMAP, wt);
   const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(lds), t);
 
   f4 o[G::NMR][4];
@@ -575,6 +597,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     row_sum(NIT, (l & 1) * 8 * NMP2, a0, unused, false);
     const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
     a0 = fmaf(tload(Wr, (l * (l + 1) / 2) * 4), fN + ((l & 1) ? -fS : fS), a0);
+    if constexpr (WGT) {
+      if (wt.wo) a0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
+    }
     y[P * K + l * l + l] = a0;
   }
   for (int it = 0; it < NIT; ++it) {
@@ -584,14 +609,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       row_lm(q, l, m);
       float ac = 0.0f, as = 0.0f;
       row_sum(it, ((l + m) & 1) * 8 * NMP2 + 2 * m, ac, as, true);
+      if constexpr (WGT) {
+        if (wt.wo) {
+          const float wl = wt.wo[weight_row(wt, P) * (L + 1) + l];
+          ac *= wl;
+          as *= wl;
+        }
+      }
       y[P * K + l * l + l + m] = ac;
       y[P * K + l * l + l - m] = as;
     }
   }
 }
 
-template <int L, typename T1, typename T2>
-hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t, hipStream_t s) {
+template <int L, typename T1, typename T2, bool WGT>
+hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t,
+                             const DegWeights& wt, hipStream_t s) {
   using G = WGeo<L>;
   // at most 2^30 workgroups per launch
   for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
@@ -599,10 +632,12 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
     const T1* a = static_cast<const T1*>(x1) + size_t(p0) * G::K;
     const T2* b = static_cast<const T2*>(x2) + size_t(p0) * G::K;
     float* yy = y + size_t(p0) * G::K;
+    DegWeights w = wt;
+    w.pbase += p0;  // the chunk's products start at p0
     if constexpr (G::NW == 1)
-      hipLaunchKernelGGL((k_full_wave<L, T1, T2>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t);
+      hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t, w);
     else
-      hipLaunchKernelGGL((k_full_wave4<L, T1, T2>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t);
+      hipLaunchKernelGGL((k_full_wave4<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t, w);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -611,13 +646,21 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
 
 // Input types: both fp32, both bf16, or fp32 x1 with bf16 x2 (a backward
 // pass: fp32 output gradient times a bf16 input); *supported = false for
-// bf16 x1 with fp32 x2.
+// bf16 x1 with fp32 x2, and for per-degree weights with mixed types.
 template <int L>
 hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                           float* y, hipStream_t s, bool* supported) {
-  if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float>(x1, x2, n, y, t, s);
-  if (it1 == IN_BF16 && it2 == IN_BF16) return launch_wave_typed<L, uint16_t, uint16_t>(x1, x2, n, y, t, s);
-  if (it1 == IN_F32 && it2 == IN_BF16) return launch_wave_typed<L, float, uint16_t>(x1, x2, n, y, t, s);
+                           float* y, const DegWeights& wt, hipStream_t s, bool* supported) {
+  if (wt.on) {
+    if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float, true>(x1, x2, n, y, t, wt, s);
+    if (it1 == IN_BF16 && it2 == IN_BF16)
+      return launch_wave_typed<L, uint16_t, uint16_t, true>(x1, x2, n, y, t, wt, s);
+    *supported = false;
+    return hipSuccess;
+  }
+  if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float, false>(x1, x2, n, y, t, wt, s);
+  if (it1 == IN_BF16 && it2 == IN_BF16)
+    return launch_wave_typed<L, uint16_t, uint16_t, false>(x1, x2, n, y, t, wt, s);
+  if (it1 == IN_F32 && it2 == IN_BF16) return launch_wave_typed<L, float, uint16_t, false>(x1, x2, n, y, t, wt, s);
   *supported = false;
   return hipSuccess;
 }
@@ -625,11 +668,11 @@ hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const vo
 }  // namespace
 
 hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                            float* y, hipStream_t s, bool* supported) {
+                            float* y, const DegWeights& wt, hipStream_t s, bool* supported) {
   *supported = true;
-  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, it1, x2, it2, n, y, s, supported);
-  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, it1, x2, it2, n, y, s, supported);
-  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, it1, x2, it2, n, y, s, supported);
+  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, it1, x2, it2, n, y, wt, s, supported);
+  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, it1, x2, it2, n, y, wt, s, supported);
+  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, it1, x2, it2, n, y, wt, s, supported);
   *supported = false;
   return hipSuccess;
 }

@@ -45,6 +45,7 @@ _SIGS = {
     "gtp_plan_destroy": (_I, [_P]),
     "gtp_full": (_I, [_P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
+    "gtp_full_weighted": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
     "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
     "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
@@ -159,6 +160,34 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
                           _stream(stream)))
+    return y
+
+
+def gtp_full_weighted(plan: Plan, x1, x2, w1=None, w2=None, wout=None, per_channel: bool = False, y=None,
+                      stream=None):
+    """y = wout * GTP(w1 * x1, w2 * x2) with per-degree weights w1[R, L1+1], w2[R, L2+1], wout[R, Lout+1]
+    (fp32 device tensors or None = ones; R = C if per_channel else 1)."""
+    import torch
+    if x1.dtype != x2.dtype:
+        raise TypeError("x1 and x2 must have the same dtype")
+    if x1.dim() != 3 or x2.dim() != 3 or x1.shape[:2] != x2.shape[:2]:
+        raise ValueError("x1, x2 must be [B, C, K] with equal B, C")
+    if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2):
+        raise ValueError("coefficient dimension does not match the plan")
+    B, C = int(x1.shape[0]), int(x1.shape[1])
+    R = C if per_channel else 1
+    ptrs = []
+    for w, L, name in ((w1, plan.L1, "w1"), (w2, plan.L2, "w2"), (wout, plan.Lout, "wout")):
+        if w is None:
+            ptrs.append(ctypes.c_void_p(None))
+            continue
+        if w.dtype != torch.float32 or tuple(w.shape) != (R, L + 1):
+            raise ValueError(f"{name} must be float32 [{R}, {L + 1}]")
+        ptrs.append(_dev(w, name))
+    if y is None:
+        y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
+    _check(lib().gtp_full_weighted(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), *ptrs,
+                                   1 if per_channel else 0, B, C, _dev(y, "y"), _stream(stream)))
     return y
 
 

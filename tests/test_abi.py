@@ -193,6 +193,31 @@ def test_backward_validation(L):
     assert b"HOST_ONLY" in L.gtp_last_error()
 
 
+def test_weighted_validation(L):
+    p = host_plan(2, 3, 4)
+    H = p.handle
+    x1, x2, y, w1, w2, wo = (fake(a) for a in (0x100000, 0x200000, 0x300000, 0x400000, 0x500000, 0x600000))
+    S = ctypes.c_void_p(0)
+    INV, OK = gtp.GTP_ERR_INVALID_ARG, gtp.GTP_OK
+    f = L.gtp_full_weighted
+    assert f(None, x1, x2, 0, w1, w2, wo, 0, 4, 4, y, S) == INV
+    assert f(H, x1, x2, 2, w1, w2, wo, 0, 4, 4, y, S) == INV  # bad dtype
+    assert f(H, x1, x2, 0, w1, w2, wo, 2, 4, 4, y, S) == INV  # per_channel not 0/1
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, -4, 4, y, S) == INV
+    assert f(H, None, x2, 0, w1, w2, wo, 0, 4, 4, y, S) == INV
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, 4, 4, None, S) == INV
+    assert f(H, x1, x2, 0, fake(0x300000 + 4), w2, wo, 0, 4, 4, y, S) == INV  # y overlaps w1
+    assert f(H, x1, x2, 0, w1, w2, fake(0x300000 - 8), 0, 4, 4, y, S) == INV  # wout (5 floats) runs into y
+    # wout's 5 floats end exactly where y starts: valid, refused only for the host-only plan
+    assert f(H, x1, x2, 0, w1, w2, fake(0x300000 - 20), 0, 4, 4, y, S) == INV
+    assert b"HOST_ONLY" in L.gtp_last_error()
+    assert f(H, x1, x2, 0, w1, fake(0x500002), wo, 0, 4, 4, y, S) == INV  # misaligned weight
+    assert f(H, x1, x2, 0, w1, w2, wo, 1, 0, 4, y, S) == OK  # empty batch
+    # valid arguments (NULL weights are ones) on a host-only plan: refused after validation
+    assert f(H, x1, x2, 0, None, None, None, 0, 4, 4, y, S) == INV
+    assert b"HOST_ONLY" in L.gtp_last_error()
+
+
 def test_stage_validation(L):
     p = host_plan(2, 3, 2)
     H = p.handle

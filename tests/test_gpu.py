@@ -479,3 +479,70 @@ def test_backward_edge_workload_sampled():
     e2 = O.max_rel_err(dx2.view(B * C, -1)[ti].cpu().numpy(), r2)
     _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
     assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
+# ------------------------------------------------------------------ weighted products (per-degree weights)
+
+WGT = [(2, 2, 2, False), (6, 6, 6, True), (6, 6, 6, False), (8, 8, 8, True), (3, 5, 4, True), (2, 2, 3, False),
+       (16, 16, 16, True), (32, 32, 32, False)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout,per_channel", WGT)
+def test_weighted_ragged(L1, L2, Lout, per_channel):
+    big = max(L1, L2, Lout) > 8
+    B, C = (37, 3) if big else (257, 5)  # a ragged number of products, channel count not a power of two
+    rng = np.random.default_rng(120 + L1 + 7 * Lout + per_channel)
+    a = rng.standard_normal((B, C, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((B, C, O.nsh(L2))).astype(np.float32)
+    R = C if per_channel else 1
+    w1 = rng.standard_normal((R, L1 + 1)).astype(np.float32)
+    w2 = rng.standard_normal((R, L2 + 1)).astype(np.float32)
+    wo = rng.standard_normal((R, Lout + 1)).astype(np.float32)
+    _say(f"weighted L1={L1} L2={L2} Lout={Lout} per_channel={per_channel} B={B} C={C}")
+    y = gtp.gtp_full_weighted(gtp.Plan(L1, L2, Lout), dev(a), dev(b), dev(w1), dev(w2), dev(wo), per_channel)
+    torch.cuda.synchronize()
+    rows = np.tile(np.arange(C) if per_channel else np.zeros(C, dtype=int), B)
+    sel = np.arange(B * C) if not big else np.arange(0, B * C, 4)
+    ref = O.gtp_weighted(a.reshape(B * C, -1)[sel], b.reshape(B * C, -1)[sel], w1[rows[sel]], w2[rows[sel]],
+                         wo[rows[sel]], L1, L2, Lout)
+    err = O.max_rel_err(y.view(B * C, -1).cpu().numpy()[sel], ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_weighted_masks_nulls_bf16_and_direct():
+    """Degree masks with NULL (all-ones) weights, bf16 inputs, and the
+    direct-convolution plan (not built for weights)."""
+    rng = np.random.default_rng(130)
+    L, B, C = 6, 300, 2
+    a = rng.standard_normal((B, C, O.nsh(L))).astype(np.float32)
+    b = rng.standard_normal((B, C, O.nsh(L))).astype(np.float32)
+    mask = np.zeros((1, L + 1), dtype=np.float32)
+    mask[0, 2] = 1.0  # partial product x^(2) (x) x2
+    _say("weighted mask / NULL weights")
+    y = gtp.gtp_full_weighted(gtp.Plan(L, L, L), dev(a), dev(b), w1=dev(mask))
+    torch.cuda.synchronize()
+    ref = O.gtp_weighted(a.reshape(B * C, -1), b.reshape(B * C, -1), mask[0], np.ones(L + 1), np.ones(L + 1), L, L, L)
+    assert O.max_rel_err(y.view(B * C, -1).cpu().numpy(), ref) <= TOL
+    # no weights at all: the plain product
+    y = gtp.gtp_full_weighted(gtp.Plan(L, L, L), dev(a), dev(b))
+    torch.cuda.synchronize()
+    assert O.max_rel_err(y.cpu().numpy(), O.gtp(a.astype(np.float64), b.astype(np.float64), L, L, L)) <= TOL
+    for Lb in (6, 16):
+        n = 200 if Lb == 6 else 24
+        bits1, v1 = inputs.round_to_bf16(rng.standard_normal((n, 1, O.nsh(Lb))).astype(np.float32))
+        bits2, v2 = inputs.round_to_bf16(rng.standard_normal((n, 1, O.nsh(Lb))).astype(np.float32))
+        wo = rng.standard_normal((1, Lb + 1)).astype(np.float32)
+        _say(f"weighted bf16 L={Lb}")
+        t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+        t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+        y = gtp.gtp_full_weighted(gtp.Plan(Lb, Lb, Lb), t1, t2, wout=dev(wo))
+        torch.cuda.synchronize()
+        ref = O.gtp_weighted(v1[:, 0], v2[:, 0], np.ones(Lb + 1), np.ones(Lb + 1), wo[0], Lb, Lb, Lb)
+        err = O.max_rel_err(y[:, 0].cpu().numpy(), ref)
+        _say(f"  err={err:.3e}")
+        assert err <= TOL, err
+    with pytest.raises(gtp.GTPError) as ei:
+        gtp.gtp_full_weighted(gtp.Plan(4, 4, 4, gtp.GTP_CONV_DIRECT), dev(a[:, :, :25]).contiguous(),
+                              dev(b[:, :, :25]).contiguous(), wout=dev(np.ones((1, 5), np.float32)))
+    assert ei.value.status == gtp.GTP_ERR_UNSUPPORTED

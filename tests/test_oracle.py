@@ -542,6 +542,74 @@ def test_vjp_is_a_truncated_product():
     assert np.abs(dx2 - O.gtp(dy, x1, Lout, L1, L2)).max() < 1e-13
 
 
+# --------------------------------------------------------------------------- weighted products
+
+def test_weighted_ones_and_constants():
+    rng = np.random.default_rng(60)
+    L1, L2, Lout = 3, 2, 4
+    a = rng.standard_normal((5, O.nsh(L1)))
+    b = rng.standard_normal((5, O.nsh(L2)))
+    y = O.gtp(a, b, L1, L2, Lout)
+    assert np.abs(O.gtp_weighted(a, b, np.ones(L1 + 1), np.ones(L2 + 1), np.ones(Lout + 1), L1, L2, Lout) - y).max() < 1e-13
+    # constant weights s1, s2, so multiply the product by s1 s2 so
+    yw = O.gtp_weighted(a, b, np.full(L1 + 1, 2.0), np.full(L2 + 1, -0.5), np.full(Lout + 1, 3.0), L1, L2, Lout)
+    assert np.abs(yw - (-3.0) * y).max() < 1e-13
+
+
+def test_weighted_degree_mask_closed_form():
+    """Keeping only degree 0 of x1 (F1 = x1_00 / sqrt(4 pi)): y = x1_00 / sqrt(4 pi) * P_Lout(x2);
+    an output mask keeps exactly the unmasked degrees of the plain product."""
+    rng = np.random.default_rng(61)
+    L1, L2, Lout = 4, 3, 5
+    a = rng.standard_normal((4, O.nsh(L1)))
+    b = rng.standard_normal((4, O.nsh(L2)))
+    m1 = np.zeros(L1 + 1)
+    m1[0] = 1.0
+    y = O.gtp_weighted(a, b, m1, np.ones(L2 + 1), np.ones(Lout + 1), L1, L2, Lout)
+    want = np.zeros((4, O.nsh(Lout)))
+    want[:, : O.nsh(L2)] = a[:, :1] / math.sqrt(4 * math.pi) * b
+    assert np.abs(y - want).max() < 1e-13
+    mo = np.array([0.0, 1.0, 0.0, 1.0, 0.0, 1.0])
+    y = O.gtp_weighted(a, b, np.ones(L1 + 1), np.ones(L2 + 1), mo, L1, L2, Lout)
+    keep = np.concatenate([np.full(2 * l + 1, mo[l]) for l in range(Lout + 1)])
+    assert np.abs(y - O.gtp(a, b, L1, L2, Lout) * keep).max() < 1e-13
+
+
+def test_weighted_degree_blocks_partition_the_product():
+    """Summing the single-block products (w1 = e_l1, w2 = e_l2) over all degree pairs gives the plain product."""
+    rng = np.random.default_rng(62)
+    L1, L2, Lout = 2, 3, 3
+    a = rng.standard_normal((3, O.nsh(L1)))
+    b = rng.standard_normal((3, O.nsh(L2)))
+    tot = np.zeros((3, O.nsh(Lout)))
+    for l1 in range(L1 + 1):
+        for l2 in range(L2 + 1):
+            e1 = np.eye(L1 + 1)[l1]
+            e2 = np.eye(L2 + 1)[l2]
+            part = O.gtp_weighted(a, b, e1, e2, np.ones(Lout + 1), L1, L2, Lout)
+            # triangle rule: the (l1, l2) block reaches only |l1 - l2| <= l <= l1 + l2 with l1 + l2 + l even
+            for l in range(Lout + 1):
+                if l < abs(l1 - l2) or l > l1 + l2 or (l1 + l2 + l) % 2:
+                    assert np.abs(part[:, l * l:(l + 1) ** 2]).max() < 1e-13
+            tot += part
+    assert np.abs(tot - O.gtp(a, b, L1, L2, Lout)).max() < 1e-13
+
+
+def test_weighted_sum_equals_scaled_route():
+    """The paper's equivalence: the double sum over degree pairs equals the
+    product of the weighted inputs' functions, scaled per output degree."""
+    rng = np.random.default_rng(63)
+    L1, L2, Lout = 5, 4, 6
+    a = rng.standard_normal((6, O.nsh(L1)))
+    b = rng.standard_normal((6, O.nsh(L2)))
+    w1 = rng.standard_normal((6, L1 + 1))
+    w2 = rng.standard_normal((6, L2 + 1))
+    wo = rng.standard_normal((6, Lout + 1))
+    ys = O.gtp_weighted(a, b, w1, w2, wo, L1, L2, Lout, mode="sum")
+    yc = O.gtp_weighted(a, b, w1, w2, wo, L1, L2, Lout, mode="scaled")
+    assert np.abs(ys - yc).max() < 1e-12
+
+
 def test_max_rel_err():
     y = np.array([[3.0, 4.0], [0.0, 0.0]])
     assert O.max_rel_err(y, y) == 0
