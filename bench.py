@@ -68,6 +68,21 @@ def formulation_flops(L1: int, L2: int, Lout: int) -> int:
     return int(round(f))
 
 
+def escn_flops(L: int) -> int:
+    """Flops per product of the rotated-frame convolution (L1 = L2 = Lout = L;
+    Sec. 3.3, eq. sh2fs-escn): x' = D x and y = D^T y' (sum_l (2l+1)^2 FMA each);
+    per mirror pair of the NT = 2L + 1 theta nodes: K FMA of synthesis, 2 adds
+    per m-part for the two nodes, the zonal filter (L + 1 FMA, 2 adds), 2
+    multiplies and 2 adds per m-part, K FMA of analysis.  An FMA counts 2.
+    The per-edge rotation matrix (built once per 64 channels) is not counted."""
+    K = (L + 1) ** 2
+    parts = 2 * L + 1
+    pairs = L + 1
+    rot = 2 * sum((2 * l + 1) ** 2 for l in range(L + 1))
+    per_pair = 2 * K + 2 * parts + 2 * (L + 1) + 2 + 4 * parts + 2 * K
+    return 2 * rot + pairs * per_pair
+
+
 def nsh(L):
     return (L + 1) * (L + 1)
 
@@ -77,8 +92,10 @@ def nsh(L):
 SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
 
 
-def dominant_kernel(workload: str, L: int):
+def dominant_kernel(workload: str, L: int, escn: bool = False):
     """(kernel, roofline bound, source file) of the kernel that dominates a workload."""
+    if escn:
+        return "k_conv_escn", "alu", "gtp_escn.hip"
     if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
         return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
     if workload == "manybody":
@@ -176,6 +193,13 @@ def make_workload(args, torch, gtp, inputs):
         plan = gtp.Plan(L, L, L)
         y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
         step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, 2)
+        if args.escn:
+            # the same product from (x1, r, h) in the edge's rotated frame
+            del t2
+            th = torch.from_numpy(h).to(dev)
+
+            def step():
+                gtp.gtp_conv_escn(plan, t1, tr, th, y=y)
 
         def oracle_sample(O, idx):
             deg = inputs.degree_of_index(L)
@@ -187,12 +211,20 @@ def make_workload(args, torch, gtp, inputs):
         desc = {"workload": "edge: B=65536 edges x C=128 channels, L1=L2=Lout=6, x1~N(0,1), "
                             "x2 = h[b,c,l] * Y_lm(r_b), r_b uniform on S^2, h~N(0,1)",
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
+        if args.escn:
+            desc["workload"] += "; gtp_conv_escn from (x1, r, h): rotated edge frame, m = 0 filter"
+            # per product: rotation in (sum (2l+1)^2 FMA), zonal theta product, rotation out;
+            # bytes: x1 and y, h, and the edge vector shared by C channels
+            return step, B * C, desc, (escn_flops(L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
+                oracle_sample, 2
         return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2
     if (args.backward or args.weighted) and w not in ("edge", "tiny", "sweep", "highdeg"):
         raise SystemExit("--backward / --weighted apply to the pair workloads (edge, tiny, sweep, highdeg)")
     if args.backward and args.weighted:
         raise SystemExit("--backward and --weighted are separate benchmarks")
+    if args.escn and (w != "edge" or args.backward or args.weighted):
+        raise SystemExit("--escn applies to the edge workload's forward product")
     if w in ("tiny", "sweep", "highdeg"):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1
@@ -313,6 +345,9 @@ def main():
     ap.add_argument("--weighted", action="store_true",
                     help="time gtp_full_weighted (per-degree weights w_l1 w_l2 w_l shared by all channels) of a "
                          "pair workload instead of gtp_full")
+    ap.add_argument("--escn", action="store_true",
+                    help="edge workload through gtp_conv_escn (the product with the SH filter taken in each edge's "
+                         "rotated frame from x1, r, h) instead of gtp_full with a prebuilt filter")
     ap.add_argument("--products", type=int, default=0,
                     help="use only the first N products of a pair workload (crossover runs of slow variants)")
     args = ap.parse_args()
@@ -360,8 +395,8 @@ def main():
     if alg_flops:
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
-        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)))
-        suffix = "_backward" if args.backward else ("_weighted" if args.weighted else "")
+        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn)
+        suffix = "_backward" if args.backward else ("_weighted" if args.weighted else ("_escn" if args.escn else ""))
         tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + suffix, ksrc)
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         roof = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
@@ -384,6 +419,8 @@ def main():
         cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
 
     metric = METRIC
+    if args.escn:
+        metric = "equivariant convolution (b,c)-products/sec at L=6 fp32, rotated edge frame; % ALU roofline on 1 MI355X"
     if args.weighted:
         metric = "weighted Gaunt TP (per-degree w_l1 w_l2 w_l) (b,c)-products/sec; % MFMA/ALU roofline on 1 MI355X"
         desc["workload"] = "weighted " + desc["workload"] + "; weights ~ N(0,1), one row for all channels"

@@ -95,6 +95,26 @@ gtp_status gtp_plan_destroy(gtp_plan p);
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 
+/* Equivariant convolution with the SH filter of an edge (Sec. 3.3
+ * "Equivariant Convolutions"; Appendix, eq. sh2fs-escn):
+ *   y[b,c] = GTP(x[b,c], F[b,c]),  F[b,c,(l,m)] = h[b,c,l] Y_l^m(r_b / |r_b|),
+ * the result of gtp_full(x, gtp_sh_filter(r, h)), computed in the frame in
+ * which the edge points at the pole: x is rotated by the real-SH matrix D_b of
+ * a rotation taking r_b / |r_b| to (0, 0, 1); there the filter has only the
+ * m = 0 coefficients h_l Y_l^0(pole) (2D Fourier coefficients only at v = 0),
+ * the product with it needs theta transforms only, and the result is rotated
+ * back by D_b^T.  (The z pole is this library's polar axis; the paper uses
+ * (0, 1, 0) in its y-up convention.)
+ * x: [B, C, (L1+1)^2] (in_dtype); r: [B, 3] fp32 edge vectors (need not be
+ * unit; a zero vector is taken as (0, 0, 1)); h: [B, C, L2+1] fp32 radial
+ * weights; y: [B, C, (Lout+1)^2] fp32, not overlapping the inputs.  The
+ * rotated-frame kernel covers L1 = L2 = Lout in 1..8 (one workgroup per edge
+ * and 64 channels, so C >= 64 fills it); other degrees, and plans built with
+ * GTP_CONV_DIRECT, build the filter in a stream-ordered workspace
+ * (hipMallocAsync) and take gtp_full. */
+gtp_status gtp_conv_escn(gtp_plan p, const void *x, gtp_dtype in_dtype, const float *r, const float *h, int64_t B,
+                         int64_t C, float *y, void *stream);
+
 /* Weighted Gaunt tensor product (Sec. 3.1, eq. tp-eq-mul-weight; Appendix
  * "Feature Interaction" weights w^l_{l1,l2} reparameterized as
  * w_{l1} w_{l2} w_l):
@@ -197,9 +217,11 @@ gtp_status gtp_plan_info(gtp_plan p, int64_t *out8);
  *   which 7: SM0P [pass][lane][v]         its m = 0 theta synthesis values (+ pole)
  *   which 8: WP   [pass][it][lane][8]     its lane-permuted theta analysis weights
  *   which 9: XMAP [lane][k]               its LDS slot of input coefficient lane + 64k
+ *   which 10: J   per degree l, (2l+1)^2    real-SH matrix of the rotation R_x(90 deg)
+ *   which 11: E   [pair][row]               theta-node rows of the rotated-frame convolution
  * with tri(l,m) = l(l+1)/2 + m, m >= 0.  Tables 5..9 exist only for
- * L1 = L2 = Lout = L in {16, 32} (length 0 otherwise); their layouts are
- * internal to that kernel.  Pass buf = NULL to
+ * L1 = L2 = Lout = L in {16, 32, 64}, tables 10..11 for L1 = L2 = Lout in
+ * 1..8 (length 0 otherwise); their layouts are internal to those kernels.  Pass buf = NULL to
  * get the length in *count; otherwise *count is the capacity in doubles. */
 gtp_status gtp_plan_table(gtp_plan p, int which, double *buf, int64_t *count);
 

@@ -23,6 +23,8 @@ Everything is numpy float64 and written to be checked against the paper by eye:
   same Gaunt tensor or the same quadrature;
 * the weighted product with per-degree weights (Sec. 3.1, eq.
   ``tp-eq-mul-weight``) as the double sum over degree pairs;
+* the equivariant convolution in the edge frame (Sec. 3.3, eq.
+  ``sh2fs-escn``): rotate, multiply by the m = 0 filter, rotate back;
 * the three stages of Sec. 3.2 individually: SH -> 2D Fourier (eq. ``sh-fs``),
   the 2D convolution (eq. ``2D-conv``) and Fourier -> SH (eq. ``fs-sh``), each
   from its plain definition;
@@ -491,6 +493,58 @@ def wigner_d_real(L: int, R: np.ndarray) -> np.ndarray:
     for l in range(L + 1):
         mask[l * l : (l + 1) ** 2, l * l : (l + 1) ** 2] = True
     return np.where(mask, D, 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Equivariant convolution in the edge frame (Sec. 3.3; Appendix, eq. sh2fs-escn)
+# ---------------------------------------------------------------------------
+
+def edge_rotation(r) -> np.ndarray:
+    """A rotation taking the direction of r to the pole (0, 0, 1).
+
+    With r / |r| = (sin b cos a, sin b sin a, cos b): R = R_y(-b) R_z(-a).
+    A zero vector gives the identity (its direction is taken as (0, 0, 1)).
+    """
+    r = np.asarray(r, dtype=np.float64)
+    n = np.linalg.norm(r)
+    if n == 0.0:
+        return np.eye(3)
+    a = math.atan2(r[1], r[0])
+    b = math.acos(max(-1.0, min(1.0, r[2] / n)))
+    ca, sa, cb, sb = math.cos(a), math.sin(a), math.cos(b), math.sin(b)
+    Rz = np.array([[ca, sa, 0.0], [-sa, ca, 0.0], [0.0, 0.0, 1.0]])   # R_z(-a)
+    Ry = np.array([[cb, 0.0, -sb], [0.0, 1.0, 0.0], [sb, 0.0, cb]])   # R_y(-b)
+    return Ry @ Rz
+
+
+def conv_escn(x, r, h, L1: int, L2: int, Lout: int, rotation=edge_rotation) -> np.ndarray:
+    """Gaunt product of x[b, c] with the SH filter h[b, c, l] Y_l(r_b / |r_b|),
+    in the steps of the rotated-frame construction (Sec. 3.3, eq. sh2fs-escn):
+
+    1. a rotation R_b taking the edge direction to the pole;
+    2. its real Wigner-D matrix D_b (degrees <= max(L1, Lout));
+    3. x' = D_b x;
+    4. the filter in the rotated frame, which has only m = 0 coefficients:
+       f[(l, 0)] = h_l Y_l^0(pole);
+    5. y' = GTP(x', f) truncated to Lout;
+    6. y = D_b^T y'.
+    x[B, C, (L1+1)^2], r[B, 3], h[B, C, L2+1]; returns y[B, C, (Lout+1)^2].
+    """
+    x = np.asarray(x, dtype=np.float64)
+    h = np.asarray(h, dtype=np.float64)
+    B, C = x.shape[:2]
+    LM = max(L1, Lout)
+    pole = real_sh(L2, np.array([0.0]), np.array([0.0]))[0]
+    y = np.empty((B, C, nsh(Lout)))
+    for b in range(B):
+        D = wigner_d_real(LM, rotation(r[b]))
+        xp = x[b] @ D[: nsh(L1), : nsh(L1)].T
+        f = np.zeros((C, nsh(L2)))
+        for l in range(L2 + 1):
+            f[:, l * l + l] = h[b, :, l] * pole[l * l + l]
+        yp = gtp(xp, f, L1, L2, Lout)
+        y[b] = yp @ D[: nsh(Lout), : nsh(Lout)]
+    return y
 
 
 # ---------------------------------------------------------------------------

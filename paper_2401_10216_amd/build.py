@@ -20,8 +20,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgtp.so")
 
-HIP_SOURCES = ["gtp_api.hip", "gtp_small.hip", "gtp_wave.hip", "gtp_generic.hip"]
-CPP_SOURCES = ["gtp_tables.cpp"]
+HIP_SOURCES = ["gtp_api.hip", "gtp_small.hip", "gtp_wave.hip", "gtp_generic.hip", "gtp_escn.hip"]
+CPP_SOURCES = ["gtp_tables.cpp", "gtp_escn_tables.cpp"]
 ARCH = "gfx950"
 # Packed fp32 VALU forms stay off: plain fp32 FMAs only.
 HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Xclang", "-target-feature", "-Xclang",

@@ -16,6 +16,7 @@
 
 #include "../../include/gtp.h"
 #include "gtp_device.hpp"
+#include "gtp_escn.hpp"
 #include "gtp_tables.hpp"
 
 struct gtp_plan_ {
@@ -26,8 +27,10 @@ struct gtp_plan_ {
   int conv = GTP_CONV_FFT;
   bool force_generic = false;
   gtp::Tables tab;
+  gtp::EscnHost esc;  // rotated-frame convolution tables (L1 = L2 = Lout <= 8)
   std::vector<float*> dbufs;
   gtp::DevTables dev{};
+  gtp::EscnDev escd{};
 };
 
 namespace {
@@ -109,6 +112,15 @@ gtp_status upload(gtp_plan_* p) {
   d.TWR = d.SMP = d.SM0P = d.WP = nullptr;
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
+  p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0};
+  if (p->esc.NPAIR) {
+    gtp::EscnDev& ed = p->escd;
+    if ((s = up(&p->esc.J, nullptr, &ed.J)) != GTP_OK) return s;
+    if ((s = up(&p->esc.E, nullptr, &ed.E)) != GTP_OK) return s;
+    ed.LM = p->esc.LM;
+    ed.NPAIR = p->esc.NPAIR;
+    ed.ERL = p->esc.ERL;
+  }
   if (t.waveL) {
     if ((s = up(&t.TWR, nullptr, &d.TWR)) != GTP_OK) return s;
     if ((s = up(&t.SMP, nullptr, &d.SMP)) != GTP_OK) return s;
@@ -158,6 +170,8 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
   p->conv = conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : GTP_CONV_FFT;
   try {
     p->tab = gtp::build_tables(L1, L2, Lout);
+    // the rotated-frame convolution kernel exists for equal degrees <= 8
+    if (L1 == L2 && L2 == Lout && L1 >= 1 && L1 <= 8) p->esc = gtp::build_escn_tables(p->tab);
   } catch (const std::bad_alloc&) {
     return fail(GTP_ERR_ALLOC, "table allocation failed");
   } catch (const std::exception& e) {
@@ -307,6 +321,57 @@ gtp_status gtp_full_weighted(gtp_plan p, const void* x1, const void* x2, gtp_dty
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
   const gtp::DegWeights wt{w1, w2, wout, C, 0, per_channel, w1 || w2 || wout};
   return run_product(p, x1, it, x2, it, n, y, static_cast<hipStream_t>(stream), "gtp_full_weighted launch", wt);
+}
+
+gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const float* r, const float* h, int64_t B,
+                         int64_t C, float* y, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  int64_t n = 0, ex = 0, eh = 0, eo = 0, er = 0;
+  if (!mul_ok(B, C, &n) || !mul_ok(B, 3, &er)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit");
+  if (!mul_ok(n, gtp::nsh(p->L1), &ex) || !mul_ok(n, p->L2 + 1, &eh) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      ex > INT64_MAX / 4 || eh > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  if (n == 0) return GTP_OK;
+  if (!x || !r || !h || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype), ny = size_t(eo) * 4;
+  if (ranges_overlap(y, ny, x, size_t(ex) * es) || ranges_overlap(y, ny, r, size_t(er) * 4) ||
+      ranges_overlap(y, ny, h, size_t(eh) * 4))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps an input");
+  if (reinterpret_cast<uintptr_t>(x) % es ||
+      (reinterpret_cast<uintptr_t>(r) | reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(y)) % 4)
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  const int64_t rf = gtp::escn_rot_floats(p->L1);
+  if (!p->force_generic && p->conv != GTP_CONV_DIRECT && p->escd.E && rf > 0) {
+    // per-edge rotation matrices in a stream-ordered workspace
+    float* dws = nullptr;
+    int64_t nd = 0;
+    if (!mul_ok(B, rf, &nd) || nd > INT64_MAX / 4) return fail(GTP_ERR_INVALID_ARG, "B too large");
+    hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&dws), size_t(nd) * sizeof(float), st);
+    if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+    bool done = false;
+    e = gtp::launch_conv_escn(p->escd, p->L1, p->L2, p->Lout, x, it, r, h, B, C, y, dws, st, &done);
+    const hipError_t e2 = hipFreeAsync(dws, st);
+    if (done) {
+      if (e != hipSuccess) return hip_fail(e, "gtp_conv_escn launch");
+      return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
+    }
+  }
+  // no rotated-frame kernel for these degrees: build the filter in a
+  // stream-ordered workspace and take the plain product (same result)
+  float* f = nullptr;
+  hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&f), size_t(n) * gtp::nsh(p->L2) * sizeof(float), st);
+  if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+  e = gtp::launch_sh_filter(p->L2, r, h, B, C, f, st);
+  s = e == hipSuccess ? run_product(p, x, it, f, gtp::IN_F32, n, y, st, "gtp_conv_escn launch")
+                      : hip_fail(e, "gtp_conv_escn filter launch");
+  const hipError_t e2 = hipFreeAsync(f, st);
+  if (s != GTP_OK) return s;
+  return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
 }
 
 gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* dy,
@@ -522,7 +587,9 @@ gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
       src = &tmp;
       break;
     }
-    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..9");
+    case 10: src = &p->esc.J; break;
+    case 11: src = &p->esc.E; break;
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..11");
   }
   if (!buf) {
     *count = int64_t(src->size());

@@ -1,0 +1,461 @@
+// Rotated-frame equivariant convolution (Sec. 3.3 "Equivariant Convolutions";
+// Appendix, eq. sh2fs-escn) for L1 = L2 = Lout = L <= 8.
+//
+// y[b,c] = GTP(x[b,c], F_b) with the SH filter F_b = sum_l h[b,c,l] Y_l(r_b /
+// |r_b|).  GTP commutes with rotations, so with a rotation R_b taking the
+// edge direction to the pole and D_b its real-SH matrix,
+//     y = D_b^T GTP(D_b x, D_b F_b),
+// and D_b F_b has only m = 0 coefficients, h_l Theta_l0(0): the filter's 2D
+// Fourier grid has only v = 0, so the product needs no phi transform at all.
+// Per m-part the rotated x is synthesised at the theta nodes (mirror pairs),
+// multiplied by the zonal filter and analysed back (the plan's S and W tables,
+// with the phi-moment factor NP or NP / 2 folded into W).
+//
+// Two kernels.  k_escn_rot builds every edge's D_b = J^T Z(-beta) J Z(-alpha)
+// once (Z: rotation about z; J: the fixed matrix of R_x(90 deg), J^T Z(t) J a
+// rotation about y) into a workspace; k_conv_escn takes one workgroup per
+// (edge, 64 channels), one product per lane: it loads D_b with its x slab,
+// applies it to each lane's x, takes the zonal product and applies D_b^T.
+// Its LDS holds the x tile, then D_b and the node-pair table, then the y
+// tile: 12.5 KB at L = 6.
+#include <type_traits>
+#include <utility>
+
+#include "gtp_device.hpp"
+#include "gtp_escn.hpp"
+
+namespace gtp {
+namespace {
+
+constexpr int kEW = 64;
+
+// Scheduling fence: bounds the loads the scheduler hoists ahead (each row of
+// D read early holds registers until it is used).
+#define GTP_ESCN_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+template <int B, int... Is, typename F>
+__device__ __forceinline__ void efor_impl(std::integer_sequence<int, Is...>, F& f) {
+  (f(std::integral_constant<int, B + Is>{}), ...);
+}
+// Compile-time loop over [B, E).
+template <int B, int E, typename F>
+__device__ __forceinline__ void efor(F&& f) {
+  if constexpr (E > B) efor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
+}
+
+constexpr int etri(int l, int m) { return l * (l + 1) / 2 + m; }
+constexpr int ensh(int L) { return (L + 1) * (L + 1); }
+// padded row length of the degree-l block of D in LDS (16-byte rows)
+constexpr int erow(int l) { return (2 * l + 1 + 3) / 4 * 4; }
+constexpr int dofs(int l) {
+  int s = 0;
+  for (int k = 0; k < l; ++k) s += (2 * k + 1) * erow(k);
+  return s;
+}
+// offset of the degree-l block of J (and T) without padding
+constexpr int jofs(int l) {
+  int s = 0;
+  for (int k = 0; k < l; ++k) s += (2 * k + 1) * (2 * k + 1);
+  return s;
+}
+
+__device__ __forceinline__ float ld_x(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float ld_x(const uint16_t* p, int64_t i) { return __uint_as_float(uint32_t(p[i]) << 16); }
+
+// node-pair table row (m-major, chunks padded to 4 floats): the unit zonal
+// filter at t_j (L + 1 values), then per m Theta_lm(t_j) for l = m..L, then
+// per m c_m W for l = m..L
+constexpr int pad4(int n) { return (n + 3) / 4 * 4; }
+template <int L>
+struct EGeo {
+  static constexpr int PZ = pad4(L + 1);
+  static constexpr int OS(int m) {
+    int o = PZ;
+    for (int k = 0; k < m; ++k) o += pad4(L + 1 - k);
+    return o;
+  }
+  static constexpr int OW(int m) { return OS(L + 1) + OS(m) - PZ; }
+  static constexpr int ERL = OW(L + 1), NPAIR = L + 1;
+};
+
+// ---------------------------------------------------------------------------
+// Per-edge rotation matrices: one wave per edge, four edges per workgroup.
+// D_b = J^T Z(-beta) J Z(-alpha) for every degree l <= L, written in the
+// padded row layout the product kernel reads (block l at dofs(l), rows of
+// erow(l) floats, padding zero).
+constexpr int kRotEdges = 4;
+
+template <int L>
+__global__ __launch_bounds__(64 * kRotEdges) void k_escn_rot(const float* __restrict__ r, int64_t B,
+                                                             float* __restrict__ Dout, EscnDev t) {
+  constexpr int H = L + 1, JS = jofs(L + 1), DS = dofs(L + 1);
+  __shared__ float Jl[JS];
+  __shared__ __align__(16) float Tw[kRotEdges][DS];  // T in D's padded row layout
+  __shared__ float4 tw[kRotEdges][H];               // (cos m a, sin m a, cos m b, sin m b)
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
+  const int64_t b = int64_t(blockIdx.x) * kRotEdges + w;
+  const bool valid = b < B;
+  float* const Tl = Tw[w];
+  float4* const trig = tw[w];
+  for (int e = tid; e < JS; e += 64 * kRotEdges) Jl[e] = t.J[e];
+  for (int e = lane; e < DS; e += 64) Tl[e] = 0.0f;  // row padding stays zero
+  if (valid && lane <= L) {
+    // the edge's angles (beta from the pole, alpha in the xy plane); a zero
+    // vector takes the direction (0, 0, 1)
+    const float rx = r[3 * b], ry = r[3 * b + 1], rz = r[3 * b + 2];
+    const float rho = sqrtf(rx * rx + ry * ry);
+    const float al = rho > 0.0f ? atan2f(ry, rx) : 0.0f;
+    const float be = (rho > 0.0f || rz != 0.0f) ? atan2f(rho, rz) : 0.0f;
+    float sa, ca, sb, cb;
+    sincosf(float(lane) * al, &sa, &ca);
+    sincosf(float(lane) * be, &sb, &cb);
+    trig[lane] = make_float4(ca, sa, cb, sb);
+  }
+  __syncthreads();
+  // T = Z(-beta) J Z(-alpha), block by block, in 2 x 2 mirror groups: rows
+  // l +- p and columns l +- q (p, q >= 0) share four entries of J and the
+  // trig values of orders p and q.  Z(-g) on a coefficient pair (c, s) of
+  // order m > 0: c' = c cos mg + s sin mg, s' = -c sin mg + s cos mg.
+  if (valid) {
+    efor<0, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), ew = erow(l);
+      for (int e = lane; e < (l + 1) * (l + 1); e += 64) {
+        const int p = e / (l + 1), q = e - p * (l + 1);
+        const float4 tq = trig[q], tp = trig[p];
+        const float* Jr = Jl + jo + (l + p) * d;  // row l + p
+        const float* Jm = Jl + jo + (l - p) * d;  // row l - p
+        // (J Z(-alpha)) at rows l +- p, columns l + q (c) and l - q (s)
+        float uc, us, vc, vs;
+        if (q > 0) {
+          uc = Jr[l + q] * tq.x - Jr[l - q] * tq.y;
+          us = Jr[l - q] * tq.x + Jr[l + q] * tq.y;
+          vc = Jm[l + q] * tq.x - Jm[l - q] * tq.y;
+          vs = Jm[l - q] * tq.x + Jm[l + q] * tq.y;
+        } else {
+          uc = us = Jr[l];
+          vc = vs = Jm[l];
+        }
+        float* Tr = Tl + dofs(l) + (l + p) * ew;
+        float* Tm = Tl + dofs(l) + (l - p) * ew;
+        if (p > 0) {
+          Tr[l + q] = tp.z * uc + tp.w * vc;
+          Tm[l + q] = -tp.w * uc + tp.z * vc;
+          if (q > 0) {
+            Tr[l - q] = tp.z * us + tp.w * vs;
+            Tm[l - q] = -tp.w * us + tp.z * vs;
+          }
+        } else {
+          Tr[l + q] = uc;
+          if (q > 0) Tr[l - q] = us;
+        }
+      }
+    });
+  }
+  __syncthreads();
+  if (!valid) return;
+  // D = J^T T: each item is four consecutive entries of one row (one J value
+  // and one 16-byte quad of T per k), stored as one 16-byte write
+  float* const Db = Dout + b * DS;
+  efor<0, L + 1>([&](auto LL) {
+    constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), nq = erow(l) / 4;
+    for (int e = lane; e < d * nq; e += 64) {
+      const int a = e / nq, q = e - a * nq;
+      float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      efor<0, d>([&](auto KK) {
+        constexpr int k = decltype(KK)::value;
+        const float jv = Jl[jo + k * d + a];
+        const float4 tv = reinterpret_cast<const float4*>(Tl + dofs(l) + k * erow(l))[q];
+        s.x = fmaf(jv, tv.x, s.x);
+        s.y = fmaf(jv, tv.y, s.y);
+        s.z = fmaf(jv, tv.z, s.z);
+        s.w = fmaf(jv, tv.w, s.w);
+      });
+      reinterpret_cast<float4*>(Db + dofs(l) + a * erow(l))[q] = s;
+    }
+  });
+}
+
+// ---------------------------------------------------------------------------
+// The product: one workgroup (one wave) per (edge, 64 channels).
+
+// degree of row R = l*l + a of the rotation blocks
+constexpr int rdeg(int R) {
+  int l = 0;
+  while ((l + 1) * (l + 1) <= R) ++l;
+  return l;
+}
+template <int E>
+__device__ __forceinline__ float f4at(const float4& v) {
+  if constexpr (E == 0) return v.x;
+  else if constexpr (E == 1) return v.y;
+  else if constexpr (E == 2) return v.z;
+  else return v.w;
+}
+// the 16-byte chunks of row R of D (LDS)
+template <int R, int NQ>
+__device__ __forceinline__ void load_drow(const float* Dl, float4 (&buf)[NQ]) {
+  constexpr int l = rdeg(R), a = R - l * l;
+  const float4* row = reinterpret_cast<const float4*>(Dl + dofs(l) + a * erow(l));
+  efor<0, erow(l) / 4>([&](auto QQ) { buf[decltype(QQ)::value] = row[decltype(QQ)::value]; });
+}
+// NQ 16-byte chunks at float offset O of a node-pair row (LDS)
+template <int O, int NQ, int NB>
+__device__ __forceinline__ void load_chunk(const float* er, float4 (&buf)[NB]) {
+  const float4* c = reinterpret_cast<const float4*>(er + O);
+  efor<0, NQ>([&](auto QQ) { buf[decltype(QQ)::value] = c[decltype(QQ)::value]; });
+}
+
+// register budget per lane: 3 waves per SIMD up to L = 6, 2 above
+constexpr int escn_waves(int L) { return L <= 6 ? 3 : 2; }
+
+template <int L, typename TIn>
+__global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(L)))) void k_conv_escn(
+    const TIn* __restrict__ x, const float* __restrict__ Dall, const float* __restrict__ h, float* __restrict__ y,
+    int64_t C, int ncb, EscnDev t) {
+  using EG = EGeo<L>;
+  constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR, ERL = EG::ERL;
+  constexpr int DS = dofs(L + 1), ES = NPAIR * ERL;
+  constexpr int XT = kEW * K;  // x / y tile
+  // once the x rows are in registers the tile's space holds D and the
+  // node-pair table (both 16-byte multiples)
+  static_assert(DS % 4 == 0 && ES % 4 == 0 && DS + ES <= XT, "LDS layout");
+  constexpr int ND4 = DS / 4, NE4 = ES / 4, RD = (ND4 + kEW - 1) / kEW, RE = (NE4 + kEW - 1) / kEW;
+  __shared__ __align__(16) float lds[XT];
+  float* const tile = lds;
+  float* const Dl = lds;
+  float* const El = lds + DS;
+
+  const int tid = threadIdx.x;
+  const int64_t b = blockIdx.x / ncb;
+  const int64_t c0 = int64_t(blockIdx.x % ncb) * kEW;
+  const int cnt = int(C - c0 < kEW ? C - c0 : kEW);
+  const int64_t p0 = b * C + c0;
+
+  // ---- 1. every load issued before the first wait: this workgroup's x slab
+  // (coalesced), the edge's rotation matrix and the node-pair table (16-byte
+  // loads), the lane's radial weights
+  // (uniform base pointers, 32-bit lane offsets)
+  const TIn* const xb = x + p0 * K;
+  const unsigned nx = unsigned(cnt * K);
+  float v[K];
+  efor<0, K>([&](auto I) {
+    constexpr int k = decltype(I)::value;
+    const unsigned i = unsigned(tid + k * kEW);
+    v[k] = ld_x(xb, i < nx ? i : nx - 1);
+  });
+  // (16-byte loads kept as plain floats; indices clamped into range: every
+  // lane loads, so the values stay in registers; the out-of-range copies are
+  // never stored)
+  float dv[4 * RD], ev[4 * RE];
+  const float4* Dg = reinterpret_cast<const float4*>(Dall + b * DS);
+  const float4* Eg = reinterpret_cast<const float4*>(t.E);
+  efor<0, RD>([&](auto I) {
+    constexpr int q = decltype(I)::value;
+    const int i = tid + q * kEW;
+    const float4 w = Dg[i < ND4 ? i : ND4 - 1];
+    dv[4 * q] = w.x;
+    dv[4 * q + 1] = w.y;
+    dv[4 * q + 2] = w.z;
+    dv[4 * q + 3] = w.w;
+  });
+  efor<0, RE>([&](auto I) {
+    constexpr int q = decltype(I)::value;
+    const int i = tid + q * kEW;
+    const float4 w = Eg[i < NE4 ? i : NE4 - 1];
+    ev[4 * q] = w.x;
+    ev[4 * q + 1] = w.y;
+    ev[4 * q + 2] = w.z;
+    ev[4 * q + 3] = w.w;
+  });
+  float hv[H];
+  const float* const hb = h + p0 * H;
+  const unsigned hl = unsigned(tid < cnt ? tid : cnt - 1);  // lanes past the last channel read a valid row
+  efor<0, H>([&](auto I) { hv[decltype(I)::value] = hb[hl * H + decltype(I)::value]; });
+
+  // ---- 2. x rows into registers through the tile, then D and the table
+  // into the tile's space
+  efor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
+  __syncthreads();
+  float xr[K];
+  efor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
+  __syncthreads();
+  efor<0, RD>([&](auto I) {
+    constexpr int q = decltype(I)::value;
+    const int i = tid + q * kEW;
+    if (i < ND4) reinterpret_cast<float4*>(Dl)[i] = make_float4(dv[4 * q], dv[4 * q + 1], dv[4 * q + 2], dv[4 * q + 3]);
+  });
+  efor<0, RE>([&](auto I) {
+    constexpr int q = decltype(I)::value;
+    const int i = tid + q * kEW;
+    if (i < NE4) reinterpret_cast<float4*>(El)[i] = make_float4(ev[4 * q], ev[4 * q + 1], ev[4 * q + 2], ev[4 * q + 3]);
+  });
+  __syncthreads();
+  // ---- 3. x' = D x, row by row over all degrees (row R = l*l + a); each
+  // row's 16-byte LDS reads (the same address in every lane) are issued
+  // before the previous row is consumed
+  constexpr int NQM = erow(L) / 4;
+  float xp[K];
+  {
+    float4 cur[NQM], nxt[NQM];
+    load_drow<0>(Dl, cur);
+    efor<0, K>([&](auto RR) {
+      constexpr int R = decltype(RR)::value, l = rdeg(R), d = 2 * l + 1;
+      if constexpr (R + 1 < K) load_drow<R + 1>(Dl, nxt);
+      GTP_ESCN_FENCE();
+      float s = 0.0f;
+      efor<0, erow(l) / 4>([&](auto QQ) {
+        constexpr int q = decltype(QQ)::value;
+        efor<0, 4>([&](auto EE) {
+          constexpr int bb = 4 * q + decltype(EE)::value;
+          if constexpr (bb < d) s = fmaf(f4at<decltype(EE)::value>(cur[q]), xr[l * l + bb], s);
+        });
+      });
+      xp[R] = s;
+      GTP_ESCN_FENCE();
+      if constexpr (R + 1 < K) efor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
+    });
+  }
+
+  // ---- 4. product with the zonal filter, mirror pair by mirror pair (table
+  // rows read from LDS, 16 bytes at a time, the same address in every lane;
+  // the chunks of order m + 1 are requested before those of order m are used)
+  float acc[K];
+  efor<0, K>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+#pragma unroll 1
+  for (int j = 0; j < NPAIR; ++j) {
+    GTP_ESCN_FENCE();
+    const float* er = El + j * ERL;
+    float4 zc[EG::PZ / 4];
+    efor<0, EG::PZ / 4>([&](auto QQ) { zc[decltype(QQ)::value] = reinterpret_cast<const float4*>(er)[decltype(QQ)::value]; });
+    constexpr int NCM = pad4(L + 1) / 4;  // chunks of the longest order (m = 0)
+    float4 sc[NCM], wc[NCM], sn[NCM], wn[NCM];
+    load_chunk<EG::OS(0), NCM>(er, sc);
+    load_chunk<EG::OW(0), NCM>(er, wc);
+    // filter at t_j and its mirror (Theta_l0(pi - t) = (-1)^l Theta_l0(t))
+    float fe = 0.0f, fo = 0.0f;
+    efor<0, H>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      const float z = f4at<l % 4>(zc[l / 4]);
+      if constexpr (l % 2 == 0) fe = fmaf(z, hv[l], fe);
+      else fo = fmaf(z, hv[l], fo);
+    });
+    const float fj = fe + fo, fm = fe - fo;
+    efor<0, L + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value, n = L + 1 - m;
+      if constexpr (m < L) {
+        load_chunk<EG::OS(m + 1), pad4(n - 1) / 4>(er, sn);
+        load_chunk<EG::OW(m + 1), pad4(n - 1) / 4>(er, wn);
+      }
+      GTP_ESCN_FENCE();
+      efor<0, (m == 0 ? 1 : 2)>([&](auto SS) {
+        constexpr int sg = decltype(SS)::value;  // 0: cos part (+m), 1: sin part (-m)
+        float ae = 0.0f, ao = 0.0f;
+        efor<m, L + 1>([&](auto LL) {
+          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m), c = l - m;
+          const float sv = f4at<c % 4>(sc[c / 4]);
+          if constexpr ((l + m) % 2 == 0) ae = fmaf(sv, xp[i], ae);
+          else ao = fmaf(sv, xp[i], ao);
+        });
+        const float pj = fj * (ae + ao), pm = fm * (ae - ao);
+        const float pe = pj + pm, po = pj - pm;
+        efor<m, L + 1>([&](auto LL) {
+          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m), c = l - m;
+          acc[i] = fmaf(f4at<c % 4>(wc[c / 4]), (l + m) % 2 == 0 ? pe : po, acc[i]);
+        });
+      });
+      GTP_ESCN_FENCE();
+      if constexpr (m < L) {
+        efor<0, pad4(n - 1) / 4>([&](auto QQ) {
+          sc[decltype(QQ)::value] = sn[decltype(QQ)::value];
+          wc[decltype(QQ)::value] = wn[decltype(QQ)::value];
+        });
+      }
+    });
+  }
+  GTP_ESCN_FENCE();
+
+  // ---- 5. y = D^T y', row by row with the same prefetch
+  float yv[K];
+  efor<0, K>([&](auto I) { yv[decltype(I)::value] = 0.0f; });
+  {
+    float4 cur[NQM], nxt[NQM];
+    load_drow<0>(Dl, cur);
+    efor<0, K>([&](auto RR) {
+      constexpr int R = decltype(RR)::value, l = rdeg(R), d = 2 * l + 1;
+      if constexpr (R + 1 < K) load_drow<R + 1>(Dl, nxt);
+      GTP_ESCN_FENCE();
+      efor<0, erow(l) / 4>([&](auto QQ) {
+        constexpr int q = decltype(QQ)::value;
+        efor<0, 4>([&](auto EE) {
+          constexpr int bb = 4 * q + decltype(EE)::value;
+          if constexpr (bb < d) yv[l * l + bb] = fmaf(f4at<decltype(EE)::value>(cur[q]), acc[R], yv[l * l + bb]);
+        });
+      });
+      GTP_ESCN_FENCE();
+      if constexpr (R + 1 < K) efor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
+    });
+  }
+
+  // ---- 6. store through the tile (coalesced)
+  __syncthreads();  // every lane is done with D and the table
+  efor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = yv[decltype(I)::value]; });
+  __syncthreads();
+  // store indices from an opaque copy of the lane id: not kept alive from the
+  // loads' index arithmetic
+  int ln = tid;
+  asm volatile("" : "+v"(ln));
+  float* const yb = y + p0 * K;
+  efor<0, K>([&](auto I) {
+    const unsigned i = unsigned(ln + decltype(I)::value * kEW);
+    if (i < nx) yb[i] = tile[i];
+  });
+}
+
+template <int L>
+hipError_t launch_l(const EscnDev& e, const void* x, int in_type, const float* r, const float* h, int64_t B,
+                    int64_t C, float* y, float* dws, hipStream_t s) {
+  if (e.ERL != EGeo<L>::ERL) return hipErrorInvalidValue;  // table layout and kernel disagree
+  const int64_t ncb = (C + kEW - 1) / kEW;
+  if (B * ncb > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((k_escn_rot<L>), dim3(unsigned((B + kRotEdges - 1) / kRotEdges)), dim3(64 * kRotEdges), 0, s, r,
+                     B, dws, e);
+  hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return err;
+  const dim3 grid(unsigned(B * ncb)), block(kEW);
+  if (in_type == IN_BF16)
+    hipLaunchKernelGGL((k_conv_escn<L, uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x), dws, h, y, C,
+                       int(ncb), e);
+  else
+    hipLaunchKernelGGL((k_conv_escn<L, float>), grid, block, 0, s, static_cast<const float*>(x), dws, h, y, C,
+                       int(ncb), e);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int64_t escn_rot_floats(int L) {
+  return (L >= 1 && L <= 8) ? dofs(L + 1) : 0;
+}
+
+hipError_t launch_conv_escn(const EscnDev& e, int L1, int L2, int Lout, const void* x, int in_type, const float* r,
+                            const float* h, int64_t B, int64_t C, float* y, float* dws, hipStream_t s,
+                            bool* supported) {
+  *supported = true;
+  if (L1 == L2 && L2 == Lout && e.E && e.LM == L1 && e.NPAIR == L1 + 1) {
+    switch (L1) {
+      case 1: return launch_l<1>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 2: return launch_l<2>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 3: return launch_l<3>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 4: return launch_l<4>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 5: return launch_l<5>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 6: return launch_l<6>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 7: return launch_l<7>(e, x, in_type, r, h, B, C, y, dws, s);
+      case 8: return launch_l<8>(e, x, in_type, r, h, B, C, y, dws, s);
+      default: break;
+    }
+  }
+  *supported = false;
+  return hipSuccess;
+}
+
+}  // namespace gtp

@@ -46,6 +46,7 @@ _SIGS = {
     "gtp_full": (_I, [_P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
     "gtp_full_weighted": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _I64, _I64, _P, _P]),
+    "gtp_conv_escn": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
     "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
     "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
     "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
@@ -160,6 +161,23 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
                           _stream(stream)))
+    return y
+
+
+def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None):
+    """y[B,C,(Lout+1)^2] = GTP(x, h[b,c,l] Y_l(r_b / |r_b|)) in the edge's rotated frame; r [B, 3], h [B, C, L2+1] fp32."""
+    import torch
+    if x.dim() != 3 or x.shape[2] != nsh(plan.L1):
+        raise ValueError("x must be [B, C, (L1+1)^2]")
+    B, C = int(x.shape[0]), int(x.shape[1])
+    if tuple(r.shape) != (B, 3) or r.dtype != torch.float32:
+        raise ValueError("r must be float32 [B, 3]")
+    if tuple(h.shape) != (B, C, plan.L2 + 1) or h.dtype != torch.float32:
+        raise ValueError("h must be float32 [B, C, L2+1]")
+    if y is None:
+        y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x.device)
+    _check(lib().gtp_conv_escn(plan.handle, _dev(x, "x"), _dtype_code(x), _dev(r, "r"), _dev(h, "h"), B, C,
+                               _dev(y, "y"), _stream(stream)))
     return y
 
 

@@ -546,3 +546,82 @@ def test_weighted_masks_nulls_bf16_and_direct():
         gtp.gtp_full_weighted(gtp.Plan(4, 4, 4, gtp.GTP_CONV_DIRECT), dev(a[:, :, :25]).contiguous(),
                               dev(b[:, :, :25]).contiguous(), wout=dev(np.ones((1, 5), np.float32)))
     assert ei.value.status == gtp.GTP_ERR_UNSUPPORTED
+
+
+# ------------------------------------------------------------------ rotated-frame equivariant convolution
+
+def _filter_ref(h, r, L2):
+    """The oracle's SH filter h[b,c,l] Y_l^m(r_b / |r_b|) (zero vector: (0, 0, 1))."""
+    rr = np.asarray(r, dtype=np.float64)
+    n = np.linalg.norm(rr, axis=1, keepdims=True)
+    u = np.where(n > 0, rr / np.where(n > 0, n, 1.0), np.array([0.0, 0.0, 1.0]))
+    deg = np.concatenate([np.full(2 * l + 1, l) for l in range(L2 + 1)])
+    return h.astype(np.float64)[:, :, deg] * O.real_sh_xyz(L2, u)[:, None, :]
+
+
+ESCN = [(1, 1, 1, 64), (2, 2, 2, 5), (3, 3, 3, 100), (4, 4, 4, 128), (5, 5, 5, 64), (6, 6, 6, 128), (6, 6, 6, 37),
+        (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout,C", ESCN)
+def test_conv_escn(L1, L2, Lout, C):
+    """Against the oracle's plain product with the SH filter (equal by equivariance);
+    special edge vectors: zero, both poles, nearly polar."""
+    B = 23
+    rng = np.random.default_rng(150 + L1 + Lout + C)
+    x = rng.standard_normal((B, C, O.nsh(L1))).astype(np.float32)
+    r = rng.standard_normal((B, 3)).astype(np.float32)
+    r[0] = 0.0
+    r[1] = [0.0, 0.0, 2.0]
+    r[2] = [0.0, 0.0, -0.5]
+    r[3] = [1e-4, -2e-4, 1.0]
+    h = rng.standard_normal((B, C, L2 + 1)).astype(np.float32)
+    _say(f"conv_escn L1={L1} L2={L2} Lout={Lout} B={B} C={C}")
+    y = gtp.gtp_conv_escn(gtp.Plan(L1, L2, Lout), dev(x), dev(r), dev(h))
+    torch.cuda.synchronize()
+    ref = oracle_pair(x.astype(np.float64).reshape(B * C, -1), _filter_ref(h, r, L2).reshape(B * C, -1), L1, L2, Lout)
+    err = O.max_rel_err(y.view(B * C, -1).cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_conv_escn_bf16_direct_plan_and_empty():
+    L, B, C = 6, 9, 64
+    rng = np.random.default_rng(160)
+    bits, xv = inputs.round_to_bf16(rng.standard_normal((B, C, O.nsh(L))).astype(np.float32))
+    r = rng.standard_normal((B, 3)).astype(np.float32)
+    h = rng.standard_normal((B, C, L + 1)).astype(np.float32)
+    ref = O.gtp(xv.astype(np.float64).reshape(B * C, -1), _filter_ref(h, r, L).reshape(B * C, -1), L, L, L)
+    _say("conv_escn bf16")
+    tx = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_conv_escn(gtp.Plan(L, L, L), tx, dev(r), dev(h))
+    torch.cuda.synchronize()
+    assert O.max_rel_err(y.view(B * C, -1).cpu().numpy(), ref) <= TOL
+    _say("conv_escn direct plan (filter + product)")
+    x = xv.astype(np.float32)
+    y = gtp.gtp_conv_escn(gtp.Plan(L, L, L, gtp.GTP_CONV_DIRECT), dev(x), dev(r), dev(h))
+    torch.cuda.synchronize()
+    assert O.max_rel_err(y.view(B * C, -1).cpu().numpy(), ref) <= TOL
+    z = torch.empty((0, C, O.nsh(L)), device="cuda:0")
+    y = gtp.gtp_conv_escn(gtp.Plan(L, L, L), z, torch.empty((0, 3), device="cuda:0"),
+                          torch.empty((0, C, L + 1), device="cuda:0"))
+    assert y.shape == (0, C, O.nsh(L))
+
+
+def test_conv_escn_edge_workload_sampled():
+    """The edge workload (B=65536, C=128, L=6) through the rotated-frame kernel,
+    a seeded subsample checked against the oracle product with its own filter."""
+    cfg = inputs.WORKLOADS["edge"]
+    B, C, L = cfg["B"], cfg["C"], 6
+    x1, r, h = inputs.edge_inputs(B, C, L)
+    _say("conv_escn edge workload full size")
+    y = gtp.gtp_conv_escn(gtp.Plan(L, L, L), torch.from_numpy(x1).cuda(),
+                          torch.from_numpy(r.astype(np.float32)).cuda(), torch.from_numpy(h).cuda())
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(cfg["index"], B * C, 4096)
+    bi, ci = idx // C, idx % C
+    x2ref = h[bi, ci][:, inputs.degree_of_index(L)] * O.real_sh_xyz(L, r[bi])
+    ref = O.gtp(x1[bi, ci].astype(np.float64), x2ref, L, L, L)
+    err = O.max_rel_err(y.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err

@@ -610,6 +610,77 @@ def test_weighted_sum_equals_scaled_route():
     assert np.abs(ys - yc).max() < 1e-12
 
 
+# --------------------------------------------------------------------------- rotated-frame convolution
+
+def _filter(h, r, L2):
+    """x2[b, c, (l, m)] = h[b, c, l] Y_l^m(r_b / |r_b|)."""
+    rr = np.asarray(r, dtype=np.float64)
+    n = np.linalg.norm(rr, axis=1, keepdims=True)
+    u = np.where(n > 0, rr / np.where(n > 0, n, 1.0), np.array([0.0, 0.0, 1.0]))
+    Y = O.real_sh_xyz(L2, u)
+    deg = np.concatenate([np.full(2 * l + 1, l) for l in range(L2 + 1)])
+    return h[:, :, deg] * Y[:, None, :]
+
+
+def test_edge_rotation_maps_direction_to_pole():
+    rng = np.random.default_rng(70)
+    for _ in range(20):
+        r = rng.standard_normal(3) * rng.uniform(0.1, 5.0)
+        R = O.edge_rotation(r)
+        assert np.allclose(R @ R.T, np.eye(3), atol=1e-14) and abs(np.linalg.det(R) - 1) < 1e-13
+        assert np.allclose(R @ (r / np.linalg.norm(r)), [0, 0, 1], atol=1e-14)
+    assert np.allclose(O.edge_rotation(np.zeros(3)), np.eye(3))
+
+
+def test_rotated_filter_has_only_m0():
+    """The premise of eq. sh2fs-escn: in the edge frame the SH filter is h_l Y_l^0(pole) at m = 0 only."""
+    rng = np.random.default_rng(71)
+    L = 5
+    for _ in range(5):
+        r = rng.standard_normal(3)
+        h = rng.standard_normal(L + 1)
+        f = _filter(h[None, None, :], r[None, :], L)[0, 0]
+        D = O.wigner_d_real(L, O.edge_rotation(r))
+        fr = D @ f
+        for l in range(L + 1):
+            want = np.zeros(2 * l + 1)
+            want[l] = h[l] * math.sqrt((2 * l + 1) / (4 * math.pi))
+            assert np.abs(fr[l * l:(l + 1) ** 2] - want).max() < 1e-12
+
+
+@pytest.mark.parametrize("L1,L2,Lout", [(1, 1, 1), (3, 3, 3), (6, 6, 6), (3, 2, 4), (2, 4, 3)])
+def test_conv_escn_equals_plain_product(L1, L2, Lout):
+    """GTP commutes with rotations: the edge-frame result equals the plain product with the filter."""
+    rng = np.random.default_rng(72 + L1 + L2)
+    B, C = 4, 3
+    x = rng.standard_normal((B, C, O.nsh(L1)))
+    r = rng.standard_normal((B, 3))
+    r[0] = [0.0, 0.0, 0.0]  # zero vector: direction (0, 0, 1)
+    r[1] = [0.0, 0.0, -2.0]  # south pole
+    h = rng.standard_normal((B, C, L2 + 1))
+    y = O.conv_escn(x, r, h, L1, L2, Lout)
+    want = O.gtp(x, _filter(h, r, L2), L1, L2, Lout)
+    assert np.abs(y - want).max() < 1e-12
+
+
+def test_conv_escn_independent_of_the_rotation_chosen():
+    """Any rotation taking the edge to the pole gives the same result (here R_z(g) R_b)."""
+    rng = np.random.default_rng(73)
+    L = 4
+    x = rng.standard_normal((3, 2, O.nsh(L)))
+    r = rng.standard_normal((3, 3))
+    h = rng.standard_normal((3, 2, L + 1))
+
+    def spun(rv):
+        g = 0.7
+        Rz = np.array([[math.cos(g), -math.sin(g), 0], [math.sin(g), math.cos(g), 0], [0, 0, 1]])
+        return Rz @ O.edge_rotation(rv)
+
+    a = O.conv_escn(x, r, h, L, L, L)
+    b = O.conv_escn(x, r, h, L, L, L, rotation=spun)
+    assert np.abs(a - b).max() < 1e-12
+
+
 def test_max_rel_err():
     y = np.array([[3.0, 4.0], [0.0, 0.0]])
     assert O.max_rel_err(y, y) == 0
