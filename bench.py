@@ -68,19 +68,21 @@ def formulation_flops(L1: int, L2: int, Lout: int) -> int:
     return int(round(f))
 
 
-def escn_flops(L: int) -> int:
+def escn_flops(L: int, C: int) -> float:
     """Flops per product of the rotated-frame convolution (L1 = L2 = Lout = L;
     Sec. 3.3, eq. sh2fs-escn): x' = D x and y = D^T y' (sum_l (2l+1)^2 FMA each);
     per mirror pair of the NT = 2L + 1 theta nodes: K FMA of synthesis, 2 adds
     per m-part for the two nodes, the zonal filter (L + 1 FMA, 2 adds), 2
-    multiplies and 2 adds per m-part, K FMA of analysis.  An FMA counts 2.
-    The per-edge rotation matrix (built once per 64 channels) is not counted."""
+    multiplies and 2 adds per m-part, K FMA of analysis; plus the edge's
+    rotation matrices, shared by its C channels: T = Z(-b) J Z(-a) (6 flops
+    per entry) and D = J^T T ((2l+1)^3 FMA per degree).  An FMA counts 2."""
     K = (L + 1) ** 2
     parts = 2 * L + 1
     pairs = L + 1
     rot = 2 * sum((2 * l + 1) ** 2 for l in range(L + 1))
     per_pair = 2 * K + 2 * parts + 2 * (L + 1) + 2 + 4 * parts + 2 * K
-    return 2 * rot + pairs * per_pair
+    per_edge = sum(6 * (2 * l + 1) ** 2 + 2 * (2 * l + 1) ** 3 for l in range(L + 1))
+    return 2 * rot + pairs * per_pair + per_edge / C
 
 
 def nsh(L):
@@ -95,7 +97,8 @@ SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
 def dominant_kernel(workload: str, L: int, escn: bool = False):
     """(kernel, roofline bound, source file) of the kernel that dominates a workload."""
     if escn:
-        return "k_conv_escn", "alu", "gtp_escn.hip"
+        # both kernels of the step (rotation matrices, then the product): one unit
+        return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
     if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
         return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
     if workload == "manybody":
@@ -215,7 +218,7 @@ def make_workload(args, torch, gtp, inputs):
             desc["workload"] += "; gtp_conv_escn from (x1, r, h): rotated edge frame, m = 0 filter"
             # per product: rotation in (sum (2l+1)^2 FMA), zonal theta product, rotation out;
             # bytes: x1 and y, h, and the edge vector shared by C channels
-            return step, B * C, desc, (escn_flops(L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
+            return step, B * C, desc, (escn_flops(L, C), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
                 oracle_sample, 2
         return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2
