@@ -1,6 +1,6 @@
 """Benchmark of the Gaunt tensor product hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg] [--L L]
+    python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg|mix] [--L L]
                     [--backward | --weighted] [--no-cpu-baseline] [--gpus 1]
 
 Default: the edge workload (B=65536 edges x C=128 channels, L1=L2=Lout=6,
@@ -99,6 +99,9 @@ def dominant_kernel(workload: str, L: int, escn: bool = False):
     if escn:
         # both kernels of the step (rotation matrices, then the product): one unit
         return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
+    if workload == "mix":
+        # pair products (thread per product) then the mix on the matrix cores: one unit
+        return "k_full_small(pairs)+k_mix_gemm", "alu", "gtp_mix.hip"
     if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
         return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
     if workload == "manybody":
@@ -289,6 +292,32 @@ def make_workload(args, torch, gtp, inputs):
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
         return step, N * C, desc, (formulation_flops(L, L, Lout) + formulation_flops(Lout, L, Lout),
                                    SURVEY_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
+    if w == "mix":
+        cfg = inputs.WORKLOADS["mix"]
+        B, C, L = cfg["B"], cfg["C"], cfg["L1"]
+        x1, x2, W = inputs.mix_inputs(B, C, L)
+        t1 = torch.from_numpy(x1).to(dev)
+        t2 = torch.from_numpy(x2).to(dev)
+        tw = torch.from_numpy(W).to(dev)
+        plan = gtp.Plan(L, L, L)
+        y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
+
+        def step():
+            gtp.gtp_channel_mix(plan, t1, t2, tw, y=y)
+
+        def oracle_sample(O, idx):
+            # idx indexes pair products (b, c1, c2); the oracle computes the
+            # whole batch entries b they fall in
+            bs = np.unique(idx // (C * C))
+            rows = lambda ix: y[torch.from_numpy(bs).to(y.device)].reshape(len(bs), -1)
+            return (lambda: O.channel_mix(x1[bs], x2[bs], W, L, L, L).reshape(len(bs), -1)), rows, len(bs) * C * C
+
+        desc = {"workload": "mix: channel mixing y[b,co] = sum_{c1,c2} W[co,c1,c2] GTP(x1[b,c1], x2[b,c2]), "
+                            "B=8192, C1=C2=Co=32, L1=L2=Lout=6, x~N(0,1), W~N(0,1/C^2)",
+                "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
+        # per pair product: the product itself and 2 Co K flops of the mix; bytes: x1, x2, y over C^2 pairs
+        return step, B * C * C, desc, (formulation_flops(L, L, L) + 2 * C * nsh(L), None), \
+            4.0 * nsh(L) * 3 * C / (C * C), oracle_sample, 6
     if w == "copy":
         # plain device copy of a known size: calibrates the HBM byte counters
         nbytes = 1 << 30
@@ -313,7 +342,9 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     n = min(1024, total)
     while True:
         idx = inputs.sample_indices(idx_cfg, total, n)
-        fn, rows = oracle_sample(O, idx)
+        got_sample = oracle_sample(O, idx)
+        fn, rows = got_sample[0], got_sample[1]
+        done = got_sample[2] if len(got_sample) > 2 else n  # products the oracle call covers
         t0 = time.perf_counter()
         ref = fn()
         dt = time.perf_counter() - t0
@@ -325,8 +356,8 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     assert idx.size and 0 <= idx.min() and idx.max() < total
     got = rows(idx).cpu().numpy()
     err = O.max_rel_err(got, ref)
-    return {"value": n / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
+    return {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
                       f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err}
 
 
@@ -422,6 +453,8 @@ def main():
         cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
 
     metric = METRIC
+    if args.workload == "mix":
+        metric = "channel-mixing Gaunt TP (b,c1,c2) pair-products/sec at L=6 fp32, C=32; % ALU roofline on 1 MI355X"
     if args.escn:
         metric = "equivariant convolution (b,c)-products/sec at L=6 fp32, rotated edge frame; % ALU roofline on 1 MI355X"
     if args.weighted:

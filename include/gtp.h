@@ -95,6 +95,21 @@ gtp_status gtp_plan_destroy(gtp_plan p);
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 
+/* Channel mixing (Appendix, combination rules of features in different
+ * channels, channel-mixing case):
+ *   y[b, co] = sum_{c1 < C1, c2 < C2} W[co, c1, c2] GTP(x1[b, c1], x2[b, c2]),
+ * O(C1 C2) full products per batch entry.  The pair products are taken by the
+ * fused product kernels (outer-product indexing) into a stream-ordered
+ * workspace (hipMallocAsync, at most 256 MiB, chunked over b) and combined as
+ * y_b = W T_b (Co x C1C2 times C1C2 x (Lout+1)^2) on the fp32 matrix cores.
+ * x1: [B, C1, (L1+1)^2], x2: [B, C2, (L2+1)^2] (in_dtype); W: [Co, C1, C2]
+ * fp32; y: [B, Co, (Lout+1)^2] fp32, not overlapping the inputs or W.
+ * C1 C2 == 0 writes zeros (x1, x2 and W may then be NULL); B Co == 0 is a
+ * no-op.  The thread-per-product
+ * kernel serves L1 = L2 = Lout <= 8; other degrees take the workgroup kernel. */
+gtp_status gtp_channel_mix(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype, const float *W,
+                           int64_t B, int64_t C1, int64_t C2, int64_t Co, float *y, void *stream);
+
 /* Equivariant convolution with the SH filter of an edge (Sec. 3.3
  * "Equivariant Convolutions"; Appendix, eq. sh2fs-escn):
  *   y[b,c] = GTP(x[b,c], F[b,c]),  F[b,c,(l,m)] = h[b,c,l] Y_l^m(r_b / |r_b|),

@@ -25,6 +25,8 @@ Everything is numpy float64 and written to be checked against the paper by eye:
   ``tp-eq-mul-weight``) as the double sum over degree pairs;
 * the equivariant convolution in the edge frame (Sec. 3.3, eq.
   ``sh2fs-escn``): rotate, multiply by the m = 0 filter, rotate back;
+* channel mixing: every pair product of two channel sets, combined with a
+  weight tensor;
 * the three stages of Sec. 3.2 individually: SH -> 2D Fourier (eq. ``sh-fs``),
   the 2D convolution (eq. ``2D-conv``) and Fourier -> SH (eq. ``fs-sh``), each
   from its plain definition;
@@ -493,6 +495,33 @@ def wigner_d_real(L: int, R: np.ndarray) -> np.ndarray:
     for l in range(L + 1):
         mask[l * l : (l + 1) ** 2, l * l : (l + 1) ** 2] = True
     return np.where(mask, D, 0.0)
+
+
+# ---------------------------------------------------------------------------
+# Channel mixing (Appendix, combination rules of features in different channels)
+# ---------------------------------------------------------------------------
+
+def channel_mix(x1, x2, W, L1: int, L2: int, Lout: int) -> np.ndarray:
+    """Channel-mixing combination of two multi-channel features:
+
+        y[b, co] = sum_{c1, c2} W[co, c1, c2] GTP(x1[b, c1], x2[b, c2]),
+
+    the O(C^2)-products rule of the appendix's discussion of channels.
+    x1[B, C1, (L1+1)^2], x2[B, C2, (L2+1)^2], W[Co, C1, C2]; returns
+    y[B, Co, (Lout+1)^2].  Every pair product is taken by ``gtp`` (or
+    ``gtp_grid`` above degree 8) and combined with its weight.
+    """
+    x1 = np.asarray(x1, dtype=np.float64)
+    x2 = np.asarray(x2, dtype=np.float64)
+    W = np.asarray(W, dtype=np.float64)
+    B, C1, _ = x1.shape
+    C2 = x2.shape[1]
+    prod = gtp if max(L1, L2, Lout) <= 8 else gtp_grid
+    T = np.empty((B, C1, C2, nsh(Lout)))
+    for c1 in range(C1):
+        a = np.repeat(x1[:, c1:c1 + 1, :], C2, axis=1)
+        T[:, c1] = prod(a, x2, L1, L2, Lout)
+    return np.einsum("oij,bijk->bok", W, T)
 
 
 # ---------------------------------------------------------------------------

@@ -323,6 +323,63 @@ gtp_status gtp_full_weighted(gtp_plan p, const void* x1, const void* x2, gtp_dty
   return run_product(p, x1, it, x2, it, n, y, static_cast<hipStream_t>(stream), "gtp_full_weighted launch", wt);
 }
 
+gtp_status gtp_channel_mix(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* W,
+                           int64_t B, int64_t C1, int64_t C2, int64_t Co, float* y, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  int64_t P = 0, nw = 0, n1 = 0, n2 = 0, no = 0, ex1 = 0, ex2 = 0, eo = 0, npair = 0;
+  if (B < 0 || C1 < 0 || C2 < 0 || Co < 0 || !mul_ok(C1, C2, &P) || !mul_ok(Co, P, &nw) || !mul_ok(B, C1, &n1) ||
+      !mul_ok(B, C2, &n2) || !mul_ok(B, Co, &no) || !mul_ok(B, P, &npair) || !mul_ok(n1, gtp::nsh(p->L1), &ex1) ||
+      !mul_ok(n2, gtp::nsh(p->L2), &ex2) || !mul_ok(no, gtp::nsh(p->Lout), &eo) || eo > INT64_MAX / 4 ||
+      nw > INT64_MAX / 4 || Co > 0x7fffffff)
+    return fail(GTP_ERR_INVALID_ARG, "sizes must be >= 0 and their products must fit in int64");
+  if (no == 0) return GTP_OK;
+  if (!y || (P > 0 && (!x1 || !x2 || !W))) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype), ny = size_t(eo) * 4;
+  if (P > 0 && (ranges_overlap(y, ny, x1, size_t(ex1) * es) || ranges_overlap(y, ny, x2, size_t(ex2) * es) ||
+                ranges_overlap(y, ny, W, size_t(nw) * 4)))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps an input or W");
+  if ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % es ||
+      (reinterpret_cast<uintptr_t>(W) | reinterpret_cast<uintptr_t>(y)) % 4)
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  const int K = gtp::nsh(p->Lout), K1 = gtp::nsh(p->L1), K2 = gtp::nsh(p->L2);
+  hipError_t e = hipSuccess;
+  if (P == 0) {  // no pair products: y = 0 (a fill kernel, not a memset node)
+    e = gtp::launch_fill_zero(y, eo, st);
+    return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_channel_mix launch");
+  }
+  // pair products of a chunk of batch entries in a stream-ordered workspace
+  // (at most 256 MiB), then the mix on the matrix cores
+  const int64_t per_b = P * K;
+  int64_t chunk = (int64_t(256) << 20) / 4 / per_b;
+  if (chunk < 1) chunk = 1;
+  if (chunk > B) chunk = B;
+  float* T = nullptr;
+  e = hipMallocAsync(reinterpret_cast<void**>(&T), size_t(chunk) * per_b * sizeof(float), st);
+  if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+  for (int64_t b0 = 0; b0 < B && e == hipSuccess; b0 += chunk) {
+    const int64_t nb = B - b0 < chunk ? B - b0 : chunk;
+    const char* a = static_cast<const char*>(x1) + size_t(b0) * C1 * K1 * es;
+    const char* c = static_cast<const char*>(x2) + size_t(b0) * C2 * K2 * es;
+    const gtp::PairIdx pi{C1, C2};
+    bool done = false;
+    if (!p->force_generic && p->conv != GTP_CONV_DIRECT)
+      e = gtp::launch_pairs_small(p->dev, a, it, c, it, nb * P, T, pi, st, &done);
+    if (!done) {
+      const gtp::DegWeights nw0{nullptr, nullptr, nullptr, 1, 0, 0, false};
+      e = gtp::launch_full_generic(p->dev, a, it, c, it, nb * P, T, 0, nw0, st, pi);
+    }
+    if (e == hipSuccess) e = gtp::launch_mix_gemm(W, T, y + size_t(b0) * Co * K, int(Co), P, K, nb, st);
+  }
+  const hipError_t e2 = hipFreeAsync(T, st);
+  if (e != hipSuccess) return hip_fail(e, "gtp_channel_mix launch");
+  return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
+}
+
 gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const float* r, const float* h, int64_t B,
                          int64_t C, float* y, void* stream) {
   gtp_status s = plan_check(p);

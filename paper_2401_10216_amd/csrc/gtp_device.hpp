@@ -50,6 +50,19 @@ struct DegWeights {
   bool on;
 };
 
+// Outer-product indexing of a batch of pair products (channel mixing):
+// product p = (b C1 + c1) C2 + c2 takes row b C1 + c1 of x1 and row b C2 + c2
+// of x2.  C2 = 0: plain indexing (product p takes row p of both).
+struct PairIdx {
+  int64_t C1, C2;
+};
+
+__device__ __forceinline__ void pair_rows(const PairIdx& q, int64_t p, int64_t& r1, int64_t& r2) {
+  const int64_t bc1 = p / q.C2;
+  r1 = bc1;
+  r2 = (bc1 / q.C1) * q.C2 + (p - bc1 * q.C2);
+}
+
 __device__ __forceinline__ int64_t weight_row(const DegWeights& w, int64_t p) {
   return w.per_channel ? (w.pbase + p) % w.C : 0;
 }
@@ -80,7 +93,19 @@ hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const v
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,
-                               int64_t n, float* y, int nu, const DegWeights& wt, hipStream_t s);
+                               int64_t n, float* y, int nu, const DegWeights& wt, hipStream_t s,
+                               const PairIdx& pi = PairIdx{0, 0});
+// All pair products T[b, c1, c2] = P_Lout(x1[b, c1] * x2[b, c2]) for n = B C1 C2
+// products (outer-product indexing) with the thread-per-product kernel, for
+// L1 = L2 = Lout <= 8 and equal input types; *supported = false otherwise.
+hipError_t launch_pairs_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                              float* y, const PairIdx& pi, hipStream_t s, bool* supported);
+// Channel mixing of pair products: y[b, co, k] = sum_p W[co, p] T[b, p, k],
+// p < P, k < K, for nb batch entries (fp32 matrix cores).
+hipError_t launch_mix_gemm(const float* W, const float* T, float* y, int Co, int64_t P, int K, int64_t nb,
+                           hipStream_t s);
+// y[0 .. n) = 0 with a kernel (safe inside captured graphs).
+hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s);
 // y[p, :(Lout+1)^2] = x[p, :(L+1)^2] truncated or zero-padded.
 hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
 // Direct 2D convolution of the real-form Fourier grids (the paper's eq.

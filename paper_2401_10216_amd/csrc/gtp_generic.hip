@@ -58,7 +58,7 @@ __host__ __device__ inline GenericLayout generic_layout(const DevTables& t, int 
 template <typename T1, typename T2>
 __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* __restrict__ x1,
                                                          const T2* __restrict__ x2, float* __restrict__ y,
-                                                         int64_t n, int nu, int JC, DegWeights wt) {
+                                                         int64_t n, int nu, int JC, DegWeights wt, PairIdx pi) {
   extern __shared__ float smem[];
   const GenericLayout g = generic_layout(t, nu, JC);
   const int tid = threadIdx.x;
@@ -75,10 +75,12 @@ __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* 
 
   for (int64_t p = blockIdx.x; p < n; p += gridDim.x) {
     const int64_t wrow = weight_row(wt, p);
+    int64_t r1 = p, r2 = p;
+    if (pi.C2) pair_rows(pi, p, r1, r2);
     for (int i = tid; i < g.K1; i += kBlock)
-      xs1[i] = ld_in(x1, p * g.K1 + i) * (wt.w1 ? wt.w1[wrow * (t.L1 + 1) + degree_of(i)] : 1.0f);
+      xs1[i] = ld_in(x1, r1 * g.K1 + i) * (wt.w1 ? wt.w1[wrow * (t.L1 + 1) + degree_of(i)] : 1.0f);
     for (int i = tid; i < g.K2; i += kBlock)
-      xs2[i] = ld_in(x2, p * g.K2 + i) * (wt.w2 ? wt.w2[wrow * (t.L2 + 1) + degree_of(i)] : 1.0f);
+      xs2[i] = ld_in(x2, r2 * g.K2 + i) * (wt.w2 ? wt.w2[wrow * (t.L2 + 1) + degree_of(i)] : 1.0f);
     float acc[kMaxOut];
 #pragma unroll
     for (int q = 0; q < kMaxOut; ++q) acc[q] = 0.0f;
@@ -476,7 +478,7 @@ int generic_chunk(const DevTables& t, int nu, size_t* lds_bytes) {
 }
 
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2, int64_t n,
-                               float* y, int nu, const DegWeights& wt, hipStream_t s) {
+                               float* y, int nu, const DegWeights& wt, hipStream_t s, const PairIdx& pi) {
   size_t lds = 0;
   const int JC = generic_chunk(t, nu, &lds);
   const dim3 grid(grid_for(n, 1)), block(kBlock);
@@ -484,16 +486,16 @@ hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, co
   using u16 = uint16_t;
   if (b1 && b2)
     hipLaunchKernelGGL((k_full_generic<u16, u16>), grid, block, lds, s, t, static_cast<const u16*>(x1),
-                       static_cast<const u16*>(x2), y, n, nu, JC, wt);
+                       static_cast<const u16*>(x2), y, n, nu, JC, wt, pi);
   else if (b1)
     hipLaunchKernelGGL((k_full_generic<u16, float>), grid, block, lds, s, t, static_cast<const u16*>(x1),
-                       static_cast<const float*>(x2), y, n, nu, JC, wt);
+                       static_cast<const float*>(x2), y, n, nu, JC, wt, pi);
   else if (b2)
     hipLaunchKernelGGL((k_full_generic<float, u16>), grid, block, lds, s, t, static_cast<const float*>(x1),
-                       static_cast<const u16*>(x2), y, n, nu, JC, wt);
+                       static_cast<const u16*>(x2), y, n, nu, JC, wt, pi);
   else
     hipLaunchKernelGGL((k_full_generic<float, float>), grid, block, lds, s, t, static_cast<const float*>(x1),
-                       static_cast<const float*>(x2), y, n, nu, JC, wt);
+                       static_cast<const float*>(x2), y, n, nu, JC, wt, pi);
   return hipGetLastError();
 }
 

@@ -426,34 +426,13 @@ constexpr int kTile = 64;  // products per workgroup (one wave)
 // stay in registers, so the budget shrinks with the degree.
 constexpr int small_waves(int L1, int L2, int LO) { return (L1 > 6 || L2 > 6 || LO > 6) ? 2 : 3; }
 
-// Coalesced read of a workgroup's kTile x K slab (lane-contiguous), every
-// load issued before the first wait.
+// Row tid (product p0 + tid, the last one for lanes past the end) of x into
+// registers, each lane loading its own row.
 template <int K, typename TIn>
-__device__ __forceinline__ void fetch_slab(const TIn* __restrict__ x, int64_t p0, int cnt, float (&v)[K]) {
+__device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0, int cnt, float (&r)[K]) {
   const int tid = threadIdx.x;
-  const int64_t base = p0 * K;
-  sfor<0, K>([&](auto I) {
-    constexpr int k = decltype(I)::value;
-    const int i = tid + k * kTile;
-    v[k] = (i < cnt * K) ? ld_in(x, base + i) : 0.0f;
-  });
-}
-template <int K>
-__device__ __forceinline__ void slab_to_tile(const float (&v)[K], float* tile) {
-  sfor<0, K>([&](auto I) { tile[threadIdx.x + decltype(I)::value * kTile] = v[decltype(I)::value]; });
-}
-
-// The slab into per-lane rows (row tid = product p0 + tid) through the LDS tile.
-template <int K, typename TIn>
-__device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0, int cnt, float* tile,
-                                          float (&r)[K]) {
-  const int tid = threadIdx.x;
-  float v[K];
-  fetch_slab<K>(x, p0, cnt, v);
-  slab_to_tile<K>(v, tile);
-  __syncthreads();
-  sfor<0, K>([&](auto I) { r[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
-  __syncthreads();
+  const TIn* const xr = x + (p0 + (tid < cnt ? tid : cnt - 1)) * K;
+  sfor<0, K>([&](auto I) { r[decltype(I)::value] = ld_in(xr, decltype(I)::value); });
 }
 
 template <int KO, int KE>
@@ -478,11 +457,12 @@ __device__ __forceinline__ void scale_by_degree(const float* __restrict__ wrow, 
   sfor<0, K>([&](auto I) { at(I) *= wl[cdeg(decltype(I)::value)]; });
 }
 
-template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT>
+template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT, bool OUT>
 __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const T1* __restrict__ x1, const T2* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
                                                       const float* __restrict__ ST, int ntS,
-                                                      const float* __restrict__ WT, int ntW, DegWeights wt) {
+                                                      const float* __restrict__ WT, int ntW, DegWeights wt,
+                                                      PairIdx pi) {
   using G = Geo<L1, L2, LO, NU>;
   constexpr int K1 = csh(L1), K2 = NU == 0 ? csh(L2) : 1, KO = csh(LO);
   constexpr int KT = cmax(cmax(K1, K2), KO);
@@ -493,18 +473,18 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
   float xa[K1];
   float acc[G::KE];
   if constexpr (NU == 0) {
-    // both slabs requested before the first wait; x1 into registers through
-    // the tile, then x2 stays in LDS, row-major with an odd row length
-    // (conflict-free reads)
-    float v1[K1], v2[K2];
-    fetch_slab<K1>(x1, p0, cnt, v1);
-    fetch_slab<K2>(x2, p0, cnt, v2);
-    slab_to_tile<K1>(v1, tile);
-    __syncthreads();
-    sfor<0, K1>([&](auto I) { xa[decltype(I)::value] = tile[tid * K1 + decltype(I)::value]; });
-    __syncthreads();
-    slab_to_tile<K2>(v2, tile);
-    __syncthreads();
+    // each lane loads its own two rows, x1 into registers and x2 into its
+    // tile row (row-major, odd row length: conflict-free reads); a wave's
+    // rows are contiguous, so every cache line still comes from HBM once.
+    // Lanes past the end repeat the last product.  Outer-product indexing
+    // (pair products of channel mixing) takes rows b C1 + c1 and b C2 + c2.
+    const int64_t p = p0 + (tid < cnt ? tid : cnt - 1);
+    int64_t r1 = p, r2 = p;
+    if constexpr (OUT) pair_rows(pi, p, r1, r2);
+    const T1* const xr1 = x1 + r1 * K1;
+    const T2* const xr2 = x2 + r2 * K2;
+    sfor<0, K1>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
+    sfor<0, K2>([&](auto I) { tile[tid * K2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
     if constexpr (WGT) {
       // each lane scales its own product: x1 in registers, x2 in its tile row
       const int64_t row = weight_row(wt, p0 + tid);
@@ -525,7 +505,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     }
     __syncthreads();
   } else {
-    load_rows<K1>(x1, p0, cnt, tile, xa);
+    load_rows<K1>(x1, p0, cnt, xa);
     RegX<K1> A{xa};
     gtp_core<L1, L2, LO, NU>(A, A, acc, ST, ntS, WT, ntW);
   }
@@ -544,7 +524,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float a[K];
-  load_rows<K>(x, p0, cnt, tile, a);
+  load_rows<K>(x, p0, cnt, a);
   float b[KO];
   {
     float acc[G1::KE];
@@ -568,12 +548,12 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   store_rows<KO, KO>(y, p0, cnt, tile, b);
 }
 
-template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT>
+template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT, bool OUT = false>
 hipError_t launch_typed(const DevTables& t, const void* x1, const void* x2, int64_t n, float* y,
-                        const DegWeights& wt, hipStream_t s) {
+                        const DegWeights& wt, hipStream_t s, const PairIdx& pi = PairIdx{0, 0}) {
   const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
-  hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, T1, T2, WGT>), grid, block, 0, s, static_cast<const T1*>(x1),
-                     static_cast<const T2*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW, wt);
+  hipLaunchKernelGGL((k_full_small<L1, L2, LO, NU, T1, T2, WGT, OUT>), grid, block, 0, s, static_cast<const T1*>(x1),
+                     static_cast<const T2*>(x2), y, n, t.ST, t.ntS, t.WT, t.ntW, wt, pi);
   return hipGetLastError();
 }
 
@@ -601,6 +581,18 @@ hipError_t launch_one(const DevTables& t, const void* x1, int it1, const void* x
     if (it1 == IN_F32 && it2 == IN_BF16)
       return launch_typed<L1, L2, LO, NU, float, uint16_t, false>(t, x1, x2, n, y, wt, s);
   }
+  *supported = false;
+  return hipSuccess;
+}
+
+// Outer-product pair products (channel mixing), equal degrees, equal types.
+template <int L>
+hipError_t launch_pairs_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                            float* y, const PairIdx& pi, hipStream_t s, bool* supported) {
+  const DegWeights nw{nullptr, nullptr, nullptr, 1, 0, 0, false};
+  if (it1 == IN_F32 && it2 == IN_F32) return launch_typed<L, L, L, 0, float, float, false, true>(t, x1, x2, n, y, nw, s, pi);
+  if (it1 == IN_BF16 && it2 == IN_BF16)
+    return launch_typed<L, L, L, 0, uint16_t, uint16_t, false, true>(t, x1, x2, n, y, nw, s, pi);
   *supported = false;
   return hipSuccess;
 }
@@ -643,6 +635,26 @@ hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const 
     return launch_one<a, 0, c, v>(t, x1, it1, x1, it1, n, y, wt, s, supported);
     GTP_SMALL_POWERS(GTP_CASE)
 #undef GTP_CASE
+  }
+  *supported = false;
+  return hipSuccess;
+}
+
+hipError_t launch_pairs_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
+                              float* y, const PairIdx& pi, hipStream_t s, bool* supported) {
+  *supported = true;
+  if (t.L1 == t.L2 && t.L2 == t.Lout) {
+    switch (t.L1) {
+      case 1: return launch_pairs_one<1>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 2: return launch_pairs_one<2>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 3: return launch_pairs_one<3>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 4: return launch_pairs_one<4>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 5: return launch_pairs_one<5>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 6: return launch_pairs_one<6>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 7: return launch_pairs_one<7>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      case 8: return launch_pairs_one<8>(t, x1, it1, x2, it2, n, y, pi, s, supported);
+      default: break;
+    }
   }
   *supported = false;
   return hipSuccess;

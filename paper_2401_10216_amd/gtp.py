@@ -47,6 +47,7 @@ _SIGS = {
     "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
     "gtp_full_weighted": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_conv_escn": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
+    "gtp_channel_mix": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _I64, _I64, _P, _P]),
     "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
     "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
     "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
@@ -161,6 +162,26 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
                           _stream(stream)))
+    return y
+
+
+def gtp_channel_mix(plan: Plan, x1, x2, W, y=None, stream=None):
+    """y[B,Co,(Lout+1)^2] = sum_{c1,c2} W[co,c1,c2] GTP(x1[:,c1], x2[:,c2]); W float32 [Co, C1, C2]."""
+    import torch
+    if x1.dtype != x2.dtype:
+        raise TypeError("x1 and x2 must have the same dtype")
+    if x1.dim() != 3 or x2.dim() != 3 or x1.shape[0] != x2.shape[0]:
+        raise ValueError("x1 [B, C1, K1] and x2 [B, C2, K2] with equal B")
+    if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2):
+        raise ValueError("coefficient dimension does not match the plan")
+    B, C1, C2 = int(x1.shape[0]), int(x1.shape[1]), int(x2.shape[1])
+    if W.dim() != 3 or tuple(W.shape[1:]) != (C1, C2) or W.dtype != torch.float32:
+        raise ValueError("W must be float32 [Co, C1, C2]")
+    Co = int(W.shape[0])
+    if y is None:
+        y = torch.empty((B, Co, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
+    _check(lib().gtp_channel_mix(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), _dev(W, "W"), B, C1,
+                                 C2, Co, _dev(y, "y"), _stream(stream)))
     return y
 
 

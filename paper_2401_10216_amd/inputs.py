@@ -20,8 +20,10 @@ Workloads (the paper ships no data; these stand in for its benchmarks):
   * ``sweep``     : B*C = 262144 vectors ([2048, 128]), L1=L2=Lout=L in
                     {4, 8, 16, 32, 64}, iid N(0,1).
   * ``highdeg``   : B=32768, C=64, L1=L2=Lout=16, inputs rounded to bf16.
+  * ``mix``       : channel mixing, B=8192, C1=C2=Co=32, L=6: x1, x2 ~ N(0,1),
+                    W ~ N(0, 1/C^2) (the O(C^2)-products combination rule).
 
-Seeds: numpy PCG64 with seed 1000 + workload index (1..5); subsample indices use
+Seeds: numpy PCG64 with seed 1000 + workload index (1..6); subsample indices use
 seed + 100.
 """
 from __future__ import annotations
@@ -34,6 +36,7 @@ WORKLOADS = {
     "manybody": dict(index=3, B=1728, C=256, L=2, nu=3, Lout=3),
     "sweep": dict(index=4, B=2048, C=128, Ls=(4, 8, 16, 32, 64)),
     "highdeg": dict(index=5, B=32768, C=64, L1=16, L2=16, Lout=16),
+    "mix": dict(index=6, B=8192, C=32, L1=6, L2=6, Lout=6),
 }
 
 
@@ -112,6 +115,16 @@ def highdeg_inputs(B: int = 32768, C: int = 64, L: int = 16, index: int = 5):
     b1, v1 = round_to_bf16(x1)
     b2, v2 = round_to_bf16(x2)
     return b1, b2, v1, v2
+
+
+def mix_inputs(B: int = 8192, C: int = 32, L: int = 6, index: int = 6):
+    """Channel-mixing workload: x1, x2 [B, C, (L+1)^2] ~ N(0,1) and a weight
+    tensor W [C, C, C] ~ N(0, 1 / C^2)."""
+    rng = rng_for(index)
+    x1 = normal(rng, (B, C, nsh(L)))
+    x2 = normal(rng, (B, C, nsh(L)))
+    W = normal(rng, (C, C, C)) / np.float32(C)
+    return x1, x2, W
 
 
 def output_gradient(index: int, shape) -> np.ndarray:

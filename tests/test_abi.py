@@ -218,6 +218,30 @@ def test_weighted_validation(L):
     assert b"HOST_ONLY" in L.gtp_last_error()
 
 
+def test_channel_mix_validation(L):
+    p = host_plan(2, 2, 2)
+    H = p.handle
+    x1, x2, W, y = fake(0x100000), fake(0x200000), fake(0x300000), fake(0x400000)
+    S = ctypes.c_void_p(0)
+    INV, OK = gtp.GTP_ERR_INVALID_ARG, gtp.GTP_OK
+    f = L.gtp_channel_mix
+    assert f(None, x1, x2, 0, W, 4, 3, 5, 2, y, S) == INV
+    assert f(H, x1, x2, 4, W, 4, 3, 5, 2, y, S) == INV  # bad dtype
+    assert f(H, x1, x2, 0, W, -1, 3, 5, 2, y, S) == INV
+    assert f(H, x1, x2, 0, W, 4, 3, -5, 2, y, S) == INV
+    assert f(H, x1, x2, 0, W, 4, 1 << 40, 1 << 40, 2, y, S) == INV  # C1 C2 overflow
+    assert f(H, x1, x2, 0, None, 4, 3, 5, 2, y, S) == INV  # W needed when C1 C2 > 0
+    assert f(H, None, x2, 0, W, 4, 3, 5, 2, y, S) == INV
+    assert f(H, x1, x2, 0, W, 4, 3, 5, 2, None, S) == INV
+    assert f(H, x1, x2, 0, W, 4, 3, 5, 2, fake(0x300000 + 8), S) == INV  # y overlaps W
+    assert f(H, x1, x2, 0, W, 4, 3, 5, 2, fake(0x100000 + 4), S) == INV  # y overlaps x1
+    assert f(H, x1, x2, 0, fake(0x300002), 4, 3, 5, 2, y, S) == INV  # misaligned
+    assert f(H, x1, x2, 0, W, 0, 3, 5, 2, y, S) == OK  # empty batch
+    assert f(H, x1, x2, 0, W, 4, 3, 5, 0, y, S) == OK  # no output channels
+    assert f(H, None, None, 0, None, 4, 0, 5, 2, y, S) == INV  # C1 = 0: zeros, but the plan is host-only
+    assert b"HOST_ONLY" in L.gtp_last_error()
+
+
 def test_stage_validation(L):
     p = host_plan(2, 3, 2)
     H = p.handle

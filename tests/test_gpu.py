@@ -625,3 +625,50 @@ def test_conv_escn_edge_workload_sampled():
     err = O.max_rel_err(y.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy(), ref)
     _say(f"  err={err:.3e}")
     assert err <= TOL, err
+
+
+# ------------------------------------------------------------------ channel mixing
+
+MIX = [(2, 2, 2, 4, 4, 4, 37), (4, 4, 4, 5, 7, 3, 19), (6, 6, 6, 8, 8, 8, 11), (8, 8, 8, 3, 4, 17, 5),
+       (2, 3, 4, 4, 3, 5, 9), (6, 6, 6, 32, 32, 32, 3)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout,C1,C2,Co,B", MIX)
+def test_channel_mix(L1, L2, Lout, C1, C2, Co, B):
+    rng = np.random.default_rng(170 + L1 + C1 + Co)
+    x1 = rng.standard_normal((B, C1, O.nsh(L1))).astype(np.float32)
+    x2 = rng.standard_normal((B, C2, O.nsh(L2))).astype(np.float32)
+    W = (rng.standard_normal((Co, C1, C2)) / math.sqrt(C1 * C2)).astype(np.float32)
+    _say(f"channel_mix L=({L1},{L2},{Lout}) C1={C1} C2={C2} Co={Co} B={B}")
+    y = gtp.gtp_channel_mix(gtp.Plan(L1, L2, Lout), dev(x1), dev(x2), dev(W))
+    torch.cuda.synchronize()
+    ref = O.channel_mix(x1, x2, W, L1, L2, Lout)
+    err = O.max_rel_err(y.cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_channel_mix_generic_bf16_and_degenerate():
+    L, B, C1, C2, Co = 4, 7, 6, 5, 4
+    rng = np.random.default_rng(180)
+    bits1, v1 = inputs.round_to_bf16(rng.standard_normal((B, C1, O.nsh(L))).astype(np.float32))
+    bits2, v2 = inputs.round_to_bf16(rng.standard_normal((B, C2, O.nsh(L))).astype(np.float32))
+    W = rng.standard_normal((Co, C1, C2)).astype(np.float32)
+    ref = O.channel_mix(v1, v2, W, L, L, L)
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    for flags in (0, gtp.GTP_FORCE_GENERIC):
+        _say(f"channel_mix bf16 flags={flags}")
+        y = gtp.gtp_channel_mix(gtp.Plan(L, L, L, flags), t1, t2, dev(W))
+        torch.cuda.synchronize()
+        assert O.max_rel_err(y.cpu().numpy(), ref) <= TOL
+    # no input channels: zeros; no batch: nothing
+    _say("channel_mix degenerate")
+    y = torch.full((B, Co, O.nsh(L)), 7.0, device="cuda:0")
+    gtp.gtp_channel_mix(gtp.Plan(L, L, L), torch.empty((B, 0, O.nsh(L)), device="cuda:0"),
+                        dev(v2.astype(np.float32)), torch.empty((Co, 0, C2), device="cuda:0"), y=y)
+    torch.cuda.synchronize()
+    assert float(y.abs().max()) == 0.0
+    z = gtp.gtp_channel_mix(gtp.Plan(L, L, L), torch.empty((0, C1, O.nsh(L)), device="cuda:0"),
+                            torch.empty((0, C2, O.nsh(L)), device="cuda:0"), dev(W))
+    assert z.shape == (0, Co, O.nsh(L))

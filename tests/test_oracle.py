@@ -610,6 +610,46 @@ def test_weighted_sum_equals_scaled_route():
     assert np.abs(ys - yc).max() < 1e-12
 
 
+# --------------------------------------------------------------------------- channel mixing
+
+def test_channel_mix_diagonal_weights_are_channel_wise():
+    """W[co, c1, c2] = d(co, c1) d(co, c2) reduces to the channel-wise product."""
+    rng = np.random.default_rng(80)
+    B, C, L = 3, 4, 2
+    x1 = rng.standard_normal((B, C, O.nsh(L)))
+    x2 = rng.standard_normal((B, C, O.nsh(L)))
+    W = np.zeros((C, C, C))
+    for c in range(C):
+        W[c, c, c] = 1.0
+    assert np.abs(O.channel_mix(x1, x2, W, L, L, L) - O.gtp(x1, x2, L, L, L)).max() < 1e-13
+
+
+def test_channel_mix_rank_one_weights():
+    """W = u (x) v (x) w: y[co] = u[co] GTP(sum_c1 v[c1] x1[c1], sum_c2 w[c2] x2[c2]) (bilinearity)."""
+    rng = np.random.default_rng(81)
+    B, C1, C2, Co, L1, L2, Lo = 2, 3, 5, 4, 2, 3, 3
+    x1 = rng.standard_normal((B, C1, O.nsh(L1)))
+    x2 = rng.standard_normal((B, C2, O.nsh(L2)))
+    u, v, w = rng.standard_normal(Co), rng.standard_normal(C1), rng.standard_normal(C2)
+    W = np.einsum("o,i,j->oij", u, v, w)
+    a = np.einsum("i,bik->bk", v, x1)
+    b = np.einsum("j,bjk->bk", w, x2)
+    want = u[None, :, None] * O.gtp(a, b, L1, L2, Lo)[:, None, :]
+    assert np.abs(O.channel_mix(x1, x2, W, L1, L2, Lo) - want).max() < 1e-12
+
+
+def test_channel_mix_single_pair_picks_one_product():
+    rng = np.random.default_rng(82)
+    B, C1, C2, Co, L = 2, 3, 2, 2, 3
+    x1 = rng.standard_normal((B, C1, O.nsh(L)))
+    x2 = rng.standard_normal((B, C2, O.nsh(L)))
+    W = np.zeros((Co, C1, C2))
+    W[1, 2, 0] = -2.5
+    y = O.channel_mix(x1, x2, W, L, L, L)
+    assert np.abs(y[:, 0]).max() == 0.0
+    assert np.abs(y[:, 1] + 2.5 * O.gtp(x1[:, 2], x2[:, 0], L, L, L)).max() < 1e-13
+
+
 # --------------------------------------------------------------------------- rotated-frame convolution
 
 def _filter(h, r, L2):
