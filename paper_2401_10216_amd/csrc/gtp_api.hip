@@ -352,15 +352,19 @@ gtp_status gtp_channel_mix(gtp_plan p, const void* x1, const void* x2, gtp_dtype
     e = gtp::launch_fill_zero(y, eo, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_channel_mix launch");
   }
-  // pair products of a chunk of batch entries in a stream-ordered workspace
-  // (at most 256 MiB), then the mix on the matrix cores
-  const int64_t per_b = P * K;
+  // the transposed weights, then the pair products of a chunk of batch
+  // entries (at most 256 MiB) in a stream-ordered workspace, then the mix on
+  // the matrix cores
+  const int64_t per_b = P * K, nwt = P * gtp::mix_cop(int(Co));
   int64_t chunk = (int64_t(256) << 20) / 4 / per_b;
   if (chunk < 1) chunk = 1;
   if (chunk > B) chunk = B;
-  float* T = nullptr;
-  e = hipMallocAsync(reinterpret_cast<void**>(&T), size_t(chunk) * per_b * sizeof(float), st);
+  float* ws = nullptr;
+  e = hipMallocAsync(reinterpret_cast<void**>(&ws), (size_t(chunk) * per_b + size_t(nwt)) * sizeof(float), st);
   if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+  float* const WT = ws;
+  float* const T = ws + nwt;
+  e = gtp::launch_mix_transpose(W, WT, int(Co), P, st);
   for (int64_t b0 = 0; b0 < B && e == hipSuccess; b0 += chunk) {
     const int64_t nb = B - b0 < chunk ? B - b0 : chunk;
     const char* a = static_cast<const char*>(x1) + size_t(b0) * C1 * K1 * es;
@@ -373,9 +377,9 @@ gtp_status gtp_channel_mix(gtp_plan p, const void* x1, const void* x2, gtp_dtype
       const gtp::DegWeights nw0{nullptr, nullptr, nullptr, 1, 0, 0, false};
       e = gtp::launch_full_generic(p->dev, a, it, c, it, nb * P, T, 0, nw0, st, pi);
     }
-    if (e == hipSuccess) e = gtp::launch_mix_gemm(W, T, y + size_t(b0) * Co * K, int(Co), P, K, nb, st);
+    if (e == hipSuccess) e = gtp::launch_mix_gemm(WT, T, y + size_t(b0) * Co * K, int(Co), P, K, nb, st);
   }
-  const hipError_t e2 = hipFreeAsync(T, st);
+  const hipError_t e2 = hipFreeAsync(ws, st);
   if (e != hipSuccess) return hip_fail(e, "gtp_channel_mix launch");
   return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
 }

@@ -101,8 +101,12 @@ hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, co
 hipError_t launch_pairs_small(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                               float* y, const PairIdx& pi, hipStream_t s, bool* supported);
 // Channel mixing of pair products: y[b, co, k] = sum_p W[co, p] T[b, p, k],
-// p < P, k < K, for nb batch entries (fp32 matrix cores).
-hipError_t launch_mix_gemm(const float* W, const float* T, float* y, int Co, int64_t P, int K, int64_t nb,
+// p < P, k < K, for nb batch entries (fp32 matrix cores), from the
+// transposed copy WT[p][co] (mix_cop(Co) columns, made by
+// launch_mix_transpose).
+int mix_cop(int Co);
+hipError_t launch_mix_transpose(const float* W, float* WT, int Co, int64_t P, hipStream_t s);
+hipError_t launch_mix_gemm(const float* WT, const float* T, float* y, int Co, int64_t P, int K, int64_t nb,
                            hipStream_t s);
 // y[0 .. n) = 0 with a kernel (safe inside captured graphs).
 hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s);

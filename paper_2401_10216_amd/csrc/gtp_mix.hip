@@ -3,13 +3,16 @@
 // The channel-mixing combination of the appendix's discussion of channels,
 // y[b, co] = sum_{c1, c2} W[co, c1, c2] GTP(x1[b, c1], x2[b, c2]), is linear in
 // the pair products T[b, p] = GTP(x1[b, c1], x2[b, c2]) (p = c1 C2 + c2), so
-// after the products it is one matrix product per batch entry:
-//     y_b (Co x K) = W (Co x P) T_b (P x K),   P = C1 C2.
-// One wave computes a 16 x 64 tile of y_b with v_mfma_f32_16x16x4f32: in
-// K-step s the A operand of lane 16 g + i is W[co0 + i][4 s + g], the B
-// operand of block nb is T_b[4 s + g][n0 + 16 nb + i]; D register r of lane
-// 16 g + i is y_b[co0 + 4 g + r][n0 + 16 nb + i].  The operands of the next
-// K-step are loaded before the current one's matrix instructions.
+// after the products it is one matrix product per batch entry,
+//     y_b^T (K x Co) = T_b^T (K x P) W^T (P x Co),   P = C1 C2,
+// taken with v_mfma_f32_16x16x4f32 (A[i][k] from lane 16 k + i, B[k][j] from
+// lane 16 k + j, D register r of lane 16 g + i = row 4 g + r, column i).
+// One wave computes a 16 (k) x 32 (co) tile: in K-step s the A operand of
+// lane 16 g + i is T_b[4 s + g][n0 + i] and the B operands are
+// W^T[4 s + g][co0 + i] and [co0 + 16 + i], all rows read as contiguous
+// 64-byte runs (W^T is a transposed copy made once per call).  The operands
+// of the next 8 K-steps are loaded before the current 8 K-steps' matrix
+// instructions.
 #include "gtp_device.hpp"
 
 namespace gtp {
@@ -17,59 +20,77 @@ namespace {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
-constexpr int kNB = 4;  // 16-column blocks per wave (64 columns)
+constexpr int kCB = 2;  // 16-column blocks of output channels per wave
+constexpr int kKB = 8;  // K-steps (4 rows of P each) per loaded block
 
-__global__ __launch_bounds__(64) void k_mix_gemm(const float* __restrict__ W, const float* __restrict__ T,
-                                                 float* __restrict__ y, int Co, int64_t P, int K, int ncot,
-                                                 int nnt) {
+// WT[p][co] = W[co][p], co < CoP (columns past Co are zero)
+__global__ __launch_bounds__(256) void k_mix_transpose(const float* __restrict__ W, float* __restrict__ WT, int Co,
+                                                       int CoP, int64_t P) {
+  const int64_t total = P * CoP;
+  for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int64_t p = e / CoP;
+    const int co = int(e - p * CoP);
+    WT[e] = co < Co ? W[int64_t(co) * P + p] : 0.0f;
+  }
+}
+
+__global__ __launch_bounds__(64) void k_mix_gemm(const float* __restrict__ WT, const float* __restrict__ T,
+                                                 float* __restrict__ y, int Co, int CoP, int64_t P, int K, int nnt,
+                                                 int nct) {
   const int lane = threadIdx.x, g = lane >> 4, i = lane & 15;
-  const int64_t b = blockIdx.x / (int64_t(ncot) * nnt);
-  const int rem = int(blockIdx.x % (int64_t(ncot) * nnt));
-  const int co0 = (rem / nnt) * 16, n0 = (rem % nnt) * (16 * kNB);
+  const int64_t b = blockIdx.x / (int64_t(nnt) * nct);
+  const int rem = int(blockIdx.x % (int64_t(nnt) * nct));
+  const int n0 = (rem / nct) * 16, co0 = (rem % nct) * (16 * kCB);
   const float* Tb = T + b * P * K;
-  const int arow = co0 + i;
-  const bool aok = arow < Co;
-  const float* Wr = W + int64_t(aok ? arow : 0) * P;
-  bool bok[kNB];
-  int bcol[kNB];
+  const int acol = n0 + i;  // row of y_b^T (coefficient index)
+  const bool aok = acol < K;
+  f4v acc[kCB];
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    bcol[nb] = n0 + 16 * nb + i;
-    bok[nb] = bcol[nb] < K;
-  }
-  f4v acc[kNB];
-#pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) acc[nb] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
-  // operands of K-step s (rows p = 4 s + g; zero past P, Co or K)
-  auto load = [&](int64_t s, float& a, float (&bv)[kNB]) {
-    const int64_t p = 4 * s + g;
-    const bool pok = p < P;
-    a = (aok && pok) ? Wr[p] : 0.0f;
-    const float* Tp = Tb + (pok ? p : 0) * K;
-#pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) bv[nb] = (pok && bok[nb]) ? Tp[bcol[nb]] : 0.0f;
+  for (int cb = 0; cb < kCB; ++cb) acc[cb] = f4v{0.0f, 0.0f, 0.0f, 0.0f};
+  // operands of K-step s (rows p = 4 s + g; zero past P or K; the W^T
+  // columns past Co are zero in the copy), a block of kKB K-steps at a time;
+  // the next block's loads are issued before this block's matrix instructions
+  struct Blk {
+    float a[kKB], b[kKB][kCB];
   };
-  const int64_t steps = (P + 3) / 4;
-  float a, bv[kNB];
-  load(0, a, bv);
-  for (int64_t s = 0; s < steps; ++s) {
-    float an = 0.0f, bn[kNB];
+  auto load = [&](int64_t blk, Blk& o) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) bn[nb] = 0.0f;
-    if (s + 1 < steps) load(s + 1, an, bn);
+    for (int t = 0; t < kKB; ++t) {
+      const int64_t p = 4 * (blk * kKB + t) + g;
+      const bool pok = p < P;
+      const int64_t pr = pok ? p : 0;
+      o.a[t] = (aok && pok) ? Tb[pr * K + acol] : 0.0f;
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[nb], acc[nb], 0, 0, 0);
-    a = an;
+      for (int cb = 0; cb < kCB; ++cb) o.b[t][cb] = pok ? WT[pr * CoP + co0 + 16 * cb + i] : 0.0f;
+    }
+  };
+  auto mma = [&](const Blk& o) {
 #pragma unroll
-    for (int nb = 0; nb < kNB; ++nb) bv[nb] = bn[nb];
+    for (int t = 0; t < kKB; ++t)
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(o.a[t], o.b[t][cb], acc[cb], 0, 0, 0);
+  };
+  const int64_t nblk = (P + 4 * kKB - 1) / (4 * kKB);
+  Blk b0, b1;
+  load(0, b0);
+  for (int64_t blk = 0; blk < nblk; blk += 2) {
+    if (blk + 1 < nblk) load(blk + 1, b1);
+    mma(b0);
+    if (blk + 1 < nblk) {
+      if (blk + 2 < nblk) load(blk + 2, b0);
+      mma(b1);
+    }
   }
+  // D[n][co]: lane 16 g + i holds n = n0 + 4 g + r, co = co0 + 16 cb + i
   float* yb = y + b * int64_t(Co) * K;
 #pragma unroll
-  for (int nb = 0; nb < kNB; ++nb) {
-    if (!bok[nb]) continue;
+  for (int cb = 0; cb < kCB; ++cb) {
+    const int co = co0 + 16 * cb + i;
+    if (co >= Co) continue;
+#pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = co0 + 4 * g + r;
-      if (row < Co) yb[int64_t(row) * K + bcol[nb]] = acc[nb][r];
+      const int n = n0 + 4 * g + r;
+      if (n < K) yb[int64_t(co) * K + n] = acc[cb][r];
     }
   }
 }
@@ -80,6 +101,8 @@ __global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_
 
 }  // namespace
 
+int mix_cop(int Co) { return (Co + 16 * kCB - 1) / (16 * kCB) * (16 * kCB); }
+
 hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   int64_t g = (n + 255) / 256;
@@ -88,13 +111,23 @@ hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_mix_gemm(const float* W, const float* T, float* y, int Co, int64_t P, int K, int64_t nb,
+hipError_t launch_mix_transpose(const float* W, float* WT, int Co, int64_t P, hipStream_t s) {
+  const int CoP = mix_cop(Co);
+  int64_t g = (P * CoP + 255) / 256;
+  if (g > 65536) g = 65536;
+  if (g < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_mix_transpose, dim3(unsigned(g)), dim3(256), 0, s, W, WT, Co, CoP, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_mix_gemm(const float* WT, const float* T, float* y, int Co, int64_t P, int K, int64_t nb,
                            hipStream_t s) {
   if (nb <= 0) return hipSuccess;
-  const int ncot = (Co + 15) / 16, nnt = (K + 16 * kNB - 1) / (16 * kNB);
-  const int64_t grid = nb * ncot * nnt;
+  const int CoP = mix_cop(Co);
+  const int nnt = (K + 15) / 16, nct = CoP / (16 * kCB);
+  const int64_t grid = nb * nnt * nct;
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(k_mix_gemm, dim3(unsigned(grid)), dim3(64), 0, s, W, T, y, Co, P, K, ncot, nnt);
+  hipLaunchKernelGGL(k_mix_gemm, dim3(unsigned(grid)), dim3(64), 0, s, WT, T, y, Co, CoP, P, K, nnt, nct);
   return hipGetLastError();
 }
 
