@@ -100,8 +100,8 @@ def dominant_kernel(workload: str, L: int, escn: bool = False):
         # both kernels of the step (rotation matrices, then the product): one unit
         return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
     if workload == "mix":
-        # pair products (thread per product) then the mix on the matrix cores: one unit
-        return "k_full_small(pairs)+k_mix_gemm", "alu", "gtp_mix.hip"
+        # pair products (thread per product) and the mix on the matrix cores in one kernel
+        return "k_mix_fused", "alu", "gtp_small.hip"
     if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
         return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
     if workload == "manybody":

@@ -36,13 +36,38 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found")
 
 
+GEN = os.path.join(BUILD, "gen")
+
+
+def generate_constants(verbose: bool = False) -> None:
+    """Compile and run the generator of the compile-time tables of the
+    thread-per-product kernels (from the library's own fp64 table builder)."""
+    os.makedirs(GEN, exist_ok=True)
+    exe = os.path.join(BUILD, "gen_small_consts")
+    cmd = ["g++", *CXX_FLAGS, "-o", exe, os.path.join(CSRC, "gen_small_consts.cpp"),
+           os.path.join(CSRC, "gtp_tables.cpp")]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if verbose or r.returncode:
+        print(" ".join(cmd))
+        print(r.stdout, r.stderr)
+    if r.returncode:
+        raise RuntimeError("generator build failed")
+    out = os.path.join(GEN, "gtp_small_consts.inc")
+    r = subprocess.run([exe, out + ".tmp"], capture_output=True, text=True)
+    if r.returncode:
+        print(r.stdout, r.stderr)
+        raise RuntimeError("generator failed")
+    os.replace(out + ".tmp", out)
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     hipcc = _hipcc()
+    generate_constants(verbose)
     jobs = []
     for s in HIP_SOURCES:
         obj = os.path.join(BUILD, s.replace(".hip", ".o"))
-        jobs.append(([hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj))
+        jobs.append(([hipcc, *HIP_FLAGS, f"-I{GEN}", "-c", os.path.join(CSRC, s), "-o", obj], obj))
     for s in CPP_SOURCES:
         obj = os.path.join(BUILD, s.replace(".cpp", ".o"))
         jobs.append((["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj))

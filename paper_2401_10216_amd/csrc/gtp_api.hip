@@ -352,6 +352,25 @@ gtp_status gtp_channel_mix(gtp_plan p, const void* x1, const void* x2, gtp_dtype
     e = gtp::launch_fill_zero(y, eo, st);
     return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_channel_mix launch");
   }
+  const int nct = gtp::mix_fused_nct(int(Co));
+  if (!p->force_generic && p->conv != GTP_CONV_DIRECT && nct > 0 && p->L1 == p->L2 && p->L2 == p->Lout &&
+      p->L1 >= 1 && p->L1 <= 8 && B <= 0x7fffffff) {
+    // one kernel: the pair products of a batch entry stay on chip; only the
+    // weights in the kernel's blocked layout go through a workspace
+    int64_t nwb = 0;
+    if (!mul_ok((P + 255) / 256 * 256, int64_t(16) * nct, &nwb) || nwb > INT64_MAX / 4)
+      return fail(GTP_ERR_INVALID_ARG, "C1*C2 too large");
+    float* wb = nullptr;
+    e = hipMallocAsync(reinterpret_cast<void**>(&wb), size_t(nwb) * sizeof(float), st);
+    if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+    bool done = false;
+    e = gtp::launch_mix_wt_blocks(W, wb, int(Co), P, nct, st);
+    if (e == hipSuccess) e = gtp::launch_mix_fused(p->dev, x1, x2, it, wb, y, B, C1, C2, int(Co), st, &done);
+    const hipError_t e2 = hipFreeAsync(wb, st);
+    if (e != hipSuccess) return hip_fail(e, "gtp_channel_mix launch");
+    if (e2 != hipSuccess) return hip_fail(e2, "hipFreeAsync");
+    if (done) return GTP_OK;
+  }
   // the transposed weights, then the pair products of a chunk of batch
   // entries (at most 256 MiB) in a stream-ordered workspace, then the mix on
   // the matrix cores

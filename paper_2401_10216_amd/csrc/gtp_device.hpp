@@ -110,6 +110,14 @@ hipError_t launch_mix_gemm(const float* WT, const float* T, float* y, int Co, in
                            hipStream_t s);
 // y[0 .. n) = 0 with a kernel (safe inside captured graphs).
 hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s);
+// Fused channel mixing for equal degrees 1..8 and Co <= 128 (*supported =
+// false otherwise): pair products and the mix in one kernel, one workgroup
+// per batch entry.  WB: the weights in the blocked layout made by
+// launch_mix_wt_blocks with mix_fused_nct(Co) 16-channel column tiles.
+int mix_fused_nct(int Co);
+hipError_t launch_mix_wt_blocks(const float* W, float* WB, int Co, int64_t P, int nct, hipStream_t s);
+hipError_t launch_mix_fused(const DevTables& t, const void* x1, const void* x2, int it, const float* WB, float* y,
+                            int64_t B, int64_t C1, int64_t C2, int Co, hipStream_t s, bool* supported);
 // y[p, :(Lout+1)^2] = x[p, :(L+1)^2] truncated or zero-padded.
 hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
 // Direct 2D convolution of the real-form Fourier grids (the paper's eq.

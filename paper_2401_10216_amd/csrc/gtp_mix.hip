@@ -95,6 +95,22 @@ __global__ __launch_bounds__(64) void k_mix_gemm(const float* __restrict__ WT, c
   }
 }
 
+// WB[q][co][g][s'] = W[co][16 q + 4 s' + g] (zero past P and Co) for
+// q < PR / 16, co < CoB: the B operands of four K-steps of the fused mix in
+// one 16-byte run per lane.
+__global__ __launch_bounds__(256) void k_mix_wt_blocks(const float* __restrict__ W, float* __restrict__ WB, int Co,
+                                                       int CoB, int64_t P, int64_t PR) {
+  const int64_t total = PR * CoB;
+  for (int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x; e < total; e += int64_t(gridDim.x) * 256) {
+    const int sp = int(e & 3), g = int((e >> 2) & 3);
+    const int64_t qc = e >> 4;
+    const int64_t q = qc / CoB;
+    const int co = int(qc - q * CoB);
+    const int64_t p = 16 * q + 4 * sp + g;
+    WB[e] = (co < Co && p < P) ? W[int64_t(co) * P + p] : 0.0f;
+  }
+}
+
 __global__ __launch_bounds__(256) void k_fill_zero(float* __restrict__ y, int64_t n) {
   for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) y[i] = 0.0f;
 }
@@ -117,6 +133,16 @@ hipError_t launch_mix_transpose(const float* W, float* WT, int Co, int64_t P, hi
   if (g > 65536) g = 65536;
   if (g < 1) return hipSuccess;
   hipLaunchKernelGGL(k_mix_transpose, dim3(unsigned(g)), dim3(256), 0, s, W, WT, Co, CoP, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_mix_wt_blocks(const float* W, float* WB, int Co, int64_t P, int nct, hipStream_t s) {
+  const int CoB = 16 * nct;
+  const int64_t PR = (P + 255) / 256 * 256;
+  int64_t g = (PR * CoB + 255) / 256;
+  if (g > 65536) g = 65536;
+  if (g < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_mix_wt_blocks, dim3(unsigned(g)), dim3(256), 0, s, W, WB, Co, CoB, P, PR);
   return hipGetLastError();
 }
 

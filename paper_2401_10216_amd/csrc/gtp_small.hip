@@ -103,6 +103,40 @@ __device__ __forceinline__ float ld_in(const uint16_t* p, int64_t i) {
 // share |cos(m p)| and |sin(m p)|, with signs set by the parity of m, so both
 // transforms work on the quarter 0 <= k <= Q and fan out.
 
+// a += s x, or a = s x for the first term of a sum: a multiply-add onto a
+// zero cannot drop the addend (signed zeros), and its three-operand form
+// cannot carry a literal constant.  The first product is kept out of
+// multiply-add fusion for the same reason (x s - y needs that form too).
+template <bool FIRST>
+__device__ __forceinline__ void mac(float& a, float s, float x) {
+  if constexpr (FIRST) {
+#pragma clang fp contract(off)
+    a = s * x;
+  } else {
+    a = fmaf(s, x, a);
+  }
+}
+
+// Whether m is the first degree of its parity (m >= 1) with a non-zero
+// cos (S = false) or sin (S = true) twiddle at sample k: the first term of a
+// phi-synthesis partial sum.
+constexpr bool first_m(int m, long long k, int NP, bool S) {
+  for (int mm = (m % 2 == 0) ? 2 : 1; mm < m; mm += 2) {
+    const float v = S ? ct_round(ct_sin2pi(mm * k, NP)) : ct_round(ct_cos2pi(mm * k, NP));
+    if (v != 0.0f) return false;
+  }
+  return true;
+}
+// Whether k is the first sample with a non-zero cos / sin twiddle of degree
+// m: the first term of a phi-analysis sum.
+constexpr bool first_k(int m, int k, int NP, bool S) {
+  for (int kk = 0; kk < k; ++kk) {
+    const float v = S ? ct_round(ct_sin2pi((long long)m * kk, NP)) : ct_round(ct_cos2pi((long long)m * kk, NP));
+    if (v != 0.0f) return false;
+  }
+  return true;
+}
+
 // F[k] = A0 + sum_m A[2m-1] cos(m p_k) + A[2m] sin(m p_k), k < NP, for a
 // function of phi-degree <= M.
 template <int M, int NP>
@@ -119,10 +153,10 @@ __device__ __forceinline__ void phi_synth(const float (&A)[2 * M + 1], float (&F
       constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
       if constexpr (m % 2 == 0) {
         if constexpr (c != 0.0f) pe = fmaf(A[2 * m - 1], c, pe);
-        if constexpr (sn != 0.0f) qe = fmaf(A[2 * m], sn, qe);
+        if constexpr (sn != 0.0f) mac<first_m(m, k, NP, true)>(qe, sn, A[2 * m]);
       } else {
-        if constexpr (c != 0.0f) po = fmaf(A[2 * m - 1], c, po);
-        if constexpr (sn != 0.0f) qo = fmaf(A[2 * m], sn, qo);
+        if constexpr (c != 0.0f) mac<first_m(m, k, NP, false)>(po, c, A[2 * m - 1]);
+        if constexpr (sn != 0.0f) mac<first_m(m, k, NP, true)>(qo, sn, A[2 * m]);
       }
     });
     if constexpr (k == 0) {
@@ -171,8 +205,8 @@ __device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
       constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
       constexpr int ic = m == 0 ? 0 : 2 * m - 1;
-      if constexpr (c != 0.0f) C[ic] = fmaf((m % 2 == 0) ? ce : co, c, C[ic]);
-      if constexpr (m > 0 && sn != 0.0f) C[2 * m] = fmaf((m % 2 == 0) ? se : so, sn, C[2 * m]);
+      if constexpr (c != 0.0f) mac<first_k(m, k, NP, false)>(C[ic], c, (m % 2 == 0) ? ce : co);
+      if constexpr (m > 0 && sn != 0.0f) mac<first_k(m, k, NP, true)>(C[2 * m], sn, (m % 2 == 0) ? se : so);
     });
   });
 }
@@ -190,11 +224,11 @@ __device__ __forceinline__ void theta_synth_pair(X x, const T& Sj, float (&Aj)[2
       constexpr int l = decltype(LL)::value;
       const float sv = Sj[ctri(l, m)];
       if constexpr ((l + m) % 2 == 0) {
-        ec = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), ec);
-        if constexpr (m > 0) es = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), es);
+        mac<l == m>(ec, sv, x(std::integral_constant<int, l * l + l + m>{}));
+        if constexpr (m > 0) mac<l == m>(es, sv, x(std::integral_constant<int, l * l + l - m>{}));
       } else {
-        oc = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), oc);
-        if constexpr (m > 0) os = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), os);
+        mac<l == m + 1>(oc, sv, x(std::integral_constant<int, l * l + l + m>{}));
+        if constexpr (m > 0) mac<l == m + 1>(os, sv, x(std::integral_constant<int, l * l + l - m>{}));
       }
     });
     if constexpr (m == 0) {
@@ -219,8 +253,8 @@ __device__ __forceinline__ void theta_synth_node(X x, const T& Sj, float (&A)[2 
     sfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float sv = (MIRROR && (l + m) % 2) ? -Sj[ctri(l, m)] : Sj[ctri(l, m)];
-      ec = fmaf(sv, x(std::integral_constant<int, l * l + l + m>{}), ec);
-      if constexpr (m > 0) es = fmaf(sv, x(std::integral_constant<int, l * l + l - m>{}), es);
+      mac<l == m>(ec, sv, x(std::integral_constant<int, l * l + l + m>{}));
+      if constexpr (m > 0) mac<l == m>(es, sv, x(std::integral_constant<int, l * l + l - m>{}));
     });
     if constexpr (m == 0) {
       A[0] = ec;
@@ -232,8 +266,9 @@ __device__ __forceinline__ void theta_synth_node(X x, const T& Sj, float (&A)[2 
 }
 
 // acc += W(t_j) * C for the moments C of one node; MIRROR uses the weights of
-// t_{NT-j}, which are (-1)^(l+m) times those of t_j.
-template <int LE, bool MIRROR, typename T>
+// t_{NT-j}, which are (-1)^(l+m) times those of t_j.  FIRST: the first node
+// with m > 0 terms (acc holds only the poles' m = 0 terms).
+template <int LE, bool MIRROR, typename T, bool FIRST = false>
 __device__ __forceinline__ void theta_analysis_node(const T& Wj, const float (&C)[2 * LE + 1],
                                                     float (&acc)[(LE + 1) * (LE + 1)]) {
   sfor<0, LE + 1>([&](auto MM) {
@@ -241,8 +276,8 @@ __device__ __forceinline__ void theta_analysis_node(const T& Wj, const float (&C
     sfor<m, LE + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float w = (MIRROR && (l + m) % 2) ? -Wj[ctri(l, m)] : Wj[ctri(l, m)];
-      acc[l * l + l + m] = fmaf(w, C[m == 0 ? 0 : 2 * m - 1], acc[l * l + l + m]);
-      if constexpr (m > 0) acc[l * l + l - m] = fmaf(w, C[2 * m], acc[l * l + l - m]);
+      mac<(FIRST && m > 0)>(acc[l * l + l + m], w, C[m == 0 ? 0 : 2 * m - 1]);
+      if constexpr (m > 0) mac<FIRST>(acc[l * l + l - m], w, C[2 * m]);
     });
   });
 }
@@ -282,21 +317,87 @@ __device__ __forceinline__ float ipow(float v) {
   }
 }
 
-// One node: phi synthesis of both functions, pointwise product (or power),
-// phi analysis of the product's moments m <= LE.
+// Quarter-angle class sums of a function of phi-degree <= M at sample k:
+// pe / po = sum over even / odd m of A_cos(m) cos(m p_k) (pe with A0), qe / qo
+// the same for the sin parts.  The samples at k, NP - k, 2Q + k, 2Q - k are
+// pe + po +- (qe + qo) and pe - po +- (qe - qo).
+template <int M, int NP, int k>
+__device__ __forceinline__ void phi_classes(const float (&A)[2 * M + 1], float& pe, float& po, float& qe,
+                                            float& qo) {
+  pe = A[0];
+  po = qe = qo = 0.0f;
+  sfor<1, M + 1>([&](auto MM) {
+    constexpr int m = decltype(MM)::value;
+    constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
+    constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
+    if constexpr (m % 2 == 0) {
+      if constexpr (c != 0.0f) pe = fmaf(A[2 * m - 1], c, pe);
+      if constexpr (sn != 0.0f) mac<first_m(m, k, NP, true)>(qe, sn, A[2 * m]);
+    } else {
+      if constexpr (c != 0.0f) mac<first_m(m, k, NP, false)>(po, c, A[2 * m - 1]);
+      if constexpr (sn != 0.0f) mac<first_m(m, k, NP, true)>(qo, sn, A[2 * m]);
+    }
+  });
+}
+
+// One node, product of two functions: the phi moments m <= LE of f g from
+// the class sums of f and g.  Summed over the four points of a quarter angle
+// (the grid's p -> -p, pi -+ p symmetry), f g folds to
+//   even-m cos: 4 (pe pe' + po po' + qe qe' + qo qo'),
+//   odd-m cos:  4 (pe po' + po pe' + qe qo' + qo qe'),
+//   even-m sin: 4 (pe qe' + po qo' + qe pe' + qo po'),
+//   odd-m sin:  4 (pe qo' + po qe' + qe po' + qo pe')
+// (2 and two points at k = 0 and k = Q), so no sample is formed; the factor
+// goes into the analysis twiddles.
+template <int L1, int L2, int LE, int NP>
+__device__ __forceinline__ void node_product_cls(const float (&A)[2 * L1 + 1], const float (&B)[2 * L2 + 1],
+                                                 float (&C)[2 * LE + 1]) {
+  static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
+  constexpr int Q = NP / 4;
+  sfor<0, 2 * LE + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
+  sfor<0, Q + 1>([&](auto KK) {
+    constexpr int k = decltype(KK)::value;
+    float pe, po, qe, qo, pf, pg, qf, qg;  // f: pe po qe qo; g: pf pg qf qg
+    phi_classes<L1, NP, k>(A, pe, po, qe, qo);
+    phi_classes<L2, NP, k>(B, pf, pg, qf, qg);
+    float ce, co = 0.0f, se = 0.0f, so = 0.0f;
+    constexpr float fac = (k == 0 || k == Q) ? 2.0f : 4.0f;
+    if constexpr (k == 0) {
+      ce = fmaf(po, pg, pe * pf);
+      co = fmaf(po, pf, pe * pg);
+    } else if constexpr (k == Q) {
+      ce = fmaf(qo, qg, pe * pf);
+      so = fmaf(qo, pf, pe * qg);
+    } else {
+      ce = fmaf(qo, qg, fmaf(qe, qf, fmaf(po, pg, pe * pf)));
+      co = fmaf(qo, qf, fmaf(qe, qg, fmaf(po, pf, pe * pg)));
+      se = fmaf(qo, pg, fmaf(qe, pf, fmaf(po, qg, pe * qf)));
+      so = fmaf(qo, pf, fmaf(qe, pg, fmaf(po, qf, pe * qg)));
+    }
+    sfor<0, LE + 1>([&](auto MM) {
+      constexpr int m = decltype(MM)::value;
+      constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
+      constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
+      constexpr int ic = m == 0 ? 0 : 2 * m - 1;
+      if constexpr (c != 0.0f) mac<first_k(m, k, NP, false)>(C[ic], fac * c, (m % 2 == 0) ? ce : co);
+      if constexpr (m > 0 && sn != 0.0f) mac<first_k(m, k, NP, true)>(C[2 * m], fac * sn, (m % 2 == 0) ? se : so);
+    });
+  });
+}
+
+// One node: the phi moments m <= LE of the product of two functions (from
+// their class sums), or of a power of one function (through its samples).
 template <int L1, int L2, int LE, int NP, int NU>
 __device__ __forceinline__ void node_product(const float (&A)[2 * L1 + 1], const float (&B)[2 * L2 + 1],
                                              float (&C)[2 * LE + 1]) {
-  float F[NP];
-  phi_synth<L1, NP>(A, F);
   if constexpr (NU == 0) {
-    float G[NP];
-    phi_synth<L2, NP>(B, G);
-    sfor<0, NP>([&](auto KK) { F[decltype(KK)::value] *= G[decltype(KK)::value]; });
+    node_product_cls<L1, L2, LE, NP>(A, B, C);
   } else {
+    float F[NP];
+    phi_synth<L1, NP>(A, F);
     sfor<0, NP>([&](auto KK) { F[decltype(KK)::value] = ipow<NU>(F[decltype(KK)::value]); });
+    phi_analysis<LE, NP>(F, C);
   }
-  phi_analysis<LE, NP>(F, C);
 }
 
 // Degree bookkeeping of one product stage.  NU = 0: x1 (deg L1) times x2
@@ -311,13 +412,94 @@ struct Geo {
   static constexpr int KE = csh(LE);
 };
 
+// Compile-time copies of the node-major S and W rows of the equal-degree
+// triples L1 = L2 = Lout = 1..8 (SmallConsts<L>::S[j][tri(l, m)], ::W[j][..]),
+// generated at build time from the same fp64 builder and fp32 rounding as a
+// plan's device tables.  Read with constant indices they become instruction
+// literals: a VALU instruction with a literal operand issues at the rate of
+// an all-VGPR one, one with a scalar-register operand at about half of it.
+#include "gtp_small_consts.inc"
+
+template <int L, int J, bool IS_W>
+struct LitRow {
+  __device__ __forceinline__ constexpr float operator[](int i) const {
+    return IS_W ? SmallConsts<L>::W[J][i] : SmallConsts<L>::S[J][i];
+  }
+};
+
+template <int L1, int L2, int LO, int NU>
+constexpr bool lit_tables() {
+  return NU == 0 && L1 == L2 && L2 == LO && L1 >= 1 && L1 <= 8;
+}
+
+// gtp_core for L1 = L2 = Lout = L with the tables as literals: the node-pair
+// loop is unrolled at compile time (NT = 2 L + 1 is odd: no equator node).
+template <int L, typename XA, typename XB>
+__device__ __forceinline__ void gtp_core_lit(XA xa, XB xb, float (&acc)[(L + 1) * (L + 1)]) {
+  using G = Geo<L, L, L, 0>;
+  constexpr int NT = G::NT, NP = G::NP;
+  static_assert(NT % 2 == 1, "equal degrees give an odd node count");
+  sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+  {
+    // poles: only m = 0 is non-zero and all phi samples are equal
+    constexpr LitRow<L, 0, false> S0{};
+    constexpr LitRow<L, 0, true> W0{};
+    float ae = 0.0f, ao = 0.0f, be = 0.0f, bo = 0.0f;
+    sfor<0, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      if constexpr (l % 2 == 0) {
+        mac<l == 0>(ae, S0[ctri(l, 0)], xa(std::integral_constant<int, l * l + l>{}));
+        mac<l == 0>(be, S0[ctri(l, 0)], xb(std::integral_constant<int, l * l + l>{}));
+      } else {
+        mac<l == 1>(ao, S0[ctri(l, 0)], xa(std::integral_constant<int, l * l + l>{}));
+        mac<l == 1>(bo, S0[ctri(l, 0)], xb(std::integral_constant<int, l * l + l>{}));
+      }
+    });
+    const float fn = (ae + ao) * (be + bo), fs = (ae - ao) * (be - bo);
+    const float ce = float(NP) * (fn + fs), co = float(NP) * (fn - fs);
+    sfor<0, L + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      acc[l * l + l] = W0[ctri(l, 0)] * ((l % 2 == 0) ? ce : co);
+    });
+  }
+  sfor<1, (NT + 1) / 2>([&](auto JJ) {
+    constexpr int j = decltype(JJ)::value;
+    constexpr LitRow<L, j, false> Sj{};
+    constexpr LitRow<L, j, true> Wj{};
+    xa.touch();
+    xb.touch();
+    float Aj[2 * L + 1], Ajp[2 * L + 1], Bj[2 * L + 1];
+    theta_synth_pair<L>(xa, Sj, Aj, Ajp);
+    theta_synth_node<L, false>(xb, Sj, Bj);
+    GTP_SCHED_FENCE();
+    {
+      float C[2 * L + 1];
+      node_product<L, L, L, NP, 0>(Aj, Bj, C);
+      theta_analysis_node<L, false, LitRow<L, j, true>, j == 1>(Wj, C, acc);
+    }
+    GTP_SCHED_FENCE();
+    {
+      theta_synth_node<L, true>(xb, Sj, Bj);
+      float C[2 * L + 1];
+      node_product<L, L, L, NP, 0>(Ajp, Bj, C);
+      theta_analysis_node<L, true>(Wj, C, acc);
+    }
+    GTP_SCHED_FENCE();
+  });
+}
+
 // acc (degree <= LE) = product of xa and xb (or xa^NU) for one lane.
 // xa(I), xb(I) return input coefficient I; ST / WT are the node-major
-// synthesis and analysis tables with row lengths ntS / ntW.
+// synthesis and analysis tables with row lengths ntS / ntW (for equal degrees
+// 1..8 the compile-time copies are used instead).
 template <int L1, int L2, int LO, int NU, typename XA, typename XB>
 __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, LO, NU>::KE],
                                          const float* __restrict__ ST, int ntS, const float* __restrict__ WT,
                                          int ntW) {
+  if constexpr (lit_tables<L1, L2, LO, NU>()) {
+    gtp_core_lit<L1>(xa, xb, acc);
+    return;
+  }
   using G = Geo<L1, L2, LO, NU>;
   constexpr int LE = G::LE, NT = G::NT, NP = G::NP;
   sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
@@ -597,6 +779,148 @@ hipError_t launch_pairs_one(const DevTables& t, const void* x1, int it1, const v
   return hipSuccess;
 }
 
+// Fused channel mixing (equal degrees L, Kd = (L+1)^2):
+//   y[b, co] = sum_p W[co, p] T[b, p],  T[b, p] = GTP(x1[b, c1], x2[b, c2]),
+// p = c1 C2 + c2.  One workgroup (four waves) per batch entry, in rounds of
+// 256 pairs: each lane takes one pair product with the thread-per-product
+// core (x2 row in its LDS row), writes the product over that row, and after
+// a barrier the waves mix the round's 256 products on the matrix cores,
+//   y_b^T (Kd x Co) += T_round^T (Kd x 256) W^T_round (256 x Co),
+// wave w taking the 16-coefficient row tiles w, w + 4, ... and every
+// 16-channel column tile (v_mfma_f32_16x16x4f32: A[i][k] from lane 16 k + i,
+// B[k][j] from lane 16 k + j, D register r of lane 16 g + i = row 4 g + r,
+// column i).  K-step s of a round covers the pair slots 4 s + g; the weights
+// come in the blocked layout WB[p / 16][co][g][s'] (p = 16 (p / 16) + 4 s' +
+// g, zero past P and Co), so one 16-byte load gives a lane its B operands of
+// four K-steps.  The partial y_b of each wave's tiles passes from one round
+// to the next through y itself (each lane reads back what it wrote; the
+// lines stay in L2), so no accumulator is live during the products.  Only
+// x1, x2, W and y touch HBM.
+typedef float mixv4 __attribute__((ext_vector_type(4)));
+constexpr int kMixThreads = 256;
+
+template <int L, typename TIn, int NCT>
+__global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(small_waves(L, L, L)))) void k_mix_fused(
+    const TIn* __restrict__ x1, const TIn* __restrict__ x2, const float* __restrict__ WB, float* __restrict__ y,
+    int64_t C1, int64_t C2, int Co, int64_t P, const float* __restrict__ ST, int ntS, const float* __restrict__ WT,
+    int ntW) {
+  constexpr int Kd = csh(L);
+  constexpr int NKT = (Kd + 15) / 16, KTW = (NKT + 3) / 4, CoB = 16 * NCT;
+  __shared__ float tile[kMixThreads * Kd];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i = lane & 15;
+  const int64_t b = blockIdx.x;
+  const int64_t nround = (P + kMixThreads - 1) / kMixThreads;
+  for (int64_t r = 0; r < nround; ++r) {
+    {
+      const int64_t p = r * kMixThreads + tid;
+      const int64_t pc = p < P ? p : P - 1;
+      const int64_t c1 = pc / C2, c2 = pc - c1 * C2;
+      const TIn* const xr1 = x1 + (b * C1 + c1) * Kd;
+      const TIn* const xr2 = x2 + (b * C2 + c2) * Kd;
+      float xa[Kd], acc[Kd];
+      sfor<0, Kd>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
+      sfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+      RegX<Kd> A{xa};
+      LdsX Bx{tile, tid * Kd};
+      gtp_core<L, L, L, 0>(A, Bx, acc, ST, ntS, WT, ntW);
+      // over the lane's own row (its x2 reads are done).  Slots past P hold
+      // a copy of the last pair's product; their weight rows are zero.
+      sfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = acc[decltype(I)::value]; });
+    }
+    // this wave's partial sums of the previous rounds (output rows k0 + 4 g +
+    // rr of channel 16 ct + i) and its first weight block, requested before
+    // the barrier so that they arrive while the other waves finish
+    mixv4 macc[KTW][NCT], bw[KTW][NCT];
+    const float* const wb = WB + ((r * 16) * CoB + i) * 16 + g * 4;
+    sfor<0, KTW>([&](auto TT) {
+      constexpr int t = decltype(TT)::value;
+      const int k0 = (wv + 4 * t) * 16;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct) {
+        const int co = ct * 16 + i;
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          const int k = k0 + 4 * g + rr;
+          macc[t][ct][rr] = (r > 0 && co < Co && k < Kd) ? y[(b * Co + co) * Kd + k] : 0.0f;
+        }
+        bw[t][ct] = *reinterpret_cast<const mixv4*>(wb + ct * 256);
+      }
+    });
+    __syncthreads();
+    sfor<0, KTW>([&](auto TT) {
+      constexpr int t = decltype(TT)::value;
+      const int k0 = (wv + 4 * t) * 16;
+      if (k0 < Kd) {  // wave-uniform
+        const int ka = k0 + i < Kd ? k0 + i : Kd - 1;
+        const bool kok = k0 + i < Kd;
+        mixv4 bn[NCT];
+#pragma unroll 2
+        for (int q = 0; q < 16; ++q) {
+          float a[4];
+#pragma unroll
+          for (int sp = 0; sp < 4; ++sp) {
+            const float v = tile[(16 * q + 4 * sp + g) * Kd + ka];
+            a[sp] = kok ? v : 0.0f;
+          }
+          const int qn = q + 1 < 16 ? q + 1 : q;
+#pragma unroll
+          for (int ct = 0; ct < NCT; ++ct)
+            bn[ct] = *reinterpret_cast<const mixv4*>(wb + int64_t(qn) * CoB * 16 + ct * 256);
+#pragma unroll
+          for (int sp = 0; sp < 4; ++sp)
+#pragma unroll
+            for (int ct = 0; ct < NCT; ++ct)
+              macc[t][ct] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[sp], bw[t][ct][sp], macc[t][ct], 0, 0, 0);
+#pragma unroll
+          for (int ct = 0; ct < NCT; ++ct) bw[t][ct] = bn[ct];
+        }
+#pragma unroll
+        for (int ct = 0; ct < NCT; ++ct) {
+          const int co = ct * 16 + i;
+#pragma unroll
+          for (int rr = 0; rr < 4; ++rr) {
+            const int k = k0 + 4 * g + rr;
+            if (co < Co && k < Kd) y[(b * Co + co) * Kd + k] = macc[t][ct][rr];
+          }
+        }
+      }
+    });
+    __syncthreads();
+  }
+}
+
+template <int L, typename TIn>
+hipError_t launch_mix_fused_typed(const DevTables& t, const void* x1, const void* x2, const float* WB, float* y,
+                                  int64_t B, int64_t C1, int64_t C2, int Co, int nct, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(B)), block(kMixThreads);
+  const int64_t P = C1 * C2;
+  const TIn* a = static_cast<const TIn*>(x1);
+  const TIn* c = static_cast<const TIn*>(x2);
+  switch (nct) {
+    case 1:
+      hipLaunchKernelGGL((k_mix_fused<L, TIn, 1>), grid, block, 0, s, a, c, WB, y, C1, C2, Co, P, t.ST, t.ntS, t.WT, t.ntW);
+      break;
+    case 2:
+      hipLaunchKernelGGL((k_mix_fused<L, TIn, 2>), grid, block, 0, s, a, c, WB, y, C1, C2, Co, P, t.ST, t.ntS, t.WT, t.ntW);
+      break;
+    case 4:
+      hipLaunchKernelGGL((k_mix_fused<L, TIn, 4>), grid, block, 0, s, a, c, WB, y, C1, C2, Co, P, t.ST, t.ntS, t.WT, t.ntW);
+      break;
+    case 8:
+      hipLaunchKernelGGL((k_mix_fused<L, TIn, 8>), grid, block, 0, s, a, c, WB, y, C1, C2, Co, P, t.ST, t.ntS, t.WT, t.ntW);
+      break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int L>
+hipError_t launch_mix_fused_one(const DevTables& t, const void* x1, const void* x2, int it, const float* WB, float* y,
+                                int64_t B, int64_t C1, int64_t C2, int Co, int nct, hipStream_t s) {
+  if (it == IN_BF16) return launch_mix_fused_typed<L, uint16_t>(t, x1, x2, WB, y, B, C1, C2, Co, nct, s);
+  return launch_mix_fused_typed<L, float>(t, x1, x2, WB, y, B, C1, C2, Co, nct, s);
+}
+
 template <int L, int LO>
 hipError_t launch_chain(const DevTables& t1, const DevTables& t2, int nu, const void* x, int in_type, int64_t n,
                         float* y, hipStream_t s) {
@@ -655,6 +979,37 @@ hipError_t launch_pairs_small(const DevTables& t, const void* x1, int it1, const
       case 8: return launch_pairs_one<8>(t, x1, it1, x2, it2, n, y, pi, s, supported);
       default: break;
     }
+  }
+  *supported = false;
+  return hipSuccess;
+}
+
+int mix_fused_nct(int Co) {
+  const int n = (Co + 15) / 16;
+  if (n <= 1) return 1;
+  if (n <= 2) return 2;
+  if (n <= 4) return 4;
+  if (n <= 8) return 8;
+  return 0;
+}
+
+hipError_t launch_mix_fused(const DevTables& t, const void* x1, const void* x2, int it, const float* WB, float* y,
+                            int64_t B, int64_t C1, int64_t C2, int Co, hipStream_t s, bool* supported) {
+  *supported = false;
+  const int nct = mix_fused_nct(Co);
+  if (nct == 0 || t.L1 != t.L2 || t.L2 != t.Lout || B <= 0 || B > 0x7fffffff || C1 <= 0 || C2 <= 0) return hipSuccess;
+  if (it != IN_F32 && it != IN_BF16) return hipSuccess;
+  *supported = true;
+  switch (t.L1) {
+    case 1: return launch_mix_fused_one<1>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 2: return launch_mix_fused_one<2>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 3: return launch_mix_fused_one<3>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 4: return launch_mix_fused_one<4>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 5: return launch_mix_fused_one<5>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 6: return launch_mix_fused_one<6>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 7: return launch_mix_fused_one<7>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    case 8: return launch_mix_fused_one<8>(t, x1, x2, it, WB, y, B, C1, C2, Co, nct, s);
+    default: break;
   }
   *supported = false;
   return hipSuccess;

@@ -629,8 +629,12 @@ def test_conv_escn_edge_workload_sampled():
 
 # ------------------------------------------------------------------ channel mixing
 
+# equal degrees 1..8 with Co <= 128 take the fused kernel (rounds of 256 pairs,
+# 16-channel column tiles in groups of 1, 2, 4 or 8); unequal degrees and
+# Co > 128 take products through a workspace, then the mix
 MIX = [(2, 2, 2, 4, 4, 4, 37), (4, 4, 4, 5, 7, 3, 19), (6, 6, 6, 8, 8, 8, 11), (8, 8, 8, 3, 4, 17, 5),
-       (2, 3, 4, 4, 3, 5, 9), (6, 6, 6, 32, 32, 32, 3)]
+       (2, 3, 4, 4, 3, 5, 9), (6, 6, 6, 32, 32, 32, 3), (6, 6, 6, 17, 19, 70, 3), (5, 5, 5, 16, 20, 40, 4),
+       (3, 3, 3, 2, 3, 1, 9), (7, 7, 7, 9, 9, 9, 3), (1, 1, 1, 40, 10, 5, 4), (6, 6, 6, 4, 4, 130, 2)]
 
 
 @pytest.mark.parametrize("L1,L2,Lout,C1,C2,Co,B", MIX)
@@ -644,6 +648,22 @@ def test_channel_mix(L1, L2, Lout, C1, C2, Co, B):
     torch.cuda.synchronize()
     ref = O.channel_mix(x1, x2, W, L1, L2, Lout)
     err = O.max_rel_err(y.cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_channel_mix_full_size():
+    """The mix workload at its full size (B=8192, C1=C2=Co=32, L=6), as the
+    bench runs it; the oracle checks 6 sampled batch entries (6144 pair
+    products)."""
+    x1, x2, W = inputs.mix_inputs()
+    B = x1.shape[0]
+    _say(f"channel_mix full size B={B} C=32 L=6")
+    y = gtp.gtp_channel_mix(gtp.Plan(6, 6, 6), dev(x1), dev(x2), dev(W))
+    torch.cuda.synchronize()
+    bs = np.array([0, 1, 4095, 4096, B - 2, B - 1])
+    ref = O.channel_mix(x1[bs], x2[bs], W, 6, 6, 6)
+    err = O.max_rel_err(y[torch.from_numpy(bs).cuda()].cpu().numpy(), ref)
     _say(f"  err={err:.3e}")
     assert err <= TOL, err
 
