@@ -91,7 +91,7 @@ def nsh(L):
 
 # device-side sources every kernel depends on (the host dispatch in
 # gtp_api.hip does not change a kernel's memory traffic)
-SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
+SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp", "gen_small_consts.cpp"]
 
 
 def dominant_kernel(workload: str, L: int, escn: bool = False):
