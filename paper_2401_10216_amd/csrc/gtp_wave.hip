@@ -283,20 +283,36 @@ struct WaveCtx {
       }
     });
 
-    // ---- 2b. sample products, folded over the 4-point sets
+    // ---- 2b. sample products, folded over the 4-point sets.  The samples at
+    // k, -k, 2Q + k, 2Q - k are pe + po +- (qe + qo) and pe - po +- (qe - qo);
+    // summed over the four points the product folds to 4 (pe pe' + po po' +
+    // qe qe' + qo qo') (even-m cos), 4 (pe po' + po pe' + qe qo' + qo qe')
+    // (odd-m cos), 4 (pe qe' + po qo' + qe pe' + qo po') (even-m sin) and
+    // 4 (pe qo' + po qe' + qe po' + qo pe') (odd-m sin), so no sample is
+    // formed; the 4 goes into the analysis weight (coinciding points at k = 0
+    // and Q are counted twice there and weighted 1/2).  At L = 64 (256
+    // registers) the samples are formed and folded instead (weights 1/2 and
+    // 1), which keeps fewer values live; the result is the same.
     lfor<0, NMB>([&](auto MB) {
       constexpr int mb = decltype(MB)::value;
       const f4 pe1 = acc[0][mb][0], po1 = acc[0][mb][1], qe1 = acc[0][mb][2], qo1 = acc[0][mb][3];
       const f4 pe2 = acc[1][mb][0], po2 = acc[1][mb][1], qe2 = acc[1][mb][2], qo2 = acc[1][mb][3];
-      const f4 s1 = pe1 + po1, d1 = pe1 - po1, s2 = qe1 + qo1, d2 = qe1 - qo1;
-      const f4 t1 = pe2 + po2, u1 = pe2 - po2, t2 = qe2 + qo2, u2 = qe2 - qo2;
-      const f4 hk = (s1 + s2) * (t1 + t2), hmk = (s1 - s2) * (t1 - t2);
-      const f4 hpk = (d1 + d2) * (u1 + u2), hpmk = (d1 - d2) * (u1 - u2);
-      const f4 a = hk + hmk, b = hpk + hpmk, dd = hk - hmk, ee = hpk - hpmk;
-      acc[0][mb][0] = a + b;
-      acc[0][mb][1] = a - b;
-      acc[0][mb][2] = dd + ee;
-      acc[0][mb][3] = dd - ee;
+      if constexpr (L < 64) {
+        acc[0][mb][0] = pe1 * pe2 + po1 * po2 + qe1 * qe2 + qo1 * qo2;
+        acc[0][mb][1] = pe1 * po2 + po1 * pe2 + qe1 * qo2 + qo1 * qe2;
+        acc[0][mb][2] = pe1 * qe2 + po1 * qo2 + qe1 * pe2 + qo1 * po2;
+        acc[0][mb][3] = pe1 * qo2 + po1 * qe2 + qe1 * po2 + qo1 * pe2;
+      } else {
+        const f4 s1 = pe1 + po1, d1 = pe1 - po1, s2 = qe1 + qo1, d2 = qe1 - qo1;
+        const f4 t1 = pe2 + po2, u1 = pe2 - po2, t2 = qe2 + qo2, u2 = qe2 - qo2;
+        const f4 hk = (s1 + s2) * (t1 + t2), hmk = (s1 - s2) * (t1 - t2);
+        const f4 hpk = (d1 + d2) * (u1 + u2), hpmk = (d1 - d2) * (u1 - u2);
+        const f4 a = hk + hmk, b = hpk + hpmk, dd = hk - hmk, ee = hpk - hpmk;
+        acc[0][mb][0] = a + b;
+        acc[0][mb][1] = a - b;
+        acc[0][mb][2] = dd + ee;
+        acc[0][mb][3] = dd - ee;
+      }
     });
 
     // ---- 2c. phi analysis contractions; operands per k block from the seeds:
@@ -318,7 +334,8 @@ struct WaveCtx {
             rot(co, so, ast[mr].z, ast[mr].w);
           }
           const int k = 16 * mb + 4 * g + r;
-          const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f : 1.0f;
+          constexpr float fold = L < 64 ? 4.0f : 1.0f;  // see the sample products
+          const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f * fold : fold;
           o[mr][0] = mfma4(wk * ce, acc[0][mb][0][r], o[mr][0]);
           o[mr][1] = mfma4(wk * co, acc[0][mb][1][r], o[mr][1]);
           o[mr][2] = mfma4(wk * se, acc[0][mb][2][r], o[mr][2]);
