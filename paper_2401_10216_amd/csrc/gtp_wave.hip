@@ -434,6 +434,35 @@ __device__ __forceinline__ void row_lm(int q, int& l, int& m) {
   m = q - l * (l - 1) / 2 + 1;
 }
 
+// LDS offset, within one pass's combined moments, of every theta-analysis
+// row q = lane + 64 it (rows with m > 0 in tri order; parity of l + m picks
+// the sum or the difference of the mirror nodes, 2 m the m-part): a
+// compile-time table, read once per pass, instead of inverting the
+// triangular index in every pass.
+template <int L>
+struct RowErTab {
+  int v[WGeo<L>::NIT * 64];
+};
+template <int L>
+constexpr RowErTab<L> make_row_er() {
+  using G = WGeo<L>;
+  RowErTab<L> t{};
+  int q = 0;
+  for (int l = 1; l <= L; ++l)
+    for (int m = 1; m <= l; ++m, ++q) t.v[q] = ((l + m) & 1) * 8 * G::NMP2 + 2 * m;
+  return t;
+}
+__device__ const RowErTab<16> kRowEr16 = make_row_er<16>();
+__device__ const RowErTab<32> kRowEr32 = make_row_er<32>();
+template <int L>
+__device__ __forceinline__ const int* row_er_table() {
+  if constexpr (L == 16) {
+    return kRowEr16.v;
+  } else {
+    return kRowEr32.v;
+  }
+}
+
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.
 template <int L, typename T1, typename T2, bool WGT>
@@ -463,27 +492,25 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     yc[decltype(IT)::value] = 0.0f;
     ys[decltype(IT)::value] = 0.0f;
   });
-  // LDS offset of row q's moment (parity of l + m, m-part), recomputed in
-  // every pass from an opaque copy of the lane id (hoisting these offsets out
-  // of the pass loop would keep a dozen registers live and spill them)
-  auto row_er = [&](int q) {
-    int l, m;
-    row_lm(q, l, m);
-    return ((l + m) & 1) * 8 * NMP2 + 2 * m;
-  };
+  const int* const er_tab = row_er_table<L>();
 
   for (int pass = 0; pass < PASSES; ++pass) {
     const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
     f4 o[1][4];
     float zz;
     w.pass(pu, o, zz);
+    // this pass's row offsets (loaded here, not held across the passes:
+    // that would keep NIT more registers live through the contractions)
+    int er[NIT];
+    lfor<0, NIT>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      er[it] = (lane + 64 * it < NROW) ? er_tab[64 * it + lane] : 0;
+    });
     w.store_moments(eo, o, zz);
     __syncthreads();
 
     // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
     const int wbase = pu * (NIT + 1) * 64 * 32;
-    int ln = lane;
-    asm volatile("" : "+v"(ln));
     if (lane <= L) {
       const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
       const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
@@ -499,10 +526,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
         const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        const int er = row_er(ln + 64 * it);
         lfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
-          const float2 cs = *reinterpret_cast<const float2*>(eo + er + jj * NMP2);
+          const float2 cs = *reinterpret_cast<const float2*>(eo + er[it] + jj * NMP2);
           yc[it] = fmaf(wv[jj], cs.x, yc[it]);
           ys[it] = fmaf(wv[jj], cs.y, ys[it]);
         });
