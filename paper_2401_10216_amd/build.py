@@ -41,11 +41,11 @@ GEN = os.path.join(BUILD, "gen")
 
 def generate_constants(verbose: bool = False) -> None:
     """Compile and run the generator of the compile-time tables of the
-    thread-per-product kernels (from the library's own fp64 table builder)."""
+    thread-per-product kernels (from the library's own fp64 table builders)."""
     os.makedirs(GEN, exist_ok=True)
     exe = os.path.join(BUILD, "gen_small_consts")
     cmd = ["g++", *CXX_FLAGS, "-o", exe, os.path.join(CSRC, "gen_small_consts.cpp"),
-           os.path.join(CSRC, "gtp_tables.cpp")]
+           os.path.join(CSRC, "gtp_tables.cpp"), os.path.join(CSRC, "gtp_escn_tables.cpp")]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if verbose or r.returncode:
         print(" ".join(cmd))
@@ -53,11 +53,13 @@ def generate_constants(verbose: bool = False) -> None:
     if r.returncode:
         raise RuntimeError("generator build failed")
     out = os.path.join(GEN, "gtp_small_consts.inc")
-    r = subprocess.run([exe, out + ".tmp"], capture_output=True, text=True)
+    out_e = os.path.join(GEN, "gtp_escn_consts.inc")
+    r = subprocess.run([exe, out + ".tmp", out_e + ".tmp"], capture_output=True, text=True)
     if r.returncode:
         print(r.stdout, r.stderr)
         raise RuntimeError("generator failed")
     os.replace(out + ".tmp", out)
+    os.replace(out_e + ".tmp", out_e)
 
 
 def build(verbose: bool = False) -> str:

@@ -78,6 +78,38 @@ struct EGeo {
   static constexpr int ERL = OW(L + 1), NPAIR = L + 1;
 };
 
+// The node-pair rows as compile-time constants (EscnConsts<L>::E[j][..], the
+// same fp64 builder and fp32 rounding as a plan's device copy): read with
+// constant indices they are instruction literals, and the product loop needs
+// neither loads nor LDS for them.
+#include "gtp_escn_consts.inc"
+
+// a += s x, or a = s x for the first term of a sum (a multiply-add onto zero
+// would need the three-operand form, which cannot carry a literal)
+template <bool FIRST>
+__device__ __forceinline__ void emac(float& a, float s, float x) {
+  if constexpr (FIRST) {
+#pragma clang fp contract(off)
+    a = s * x;
+  } else {
+    a = fmaf(s, x, a);
+  }
+}
+// first degree l (l >= l0, step 2) with a non-zero entry E[j][off + l - base]
+template <int L>
+constexpr int first_nz(int j, int off, int base, int l0) {
+  for (int l = l0; l <= L; l += 2)
+    if (EscnConsts<L>::E[j][off + l - base] != 0.0f) return l;
+  return -1;
+}
+// first node pair with a non-zero entry E[j][i]
+template <int L>
+constexpr int first_pair_nz(int i) {
+  for (int j = 0; j < EscnConsts<L>::NPAIR; ++j)
+    if (EscnConsts<L>::E[j][i] != 0.0f) return j;
+  return -1;
+}
+
 // ---------------------------------------------------------------------------
 // Per-edge rotation matrices: one wave per edge, four edges per workgroup.
 // D_b = J^T Z(-beta) J Z(-alpha) for every degree l <= L, written in the
@@ -198,12 +230,6 @@ __device__ __forceinline__ void load_drow(const float* Dl, float4 (&buf)[NQ]) {
   const float4* row = reinterpret_cast<const float4*>(Dl + dofs(l) + a * erow(l));
   efor<0, erow(l) / 4>([&](auto QQ) { buf[decltype(QQ)::value] = row[decltype(QQ)::value]; });
 }
-// NQ 16-byte chunks at float offset O of a node-pair row (LDS)
-template <int O, int NQ, int NB>
-__device__ __forceinline__ void load_chunk(const float* er, float4 (&buf)[NB]) {
-  const float4* c = reinterpret_cast<const float4*>(er + O);
-  efor<0, NQ>([&](auto QQ) { buf[decltype(QQ)::value] = c[decltype(QQ)::value]; });
-}
 
 // register budget per lane: 3 waves per SIMD up to L = 6, 2 above
 constexpr int escn_waves(int L) { return L <= 6 ? 3 : 2; }
@@ -213,17 +239,16 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     const TIn* __restrict__ x, const float* __restrict__ Dall, const float* __restrict__ h, float* __restrict__ y,
     int64_t C, int ncb, EscnDev t) {
   using EG = EGeo<L>;
-  constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR, ERL = EG::ERL;
-  constexpr int DS = dofs(L + 1), ES = NPAIR * ERL;
+  constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR;
+  static_assert(EscnConsts<L>::NPAIR == NPAIR && EscnConsts<L>::ERL == EG::ERL, "node-pair table layout");
+  constexpr int DS = dofs(L + 1);
   constexpr int XT = kEW * K;  // x / y tile
-  // once the x rows are in registers the tile's space holds D and the
-  // node-pair table (both 16-byte multiples)
-  static_assert(DS % 4 == 0 && ES % 4 == 0 && DS + ES <= XT, "LDS layout");
-  constexpr int ND4 = DS / 4, NE4 = ES / 4, RD = (ND4 + kEW - 1) / kEW, RE = (NE4 + kEW - 1) / kEW;
+  // once the x rows are in registers the tile's space holds D (16-byte rows)
+  static_assert(DS % 4 == 0 && DS <= XT, "LDS layout");
+  constexpr int ND4 = DS / 4, RD = (ND4 + kEW - 1) / kEW;
   __shared__ __align__(16) float lds[XT];
   float* const tile = lds;
   float* const Dl = lds;
-  float* const El = lds + DS;
 
   const int tid = threadIdx.x;
   const int64_t b = blockIdx.x / ncb;
@@ -232,8 +257,8 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   const int64_t p0 = b * C + c0;
 
   // ---- 1. every load issued before the first wait: this workgroup's x slab
-  // (coalesced), the edge's rotation matrix and the node-pair table (16-byte
-  // loads), the lane's radial weights
+  // (coalesced), the edge's rotation matrix (16-byte loads), the lane's
+  // radial weights
   // (uniform base pointers, 32-bit lane offsets)
   const TIn* const xb = x + p0 * K;
   const unsigned nx = unsigned(cnt * K);
@@ -246,9 +271,8 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   // (16-byte loads kept as plain floats; indices clamped into range: every
   // lane loads, so the values stay in registers; the out-of-range copies are
   // never stored)
-  float dv[4 * RD], ev[4 * RE];
+  float dv[4 * RD];
   const float4* Dg = reinterpret_cast<const float4*>(Dall + b * DS);
-  const float4* Eg = reinterpret_cast<const float4*>(t.E);
   efor<0, RD>([&](auto I) {
     constexpr int q = decltype(I)::value;
     const int i = tid + q * kEW;
@@ -258,22 +282,13 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     dv[4 * q + 2] = w.z;
     dv[4 * q + 3] = w.w;
   });
-  efor<0, RE>([&](auto I) {
-    constexpr int q = decltype(I)::value;
-    const int i = tid + q * kEW;
-    const float4 w = Eg[i < NE4 ? i : NE4 - 1];
-    ev[4 * q] = w.x;
-    ev[4 * q + 1] = w.y;
-    ev[4 * q + 2] = w.z;
-    ev[4 * q + 3] = w.w;
-  });
   float hv[H];
   const float* const hb = h + p0 * H;
   const unsigned hl = unsigned(tid < cnt ? tid : cnt - 1);  // lanes past the last channel read a valid row
   efor<0, H>([&](auto I) { hv[decltype(I)::value] = hb[hl * H + decltype(I)::value]; });
 
-  // ---- 2. x rows into registers through the tile, then D and the table
-  // into the tile's space
+  // ---- 2. x rows into registers through the tile, then D into the tile's
+  // space
   efor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
   __syncthreads();
   float xr[K];
@@ -283,11 +298,6 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     constexpr int q = decltype(I)::value;
     const int i = tid + q * kEW;
     if (i < ND4) reinterpret_cast<float4*>(Dl)[i] = make_float4(dv[4 * q], dv[4 * q + 1], dv[4 * q + 2], dv[4 * q + 3]);
-  });
-  efor<0, RE>([&](auto I) {
-    constexpr int q = decltype(I)::value;
-    const int i = tid + q * kEW;
-    if (i < NE4) reinterpret_cast<float4*>(El)[i] = make_float4(ev[4 * q], ev[4 * q + 1], ev[4 * q + 2], ev[4 * q + 3]);
   });
   __syncthreads();
   // ---- 3. x' = D x, row by row over all degrees (row R = l*l + a); each
@@ -316,62 +326,49 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     });
   }
 
-  // ---- 4. product with the zonal filter, mirror pair by mirror pair (table
-  // rows read from LDS, 16 bytes at a time, the same address in every lane;
-  // the chunks of order m + 1 are requested before those of order m are used)
+  // ---- 4. product with the zonal filter, mirror pair by mirror pair (the
+  // pair loop unrolled: table values are literals, zero entries dropped)
   float acc[K];
   efor<0, K>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
-#pragma unroll 1
-  for (int j = 0; j < NPAIR; ++j) {
+  efor<0, NPAIR>([&](auto JJ) {
+    constexpr int j = decltype(JJ)::value;
     GTP_ESCN_FENCE();
-    const float* er = El + j * ERL;
-    float4 zc[EG::PZ / 4];
-    efor<0, EG::PZ / 4>([&](auto QQ) { zc[decltype(QQ)::value] = reinterpret_cast<const float4*>(er)[decltype(QQ)::value]; });
-    constexpr int NCM = pad4(L + 1) / 4;  // chunks of the longest order (m = 0)
-    float4 sc[NCM], wc[NCM], sn[NCM], wn[NCM];
-    load_chunk<EG::OS(0), NCM>(er, sc);
-    load_chunk<EG::OW(0), NCM>(er, wc);
     // filter at t_j and its mirror (Theta_l0(pi - t) = (-1)^l Theta_l0(t))
     float fe = 0.0f, fo = 0.0f;
     efor<0, H>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
-      const float z = f4at<l % 4>(zc[l / 4]);
-      if constexpr (l % 2 == 0) fe = fmaf(z, hv[l], fe);
-      else fo = fmaf(z, hv[l], fo);
+      constexpr float z = EscnConsts<L>::E[j][l];
+      if constexpr (z != 0.0f) {
+        if constexpr (l % 2 == 0) emac<l == first_nz<L>(j, 0, 0, 0)>(fe, z, hv[l]);
+        else emac<l == first_nz<L>(j, 0, 0, 1)>(fo, z, hv[l]);
+      }
     });
     const float fj = fe + fo, fm = fe - fo;
     efor<0, L + 1>([&](auto MM) {
-      constexpr int m = decltype(MM)::value, n = L + 1 - m;
-      if constexpr (m < L) {
-        load_chunk<EG::OS(m + 1), pad4(n - 1) / 4>(er, sn);
-        load_chunk<EG::OW(m + 1), pad4(n - 1) / 4>(er, wn);
-      }
-      GTP_ESCN_FENCE();
+      constexpr int m = decltype(MM)::value;
       efor<0, (m == 0 ? 1 : 2)>([&](auto SS) {
         constexpr int sg = decltype(SS)::value;  // 0: cos part (+m), 1: sin part (-m)
         float ae = 0.0f, ao = 0.0f;
         efor<m, L + 1>([&](auto LL) {
-          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m), c = l - m;
-          const float sv = f4at<c % 4>(sc[c / 4]);
-          if constexpr ((l + m) % 2 == 0) ae = fmaf(sv, xp[i], ae);
-          else ao = fmaf(sv, xp[i], ao);
+          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m);
+          constexpr float sv = EscnConsts<L>::E[j][EG::OS(m) + l - m];
+          if constexpr (sv != 0.0f) {
+            if constexpr ((l + m) % 2 == 0) emac<l == first_nz<L>(j, EG::OS(m), m, m)>(ae, sv, xp[i]);
+            else emac<l == first_nz<L>(j, EG::OS(m), m, m + 1)>(ao, sv, xp[i]);
+          }
         });
         const float pj = fj * (ae + ao), pm = fm * (ae - ao);
         const float pe = pj + pm, po = pj - pm;
         efor<m, L + 1>([&](auto LL) {
-          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m), c = l - m;
-          acc[i] = fmaf(f4at<c % 4>(wc[c / 4]), (l + m) % 2 == 0 ? pe : po, acc[i]);
+          constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m);
+          constexpr int wi = EG::OW(m) + l - m;
+          constexpr float wv = EscnConsts<L>::E[j][wi];
+          if constexpr (wv != 0.0f) emac<j == first_pair_nz<L>(wi)>(acc[i], wv, (l + m) % 2 == 0 ? pe : po);
         });
       });
       GTP_ESCN_FENCE();
-      if constexpr (m < L) {
-        efor<0, pad4(n - 1) / 4>([&](auto QQ) {
-          sc[decltype(QQ)::value] = sn[decltype(QQ)::value];
-          wc[decltype(QQ)::value] = wn[decltype(QQ)::value];
-        });
-      }
     });
-  }
+  });
   GTP_ESCN_FENCE();
 
   // ---- 5. y = D^T y', row by row with the same prefetch
