@@ -90,8 +90,13 @@ def nsh(L):
 
 
 # device-side sources every kernel depends on (the host dispatch in
-# gtp_api.hip does not change a kernel's memory traffic)
-SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp", "gen_small_consts.cpp"]
+# gtp_api.hip does not change a kernel's memory traffic), and those of single
+# kernel files (build-time constants, their tables)
+SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
+KERNEL_SOURCES = {
+    "gtp_small.hip": ["gen_small_consts.cpp"],
+    "gtp_escn.hip": ["gen_small_consts.cpp", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
+}
 
 
 def dominant_kernel(workload: str, L: int, escn: bool = False):
@@ -112,7 +117,7 @@ def dominant_kernel(workload: str, L: int, escn: bool = False):
 def kernel_sources_sha(kernel_source: str) -> str:
     """Hash of the sources that make up one kernel's launch path."""
     h = hashlib.sha256()
-    for f in sorted(SHARED_SOURCES + [kernel_source]):
+    for f in sorted(SHARED_SOURCES + KERNEL_SOURCES.get(kernel_source, []) + [kernel_source]):
         with open(os.path.join(ROOT, "paper_2401_10216_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
