@@ -1,6 +1,6 @@
 // Channel mixing of pair products on the fp32 matrix cores (gfx950).
 //
-// The channel-mixing combination of the appendix's discussion of channels,
+// The channel-mixing rule of the appendix (Implementation Details),
 // y[b, co] = sum_{c1, c2} W[co, c1, c2] GTP(x1[b, c1], x2[b, c2]), is linear in
 // the pair products T[b, p] = GTP(x1[b, c1], x2[b, c2]) (p = c1 C2 + c2), so
 // after the products it is one matrix product per batch entry,

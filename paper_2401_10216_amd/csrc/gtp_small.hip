@@ -6,8 +6,12 @@
 // into the theta part: table S), the samples are multiplied pointwise, and the
 // forward transforms followed by step 3 (table W) give the SH coefficients.
 // The theta transforms use the grid's mirror symmetry t <-> pi - t (Theta_lm
-// has parity (-1)^(l+m)), the phi transforms use p <-> -p and are unrolled
-// direct DFTs with compile-time twiddles.  Nothing but x and y touches HBM.
+// has parity (-1)^(l+m)), the phi transforms use p <-> -p and pi -+ p: they
+// are unrolled direct DFTs with compile-time twiddles, and the pointwise
+// product is taken, already folded over each quarter angle's four points,
+// from the two inputs' quarter-angle class sums.  For equal degrees the S
+// and W rows are compile-time constants too.  Nothing but x and y touches
+// HBM.
 #include <type_traits>
 #include <utility>
 
@@ -536,7 +540,8 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
     });
   }
 
-  // Interior mirror pairs (j, NT - j), 1 <= j < NT / 2.
+  // Interior mirror pairs (j, NT - j), 1 <= j < NT / 2 (runtime tables:
+  // degree triples without compile-time constants).
   // The node-pair tables are software-pipelined through scalar registers:
   // S of pair j + 1 and W of pair j are requested after the first LDS reads
   // of pair j (LDS reads share the scalar loads' wait counter) and arrive
@@ -779,7 +784,8 @@ hipError_t launch_pairs_one(const DevTables& t, const void* x1, int it1, const v
   return hipSuccess;
 }
 
-// Fused channel mixing (equal degrees L, Kd = (L+1)^2):
+// Fused channel mixing (the channel-mixing rule of the appendix, Implementation
+// Details; equal degrees L, Kd = (L+1)^2):
 //   y[b, co] = sum_p W[co, p] T[b, p],  T[b, p] = GTP(x1[b, c1], x2[b, c2]),
 // p = c1 C2 + c2.  One workgroup (four waves) per batch entry, in rounds of
 // 256 pairs: each lane takes one pair product with the thread-per-product
