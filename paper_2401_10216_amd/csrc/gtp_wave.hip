@@ -480,7 +480,6 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   const int64_t P = blockIdx.x;
   if (P >= n) return;  // whole-wave exit (one product per workgroup)
   stage_x<L, WGT>(xs, x1, x2, P, lane, t.XMAP, wt);
-  const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(xs), t);
 
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
   const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
@@ -496,6 +495,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
 
   for (int pass = 0; pass < PASSES; ++pass) {
     const int pu = __builtin_amdgcn_readfirstlane(pass);  // uniform: keep it scalar
+    // the pass context from an opaque copy of the lane id: its lane-derived
+    // offsets are recomputed each pass instead of being held (or spilled)
+    // across the passes
+    int lnp = lane;
+    asm volatile("" : "+v"(lnp));
+    const WaveCtx<L> w(lnp, reinterpret_cast<const float4*>(xs), t);
     f4 o[1][4];
     float zz;
     w.pass(pu, o, zz);
@@ -541,6 +546,9 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   // poles (only the m = 0 parts are non-zero there) and the stores
   float p1, p2;
   {
+    int lnp = lane;
+    asm volatile("" : "+v"(lnp));
+    const WaveCtx<L> w(lnp, reinterpret_cast<const float4*>(xs), t);
     float sv[G::NV0P];
     w.m0_load(PASSES, sv);
     w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
