@@ -813,10 +813,14 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(sma
   constexpr int Kd = csh(L);
   constexpr int NKT = (Kd + 15) / 16, KTW = (NKT + 3) / 4, CoB = 16 * NCT;
   __shared__ float tile[kMixThreads * Kd];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i = lane & 15;
   const int64_t b = blockIdx.x;
   const int64_t nround = (P + kMixThreads - 1) / kMixThreads;
   for (int64_t r = 0; r < nround; ++r) {
+    // thread-derived indices from an opaque copy of the thread id each round
+    // (recomputed, not held across the product)
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, i = lane & 15;
     {
       const int64_t p = r * kMixThreads + tid;
       const int64_t pc = p < P ? p : P - 1;
