@@ -686,9 +686,13 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     gtp_core<L1, L2, LO, NU>(A, B, acc, ST, ntS, WT, ntW);
     if constexpr (WGT) {
       // outputs above degree LE are zeros and stay zeros
-      if (wt.wo)
-        scale_by_degree<G::LE, G::KE>(wt.wo + weight_row(wt, p0 + tid) * (LO + 1),
+      if (wt.wo) {
+        // the row index from an opaque copy of the lane id (not held across the core)
+        int tq = threadIdx.x;
+        asm volatile("" : "+v"(tq));
+        scale_by_degree<G::LE, G::KE>(wt.wo + weight_row(wt, p0 + tq) * (LO + 1),
                                       [&](auto I) -> float& { return acc[decltype(I)::value]; });
+      }
     }
     __syncthreads();
   } else {
