@@ -826,9 +826,10 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(sma
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, i = lane & 15;
     {
-      const int64_t p = r * kMixThreads + tid;
-      const int64_t pc = p < P ? p : P - 1;
-      const int64_t c1 = pc / C2, c2 = pc - c1 * C2;
+      // pair index split in 32 bits (the launcher takes C1 C2 < 2^31)
+      const unsigned pl = unsigned(r) * kMixThreads + unsigned(tid);
+      const unsigned pc = pl < unsigned(P) ? pl : unsigned(P) - 1u;
+      const unsigned c1 = pc / unsigned(C2), c2 = pc - c1 * unsigned(C2);
       const TIn* const xr1 = x1 + (b * C1 + c1) * Kd;
       const TIn* const xr2 = x2 + (b * C2 + c2) * Kd;
       float xa[Kd], acc[Kd];
@@ -1011,7 +1012,9 @@ hipError_t launch_mix_fused(const DevTables& t, const void* x1, const void* x2, 
                             int64_t B, int64_t C1, int64_t C2, int Co, hipStream_t s, bool* supported) {
   *supported = false;
   const int nct = mix_fused_nct(Co);
-  if (nct == 0 || t.L1 != t.L2 || t.L2 != t.Lout || B <= 0 || B > 0x7fffffff || C1 <= 0 || C2 <= 0) return hipSuccess;
+  if (nct == 0 || t.L1 != t.L2 || t.L2 != t.Lout || B <= 0 || B > 0x7fffffff || C1 <= 0 || C2 <= 0 ||
+      C1 * C2 > 0x7fffffff - kMixThreads)
+    return hipSuccess;
   if (it != IN_F32 && it != IN_BF16) return hipSuccess;
   *supported = true;
   switch (t.L1) {
