@@ -43,7 +43,6 @@ __device__ __forceinline__ void efor(F&& f) {
   if constexpr (E > B) efor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
 }
 
-constexpr int etri(int l, int m) { return l * (l + 1) / 2 + m; }
 constexpr int ensh(int L) { return (L + 1) * (L + 1); }
 // padded row length of the degree-l block of D in LDS (16-byte rows)
 constexpr int erow(int l) { return (2 * l + 1 + 3) / 4 * 4; }
@@ -237,7 +236,7 @@ constexpr int escn_waves(int L) { return L <= 6 ? 3 : 2; }
 template <int L, typename TIn>
 __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(L)))) void k_conv_escn(
     const TIn* __restrict__ x, const float* __restrict__ Dall, const float* __restrict__ h, float* __restrict__ y,
-    int64_t C, int ncb, EscnDev t) {
+    int64_t C, int ncb) {
   using EG = EGeo<L>;
   constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR;
   static_assert(EscnConsts<L>::NPAIR == NPAIR && EscnConsts<L>::ERL == EG::ERL, "node-pair table layout");
@@ -421,10 +420,10 @@ hipError_t launch_l(const EscnDev& e, const void* x, int in_type, const float* r
   const dim3 grid(unsigned(B * ncb)), block(kEW);
   if (in_type == IN_BF16)
     hipLaunchKernelGGL((k_conv_escn<L, uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x), dws, h, y, C,
-                       int(ncb), e);
+                       int(ncb));
   else
     hipLaunchKernelGGL((k_conv_escn<L, float>), grid, block, 0, s, static_cast<const float*>(x), dws, h, y, C,
-                       int(ncb), e);
+                       int(ncb));
   return hipGetLastError();
 }
 

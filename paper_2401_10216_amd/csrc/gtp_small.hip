@@ -808,9 +808,12 @@ hipError_t launch_pairs_one(const DevTables& t, const void* x1, int it1, const v
 // x1, x2, W and y touch HBM.
 typedef float mixv4 __attribute__((ext_vector_type(4)));
 constexpr int kMixThreads = 256;
+// waves per SIMD of the fused mix: the thread-per-product core's budget,
+// except at L = 8 where the 81 KB tile admits one workgroup per CU anyway
+constexpr int mix_waves(int L) { return L == 8 ? 1 : small_waves(L, L, L); }
 
 template <int L, typename TIn, int NCT>
-__global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(small_waves(L, L, L)))) void k_mix_fused(
+__global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix_waves(L)))) void k_mix_fused(
     const TIn* __restrict__ x1, const TIn* __restrict__ x2, const float* __restrict__ WB, float* __restrict__ y,
     int64_t C1, int64_t C2, int Co, int64_t P, const float* __restrict__ ST, int ntS, const float* __restrict__ WT,
     int ntW) {
