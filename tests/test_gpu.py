@@ -120,6 +120,30 @@ def test_direct_convolution(L1, L2, Lout, n):
     assert err <= TOL, err
 
 
+@pytest.mark.parametrize("L", [5, 6, 7])
+@pytest.mark.parametrize("offset", [0, 1])
+def test_x2_slab_loads_aligned_and_offset(L, offset):
+    """Full workgroups of 64 products read their x2 rows as one slab straight
+    into LDS when x2 is 16-byte aligned (degrees 5..7); an x2 one float off
+    that alignment, and the ragged last workgroup, take per-lane loads.
+    4 full workgroups + 37 products."""
+    n = 4 * 64 + 37
+    rng = np.random.default_rng(300 + 10 * L + offset)
+    a = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    K = O.nsh(L)
+    store = torch.zeros(n * K + 4, device="cuda:0")
+    x2 = store[offset:offset + n * K].view(n, 1, K)
+    x2.copy_(dev(b))
+    assert (x2.data_ptr() % 16 == 0) == (offset == 0)
+    _say(f"x2 slab loads L={L} offset={offset} n={n}")
+    y = gtp.gtp_full(gtp.Plan(L, L, L), dev(a), x2)
+    torch.cuda.synchronize()
+    err = O.max_rel_err(y.cpu().numpy(), O.gtp(a, b, L, L, L))
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
 def test_direct_convolution_bf16_and_empty():
     L = 4
     rng = np.random.default_rng(44)
