@@ -236,7 +236,7 @@ constexpr int escn_waves(int L) { return L <= 6 ? 3 : 2; }
 template <int L, typename TIn>
 __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(L)))) void k_conv_escn(
     const TIn* __restrict__ x, const float* __restrict__ Dall, const float* __restrict__ h, float* __restrict__ y,
-    int64_t C, int ncb) {
+    int64_t C, int ncb, int dma) {
   using EG = EGeo<L>;
   constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR;
   static_assert(EscnConsts<L>::NPAIR == NPAIR && EscnConsts<L>::ERL == EG::ERL, "node-pair table layout");
@@ -262,11 +262,32 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   const TIn* const xb = x + p0 * K;
   const unsigned nx = unsigned(cnt * K);
   float v[K];
-  efor<0, K>([&](auto I) {
-    constexpr int k = decltype(I)::value;
-    const unsigned i = unsigned(tid + k * kEW);
-    v[k] = ld_x(xb, i < nx ? i : nx - 1);
-  });
+  bool staged = false;
+  if constexpr (std::is_same<TIn, float>::value) {
+    if (dma && cnt == kEW && ((p0 * K) & 3) == 0) {
+      // the slab is laid out as the tile: coalesced 16-byte loads straight
+      // into LDS (lane q 64 + tid carries floats 4 (q 64 + tid) .. + 3); a
+      // whole number of 16-byte runs (64 K floats) from a 16-byte aligned
+      // start (base checked by the host, offset here)
+      typedef __attribute__((address_space(3))) void lds_void;
+      typedef const __attribute__((address_space(1))) void glb_void;
+      constexpr int NF = kEW * K, NQ = (NF + 255) / 256;
+      efor<0, NQ>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        const int e = (q * 64 + tid) * 4;
+        if (q + 1 < NQ || e < NF)
+          __builtin_amdgcn_global_load_lds((glb_void*)(xb + e), (lds_void*)(tile + q * 256), 16, 0, 0);
+      });
+      staged = true;
+    }
+  }
+  if (!staged) {
+    efor<0, K>([&](auto I) {
+      constexpr int k = decltype(I)::value;
+      const unsigned i = unsigned(tid + k * kEW);
+      v[k] = ld_x(xb, i < nx ? i : nx - 1);
+    });
+  }
   // (16-byte loads kept as plain floats; indices clamped into range: every
   // lane loads, so the values stay in registers; the out-of-range copies are
   // never stored)
@@ -288,7 +309,11 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
 
   // ---- 2. x rows into registers through the tile, then D into the tile's
   // space
-  efor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
+  if (staged) {
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slab is in LDS
+  } else {
+    efor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
+  }
   __syncthreads();
   float xr[K];
   efor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
@@ -420,10 +445,10 @@ hipError_t launch_l(const EscnDev& e, const void* x, int in_type, const float* r
   const dim3 grid(unsigned(B * ncb)), block(kEW);
   if (in_type == IN_BF16)
     hipLaunchKernelGGL((k_conv_escn<L, uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x), dws, h, y, C,
-                       int(ncb));
+                       int(ncb), 0);
   else
     hipLaunchKernelGGL((k_conv_escn<L, float>), grid, block, 0, s, static_cast<const float*>(x), dws, h, y, C,
-                       int(ncb));
+                       int(ncb), int(reinterpret_cast<uintptr_t>(x) % 16 == 0));
   return hipGetLastError();
 }
 

@@ -583,8 +583,10 @@ def _filter_ref(h, r, L2):
     return h.astype(np.float64)[:, :, deg] * O.real_sh_xyz(L2, u)[:, None, :]
 
 
+# (full 64-channel workgroups read their x slab straight into LDS when it
+# starts 16-byte aligned: C = 65 and 70 mix aligned and unaligned slabs)
 ESCN = [(1, 1, 1, 64), (2, 2, 2, 5), (3, 3, 3, 100), (4, 4, 4, 128), (5, 5, 5, 64), (6, 6, 6, 128), (6, 6, 6, 37),
-        (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3)]
+        (6, 6, 6, 65), (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3)]
 
 
 @pytest.mark.parametrize("L1,L2,Lout,C", ESCN)
