@@ -632,7 +632,15 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
   });
   __syncthreads();
   float* out = y + p0 * KO;
-  for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
+  if (cnt == kTile && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
+    // a full workgroup's rows are 64 KO floats, a whole number of 16-byte
+    // runs: 16-byte stores (the tile is 16-byte aligned)
+    typedef float sv4 __attribute__((ext_vector_type(4)));
+    constexpr int N4 = kTile * KO / 4;
+    for (int i = tid; i < N4; i += kTile) reinterpret_cast<sv4*>(out)[i] = reinterpret_cast<const sv4*>(tile)[i];
+  } else {
+    for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
+  }
 }
 
 // Per-degree weights of one lane's product (WGT = true): scale the K values
@@ -736,7 +744,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   using G1 = Geo<L, L, LO, 0>;
   using G2 = Geo<LO, L, LO, 0>;
   constexpr int KT = cmax(K, KO);
-  __shared__ float tile[kTile * KT];
+  __shared__ __align__(16) float tile[kTile * KT];
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float a[K];
