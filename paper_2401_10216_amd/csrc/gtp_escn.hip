@@ -426,10 +426,21 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   int ln = tid;
   asm volatile("" : "+v"(ln));
   float* const yb = y + p0 * K;
-  efor<0, K>([&](auto I) {
-    const unsigned i = unsigned(ln + decltype(I)::value * kEW);
-    if (i < nx) yb[i] = tile[i];
-  });
+  if (cnt == kEW && (reinterpret_cast<uintptr_t>(yb) & 15) == 0) {
+    // a full workgroup's rows (64 K floats, a whole number of 16-byte runs)
+    // in 16-byte stores from the 16-byte aligned tile
+    typedef float sv4 __attribute__((ext_vector_type(4)));
+    constexpr int N4 = kEW * K / 4, NQ = (N4 + kEW - 1) / kEW;
+    efor<0, NQ>([&](auto Q) {
+      const int i4 = ln + decltype(Q)::value * kEW;
+      if (i4 < N4) reinterpret_cast<sv4*>(yb)[i4] = reinterpret_cast<const sv4*>(tile)[i4];
+    });
+  } else {
+    efor<0, K>([&](auto I) {
+      const unsigned i = unsigned(ln + decltype(I)::value * kEW);
+      if (i < nx) yb[i] = tile[i];
+    });
+  }
 }
 
 template <int L>
