@@ -339,18 +339,21 @@ def test_selfproduct_variants(L, nu, Lout, mode):
     assert err <= TOL, err
 
 
-@pytest.mark.parametrize("L,n", [(4, 262144), (8, 262144), (16, 262144), (32, 262144), (64, 262144)])
-def test_sweep_sampled(L, n):
+@pytest.mark.parametrize("L", [4, 8, 16, 32, 64])
+def test_sweep_sampled(L):
+    """The degree sweep at its full size and launch shape ([2048, 128, K]
+    inputs, 262144 products): a seeded subsample checked one by one."""
     x1, x2 = inputs.sweep_inputs(L)
-    x1 = x1.reshape(-1, O.nsh(L))[:n]
-    x2 = x2.reshape(-1, O.nsh(L))[:n]
-    _say(f"sweep L={L} n={n}")
+    B, C = x1.shape[0], x1.shape[1]
+    n = B * C
+    _say(f"sweep L={L} B={B} C={C}")
     plan = gtp.Plan(L, L, L)
-    y = gtp.gtp_full(plan, dev(x1)[:, None], dev(x2)[:, None])
+    y = gtp.gtp_full(plan, dev(x1), dev(x2))
     torch.cuda.synchronize()
     idx = inputs.sample_indices(4, n, 256 if L >= 32 else 1024)
-    yf = y[torch.from_numpy(idx).cuda(), 0].cpu().numpy()
-    ref = oracle_pair(x1[idx].astype(np.float64), x2[idx].astype(np.float64), L, L, L)
+    yf = y.view(n, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    a, b = x1.reshape(n, -1)[idx], x2.reshape(n, -1)[idx]
+    ref = oracle_pair(a.astype(np.float64), b.astype(np.float64), L, L, L)
     err = O.max_rel_err(yf, ref)
     _say(f"  err={err:.3e}")
     assert err <= TOL
@@ -530,6 +533,30 @@ def test_weighted_ragged(L1, L2, Lout, per_channel):
     ref = O.gtp_weighted(a.reshape(B * C, -1)[sel], b.reshape(B * C, -1)[sel], w1[rows[sel]], w2[rows[sel]],
                          wo[rows[sel]], L1, L2, Lout)
     err = O.max_rel_err(y.view(B * C, -1).cpu().numpy()[sel], ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
+
+
+def test_weighted_edge_workload_sampled():
+    """Weighted products at the edge workload's full size (B=65536, C=128,
+    L=6, one weight row shared by every channel), as the weighted benchmark
+    launches them: a seeded subsample checked one by one."""
+    cfg = inputs.WORKLOADS["edge"]
+    B, C, L = cfg["B"], cfg["C"], cfg["L1"]
+    x1, r, h = inputs.edge_inputs(B, C, L)
+    t1 = dev(x1)
+    t2 = gtp.gtp_sh_filter(L, dev(r.astype(np.float32)), dev(h))
+    rng = np.random.default_rng(140)
+    w = [rng.standard_normal((1, L + 1)).astype(np.float32) for _ in range(3)]
+    _say("weighted edge full size")
+    y = gtp.gtp_full_weighted(gtp.Plan(L, L, L), t1, t2, dev(w[0]), dev(w[1]), dev(w[2]), False)
+    torch.cuda.synchronize()
+    idx = inputs.sample_indices(7, B * C, 4096)
+    bi, ci = idx // C, idx % C
+    a = x1[bi, ci].astype(np.float64)
+    b = h[bi, ci][:, inputs.degree_of_index(L)] * O.real_sh_xyz(L, r[bi])
+    ref = O.gtp_weighted(a, b, w[0][0], w[1][0], w[2][0], L, L, L)
+    err = O.max_rel_err(y.view(B * C, -1)[torch.from_numpy(idx).cuda()].cpu().numpy(), ref)
     _say(f"  err={err:.3e}")
     assert err <= TOL, err
 
