@@ -109,11 +109,17 @@ struct WGeo {
   static constexpr int NXKP = (NXK + 3) / 4 * 4;
 };
 
+// The value of lane i ^ 8: a DPP rotate by 8 within each 16-lane row (a
+// plain VALU move, no LDS round trip as with a lane permute).
+__device__ __forceinline__ float xor8(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128 /* row_ror:8 */, 0xf, 0xf, true));
+}
+
 // m = 0 theta synthesis reduction: lane (g, 8h + pi) holds the partial sum
 // over l = g + 4h (mod 8); returns the value at the lane's column node (the
 // node itself for h = 0, its mirror, odd l negated, for h = 1).
 __device__ __forceinline__ float m0_reduce(float a, int g, int h) {
-  a += __shfl_xor(a, 8);
+  a += xor8(a);
   const float t = __shfl_xor(a, 16);
   const float sum = a + t, dif = (g & 1) ? t - a : a - t;
   const float node = sum + __shfl_xor(sum, 32), mirror = dif + __shfl_xor(dif, 32);
@@ -133,12 +139,13 @@ template <int L>
 struct WaveCtx {
   using G = WGeo<L>;
   int lane, g, h, pi;
+  float sg;  // +1 for h = 0 (node), -1 for h = 1 (mirror)
   const float4* xq;
   __amdgpu_buffer_rsrc_t SPr, S0r;
   const float* TWR;
 
   __device__ __forceinline__ WaveCtx(int lane_, const float4* xq_, const DevTables& t)
-      : lane(lane_), g(lane_ >> 4), h((lane_ >> 3) & 1), pi(lane_ & 7), xq(xq_), TWR(t.TWR) {
+      : lane(lane_), g(lane_ >> 4), h((lane_ >> 3) & 1), pi(lane_ & 7), sg(h ? -1.0f : 1.0f), xq(xq_), TWR(t.TWR) {
     SPr = table_rsrc(t.SMP, G::PASSES * G::TU2 * 64 * 4);
     S0r = table_rsrc(t.SM0P, (G::PASSES + 1) * 64 * G::NV0P);
   }
@@ -255,13 +262,13 @@ struct WaveCtx {
           ast[mr] = seeds[(G::AST + 4 * mr) / 4];
         });
       }
-      // column value: node jp (h = 0: own even + partner odd) or its mirror (h = 1: partner even - own odd)
+      // column value: node jp (h = 0: own even + partner odd) or its mirror
+      // (h = 1: partner even - own odd); sg * v + partner is exact for sg = +-1
       f4 Bo, Be;
       lfor<0, 4>([&](auto C) {
         constexpr int cc = decltype(C)::value;
-        const float po = __shfl_xor(Vo[cc], 8), pe = __shfl_xor(Ve[cc], 8);
-        Bo[cc] = h ? po - Vo[cc] : po + Vo[cc];
-        Be[cc] = h ? pe - Ve[cc] : pe + Ve[cc];
+        Bo[cc] = fmaf(sg, Vo[cc], xor8(Vo[cc]));
+        Be[cc] = fmaf(sg, Ve[cc], xor8(Ve[cc]));
       });
       lfor<0, NMB>([&](auto MB) {
         constexpr int mb = decltype(MB)::value;
@@ -360,16 +367,15 @@ struct WaveCtx {
         lfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
           const int m = 2 * (16 * mr + 4 * g + r) + (odd ? 1 : 2);
-          const float pc = __shfl_xor(o[mr][odd][r], 8), ps = __shfl_xor(o[mr][odd + 2][r], 8);
-          const float vc = h ? pc - o[mr][odd][r] : pc + o[mr][odd][r];
-          const float vs = h ? ps - o[mr][odd + 2][r] : ps + o[mr][odd + 2][r];
+          const float vc = fmaf(sg, o[mr][odd][r], xor8(o[mr][odd][r]));
+          const float vs = fmaf(sg, o[mr][odd + 2][r], xor8(o[mr][odd + 2][r]));
           // m-rows past L exist only at L = 16 (16 rows per class)
           if (L != 16 || m <= L) *reinterpret_cast<float2*>(eoh + 2 * m) = make_float2(vc, vs);
         });
       });
     });
-    const float pz = __shfl_xor(zz, 8);
-    if (g == 0) eoh[0] = h ? pz - zz : pz + zz;
+    const float vz = fmaf(sg, zz, xor8(zz));
+    if (g == 0) eoh[0] = vz;
   }
 };
 
@@ -554,7 +560,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
   }
   const float f = p1 * p2 * float(NP);
-  const float fN = __shfl(f, 0), fS = __shfl(f, 8);
+  const float fN = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 0));  // wave-uniform
+  const float fS = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 8));
   if (lane <= L) {
     const int l = lane;
     y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
@@ -618,7 +625,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
   }
   const float f = p1 * p2 * float(NP);
-  const float fN = __shfl(f, 0), fS = __shfl(f, 8);
+  const float fN = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 0));  // wave-uniform
+  const float fS = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 8));
   __syncthreads();  // the x image is dead
   w.store_moments(eo_odd + wave * EOP, o, zz);
   __syncthreads();
