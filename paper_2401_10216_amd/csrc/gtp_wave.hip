@@ -115,14 +115,28 @@ __device__ __forceinline__ float xor8(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128 /* row_ror:8 */, 0xf, 0xf, true));
 }
 
+// The two rows of each 16-lane row pair (2k, 2k + 1), in every lane of the
+// pair: gfx950's permlane16 swap of a value with itself leaves row 2k's
+// value in the first result and row 2k + 1's in the second.  Likewise the
+// two 32-lane halves (permlane32 swap).
+__device__ __forceinline__ void row_pair(float v, float& even, float& odd) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  even = __uint_as_float(r[0]);
+  odd = __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float half_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // m = 0 theta synthesis reduction: lane (g, 8h + pi) holds the partial sum
 // over l = g + 4h (mod 8); returns the value at the lane's column node (the
 // node itself for h = 0, its mirror, odd l negated, for h = 1).
-__device__ __forceinline__ float m0_reduce(float a, int g, int h) {
+__device__ __forceinline__ float m0_reduce(float a, int h) {
   a += xor8(a);
-  const float t = __shfl_xor(a, 16);
-  const float sum = a + t, dif = (g & 1) ? t - a : a - t;
-  const float node = sum + __shfl_xor(sum, 32), mirror = dif + __shfl_xor(dif, 32);
+  float e, o;  // rows g = 0, 2 (l = 0, 2 mod 4) and g = 1, 3 (l = 1, 3 mod 4)
+  row_pair(a, e, o);
+  const float node = half_sum(e + o), mirror = half_sum(e - o);
   return h ? mirror : node;
 }
 
@@ -174,8 +188,8 @@ struct WaveCtx {
         s2 = fmaf(sv[v], q.z, s2);
       }
     });
-    a1 = m0_reduce(s1, g, h);
-    a2 = m0_reduce(s2, g, h);
+    a1 = m0_reduce(s1, h);
+    a2 = m0_reduce(s2, h);
   }
 
   // One pass (8 mirror pairs, jp = 8 pu + pi + 1): theta synthesis, phi
@@ -351,8 +365,11 @@ struct WaveCtx {
         });
       });
     });
-    zz += __shfl_xor(zz, 16);
-    zz += __shfl_xor(zz, 32);
+    {
+      float ze, zo;
+      row_pair(zz, ze, zo);
+      zz = half_sum(ze + zo);
+    }
   }
 
   // ---- 3. mirror combination into LDS, eo[parity][pi][slot]: parity 0 =
