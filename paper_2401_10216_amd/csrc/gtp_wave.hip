@@ -66,6 +66,9 @@ __device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
 // All table reads are lane-permuted copies read as one 16-byte load per lane
 // (the texture-address unit, not the bytes, bounds the table traffic).
 typedef float f4 __attribute__((ext_vector_type(4)));
+// an 8-byte-aligned (cos, sin) moment pair, read from LDS as one 64-bit load
+// whose immediate offset reaches the whole moment block
+typedef float f2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ f4 mfma4(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -247,10 +250,12 @@ struct WaveCtx {
     f4 ast[NMR];
     lfor<0, NKS>([&](auto SS) {
       constexpr int s = decltype(SS)::value;
-      const int c = 4 * s + g;
+      // the x block of m-pair c = 4 s + g: xb(4 s + g) = xb(4 s) + g (1 + 4 nu(s)),
+      // written so that only the g term is left to run time
+      const int xo = G::xb(4 * s) + g * (1 + 4 * G::nu(s));
       // this lane's parity: h = 0 takes (mo, l_a) and (mo+1, l_b), h = 1 (mo, l_b) and (mo+1, l_a)
-      const float4* xa = xq + G::xb(c) + h;
-      const float4* xe = xq + G::xb(c) + 3 - h;
+      const float4* xa = xq + xo + h;
+      const float4* xe = xq + xo + 3 - h;
       f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
       lfor<0, G::nu(s) / 2>([&](auto U2) {
         constexpr int u2 = decltype(U2)::value, tt = G::u2off(s) + u2;
@@ -496,8 +501,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
   constexpr int NJ = G::NJ, NP = G::NP;
   constexpr int NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
-  __shared__ __align__(16) float xs[G::XQ * 4];
-  __shared__ __align__(16) float eo[G::EOP];
+  // the moments first: their reads then carry small immediate offsets
+  __shared__ __align__(16) float lds[G::EOP + G::XQ * 4];
+  float* const eo = lds;
+  float* const xs = lds + G::EOP;
 
   const int lane = threadIdx.x;
   const int64_t P = blockIdx.x;
@@ -556,7 +563,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
         lfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
-          const float2 cs = *reinterpret_cast<const float2*>(eo + er[it] + jj * NMP2);
+          const f2 cs = *reinterpret_cast<const f2*>(eo + er[it] + jj * NMP2);
           yc[it] = fmaf(wv[jj], cs.x, yc[it]);
           ys[it] = fmaf(wv[jj], cs.y, ys[it]);
         });
@@ -660,7 +667,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
       lfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
-        const float2 cs = *reinterpret_cast<const float2*>(eop + er + jj * NMP2);
+        const f2 cs = *reinterpret_cast<const f2*>(eop + er + jj * NMP2);
         ac = fmaf(wv[jj], cs.x, ac);
         if (with_sin) as = fmaf(wv[jj], cs.y, as);
       });
