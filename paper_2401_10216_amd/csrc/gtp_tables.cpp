@@ -191,13 +191,17 @@ Tables build_tables(int L1, int L2, int Lout) {
 //   TWR[lane][TWRN]  seeds of the phi operands for rotation recurrences
 //                    (NMBP = NMB rounded up to even; NMR = 16-row blocks of
 //                    analysis m-rows per class, L / 32 at L = 64, else 1): per
-//                    mb (k = 16 mb + i, zero for k > Q) cos/sin of (2g+2) phi_k,
-//                    cos/sin of (2g+1) phi_k, cos/sin of 8 phi_k (entries
-//                    6 mb .. 6 mb + 5); from ASD = 6 NMBP, per (mr, mb)
-//                    (k0 = 16 mb + 4 g, m = 2(16 mr + i) + 2) cos/sin of m phi_k0
-//                    and of (m - 1) phi_k0 (entries ASD + 4 (mr NMBP + mb) ..);
-//                    from AST = ASD + 4 NMR NMBP, per mr cos/sin of m phi_1 and
-//                    of (m - 1) phi_1; zero where m > L.  TWRN = AST + 4 NMR.
+//                    mb (k = 16 mb + 4 (i mod 4) + i / 4, zero for k > Q: the
+//                    synthesis row i holds that sample, so that register r of
+//                    lane group g of the result holds sample 16 mb + 4 r + g)
+//                    cos/sin of (2g+2) phi_k, cos/sin of (2g+1) phi_k, cos/sin
+//                    of 8 phi_k (entries 6 mb .. 6 mb + 5); from ASD = 6 NMBP,
+//                    per (mr, mb) (k0 = 16 mb + g, m = 2(16 mr + i) + 2) cos/sin
+//                    of m phi_k0 and of (m - 1) phi_k0 (entries
+//                    ASD + 4 (mr NMBP + mb) ..); from AST = ASD + 4 NMR NMBP,
+//                    per mr cos/sin of m phi_4 and of (m - 1) phi_4 (the step
+//                    from register r to r + 1); zero where m > L.
+//                    TWRN = AST + 4 NMR.
 //   SMP[pass][s][u2][lane][4]  Theta_{mo+2u+h, mo}(t_jp),
 //                    Theta_{me+2u-h, me}(t_jp) for u = 2 u2, then u = 2 u2 + 1
 //                    (mo = 8s + 2g + 1, me = mo + 1; zero outside m <= l <= L);
@@ -258,7 +262,7 @@ void build_wave_tables(Tables& t) {
     const int g = lane / 16, i = lane % 16;
     double* o = &t.TWR[size_t(lane) * TWRN];
     for (int mb = 0; mb < NMB; ++mb) {
-      const int k = 16 * mb + i;
+      const int k = 16 * mb + 4 * (i % 4) + i / 4;
       if (k <= Q) {
         o[6 * mb + 0] = trig(false, 2 * g + 2, k);
         o[6 * mb + 1] = trig(true, 2 * g + 2, k);
@@ -267,7 +271,7 @@ void build_wave_tables(Tables& t) {
         o[6 * mb + 4] = trig(false, 8, k);
         o[6 * mb + 5] = trig(true, 8, k);
       }
-      const int k0 = 16 * mb + 4 * g;
+      const int k0 = 16 * mb + g;
       for (int mr = 0; mr < NMR; ++mr) {
         const int me = 2 * (16 * mr + i) + 2, mo = me - 1;
         double* a = &o[ASD + 4 * (mr * NMBP + mb)];
@@ -284,12 +288,12 @@ void build_wave_tables(Tables& t) {
     for (int mr = 0; mr < NMR; ++mr) {
       const int me = 2 * (16 * mr + i) + 2, mo = me - 1;
       if (me <= L) {
-        o[AST + 4 * mr + 0] = trig(false, me, 1);
-        o[AST + 4 * mr + 1] = trig(true, me, 1);
+        o[AST + 4 * mr + 0] = trig(false, me, 4);
+        o[AST + 4 * mr + 1] = trig(true, me, 4);
       }
       if (mo <= L) {
-        o[AST + 4 * mr + 2] = trig(false, mo, 1);
-        o[AST + 4 * mr + 3] = trig(true, mo, 1);
+        o[AST + 4 * mr + 2] = trig(false, mo, 4);
+        o[AST + 4 * mr + 3] = trig(true, mo, 4);
       }
     }
   }

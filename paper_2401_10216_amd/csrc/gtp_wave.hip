@@ -57,7 +57,9 @@ __device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
 //              (w_k = 1/2 at k = 0, Q, where a 4-point set repeats points).
 // The accumulator layout of one contraction is the B layout of the next
 // (register r of lane (g, i) holds row 4 g + r, column i), so nothing moves
-// between them.  The A operands are generated in registers from per-lane
+// between them; synthesis row 4 g + r computes sample k = 16 mb + 4 r + g, so
+// that each analysis contraction (fixed r, K index g) takes four consecutive
+// samples and those past Q drop out whole.  The A operands are generated in registers from per-lane
 // seeds by angle-addition rotations.  Theta synthesis (VALU) produces the B
 // operands in place: in K-step s lane (g, 8h + pi) sums the m-parts
 // m = 8s + 2g + 1 and + 2 at node jp over the l with l - m = h (mod 2); one
@@ -342,8 +344,10 @@ struct WaveCtx {
     });
 
     // ---- 2c. phi analysis contractions; operands per k block from the seeds:
-    // w_k trig(m phi_k), k = 16 mb + 4 g + r, m = 2(16 mr + i) + 2 (even
-    // types) or + 1 (odd types)
+    // w_k trig(m phi_k), k = 16 mb + 4 r + g (the synthesis rows are ordered
+    // so that register r of lane group g holds that sample), m = 2(16 mr + i)
+    // + 2 (even types) or + 1 (odd types).  A contraction whose four samples
+    // all lie past Q (weight zero) is skipped.
     lfor<0, NMR>([&](auto MR) {
       lfor<0, 4>([&](auto TY) { o[decltype(MR)::value][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
     });
@@ -355,18 +359,20 @@ struct WaveCtx {
         float ce = asd[mr][4 * mb + 0], se = asd[mr][4 * mb + 1], co = asd[mr][4 * mb + 2], so = asd[mr][4 * mb + 3];
         lfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
-          if constexpr (r > 0) {
-            rot(ce, se, ast[mr].x, ast[mr].y);
-            rot(co, so, ast[mr].z, ast[mr].w);
+          if constexpr (16 * mb + 4 * r <= G::Q) {
+            if constexpr (r > 0) {
+              rot(ce, se, ast[mr].x, ast[mr].y);
+              rot(co, so, ast[mr].z, ast[mr].w);
+            }
+            const int k = 16 * mb + 4 * r + g;
+            constexpr float fold = L < 64 ? 4.0f : 1.0f;  // see the sample products
+            const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f * fold : fold;
+            o[mr][0] = mfma4(wk * ce, acc[0][mb][0][r], o[mr][0]);
+            o[mr][1] = mfma4(wk * co, acc[0][mb][1][r], o[mr][1]);
+            o[mr][2] = mfma4(wk * se, acc[0][mb][2][r], o[mr][2]);
+            o[mr][3] = mfma4(wk * so, acc[0][mb][3][r], o[mr][3]);
+            if constexpr (mr == 0) zz = fmaf(wk, acc[0][mb][0][r], zz);
           }
-          const int k = 16 * mb + 4 * g + r;
-          constexpr float fold = L < 64 ? 4.0f : 1.0f;  // see the sample products
-          const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f * fold : fold;
-          o[mr][0] = mfma4(wk * ce, acc[0][mb][0][r], o[mr][0]);
-          o[mr][1] = mfma4(wk * co, acc[0][mb][1][r], o[mr][1]);
-          o[mr][2] = mfma4(wk * se, acc[0][mb][2][r], o[mr][2]);
-          o[mr][3] = mfma4(wk * so, acc[0][mb][3][r], o[mr][3]);
-          if constexpr (mr == 0) zz = fmaf(wk, acc[0][mb][0][r], zz);
         });
       });
     });

@@ -161,10 +161,12 @@ def replay(plan, L, x1, x2):
             for mb in range(NMB):
                 ce, se, co, so = (TWR[:, ASD + 4 * (mr * NMBP + mb) + e].copy() for e in range(4))
                 for r in range(4):
+                    if 16 * mb + 4 * r > Q:
+                        break  # all four samples past Q: the kernel skips the contraction
                     if r:
                         ce, se = _rot(ce, se, st[:, 0], st[:, 1])
                         co, so = _rot(co, so, st[:, 2], st[:, 3])
-                    k = 16 * mb + 4 * g + r
+                    k = 16 * mb + 4 * r + g  # register r of lane group g holds this sample
                     w = np.where(k > Q, 0.0, np.where((k == 0) | (k == Q), 0.5, 1.0))
                     for ty, opnd in enumerate((ce, co, se, so)):
                         o[mr, ty] = _mfma(w * opnd, acc[0, mb, ty][:, r], o[mr, ty])
@@ -263,16 +265,24 @@ def test_seed_table_angles(L):
     for lane in range(64):
         g, i = lane // 16, lane % 16
         for mb in range(G["NMB"]):
-            k = 16 * mb + i
+            # synthesis row i computes sample 16 mb + 4 (i mod 4) + i // 4
+            k = 16 * mb + 4 * (i % 4) + i // 4
             want = [*cs(2 * g + 2, k), *cs(2 * g + 1, k), *cs(8, k)] if k <= Q else [0.0] * 6
             assert np.allclose(TWR[lane, 6 * mb:6 * mb + 6], want, atol=1e-14)
-            k0 = 16 * mb + 4 * g
+            k0 = 16 * mb + g
             for mr in range(G["NMR"]):
                 me = 2 * (16 * mr + i) + 2
                 want = [*cs(me, k0), *cs(me - 1, k0)]
                 want = [v if (me - e // 2) <= L else 0.0 for e, v in enumerate(want)]
                 a = G["ASD"] + 4 * (mr * NMBP + mb)
                 assert np.allclose(TWR[lane, a:a + 4], want, atol=1e-14)
+        for mr in range(G["NMR"]):
+            # rotation from register r to r + 1: four samples on
+            me = 2 * (16 * mr + i) + 2
+            want = [*cs(me, 4), *cs(me - 1, 4)]
+            want = [v if (me - e // 2) <= L else 0.0 for e, v in enumerate(want)]
+            a = G["AST"] + 4 * mr
+            assert np.allclose(TWR[lane, a:a + 4], want, atol=1e-14)
 
 
 @pytest.mark.parametrize("L", [16, 32, 64])
