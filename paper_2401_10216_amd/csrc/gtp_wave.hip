@@ -739,6 +739,8 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
 template <int L>
 hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                            float* y, const DegWeights& wt, hipStream_t s, bool* supported) {
+  // the scatter map's slots must fit the kernel's LDS image
+  if (t.XQUADS != WGeo<L>::XQ) return hipErrorInvalidValue;
   if (wt.on) {
     if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float, true>(x1, x2, n, y, t, wt, s);
     if (it1 == IN_BF16 && it2 == IN_BF16)
