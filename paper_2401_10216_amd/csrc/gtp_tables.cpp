@@ -221,7 +221,10 @@ Tables build_tables(int L1, int L2, int Lout) {
 //                    (quad l), then for each m-pair c (m = 2c + 1, 2c + 2) 4
 //                    quads per u-step (2c+1, l_a), (2c+1, l_b), (2c+2, l_a),
 //                    (2c+2, l_b) with l_a = 2c + 1 + 2u, l_b = l_a + 1, for
-//                    nu(c / 4) u-steps, and one pad quad.
+//                    the nu(c / 4) - c % 4 u-steps that hold a coefficient,
+//                    and one pad quad.  XQUADS also covers the reads of every
+//                    group's nu(c / 4) u-steps (past its block: the next
+//                    blocks, then a zero tail).
 void build_wave_tables(Tables& t) {
   const int L = t.L1;
   if (t.L2 != L || t.Lout != L || (L != 16 && L != 32 && L != 64)) throw std::invalid_argument("wave tables: bad degree");
@@ -237,7 +240,7 @@ void build_wave_tables(Tables& t) {
   // x scatter map; pair blocks hold nu(s) = L/2 - 4s u-steps (s = c / 4)
   std::vector<int> xb(L / 2 + 1);
   xb[0] = L + 1;
-  for (int c = 0; c < L / 2; ++c) xb[c + 1] = xb[c] + 4 * (L / 2 - 4 * (c / 4)) + 1;
+  for (int c = 0; c < L / 2; ++c) xb[c + 1] = xb[c] + 4 * (L / 2 - 4 * (c / 4) - c % 4) + 1;
   const int K = (L + 1) * (L + 1);
   std::vector<int> xmap(K, 0);
   for (int l = 0; l <= L; ++l)
@@ -251,6 +254,7 @@ void build_wave_tables(Tables& t) {
       xmap[size_t(l) * l + l + ms] = 4 * quad + (ms < 0 ? 1 : 0);
     }
   t.XQUADS = xb[L / 2];
+  for (int c = 0; c < L / 2; ++c) t.XQUADS = std::max(t.XQUADS, xb[c] + 4 * (L / 2 - 4 * (c / 4)));
   const int NXK = (K + NTH - 1) / NTH, NXKP = (NXK + 3) / 4 * 4;
   t.XMAPP.assign(size_t(NTH) * NXKP, -1);
   for (int tid = 0; tid < NTH; ++tid)

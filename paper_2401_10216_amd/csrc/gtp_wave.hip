@@ -100,11 +100,23 @@ struct WGeo {
   // u-steps (two degrees each) of K-step s
   __host__ __device__ static constexpr int nu(int s) { return L / 2 - 4 * s; }
   // quad offset of the x block of m-pair c = 4 s + g (m = 2c + 1, 2c + 2): the
-  // m = 0 block (L + 1 quads) first, then 4 nu(s) quads + 1 pad per pair
+  // m = 0 block (L + 1 quads) first, then per pair 4 quads for each of the
+  // nu(s) - g u-steps that hold a coefficient, + 1 pad.  Group g still runs
+  // all nu(s) u-steps of its K-step: the last g of them read the next blocks
+  // (finite values, whose theta-table entries are zero: l > L there), the
+  // last blocks' a zero tail.
   __host__ __device__ static constexpr int xb(int c) {
-    return (L + 1) + c + 4 * (4 * ((c / 4) * (L / 2) - 2 * (c / 4) * (c / 4 - 1)) + (c % 4) * nu(c / 4));
+    int q = L + 1;
+    for (int i = 0; i < c; ++i) q += 4 * (nu(i / 4) - i % 4) + 1;
+    return q;
   }
-  static constexpr int XQ = xb(L / 2);
+  // quads the image spans: the blocks and the reach of every group's reads
+  __host__ __device__ static constexpr int x_quads() {
+    int e = xb(L / 2);
+    for (int c = 0; c < L / 2; ++c) e = e > xb(c) + 4 * nu(c / 4) ? e : xb(c) + 4 * nu(c / 4);
+    return e;
+  }
+  static constexpr int XQ = x_quads();
   // u-step pairs before K-step s, and in all K-steps
   __host__ __device__ static constexpr int u2off(int s) { return s * (L / 4) - s * (s - 1); }
   static constexpr int TU2 = u2off(NKS);
@@ -252,9 +264,9 @@ struct WaveCtx {
     f4 ast[NMR];
     lfor<0, NKS>([&](auto SS) {
       constexpr int s = decltype(SS)::value;
-      // the x block of m-pair c = 4 s + g: xb(4 s + g) = xb(4 s) + g (1 + 4 nu(s)),
-      // written so that only the g term is left to run time
-      const int xo = G::xb(4 * s) + g * (1 + 4 * G::nu(s));
+      // the x block of m-pair c = 4 s + g: xb(4 s + g) = xb(4 s) + g (4 nu(s) + 1)
+      // - 2 g (g - 1), written so that only the g terms are left to run time
+      const int xo = G::xb(4 * s) + g * (4 * G::nu(s) + 1) - 2 * g * (g - 1);
       // this lane's parity: h = 0 takes (mo, l_a) and (mo+1, l_b), h = 1 (mo, l_b) and (mo+1, l_a)
       const float4* xa = xq + xo + h;
       const float4* xe = xq + xo + 3 - h;
@@ -522,7 +534,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   // theta-analysis rows: tri(l, 0) with l = lane (l <= L), and the rows with
   // m > 0 numbered q = lane + 64 it
   float y0 = 0.0f, yc[NIT], ys[NIT];
-  const int wr0 = (lane * (lane + 1) / 2) * 4, er0 = (lane & 1) * 8 * NMP2;
+  const int wr0 = (lane * (lane + 1) / 2) * 4;
   lfor<0, NIT>([&](auto IT) {
     yc[decltype(IT)::value] = 0.0f;
     ys[decltype(IT)::value] = 0.0f;
@@ -558,7 +570,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
       const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
       lfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
-        y0 = fmaf(wv[jj], eo[er0 + jj * NMP2], y0);
+        y0 = fmaf(wv[jj], eo[(lnp & 1) * 8 * NMP2 + jj * NMP2], y0);  // row tri(lane, 0)
       });
     }
     lfor<0, NIT>([&](auto IT) {

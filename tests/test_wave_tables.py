@@ -40,10 +40,12 @@ def _geo(L, NP):
     G["TU2"] = G["u2off"](G["NKS"])
 
     def xb(c):
-        return (L + 1) + sum(4 * nu(q // 4) + 1 for q in range(c))
+        # pair blocks hold the nu(s) - g u-steps that have a coefficient, + 1 pad
+        return (L + 1) + sum(4 * (nu(q // 4) - q % 4) + 1 for q in range(c))
 
     G["xb"] = xb
-    G["XQ"] = xb(L // 2)
+    # the image also covers every group's reads of all nu(s) u-steps
+    G["XQ"] = max([xb(L // 2)] + [xb(c) + 4 * nu(c // 4) for c in range(L // 2)])
     return G
 
 
