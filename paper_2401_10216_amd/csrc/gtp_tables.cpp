@@ -196,8 +196,10 @@ Tables build_tables(int L1, int L2, int Lout) {
 //                    lane group g of the result holds sample 16 mb + 4 r + g)
 //                    cos/sin of (2g+2) phi_k, cos/sin of (2g+1) phi_k, cos/sin
 //                    of 8 phi_k (entries 6 mb .. 6 mb + 5); from ASD = 6 NMBP,
-//                    per (mr, mb) (k0 = 16 mb + g, m = 2(16 mr + i) + 2) cos/sin
-//                    of m phi_k0 and of (m - 1) phi_k0 (entries
+//                    per (mr, mb) (k0 = 16 mb + g, m = 2(16 mr + i) + 2) fold
+//                    times cos/sin of m phi_k0 and of (m - 1) phi_k0 (fold = 4
+//                    below L = 64, where the kernel folds the sample products
+//                    as class sums, else 1; entries
 //                    ASD + 4 (mr NMBP + mb) ..); from AST = ASD + 4 NMR NMBP,
 //                    per mr cos/sin of m phi_4 and of (m - 1) phi_4 (the step
 //                    from register r to r + 1); zero where m > L.
@@ -232,6 +234,9 @@ void build_wave_tables(Tables& t) {
   const int NMBP = (NMB + 1) / 2 * 2;                        // seed layout per lane
   const int NMR = L > 32 ? L / 32 : 1, ASD = 6 * NMBP, AST = ASD + 4 * NMR * NMBP, TWRN = AST + 4 * NMR;
   const int NTH = L > 32 ? 256 : 64;                         // threads per product
+  // weight every phi sample shares in the analysis: the 4-point sets' products
+  // enter as class sums (a quarter of the four sample products) below L = 64
+  const double fold = L < 64 ? 4.0 : 1.0;
   auto trig = [&](bool is_sin, int m, int k) {
     const double ang = 2.0 * kPi * double((int64_t(m) * k) % NP) / NP;
     return is_sin ? std::sin(ang) : std::cos(ang);
@@ -280,12 +285,12 @@ void build_wave_tables(Tables& t) {
         const int me = 2 * (16 * mr + i) + 2, mo = me - 1;
         double* a = &o[ASD + 4 * (mr * NMBP + mb)];
         if (me <= L) {
-          a[0] = trig(false, me, k0);
-          a[1] = trig(true, me, k0);
+          a[0] = fold * trig(false, me, k0);
+          a[1] = fold * trig(true, me, k0);
         }
         if (mo <= L) {
-          a[2] = trig(false, mo, k0);
-          a[3] = trig(true, mo, k0);
+          a[2] = fold * trig(false, mo, k0);
+          a[3] = fold * trig(true, mo, k0);
         }
       }
     }

@@ -127,7 +127,8 @@ struct WGeo {
 };
 
 // The value of lane i ^ 8: a DPP rotate by 8 within each 16-lane row (a
-// plain VALU move, no LDS round trip as with a lane permute).
+// plain VALU move, no LDS round trip as with a lane permute).  These
+// exchanges run with all 64 lanes active (no divergent branch around them).
 __device__ __forceinline__ float xor8(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128 /* row_ror:8 */, 0xf, 0xf, true));
 }
@@ -356,7 +357,7 @@ struct WaveCtx {
     });
 
     // ---- 2c. phi analysis contractions; operands per k block from the seeds:
-    // w_k trig(m phi_k), k = 16 mb + 4 r + g (the synthesis rows are ordered
+    // w_k trig(m phi_k) (the seeds hold fold * trig), k = 16 mb + 4 r + g (the synthesis rows are ordered
     // so that register r of lane group g holds that sample), m = 2(16 mr + i)
     // + 2 (even types) or + 1 (odd types).  A contraction whose four samples
     // all lie past Q (weight zero) is skipped.
@@ -376,14 +377,25 @@ struct WaveCtx {
               rot(ce, se, ast[mr].x, ast[mr].y);
               rot(co, so, ast[mr].z, ast[mr].w);
             }
-            const int k = 16 * mb + 4 * r + g;
-            constexpr float fold = L < 64 ? 4.0f : 1.0f;  // see the sample products
-            const float wk = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f * fold : fold;
-            o[mr][0] = mfma4(wk * ce, acc[0][mb][0][r], o[mr][0]);
-            o[mr][1] = mfma4(wk * co, acc[0][mb][1][r], o[mr][1]);
-            o[mr][2] = mfma4(wk * se, acc[0][mb][2][r], o[mr][2]);
-            o[mr][3] = mfma4(wk * so, acc[0][mb][3][r], o[mr][3]);
-            if constexpr (mr == 0) zz = fmaf(wk, acc[0][mb][0][r], zz);
+            // the seeds carry the weight shared by all samples (fold: see the
+            // sample products); only a contraction holding k = 0, Q or samples
+            // past Q scales its operands by 1/2 or 0 per lane
+            constexpr float fold = L < 64 ? 4.0f : 1.0f;
+            if constexpr (16 * mb + 4 * r > 0 && 16 * mb + 4 * r + 3 < G::Q) {
+              o[mr][0] = mfma4(ce, acc[0][mb][0][r], o[mr][0]);
+              o[mr][1] = mfma4(co, acc[0][mb][1][r], o[mr][1]);
+              o[mr][2] = mfma4(se, acc[0][mb][2][r], o[mr][2]);
+              o[mr][3] = mfma4(so, acc[0][mb][3][r], o[mr][3]);
+              if constexpr (mr == 0) zz = fmaf(fold, acc[0][mb][0][r], zz);
+            } else {
+              const int k = 16 * mb + 4 * r + g;
+              const float wr = k > G::Q ? 0.0f : (k == 0 || k == G::Q) ? 0.5f : 1.0f;
+              o[mr][0] = mfma4(wr * ce, acc[0][mb][0][r], o[mr][0]);
+              o[mr][1] = mfma4(wr * co, acc[0][mb][1][r], o[mr][1]);
+              o[mr][2] = mfma4(wr * se, acc[0][mb][2][r], o[mr][2]);
+              o[mr][3] = mfma4(wr * so, acc[0][mb][3][r], o[mr][3]);
+              if constexpr (mr == 0) zz = fmaf(wr * fold, acc[0][mb][0][r], zz);
+            }
           }
         });
       });

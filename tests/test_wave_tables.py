@@ -149,12 +149,20 @@ def replay(plan, L, x1, x2):
         for mb in range(NMB):
             pe1, po1, qe1, qo1 = acc[0, mb]
             pe2, po2, qe2, qo2 = acc[1, mb]
+            if L < 64:
+                # class sums: a quarter of the four sample products (the seeds carry the 4)
+                acc[0, mb] = np.stack([pe1 * pe2 + po1 * po2 + qe1 * qe2 + qo1 * qo2,
+                                       pe1 * po2 + po1 * pe2 + qe1 * qo2 + qo1 * qe2,
+                                       pe1 * qe2 + po1 * qo2 + qe1 * pe2 + qo1 * po2,
+                                       pe1 * qo2 + po1 * qe2 + qe1 * po2 + qo1 * pe2])
+                continue
             s1, d1, s2, d2 = pe1 + po1, pe1 - po1, qe1 + qo1, qe1 - qo1
             t1, u1, t2, u2_ = pe2 + po2, pe2 - po2, qe2 + qo2, qe2 - qo2
             hk, hmk = (s1 + s2) * (t1 + t2), (s1 - s2) * (t1 - t2)
             hpk, hpmk = (d1 + d2) * (u1 + u2_), (d1 - d2) * (u1 - u2_)
             a, b, dd, ee = hk + hmk, hpk + hpmk, hk - hmk, hpk - hpmk
             acc[0, mb] = np.stack([a + b, a - b, dd + ee, dd - ee])
+        fold = 4.0 if L < 64 else 1.0
         NMR, ASD, AST = G["NMR"], G["ASD"], G["AST"]
         o = np.zeros((NMR, 4, 64, 4))
         zz = np.zeros(64)
@@ -173,7 +181,7 @@ def replay(plan, L, x1, x2):
                     for ty, opnd in enumerate((ce, co, se, so)):
                         o[mr, ty] = _mfma(w * opnd, acc[0, mb, ty][:, r], o[mr, ty])
                     if mr == 0:
-                        zz += w * acc[0, mb, 0][:, r]
+                        zz += w * fold * acc[0, mb, 0][:, r]
         zz = zz + _xor(zz, 16)
         zz = zz + _xor(zz, 32)
         eo = np.zeros(2 * 8 * NMP2)
@@ -272,9 +280,10 @@ def test_seed_table_angles(L):
             want = [*cs(2 * g + 2, k), *cs(2 * g + 1, k), *cs(8, k)] if k <= Q else [0.0] * 6
             assert np.allclose(TWR[lane, 6 * mb:6 * mb + 6], want, atol=1e-14)
             k0 = 16 * mb + g
+            fold = 4.0 if L < 64 else 1.0  # the weight all analysis samples share
             for mr in range(G["NMR"]):
                 me = 2 * (16 * mr + i) + 2
-                want = [*cs(me, k0), *cs(me - 1, k0)]
+                want = [fold * v for v in (*cs(me, k0), *cs(me - 1, k0))]
                 want = [v if (me - e // 2) <= L else 0.0 for e, v in enumerate(want)]
                 a = G["ASD"] + 4 * (mr * NMBP + mb)
                 assert np.allclose(TWR[lane, a:a + 4], want, atol=1e-14)
