@@ -59,8 +59,8 @@ __device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
 // (register r of lane (g, i) holds row 4 g + r, column i), so nothing moves
 // between them; synthesis row 4 g + r computes sample k = 16 mb + 4 r + g, so
 // that each analysis contraction (fixed r, K index g) takes four consecutive
-// samples and those past Q drop out whole.  The A operands are generated in registers from per-lane
-// seeds by angle-addition rotations.  Theta synthesis (VALU) produces the B
+// samples and those past Q drop out whole.  The A operands are generated in
+// registers from per-lane seeds by angle-addition rotations.  Theta synthesis (VALU) produces the B
 // operands in place: in K-step s lane (g, 8h + pi) sums the m-parts
 // m = 8s + 2g + 1 and + 2 at node jp over the l with l - m = h (mod 2); one
 // exchange between lanes i and i ^ 8 then gives node jp (even + odd) and its
@@ -357,10 +357,11 @@ struct WaveCtx {
     });
 
     // ---- 2c. phi analysis contractions; operands per k block from the seeds:
-    // w_k trig(m phi_k) (the seeds hold fold * trig), k = 16 mb + 4 r + g (the synthesis rows are ordered
-    // so that register r of lane group g holds that sample), m = 2(16 mr + i)
-    // + 2 (even types) or + 1 (odd types).  A contraction whose four samples
-    // all lie past Q (weight zero) is skipped.
+    // w_k trig(m phi_k) (the seeds hold fold * trig), k = 16 mb + 4 r + g
+    // (the synthesis rows are ordered so that register r of lane group g
+    // holds that sample), m = 2(16 mr + i) + 2 (even types) or + 1 (odd
+    // types).  A contraction whose four samples all lie past Q (weight zero)
+    // is skipped.
     lfor<0, NMR>([&](auto MR) {
       lfor<0, 4>([&](auto TY) { o[decltype(MR)::value][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
     });
