@@ -363,9 +363,26 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     assert idx.size and 0 <= idx.min() and idx.max() < total
     got = rows(idx).cpu().numpy()
     err = O.max_rel_err(got, ref)
-    return {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
-                      f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err}
+    out = {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{done} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
+                     f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err, "one_core": None}
+    # the same oracle on one core, on a smaller seeded subsample (about a
+    # quarter of the time above if the threads scaled perfectly)
+    try:
+        from threadpoolctl import threadpool_limits
+    except Exception:
+        return out
+    n1 = max(16, min(total, n // max(1, 4 * int(threads))))
+    idx1 = inputs.sample_indices(idx_cfg + 50, total, n1)
+    got1 = oracle_sample(O, idx1)
+    done1 = got1[2] if len(got1) > 2 else n1
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        got1[0]()
+        dt1 = time.perf_counter() - t0
+    out["one_core"] = {"value": done1 / dt1, "unit": "products/s", "cores": 1,
+                       "sample": f"{done1} seeded products, {dt1:.2f} s"}
+    return out
 
 
 def main():
