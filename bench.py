@@ -363,7 +363,13 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     assert idx.size and 0 <= idx.min() and idx.max() < total
     got = rows(idx).cpu().numpy()
     err = O.max_rel_err(got, ref)
-    out = {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle",
+    host = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            host = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), None)
+    except OSError:
+        pass
+    out = {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle", "host": host,
            "sample": f"{done} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
                      f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err, "one_core": None}
     # the same oracle on one core, on a smaller seeded subsample (about a
