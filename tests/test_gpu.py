@@ -200,18 +200,46 @@ def test_empty_and_single():
     assert O.max_rel_err(y, O.gtp(a, b, 3, 3, 3)) <= TOL
 
 
-def test_deterministic_and_streams():
-    L = 6
+def _f32(rng, *shape):
+    return dev(rng.standard_normal(shape).astype(np.float32))
+
+
+# one call per kernel family: thread-per-product (L = 6), matrix cores (L = 16,
+# 32, 64), the generic workgroup kernel (degrees without a specialised one),
+# the rotated frame, the fused channel mix and the many-body chain
+DETERMINISM_CASES = {
+    "small_L6": lambda rng: (lambda p, a, b: gtp.gtp_full(p, a, b), gtp.Plan(6, 6, 6), _f32(rng, 4096, 1, 49),
+                             _f32(rng, 4096, 1, 49)),
+    "wave_L16": lambda rng: (lambda p, a, b: gtp.gtp_full(p, a, b), gtp.Plan(16, 16, 16), _f32(rng, 300, 1, 289),
+                             _f32(rng, 300, 1, 289)),
+    "wave_L32": lambda rng: (lambda p, a, b: gtp.gtp_full(p, a, b), gtp.Plan(32, 32, 32), _f32(rng, 130, 1, 1089),
+                             _f32(rng, 130, 1, 1089)),
+    "wave4_L64": lambda rng: (lambda p, a, b: gtp.gtp_full(p, a, b), gtp.Plan(64, 64, 64), _f32(rng, 20, 1, 4225),
+                              _f32(rng, 20, 1, 4225)),
+    "generic": lambda rng: (lambda p, a, b: gtp.gtp_full(p, a, b), gtp.Plan(10, 9, 12), _f32(rng, 77, 1, 121),
+                            _f32(rng, 77, 1, 100)),
+    "escn_L6": lambda rng: (lambda p, a, b: gtp.gtp_conv_escn(p, a, b[0], b[1]), gtp.Plan(6, 6, 6),
+                            _f32(rng, 70, 64, 49), (_f32(rng, 70, 3), _f32(rng, 70, 64, 7))),
+    "mix_L6": lambda rng: (lambda p, a, b: gtp.gtp_channel_mix(p, a, b[0], b[1]), gtp.Plan(6, 6, 6),
+                           _f32(rng, 9, 17, 49), (_f32(rng, 9, 19, 49), _f32(rng, 23, 17, 19))),
+    "self_L2": lambda rng: (lambda p, a, b: gtp.gtp_selfproduct(a, 2, 3, 3, gtp.GTP_SELF_STEPWISE), None,
+                            _f32(rng, 300, 8, 9), None),
+}
+
+
+@pytest.mark.parametrize("kind", list(DETERMINISM_CASES))
+def test_deterministic_and_streams(kind):
+    """Two calls, the second on another stream, give bitwise equal results
+    (no atomics or order-dependent reductions in any kernel)."""
     rng = np.random.default_rng(5)
-    a = dev(rng.standard_normal((4096, 1, 49)))
-    b = dev(rng.standard_normal((4096, 1, 49)))
-    plan = gtp.Plan(L, L, L)
-    y1 = gtp.gtp_full(plan, a, b)
+    fn, plan, a, b = DETERMINISM_CASES[kind](rng)
+    _say(f"determinism {kind}")
+    y1 = fn(plan, a, b)
     s = torch.cuda.Stream()
     with torch.cuda.stream(s):
-        y2 = gtp.gtp_full(plan, a, b)
+        y2 = fn(plan, a, b)
     torch.cuda.synchronize()
-    assert torch.equal(y1, y2)
+    assert y1.shape == y2.shape and torch.equal(y1, y2)
 
 
 # ------------------------------------------------------------------ the three stages
