@@ -120,6 +120,27 @@ def test_direct_convolution(L1, L2, Lout, n):
     assert err <= TOL, err
 
 
+@pytest.mark.parametrize("L,n", [(4, 300), (8, 200), (16, 64), (32, 24)])
+def test_direct_and_convolution_theorem_agree(L, n):
+    """The two step-2 algorithms at the sweep's degrees (L = 64 has no direct
+    kernel: its LDS would not fit): the direct convolution against the shipped
+    convolution-theorem kernels, and at L = 32 against the oracle too."""
+    rng = np.random.default_rng(90 + L)
+    a = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    _say(f"direct vs convolution theorem L={L} n={n}")
+    yd = run_full(gtp.Plan(L, L, L, gtp.GTP_CONV_DIRECT), a, b)
+    yf = run_full(gtp.Plan(L, L, L), a, b)
+    err = O.max_rel_err(yd, yf.astype(np.float64))
+    _say(f"  direct vs shipped err={err:.3e}")
+    assert err <= 2 * TOL, err  # each within TOL of the exact product
+    if L == 32:
+        ref = oracle_pair(a[:4].astype(np.float64), b[:4].astype(np.float64), L, L, L)
+        err = O.max_rel_err(yd[:4], ref)
+        _say(f"  direct vs oracle err={err:.3e}")
+        assert err <= TOL, err
+
+
 @pytest.mark.parametrize("L", [5, 6, 7])
 @pytest.mark.parametrize("offset", [0, 1])
 def test_x2_slab_loads_aligned_and_offset(L, offset):
