@@ -522,6 +522,16 @@ __device__ __forceinline__ const int* row_er_table() {
   }
 }
 
+// Product of workgroup w among n: the dispatcher deals workgroups to the 8
+// XCDs round robin (w mod 8), so XCD x takes the x-th contiguous run of
+// products (runs of n / 8, the first n mod 8 one longer).  Neighbouring rows
+// share cache lines; this keeps both readers of a line in one XCD's L2.
+// A bijection of [0, n).
+__device__ __forceinline__ int64_t xcd_product(int64_t w, int64_t n) {
+  const int64_t q = n >> 3, r = n & 7, x = w & 7;
+  return x * q + (x < r ? x : r) + (w >> 3);
+}
+
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.
 template <int L, typename T1, typename T2, bool WGT>
@@ -538,8 +548,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   float* const xs = lds + G::EOP;
 
   const int lane = threadIdx.x;
-  const int64_t P = blockIdx.x;
-  if (P >= n) return;  // whole-wave exit (one product per workgroup)
+  if (int64_t(blockIdx.x) >= n) return;  // whole-wave exit (one product per workgroup)
+  const int64_t P = xcd_product(blockIdx.x, n);
   stage_x<L, WGT>(xs, x1, x2, P, lane, t.XMAP, wt);
 
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
@@ -662,8 +672,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   float* const eo_even = lds + XF;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t P = blockIdx.x;
-  if (P >= n) return;  // whole-workgroup exit (one product per workgroup)
+  if (int64_t(blockIdx.x) >= n) return;  // whole-workgroup exit (one product per workgroup)
+  const int64_t P = xcd_product(blockIdx.x, n);
   stage_x<L, WGT>(lds, x1, x2, P, tid, t.XMAP, wt);
   const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(lds), t);
 
