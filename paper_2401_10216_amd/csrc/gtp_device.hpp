@@ -75,6 +75,17 @@ __device__ __forceinline__ int degree_of(int i) {
   return l;
 }
 
+// Logical index of workgroup w among n: the dispatcher deals workgroups to
+// the 8 XCDs round robin (w mod 8), so XCD x takes the x-th contiguous run of
+// logical indices (runs of n / 8, the first n mod 8 one longer).  Work items
+// with neighbouring indices share cache lines (adjacent rows, one edge's
+// rotation matrices); this keeps their readers in one XCD's L2.  A bijection
+// of [0, n).
+__device__ __forceinline__ int64_t xcd_product(int64_t w, int64_t n) {
+  const int64_t q = n >> 3, r = n & 7, x = w & 7;
+  return x * q + (x < r ? x : r) + (w >> 3);
+}
+
 // Launchers (return the launch's hipError_t).  n = number of products.
 // Thread-per-product fused kernel for the degree triples it is instantiated
 // for; *supported = false when (L1, L2, Lout, nu) or the pair of input types

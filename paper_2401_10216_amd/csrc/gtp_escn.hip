@@ -250,8 +250,11 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   float* const Dl = lds;
 
   const int tid = threadIdx.x;
-  const int64_t b = blockIdx.x / ncb;
-  const int64_t c0 = int64_t(blockIdx.x % ncb) * kEW;
+  // XCD-aware: the ncb workgroups of an edge (which read its rotation
+  // matrices) run on one XCD
+  const int64_t wg = xcd_product(blockIdx.x, gridDim.x);
+  const int64_t b = wg / ncb;
+  const int64_t c0 = (wg % ncb) * kEW;
   const int cnt = int(C - c0 < kEW ? C - c0 : kEW);
   const int64_t p0 = b * C + c0;
 

@@ -522,16 +522,6 @@ __device__ __forceinline__ const int* row_er_table() {
   }
 }
 
-// Product of workgroup w among n: the dispatcher deals workgroups to the 8
-// XCDs round robin (w mod 8), so XCD x takes the x-th contiguous run of
-// products (runs of n / 8, the first n mod 8 one longer).  Neighbouring rows
-// share cache lines; this keeps both readers of a line in one XCD's L2.
-// A bijection of [0, n).
-__device__ __forceinline__ int64_t xcd_product(int64_t w, int64_t n) {
-  const int64_t q = n >> 3, r = n & 7, x = w & 7;
-  return x * q + (x < r ? x : r) + (w >> 3);
-}
-
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.
 template <int L, typename T1, typename T2, bool WGT>
