@@ -106,6 +106,41 @@ def _dev(t, name):
     return ctypes.c_void_p(t.data_ptr())
 
 
+def _want(t, name, shape, dtypes, device=None):
+    """Validate a caller-supplied tensor before anything reaches the library:
+    exact shape, one of the allowed dtypes, contiguous, on the device of the
+    other operands.  Raises TypeError (dtype) or ValueError (everything else)
+    and returns the tensor's device pointer."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}; expected " + " or ".join(str(d) for d in dtypes))
+    if tuple(t.shape) != tuple(int(v) for v in shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}; expected {tuple(int(v) for v in shape)}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}; the other operands are on {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _on_gpu(t, name):
+    """Last check before a call: the operands (all on t's device) are device tensors."""
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+
+
+def _f32():
+    import torch
+    return (torch.float32,)
+
+
+def _inputs():
+    import torch
+    return (torch.float32, torch.bfloat16)
+
+
 def nsh(L: int) -> int:
     return (L + 1) * (L + 1)
 
@@ -158,10 +193,14 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
     if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2):
         raise ValueError("coefficient dimension does not match the plan")
     B, C = int(x1.shape[0]), int(x1.shape[1])
+    code = _dtype_code(x1)
+    p1 = _want(x1, "x1", x1.shape, _inputs())
+    p2 = _want(x2, "x2", x2.shape, _inputs(), x1.device)
     if y is None:
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
-    _check(lib().gtp_full(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), B, C, _dev(y, "y"),
-                          _stream(stream)))
+    py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x1.device)
+    _on_gpu(x1, "x1")
+    _check(lib().gtp_full(plan.handle, p1, p2, code, B, C, py, _stream(stream)))
     return y
 
 
@@ -178,10 +217,15 @@ def gtp_channel_mix(plan: Plan, x1, x2, W, y=None, stream=None):
     if W.dim() != 3 or tuple(W.shape[1:]) != (C1, C2) or W.dtype != torch.float32:
         raise ValueError("W must be float32 [Co, C1, C2]")
     Co = int(W.shape[0])
+    code = _dtype_code(x1)
+    p1 = _want(x1, "x1", x1.shape, _inputs())
+    p2 = _want(x2, "x2", x2.shape, _inputs(), x1.device)
+    pw = _want(W, "W", (Co, C1, C2), _f32(), x1.device)
     if y is None:
         y = torch.empty((B, Co, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
-    _check(lib().gtp_channel_mix(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), _dev(W, "W"), B, C1,
-                                 C2, Co, _dev(y, "y"), _stream(stream)))
+    py = _want(y, "y", (B, Co, nsh(plan.Lout)), _f32(), x1.device)
+    _on_gpu(x1, "x1")
+    _check(lib().gtp_channel_mix(plan.handle, p1, p2, code, pw, B, C1, C2, Co, py, _stream(stream)))
     return y
 
 
@@ -195,10 +239,15 @@ def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None):
         raise ValueError("r must be float32 [B, 3]")
     if tuple(h.shape) != (B, C, plan.L2 + 1) or h.dtype != torch.float32:
         raise ValueError("h must be float32 [B, C, L2+1]")
+    code = _dtype_code(x)
+    px = _want(x, "x", x.shape, _inputs())
+    pr = _want(r, "r", (B, 3), _f32(), x.device)
+    ph = _want(h, "h", (B, C, plan.L2 + 1), _f32(), x.device)
     if y is None:
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x.device)
-    _check(lib().gtp_conv_escn(plan.handle, _dev(x, "x"), _dtype_code(x), _dev(r, "r"), _dev(h, "h"), B, C,
-                               _dev(y, "y"), _stream(stream)))
+    py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x.device)
+    _on_gpu(x, "x")
+    _check(lib().gtp_conv_escn(plan.handle, px, code, pr, ph, B, C, py, _stream(stream)))
     return y
 
 
@@ -220,13 +269,16 @@ def gtp_full_weighted(plan: Plan, x1, x2, w1=None, w2=None, wout=None, per_chann
         if w is None:
             ptrs.append(ctypes.c_void_p(None))
             continue
-        if w.dtype != torch.float32 or tuple(w.shape) != (R, L + 1):
-            raise ValueError(f"{name} must be float32 [{R}, {L + 1}]")
-        ptrs.append(_dev(w, name))
+        ptrs.append(_want(w, name, (R, L + 1), _f32(), x1.device))
+    code = _dtype_code(x1)
+    p1 = _want(x1, "x1", x1.shape, _inputs())
+    p2 = _want(x2, "x2", x2.shape, _inputs(), x1.device)
     if y is None:
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
-    _check(lib().gtp_full_weighted(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), *ptrs,
-                                   1 if per_channel else 0, B, C, _dev(y, "y"), _stream(stream)))
+    py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x1.device)
+    _on_gpu(x1, "x1")
+    _check(lib().gtp_full_weighted(plan.handle, p1, p2, code, *ptrs, 1 if per_channel else 0, B, C, py,
+                                   _stream(stream)))
     return y
 
 
@@ -243,45 +295,69 @@ def gtp_full_backward(plan: Plan, x1, x2, dy, need_dx1: bool = True, need_dx2: b
     if dy.dtype != torch.float32:
         raise TypeError("dy must be float32")
     B, C = int(x1.shape[0]), int(x1.shape[1])
+    code = _dtype_code(x1)
+    px1 = _want(x1, "x1", x1.shape, _inputs())
+    px2 = _want(x2, "x2", x2.shape, _inputs(), x1.device)
+    pdy = _want(dy, "dy", (B, C, nsh(plan.Lout)), _f32(), x1.device)
     if need_dx1 and dx1 is None:
         dx1 = torch.empty((B, C, nsh(plan.L1)), dtype=torch.float32, device=x1.device)
     if need_dx2 and dx2 is None:
         dx2 = torch.empty((B, C, nsh(plan.L2)), dtype=torch.float32, device=x1.device)
-    p1 = _dev(dx1, "dx1") if need_dx1 else ctypes.c_void_p(None)
-    p2 = _dev(dx2, "dx2") if need_dx2 else ctypes.c_void_p(None)
-    _check(lib().gtp_full_backward(plan.handle, _dev(x1, "x1"), _dev(x2, "x2"), _dtype_code(x1), _dev(dy, "dy"), B, C,
-                                   p1, p2, _stream(stream)))
+    p1 = _want(dx1, "dx1", (B, C, nsh(plan.L1)), _f32(), x1.device) if need_dx1 else ctypes.c_void_p(None)
+    p2 = _want(dx2, "dx2", (B, C, nsh(plan.L2)), _f32(), x1.device) if need_dx2 else ctypes.c_void_p(None)
+    _on_gpu(x1, "x1")
+    _check(lib().gtp_full_backward(plan.handle, px1, px2, code, pdy, B, C, p1, p2, _stream(stream)))
     return (dx1 if need_dx1 else None), (dx2 if need_dx2 else None)
 
 
 def gtp_sh2fourier(plan: Plan, which: int, x, grid=None, stream=None):
     """Complex grids [n, 2L+1, 2L+1] (as torch.complex64) of x[n, (L+1)^2]."""
     import torch
+    if which not in (1, 2):
+        raise ValueError("which must be 1 or 2")
     L = plan.L1 if which == 1 else plan.L2
+    if x.dim() != 2:
+        raise ValueError("x must be [n, (L+1)^2]")
     n = int(x.shape[0])
+    code = _dtype_code(x)
+    px = _want(x, "x", (n, nsh(L)), _inputs())
     if grid is None:
         grid = torch.empty((n, 2 * L + 1, 2 * L + 1), dtype=torch.complex64, device=x.device)
-    _check(lib().gtp_sh2fourier(plan.handle, which, _dev(x, "x"), _dtype_code(x), n, _dev(grid, "grid"),
-                                _stream(stream)))
+    pg = _want(grid, "grid", (n, 2 * L + 1, 2 * L + 1), (torch.complex64,), x.device)
+    _on_gpu(x, "x")
+    _check(lib().gtp_sh2fourier(plan.handle, which, px, code, n, pg, _stream(stream)))
     return grid
 
 
 def gtp_fourier_conv(plan: Plan, g1, g2, g3=None, stream=None):
     import torch
+    if g1.dim() != 3:
+        raise ValueError("g1 must be [n, 2 L1 + 1, 2 L1 + 1]")
     n = int(g1.shape[0])
-    D3 = 2 * (plan.L1 + plan.L2) + 1
+    D1, D2, D3 = 2 * plan.L1 + 1, 2 * plan.L2 + 1, 2 * (plan.L1 + plan.L2) + 1
+    c64 = (torch.complex64,)
+    p1 = _want(g1, "g1", (n, D1, D1), c64)
+    p2 = _want(g2, "g2", (n, D2, D2), c64, g1.device)
     if g3 is None:
         g3 = torch.empty((n, D3, D3), dtype=torch.complex64, device=g1.device)
-    _check(lib().gtp_fourier_conv(plan.handle, _dev(g1, "g1"), _dev(g2, "g2"), n, _dev(g3, "g3"), _stream(stream)))
+    p3 = _want(g3, "g3", (n, D3, D3), c64, g1.device)
+    _on_gpu(g1, "g1")
+    _check(lib().gtp_fourier_conv(plan.handle, p1, p2, n, p3, _stream(stream)))
     return g3
 
 
 def gtp_fourier2sh(plan: Plan, g3, y=None, stream=None):
     import torch
+    if g3.dim() != 3:
+        raise ValueError("g3 must be [n, 2U + 1, 2U + 1]")
     n = int(g3.shape[0])
+    D3 = 2 * (plan.L1 + plan.L2) + 1
+    p3 = _want(g3, "g3", (n, D3, D3), (torch.complex64,))
     if y is None:
         y = torch.empty((n, nsh(plan.Lout)), dtype=torch.float32, device=g3.device)
-    _check(lib().gtp_fourier2sh(plan.handle, _dev(g3, "g3"), n, _dev(y, "y"), _stream(stream)))
+    py = _want(y, "y", (n, nsh(plan.Lout)), _f32(), g3.device)
+    _on_gpu(g3, "g3")
+    _check(lib().gtp_fourier2sh(plan.handle, p3, n, py, _stream(stream)))
     return y
 
 
@@ -290,22 +366,32 @@ def gtp_selfproduct(x, L: int, nu: int, Lout: int, mode: int = GTP_SELF_STEPWISE
     if x.dim() != 3 or x.shape[2] != nsh(L):
         raise ValueError("x must be [B, C, (L+1)^2]")
     B, C = int(x.shape[0]), int(x.shape[1])
+    code = _dtype_code(x)
+    px = _want(x, "x", x.shape, _inputs())
     if y is None:
         y = torch.empty((B, C, nsh(Lout)), dtype=torch.float32, device=x.device)
-    _check(lib().gtp_selfproduct(L, nu, Lout, mode, _dev(x, "x"), _dtype_code(x), B, C, _dev(y, "y"),
-                                 _stream(stream)))
+    py = _want(y, "y", (B, C, nsh(Lout)), _f32(), x.device)
+    _on_gpu(x, "x")
+    _check(lib().gtp_selfproduct(L, nu, Lout, mode, px, code, B, C, py, _stream(stream)))
     return y
 
 
 def gtp_sh_filter(L: int, r, h=None, out=None, stream=None):
     """out[B,C,(L+1)^2] = h[B,C,L+1] * Y(r_b); h=None gives Y(r) with C = 1."""
     import torch
+    if r.dim() != 2:
+        raise ValueError("r must be [B, 3]")
     B = int(r.shape[0])
+    pr = _want(r, "r", (B, 3), _f32())
+    if h is not None and h.dim() != 3:
+        raise ValueError("h must be [B, C, L+1]")
     C = 1 if h is None else int(h.shape[1])
+    hp = ctypes.c_void_p(None) if h is None else _want(h, "h", (B, C, L + 1), _f32(), r.device)
     if out is None:
         out = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=r.device)
-    hp = ctypes.c_void_p(None) if h is None else _dev(h, "h")
-    _check(lib().gtp_sh_filter(L, _dev(r, "r"), hp, B, C, _dev(out, "out"), _stream(stream)))
+    po = _want(out, "out", (B, C, nsh(L)), _f32(), r.device)
+    _on_gpu(r, "r")
+    _check(lib().gtp_sh_filter(L, pr, hp, B, C, po, _stream(stream)))
     return out
 
 
