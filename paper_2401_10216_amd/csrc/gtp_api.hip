@@ -4,6 +4,7 @@
 
 #include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <map>
 #include <memory>
@@ -65,10 +66,40 @@ bool mul_ok(int64_t a, int64_t b, int64_t* out) {
 }
 
 size_t dtype_size(gtp_dtype d) { return d == GTP_BF16 ? 2 : 4; }
+
+// Whether every pointer is a multiple of `align` bytes (NULL passes).
+template <typename... Ps>
+bool aligned(size_t align, Ps... ps) {
+  return ((reinterpret_cast<uintptr_t>(ps) % align == 0) && ...);
+}
+
+// Test hook: GTP_TEST_FAIL_ALLOC=host makes the host table build fail as if
+// out of memory; GTP_TEST_FAIL_ALLOC=<n> makes the n-th device allocation of
+// a plan (counting from 0) fail.  Read at every plan creation; unset in
+// normal use.
+long fail_alloc_hook(bool* host) {
+  const char* v = std::getenv("GTP_TEST_FAIL_ALLOC");
+  *host = false;
+  if (!v || !*v) return -1;
+  if (std::strcmp(v, "host") == 0) {
+    *host = true;
+    return -1;
+  }
+  char* end = nullptr;
+  const long n = std::strtol(v, &end, 10);
+  return (end && *end == '\0' && n >= 0) ? n : -1;
+}
 bool dtype_ok(gtp_dtype d) { return d == GTP_F32 || d == GTP_BF16; }
 
-gtp_status upload(gtp_plan_* p) {
+gtp_status upload(gtp_plan_* p, long fail_at) {
   using gtp::ntri;
+  long nalloc = 0;
+  // every device allocation of the plan goes through here (fail_at >= 0: the
+  // test hook fails that one)
+  auto dmalloc = [&](void** d, size_t bytes) -> hipError_t {
+    if (nalloc++ == fail_at) return hipErrorOutOfMemory;
+    return hipMalloc(d, bytes);
+  };
   const gtp::Tables& t = p->tab;
   const int nmp = 2 * t.Mphi + 1;
   const int ntE = ntri(t.Le);
@@ -85,7 +116,7 @@ gtp_status upload(gtp_plan_* p) {
     std::vector<float> h(cnt ? cnt : 1, 0.0f);
     for (size_t i = 0; i < cnt; ++i) h[i] = src64 ? float((*src64)[i]) : (*src32)[i];
     float* d = nullptr;
-    hipError_t e = hipMalloc(&d, h.size() * sizeof(float));
+    hipError_t e = dmalloc(reinterpret_cast<void**>(&d), h.size() * sizeof(float));
     if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMalloc: ") + hipGetErrorString(e));
     p->dbufs.push_back(d);
     e = hipMemcpy(d, h.data(), h.size() * sizeof(float), hipMemcpyHostToDevice);
@@ -127,7 +158,7 @@ gtp_status upload(gtp_plan_* p) {
     if ((s = up(&t.SM0P, nullptr, &d.SM0P)) != GTP_OK) return s;
     if ((s = up(&t.WP, nullptr, &d.WP)) != GTP_OK) return s;
     int* dm = nullptr;
-    hipError_t e = hipMalloc(&dm, t.XMAPP.size() * sizeof(int));
+    hipError_t e = dmalloc(reinterpret_cast<void**>(&dm), t.XMAPP.size() * sizeof(int));
     if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMalloc: ") + hipGetErrorString(e));
     p->dbufs.push_back(reinterpret_cast<float*>(dm));
     e = hipMemcpy(dm, t.XMAPP.data(), t.XMAPP.size() * sizeof(int), hipMemcpyHostToDevice);
@@ -168,7 +199,10 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
   // The convolution-theorem path is used at every degree: its flop count is
   // below the direct real-form convolution's from L = 2 on.
   p->conv = conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : GTP_CONV_FFT;
+  bool fail_host = false;
+  const long fail_dev = fail_alloc_hook(&fail_host);
   try {
+    if (fail_host) throw std::bad_alloc();
     p->tab = gtp::build_tables(L1, L2, Lout);
     // the rotated-frame convolution kernel exists for equal degrees <= 8
     if (L1 == L2 && L2 == Lout && L1 >= 1 && L1 <= 8) p->esc = gtp::build_escn_tables(p->tab);
@@ -182,7 +216,7 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
     if (s != GTP_OK) return s;
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    s = upload(p.get());
+    s = upload(p.get(), fail_dev);
     if (s != GTP_OK) {
       release(p.get());
       return s;
@@ -508,12 +542,14 @@ gtp_status gtp_sh2fourier(gtp_plan p, int which, const void* x, gtp_dtype in_dty
   if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "bad in_dtype");
   const int L = which == 1 ? p->L1 : p->L2;
   int64_t ex = 0, eg = 0;
-  if (!mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, int64_t(2) * (2 * L + 1) * (2 * L + 1), &eg) || eg > INT64_MAX / 4)
+  if (!mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, int64_t(2) * (2 * L + 1) * (2 * L + 1), &eg) || eg > INT64_MAX / 4 ||
+      ex > INT64_MAX / 4)
     return fail(GTP_ERR_INVALID_ARG, "n must be >= 0 and n * grid size must fit");
   if (n == 0) return GTP_OK;
   if (!x || !grid) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
   if (ranges_overlap(grid, size_t(eg) * 4, x, size_t(ex) * dtype_size(in_dtype)))
     return fail(GTP_ERR_INVALID_ARG, "grid overlaps x");
+  if (!aligned(dtype_size(in_dtype), x) || !aligned(4, grid)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   if ((s = device_ready(p)) != GTP_OK) return s;
   hipError_t e = gtp::launch_sh2fourier(p->dev, L, x, in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32, n, grid,
                                         static_cast<hipStream_t>(stream));
@@ -532,6 +568,7 @@ gtp_status gtp_fourier_conv(gtp_plan p, const float* g1, const float* g2, int64_
   if (!g1 || !g2 || !g3) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
   if (ranges_overlap(g3, size_t(e3) * 4, g1, size_t(e1) * 4) || ranges_overlap(g3, size_t(e3) * 4, g2, size_t(e2) * 4))
     return fail(GTP_ERR_INVALID_ARG, "g3 overlaps g1 or g2");
+  if (!aligned(4, g1, g2, g3)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   if ((s = device_ready(p)) != GTP_OK) return s;
   hipError_t e = gtp::launch_fourier_conv(p->L1, p->L2, g1, g2, n, g3, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_fourier_conv launch");
@@ -542,11 +579,12 @@ gtp_status gtp_fourier2sh(gtp_plan p, const float* g3, int64_t n, float* y, void
   if (s != GTP_OK) return s;
   const int64_t D3 = 2 * (p->L1 + p->L2) + 1;
   int64_t e3 = 0, eo = 0;
-  if (!mul_ok(n, 2 * D3 * D3, &e3) || !mul_ok(n, gtp::nsh(p->Lout), &eo) || e3 > INT64_MAX / 4)
+  if (!mul_ok(n, 2 * D3 * D3, &e3) || !mul_ok(n, gtp::nsh(p->Lout), &eo) || e3 > INT64_MAX / 4 || eo > INT64_MAX / 4)
     return fail(GTP_ERR_INVALID_ARG, "n must be >= 0 and n * grid size must fit");
   if (n == 0) return GTP_OK;
   if (!g3 || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
   if (ranges_overlap(y, size_t(eo) * 4, g3, size_t(e3) * 4)) return fail(GTP_ERR_INVALID_ARG, "y overlaps g3");
+  if (!aligned(4, g3, y)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   if ((s = device_ready(p)) != GTP_OK) return s;
   hipError_t e = gtp::launch_fourier2sh(p->dev, g3, n, y, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_fourier2sh launch");
@@ -561,12 +599,14 @@ gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void* x
     return fail(GTP_ERR_UNSUPPORTED, "fused mode needs nu * L <= 64");
   if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "bad in_dtype");
   int64_t n = 0, ex = 0, eo = 0;
-  if (!mul_ok(B, C, &n) || !mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, gtp::nsh(Lout), &eo) || eo > INT64_MAX / 4)
+  if (!mul_ok(B, C, &n) || !mul_ok(n, gtp::nsh(L), &ex) || !mul_ok(n, gtp::nsh(Lout), &eo) || eo > INT64_MAX / 4 ||
+      ex > INT64_MAX / 4)
     return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and sizes must fit");
   if (n == 0) return GTP_OK;
   if (!x || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
   if (ranges_overlap(y, size_t(eo) * 4, x, size_t(ex) * dtype_size(in_dtype)))
     return fail(GTP_ERR_INVALID_ARG, "y overlaps x");
+  if (!aligned(dtype_size(in_dtype), x) || !aligned(4, y)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   gtp_status s = check_device();
   if (s != GTP_OK) return s;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -628,6 +668,7 @@ gtp_status gtp_sh_filter(int L, const float* r, const float* h, int64_t B, int64
   if (ranges_overlap(out, size_t(eo) * 4, r, size_t(B) * 12) ||
       (h && ranges_overlap(out, size_t(eo) * 4, h, size_t(n) * (L + 1) * 4)))
     return fail(GTP_ERR_INVALID_ARG, "out overlaps an input");
+  if (!aligned(4, r, h, out)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
   gtp_status s = check_device();
   if (s != GTP_OK) return s;
   hipError_t e = gtp::launch_sh_filter(L, r, h, B, C, out, static_cast<hipStream_t>(stream));

@@ -285,3 +285,47 @@ def test_status_strings(L):
     for s, name in gtp._STATUS.items():
         assert L.gtp_status_str(s).decode() == name
     assert L.gtp_status_str(99).decode() == "GTP_ERR_UNKNOWN"
+
+
+def test_alignment_checked_everywhere(L):
+    """Every entry point refuses a pointer that is not a multiple of its
+    element size (2 bytes for bf16 inputs, 4 for fp32 data) before any HIP
+    call."""
+    p = host_plan(2, 3, 2)
+    H = p.handle
+    a, b, c = fake(0x100000), fake(0x200000), fake(0x300000)
+    S = ctypes.c_void_p(0)
+    INV = gtp.GTP_ERR_INVALID_ARG
+
+    def misaligned(status):
+        return status == INV and b"misaligned" in L.gtp_last_error()
+
+    assert misaligned(L.gtp_sh2fourier(H, 1, fake(0x100002), 0, 4, b, S))  # f32 x
+    assert misaligned(L.gtp_sh2fourier(H, 1, fake(0x100001), 1, 4, b, S))  # bf16 x
+    assert misaligned(L.gtp_sh2fourier(H, 1, a, 0, 4, fake(0x200002), S))  # grid
+    assert not misaligned(L.gtp_sh2fourier(H, 1, fake(0x100002), 1, 4, b, S))  # bf16 at 2 bytes is fine
+    assert misaligned(L.gtp_fourier_conv(H, a, fake(0x200001), 4, c, S))
+    assert misaligned(L.gtp_fourier_conv(H, a, b, 4, fake(0x300002), S))
+    assert misaligned(L.gtp_fourier2sh(H, fake(0x100002), 4, c, S))
+    assert misaligned(L.gtp_fourier2sh(H, a, 4, fake(0x300003), S))
+    assert misaligned(L.gtp_selfproduct(2, 3, 3, 0, fake(0x100002), 0, 4, 4, c, S))
+    assert misaligned(L.gtp_selfproduct(2, 3, 3, 0, fake(0x100001), 1, 4, 4, c, S))
+    assert misaligned(L.gtp_selfproduct(2, 3, 3, 0, a, 0, 4, 4, fake(0x300002), S))
+    assert misaligned(L.gtp_sh_filter(3, fake(0x100002), None, 4, 1, c, S))
+    assert misaligned(L.gtp_sh_filter(3, a, fake(0x200001), 4, 2, c, S))
+    assert misaligned(L.gtp_sh_filter(3, a, b, 4, 2, fake(0x300002), S))
+    # the input size is bounded like the output size
+    assert L.gtp_selfproduct(64, 2, 0, 0, a, 0, 1 << 25, 1 << 25, c, S) == INV
+
+
+def test_fail_alloc_hook_reports_alloc_error(L, monkeypatch):
+    """GTP_TEST_FAIL_ALLOC=host makes the fp64 table build fail as if out of
+    memory: plan creation returns GTP_ERR_ALLOC with nothing leaked."""
+    h = ctypes.c_void_p()
+    monkeypatch.setenv("GTP_TEST_FAIL_ALLOC", "host")
+    assert L.gtp_plan_create(ctypes.byref(h), 3, 3, 3, gtp.GTP_PLAN_HOST_ONLY) == gtp.GTP_ERR_ALLOC
+    assert h.value is None
+    assert b"allocation" in L.gtp_last_error()
+    monkeypatch.delenv("GTP_TEST_FAIL_ALLOC")
+    assert L.gtp_plan_create(ctypes.byref(h), 3, 3, 3, gtp.GTP_PLAN_HOST_ONLY) == gtp.GTP_OK
+    assert L.gtp_plan_destroy(h) == gtp.GTP_OK

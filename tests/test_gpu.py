@@ -805,3 +805,22 @@ def test_channel_mix_generic_bf16_and_degenerate():
     z = gtp.gtp_channel_mix(gtp.Plan(L, L, L), torch.empty((0, C1, O.nsh(L)), device="cuda:0"),
                             torch.empty((0, C2, O.nsh(L)), device="cuda:0"), dev(W))
     assert z.shape == (0, Co, O.nsh(L))
+
+
+def test_plan_device_allocation_failure(monkeypatch):
+    """GTP_TEST_FAIL_ALLOC=<n> fails the plan's n-th device allocation: plan
+    creation returns GTP_ERR_ALLOC, frees what it had allocated, and the next
+    plan works."""
+    import ctypes
+    L = gtp.lib()
+    for n, degs in ((0, (2, 2, 2)), (3, (6, 6, 6)), (12, (32, 32, 32))):
+        monkeypatch.setenv("GTP_TEST_FAIL_ALLOC", str(n))
+        h = ctypes.c_void_p()
+        _say(f"fail allocation {n} of plan {degs}")
+        assert L.gtp_plan_create(ctypes.byref(h), *degs, 0) == gtp.GTP_ERR_ALLOC
+        assert h.value is None
+    monkeypatch.delenv("GTP_TEST_FAIL_ALLOC")
+    rng = np.random.default_rng(3)
+    a = rng.standard_normal((100, 1, 49)).astype(np.float32)
+    y = run_full(gtp.Plan(6, 6, 6), a, a)
+    assert O.max_rel_err(y, O.gtp(a.astype(np.float64), a.astype(np.float64), 6, 6, 6)) <= TOL
