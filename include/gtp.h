@@ -130,6 +130,25 @@ gtp_status gtp_channel_mix(gtp_plan p, const void *x1, const void *x2, gtp_dtype
 gtp_status gtp_conv_escn(gtp_plan p, const void *x, gtp_dtype in_dtype, const float *r, const float *h, int64_t B,
                          int64_t C, float *y, void *stream);
 
+/* gtp_conv_escn without any device allocation, for callers that cannot
+ * allocate: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, result and errors as gtp_conv_escn; no
+ * hipMalloc / hipMallocAsync / hipFree / allocating library call is made.
+ * The per-edge rotation matrices (or, for degrees without a rotated-frame
+ * kernel, the filter rows) go to a static device scratch array of
+ * GTP_NOALLOC_SCRATCH_BYTES (64 MiB) per device, which exists from the
+ * library's load on that device until the process ends; the edges are
+ * processed in chunks that fit it.  Returns GTP_ERR_UNSUPPORTED (before any
+ * HIP call) when one edge alone needs more: C (L2+1)^2 4 bytes above 64 MiB
+ * on the filter route.  Every call on a device shares that device's array
+ * and leaves it holding the last chunk's values (each launch writes what it
+ * reads, nothing has to start at zero): calls that may overlap on one device
+ * (different streams, different host threads) race and must be serialised
+ * by the caller.  The plan must have been created on the current device. */
+#define GTP_NOALLOC_SCRATCH_BYTES (64ll << 20)
+gtp_status gtp_conv_escn_noalloc(gtp_plan p, const void *x, gtp_dtype in_dtype, const float *r, const float *h,
+                                 int64_t B, int64_t C, float *y, void *stream);
+
 /* Weighted Gaunt tensor product (Sec. 3.1, eq. tp-eq-mul-weight; Appendix
  * "Feature Interaction" weights w^l_{l1,l2} reparameterized as
  * w_{l1} w_{l2} w_l):

@@ -22,6 +22,7 @@
 
 struct gtp_plan_ {
   int L1 = 0, L2 = 0, Lout = 0;
+  float* scratch = nullptr;  // this device's copy of the static scratch array (gtp_conv_escn_noalloc)
   unsigned flags = 0;
   bool host_only = true;
   int device = -1;
@@ -33,6 +34,14 @@ struct gtp_plan_ {
   gtp::DevTables dev{};
   gtp::EscnDev escd{};
 };
+
+// Device scratch of the allocation-free entry point: one copy per device,
+// allocated with the library's code object and held until the process ends.
+// Host code never passes this name to a kernel (on the host it is only a
+// stand-in for the symbol); it uses the address hipGetSymbolAddress returns
+// for the current device, kept in each plan.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
 
 namespace {
 
@@ -216,6 +225,12 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
     if (s != GTP_OK) return s;
     hipError_t e = hipGetDevice(&p->device);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    // this device's address of the scratch array (set-up of the
+    // allocation-free entry point; the plan is used only on this device)
+    void* sp = nullptr;
+    e = hipGetSymbolAddress(&sp, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    p->scratch = static_cast<float*>(sp);
     s = upload(p.get(), fail_dev);
     if (s != GTP_OK) {
       release(p.get());
@@ -286,6 +301,36 @@ gtp_status run_product(gtp_plan p, const void* x1, int it1, const void* x2, int 
   }
   e = gtp::launch_full_generic(p->dev, x1, it1, x2, it2, n, y, 0, wt, st);
   return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+}
+
+// Argument checks shared by both rotated-frame entry points (all before any
+// HIP call); *n = B C.
+gtp_status escn_check(gtp_plan p, const void* x, gtp_dtype in_dtype, const float* r, const float* h, int64_t B,
+                      int64_t C, float* y, int64_t* n_out) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  int64_t n = 0, ex = 0, eh = 0, eo = 0, er = 0;
+  if (!mul_ok(B, C, &n) || !mul_ok(B, 3, &er)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit");
+  if (!mul_ok(n, gtp::nsh(p->L1), &ex) || !mul_ok(n, p->L2 + 1, &eh) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      ex > INT64_MAX / 4 || eh > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  *n_out = n;
+  if (n == 0) return GTP_OK;
+  if (!x || !r || !h || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const size_t es = dtype_size(in_dtype), ny = size_t(eo) * 4;
+  if (ranges_overlap(y, ny, x, size_t(ex) * es) || ranges_overlap(y, ny, r, size_t(er) * 4) ||
+      ranges_overlap(y, ny, h, size_t(eh) * 4))
+    return fail(GTP_ERR_INVALID_ARG, "y overlaps an input");
+  if (!aligned(es, x) || !aligned(4, r, h, y)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  return GTP_OK;
+}
+
+// Whether the plan's rotated-frame convolution runs on its own kernels
+// (L1 = L2 = Lout in 1..8, convolution-theorem plan) rather than as filter +
+// plain product.
+bool escn_rotated(gtp_plan p) {
+  return !p->force_generic && p->conv != GTP_CONV_DIRECT && p->esc.NPAIR > 0 && gtp::escn_rot_floats(p->L1) > 0;
 }
 
 }  // namespace
@@ -439,28 +484,14 @@ gtp_status gtp_channel_mix(gtp_plan p, const void* x1, const void* x2, gtp_dtype
 
 gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const float* r, const float* h, int64_t B,
                          int64_t C, float* y, void* stream) {
-  gtp_status s = plan_check(p);
-  if (s != GTP_OK) return s;
-  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
-  int64_t n = 0, ex = 0, eh = 0, eo = 0, er = 0;
-  if (!mul_ok(B, C, &n) || !mul_ok(B, 3, &er)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit");
-  if (!mul_ok(n, gtp::nsh(p->L1), &ex) || !mul_ok(n, p->L2 + 1, &eh) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
-      ex > INT64_MAX / 4 || eh > INT64_MAX / 4 || eo > INT64_MAX / 4)
-    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
-  if (n == 0) return GTP_OK;
-  if (!x || !r || !h || !y) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
-  const size_t es = dtype_size(in_dtype), ny = size_t(eo) * 4;
-  if (ranges_overlap(y, ny, x, size_t(ex) * es) || ranges_overlap(y, ny, r, size_t(er) * 4) ||
-      ranges_overlap(y, ny, h, size_t(eh) * 4))
-    return fail(GTP_ERR_INVALID_ARG, "y overlaps an input");
-  if (reinterpret_cast<uintptr_t>(x) % es ||
-      (reinterpret_cast<uintptr_t>(r) | reinterpret_cast<uintptr_t>(h) | reinterpret_cast<uintptr_t>(y)) % 4)
-    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  int64_t n = 0;
+  gtp_status s = escn_check(p, x, in_dtype, r, h, B, C, y, &n);
+  if (s != GTP_OK || n == 0) return s;
   if ((s = device_ready(p)) != GTP_OK) return s;
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
   const int64_t rf = gtp::escn_rot_floats(p->L1);
-  if (!p->force_generic && p->conv != GTP_CONV_DIRECT && p->escd.E && rf > 0) {
+  if (escn_rotated(p)) {
     // per-edge rotation matrices in a stream-ordered workspace
     float* dws = nullptr;
     int64_t nd = 0;
@@ -486,6 +517,54 @@ gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const fl
   const hipError_t e2 = hipFreeAsync(f, st);
   if (s != GTP_OK) return s;
   return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
+}
+
+gtp_status gtp_conv_escn_noalloc(gtp_plan p, const void* x, gtp_dtype in_dtype, const float* r, const float* h,
+                                 int64_t B, int64_t C, float* y, void* stream) {
+  int64_t n = 0;
+  gtp_status s = escn_check(p, x, in_dtype, r, h, B, C, y, &n);
+  if (s != GTP_OK || n == 0) return s;
+  // scratch floats one edge needs: its rotation matrices (rotated-frame
+  // kernels) or its C filter rows (filter + plain product)
+  const bool rot = escn_rotated(p);
+  const int64_t cap = int64_t(kScratchBytes / sizeof(float));
+  const int64_t per_edge = rot ? gtp::escn_rot_floats(p->L1) : (C <= cap / gtp::nsh(p->L2) ? C * gtp::nsh(p->L2) : -1);
+  if (per_edge < 0 || per_edge > cap)
+    return fail(GTP_ERR_UNSUPPORTED, "one edge needs more than the " + std::to_string(kScratchBytes) +
+                                         " bytes of scratch of the allocation-free entry point (C * (L2+1)^2 * 4 "
+                                         "bytes of filter when no rotated-frame kernel serves the plan)");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  if (!p->scratch) return fail(GTP_ERR_HIP, "plan has no scratch address");
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  const size_t es = dtype_size(in_dtype);
+  const int64_t K1 = gtp::nsh(p->L1), Ko = gtp::nsh(p->Lout), H = p->L2 + 1;
+  // edges in chunks that fit the scratch; the launches of a chunk are
+  // stream-ordered after those of the previous one, so each chunk reuses the
+  // whole array.  Every scratch entry a kernel reads was written earlier in
+  // the same chunk: nothing needs clearing.
+  const int64_t chunk = cap / per_edge < B ? cap / per_edge : B;
+  for (int64_t b0 = 0; b0 < B; b0 += chunk) {
+    const int64_t nb = B - b0 < chunk ? B - b0 : chunk;
+    const void* xc = static_cast<const char*>(x) + size_t(b0) * C * K1 * es;
+    const float* rc = r + size_t(b0) * 3;
+    const float* hc = h + size_t(b0) * C * H;
+    float* yc = y + size_t(b0) * C * Ko;
+    hipError_t e = hipSuccess;
+    if (rot) {
+      bool done = false;
+      e = gtp::launch_conv_escn(p->escd, p->L1, p->L2, p->Lout, xc, it, rc, hc, nb, C, yc, p->scratch, st, &done);
+      if (!done) return fail(GTP_ERR_HIP, "rotated-frame kernel missing for a plan that has its tables");
+      if (e != hipSuccess) return hip_fail(e, "gtp_conv_escn_noalloc launch");
+    } else {
+      e = gtp::launch_sh_filter(p->L2, rc, hc, nb, C, p->scratch, st);
+      if (e != hipSuccess) return hip_fail(e, "gtp_conv_escn_noalloc filter launch");
+      if ((s = run_product(p, xc, it, p->scratch, gtp::IN_F32, nb * C, yc, st, "gtp_conv_escn_noalloc launch")) !=
+          GTP_OK)
+        return s;
+    }
+  }
+  return GTP_OK;
 }
 
 gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype, const float* dy,

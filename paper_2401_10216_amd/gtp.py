@@ -47,6 +47,7 @@ _SIGS = {
     "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
     "gtp_full_weighted": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_conv_escn": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
+    "gtp_conv_escn_noalloc": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
     "gtp_channel_mix": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _I64, _I64, _P, _P]),
     "gtp_sh2fourier": (_I, [_P, _I, _P, _I, _I64, _P, _P]),
     "gtp_fourier_conv": (_I, [_P, _P, _P, _I64, _P, _P]),
@@ -229,8 +230,10 @@ def gtp_channel_mix(plan: Plan, x1, x2, W, y=None, stream=None):
     return y
 
 
-def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None):
-    """y[B,C,(Lout+1)^2] = GTP(x, h[b,c,l] Y_l(r_b / |r_b|)) in the edge's rotated frame; r [B, 3], h [B, C, L2+1] fp32."""
+def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None, noalloc: bool = False):
+    """y[B,C,(Lout+1)^2] = GTP(x, h[b,c,l] Y_l(r_b / |r_b|)) in the edge's rotated frame; r [B, 3], h [B, C, L2+1] fp32.
+    noalloc=True calls gtp_conv_escn_noalloc (static device scratch, no allocation by the library; y must then be
+    given for no allocation to happen at all)."""
     import torch
     if x.dim() != 3 or x.shape[2] != nsh(plan.L1):
         raise ValueError("x must be [B, C, (L1+1)^2]")
@@ -247,7 +250,8 @@ def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None):
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x.device)
     py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x.device)
     _on_gpu(x, "x")
-    _check(lib().gtp_conv_escn(plan.handle, px, code, pr, ph, B, C, py, _stream(stream)))
+    fn = lib().gtp_conv_escn_noalloc if noalloc else lib().gtp_conv_escn
+    _check(fn(plan.handle, px, code, pr, ph, B, C, py, _stream(stream)))
     return y
 
 

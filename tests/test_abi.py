@@ -329,3 +329,28 @@ def test_fail_alloc_hook_reports_alloc_error(L, monkeypatch):
     monkeypatch.delenv("GTP_TEST_FAIL_ALLOC")
     assert L.gtp_plan_create(ctypes.byref(h), 3, 3, 3, gtp.GTP_PLAN_HOST_ONLY) == gtp.GTP_OK
     assert L.gtp_plan_destroy(h) == gtp.GTP_OK
+
+
+def test_noalloc_escn_validation(L):
+    """gtp_conv_escn_noalloc shares gtp_conv_escn's checks and refuses, before
+    any HIP call, an edge whose scratch needs exceed the static array."""
+    x, r, h, y = fake(0x1000000), fake(0x2000000), fake(0x3000000), fake(0x40000000)
+    S = ctypes.c_void_p(0)
+    INV = gtp.GTP_ERR_INVALID_ARG
+    f = L.gtp_conv_escn_noalloc
+    p = host_plan(6, 6, 6)
+    assert f(None, x, 0, r, h, 4, 4, y, S) == INV
+    assert f(p.handle, x, 3, r, h, 4, 4, y, S) == INV
+    assert f(p.handle, x, 0, r, h, -1, 4, y, S) == INV
+    assert f(p.handle, x, 0, None, h, 4, 4, y, S) == INV
+    assert f(p.handle, x, 0, r, h, 4, 4, fake(0x1000000 + 8), S) == INV  # y overlaps x
+    assert f(p.handle, x, 0, fake(0x2000002), h, 4, 4, y, S) == INV  # misaligned r
+    assert f(p.handle, x, 0, r, h, 0, 4, y, S) == gtp.GTP_OK
+    assert f(p.handle, x, 0, r, h, 4, 4, y, S) == INV and b"HOST_ONLY" in L.gtp_last_error()
+    q = host_plan(2, 64, 2)  # filter route: C * 65^2 * 4 bytes per edge
+    C = (64 << 20) // (4 * 65 * 65) + 1
+    assert f(q.handle, x, 0, r, h, 1, C, y, S) == gtp.GTP_ERR_UNSUPPORTED
+    assert b"scratch" in L.gtp_last_error()
+    # a huge channel count: refused without overflowing on the way
+    assert f(q.handle, x, 0, r, fake(1 << 47), 1, 1 << 40, fake(1 << 50), S) == gtp.GTP_ERR_UNSUPPORTED
+    assert f(q.handle, x, 0, r, h, 2, C - 1, y, S) == INV and b"HOST_ONLY" in L.gtp_last_error()
