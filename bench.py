@@ -257,7 +257,8 @@ def make_workload(args, torch, gtp, inputs):
             t1 = torch.from_numpy(x1).to(dev)
             t2 = torch.from_numpy(x2).to(dev)
             in_bytes = 4
-        flags = {"auto": 0, "direct": gtp.GTP_CONV_DIRECT, "generic": gtp.GTP_FORCE_GENERIC}[args.conv]
+        flags = {"auto": 0, "direct": gtp.GTP_CONV_DIRECT, "generic": gtp.GTP_FORCE_GENERIC,
+                 "fft": gtp.GTP_CONV_FFT, "dft": gtp.GTP_CONV_DFT}[args.conv]
         plan = gtp.Plan(L, L, L, flags)
         if args.products:
             # crossover runs: the first N products, as [N, 1, K]
@@ -399,10 +400,11 @@ def main():
     ap.add_argument("--workload", default="edge")
     ap.add_argument("--L", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--conv", choices=["auto", "direct", "generic"], default="auto",
-                    help="step-2 algorithm for the convolution crossover: auto (the shipped kernels), direct "
+    ap.add_argument("--conv", choices=["auto", "direct", "generic", "fft", "dft"], default="auto",
+                    help="step-2 algorithm for the convolution crossover: auto (the measured fastest), direct "
                          "(fused direct real-form convolution), generic (workgroup-per-product convolution "
-                         "theorem, the direct kernel's structural twin)")
+                         "theorem, the direct kernel's structural twin), fft (convolution theorem with radix-2 FFT "
+                         "phi transforms), dft (convolution theorem with direct symmetric DFT phi transforms)")
     ap.add_argument("--backward", action="store_true",
                     help="time the backward pass (gtp_full_backward: both input gradients for a seeded dy) "
                          "of a pair workload instead of gtp_full")

@@ -58,10 +58,13 @@ typedef enum {
 
 typedef enum { GTP_F32 = 0, GTP_BF16 = 1 } gtp_dtype;
 
-/* Plan flags (bitwise or). */
-#define GTP_CONV_AUTO 0u      /* pick the 2D-convolution algorithm by measured crossover */
-#define GTP_CONV_DIRECT 1u    /* direct 2D convolution of the Fourier grids (eq. 2D-conv) */
-#define GTP_CONV_FFT 2u       /* convolution theorem: transform, pointwise product, transform back */
+/* Plan flags (bitwise or).  The two low bits pick step 2 (eq. 2D-conv). */
+#define GTP_CONV_AUTO 0u      /* the algorithm the measured crossover picks for the degrees */
+#define GTP_CONV_DIRECT 1u    /* direct 2D convolution of the Fourier grids */
+#define GTP_CONV_FFT 2u       /* convolution theorem, phi transforms by radix-2 FFTs where the library has such a
+                                 kernel (L1 = L2 = Lout in {16, 32}), by the direct DFTs below otherwise */
+#define GTP_CONV_DFT 3u       /* convolution theorem, phi transforms as direct DFTs over the 4-fold symmetric
+                                 sample grid (unrolled at small degree, matrix-core contractions from 16 on) */
 #define GTP_PLAN_HOST_ONLY 16u /* build the fp64 tables only; no HIP call (host-side checks) */
 
 /* Many-body modes for gtp_selfproduct. */
@@ -88,10 +91,11 @@ gtp_status gtp_plan_destroy(gtp_plan p);
  * x1: [B, C, (L1+1)^2], x2: [B, C, (L2+1)^2] of type in_dtype;
  * y: [B, C, (Lout+1)^2] fp32.  B*C == 0 is a successful no-op.  y must not
  * overlap x1 or x2.  The Fourier grids never leave the chip.  The plan's
- * GTP_CONV_* flag picks step 2 (eq. 2D-conv): the convolution theorem
- * (GTP_CONV_FFT, and GTP_CONV_AUTO, which measured faster at every degree)
- * or the direct real-form convolution (GTP_CONV_DIRECT; GTP_ERR_UNSUPPORTED
- * when its per-product working set exceeds 64 KB of LDS, about L1 = L2 = 40). */
+ * GTP_CONV_* flag picks step 2 (eq. 2D-conv): the convolution theorem with
+ * radix-2 FFTs (GTP_CONV_FFT) or direct DFTs (GTP_CONV_DFT) for the phi
+ * transforms, or the direct real-form convolution (GTP_CONV_DIRECT;
+ * GTP_ERR_UNSUPPORTED when its per-product working set exceeds 64 KB of LDS,
+ * about L1 = L2 = 40); GTP_CONV_AUTO takes the measured fastest. */
 gtp_status gtp_full(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
                     int64_t B, int64_t C, float *y, void *stream);
 
@@ -237,7 +241,7 @@ int64_t gtp_grid_floats(gtp_plan p, int which);
 
 /* Plan geometry: out[0..7] = {L1, L2, Lout, U = L1+L2, Le = min(Lout, U),
  * NT (theta intervals of the sampling grid on [0, pi]), NP (phi samples),
- * conv algorithm actually used by gtp_full (GTP_CONV_DIRECT or GTP_CONV_FFT)}. */
+ * step-2 algorithm gtp_full actually runs: GTP_CONV_DIRECT, GTP_CONV_FFT or GTP_CONV_DFT}. */
 gtp_status gtp_plan_info(gtp_plan p, int64_t *out8);
 
 /* Copy one of the plan's fp64 host tables (test aid, host memory):

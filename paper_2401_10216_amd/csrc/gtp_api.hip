@@ -26,7 +26,7 @@ struct gtp_plan_ {
   unsigned flags = 0;
   bool host_only = true;
   int device = -1;
-  int conv = GTP_CONV_FFT;
+  int conv = GTP_CONV_DFT;
   bool force_generic = false;
   gtp::Tables tab;
   gtp::EscnHost esc;  // rotated-frame convolution tables (L1 = L2 = Lout <= 8)
@@ -152,6 +152,7 @@ gtp_status upload(gtp_plan_* p, long fail_at) {
   d.TWR = d.SMP = d.SM0P = d.WP = nullptr;
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
+  d.phi_fft = p->conv == GTP_CONV_FFT ? 1 : 0;
   p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0};
   if (p->esc.NPAIR) {
     gtp::EscnDev& ed = p->escd;
@@ -189,13 +190,24 @@ gtp_status check_device() {
   return GTP_OK;
 }
 
+// The 2D-convolution algorithm of GTP_CONV_AUTO, from the measured crossover:
+// the convolution theorem at every degree (faster than the direct
+// convolution from L = 2 on), with the phi transforms as direct symmetric
+// DFTs (unrolled, or contractions on the matrix cores) wherever they beat the
+// radix-2 FFT kernels.
+unsigned auto_conv(int L1, int L2, int Lout) {
+  (void)L1;
+  (void)L2;
+  (void)Lout;
+  return GTP_CONV_DFT;
+}
+
 gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, int maxL) {
   if (!out) return fail(GTP_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (L1 < 0 || L2 < 0 || Lout < 0 || L1 > maxL || L2 > maxL || Lout > kMaxLout)
     return fail(GTP_ERR_INVALID_ARG, "degrees must satisfy 0 <= L1, L2, Lout <= 64");
   const unsigned conv = flags & 3u;
-  if (conv == 3u) return fail(GTP_ERR_INVALID_ARG, "GTP_CONV_DIRECT and GTP_CONV_FFT are exclusive");
   if (flags & ~(3u | GTP_PLAN_HOST_ONLY | kForceGeneric)) return fail(GTP_ERR_INVALID_ARG, "unknown flag bits");
   std::unique_ptr<gtp_plan_> p(new (std::nothrow) gtp_plan_);
   if (!p) return fail(GTP_ERR_ALLOC, "host allocation failed");
@@ -205,9 +217,7 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
   p->flags = flags;
   p->host_only = (flags & GTP_PLAN_HOST_ONLY) != 0;
   p->force_generic = (flags & kForceGeneric) != 0;
-  // The convolution-theorem path is used at every degree: its flop count is
-  // below the direct real-form convolution's from L = 2 on.
-  p->conv = conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : GTP_CONV_FFT;
+  p->conv = conv == GTP_CONV_AUTO ? int(auto_conv(L1, L2, Lout)) : int(conv);
   bool fail_host = false;
   const long fail_dev = fail_alloc_hook(&fail_host);
   try {
@@ -596,7 +606,7 @@ gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dty
   // coefficient is symmetric in its three (l, m) pairs, so the gradient of
   // <dy, GTP(x1, x2)> in x1 is the product of the functions of dy and x2
   // projected to degree L1 (and likewise for x2).
-  const unsigned conv = p->conv == GTP_CONV_DIRECT ? GTP_CONV_DIRECT : 0u;
+  const unsigned conv = p->flags & 3u;  // the same request for the gradient plans
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
   if (dx1) {
@@ -763,7 +773,10 @@ int64_t gtp_grid_floats(gtp_plan p, int which) {
 gtp_status gtp_plan_info(gtp_plan p, int64_t* out8) {
   if (!p || !out8) return fail(GTP_ERR_INVALID_ARG, "NULL argument");
   const gtp::Tables& t = p->tab;
-  const int64_t v[8] = {t.L1, t.L2, t.Lout, t.U, t.Le, t.NT, t.NP, p->conv};
+  // the FFT request is served by the radix-FFT kernels at equal degrees 16, 32
+  const bool radix = p->conv == GTP_CONV_FFT && !p->force_generic && (t.waveL == 16 || t.waveL == 32);
+  const int64_t used = p->conv == GTP_CONV_FFT && !radix ? GTP_CONV_DFT : p->conv;
+  const int64_t v[8] = {t.L1, t.L2, t.Lout, t.U, t.Le, t.NT, t.NP, used};
   std::memcpy(out8, v, sizeof(v));
   return GTP_OK;
 }

@@ -30,6 +30,7 @@ struct DevTables {
   const float* WP;    // [pass][it][lane][8]    theta analysis weights
   const int* XMAP;    // [lane][k]              LDS slot of input coefficient lane + 64 k
   int XQUADS;
+  int phi_fft;        // 1: the matrix-core kernel's phi transforms by radix-2 FFT (GTP_CONV_FFT)
 };
 
 enum InType : int { IN_F32 = 0, IN_BF16 = 1 };

@@ -21,6 +21,7 @@
 #include <type_traits>
 #include <utility>
 
+#include "gtp_ct.hpp"
 #include "gtp_device.hpp"
 #include "gtp_escn.hpp"
 
@@ -32,16 +33,6 @@ constexpr int kEW = 64;
 // Scheduling fence: bounds the loads the scheduler hoists ahead (each row of
 // D read early holds registers until it is used).
 #define GTP_ESCN_FENCE() __builtin_amdgcn_sched_barrier(0)
-
-template <int B, int... Is, typename F>
-__device__ __forceinline__ void efor_impl(std::integer_sequence<int, Is...>, F& f) {
-  (f(std::integral_constant<int, B + Is>{}), ...);
-}
-// Compile-time loop over [B, E).
-template <int B, int E, typename F>
-__device__ __forceinline__ void efor(F&& f) {
-  if constexpr (E > B) efor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
-}
 
 constexpr int ensh(int L) { return (L + 1) * (L + 1); }
 // padded row length of the degree-l block of D in LDS (16-byte rows)
@@ -148,7 +139,7 @@ __global__ __launch_bounds__(64 * kRotEdges) void k_escn_rot(const float* __rest
   // trig values of orders p and q.  Z(-g) on a coefficient pair (c, s) of
   // order m > 0: c' = c cos mg + s sin mg, s' = -c sin mg + s cos mg.
   if (valid) {
-    efor<0, L + 1>([&](auto LL) {
+    cfor<0, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), ew = erow(l);
       for (int e = lane; e < (l + 1) * (l + 1); e += 64) {
         const int p = e / (l + 1), q = e - p * (l + 1);
@@ -187,12 +178,12 @@ __global__ __launch_bounds__(64 * kRotEdges) void k_escn_rot(const float* __rest
   // D = J^T T: each item is four consecutive entries of one row (one J value
   // and one 16-byte quad of T per k), stored as one 16-byte write
   float* const Db = Dout + b * DS;
-  efor<0, L + 1>([&](auto LL) {
+  cfor<0, L + 1>([&](auto LL) {
     constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), nq = erow(l) / 4;
     for (int e = lane; e < d * nq; e += 64) {
       const int a = e / nq, q = e - a * nq;
       float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-      efor<0, d>([&](auto KK) {
+      cfor<0, d>([&](auto KK) {
         constexpr int k = decltype(KK)::value;
         const float jv = Jl[jo + k * d + a];
         const float4 tv = reinterpret_cast<const float4*>(Tl + dofs(l) + k * erow(l))[q];
@@ -227,7 +218,7 @@ template <int R, int NQ>
 __device__ __forceinline__ void load_drow(const float* Dl, float4 (&buf)[NQ]) {
   constexpr int l = rdeg(R), a = R - l * l;
   const float4* row = reinterpret_cast<const float4*>(Dl + dofs(l) + a * erow(l));
-  efor<0, erow(l) / 4>([&](auto QQ) { buf[decltype(QQ)::value] = row[decltype(QQ)::value]; });
+  cfor<0, erow(l) / 4>([&](auto QQ) { buf[decltype(QQ)::value] = row[decltype(QQ)::value]; });
 }
 
 // register budget per lane: 3 waves per SIMD up to L = 6, 2 above
@@ -275,7 +266,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
       typedef __attribute__((address_space(3))) void lds_void;
       typedef const __attribute__((address_space(1))) void glb_void;
       constexpr int NF = kEW * K, NQ = (NF + 255) / 256;
-      efor<0, NQ>([&](auto Q) {
+      cfor<0, NQ>([&](auto Q) {
         constexpr int q = decltype(Q)::value;
         const int e = (q * 64 + tid) * 4;
         if (q + 1 < NQ || e < NF)
@@ -285,7 +276,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     }
   }
   if (!staged) {
-    efor<0, K>([&](auto I) {
+    cfor<0, K>([&](auto I) {
       constexpr int k = decltype(I)::value;
       const unsigned i = unsigned(tid + k * kEW);
       v[k] = ld_x(xb, i < nx ? i : nx - 1);
@@ -296,7 +287,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   // never stored)
   float dv[4 * RD];
   const float4* Dg = reinterpret_cast<const float4*>(Dall + b * DS);
-  efor<0, RD>([&](auto I) {
+  cfor<0, RD>([&](auto I) {
     constexpr int q = decltype(I)::value;
     const int i = tid + q * kEW;
     const float4 w = Dg[i < ND4 ? i : ND4 - 1];
@@ -308,20 +299,20 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   float hv[H];
   const float* const hb = h + p0 * H;
   const unsigned hl = unsigned(tid < cnt ? tid : cnt - 1);  // lanes past the last channel read a valid row
-  efor<0, H>([&](auto I) { hv[decltype(I)::value] = hb[hl * H + decltype(I)::value]; });
+  cfor<0, H>([&](auto I) { hv[decltype(I)::value] = hb[hl * H + decltype(I)::value]; });
 
   // ---- 2. x rows into registers through the tile, then D into the tile's
   // space
   if (staged) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slab is in LDS
   } else {
-    efor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
+    cfor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
   }
   __syncthreads();
   float xr[K];
-  efor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
+  cfor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
   __syncthreads();
-  efor<0, RD>([&](auto I) {
+  cfor<0, RD>([&](auto I) {
     constexpr int q = decltype(I)::value;
     const int i = tid + q * kEW;
     if (i < ND4) reinterpret_cast<float4*>(Dl)[i] = make_float4(dv[4 * q], dv[4 * q + 1], dv[4 * q + 2], dv[4 * q + 3]);
@@ -335,34 +326,34 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   {
     float4 cur[NQM], nxt[NQM];
     load_drow<0>(Dl, cur);
-    efor<0, K>([&](auto RR) {
+    cfor<0, K>([&](auto RR) {
       constexpr int R = decltype(RR)::value, l = rdeg(R), d = 2 * l + 1;
       if constexpr (R + 1 < K) load_drow<R + 1>(Dl, nxt);
       GTP_ESCN_FENCE();
       float s = 0.0f;
-      efor<0, erow(l) / 4>([&](auto QQ) {
+      cfor<0, erow(l) / 4>([&](auto QQ) {
         constexpr int q = decltype(QQ)::value;
-        efor<0, 4>([&](auto EE) {
+        cfor<0, 4>([&](auto EE) {
           constexpr int bb = 4 * q + decltype(EE)::value;
           if constexpr (bb < d) s = fmaf(f4at<decltype(EE)::value>(cur[q]), xr[l * l + bb], s);
         });
       });
       xp[R] = s;
       GTP_ESCN_FENCE();
-      if constexpr (R + 1 < K) efor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
+      if constexpr (R + 1 < K) cfor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
     });
   }
 
   // ---- 4. product with the zonal filter, mirror pair by mirror pair (the
   // pair loop unrolled: table values are literals, zero entries dropped)
   float acc[K];
-  efor<0, K>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
-  efor<0, NPAIR>([&](auto JJ) {
+  cfor<0, K>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+  cfor<0, NPAIR>([&](auto JJ) {
     constexpr int j = decltype(JJ)::value;
     GTP_ESCN_FENCE();
     // filter at t_j and its mirror (Theta_l0(pi - t) = (-1)^l Theta_l0(t))
     float fe = 0.0f, fo = 0.0f;
-    efor<0, H>([&](auto LL) {
+    cfor<0, H>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       constexpr float z = EscnConsts<L>::E[j][l];
       if constexpr (z != 0.0f) {
@@ -371,12 +362,12 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
       }
     });
     const float fj = fe + fo, fm = fe - fo;
-    efor<0, L + 1>([&](auto MM) {
+    cfor<0, L + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
-      efor<0, (m == 0 ? 1 : 2)>([&](auto SS) {
+      cfor<0, (m == 0 ? 1 : 2)>([&](auto SS) {
         constexpr int sg = decltype(SS)::value;  // 0: cos part (+m), 1: sin part (-m)
         float ae = 0.0f, ao = 0.0f;
-        efor<m, L + 1>([&](auto LL) {
+        cfor<m, L + 1>([&](auto LL) {
           constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m);
           constexpr float sv = EscnConsts<L>::E[j][EG::OS(m) + l - m];
           if constexpr (sv != 0.0f) {
@@ -386,7 +377,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
         });
         const float pj = fj * (ae + ao), pm = fm * (ae - ao);
         const float pe = pj + pm, po = pj - pm;
-        efor<m, L + 1>([&](auto LL) {
+        cfor<m, L + 1>([&](auto LL) {
           constexpr int l = decltype(LL)::value, i = l * l + l + (sg ? -m : m);
           constexpr int wi = EG::OW(m) + l - m;
           constexpr float wv = EscnConsts<L>::E[j][wi];
@@ -400,29 +391,29 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
 
   // ---- 5. y = D^T y', row by row with the same prefetch
   float yv[K];
-  efor<0, K>([&](auto I) { yv[decltype(I)::value] = 0.0f; });
+  cfor<0, K>([&](auto I) { yv[decltype(I)::value] = 0.0f; });
   {
     float4 cur[NQM], nxt[NQM];
     load_drow<0>(Dl, cur);
-    efor<0, K>([&](auto RR) {
+    cfor<0, K>([&](auto RR) {
       constexpr int R = decltype(RR)::value, l = rdeg(R), d = 2 * l + 1;
       if constexpr (R + 1 < K) load_drow<R + 1>(Dl, nxt);
       GTP_ESCN_FENCE();
-      efor<0, erow(l) / 4>([&](auto QQ) {
+      cfor<0, erow(l) / 4>([&](auto QQ) {
         constexpr int q = decltype(QQ)::value;
-        efor<0, 4>([&](auto EE) {
+        cfor<0, 4>([&](auto EE) {
           constexpr int bb = 4 * q + decltype(EE)::value;
           if constexpr (bb < d) yv[l * l + bb] = fmaf(f4at<decltype(EE)::value>(cur[q]), acc[R], yv[l * l + bb]);
         });
       });
       GTP_ESCN_FENCE();
-      if constexpr (R + 1 < K) efor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
+      if constexpr (R + 1 < K) cfor<0, NQM>([&](auto QQ) { cur[decltype(QQ)::value] = nxt[decltype(QQ)::value]; });
     });
   }
 
   // ---- 6. store through the tile (coalesced)
   __syncthreads();  // every lane is done with D and the table
-  efor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = yv[decltype(I)::value]; });
+  cfor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = yv[decltype(I)::value]; });
   __syncthreads();
   // store indices from an opaque copy of the lane id: not kept alive from the
   // loads' index arithmetic
@@ -434,12 +425,12 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     // in 16-byte stores from the 16-byte aligned tile
     typedef float sv4 __attribute__((ext_vector_type(4)));
     constexpr int N4 = kEW * K / 4, NQ = (N4 + kEW - 1) / kEW;
-    efor<0, NQ>([&](auto Q) {
+    cfor<0, NQ>([&](auto Q) {
       const int i4 = ln + decltype(Q)::value * kEW;
       if (i4 < N4) reinterpret_cast<sv4*>(yb)[i4] = reinterpret_cast<const sv4*>(tile)[i4];
     });
   } else {
-    efor<0, K>([&](auto I) {
+    cfor<0, K>([&](auto I) {
       const unsigned i = unsigned(ln + decltype(I)::value * kEW);
       if (i < nx) yb[i] = tile[i];
     });

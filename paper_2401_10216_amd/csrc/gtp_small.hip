@@ -15,6 +15,7 @@
 #include <type_traits>
 #include <utility>
 
+#include "gtp_ct.hpp"
 #include "gtp_device.hpp"
 
 // Scheduling fence between the per-node stages: keeps the two mirror nodes
@@ -24,50 +25,6 @@
 
 namespace gtp {
 namespace {
-
-constexpr double kPiD = 3.14159265358979323846264338327950288;
-
-// cos / sin of 2 pi k / N by exact integer reduction and a Taylor series,
-// evaluated at compile time (fp64, rounded once to fp32 where used).
-constexpr double ct_angle(long long k, long long N) {
-  long long r = k % N;
-  if (r < 0) r += N;
-  double x = 2.0 * kPiD * double(r) / double(N);
-  if (x > kPiD) x -= 2.0 * kPiD;
-  return x;
-}
-constexpr double ct_cos2pi(long long k, long long N) {
-  const double x = ct_angle(k, N);
-  double term = 1.0, sum = 1.0;
-  for (int i = 1; i < 40; ++i) {
-    term *= -x * x / double((2 * i - 1) * (2 * i));
-    sum += term;
-  }
-  return sum;
-}
-constexpr double ct_sin2pi(long long k, long long N) {
-  const double x = ct_angle(k, N);
-  double term = x, sum = x;
-  for (int i = 1; i < 40; ++i) {
-    term *= -x * x / double((2 * i) * (2 * i + 1));
-    sum += term;
-  }
-  return sum;
-}
-constexpr float ct_round(double v) {
-  // exact zeros and units stay exact; everything else rounds to fp32
-  return (v > -1e-15 && v < 1e-15) ? 0.0f : float(v);
-}
-
-template <int B, int... Is, typename F>
-__device__ __forceinline__ void sfor_impl(std::integer_sequence<int, Is...>, F& f) {
-  (f(std::integral_constant<int, B + Is>{}), ...);
-}
-// Compile-time loop over [B, E).
-template <int B, int E, typename F>
-__device__ __forceinline__ void sfor(F&& f) {
-  if constexpr (E > B) sfor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
-}
 
 constexpr int ctri(int l, int m) { return l * (l + 1) / 2 + m; }
 // degree of coefficient index i = l*l + l + m
@@ -147,11 +104,11 @@ template <int M, int NP>
 __device__ __forceinline__ void phi_synth(const float (&A)[2 * M + 1], float (&F)[NP]) {
   static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
   constexpr int Q = NP / 4;
-  sfor<0, Q + 1>([&](auto KK) {
+  cfor<0, Q + 1>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     // partial sums over even / odd m of the cos and sin parts
     float pe = A[0], po = 0.0f, qe = 0.0f, qo = 0.0f;
-    sfor<1, M + 1>([&](auto MM) {
+    cfor<1, M + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
       constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
@@ -184,8 +141,8 @@ template <int MO, int NP>
 __device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 * MO + 1]) {
   static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
   constexpr int Q = NP / 4;
-  sfor<0, 2 * MO + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
-  sfor<0, Q + 1>([&](auto KK) {
+  cfor<0, 2 * MO + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
+  cfor<0, Q + 1>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     // even-m / odd-m folds of the four points sharing this quarter angle
     float ce, co, se = 0.0f, so = 0.0f;
@@ -204,7 +161,7 @@ __device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 
       se = d + e;
       so = d - e;
     }
-    sfor<0, MO + 1>([&](auto MM) {
+    cfor<0, MO + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
       constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
@@ -221,10 +178,10 @@ __device__ __forceinline__ void phi_analysis(const float (&F)[NP], float (&C)[2 
 template <int L, typename X, typename T>
 __device__ __forceinline__ void theta_synth_pair(X x, const T& Sj, float (&Aj)[2 * L + 1],
                                                  float (&Ajp)[2 * L + 1]) {
-  sfor<0, L + 1>([&](auto MM) {
+  cfor<0, L + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     float ec = 0.0f, oc = 0.0f, es = 0.0f, os = 0.0f;
-    sfor<m, L + 1>([&](auto LL) {
+    cfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float sv = Sj[ctri(l, m)];
       if constexpr ((l + m) % 2 == 0) {
@@ -251,10 +208,10 @@ __device__ __forceinline__ void theta_synth_pair(X x, const T& Sj, float (&Aj)[2
 // MIRROR = true gives t_{NT-j} (Theta_lm picks up (-1)^(l+m)).
 template <int L, bool MIRROR, typename X, typename T>
 __device__ __forceinline__ void theta_synth_node(X x, const T& Sj, float (&A)[2 * L + 1]) {
-  sfor<0, L + 1>([&](auto MM) {
+  cfor<0, L + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     float ec = 0.0f, es = 0.0f;
-    sfor<m, L + 1>([&](auto LL) {
+    cfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float sv = (MIRROR && (l + m) % 2) ? -Sj[ctri(l, m)] : Sj[ctri(l, m)];
       mac<l == m>(ec, sv, x(std::integral_constant<int, l * l + l + m>{}));
@@ -275,9 +232,9 @@ __device__ __forceinline__ void theta_synth_node(X x, const T& Sj, float (&A)[2 
 template <int LE, bool MIRROR, typename T, bool FIRST = false>
 __device__ __forceinline__ void theta_analysis_node(const T& Wj, const float (&C)[2 * LE + 1],
                                                     float (&acc)[(LE + 1) * (LE + 1)]) {
-  sfor<0, LE + 1>([&](auto MM) {
+  cfor<0, LE + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
-    sfor<m, LE + 1>([&](auto LL) {
+    cfor<m, LE + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float w = (MIRROR && (l + m) % 2) ? -Wj[ctri(l, m)] : Wj[ctri(l, m)];
       mac<(FIRST && m > 0)>(acc[l * l + l + m], w, C[m == 0 ? 0 : 2 * m - 1]);
@@ -289,10 +246,10 @@ __device__ __forceinline__ void theta_analysis_node(const T& Wj, const float (&C
 // Theta synthesis at the equator (only even l + m survive).
 template <int L, typename X>
 __device__ __forceinline__ void theta_synth_eq(X x, const float* __restrict__ Sj, float (&A)[2 * L + 1]) {
-  sfor<0, L + 1>([&](auto MM) {
+  cfor<0, L + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     float ec = 0.0f, es = 0.0f;
-    sfor<m, L + 1>([&](auto LL) {
+    cfor<m, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       if constexpr ((l + m) % 2 == 0) {
         const float sv = Sj[ctri(l, m)];
@@ -330,7 +287,7 @@ __device__ __forceinline__ void phi_classes(const float (&A)[2 * M + 1], float& 
                                             float& qo) {
   pe = A[0];
   po = qe = qo = 0.0f;
-  sfor<1, M + 1>([&](auto MM) {
+  cfor<1, M + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value;
     constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
     constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
@@ -358,8 +315,8 @@ __device__ __forceinline__ void node_product_cls(const float (&A)[2 * L1 + 1], c
                                                  float (&C)[2 * LE + 1]) {
   static_assert(NP % 4 == 0, "phi grid size must be a multiple of 4");
   constexpr int Q = NP / 4;
-  sfor<0, 2 * LE + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
-  sfor<0, Q + 1>([&](auto KK) {
+  cfor<0, 2 * LE + 1>([&](auto I) { C[decltype(I)::value] = 0.0f; });
+  cfor<0, Q + 1>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     float pe, po, qe, qo, pf, pg, qf, qg;  // f: pe po qe qo; g: pf pg qf qg
     phi_classes<L1, NP, k>(A, pe, po, qe, qo);
@@ -378,7 +335,7 @@ __device__ __forceinline__ void node_product_cls(const float (&A)[2 * L1 + 1], c
       se = fmaf(qo, pg, fmaf(qe, pf, fmaf(po, qg, pe * qf)));
       so = fmaf(qo, pf, fmaf(qe, pg, fmaf(po, qf, pe * qg)));
     }
-    sfor<0, LE + 1>([&](auto MM) {
+    cfor<0, LE + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
       constexpr float c = ct_round(ct_cos2pi((long long)m * k, NP));
       constexpr float sn = ct_round(ct_sin2pi((long long)m * k, NP));
@@ -399,7 +356,7 @@ __device__ __forceinline__ void node_product(const float (&A)[2 * L1 + 1], const
   } else {
     float F[NP];
     phi_synth<L1, NP>(A, F);
-    sfor<0, NP>([&](auto KK) { F[decltype(KK)::value] = ipow<NU>(F[decltype(KK)::value]); });
+    cfor<0, NP>([&](auto KK) { F[decltype(KK)::value] = ipow<NU>(F[decltype(KK)::value]); });
     phi_analysis<LE, NP>(F, C);
   }
 }
@@ -443,13 +400,13 @@ __device__ __forceinline__ void gtp_core_lit(XA xa, XB xb, float (&acc)[(L + 1) 
   using G = Geo<L, L, L, 0>;
   constexpr int NT = G::NT, NP = G::NP;
   static_assert(NT % 2 == 1, "equal degrees give an odd node count");
-  sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+  cfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
   {
     // poles: only m = 0 is non-zero and all phi samples are equal
     constexpr LitRow<L, 0, false> S0{};
     constexpr LitRow<L, 0, true> W0{};
     float ae = 0.0f, ao = 0.0f, be = 0.0f, bo = 0.0f;
-    sfor<0, L + 1>([&](auto LL) {
+    cfor<0, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       if constexpr (l % 2 == 0) {
         mac<l == 0>(ae, S0[ctri(l, 0)], xa(std::integral_constant<int, l * l + l>{}));
@@ -461,12 +418,12 @@ __device__ __forceinline__ void gtp_core_lit(XA xa, XB xb, float (&acc)[(L + 1) 
     });
     const float fn = (ae + ao) * (be + bo), fs = (ae - ao) * (be - bo);
     const float ce = float(NP) * (fn + fs), co = float(NP) * (fn - fs);
-    sfor<0, L + 1>([&](auto LL) {
+    cfor<0, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       acc[l * l + l] = W0[ctri(l, 0)] * ((l % 2 == 0) ? ce : co);
     });
   }
-  sfor<1, (NT + 1) / 2>([&](auto JJ) {
+  cfor<1, (NT + 1) / 2>([&](auto JJ) {
     constexpr int j = decltype(JJ)::value;
     constexpr LitRow<L, j, false> Sj{};
     constexpr LitRow<L, j, true> Wj{};
@@ -506,13 +463,13 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
   }
   using G = Geo<L1, L2, LO, NU>;
   constexpr int LE = G::LE, NT = G::NT, NP = G::NP;
-  sfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
+  cfor<0, G::KE>([&](auto I) { acc[decltype(I)::value] = 0.0f; });
 
   // Poles (t = 0 and t = pi): only m = 0 is non-zero; the phi samples are all
   // equal, so the m = 0 moment is NP times the product value.
   {
     float ae = 0.0f, ao = 0.0f, be = 0.0f, bo = 0.0f;
-    sfor<0, L1 + 1>([&](auto LL) {
+    cfor<0, L1 + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float sv = ST[ctri(l, 0)];
       if constexpr (l % 2 == 0) ae = fmaf(sv, xa(std::integral_constant<int, l * l + l>{}), ae);
@@ -520,7 +477,7 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
     });
     float fn, fs;
     if constexpr (NU == 0) {
-      sfor<0, L2 + 1>([&](auto LL) {
+      cfor<0, L2 + 1>([&](auto LL) {
         constexpr int l = decltype(LL)::value;
         const float sv = ST[ctri(l, 0)];
         if constexpr (l % 2 == 0) be = fmaf(sv, xb(std::integral_constant<int, l * l + l>{}), be);
@@ -533,7 +490,7 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
       fs = ipow<NU>(ae - ao);
     }
     const float ce = float(NP) * (fn + fs), co = float(NP) * (fn - fs);
-    sfor<0, LE + 1>([&](auto LL) {
+    cfor<0, LE + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       const float w = WT[ctri(l, 0)];
       acc[l * l + l] = fmaf(w, (l % 2 == 0) ? ce : co, acc[l * l + l]);
@@ -549,7 +506,7 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
   constexpr int NS = ctri(cmax(L1, L2), cmax(L1, L2)) + 1;
   constexpr int NW = ctri(LE, LE) + 1;
   float scur[NS];
-  sfor<0, NS>([&](auto I) { scur[decltype(I)::value] = ST[ntS + decltype(I)::value]; });
+  cfor<0, NS>([&](auto I) { scur[decltype(I)::value] = ST[ntS + decltype(I)::value]; });
   for (int j = 1; 2 * j < NT; ++j) {
     xa.touch();
     xb.touch();
@@ -561,13 +518,13 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
     if constexpr (NU == 0) theta_synth_node<L2, false>(xb, scur, Bj);
     GTP_SCHED_FENCE();
     float sb[NS];
-    sfor<0, NS>([&](auto I) { sb[decltype(I)::value] = scur[decltype(I)::value]; });
+    cfor<0, NS>([&](auto I) { sb[decltype(I)::value] = scur[decltype(I)::value]; });
     // row j + 1 always exists (j + 1 <= NT), even when it is not used
     const float* Sn = ST + (j + 1) * ntS;
-    sfor<0, NS>([&](auto I) { scur[decltype(I)::value] = Sn[decltype(I)::value]; });
+    cfor<0, NS>([&](auto I) { scur[decltype(I)::value] = Sn[decltype(I)::value]; });
     const float* Wj = WT + j * ntW;
     float wcur[NW];
-    sfor<0, NW>([&](auto I) { wcur[decltype(I)::value] = Wj[decltype(I)::value]; });
+    cfor<0, NW>([&](auto I) { wcur[decltype(I)::value] = Wj[decltype(I)::value]; });
     GTP_SCHED_FENCE();
     {
       float C[2 * LE + 1];
@@ -594,9 +551,9 @@ __device__ __forceinline__ void gtp_core(XA xa, XB xb, float (&acc)[Geo<L1, L2, 
     if constexpr (NU == 0) theta_synth_eq<L2>(xb, Sj, B);
     float Cq[2 * LE + 1];
     node_product<L1, L2, LE, NP, NU>(A, B, Cq);
-    sfor<0, LE + 1>([&](auto MM) {
+    cfor<0, LE + 1>([&](auto MM) {
       constexpr int m = decltype(MM)::value;
-      sfor<m, LE + 1>([&](auto LL) {
+      cfor<m, LE + 1>([&](auto LL) {
         constexpr int l = decltype(LL)::value;
         if constexpr ((l + m) % 2 == 0) {
           const float w = Wj[ctri(l, m)];
@@ -619,14 +576,14 @@ template <int K, typename TIn>
 __device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0, int cnt, float (&r)[K]) {
   const int tid = threadIdx.x;
   const TIn* const xr = x + (p0 + (tid < cnt ? tid : cnt - 1)) * K;
-  sfor<0, K>([&](auto I) { r[decltype(I)::value] = ld_in(xr, decltype(I)::value); });
+  cfor<0, K>([&](auto I) { r[decltype(I)::value] = ld_in(xr, decltype(I)::value); });
 }
 
 template <int KO, int KE>
 __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, int cnt, float* tile,
                                            const float (&acc)[KE]) {
   const int tid = threadIdx.x;
-  sfor<0, KO>([&](auto I) {
+  cfor<0, KO>([&](auto I) {
     constexpr int i = decltype(I)::value;
     tile[tid * KO + i] = (i < KE) ? acc[i < KE ? i : 0] : 0.0f;
   });
@@ -648,8 +605,8 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
 template <int L, int K, typename V>
 __device__ __forceinline__ void scale_by_degree(const float* __restrict__ wrow, V&& at) {
   float wl[L + 1];
-  sfor<0, L + 1>([&](auto LL) { wl[decltype(LL)::value] = wrow[decltype(LL)::value]; });
-  sfor<0, K>([&](auto I) { at(I) *= wl[cdeg(decltype(I)::value)]; });
+  cfor<0, L + 1>([&](auto LL) { wl[decltype(LL)::value] = wrow[decltype(LL)::value]; });
+  cfor<0, K>([&](auto I) { at(I) *= wl[cdeg(decltype(I)::value)]; });
 }
 
 template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT, bool OUT>
@@ -678,7 +635,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     if constexpr (OUT) pair_rows(pi, p, r1, r2);
     const T1* const xr1 = x1 + r1 * K1;
     const T2* const xr2 = x2 + r2 * K2;
-    sfor<0, K1>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
+    cfor<0, K1>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
     bool staged = false;
     // (measured: 2.4 % faster at L = 6; at L = 4 4 % and at L = 8 1 % slower
     // than the per-lane loads, so degrees 5..7 only)
@@ -693,7 +650,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
         typedef const __attribute__((address_space(1))) void glb_void;
         constexpr int NF = kTile * K2, NQ = (NF + 255) / 256;
         const float* const slab = x2 + p0 * K2;
-        sfor<0, NQ>([&](auto Q) {
+        cfor<0, NQ>([&](auto Q) {
           constexpr int q = decltype(Q)::value;
           const int e = (q * 64 + tid) * 4;
           if (q + 1 < NQ || e < NF)
@@ -704,7 +661,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
       }
     }
     if (!staged)
-      sfor<0, K2>([&](auto I) { tile[tid * K2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+      cfor<0, K2>([&](auto I) { tile[tid * K2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
     if constexpr (WGT) {
       // each lane scales its own product: x1 in registers, x2 in its tile row
       const int64_t row = weight_row(wt, p0 + tid);
@@ -754,7 +711,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
     float acc[G1::KE];
     RegX<K> A{a};
     gtp_core<L, L, LO, 0>(A, A, acc, t1.ST, t1.ntS, t1.WT, t1.ntW);
-    sfor<0, KO>([&](auto I) {
+    cfor<0, KO>([&](auto I) {
       constexpr int i = decltype(I)::value;
       b[i] = i < G1::KE ? acc[i < G1::KE ? i : 0] : 0.0f;
     });
@@ -764,7 +721,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
     RegX<K> A{a};
     RegX<KO> Bv{b};
     gtp_core<LO, L, LO, 0>(Bv, A, acc, t2.ST, t2.ntS, t2.WT, t2.ntW);
-    sfor<0, KO>([&](auto I) {
+    cfor<0, KO>([&](auto I) {
       constexpr int i = decltype(I)::value;
       b[i] = i < G2::KE ? acc[i < G2::KE ? i : 0] : 0.0f;
     });
@@ -870,21 +827,21 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
       const TIn* const xr1 = x1 + (b * C1 + c1) * Kd;
       const TIn* const xr2 = x2 + (b * C2 + c2) * Kd;
       float xa[Kd], acc[Kd];
-      sfor<0, Kd>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
-      sfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+      cfor<0, Kd>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
+      cfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
       RegX<Kd> A{xa};
       LdsX Bx{tile, tid * Kd};
       gtp_core<L, L, L, 0>(A, Bx, acc, ST, ntS, WT, ntW);
       // over the lane's own row (its x2 reads are done).  Slots past P hold
       // a copy of the last pair's product; their weight rows are zero.
-      sfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = acc[decltype(I)::value]; });
+      cfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = acc[decltype(I)::value]; });
     }
     // this wave's partial sums of the previous rounds (output rows k0 + 4 g +
     // rr of channel 16 ct + i) and its first weight block, requested before
     // the barrier so that they arrive while the other waves finish
     mixv4 macc[KTW][NCT], bw[KTW][NCT];
     const float* const wb = WB + ((r * 16) * CoB + i) * 16 + g * 4;
-    sfor<0, KTW>([&](auto TT) {
+    cfor<0, KTW>([&](auto TT) {
       constexpr int t = decltype(TT)::value;
       const int k0 = (wv + 4 * t) * 16;
 #pragma unroll
@@ -899,7 +856,7 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
       }
     });
     __syncthreads();
-    sfor<0, KTW>([&](auto TT) {
+    cfor<0, KTW>([&](auto TT) {
       constexpr int t = decltype(TT)::value;
       const int k0 = (wv + 4 * t) * 16;
       if (k0 < Kd) {  // wave-uniform

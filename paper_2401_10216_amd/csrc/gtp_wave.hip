@@ -8,19 +8,12 @@
 #include <type_traits>
 #include <utility>
 
+#include "gtp_ct.hpp"
 #include "gtp_device.hpp"
+#include "gtp_fft.hpp"
 
 namespace gtp {
 namespace {
-
-template <int B, int... Is, typename F>
-__device__ __forceinline__ void lfor_impl(std::integer_sequence<int, Is...>, F& f) {
-  (f(std::integral_constant<int, B + Is>{}), ...);
-}
-template <int B, int E, typename F>
-__device__ __forceinline__ void lfor(F&& f) {
-  if constexpr (E > B) lfor_impl<B>(std::make_integer_sequence<int, E - B>{}, f);
-}
 
 // Table reads go through buffer resources: 32-bit offsets (the wave-uniform
 // part in a scalar register), and reads past the table return zero.
@@ -126,6 +119,47 @@ struct WGeo {
   static constexpr int NXKP = (NXK + 3) / 4 * 4;
 };
 
+// Sizes of the FFT variant (radix-2 phi transforms of length NF = N1 N2,
+// NF >= 3L + 1: alias-free for the output moments |m| <= L of a product of
+// phi-degree 2L).  Per pass, in LDS: the packed spectra of the 16 column
+// nodes (NS = 2L + 1 entries each), the column-stage output T and the
+// row-stage output T2 (which reuses the spectra's space); the row strides
+// are padded by one complex entry against bank conflicts.
+template <int L>
+struct FGeo {
+  static constexpr int NF = L <= 16 ? 64 : (L <= 32 ? 128 : 256);
+  static constexpr int N1 = L <= 32 ? 8 : 16;  // column DFTs (over m1 / k1)
+  static constexpr int N2 = NF / N1;           // row DFTs (over m2 / k2)
+  static constexpr int NS = 2 * L + 1;         // packed spectrum of one node: m = 0..L, then -L..-1
+  static constexpr int H2 = N2 / 2 + 1;        // forward row outputs of a real row
+  static constexpr int TS = NF + 1;            // T column-node stride (complex entries)
+  static constexpr int T2S = H2 * N1 + 1;      // T2 column-node stride
+  static constexpr int AC = (16 * NS > 16 * T2S) ? 16 * NS : 16 * T2S;  // complex entries of A (spectra / T2)
+  static constexpr int TC = 16 * TS;                                    // complex entries of T
+  static_assert(NF >= 3 * L + 1 && NF == N1 * N2, "FFT length");
+};
+
+// exp(i 2 pi j / NF), j < NF (fp32 from fp64 compile-time values)
+template <int NF>
+struct TwTab {
+  cpx v[NF];
+};
+template <int NF>
+constexpr TwTab<NF> make_tw() {
+  TwTab<NF> t{};
+  for (int j = 0; j < NF; ++j) t.v[j] = cpx{ct_round(ct_cos2pi(j, NF)), ct_round(ct_sin2pi(j, NF))};
+  return t;
+}
+__device__ const TwTab<64> kTw64 = make_tw<64>();
+__device__ const TwTab<128> kTw128 = make_tw<128>();
+__device__ const TwTab<256> kTw256 = make_tw<256>();
+template <int NF>
+__device__ __forceinline__ cpx tw_root(int j) {
+  if constexpr (NF == 64) return kTw64.v[j];
+  else if constexpr (NF == 128) return kTw128.v[j];
+  else return kTw256.v[j];
+}
+
 // The value of lane i ^ 8: a DPP rotate by 8 within each 16-lane row (a
 // plain VALU move, no LDS round trip as with a lane permute).  These
 // exchanges run with all 64 lanes active (no divergent branch around them).
@@ -186,7 +220,7 @@ struct WaveCtx {
   // pass = PASSES gives the poles.  Split into the table read and the sums so
   // that other loads can be issued in between.
   __device__ __forceinline__ void m0_load(int pass, float (&sv)[G::NV0P]) const {
-    lfor<0, G::NV0P / 4>([&](auto V4) {
+    cfor<0, G::NV0P / 4>([&](auto V4) {
       constexpr int v4 = decltype(V4)::value;
       const float4 w = tload4_s(S0r, lane * G::NV0P * 4 + 16 * v4, pass * 64 * G::NV0P * 4);
       sv[4 * v4] = w.x;
@@ -197,7 +231,7 @@ struct WaveCtx {
   }
   __device__ __forceinline__ void m0_finish(const float (&sv)[G::NV0P], float& a1, float& a2) const {
     float s1 = 0.0f, s2 = 0.0f;
-    lfor<0, G::NV0>([&](auto V) {
+    cfor<0, G::NV0>([&](auto V) {
       constexpr int v = decltype(V)::value;
       const int l = 8 * v + g + 4 * h;
       if (8 * v + 7 <= L || l <= L) {
@@ -214,7 +248,11 @@ struct WaveCtx {
   // synthesis contractions, sample products, phi analysis contractions.
   // Returns the analysis accumulators o[mr][type] (row 4g + r of m-row block
   // mr, column i) and zz, the m = 0 moment of the lane's column node.
-  __device__ __forceinline__ void pass(int pu, f4 (&o)[G::NMR][4], float& zz) const {
+  // FFT = true (the radix-FFT variant) runs the theta synthesis only and
+  // writes each column node's packed phi spectrum to spec (phi_fft takes it
+  // from there); o and zz are then not written.
+  template <bool FFT = false>
+  __device__ __forceinline__ void pass(int pu, f4 (&o)[G::NMR][4], float& zz, float2* spec = nullptr) const {
     constexpr int NMB = G::NMB, NMBP = G::NMBP, NKS = G::NKS, TWRN = G::TWRN, NMR = G::NMR;
     // loads first (m = 0 part, the first theta-table steps, the first phi
     // operands), then the m = 0 sums
@@ -223,21 +261,21 @@ struct WaveCtx {
     float s0v[G::NV0P];
     m0_load(pu, s0v);
     float4 sring[D];
-    lfor<0, D>([&](auto T) {
+    cfor<0, D>([&](auto T) {
       constexpr int tt = decltype(T)::value;
       if constexpr (tt < G::TU2) sring[tt] = tload4_s(SPr, lane * 16, sbase + tt * 64 * 16);
     });
     // synthesis operands twc[type][mb] of K-step 0 and the rotation by 8 phi_k
     const f4* seeds = reinterpret_cast<const f4*>(TWR + lane * TWRN);
     float twc[4][NMB], r8c[NMB], r8s[NMB];
-    {
+    if constexpr (!FFT) {
       float sd[6 * NMBP];
-      lfor<0, 6 * NMBP / 4>([&](auto Q4) {
+      cfor<0, 6 * NMBP / 4>([&](auto Q4) {
         constexpr int q4 = decltype(Q4)::value;
         const f4 v = seeds[q4];
-        lfor<0, 4>([&](auto E) { sd[4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
+        cfor<0, 4>([&](auto E) { sd[4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
       });
-      lfor<0, NMB>([&](auto MB) {
+      cfor<0, NMB>([&](auto MB) {
         constexpr int mb = decltype(MB)::value;
         twc[0][mb] = sd[6 * mb + 0];  // cos, even m
         twc[2][mb] = sd[6 * mb + 1];  // sin, even m
@@ -252,18 +290,23 @@ struct WaveCtx {
 
     // ---- 1 + 2a. theta synthesis feeding the phi-synthesis contractions
     f4 acc[2][NMB][4];  // [input][k block][type]
-    lfor<0, NMB>([&](auto MB) {
+    // the FFT variant's packed spectrum of the lane's column node (see phi_fft)
+    float2* const sc = spec + (8 * h + pi) * FGeo<L>::NS;
+    if constexpr (FFT) {
+      if (g == 0) sc[0] = make_float2(2.0f * c1, 2.0f * c2);
+    }
+    if constexpr (!FFT) cfor<0, NMB>([&](auto MB) {
       constexpr int mb = decltype(MB)::value;
       acc[0][mb][0] = f4{c1, c1, c1, c1};  // m = 0 enters every pe sample
       acc[1][mb][0] = f4{c2, c2, c2, c2};
-      lfor<1, 4>([&](auto TY) {
+      cfor<1, 4>([&](auto TY) {
         acc[0][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
         acc[1][mb][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f};
       });
     });
     float asd[NMR][4 * NMB];  // analysis seeds, read during the last K-step
     f4 ast[NMR];
-    lfor<0, NKS>([&](auto SS) {
+    cfor<0, NKS>([&](auto SS) {
       constexpr int s = decltype(SS)::value;
       // the x block of m-pair c = 4 s + g: xb(4 s + g) = xb(4 s) + g (4 nu(s) + 1)
       // - 2 g (g - 1), written so that only the g terms are left to run time
@@ -272,11 +315,11 @@ struct WaveCtx {
       const float4* xa = xq + xo + h;
       const float4* xe = xq + xo + 3 - h;
       f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
-      lfor<0, G::nu(s) / 2>([&](auto U2) {
+      cfor<0, G::nu(s) / 2>([&](auto U2) {
         constexpr int u2 = decltype(U2)::value, tt = G::u2off(s) + u2;
         const float4 sv = sring[tt % D];
         if constexpr (tt + D < G::TU2) sring[tt % D] = tload4_s(SPr, lane * 16, sbase + (tt + D) * 64 * 16);
-        lfor<0, 2>([&](auto E) {
+        cfor<0, 2>([&](auto E) {
           constexpr int u = 2 * u2 + decltype(E)::value;
           const float so = E == 0 ? sv.x : sv.z, se = E == 0 ? sv.y : sv.w;
           const float4 qa = xa[4 * u], qe = xe[4 * u];
@@ -285,13 +328,13 @@ struct WaveCtx {
         });
         __builtin_amdgcn_sched_barrier(0);  // keep the prefetch distance
       });
-      if constexpr (s == NKS - 1) {
-        lfor<0, NMR>([&](auto MR) {
+      if constexpr (s == NKS - 1 && !FFT) {
+        cfor<0, NMR>([&](auto MR) {
           constexpr int mr = decltype(MR)::value;
-          lfor<0, NMB>([&](auto Q4) {
+          cfor<0, NMB>([&](auto Q4) {
             constexpr int q4 = decltype(Q4)::value;
             const f4 v = seeds[(G::ASD + 4 * (mr * NMBP + q4)) / 4];
-            lfor<0, 4>([&](auto E) { asd[mr][4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
+            cfor<0, 4>([&](auto E) { asd[mr][4 * q4 + decltype(E)::value] = v[decltype(E)::value]; });
           });
           ast[mr] = seeds[(G::AST + 4 * mr) / 4];
         });
@@ -299,24 +342,36 @@ struct WaveCtx {
       // column value: node jp (h = 0: own even + partner odd) or its mirror
       // (h = 1: partner even - own odd); sg * v + partner is exact for sg = +-1
       f4 Bo, Be;
-      lfor<0, 4>([&](auto C) {
+      cfor<0, 4>([&](auto C) {
         constexpr int cc = decltype(C)::value;
         Bo[cc] = fmaf(sg, Vo[cc], xor8(Vo[cc]));
         Be[cc] = fmaf(sg, Ve[cc], xor8(Ve[cc]));
       });
-      lfor<0, NMB>([&](auto MB) {
-        constexpr int mb = decltype(MB)::value;
-        lfor<0, 2>([&](auto TI) {
-          constexpr int ti = decltype(TI)::value;
-          acc[ti][mb][0] = mfma4(twc[0][mb], Be[2 * ti], acc[ti][mb][0]);
-          acc[ti][mb][1] = mfma4(twc[1][mb], Bo[2 * ti], acc[ti][mb][1]);
-          acc[ti][mb][2] = mfma4(twc[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
-          acc[ti][mb][3] = mfma4(twc[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
+      if constexpr (FFT) {
+        // B = (x1 cos, x1 sin, x2 cos, x2 sin) of m-parts mo = 8 s + 2 g + 1
+        // (Bo) and mo + 1 (Be): twice the packed coefficients
+        // d_{+m} = (a1 + b2, a2 - b1), d_{-m} = (a1 - b2, a2 + b1)
+        constexpr int NS = FGeo<L>::NS;
+        const int mo = 8 * s + 2 * g + 1;
+        sc[mo] = make_float2(Bo[0] + Bo[3], Bo[2] - Bo[1]);
+        sc[NS - mo] = make_float2(Bo[0] - Bo[3], Bo[2] + Bo[1]);
+        sc[mo + 1] = make_float2(Be[0] + Be[3], Be[2] - Be[1]);
+        sc[NS - mo - 1] = make_float2(Be[0] - Be[3], Be[2] + Be[1]);
+      } else {
+        cfor<0, NMB>([&](auto MB) {
+          constexpr int mb = decltype(MB)::value;
+          cfor<0, 2>([&](auto TI) {
+            constexpr int ti = decltype(TI)::value;
+            acc[ti][mb][0] = mfma4(twc[0][mb], Be[2 * ti], acc[ti][mb][0]);
+            acc[ti][mb][1] = mfma4(twc[1][mb], Bo[2 * ti], acc[ti][mb][1]);
+            acc[ti][mb][2] = mfma4(twc[2][mb], Be[2 * ti + 1], acc[ti][mb][2]);
+            acc[ti][mb][3] = mfma4(twc[3][mb], Bo[2 * ti + 1], acc[ti][mb][3]);
+          });
         });
-      });
-      if constexpr (s + 1 < NKS) {
+      }
+      if constexpr (s + 1 < NKS && !FFT) {
         // next K-step: m -> m + 8
-        lfor<0, NMB>([&](auto MB) {
+        cfor<0, NMB>([&](auto MB) {
           constexpr int mb = decltype(MB)::value;
           rot(twc[0][mb], twc[2][mb], r8c[mb], r8s[mb]);
           rot(twc[1][mb], twc[3][mb], r8c[mb], r8s[mb]);
@@ -324,6 +379,7 @@ struct WaveCtx {
       }
     });
 
+    if constexpr (FFT) return;
     // ---- 2b. sample products, folded over the 4-point sets.  The samples at
     // k, -k, 2Q + k, 2Q - k are pe + po +- (qe + qo) and pe - po +- (qe - qo);
     // summed over the four points the product folds to 4 (pe pe' + po po' +
@@ -334,7 +390,7 @@ struct WaveCtx {
     // and Q are counted twice there and weighted 1/2).  At L = 64 (256
     // registers) the samples are formed and folded instead (weights 1/2 and
     // 1), which keeps fewer values live; the result is the same.
-    lfor<0, NMB>([&](auto MB) {
+    cfor<0, NMB>([&](auto MB) {
       constexpr int mb = decltype(MB)::value;
       const f4 pe1 = acc[0][mb][0], po1 = acc[0][mb][1], qe1 = acc[0][mb][2], qo1 = acc[0][mb][3];
       const f4 pe2 = acc[1][mb][0], po2 = acc[1][mb][1], qe2 = acc[1][mb][2], qo2 = acc[1][mb][3];
@@ -362,16 +418,16 @@ struct WaveCtx {
     // holds that sample), m = 2(16 mr + i) + 2 (even types) or + 1 (odd
     // types).  A contraction whose four samples all lie past Q (weight zero)
     // is skipped.
-    lfor<0, NMR>([&](auto MR) {
-      lfor<0, 4>([&](auto TY) { o[decltype(MR)::value][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
+    cfor<0, NMR>([&](auto MR) {
+      cfor<0, 4>([&](auto TY) { o[decltype(MR)::value][decltype(TY)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
     });
     zz = 0.0f;
-    lfor<0, NMB>([&](auto MB) {
+    cfor<0, NMB>([&](auto MB) {
       constexpr int mb = decltype(MB)::value;
-      lfor<0, NMR>([&](auto MR) {
+      cfor<0, NMR>([&](auto MR) {
         constexpr int mr = decltype(MR)::value;
         float ce = asd[mr][4 * mb + 0], se = asd[mr][4 * mb + 1], co = asd[mr][4 * mb + 2], so = asd[mr][4 * mb + 3];
-        lfor<0, 4>([&](auto R) {
+        cfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
           if constexpr (16 * mb + 4 * r <= G::Q) {
             if constexpr (r > 0) {
@@ -413,11 +469,11 @@ struct WaveCtx {
   // 2m + 1 = sin m
   __device__ __forceinline__ void store_moments(float* eo, const f4 (&o)[G::NMR][4], float zz) const {
     float* const eoh = eo + (h * 8 + pi) * G::NMP2;
-    lfor<0, G::NMR>([&](auto MR) {
+    cfor<0, G::NMR>([&](auto MR) {
       constexpr int mr = decltype(MR)::value;
-      lfor<0, 2>([&](auto PAR) {
+      cfor<0, 2>([&](auto PAR) {
         constexpr int odd = decltype(PAR)::value;  // types odd (cos), odd + 2 (sin)
-        lfor<0, 4>([&](auto R) {
+        cfor<0, 4>([&](auto R) {
           constexpr int r = decltype(R)::value;
           const int m = 2 * (16 * mr + 4 * g + r) + (odd ? 1 : 2);
           const float vc = fmaf(sg, o[mr][odd][r], xor8(o[mr][odd][r]));
@@ -430,6 +486,139 @@ struct WaveCtx {
     const float vz = fmaf(sg, zz, xor8(zz));
     if (g == 0) eoh[0] = vz;
   }
+
+  // ---- 2 (FFT variant). The phi transforms of one pass by radix-2 FFTs of
+  // length NF = N1 N2 (four-step split, index n = N2 n1 + n2 on the
+  // spectrum side, k = k1 + N1 k2 on the sample side).  A holds, for each of
+  // the 16 column nodes, twice the packed spectrum d_m = c1_m + i c2_m of the
+  // two inputs (c_m the complex Fourier coefficients of the node's phi
+  // function, |m| <= L), so that one inverse transform gives 2 (f1 + i f2) at
+  // the NF samples and the product is Re * Im.  Then:
+  //   1. columns (node, n2): inverse DFT over n1 of d[N2 n1 + n2], times
+  //      exp(+i 2 pi n2 k1 / NF)                                    -> T[node][k1][n2]
+  //   2. rows (node, k1): inverse DFT over n2 (the samples k1 + N1 k2), the
+  //      product g, forward DFT over k2 of the real g (outputs m2 <= N2/2),
+  //      times exp(-i 2 pi m2 k1 / NF)                              -> T2[node][m2][k1]
+  //   3. columns (pair, m2): forward DFT over k1 of the node's and the
+  //      mirror's column; the outputs with |m| <= L are the moments
+  //      sum_k g cos(m p_k) and sum_k g sin(m p_k), combined into the sum and
+  //      difference of the mirror nodes (the layout store_moments writes).
+  // The moments are rescaled to the plan's NP-point convention (NP / NF,
+  // and 1/8 for the factors 2 of the packing and of the real transform).
+  __device__ __forceinline__ void phi_fft(float* eo, float2* A, float2* T) const {
+    using F = FGeo<L>;
+    constexpr int NF = F::NF, N1 = F::N1, N2 = F::N2, NS = F::NS, H2 = F::H2, TS = F::TS, T2S = F::T2S;
+    const int ci = lane & 15, q = lane >> 4;
+    // 1. columns n2 = q + 4 t of node ci
+    cfor<0, N2 / 4>([&](auto TT) {
+      const int n2 = q + 4 * decltype(TT)::value;
+      const float2* sp = A + ci * NS;
+      cpx a[N1];
+      cfor<0, N1>([&](auto M1) {
+        constexpr int lo = N2 * decltype(M1)::value, hi = lo + N2 - 1;
+        // spectrum index n = lo + n2 holds m = n (n <= L) or m = n - NF (n >= NF - L)
+        if constexpr (hi <= L) {
+          const float2 v = sp[lo + n2];
+          a[decltype(M1)::value] = {v.x, v.y};
+        } else if constexpr (lo >= NF - L) {
+          const float2 v = sp[NS - NF + lo + n2];
+          a[decltype(M1)::value] = {v.x, v.y};
+        } else if constexpr (lo <= L) {
+          const int n = lo + n2;
+          const float2 v = sp[n <= L ? n : 0];
+          a[decltype(M1)::value] = n <= L ? cpx{v.x, v.y} : cpx{0.0f, 0.0f};
+        } else if constexpr (hi >= NF - L) {
+          const int n = lo + n2;
+          const float2 v = sp[n >= NF - L ? NS - NF + n : 0];
+          a[decltype(M1)::value] = n >= NF - L ? cpx{v.x, v.y} : cpx{0.0f, 0.0f};
+        } else {
+          a[decltype(M1)::value] = {0.0f, 0.0f};
+        }
+      });
+      fft_reg<N1, +1>(a);
+      cpx w[N1];
+      cpowers<N1>(tw_root<NF>(n2), w);
+      float2* tp = T + ci * TS + n2;
+      cfor<0, N1>([&](auto K1) {
+        constexpr int k1 = decltype(K1)::value;
+        const cpx v = k1 == 0 ? a[0] : cmul(a[k1], w[k1]);
+        tp[k1 * N2] = make_float2(v.re, v.im);
+      });
+    });
+    __syncthreads();
+    // 2. rows k1 = q + 4 t of node ci
+    cfor<0, N1 / 4>([&](auto TT) {
+      const int k1 = q + 4 * decltype(TT)::value;
+      const float2* tp = T + ci * TS + k1 * N2;
+      cpx a[N2];
+      cfor<0, N2>([&](auto M2) {
+        const float2 v = tp[decltype(M2)::value];
+        a[decltype(M2)::value] = {v.x, v.y};
+      });
+      fft_reg<N2, +1>(a);
+      float gv[N2];
+      cfor<0, N2>([&](auto K2) { gv[decltype(K2)::value] = a[decltype(K2)::value].re * a[decltype(K2)::value].im; });
+      cpx X2[H2];
+      rfft2_fwd<N2>(gv, X2);
+      cpx w[H2];
+      cpowers<H2>(cconj(tw_root<NF>(k1)), w);
+      float2* t2 = A + ci * T2S + k1;
+      cfor<0, H2>([&](auto M2) {
+        constexpr int m2 = decltype(M2)::value;
+        const cpx v = m2 == 0 ? X2[0] : cmul(X2[m2], w[m2]);
+        t2[m2 * N1] = make_float2(v.re, v.im);
+      });
+    });
+    __syncthreads();
+    // 3. columns m2 of pair pp (node column pp, mirror column 8 + pp); lanes
+    // with m2 = 0 also take the column N2 / 2
+    const int pp = lane & 7, cm = lane >> 3;
+    constexpr float scale = float(G::NP) / (8.0f * float(NF));
+    auto column = [&](int m2) {
+      cpx bn[N1], bm[N1];
+      const float2* t2n = A + pp * T2S + m2 * N1;
+      const float2* t2m = A + (8 + pp) * T2S + m2 * N1;
+      cfor<0, N1>([&](auto K1) {
+        constexpr int k1 = decltype(K1)::value;
+        const float2 u = t2n[k1], v = t2m[k1];
+        bn[k1] = {u.x, u.y};
+        bm[k1] = {v.x, v.y};
+      });
+      fft_reg<N1, -1>(bn);
+      fft_reg<N1, -1>(bm);
+      float* es = eo + pp * G::NMP2;          // sum of the mirror nodes
+      float* ed = eo + (8 + pp) * G::NMP2;    // difference
+      // moment m from X = sum_k g exp(-i m p_k): cos part Re X, sin part -Im X
+      auto emit = [&](int m, cpx xn, cpx xm) {
+        es[2 * m] = (xn.re + xm.re) * scale;
+        ed[2 * m] = (xn.re - xm.re) * scale;
+        if (m > 0) {
+          es[2 * m + 1] = -(xn.im + xm.im) * scale;
+          ed[2 * m + 1] = -(xn.im - xm.im) * scale;
+        }
+      };
+      // m = N2 m1 + m2 <= L from output m1; m = N2 a - m2 <= L (0 < m2 < N2 / 2)
+      // from output N1 - a, conjugated (the transform of a real g)
+      cfor<0, N1>([&](auto M1) {
+        constexpr int m1 = decltype(M1)::value;
+        if constexpr (N2 * m1 <= L) {
+          const int m = N2 * m1 + m2;
+          if (m <= L) emit(m, bn[m1], bm[m1]);
+        }
+      });
+      if (m2 != 0 && 2 * m2 != N2) {
+        cfor<1, N1>([&](auto AA) {
+          constexpr int aa = decltype(AA)::value;
+          if constexpr (N2 * aa - N2 / 2 < L + 1) {
+            const int m = N2 * aa - m2;
+            if (m <= L) emit(m, cconj(bn[N1 - aa]), cconj(bm[N1 - aa]));
+          }
+        });
+      }
+    };
+    if (cm < N2 / 2) column(cm);
+    if (cm == 0) column(N2 / 2);
+  }
 };
 
 // x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
@@ -440,7 +629,7 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
   using G = WGeo<L>;
   constexpr int K = G::K, NTH = G::NTH, NXK = G::NXK, NXKP = G::NXKP;
   int slot[NXKP];
-  lfor<0, NXKP / 4>([&](auto K4) {
+  cfor<0, NXKP / 4>([&](auto K4) {
     constexpr int k4 = decltype(K4)::value;
     const int4 v = reinterpret_cast<const int4*>(xmap + tid * NXKP)[k4];
     slot[4 * k4] = v.x;
@@ -449,7 +638,7 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
     slot[4 * k4 + 3] = v.w;
   });
   float v1[NXK], v2[NXK];
-  lfor<0, NXK>([&](auto KK) {
+  cfor<0, NXK>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     const int e = tid + NTH * k;
     if (NTH * k + NTH - 1 < K || e < K) {
@@ -460,7 +649,7 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
   if constexpr (WGT) {
     // per-degree weights of this product (Sec. 3.1), gathered per coefficient
     const int64_t row = weight_row(wt, P) * (L + 1);
-    lfor<0, NXK>([&](auto KK) {
+    cfor<0, NXK>([&](auto KK) {
       constexpr int k = decltype(KK)::value;
       const int e = tid + NTH * k;
       if (NTH * k + NTH - 1 < K || e < K) {
@@ -470,12 +659,12 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
       }
     });
   }
-  lfor<0, G::XQ / NTH>([&](auto Z) {
+  cfor<0, G::XQ / NTH>([&](auto Z) {
     reinterpret_cast<float4*>(xs)[tid + NTH * decltype(Z)::value] = make_float4(0.f, 0.f, 0.f, 0.f);
   });
   if (tid < G::XQ % NTH) reinterpret_cast<float4*>(xs)[tid + NTH * (G::XQ / NTH)] = make_float4(0.f, 0.f, 0.f, 0.f);
   __syncthreads();
-  lfor<0, NXK>([&](auto KK) {
+  cfor<0, NXK>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     if (NTH * k + NTH - 1 < K || tid + NTH * k < K) {
       xs[slot[k]] = v1[k];
@@ -523,9 +712,10 @@ __device__ __forceinline__ const int* row_er_table() {
 }
 
 // L in {16, 32}: one wave per product; theta analysis accumulates in
-// registers after every pass.
-template <int L, typename T1, typename T2, bool WGT>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_full_wave(
+// registers after every pass.  FFT: the phi transforms by radix-2 FFTs
+// (phi_fft) instead of the direct-DFT contractions on the matrix cores.
+template <int L, typename T1, typename T2, bool WGT, bool FFT>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3))) void k_full_wave(
     const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
     DegWeights wt) {
   using G = WGeo<L>;
@@ -533,9 +723,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   constexpr int NJ = G::NJ, NP = G::NP;
   constexpr int NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW, NIT = G::NIT;
   // the moments first: their reads then carry small immediate offsets
-  __shared__ __align__(16) float lds[G::EOP + G::XQ * 4];
+  constexpr int FFTF = FFT ? 2 * (FGeo<L>::AC + FGeo<L>::TC) : 0;  // the FFT variant's spectra and T
+  __shared__ __align__(16) float lds[G::EOP + G::XQ * 4 + FFTF];
   float* const eo = lds;
   float* const xs = lds + G::EOP;
+  float2* const fa = reinterpret_cast<float2*>(lds + G::EOP + G::XQ * 4);
+  float2* const ft = fa + (FFT ? FGeo<L>::AC : 0);
 
   const int lane = threadIdx.x;
   if (int64_t(blockIdx.x) >= n) return;  // whole-wave exit (one product per workgroup)
@@ -548,7 +741,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   // m > 0 numbered q = lane + 64 it
   float y0 = 0.0f, yc[NIT], ys[NIT];
   const int wr0 = (lane * (lane + 1) / 2) * 4;
-  lfor<0, NIT>([&](auto IT) {
+  cfor<0, NIT>([&](auto IT) {
     yc[decltype(IT)::value] = 0.0f;
     ys[decltype(IT)::value] = 0.0f;
   });
@@ -564,15 +757,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
     const WaveCtx<L> w(lnp, reinterpret_cast<const float4*>(xs), t);
     f4 o[1][4];
     float zz;
-    w.pass(pu, o, zz);
+    w.template pass<FFT>(pu, o, zz, fa);
     // this pass's row offsets (loaded here, not held across the passes:
     // that would keep NIT more registers live through the contractions)
     int er[NIT];
-    lfor<0, NIT>([&](auto IT) {
+    cfor<0, NIT>([&](auto IT) {
       constexpr int it = decltype(IT)::value;
       er[it] = (lane + 64 * it < NROW) ? er_tab[64 * it + lane] : 0;
     });
-    w.store_moments(eo, o, zz);
+    if constexpr (FFT) {
+      __syncthreads();  // the spectra of all 16 column nodes are in LDS
+      w.phi_fft(eo, fa, ft);
+    } else {
+      w.store_moments(eo, o, zz);
+    }
     __syncthreads();
 
     // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
@@ -581,18 +779,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
       const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
       const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
       const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-      lfor<0, 8>([&](auto JJ) {
+      cfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
         y0 = fmaf(wv[jj], eo[(lnp & 1) * 8 * NMP2 + jj * NMP2], y0);  // row tri(lane, 0)
       });
     }
-    lfor<0, NIT>([&](auto IT) {
+    cfor<0, NIT>([&](auto IT) {
       constexpr int it = decltype(IT)::value;
       if (lane + 64 * it < NROW) {
         const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
         const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-        lfor<0, 8>([&](auto JJ) {
+        cfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
           const f2 cs = *reinterpret_cast<const f2*>(eo + er[it] + jj * NMP2);
           yc[it] = fmaf(wv[jj], cs.x, yc[it]);
@@ -627,7 +825,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3))) void k_
   }
   int ln = lane;
   asm volatile("" : "+v"(ln));
-  lfor<0, NIT>([&](auto IT) {
+  cfor<0, NIT>([&](auto IT) {
     constexpr int it = decltype(IT)::value;
     const int q = ln + 64 * it;
     if (q < NROW) {
@@ -690,13 +888,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   // the m > 0 rows q = tid + 256 it; weights WP[it][tid][j - 1], j = 1..L
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, (NIT + 1) * NTH * L);
   auto row_sum = [&](int it, int er, float& ac, float& as, bool with_sin) {
-    lfor<0, PASSES>([&](auto PP) {
+    cfor<0, PASSES>([&](auto PP) {
       constexpr int pp = decltype(PP)::value;  // pass: pairs 8 pp + 1 .. 8 pp + 8
       const float* eop = (pp % 2 == 0 ? eo_even : eo_odd) + (pp / 2) * EOP;
       const float4 w0 = tload4_s(WPr, tid * L * 4 + pp * 32, it * NTH * L * 4);
       const float4 w1 = tload4_s(WPr, tid * L * 4 + pp * 32 + 16, it * NTH * L * 4);
       const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-      lfor<0, 8>([&](auto JJ) {
+      cfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
         const f2 cs = *reinterpret_cast<const f2*>(eop + er + jj * NMP2);
         ac = fmaf(wv[jj], cs.x, ac);
@@ -739,6 +937,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
 template <int L, typename T1, typename T2, bool WGT>
 hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t,
                              const DegWeights& wt, hipStream_t s) {
+  // the radix-FFT phi transforms where the plan asks for them and a
+  // one-wave kernel exists (L = 16, 32)
+  const bool fft = t.phi_fft != 0 && WGeo<L>::NW == 1;
   using G = WGeo<L>;
   // at most 2^30 workgroups per launch
   for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
@@ -748,9 +949,13 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
     float* yy = y + size_t(p0) * G::K;
     DegWeights w = wt;
     w.pbase += p0;  // the chunk's products start at p0
-    if constexpr (G::NW == 1)
-      hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t, w);
-    else
+    if constexpr (G::NW == 1) {
+      if (fft)
+        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, true>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t, w);
+      else
+        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, false>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t,
+                           w);
+    } else
       hipLaunchKernelGGL((k_full_wave4<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t, w);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

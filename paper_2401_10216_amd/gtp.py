@@ -16,7 +16,7 @@ LIB_PATH = os.path.join(PKG, "libgtp.so")
 
 GTP_OK, GTP_ERR_INVALID_ARG, GTP_ERR_UNSUPPORTED, GTP_ERR_NO_DEVICE, GTP_ERR_HIP, GTP_ERR_ALLOC = range(6)
 GTP_F32, GTP_BF16 = 0, 1
-GTP_CONV_AUTO, GTP_CONV_DIRECT, GTP_CONV_FFT = 0, 1, 2
+GTP_CONV_AUTO, GTP_CONV_DIRECT, GTP_CONV_FFT, GTP_CONV_DFT = 0, 1, 2, 3
 GTP_PLAN_HOST_ONLY = 16
 GTP_FORCE_GENERIC = 32  # internal: use the workgroup-per-product kernel
 GTP_SELF_STEPWISE, GTP_SELF_FUSED = 0, 1

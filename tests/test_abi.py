@@ -126,7 +126,7 @@ def test_plan_create_rejects_bad_degrees(L):
     for args in [(-1, 2, 2), (2, -1, 2), (2, 2, -1), (65, 2, 2), (2, 65, 2), (2, 2, 65)]:
         assert L.gtp_plan_create(ctypes.byref(h), *args, gtp.GTP_PLAN_HOST_ONLY) == gtp.GTP_ERR_INVALID_ARG
     assert L.gtp_plan_create(None, 1, 1, 1, gtp.GTP_PLAN_HOST_ONLY) == gtp.GTP_ERR_INVALID_ARG
-    assert L.gtp_plan_create(ctypes.byref(h), 1, 1, 1, 3) == gtp.GTP_ERR_INVALID_ARG  # DIRECT|FFT
+    assert L.gtp_plan_create(ctypes.byref(h), 1, 1, 1, 1 << 5 | 1 << 6) == gtp.GTP_ERR_INVALID_ARG
     assert L.gtp_plan_create(ctypes.byref(h), 1, 1, 1, 1 << 10) == gtp.GTP_ERR_INVALID_ARG
     assert L.gtp_plan_destroy(None) == gtp.GTP_OK
 

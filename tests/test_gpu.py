@@ -824,3 +824,90 @@ def test_plan_device_allocation_failure(monkeypatch):
     a = rng.standard_normal((100, 1, 49)).astype(np.float32)
     y = run_full(gtp.Plan(6, 6, 6), a, a)
     assert O.max_rel_err(y, O.gtp(a.astype(np.float64), a.astype(np.float64), 6, 6, 6)) <= TOL
+
+
+# ------------------------------------------------------------------ radix-FFT phi transforms (GTP_CONV_FFT)
+
+@pytest.mark.parametrize("L,n", [(16, 64 * 5 + 3), (32, 200)])
+def test_fft_phi_transforms(L, n):
+    """The matrix-core kernel with its phi transforms by radix-2 FFT against
+    the oracle (every product of a ragged batch at L = 16, a sample at 32),
+    and against the direct-DFT kernel on the same inputs."""
+    rng = np.random.default_rng(900 + L)
+    a = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    plan = gtp.Plan(L, L, L, gtp.GTP_CONV_FFT)
+    assert plan.info()["conv"] == gtp.GTP_CONV_FFT
+    _say(f"fft L={L} n={n}")
+    y = run_full(plan, a, b)
+    idx = np.arange(n) if L <= 16 else np.r_[0:8, n - 8:n, 64:72]
+    ref = O.gtp_grid(a[idx, 0].astype(np.float64), b[idx, 0].astype(np.float64), L, L, L)
+    err = O.max_rel_err(y[idx, 0], ref)
+    yd = run_full(gtp.Plan(L, L, L, gtp.GTP_CONV_DFT), a, b)
+    errd = O.max_rel_err(y, yd)
+    _say(f"  vs oracle {err:.3e}, vs DFT kernel {errd:.3e}")
+    assert err <= TOL and errd <= TOL
+
+
+@pytest.mark.parametrize("L", [16, 32])
+def test_fft_phi_transforms_bf16_weighted_backward(L):
+    """The FFT variant with bf16 inputs, per-degree weights and in the
+    backward pass (all through the same kernel template)."""
+    n = 130
+    rng = np.random.default_rng(950 + L)
+    x = rng.standard_normal((3, n, 1, O.nsh(L))).astype(np.float32)
+    plan = gtp.Plan(L, L, L, gtp.GTP_CONV_FFT)
+    idx = np.r_[0:4, n - 4:n]
+    # bf16 inputs
+    bits1, v1 = inputs.round_to_bf16(x[0])
+    bits2, v2 = inputs.round_to_bf16(x[1])
+    t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+    t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_full(plan, t1, t2)
+    torch.cuda.synchronize()
+    ref = O.gtp_grid(v1[idx, 0].astype(np.float64), v2[idx, 0].astype(np.float64), L, L, L)
+    assert O.max_rel_err(y.cpu().numpy()[idx, 0].astype(np.float64), ref) <= TOL
+    # per-degree weights
+    w = [rng.standard_normal((1, L + 1)).astype(np.float32) for _ in range(3)]
+    yw = gtp.gtp_full_weighted(plan, dev(x[0]), dev(x[1]), *[dev(v) for v in w])
+    torch.cuda.synchronize()
+    refw = O.gtp_weighted(x[0][idx, 0].astype(np.float64), x[1][idx, 0].astype(np.float64), w[0][0], w[1][0], w[2][0],
+                          L, L, L)
+    assert O.max_rel_err(yw.cpu().numpy()[idx, 0].astype(np.float64), refw) <= TOL
+    # backward
+    dx1, dx2 = gtp.gtp_full_backward(plan, dev(x[0]), dev(x[1]), dev(x[2]))
+    torch.cuda.synchronize()
+    r1, r2 = O.gtp_vjp(x[0][idx, 0].astype(np.float64), x[1][idx, 0].astype(np.float64),
+                       x[2][idx, 0].astype(np.float64), L, L, L)
+    assert O.max_rel_err(dx1.cpu().numpy()[idx, 0].astype(np.float64), r1) <= TOL
+    assert O.max_rel_err(dx2.cpu().numpy()[idx, 0].astype(np.float64), r2) <= TOL
+
+
+@pytest.mark.parametrize("L", [16, 32])
+def test_fft_sweep_sampled(L):
+    """The FFT variant at the degree sweep's full size and launch shape
+    ([2048, 128, K], 262144 products): a seeded sample, the last products
+    included, against the oracle."""
+    x1, x2 = inputs.sweep_inputs(L)
+    n = x1.shape[0] * x1.shape[1]
+    _say(f"fft sweep L={L}")
+    y = gtp.gtp_full(gtp.Plan(L, L, L, gtp.GTP_CONV_FFT), dev(x1), dev(x2))
+    torch.cuda.synchronize()
+    idx = np.unique(np.r_[inputs.sample_indices(4, n, 256), n - 8:n])
+    yf = y.view(n, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    ref = O.gtp_grid(x1.reshape(n, -1)[idx].astype(np.float64), x2.reshape(n, -1)[idx].astype(np.float64), L, L, L)
+    err = O.max_rel_err(yf, ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL
+
+
+def test_fft_request_without_radix_kernel_runs_dft():
+    """GTP_CONV_FFT where no radix kernel exists (small or unequal degrees)
+    reports and runs the direct-DFT forms."""
+    for degs in ((6, 6, 6), (16, 16, 12), (64, 64, 64)):
+        plan = gtp.Plan(*degs, gtp.GTP_CONV_FFT)
+        assert plan.info()["conv"] == gtp.GTP_CONV_DFT, degs
+    rng = np.random.default_rng(5)
+    a = rng.standard_normal((70, 1, 49)).astype(np.float32)
+    y = run_full(gtp.Plan(6, 6, 6, gtp.GTP_CONV_FFT), a, a)
+    assert O.max_rel_err(y, O.gtp(a.astype(np.float64), a.astype(np.float64), 6, 6, 6)) <= TOL
