@@ -34,10 +34,33 @@ PEAK_HBM_GBS = 8000.0     # MI355X HBM3E
 
 # Flops per (b,c)-product of the paper's Fourier method counted for an
 # FFT-based real-form convolution (sparse change of basis, min(direct, FFT)
-# convolution, projection to Lout): the reference figures the 50 % targets
-# were set with.
+# convolution, projection to Lout): the figures the 50 % targets were set
+# with, reported as context only (the kernels run a formulation with fewer
+# flops, whose own count sets the roofline).
 SURVEY_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
 SURVEY_FLOPS_MANYBODY = 2200
+
+# Flops per product of the thread-per-product kernel at equal degrees
+# L1 = L2 = Lout = L (fp32 inputs) as it runs: 2 FMA + MUL + ADD per lane (one
+# lane is one product).  L = 4, 6, 8: the SQ_INSTS_VALU_FMA_F32 / _MUL_F32 /
+# _ADD_F32 counters per wave; the others: the same count read off the
+# kernel's instruction stream, which is loop-free per lane and equals the
+# counters where both exist.  Below the structural count of the formulation
+# (formulation_flops) because the compiler folds twiddles of +-1 and constant
+# products.
+SMALL_KERNEL_FLOPS = {1: 80, 2: 422, 3: 1224, 4: 2648, 5: 4232, 6: 7446, 7: 11392, 8: 17652}
+# the stepwise many-body chain L = 2, nu = 3, Lout = 3 (one kernel), counted the same way
+STEPWISE_FLOPS_L2_NU3_LOUT3 = 829
+
+
+def kernel_flops(L1: int, L2: int, Lout: int) -> int:
+    """Algorithmic flops per product of the kernel that runs (L1, L2, Lout):
+    the executed count of the thread-per-product kernel for equal degrees up
+    to 8, else the formulation's structural count (which leaves out the
+    matrix cores' padding rows and columns)."""
+    if L1 == L2 == Lout and L1 in SMALL_KERNEL_FLOPS:
+        return SMALL_KERNEL_FLOPS[L1]
+    return formulation_flops(L1, L2, Lout)
 
 
 def formulation_flops(L1: int, L2: int, Lout: int) -> int:
@@ -68,6 +91,48 @@ def formulation_flops(L1: int, L2: int, Lout: int) -> int:
     f += 2 * (2 * Le + 1) * pairs
     f += 2 * (Le + 1) ** 2 * pairs + 4 * (Le + 1)
     return int(round(f))
+
+
+def _fft_flops(N: int, nonzero_in: int = -1) -> int:
+    """Flops of the in-register radix-2 complex DFT of length N (gtp_fft.hpp):
+    4 per butterfly (a complex add and subtract) plus the twiddle products
+    (6 for a general one, 4 for an odd multiple of an eighth turn, none for a
+    quarter turn)."""
+    f, length = 0, 2
+    while length <= N:
+        half = length // 2
+        for j in range(half):
+            if j == 0 or 4 * j == length or 4 * j == 3 * length:
+                tw = 0
+            elif (8 * j) % length == 0:
+                tw = 4
+            else:
+                tw = 6
+            f += (N // length) * (4 + tw)
+        length *= 2
+    return f
+
+
+def fft_variant_flops(L: int) -> int:
+    """Flops per product of the matrix-core kernel's radix-FFT variant
+    (L1 = L2 = Lout = L in {16, 32}): the theta stages as in the DFT form, and
+    per pass of 16 theta nodes the three FFT stages of phi_fft -- 16 N2
+    column DFTs of length N1 with their twiddle powers and products, 16 N1 row
+    DFTs of length N2 with the sample products and the real forward transform
+    (a length-N2/2 DFT and N2/2 + 1 recombinations), 8 (N2/2 + 1) pairs of
+    forward column DFTs of length N1."""
+    NF = 64 if L <= 16 else 128
+    N1 = 8
+    N2 = NF // N1
+    U = 2 * L
+    pairs = U / 2
+    K = (L + 1) ** 2
+    theta = 2 * (2 * K * pairs + 2 * (2 * L + 1) * pairs + 4 * (L + 1)) + 2 * (L + 1) ** 2 * pairs + 4 * (L + 1)
+    col = _fft_flops(N1) + 6 * (N1 - 2) + 6 * (N1 - 1)
+    row = _fft_flops(N2) + N2 + _fft_flops(N2 // 2) + (N2 // 2 + 1) * 10 + 6 * (N2 // 2 - 1) + 6 * (N2 // 2)
+    fwd = 2 * _fft_flops(N1) + 4 * 2 * (L + 1) / (N2 // 2 + 1)
+    per_pass = 16 * N2 * col + 16 * N1 * row + 8 * (N2 // 2 + 1) * fwd
+    return int(round(theta + (L // 8) * per_pass))
 
 
 def escn_flops(L: int, C: int) -> float:
@@ -230,7 +295,7 @@ def make_workload(args, torch, gtp, inputs):
             # bytes: x1 and y, h, and the edge vector shared by C channels
             return step, B * C, desc, (escn_flops(L, C), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
                 oracle_sample, 2
-        return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
+        return step, B * C, desc, (kernel_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2
     if (args.backward or args.weighted) and w not in ("edge", "tiny", "sweep", "highdeg"):
         raise SystemExit("--backward / --weighted apply to the pair workloads (edge, tiny, sweep, highdeg)")
@@ -242,6 +307,14 @@ def make_workload(args, torch, gtp, inputs):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1
             x1, x2 = inputs.pair_inputs(1, B, C, L, L)
+        elif w == "sweep" and args.degrees:
+            # unequal degrees: the sweep's batch shape, iid N(0,1) of each degree
+            L1d, L2d, Lod = (int(v) for v in args.degrees.split(","))
+            B, C, idx_cfg = 2048, 128, 4
+            rng = inputs.rng_for(4, 10 * (L1d + 100 * L2d + 10000 * Lod))
+            x1 = inputs.normal(rng, (B, C, nsh(L1d)))
+            x2 = inputs.normal(rng, (B, C, nsh(L2d)))
+            L = L1d
         elif w == "sweep":
             L = args.L
             B, C, idx_cfg = 2048, 128, 4
@@ -259,16 +332,17 @@ def make_workload(args, torch, gtp, inputs):
             in_bytes = 4
         flags = {"auto": 0, "direct": gtp.GTP_CONV_DIRECT, "generic": gtp.GTP_FORCE_GENERIC,
                  "fft": gtp.GTP_CONV_FFT, "dft": gtp.GTP_CONV_DFT}[args.conv]
-        plan = gtp.Plan(L, L, L, flags)
+        L1, L2, Lo = (L1d, L2d, Lod) if (w == "sweep" and args.degrees) else (L, L, L)
+        plan = gtp.Plan(L1, L2, Lo, flags)
         if args.products:
             # crossover runs: the first N products, as [N, 1, K]
             C = 1
             B = min(args.products, t1.shape[0] * t1.shape[1])
-            t1 = t1.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
-            t2 = t2.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
-            x1 = x1.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
-            x2 = x2.reshape(-1, nsh(L))[:B].reshape(B, 1, -1)
-        y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
+            t1 = t1.reshape(-1, nsh(L1))[:B].reshape(B, 1, -1)
+            t2 = t2.reshape(-1, nsh(L2))[:B].reshape(B, 1, -1)
+            x1 = x1.reshape(-1, nsh(L1))[:B].reshape(B, 1, -1)
+            x2 = x2.reshape(-1, nsh(L2))[:B].reshape(B, 1, -1)
+        y = torch.empty((B, C, nsh(Lo)), dtype=torch.float32, device=dev)
         step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, idx_cfg)
 
         def oracle_sample(O, idx):
@@ -276,12 +350,16 @@ def make_workload(args, torch, gtp, inputs):
             b = x2.reshape(B * C, -1)[idx].astype("float64")
             return oracle_of(O, idx, a, b), result
 
-        desc = {"workload": f"{w}: B={B} x C={C}, L1=L2=Lout={L}, iid N(0,1)" + (" rounded to bf16" if w == "highdeg" else ""),
-                "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "bf16" if w == "highdeg" else "f32"}
+        degs = f"L1=L2=Lout={L}" if (L1, L2) == (L, L) and Lo == L else f"L1={L1}, L2={L2}, Lout={Lo}"
+        desc = {"workload": f"{w}: B={B} x C={C}, {degs}, iid N(0,1)" + (" rounded to bf16" if w == "highdeg" else ""),
+                "B": B, "C": C, "L1": L1, "L2": L2, "Lout": Lo, "in_dtype": "bf16" if w == "highdeg" else "f32"}
         if args.conv != "auto":
             desc["conv"] = args.conv
-        return step, B * C, desc, (formulation_flops(L, L, L), SURVEY_FLOPS.get(L)), \
-            in_bytes * 2 * nsh(L) + 4 * nsh(L), oracle_sample, idx_cfg
+        fl = kernel_flops(L1, L2, Lo)
+        if args.conv == "fft" and L1 == L2 == Lo and L in (16, 32):
+            fl = fft_variant_flops(L)
+        return step, B * C, desc, (fl, SURVEY_FLOPS.get(L) if (L1, L2, Lo) == (L, L, L) else None), \
+            in_bytes * (nsh(L1) + nsh(L2)) + 4 * nsh(Lo), oracle_sample, idx_cfg
     if w == "manybody":
         N, C, L, nu, Lout = 1728, 256, 2, 3, 3
         x = inputs.manybody_inputs(N, C, L)
@@ -298,8 +376,8 @@ def make_workload(args, torch, gtp, inputs):
 
         desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
-        return step, N * C, desc, (formulation_flops(L, L, Lout) + formulation_flops(Lout, L, Lout),
-                                   SURVEY_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), oracle_sample, 3
+        return step, N * C, desc, (STEPWISE_FLOPS_L2_NU3_LOUT3, SURVEY_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), \
+            oracle_sample, 3
     if w == "mix":
         cfg = inputs.WORKLOADS["mix"]
         B, C, L = cfg["B"], cfg["C"], cfg["L1"]
@@ -324,29 +402,25 @@ def make_workload(args, torch, gtp, inputs):
                             "B=8192, C1=C2=Co=32, L1=L2=Lout=6, x~N(0,1), W~N(0,1/C^2)",
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
         # per pair product: the product itself and 2 Co K flops of the mix; bytes: x1, x2, y over C^2 pairs
-        return step, B * C * C, desc, (formulation_flops(L, L, L) + 2 * C * nsh(L), None), \
+        return step, B * C * C, desc, (kernel_flops(L, L, L) + 2 * C * nsh(L), None), \
             4.0 * nsh(L) * 3 * C / (C * C), oracle_sample, 6
-    if w == "copy":
-        # plain device copy of a known size: calibrates the HBM byte counters
-        nbytes = 1 << 30
-        src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
-        dst = torch.empty_like(src)
-
-        def step():
-            dst.copy_(src)
-
-        desc = {"workload": "copy: 1 GiB fp32 device-to-device copy (HBM counter calibration)", "bytes": nbytes}
-        return step, nbytes, desc, None, 2, None, 0
     raise SystemExit(f"unknown workload {w}")
 
 
 def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
-    """Time the oracle on a seeded subsample sized to roughly budget_s seconds."""
+    """Time the oracle on a seeded subsample sized to roughly budget_s seconds,
+    on every host core this process may run on (its CPU affinity set): the
+    oracle's BLAS thread pool is sized to that count."""
     try:
-        from threadpoolctl import threadpool_info
+        cpus = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cpus = os.cpu_count() or 1
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        limits = threadpool_limits(limits=cpus)
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
-        threads = os.cpu_count() or 1
+        limits, threads = None, cpus
     n = min(1024, total)
     while True:
         idx = inputs.sample_indices(idx_cfg, total, n)
@@ -359,6 +433,8 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
         if dt >= 0.6 * budget_s or n >= total:
             break
         n = int(min(total, max(2 * n, n * budget_s / max(dt, 1e-3))))
+    if limits is not None:
+        limits.restore_original_limits()
     # rows(idx) gathers the device results of exactly these products (each
     # index < total, checked on the host first)
     assert idx.size and 0 <= idx.min() and idx.max() < total
@@ -371,6 +447,7 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     except OSError:
         pass
     out = {"value": done / dt, "unit": "products/s", "cores": int(threads), "kind": "oracle", "host": host,
+           "host_cpus_in_affinity": cpus, "nproc": os.cpu_count(),
            "sample": f"{done} seeded products of the same workload, fp64 numpy oracle (dense real-Gaunt contraction), "
                      f"{dt:.2f} s", "max_rel_err_gpu_vs_oracle": err, "one_core": None}
     # the same oracle on one core, on a smaller seeded subsample (about a
@@ -390,6 +467,40 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
     out["one_core"] = {"value": done1 / dt1, "unit": "products/s", "cores": 1,
                        "sample": f"{done1} seeded products, {dt1:.2f} s"}
     return out
+
+
+def stream_roofs(args, torch, gtp):
+    """The HBM roof as the chip reaches it: 1 GiB read-only, write-only and
+    copy sweeps by the library's streaming probes (16-byte accesses,
+    non-temporal stores), and torch's device copy, each timed with HIP events
+    on the launch stream.  Also the calibration workload of the FETCH_SIZE /
+    WRITE_SIZE counters (k_probe_copy moves a known 1 GiB each way)."""
+    nbytes = 1 << 30
+    dev = torch.device("cuda:0")
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    out = {"workload": "copy: HBM streaming roofs on 1 GiB buffers", "bytes": nbytes}
+    probes = [("read", lambda: gtp.gtp_stream_probe(0, src, sink), nbytes),
+              ("write", lambda: gtp.gtp_stream_probe(1, None, dst), nbytes),
+              ("copy", lambda: gtp.gtp_stream_probe(2, src, dst), 2 * nbytes),
+              ("torch_copy", lambda: dst.copy_(src), 2 * nbytes)]
+    for name, fn, moved in probes:
+        for _ in range(args.warmup):
+            fn()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.steps
+        out[name] = {"ms": round(ms, 4), "GBps": round(moved / (ms * 1e-3) / 1e9, 1),
+                     "frac_of_8TBps": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -414,6 +525,8 @@ def main():
     ap.add_argument("--escn", action="store_true",
                     help="edge workload through gtp_conv_escn (the product with the SH filter taken in each edge's "
                          "rotated frame from x1, r, h) instead of gtp_full with a prebuilt filter")
+    ap.add_argument("--degrees", default="",
+                    help="L1,L2,Lout of the sweep workload (its batch shape) instead of --L for all three")
     ap.add_argument("--products", type=int, default=0,
                     help="use only the first N products of a pair workload (crossover runs of slow variants)")
     args = ap.parse_args()
@@ -428,6 +541,9 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     gtp.lib()  # fails loudly if the HIP library is not built
+    if args.workload == "copy":
+        stream_roofs(args, torch, gtp)
+        return
     step, products, desc, alg_flops, alg_bytes, oracle_sample, idx_cfg = make_workload(args, torch, gtp, inputs)
 
     for _ in range(args.warmup):
@@ -467,9 +583,7 @@ def main():
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         comp = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "alg_flops_per_product": alg_flops,
-                "survey_flops_per_product": survey_flops,
-                "frac_at_survey_flops": (round(survey_flops * products / (kernel_ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4)
-                                         if survey_flops else None)}
+                "survey_flops_per_product": survey_flops}
         hbm_gbs = alg_bytes * products / (kernel_ms * 1e-3) / 1e9
         hbm = {"bound": "hbm", "achieved": round(hbm_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                "frac": round(hbm_gbs / PEAK_HBM_GBS, 4), "alg_bytes_per_product": alg_bytes}
@@ -481,10 +595,6 @@ def main():
             roof = dict(comp, hbm=hbm)
         roof.update({"traffic": tb, "kernel": kname, "kernel_ms": round(kernel_ms, 5)})
 
-    if args.workload == "copy":
-        print(json.dumps({"workload": "copy", "bytes_per_step": products, "ms_per_step": kernel_ms,
-                          "GBps_read_plus_write": 2 * products / (kernel_ms * 1e-3) / 1e9}), flush=True)
-        return
     cpu = None
     if not args.no_cpu_baseline:
         from oracle import gtp_oracle as O

@@ -170,6 +170,30 @@ gtp_status gtp_full_weighted(gtp_plan p, const void *x1, const void *x2, gtp_dty
                              const float *w2, const float *wout, int per_channel, int64_t B, int64_t C, float *y,
                              void *stream);
 
+/* Backward pass of gtp_full_weighted, weight gradients included (Sec. 3.1,
+ * eq. tp-eq-mul-weight; the learnable weights of the feature-interaction
+ * layers).  With y = wout GTP(w1 x1, w2 x2) and a loss gradient dy, writes
+ *   dx1   = w1 P_L1 GTP(wout dy, w2 x2)                 [B, C, (L1+1)^2],
+ *   dx2   = w2 P_L2 GTP(wout dy, w1 x1)                 [B, C, (L2+1)^2],
+ *   dw1[r, l1] = sum over the products of weight row r of
+ *                <x1, P_L1 GTP(wout dy, w2 x2)> on degree l1     [R, L1+1],
+ *   dw2 likewise                                                 [R, L2+1],
+ *   dwout[r, l] = sum over row r of <dy, GTP(w1 x1, w2 x2)> on degree l
+ *                                                                [R, Lout+1],
+ * R = C with per_channel = 1 (row c holds channel c's products), else 1.
+ * Weights as in gtp_full_weighted (NULL = ones; the gradient is still that
+ * of a weight of ones).  Any of dx1, dx2, dw1, dw2, dwout may be NULL (not
+ * computed); the rest are written, not accumulated, and must not overlap an
+ * input or each other.  The sums over the products are deterministic (fixed
+ * order, no atomics).  Uses a stream-ordered workspace (hipMallocAsync) for
+ * the partial sums and the products that are not outputs.  B*C == 0 writes
+ * zero weight gradients.  GTP_ERR_UNSUPPORTED for GTP_CONV_DIRECT plans and
+ * more than 65535 weight rows. */
+gtp_status gtp_full_weighted_backward(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype,
+                                      const float *w1, const float *w2, const float *wout, int per_channel,
+                                      const float *dy, int64_t B, int64_t C, float *dx1, float *dx2, float *dw1,
+                                      float *dw2, float *dwout, void *stream);
+
 /* Backward pass (vector-Jacobian product) of gtp_full: given the gradient dy
  * of a scalar loss with respect to y = gtp_full(x1, x2), the gradients
  *   dx1[b,c,i] = sum_{j,k} G_{i j k} x2[b,c,j] dy[b,c,k]   (i over degrees <= L1),
@@ -233,6 +257,13 @@ gtp_status gtp_selfproduct(int L, int nu, int Lout, unsigned mode, const void *x
  * for h = 1 (then C must be 1); out: [B, C, (L+1)^2] fp32.  0 <= L <= 64. */
 gtp_status gtp_sh_filter(int L, const float *r, const float *h, int64_t B, int64_t C, float *out,
                          void *stream);
+
+/* HBM streaming probe (measurement aid: the roof the HBM-bound kernels are
+ * read against).  mode 0: read nbytes of src (dst: a device float written
+ * only if the data holds a NaN); 1: write nbytes to dst (non-temporal
+ * stores); 2: copy nbytes from src to dst (non-overlapping).  Device
+ * pointers 16-byte aligned, nbytes >= 0 a multiple of 16. */
+gtp_status gtp_stream_probe(int mode, const void *src, void *dst, int64_t nbytes, void *stream);
 
 /* Number of floats of one per-product public grid: which = 1 or 2 gives the
  * input grids (2 * (2L+1)^2), which = 3 the product grid (2 * (2U+1)^2).

@@ -290,6 +290,43 @@ def gtp_weighted(x1, x2, w1, w2, wo, L1: int, L2: int, Lout: int, mode: str = "a
     raise ValueError(mode)
 
 
+def gtp_weighted_vjp(x1, x2, w1, w2, wo, dy, L1: int, L2: int, Lout: int):
+    """Gradients of s = sum_k dy[k] y[k] with y = gtp_weighted(x1, x2, w1, w2,
+    wo) (Sec. 3.1, eq. tp-eq-mul-weight), from the definition
+
+        y_k = wo[l(k)] sum_{i,j} w1[l(i)] w2[l(j)] G[i, j, k] x1_i x2_j
+
+    (l(.) the degree of a coefficient index):
+      dx1_i     = w1[l(i)] sum_{j,k} G[i, j, k] (w2 x2)_j (wo dy)_k,
+      dw1[l1]   = sum_{i of degree l1} x1_i sum_{j,k} G[i, j, k] (w2 x2)_j (wo dy)_k,
+      (x2 and w2 alike), and
+      dwo[l]    = sum_{k of degree l} dy_k sum_{i,j} G[i, j, k] (w1 x1)_i (w2 x2)_j.
+    The contractions over G are gtp_vjp and gtp of the weighted inputs.
+    Weight gradients are per product ([n, L + 1]); summing them over the
+    products that share a weight row gives that row's gradient.
+    Returns (dx1, dx2, dw1, dw2, dwo) in float64."""
+    x1 = np.asarray(x1, dtype=np.float64).reshape(-1, nsh(L1))
+    x2 = np.asarray(x2, dtype=np.float64).reshape(-1, nsh(L2))
+    dy = np.asarray(dy, dtype=np.float64).reshape(-1, nsh(Lout))
+    n = x1.shape[0]
+    w1 = np.broadcast_to(np.asarray(w1, dtype=np.float64), (n, L1 + 1))
+    w2 = np.broadcast_to(np.asarray(w2, dtype=np.float64), (n, L2 + 1))
+    wo = np.broadcast_to(np.asarray(wo, dtype=np.float64), (n, Lout + 1))
+    d1, d2, do = degree_index(L1), degree_index(L2), degree_index(Lout)
+    u1, u2 = gtp_vjp(x1 * w1[:, d1], x2 * w2[:, d2], dy * wo[:, do], L1, L2, Lout)
+    z = gtp(x1 * w1[:, d1], x2 * w2[:, d2], L1, L2, Lout) if max(L1, L2, Lout) <= 8 else \
+        gtp_grid(x1 * w1[:, d1], x2 * w2[:, d2], L1, L2, Lout)
+
+    def per_degree(a, b, L):
+        return np.stack([(a[:, l * l:(l + 1) ** 2] * b[:, l * l:(l + 1) ** 2]).sum(1) for l in range(L + 1)], 1)
+    return (w1[:, d1] * u1, w2[:, d2] * u2, per_degree(x1, u1, L1), per_degree(x2, u2, L2), per_degree(dy, z, Lout))
+
+
+def degree_index(L: int) -> np.ndarray:
+    """Degree l of every coefficient index i = l*l + l + m, i < (L+1)^2."""
+    return np.concatenate([np.full(2 * l + 1, l) for l in range(L + 1)])
+
+
 def gtp_vjp(x1, x2, dy, L1: int, L2: int, Lout: int, chunk: int = 2048, mode: str = "auto"):
     """Gradients of s = sum_k dy[k] y[k], y = gtp(x1, x2, L1, L2, Lout).
 

@@ -2,6 +2,7 @@
 // of it before the first HIP call), table upload and kernel dispatch.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -308,6 +309,29 @@ gtp_status run_product(gtp_plan p, const void* x1, int it1, const void* x2, int 
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
     e = gtp::launch_full_wave(p->dev, x1, it1, x2, it2, n, y, wt, st, &done);
     if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+    if (!wt.on) {
+      // no kernel for these exact degrees: the equal-degree kernel of the
+      // padded degree A (the inputs read with zeros above their degrees, the
+      // outputs above Lout dropped; exact, see k_full_small_pad)
+      const int A = std::max({1, p->L1, p->L2, std::min(p->Lout, p->L1 + p->L2)});
+      const int k1 = gtp::nsh(p->L1), k2 = gtp::nsh(p->L2), ko = gtp::nsh(p->Lout);
+      if (p->Lout == 0) {
+        // one output, the projection onto Y_0^0: a dot product (k_dot0)
+        e = gtp::launch_dot0(x1, it1, k1, x2, it2, k2, n, y, st, &done);
+        if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+      }
+      if (A <= 8) {
+        e = gtp::launch_full_small_padded(A, x1, it1, k1, x2, it2, k2, n, y, ko, st, &done);
+        if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+      } else if (A <= kMaxL) {
+        const int W = A <= 16 ? 16 : (A <= 32 ? 32 : 64);
+        gtp_plan q = nullptr;
+        const gtp_status s = cached_plan(W, W, W, GTP_CONV_DFT, &q);
+        if (s != GTP_OK) return s;
+        e = gtp::launch_full_wave(q->dev, x1, it1, x2, it2, n, y, wt, st, &done, k1, k2, ko);
+        if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
+      }
+    }
   }
   e = gtp::launch_full_generic(p->dev, x1, it1, x2, it2, n, y, 0, wt, st);
   return e == hipSuccess ? GTP_OK : hip_fail(e, what);
@@ -623,6 +647,120 @@ gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dty
   return GTP_OK;
 }
 
+gtp_status gtp_full_weighted_backward(gtp_plan p, const void* x1, const void* x2, gtp_dtype in_dtype,
+                                      const float* w1, const float* w2, const float* wout, int per_channel,
+                                      const float* dy, int64_t B, int64_t C, float* dx1, float* dx2, float* dw1,
+                                      float* dw2, float* dwout, void* stream) {
+  gtp_status s = plan_check(p);
+  if (s != GTP_OK) return s;
+  if (!dtype_ok(in_dtype)) return fail(GTP_ERR_INVALID_ARG, "in_dtype must be GTP_F32 or GTP_BF16");
+  if (per_channel != 0 && per_channel != 1) return fail(GTP_ERR_INVALID_ARG, "per_channel must be 0 or 1");
+  int64_t n = 0, e1 = 0, e2 = 0, eo = 0;
+  if (!mul_ok(B, C, &n)) return fail(GTP_ERR_INVALID_ARG, "B and C must be >= 0 and B*C must fit in int64");
+  if (!mul_ok(n, gtp::nsh(p->L1), &e1) || !mul_ok(n, gtp::nsh(p->L2), &e2) || !mul_ok(n, gtp::nsh(p->Lout), &eo) ||
+      e1 > INT64_MAX / 4 || e2 > INT64_MAX / 4 || eo > INT64_MAX / 4)
+    return fail(GTP_ERR_INVALID_ARG, "B*C*(L+1)^2 overflows");
+  const bool any = dx1 || dx2 || dw1 || dw2 || dwout;
+  if (n == 0 && !(dw1 || dw2 || dwout)) return GTP_OK;
+  if (!any) return GTP_OK;
+  if (n > 0 && (!x1 || !x2 || !dy)) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  const int64_t R = per_channel ? C : 1;
+  if (R > 65535) return fail(GTP_ERR_UNSUPPORTED, "more than 65535 weight rows");
+  const size_t es = dtype_size(in_dtype);
+  const size_t rb1 = size_t(R) * (p->L1 + 1) * 4, rb2 = size_t(R) * (p->L2 + 1) * 4, rbo = size_t(R) * (p->Lout + 1) * 4;
+  // every output against every input and every other output
+  const struct {
+    const void* ptr;
+    size_t bytes;
+  } ins[] = {{x1, size_t(e1) * es}, {x2, size_t(e2) * es}, {dy, size_t(eo) * 4}, {w1, rb1}, {w2, rb2}, {wout, rbo}},
+    outs[] = {{dx1, size_t(e1) * 4}, {dx2, size_t(e2) * 4}, {dw1, rb1}, {dw2, rb2}, {dwout, rbo}};
+  for (const auto& o : outs) {
+    if (!o.ptr || !o.bytes) continue;
+    for (const auto& in : ins)
+      if (in.ptr && in.bytes && ranges_overlap(o.ptr, o.bytes, in.ptr, in.bytes))
+        return fail(GTP_ERR_INVALID_ARG, "an output overlaps an input");
+    for (const auto& o2 : outs)
+      if (&o2 != &o && o2.ptr && o2.bytes && ranges_overlap(o.ptr, o.bytes, o2.ptr, o2.bytes))
+        return fail(GTP_ERR_INVALID_ARG, "two outputs overlap");
+  }
+  if (!aligned(es, x1, x2) || !aligned(4, dy, w1, w2, wout, dx1, dx2, dw1, dw2, dwout))
+    return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if (p->conv == GTP_CONV_DIRECT) return fail(GTP_ERR_UNSUPPORTED, "per-degree weights are not built for the direct "
+                                                                   "convolution path");
+  if ((s = device_ready(p)) != GTP_OK) return s;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  // y = wout GTP(w1 x1, w2 x2): with u1 = P_L1 GTP(wout dy, w2 x2) and
+  // u2 = P_L2 GTP(wout dy, w1 x1) the gradients with respect to the weighted
+  // inputs (the Gaunt coefficient is symmetric in its three (l, m) pairs),
+  //   dx1 = w1 u1,  dw1[r, l1] = sum over row r of <x1, u1> on degree l1
+  // (likewise for x2), and with z = GTP(w1 x1, w2 x2)
+  //   dwout[r, l] = sum over row r of <dy, z> on degree l.
+  const int64_t nchunk = gtp::wgrad_nchunk(B, C, per_channel);
+  const bool need_u1 = dx1 || dw1, need_u2 = dx2 || dw2;
+  // workspace: u1 / u2 where dx1 / dx2 are not given, z, and the partials
+  const int64_t f_u1 = (need_u1 && !dx1) ? e1 : 0, f_u2 = (need_u2 && !dx2) ? e2 : 0, f_z = dwout ? eo : 0;
+  const int64_t Lmax = std::max({p->L1, p->L2, p->Lout});
+  const int64_t f_part = nchunk * R * (Lmax + 1);
+  const int64_t total = f_u1 + f_u2 + f_z + f_part;
+  float* ws = nullptr;
+  hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&ws), size_t(total > 0 ? total : 1) * sizeof(float), st);
+  if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
+  float* const u1 = dx1 ? dx1 : ws;
+  float* const u2 = dx2 ? dx2 : ws + f_u1;
+  float* const z = ws + f_u1 + f_u2;
+  float* const part = z + f_z;
+  const unsigned conv = p->flags & 3u;
+  s = GTP_OK;
+  if (n > 0 && need_u1) {
+    gtp_plan q = p;
+    if ((p->Lout != p->L1 || p->L1 != p->L2) && (s = cached_plan(p->Lout, p->L2, p->L1, conv, &q)) != GTP_OK) {
+    } else {
+      // slot 1 = dy weighted by wout, slot 2 = x2 weighted by w2, no output weight
+      const gtp::DegWeights wt{wout, w2, nullptr, C, 0, per_channel, wout || w2};
+      s = run_product(q, dy, gtp::IN_F32, x2, it, n, u1, st, "gtp_full_weighted_backward launch", wt);
+      if (s == GTP_OK) {
+        e = gtp::launch_wgrad(x1, it, u1, dx1, w1, B, C, p->L1, per_channel, part, dw1, st);
+        if (e != hipSuccess) s = hip_fail(e, "gtp_full_weighted_backward reduction");
+      }
+    }
+  }
+  if (s == GTP_OK && n > 0 && need_u2) {
+    gtp_plan q = p;
+    if ((p->Lout != p->L1 || p->L1 != p->L2) && (s = cached_plan(p->Lout, p->L1, p->L2, conv, &q)) != GTP_OK) {
+    } else {
+      const gtp::DegWeights wt{wout, w1, nullptr, C, 0, per_channel, wout || w1};
+      s = run_product(q, dy, gtp::IN_F32, x1, it, n, u2, st, "gtp_full_weighted_backward launch", wt);
+      if (s == GTP_OK) {
+        e = gtp::launch_wgrad(x2, it, u2, dx2, w2, B, C, p->L2, per_channel, part, dw2, st);
+        if (e != hipSuccess) s = hip_fail(e, "gtp_full_weighted_backward reduction");
+      }
+    }
+  }
+  if (s == GTP_OK && n > 0 && dwout) {
+    const gtp::DegWeights wt{w1, w2, nullptr, C, 0, per_channel, w1 || w2};
+    s = run_product(p, x1, it, x2, it, n, z, st, "gtp_full_weighted_backward launch", wt);
+    if (s == GTP_OK) {
+      e = gtp::launch_wgrad(dy, gtp::IN_F32, z, nullptr, nullptr, B, C, p->Lout, per_channel, part, dwout, st);
+      if (e != hipSuccess) s = hip_fail(e, "gtp_full_weighted_backward reduction");
+    }
+  }
+  if (s == GTP_OK && n == 0) {
+    // no products: the weight gradients are zero
+    for (auto [dw, L] : {std::pair<float*, int>{dw1, p->L1}, {dw2, p->L2}, {dwout, p->Lout}}) {
+      if (!dw) continue;
+      e = gtp::launch_fill_zero(dw, R * (L + 1), st);
+      if (e != hipSuccess) {
+        s = hip_fail(e, "gtp_full_weighted_backward launch");
+        break;
+      }
+    }
+  }
+  const hipError_t ef = hipFreeAsync(ws, st);
+  if (s != GTP_OK) return s;
+  return ef == hipSuccess ? GTP_OK : hip_fail(ef, "hipFreeAsync");
+}
+
 gtp_status gtp_sh2fourier(gtp_plan p, int which, const void* x, gtp_dtype in_dtype, int64_t n, float* grid,
                           void* stream) {
   gtp_status s = plan_check(p);
@@ -762,6 +900,20 @@ gtp_status gtp_sh_filter(int L, const float* r, const float* h, int64_t B, int64
   if (s != GTP_OK) return s;
   hipError_t e = gtp::launch_sh_filter(L, r, h, B, C, out, static_cast<hipStream_t>(stream));
   return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_sh_filter launch");
+}
+
+gtp_status gtp_stream_probe(int mode, const void* src, void* dst, int64_t nbytes, void* stream) {
+  if (mode < 0 || mode > 2) return fail(GTP_ERR_INVALID_ARG, "mode must be 0 (read), 1 (write) or 2 (copy)");
+  if (nbytes < 0 || nbytes % 16) return fail(GTP_ERR_INVALID_ARG, "nbytes must be a non-negative multiple of 16");
+  if (nbytes == 0) return GTP_OK;
+  if (!dst || (mode != 1 && !src)) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
+  if (!aligned(16, src, dst)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  if (mode == 2 && ranges_overlap(src, size_t(nbytes), dst, size_t(nbytes)))
+    return fail(GTP_ERR_INVALID_ARG, "src and dst overlap");
+  gtp_status s = check_device();
+  if (s != GTP_OK) return s;
+  const hipError_t e = gtp::launch_stream_probe(mode, src, dst, nbytes, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_stream_probe launch");
 }
 
 int64_t gtp_grid_floats(gtp_plan p, int which) {

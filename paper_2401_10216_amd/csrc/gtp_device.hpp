@@ -100,8 +100,16 @@ hipError_t launch_self_stepwise_small(const DevTables& t1, const DevTables& t2, 
 // Wave-per-product fused kernel with the phi stage on the matrix cores, for
 // L1 = L2 = Lout = L in {16, 32, 64}; *supported = false otherwise, or for a
 // bf16 x1 with an fp32 x2.
+// Degree-padded thread-per-product kernel (padded degree L in 1..8, tables
+// compiled in): inputs of k1 / k2 coefficients per row read as degree-L
+// vectors (zeros above), ko outputs per row written (zeros above degree L).
+hipError_t launch_full_small_padded(int L, const void* x1, int it1, int k1, const void* x2, int it2, int k2,
+                                    int64_t n, float* y, int ko, hipStream_t s, bool* supported);
+// k1, k2, ko > 0: a plan of lower degrees padded to the tables' degree
+// (input rows of k1 / k2 coefficients, output rows of ko; no weights).
 hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                            float* y, const DegWeights& wt, hipStream_t s, bool* supported);
+                            float* y, const DegWeights& wt, hipStream_t s, bool* supported, int k1 = 0, int k2 = 0,
+                            int ko = 0);
 // Workgroup-per-product fused kernel, any degrees (nu = 0: x1 * x2;
 // nu >= 2: x1^nu with the plan built for U = nu * L).
 hipError_t launch_full_generic(const DevTables& t, const void* x1, int type1, const void* x2, int type2,
@@ -122,6 +130,19 @@ hipError_t launch_mix_gemm(const float* WT, const float* T, float* y, int Co, in
                            hipStream_t s);
 // y[0 .. n) = 0 with a kernel (safe inside captured graphs).
 hipError_t launch_fill_zero(float* y, int64_t n, hipStream_t s);
+// Weight gradients of the weighted product (gtp_wgrad.hip): per-chunk
+// partial sums of per-degree dot products of a (in_type) and u over the
+// products of each weight row (rows = C with per_channel, else 1), optionally
+// writing out = w[row, l] u, then (dw != null) the chunks summed into
+// dw[row, l].  partial: wgrad_nchunk(B, C, per_channel) * rows * (L + 1) floats.
+int64_t wgrad_chunk(int64_t B, int64_t C, int per_channel);
+int64_t wgrad_nchunk(int64_t B, int64_t C, int per_channel);
+hipError_t launch_wgrad(const void* a, int a_type, const float* u, float* out, const float* w, int64_t B, int64_t C,
+                        int L, int per_channel, float* partial, float* dw, hipStream_t s);
+
+// HBM streaming probes: mode 0 reads nbytes of src (dst receives at most one
+// float), 1 writes nbytes to dst, 2 copies src to dst; 16-byte accesses.
+hipError_t launch_stream_probe(int mode, const void* src, void* dst, int64_t nbytes, hipStream_t s);
 // Fused channel mixing for equal degrees 1..8 and Co <= 128 (*supported =
 // false otherwise): pair products and the mix in one kernel, one workgroup
 // per batch entry.  WB: the weights in the blocked layout made by
@@ -131,6 +152,9 @@ hipError_t launch_mix_wt_blocks(const float* W, float* WB, int Co, int64_t P, in
 hipError_t launch_mix_fused(const DevTables& t, const void* x1, const void* x2, int it, const float* WB, float* y,
                             int64_t B, int64_t C1, int64_t C2, int Co, hipStream_t s, bool* supported);
 // y[p, :(Lout+1)^2] = x[p, :(L+1)^2] truncated or zero-padded.
+// Lout = 0 products: y = <x1, x2> / sqrt(4 pi) over the common coefficients.
+hipError_t launch_dot0(const void* x1, int it1, int k1, const void* x2, int it2, int k2, int64_t n, float* y,
+                       hipStream_t s, bool* supported);
 hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* y, int Lout, hipStream_t s);
 // Direct 2D convolution of the real-form Fourier grids (the paper's eq.
 // 2D-conv without the convolution theorem), workgroup per product.

@@ -520,6 +520,41 @@ hipError_t launch_pad_copy(const void* x, int in_type, int L, int64_t n, float* 
   return hipGetLastError();
 }
 
+// Lout = 0: the only output is the projection of F1 F2 onto Y_0^0, i.e.
+// (1 / sqrt(4 pi)) int F1 F2 dOmega, which orthonormality of the real SH
+// turns into the dot product of the coefficients both inputs have (Sec. 3.1,
+// the Gaunt coefficient with (l, m) = (0, 0)).  One lane per product.
+template <typename T1, typename T2>
+__global__ __launch_bounds__(kBlock) void k_dot0(const T1* __restrict__ x1, int k1, const T2* __restrict__ x2,
+                                                 int k2, int64_t n, float* __restrict__ y) {
+  const int kc = k1 < k2 ? k1 : k2;
+  for (int64_t p = int64_t(blockIdx.x) * kBlock + threadIdx.x; p < n; p += int64_t(gridDim.x) * kBlock) {
+    float a = 0.0f;
+    for (int i = 0; i < kc; ++i) a = fmaf(ld_in(x1, p * k1 + i), ld_in(x2, p * k2 + i), a);
+    y[p] = a * 0.28209479177387814f;  // 1 / sqrt(4 pi)
+  }
+}
+
+hipError_t launch_dot0(const void* x1, int it1, int k1, const void* x2, int it2, int k2, int64_t n, float* y,
+                       hipStream_t s, bool* supported) {
+  *supported = true;
+  const dim3 g(grid_for(n, kBlock)), b(kBlock);
+  if (it1 == IN_F32 && it2 == IN_F32)
+    hipLaunchKernelGGL((k_dot0<float, float>), g, b, 0, s, static_cast<const float*>(x1), k1,
+                       static_cast<const float*>(x2), k2, n, y);
+  else if (it1 == IN_BF16 && it2 == IN_BF16)
+    hipLaunchKernelGGL((k_dot0<uint16_t, uint16_t>), g, b, 0, s, static_cast<const uint16_t*>(x1), k1,
+                       static_cast<const uint16_t*>(x2), k2, n, y);
+  else if (it1 == IN_F32 && it2 == IN_BF16)
+    hipLaunchKernelGGL((k_dot0<float, uint16_t>), g, b, 0, s, static_cast<const float*>(x1), k1,
+                       static_cast<const uint16_t*>(x2), k2, n, y);
+  else {
+    *supported = false;
+    return hipSuccess;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_full_direct(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
                               float* y, hipStream_t s) {
   const size_t lds = size_t(direct_layout(t).total) * sizeof(float);

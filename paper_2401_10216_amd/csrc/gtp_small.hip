@@ -638,7 +638,8 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     cfor<0, K1>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
     bool staged = false;
     // (measured: 2.4 % faster at L = 6; at L = 4 4 % and at L = 8 1 % slower
-    // than the per-lane loads, so degrees 5..7 only)
+    // than the per-lane loads, so degrees 5..7 only.  Staging x1 the same way,
+    // through the tile before x2, measured 1 % slower at L = 6.)
     if constexpr (std::is_same<T2, float>::value && !OUT && L2 >= 5 && L2 <= 7) {
       if (dma && cnt == kTile) {
         // a full workgroup's x2 rows are one contiguous slab laid out as the
@@ -691,6 +692,80 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     gtp_core<L1, L2, LO, NU>(A, A, acc, ST, ntS, WT, ntW);
   }
   store_rows<KO, G::KE>(y, p0, cnt, tile, acc);
+}
+
+// Degree-padded product: a plan of degrees (a, b, c) whose padded degree
+// L = max(a, b, min(c, a + b)) is at most 8 runs on the equal-degree core of
+// degree L (compile-time tables).  The inputs are read as degree-L vectors
+// whose coefficients above their own degrees are zero (rows of k1 = (a+1)^2
+// and k2 = (b+1)^2 values), and the first ko = (c+1)^2 outputs are written
+// (zeros above degree L when c > L).  Exact: the degree-L sampling grid
+// integrates the product of any two degree-L functions exactly, and
+// zero-padding or truncating the coefficient vectors changes nothing else.
+template <int L, typename T1, typename T2>
+__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L, L, L)))) void k_full_small_pad(
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, int k1, int k2, int ko) {
+  constexpr int K = csh(L);
+  __shared__ __align__(16) float tile[kTile * K];
+  const int tid = threadIdx.x;
+  const int64_t p0 = int64_t(blockIdx.x) * kTile;
+  const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
+  const int64_t p = p0 + (tid < cnt ? tid : cnt - 1);
+  const int row = tid < cnt ? tid : cnt - 1;
+  // The workgroup's rows of each input are one contiguous slab: coalesced
+  // loads of the slab into the tile (compact rows of k floats), then each
+  // lane takes its own row out of LDS, zero-padded to degree L.
+  auto slab_to_tile = [&](auto src, int k) {
+    const int tot = cnt * k;
+    int e = tid;
+    for (; e + 3 * kTile < tot; e += 4 * kTile) {
+      const float v0 = ld_in(src, e), v1 = ld_in(src, e + kTile), v2 = ld_in(src, e + 2 * kTile),
+                  v3 = ld_in(src, e + 3 * kTile);
+      tile[e] = v0;
+      tile[e + kTile] = v1;
+      tile[e + 2 * kTile] = v2;
+      tile[e + 3 * kTile] = v3;
+    }
+    for (; e < tot; e += kTile) tile[e] = ld_in(src, e);
+    __syncthreads();
+  };
+  float xa[K];
+  slab_to_tile(x1 + p0 * k1, k1);
+  cfor<0, K>([&](auto I) {
+    constexpr int i = decltype(I)::value;
+    const float v = tile[row * k1 + (i < k1 ? i : 0)];  // in-bounds index, then the select
+    xa[i] = i < k1 ? v : 0.0f;
+  });
+  __syncthreads();
+  {
+    float xb[K];
+    slab_to_tile(x2 + p0 * k2, k2);
+    cfor<0, K>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      const float v = tile[row * k2 + (i < k2 ? i : 0)];
+      xb[i] = i < k2 ? v : 0.0f;
+    });
+    __syncthreads();
+    cfor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = xb[decltype(I)::value]; });
+  }
+  float acc[K];
+  RegX<K> A{xa};
+  LdsX B{tile, tid * K};
+  gtp_core<L, L, L, 0>(A, B, acc, nullptr, 0, nullptr, 0);
+  __syncthreads();
+  if (ko <= K) {
+    cfor<0, K>([&](auto I) {
+      constexpr int i = decltype(I)::value;
+      if (i < ko) tile[tid * ko + i] = acc[i];
+    });
+    __syncthreads();
+    float* const out = y + p0 * ko;
+    for (int i = tid; i < cnt * ko; i += kTile) out[i] = tile[i];
+  } else if (tid < cnt) {
+    float* const out = y + p * ko;
+    cfor<0, K>([&](auto I) { out[decltype(I)::value] = acc[decltype(I)::value]; });
+    for (int i = K; i < ko; ++i) out[i] = 0.0f;
+  }
 }
 
 // Stepwise many-body chain: B_2 = P_LO(A A), B_{k+1} = P_LO(B_k A).
@@ -968,6 +1043,44 @@ hipError_t launch_full_small(const DevTables& t, const void* x1, int it1, const 
     return launch_one<a, 0, c, v>(t, x1, it1, x1, it1, n, y, wt, s, supported);
     GTP_SMALL_POWERS(GTP_CASE)
 #undef GTP_CASE
+  }
+  *supported = false;
+  return hipSuccess;
+}
+
+template <int L>
+hipError_t launch_pad_one(const void* x1, int it1, const void* x2, int it2, int64_t n, float* y, int k1, int k2,
+                          int ko, hipStream_t s, bool* supported) {
+  const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
+  if (it1 == IN_F32 && it2 == IN_F32)
+    hipLaunchKernelGGL((k_full_small_pad<L, float, float>), grid, block, 0, s, static_cast<const float*>(x1),
+                       static_cast<const float*>(x2), y, n, k1, k2, ko);
+  else if (it1 == IN_BF16 && it2 == IN_BF16)
+    hipLaunchKernelGGL((k_full_small_pad<L, uint16_t, uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x1),
+                       static_cast<const uint16_t*>(x2), y, n, k1, k2, ko);
+  else if (it1 == IN_F32 && it2 == IN_BF16)
+    hipLaunchKernelGGL((k_full_small_pad<L, float, uint16_t>), grid, block, 0, s, static_cast<const float*>(x1),
+                       static_cast<const uint16_t*>(x2), y, n, k1, k2, ko);
+  else {
+    *supported = false;
+    return hipSuccess;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_full_small_padded(int L, const void* x1, int it1, int k1, const void* x2, int it2, int k2,
+                                    int64_t n, float* y, int ko, hipStream_t s, bool* supported) {
+  *supported = true;
+  switch (L) {
+    case 1: return launch_pad_one<1>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 2: return launch_pad_one<2>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 3: return launch_pad_one<3>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 4: return launch_pad_one<4>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 5: return launch_pad_one<5>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 6: return launch_pad_one<6>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 7: return launch_pad_one<7>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    case 8: return launch_pad_one<8>(x1, it1, x2, it2, n, y, k1, k2, ko, s, supported);
+    default: break;
   }
   *supported = false;
   return hipSuccess;

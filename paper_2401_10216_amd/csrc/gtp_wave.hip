@@ -623,9 +623,11 @@ struct WaveCtx {
 
 // x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
 // threads of the workgroup: every load is issued before the first wait
-template <int L, bool WGT, typename T1, typename T2>
+// PAD: the rows hold k1 / k2 <= K coefficients (inputs of lower degree read
+// as degree-L vectors with zeros above their own degrees).
+template <int L, bool WGT, bool PAD = false, typename T1, typename T2>
 __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, int64_t P, int tid,
-                                        const int* xmap, const DegWeights& wt) {
+                                        const int* xmap, const DegWeights& wt, int k1 = 0, int k2 = 0) {
   using G = WGeo<L>;
   constexpr int K = G::K, NTH = G::NTH, NXK = G::NXK, NXKP = G::NXKP;
   int slot[NXKP];
@@ -642,8 +644,16 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
     constexpr int k = decltype(KK)::value;
     const int e = tid + NTH * k;
     if (NTH * k + NTH - 1 < K || e < K) {
-      v1[k] = ld_in_any(x1, P * K + e);
-      v2[k] = ld_in_any(x2, P * K + e);
+      if constexpr (PAD) {
+        // in-bounds index first, then the select: no load past a row's end
+        const float a = ld_in_any(x1, P * k1 + (e < k1 ? e : 0));
+        const float b = ld_in_any(x2, P * k2 + (e < k2 ? e : 0));
+        v1[k] = e < k1 ? a : 0.0f;
+        v2[k] = e < k2 ? b : 0.0f;
+      } else {
+        v1[k] = ld_in_any(x1, P * K + e);
+        v2[k] = ld_in_any(x2, P * K + e);
+      }
     }
   });
   if constexpr (WGT) {
@@ -672,6 +682,22 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
     }
   });
   __syncthreads();
+}
+
+// Output coefficient i of product P: rows of K (unpadded) or of ko values,
+// of which those past ko (degrees above the plan's Lout) are not written.
+template <bool PAD, int K>
+__device__ __forceinline__ void store_out(float* y, int64_t P, int ko, int i, float v) {
+  if constexpr (PAD) {
+    if (i < ko) y[P * ko + i] = v;
+  } else {
+    y[P * K + i] = v;
+  }
+}
+// A padded plan's outputs above degree L (when its Lout > L) are zeros.
+template <int K>
+__device__ __forceinline__ void zero_tail(float* y, int64_t P, int ko, int tid, int nth) {
+  for (int i = K + tid; i < ko; i += nth) y[P * ko + i] = 0.0f;
 }
 
 // degree l and order m > 0 of the q-th output row with m > 0 in tri order
@@ -714,10 +740,12 @@ __device__ __forceinline__ const int* row_er_table() {
 // L in {16, 32}: one wave per product; theta analysis accumulates in
 // registers after every pass.  FFT: the phi transforms by radix-2 FFTs
 // (phi_fft) instead of the direct-DFT contractions on the matrix cores.
-template <int L, typename T1, typename T2, bool WGT, bool FFT>
+// PAD: a plan of lower degrees padded to L (rows of k1, k2 inputs, ko outputs;
+// see stage_x and store_row).
+template <int L, typename T1, typename T2, bool WGT, bool FFT, bool PAD = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3))) void k_full_wave(
     const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
-    DegWeights wt) {
+    DegWeights wt, int k1, int k2, int ko) {
   using G = WGeo<L>;
   static_assert(L % 16 == 0 && L <= 32, "L must be 16 or 32");
   constexpr int NJ = G::NJ, NP = G::NP;
@@ -733,7 +761,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
   const int lane = threadIdx.x;
   if (int64_t(blockIdx.x) >= n) return;  // whole-wave exit (one product per workgroup)
   const int64_t P = xcd_product(blockIdx.x, n);
-  stage_x<L, WGT>(xs, x1, x2, P, lane, t.XMAP, wt);
+  stage_x<L, WGT, PAD>(xs, x1, x2, P, lane, t.XMAP, wt, k1, k2);
 
   const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, PASSES * (NIT + 1) * 64 * 8);
   const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
@@ -821,7 +849,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
     if constexpr (WGT) {
       if (wt.wo) y0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
     }
-    y[P * K + l * l + l] = y0;
+    store_out<PAD, K>(y, P, ko, l * l + l, y0);
   }
   int ln = lane;
   asm volatile("" : "+v"(ln));
@@ -835,10 +863,11 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
       if constexpr (WGT) {
         if (wt.wo) wl = wt.wo[weight_row(wt, P) * (L + 1) + l];
       }
-      y[P * K + l * l + l + m] = yc[it] * wl;
-      y[P * K + l * l + l - m] = ys[it] * wl;
+      store_out<PAD, K>(y, P, ko, l * l + l + m, yc[it] * wl);
+      store_out<PAD, K>(y, P, ko, l * l + l - m, ys[it] * wl);
     }
   });
+  if constexpr (PAD) zero_tail<K>(y, P, ko, lane, 64);
 }
 
 // L = 64: four waves per product (256 threads), wave v runs passes 2v and
@@ -846,10 +875,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
 // second stay in registers until every wave is done with the x image, then
 // go into its place.  The 256 threads then do the theta analysis, each over
 // all 64 mirror pairs of its output rows.
-template <int L, typename T1, typename T2, bool WGT>
+template <int L, typename T1, typename T2, bool WGT, bool PAD = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_full_wave4(
     const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
-    DegWeights wt) {
+    DegWeights wt, int k1, int k2, int ko) {
   using G = WGeo<L>;
   static_assert(G::NW == 4 && G::PASSES == 8, "four waves, two passes each");
   constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
@@ -862,7 +891,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (int64_t(blockIdx.x) >= n) return;  // whole-workgroup exit (one product per workgroup)
   const int64_t P = xcd_product(blockIdx.x, n);
-  stage_x<L, WGT>(lds, x1, x2, P, tid, t.XMAP, wt);
+  stage_x<L, WGT, PAD>(lds, x1, x2, P, tid, t.XMAP, wt, k1, k2);
   const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(lds), t);
 
   f4 o[G::NMR][4];
@@ -912,7 +941,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
     if constexpr (WGT) {
       if (wt.wo) a0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
     }
-    y[P * K + l * l + l] = a0;
+    store_out<PAD, K>(y, P, ko, l * l + l, a0);
   }
   for (int it = 0; it < NIT; ++it) {
     const int q = tid + NTH * it;
@@ -928,15 +957,17 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
           as *= wl;
         }
       }
-      y[P * K + l * l + l + m] = ac;
-      y[P * K + l * l + l - m] = as;
+      store_out<PAD, K>(y, P, ko, l * l + l + m, ac);
+      store_out<PAD, K>(y, P, ko, l * l + l - m, as);
     }
   }
+  if constexpr (PAD) zero_tail<K>(y, P, ko, tid, NTH);
 }
 
-template <int L, typename T1, typename T2, bool WGT>
+template <int L, typename T1, typename T2, bool WGT, bool PAD = false>
 hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t,
-                             const DegWeights& wt, hipStream_t s) {
+                             const DegWeights& wt, hipStream_t s, int k1 = WGeo<L>::K, int k2 = WGeo<L>::K,
+                             int ko = WGeo<L>::K) {
   // the radix-FFT phi transforms where the plan asks for them and a
   // one-wave kernel exists (L = 16, 32)
   const bool fft = t.phi_fft != 0 && WGeo<L>::NW == 1;
@@ -944,19 +975,22 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
   // at most 2^30 workgroups per launch
   for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
     const int64_t nn = n - p0 < (int64_t(1) << 30) ? n - p0 : (int64_t(1) << 30);
-    const T1* a = static_cast<const T1*>(x1) + size_t(p0) * G::K;
-    const T2* b = static_cast<const T2*>(x2) + size_t(p0) * G::K;
-    float* yy = y + size_t(p0) * G::K;
+    const T1* a = static_cast<const T1*>(x1) + size_t(p0) * k1;
+    const T2* b = static_cast<const T2*>(x2) + size_t(p0) * k2;
+    float* yy = y + size_t(p0) * ko;
     DegWeights w = wt;
     w.pbase += p0;  // the chunk's products start at p0
     if constexpr (G::NW == 1) {
-      if (fft)
-        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, true>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t, w);
+      if (fft && !PAD)
+        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, true>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t, w,
+                           k1, k2, ko);
       else
-        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, false>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn, t,
-                           w);
-    } else
-      hipLaunchKernelGGL((k_full_wave4<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t, w);
+        hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, false, PAD>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn,
+                           t, w, k1, k2, ko);
+    } else {
+      hipLaunchKernelGGL((k_full_wave4<L, T1, T2, WGT, PAD>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t,
+                         w, k1, k2, ko);
+    }
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -965,12 +999,27 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
 
 // Input types: both fp32, both bf16, or fp32 x1 with bf16 x2 (a backward
 // pass: fp32 output gradient times a bf16 input); *supported = false for
-// bf16 x1 with fp32 x2, and for per-degree weights with mixed types.
+// bf16 x1 with fp32 x2, and for per-degree weights with mixed types.  k1,
+// k2, ko > 0: a padded plan (no weights).
 template <int L>
 hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                           float* y, const DegWeights& wt, hipStream_t s, bool* supported) {
+                           float* y, const DegWeights& wt, hipStream_t s, bool* supported, int k1, int k2, int ko) {
   // the scatter map's slots must fit the kernel's LDS image
   if (t.XQUADS != WGeo<L>::XQ) return hipErrorInvalidValue;
+  if (ko > 0) {
+    if (wt.on || k1 > WGeo<L>::K || k2 > WGeo<L>::K) {
+      *supported = false;
+      return hipSuccess;
+    }
+    if (it1 == IN_F32 && it2 == IN_F32)
+      return launch_wave_typed<L, float, float, false, true>(x1, x2, n, y, t, wt, s, k1, k2, ko);
+    if (it1 == IN_BF16 && it2 == IN_BF16)
+      return launch_wave_typed<L, uint16_t, uint16_t, false, true>(x1, x2, n, y, t, wt, s, k1, k2, ko);
+    if (it1 == IN_F32 && it2 == IN_BF16)
+      return launch_wave_typed<L, float, uint16_t, false, true>(x1, x2, n, y, t, wt, s, k1, k2, ko);
+    *supported = false;
+    return hipSuccess;
+  }
   if (wt.on) {
     if (it1 == IN_F32 && it2 == IN_F32) return launch_wave_typed<L, float, float, true>(x1, x2, n, y, t, wt, s);
     if (it1 == IN_BF16 && it2 == IN_BF16)
@@ -989,11 +1038,11 @@ hipError_t launch_wave_one(const DevTables& t, const void* x1, int it1, const vo
 }  // namespace
 
 hipError_t launch_full_wave(const DevTables& t, const void* x1, int it1, const void* x2, int it2, int64_t n,
-                            float* y, const DegWeights& wt, hipStream_t s, bool* supported) {
+                            float* y, const DegWeights& wt, hipStream_t s, bool* supported, int k1, int k2, int ko) {
   *supported = true;
-  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, it1, x2, it2, n, y, wt, s, supported);
-  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, it1, x2, it2, n, y, wt, s, supported);
-  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, it1, x2, it2, n, y, wt, s, supported);
+  if (t.waveL == 16 && t.SMP) return launch_wave_one<16>(t, x1, it1, x2, it2, n, y, wt, s, supported, k1, k2, ko);
+  if (t.waveL == 32 && t.SMP) return launch_wave_one<32>(t, x1, it1, x2, it2, n, y, wt, s, supported, k1, k2, ko);
+  if (t.waveL == 64 && t.SMP) return launch_wave_one<64>(t, x1, it1, x2, it2, n, y, wt, s, supported, k1, k2, ko);
   *supported = false;
   return hipSuccess;
 }

@@ -46,6 +46,7 @@ _SIGS = {
     "gtp_full": (_I, [_P, _P, _P, _I, _I64, _I64, _P, _P]),
     "gtp_full_backward": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P]),
     "gtp_full_weighted": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _I64, _I64, _P, _P]),
+    "gtp_full_weighted_backward": (_I, [_P, _P, _P, _I, _P, _P, _P, _I, _P, _I64, _I64, _P, _P, _P, _P, _P, _P]),
     "gtp_conv_escn": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
     "gtp_conv_escn_noalloc": (_I, [_P, _P, _I, _P, _P, _I64, _I64, _P, _P]),
     "gtp_channel_mix": (_I, [_P, _P, _P, _I, _P, _I64, _I64, _I64, _I64, _P, _P]),
@@ -54,6 +55,7 @@ _SIGS = {
     "gtp_fourier2sh": (_I, [_P, _P, _I64, _P, _P]),
     "gtp_selfproduct": (_I, [_I, _I, _I, _U, _P, _I, _I64, _I64, _P, _P]),
     "gtp_sh_filter": (_I, [_I, _P, _P, _I64, _I64, _P, _P]),
+    "gtp_stream_probe": (_I, [_I, _P, _P, _I64, _P]),
     "gtp_grid_floats": (_I64, [_P, _I]),
     "gtp_plan_info": (_I, [_P, ctypes.POINTER(_I64)]),
     "gtp_plan_table": (_I, [_P, _I, _DP, ctypes.POINTER(_I64)]),
@@ -286,6 +288,40 @@ def gtp_full_weighted(plan: Plan, x1, x2, w1=None, w2=None, wout=None, per_chann
     return y
 
 
+def gtp_full_weighted_backward(plan: Plan, x1, x2, dy, w1=None, w2=None, wout=None, per_channel: bool = False,
+                               need=("dx1", "dx2", "dw1", "dw2", "dwout"), stream=None):
+    """Gradients of <dy, gtp_full_weighted(x1, x2, w1, w2, wout)>: a dict with the requested keys among dx1, dx2
+    ([B, C, K] fp32) and dw1, dw2, dwout ([R, L+1] fp32, R = C if per_channel else 1)."""
+    import torch
+    if x1.dtype != x2.dtype:
+        raise TypeError("x1 and x2 must have the same dtype")
+    if x1.dim() != 3 or x2.dim() != 3 or x1.shape[:2] != x2.shape[:2]:
+        raise ValueError("x1, x2 must be [B, C, K] with equal B, C")
+    if x1.shape[2] != nsh(plan.L1) or x2.shape[2] != nsh(plan.L2):
+        raise ValueError("coefficient dimension does not match the plan")
+    unknown = set(need) - {"dx1", "dx2", "dw1", "dw2", "dwout"}
+    if unknown:
+        raise ValueError(f"unknown gradients {sorted(unknown)}")
+    B, C = int(x1.shape[0]), int(x1.shape[1])
+    R = C if per_channel else 1
+    code = _dtype_code(x1)
+    px1 = _want(x1, "x1", x1.shape, _inputs())
+    px2 = _want(x2, "x2", x2.shape, _inputs(), x1.device)
+    pdy = _want(dy, "dy", (B, C, nsh(plan.Lout)), _f32(), x1.device)
+    ws = []
+    for w, L, name in ((w1, plan.L1, "w1"), (w2, plan.L2, "w2"), (wout, plan.Lout, "wout")):
+        ws.append(ctypes.c_void_p(None) if w is None else _want(w, name, (R, L + 1), _f32(), x1.device))
+    shapes = {"dx1": (B, C, nsh(plan.L1)), "dx2": (B, C, nsh(plan.L2)), "dw1": (R, plan.L1 + 1),
+              "dw2": (R, plan.L2 + 1), "dwout": (R, plan.Lout + 1)}
+    out = {k: torch.empty(shapes[k], dtype=torch.float32, device=x1.device) for k in need}
+    ptr = {k: (ctypes.c_void_p(out[k].data_ptr()) if k in out else ctypes.c_void_p(None)) for k in shapes}
+    _on_gpu(x1, "x1")
+    _check(lib().gtp_full_weighted_backward(plan.handle, px1, px2, code, *ws, 1 if per_channel else 0, pdy, B, C,
+                                            ptr["dx1"], ptr["dx2"], ptr["dw1"], ptr["dw2"], ptr["dwout"],
+                                            _stream(stream)))
+    return out
+
+
 def gtp_full_backward(plan: Plan, x1, x2, dy, need_dx1: bool = True, need_dx2: bool = True, dx1=None, dx2=None,
                       stream=None):
     """(dx1, dx2): gradients of <dy, gtp_full(x1, x2)> in x1 and x2 (fp32; None when not requested)."""
@@ -397,6 +433,15 @@ def gtp_sh_filter(L: int, r, h=None, out=None, stream=None):
     _on_gpu(r, "r")
     _check(lib().gtp_sh_filter(L, pr, hp, B, C, po, _stream(stream)))
     return out
+
+
+def gtp_stream_probe(mode: int, src, dst, stream=None):
+    """HBM streaming probe: mode 0 reads src (dst: >= 1 float), 1 writes dst, 2 copies src to dst."""
+    nbytes = (dst if mode == 1 else src).numel() * (dst if mode == 1 else src).element_size()
+    if mode == 2 and dst.numel() * dst.element_size() < nbytes:
+        raise ValueError("dst smaller than src")
+    sp = ctypes.c_void_p(None) if mode == 1 else ctypes.c_void_p(src.data_ptr())
+    _check(lib().gtp_stream_probe(mode, sp, ctypes.c_void_p(dst.data_ptr()), nbytes, _stream(stream)))
 
 
 def gtp_debug_host_pipeline(plan: Plan, x1, x2):

@@ -354,3 +354,42 @@ def test_noalloc_escn_validation(L):
     # a huge channel count: refused without overflowing on the way
     assert f(q.handle, x, 0, r, fake(1 << 47), 1, 1 << 40, fake(1 << 50), S) == gtp.GTP_ERR_UNSUPPORTED
     assert f(q.handle, x, 0, r, h, 2, C - 1, y, S) == INV and b"HOST_ONLY" in L.gtp_last_error()
+
+
+def test_stream_probe_validation(L):
+    a, b = fake(0x100000), fake(0x200000)
+    S = ctypes.c_void_p(0)
+    INV = gtp.GTP_ERR_INVALID_ARG
+    assert L.gtp_stream_probe(3, a, b, 64, S) == INV
+    assert L.gtp_stream_probe(0, a, b, 20, S) == INV  # not a multiple of 16
+    assert L.gtp_stream_probe(0, a, b, -16, S) == INV
+    assert L.gtp_stream_probe(0, None, b, 64, S) == INV
+    assert L.gtp_stream_probe(1, None, None, 64, S) == INV
+    assert L.gtp_stream_probe(2, a, fake(0x100000 + 32), 64, S) == INV  # overlap
+    assert L.gtp_stream_probe(2, fake(0x100008), b, 64, S) == INV  # misaligned
+    assert L.gtp_stream_probe(2, a, b, 0, S) == gtp.GTP_OK
+
+
+def test_weighted_backward_validation(L):
+    p = host_plan(2, 3, 4)
+    H = p.handle
+    x1, x2, dy = fake(0x100000), fake(0x200000), fake(0x300000)
+    w1, w2, wo = fake(0x400000), fake(0x500000), fake(0x600000)
+    d1, d2, g1, g2, go = fake(0x700000), fake(0x800000), fake(0x900000), fake(0xa00000), fake(0xb00000)
+    S = ctypes.c_void_p(0)
+    INV, OK = gtp.GTP_ERR_INVALID_ARG, gtp.GTP_OK
+    f = L.gtp_full_weighted_backward
+    assert f(None, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, g2, go, S) == INV
+    assert f(H, x1, x2, 5, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, g2, go, S) == INV  # dtype
+    assert f(H, x1, x2, 0, w1, w2, wo, 2, dy, 4, 4, d1, d2, g1, g2, go, S) == INV  # per_channel
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, -4, 4, d1, d2, g1, g2, go, S) == INV
+    assert f(H, None, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, g2, go, S) == INV
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, fake(0x300000 + 4), d2, g1, g2, go, S) == INV  # dx1 over dy
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, fake(0x400000), g2, go, S) == INV  # dw1 over w1
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, fake(0x900000 + 4), go, S) == INV  # dw2 over dw1
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, g2, fake(0xb00002), S) == INV  # misaligned
+    assert f(H, x1, x2, 0, w1, w2, wo, 1, dy, 4, 1 << 17, None, None, g1, None, None, S) == gtp.GTP_ERR_UNSUPPORTED
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, None, None, None, None, None, S) == OK  # nothing requested
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 0, 4, d1, d2, None, None, None, S) == OK  # empty, no weight grads
+    assert f(H, x1, x2, 0, w1, w2, wo, 0, dy, 4, 4, d1, d2, g1, g2, go, S) == INV
+    assert b"HOST_ONLY" in L.gtp_last_error()

@@ -826,6 +826,45 @@ def test_plan_device_allocation_failure(monkeypatch):
     assert O.max_rel_err(y, O.gtp(a.astype(np.float64), a.astype(np.float64), 6, 6, 6)) <= TOL
 
 
+# ------------------------------------------------------------------ degree-padded kernels
+
+PADDED = [(6, 6, 2, False), (4, 6, 5, True), (1, 8, 8, False), (0, 0, 0, False), (3, 2, 11, False),
+          (10, 3, 7, False), (12, 12, 12, True), (9, 16, 4, False), (20, 9, 30, False), (24, 24, 24, True),
+          (40, 40, 40, False), (33, 2, 35, False), (5, 60, 64, False)]
+
+
+@pytest.mark.parametrize("L1,L2,Lout,bf16", PADDED)
+def test_padded_degrees(L1, L2, Lout, bf16):
+    """Degree triples without a kernel of their own run on the equal-degree
+    kernel of the padded degree max(L1, L2, min(Lout, L1 + L2)) (thread per
+    product up to 8, the matrix-core kernels of 16, 32, 64 above): a ragged
+    batch against the oracle, and against the workgroup kernel."""
+    n = 64 * 3 + 21 if max(L1, L2, Lout) <= 32 else 40
+    rng = np.random.default_rng(1000 + L1 + 70 * L2 + 4900 * Lout)
+    a = rng.standard_normal((n, 1, O.nsh(L1))).astype(np.float32)
+    b = rng.standard_normal((n, 1, O.nsh(L2))).astype(np.float32)
+    _say(f"padded L1={L1} L2={L2} Lout={Lout} bf16={bf16} n={n}")
+    plan = gtp.Plan(L1, L2, Lout)
+    if bf16:
+        b1, a = inputs.round_to_bf16(a)
+        b2, b = inputs.round_to_bf16(b)
+        y = gtp.gtp_full(plan, torch.from_numpy(b1.view(np.int16)).cuda().view(torch.bfloat16),
+                         torch.from_numpy(b2.view(np.int16)).cuda().view(torch.bfloat16))
+        torch.cuda.synchronize()
+        y = y.cpu().numpy().astype(np.float64)
+    else:
+        y = run_full(plan, a, b)
+    assert y.shape == (n, 1, O.nsh(Lout))
+    idx = np.arange(n) if max(L1, L2, Lout) <= 16 else np.r_[0:6, n - 6:n]
+    ref = oracle_pair(a[idx].astype(np.float64), b[idx].astype(np.float64), L1, L2, Lout)
+    err = O.max_rel_err(y[idx], ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL
+    if not bf16 and max(L1, L2, Lout) <= 16:
+        yg = run_full(gtp.Plan(L1, L2, Lout, gtp.GTP_FORCE_GENERIC), a, b)
+        assert O.max_rel_err(y, yg) <= TOL
+
+
 # ------------------------------------------------------------------ radix-FFT phi transforms (GTP_CONV_FFT)
 
 @pytest.mark.parametrize("L,n", [(16, 64 * 5 + 3), (32, 200)])
@@ -911,3 +950,74 @@ def test_fft_request_without_radix_kernel_runs_dft():
     a = rng.standard_normal((70, 1, 49)).astype(np.float32)
     y = run_full(gtp.Plan(6, 6, 6, gtp.GTP_CONV_FFT), a, a)
     assert O.max_rel_err(y, O.gtp(a.astype(np.float64), a.astype(np.float64), 6, 6, 6)) <= TOL
+
+
+# ------------------------------------------------------------------ weighted backward with weight gradients
+
+WBWD = [(2, 2, 2, False, "f32"), (6, 6, 6, True, "f32"), (4, 3, 5, False, "f32"), (6, 6, 6, False, "bf16"),
+        (16, 16, 16, True, "f32"), (8, 8, 8, False, "f32")]
+
+
+@pytest.mark.parametrize("L1,L2,Lout,per_channel,dt", WBWD)
+def test_weighted_backward_gradients(L1, L2, Lout, per_channel, dt):
+    """gtp_full_weighted_backward against the oracle's gradients of
+    <dy, gtp_weighted(...)>: input gradients per product, weight gradients
+    summed over the products of each weight row (the oracle's per-product
+    contributions summed in fp64)."""
+    B, C = (37, 5) if max(L1, L2, Lout) <= 8 else (6, 4)
+    rng = np.random.default_rng(1200 + L1 + 10 * L2 + 100 * Lout + per_channel)
+    x1 = rng.standard_normal((B, C, O.nsh(L1))).astype(np.float32)
+    x2 = rng.standard_normal((B, C, O.nsh(L2))).astype(np.float32)
+    dy = rng.standard_normal((B, C, O.nsh(Lout))).astype(np.float32)
+    R = C if per_channel else 1
+    w = [rng.standard_normal((R, L + 1)).astype(np.float32) for L in (L1, L2, Lout)]
+    plan = gtp.Plan(L1, L2, Lout)
+    if dt == "bf16":
+        b1, x1 = inputs.round_to_bf16(x1)
+        b2, x2 = inputs.round_to_bf16(x2)
+        t1 = torch.from_numpy(b1.view(np.int16)).cuda().view(torch.bfloat16)
+        t2 = torch.from_numpy(b2.view(np.int16)).cuda().view(torch.bfloat16)
+    else:
+        t1, t2 = dev(x1), dev(x2)
+    _say(f"weighted backward L=({L1},{L2},{Lout}) per_channel={per_channel} {dt}")
+    g = gtp.gtp_full_weighted_backward(plan, t1, t2, dev(dy), *[dev(v) for v in w], per_channel=per_channel)
+    torch.cuda.synchronize()
+    rows = np.tile(np.arange(C), B) if per_channel else np.zeros(B * C, int)
+    ref = O.gtp_weighted_vjp(x1.reshape(B * C, -1), x2.reshape(B * C, -1), w[0][rows], w[1][rows], w[2][rows],
+                             dy.reshape(B * C, -1), L1, L2, Lout)
+    for k, r in (("dx1", ref[0]), ("dx2", ref[1])):
+        err = O.max_rel_err(g[k].cpu().numpy().reshape(B * C, -1).astype(np.float64), r)
+        _say(f"  {k} err={err:.3e}")
+        assert err <= TOL, (k, err)
+    for k, r in (("dw1", ref[2]), ("dw2", ref[3]), ("dwout", ref[4])):
+        want = np.zeros((R, r.shape[1]))
+        np.add.at(want, rows, r)
+        got = g[k].cpu().numpy().astype(np.float64)
+        # a sum over B C / R products: relative to the sum of the magnitudes
+        mag = np.zeros_like(want)
+        np.add.at(mag, rows, np.abs(r))
+        err = (np.abs(got - want) / np.maximum(mag, 1e-30)).max()
+        _say(f"  {k} err={err:.3e}")
+        assert err <= TOL, (k, err)
+
+
+def test_weighted_backward_subsets_and_empty():
+    """Any subset of the gradients; NULL weights are ones; an empty batch
+    gives zero weight gradients."""
+    rng = np.random.default_rng(77)
+    B, C, L = 20, 3, 4
+    x1 = rng.standard_normal((B, C, 25)).astype(np.float32)
+    x2 = rng.standard_normal((B, C, 25)).astype(np.float32)
+    dy = rng.standard_normal((B, C, 25)).astype(np.float32)
+    plan = gtp.Plan(L, L, L)
+    full = gtp.gtp_full_weighted_backward(plan, dev(x1), dev(x2), dev(dy))
+    part = gtp.gtp_full_weighted_backward(plan, dev(x1), dev(x2), dev(dy), need=("dw2",))
+    torch.cuda.synchronize()
+    assert set(part) == {"dw2"}
+    assert np.array_equal(part["dw2"].cpu().numpy(), full["dw2"].cpu().numpy())
+    p1, p2 = O.gtp_vjp(x1.reshape(-1, 25), x2.reshape(-1, 25), dy.reshape(-1, 25), L, L, L)
+    assert O.max_rel_err(full["dx1"].cpu().numpy().reshape(-1, 25).astype(np.float64), p1) <= TOL
+    z = np.zeros((0, C, 25), np.float32)
+    e = gtp.gtp_full_weighted_backward(plan, dev(z), dev(z), dev(z), need=("dw1", "dwout"), per_channel=True)
+    torch.cuda.synchronize()
+    assert e["dw1"].shape == (C, L + 1) and not e["dw1"].cpu().numpy().any() and not e["dwout"].cpu().numpy().any()

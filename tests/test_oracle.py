@@ -726,3 +726,51 @@ def test_max_rel_err():
     assert O.max_rel_err(y, y) == 0
     assert abs(O.max_rel_err(y + [[0.5, 0], [0, 0]], y) - 0.1) < 1e-15
     assert abs(O.max_rel_err(y + [[0, 0], [0, 1e-3]], y) - 1e-3) < 1e-15
+
+
+@pytest.mark.parametrize("L1,L2,Lout", [(2, 2, 2), (3, 1, 4), (2, 3, 1), (12, 10, 12)])
+def test_weighted_vjp_pins(L1, L2, Lout):
+    """gtp_weighted_vjp against what the definition fixes: s = <dy, y> is
+    linear in each weight row, so a unit step of one weight changes s by
+    exactly that weight's gradient (finite difference, exact); s is
+    homogeneous of degree one in each of w1, w2, wo and x1, x2, so
+    sum_l w[l] dw[l] = s = <dx1, x1> = <dx2, x2> (Euler); with unit weights
+    the input gradients are the plain product's (gtp_vjp); weights that are
+    zero outside one degree pick that degree's block."""
+    rng = np.random.default_rng(L1 + 10 * L2 + 100 * Lout)
+    n = 5
+    x1 = rng.standard_normal((n, O.nsh(L1)))
+    x2 = rng.standard_normal((n, O.nsh(L2)))
+    dy = rng.standard_normal((n, O.nsh(Lout)))
+    w1 = rng.standard_normal(L1 + 1)
+    w2 = rng.standard_normal(L2 + 1)
+    wo = rng.standard_normal(Lout + 1)
+
+    def s_of(a, b, c):
+        return np.sum(dy * O.gtp_weighted(x1, x2, a, b, c, L1, L2, Lout), axis=1)
+
+    dx1, dx2, dw1, dw2, dwo = O.gtp_weighted_vjp(x1, x2, w1, w2, wo, dy, L1, L2, Lout)
+    s0 = s_of(w1, w2, wo)
+    scale = np.abs(s0).max() + 1.0
+    for l in range(L1 + 1):
+        e = np.zeros(L1 + 1)
+        e[l] = 1.0
+        assert np.abs(s_of(w1 + e, w2, wo) - s0 - dw1[:, l]).max() < 1e-10 * scale
+    for l in range(L2 + 1):
+        e = np.zeros(L2 + 1)
+        e[l] = 1.0
+        assert np.abs(s_of(w1, w2 + e, wo) - s0 - dw2[:, l]).max() < 1e-10 * scale
+    for l in range(Lout + 1):
+        e = np.zeros(Lout + 1)
+        e[l] = 1.0
+        assert np.abs(s_of(w1, w2, wo + e) - s0 - dwo[:, l]).max() < 1e-10 * scale
+    for g in (dw1 @ w1, dw2 @ w2, dwo @ wo, np.sum(dx1 * x1, 1), np.sum(dx2 * x2, 1)):
+        assert np.abs(g - s0).max() < 1e-10 * scale
+    p1, p2 = O.gtp_vjp(x1, x2, dy, L1, L2, Lout)
+    u1, u2, *_ = O.gtp_weighted_vjp(x1, x2, np.ones(L1 + 1), np.ones(L2 + 1), np.ones(Lout + 1), dy, L1, L2, Lout)
+    assert np.abs(u1 - p1).max() < 1e-12 * scale and np.abs(u2 - p2).max() < 1e-12 * scale
+    # a degree mask on x1 keeps only that degree's block of dx1
+    m = np.zeros(L1 + 1)
+    m[1] = 1.0
+    q1, *_ = O.gtp_weighted_vjp(x1, x2, m, w2, wo, dy, L1, L2, Lout)
+    assert np.abs(np.delete(q1, np.arange(1, 4), axis=1)).max() == 0.0
