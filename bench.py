@@ -115,14 +115,14 @@ def _fft_flops(N: int, nonzero_in: int = -1) -> int:
 
 def fft_variant_flops(L: int) -> int:
     """Flops per product of the matrix-core kernel's radix-FFT variant
-    (L1 = L2 = Lout = L in {16, 32}): the theta stages as in the DFT form, and
+    (L1 = L2 = Lout = L in {16, 32, 64}): the theta stages as in the DFT form, and
     per pass of 16 theta nodes the three FFT stages of phi_fft -- 16 N2
     column DFTs of length N1 with their twiddle powers and products, 16 N1 row
     DFTs of length N2 with the sample products and the real forward transform
     (a length-N2/2 DFT and N2/2 + 1 recombinations), 8 (N2/2 + 1) pairs of
     forward column DFTs of length N1."""
-    NF = 64 if L <= 16 else 128
-    N1 = 8
+    NF = 64 if L <= 16 else (128 if L <= 32 else 256)
+    N1 = 8 if L <= 32 else 16
     N2 = NF // N1
     U = 2 * L
     pairs = U / 2
@@ -159,15 +159,18 @@ def nsh(L):
 # device-side sources every kernel depends on (the host dispatch in
 # gtp_api.hip does not change a kernel's memory traffic), and those of single
 # kernel files (build-time constants, their tables)
-SHARED_SOURCES = ["gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
+SHARED_SOURCES = ["gtp_ct.hpp", "gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
 KERNEL_SOURCES = {
     "gtp_small.hip": ["gen_small_consts.cpp"],
     "gtp_escn.hip": ["gen_small_consts.cpp", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
+    "gtp_wave.hip": ["gtp_fft.hpp"],
 }
 
 
-def dominant_kernel(workload: str, L: int, escn: bool = False):
+def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto"):
     """(kernel, roofline bound, source file) of the kernel that dominates a workload."""
+    if conv == "fft" and workload in ("sweep", "highdeg") and L in (16, 32, 64):
+        return ("k_full_wave4_fft" if L > 32 else "k_full_wave (FFT)"), "alu", "gtp_wave.hip"
     if escn:
         # both kernels of the step (rotation matrices, then the product): one unit
         return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
@@ -356,7 +359,7 @@ def make_workload(args, torch, gtp, inputs):
         if args.conv != "auto":
             desc["conv"] = args.conv
         fl = kernel_flops(L1, L2, Lo)
-        if args.conv == "fft" and L1 == L2 == Lo and L in (16, 32):
+        if args.conv == "fft" and L1 == L2 == Lo and L in (16, 32, 64):
             fl = fft_variant_flops(L)
         return step, B * C, desc, (fl, SURVEY_FLOPS.get(L) if (L1, L2, Lo) == (L, L, L) else None), \
             in_bytes * (nsh(L1) + nsh(L2)) + 4 * nsh(Lo), oracle_sample, idx_cfg
@@ -577,8 +580,10 @@ def main():
     if alg_flops:
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
-        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn)
+        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn, args.conv)
         suffix = "_backward" if args.backward else ("_weighted" if args.weighted else ("_escn" if args.escn else ""))
+        if args.conv != "auto":
+            suffix += "_" + args.conv
         tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + suffix, ksrc)
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         comp = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",

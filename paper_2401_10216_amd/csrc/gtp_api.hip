@@ -926,7 +926,7 @@ gtp_status gtp_plan_info(gtp_plan p, int64_t* out8) {
   if (!p || !out8) return fail(GTP_ERR_INVALID_ARG, "NULL argument");
   const gtp::Tables& t = p->tab;
   // the FFT request is served by the radix-FFT kernels at equal degrees 16, 32
-  const bool radix = p->conv == GTP_CONV_FFT && !p->force_generic && (t.waveL == 16 || t.waveL == 32);
+  const bool radix = p->conv == GTP_CONV_FFT && !p->force_generic && t.waveL > 0;
   const int64_t used = p->conv == GTP_CONV_FFT && !radix ? GTP_CONV_DFT : p->conv;
   const int64_t v[8] = {t.L1, t.L2, t.Lout, t.U, t.Le, t.NT, t.NP, used};
   std::memcpy(out8, v, sizeof(v));

@@ -250,20 +250,24 @@ struct WaveCtx {
   // mr, column i) and zz, the m = 0 moment of the lane's column node.
   // FFT = true (the radix-FFT variant) runs the theta synthesis only and
   // writes each column node's packed phi spectrum to spec (phi_fft takes it
-  // from there); o and zz are then not written.
-  template <bool FFT = false>
+  // from there); o and zz are then not written.  K-steps S0..S1-1 only (the
+  // m-parts 8 S0 + 1 .. 8 S1; the m = 0 part with S0 = 0): the four waves of
+  // the L = 64 FFT kernel split one pass's synthesis this way.
+  template <bool FFT = false, int S0 = 0, int S1 = G::NKS>
   __device__ __forceinline__ void pass(int pu, f4 (&o)[G::NMR][4], float& zz, float2* spec = nullptr) const {
     constexpr int NMB = G::NMB, NMBP = G::NMBP, NKS = G::NKS, TWRN = G::TWRN, NMR = G::NMR;
+    static_assert(FFT || (S0 == 0 && S1 == NKS), "a K-step window only in the FFT variant");
     // loads first (m = 0 part, the first theta-table steps, the first phi
     // operands), then the m = 0 sums
     constexpr int D = 5;  // theta-table steps in flight
+    constexpr int T0 = G::u2off(S0), T1 = G::u2off(S1);  // the window's table steps
     const int sbase = pu * G::TU2 * 64 * 16;
     float s0v[G::NV0P];
-    m0_load(pu, s0v);
+    if constexpr (S0 == 0) m0_load(pu, s0v);
     float4 sring[D];
     cfor<0, D>([&](auto T) {
-      constexpr int tt = decltype(T)::value;
-      if constexpr (tt < G::TU2) sring[tt] = tload4_s(SPr, lane * 16, sbase + tt * 64 * 16);
+      constexpr int tt = T0 + decltype(T)::value;
+      if constexpr (tt < T1) sring[tt - T0] = tload4_s(SPr, lane * 16, sbase + tt * 64 * 16);
     });
     // synthesis operands twc[type][mb] of K-step 0 and the rotation by 8 phi_k
     const f4* seeds = reinterpret_cast<const f4*>(TWR + lane * TWRN);
@@ -285,14 +289,14 @@ struct WaveCtx {
         r8s[mb] = sd[6 * mb + 5];
       });
     }
-    float c1, c2;
-    m0_finish(s0v, c1, c2);
+    float c1 = 0.0f, c2 = 0.0f;
+    if constexpr (S0 == 0) m0_finish(s0v, c1, c2);
 
     // ---- 1 + 2a. theta synthesis feeding the phi-synthesis contractions
     f4 acc[2][NMB][4];  // [input][k block][type]
     // the FFT variant's packed spectrum of the lane's column node (see phi_fft)
     float2* const sc = spec + (8 * h + pi) * FGeo<L>::NS;
-    if constexpr (FFT) {
+    if constexpr (FFT && S0 == 0) {
       if (g == 0) sc[0] = make_float2(2.0f * c1, 2.0f * c2);
     }
     if constexpr (!FFT) cfor<0, NMB>([&](auto MB) {
@@ -306,7 +310,7 @@ struct WaveCtx {
     });
     float asd[NMR][4 * NMB];  // analysis seeds, read during the last K-step
     f4 ast[NMR];
-    cfor<0, NKS>([&](auto SS) {
+    cfor<S0, S1>([&](auto SS) {
       constexpr int s = decltype(SS)::value;
       // the x block of m-pair c = 4 s + g: xb(4 s + g) = xb(4 s) + g (4 nu(s) + 1)
       // - 2 g (g - 1), written so that only the g terms are left to run time
@@ -317,8 +321,8 @@ struct WaveCtx {
       f4 Vo = {0.0f, 0.0f, 0.0f, 0.0f}, Ve = Vo;
       cfor<0, G::nu(s) / 2>([&](auto U2) {
         constexpr int u2 = decltype(U2)::value, tt = G::u2off(s) + u2;
-        const float4 sv = sring[tt % D];
-        if constexpr (tt + D < G::TU2) sring[tt % D] = tload4_s(SPr, lane * 16, sbase + (tt + D) * 64 * 16);
+        const float4 sv = sring[(tt - T0) % D];
+        if constexpr (tt + D < T1) sring[(tt - T0) % D] = tload4_s(SPr, lane * 16, sbase + (tt + D) * 64 * 16);
         cfor<0, 2>([&](auto E) {
           constexpr int u = 2 * u2 + decltype(E)::value;
           const float so = E == 0 ? sv.x : sv.z, se = E == 0 ? sv.y : sv.w;
@@ -620,6 +624,128 @@ struct WaveCtx {
     if (cm == 0) column(N2 / 2);
   }
 };
+
+// The phi transforms of one pass by radix-2 FFTs, shared by the NTH threads
+// of a multi-wave workgroup (the L = 64 FFT kernel), one half pass at a time
+// (half h: the mirror pairs 4 h .. 4 h + 3, i.e. the columns 4 h + j and
+// 8 + 4 h + j, j < 4).  The steps of WaveCtx::phi_fft with 8 nodes: (1)
+// column tasks (node, n2), (2) row tasks (node, k1), their results first held
+// in registers so that T2 can take T's place, (3) forward column tasks
+// (pair, m2).  A holds the 16 columns' packed spectra; T the half's column
+// outputs, then its T2.  All NTH threads call it (it has barriers).
+template <int L>
+__device__ __forceinline__ void phi_fft_half(int tid, int half, float* eo, const float2* A, float2* T) {
+  using F = FGeo<L>;
+  using G = WGeo<L>;
+  constexpr int NF = F::NF, N1 = F::N1, N2 = F::N2, NS = F::NS, H2 = F::H2, TS = F::TS, T2S = F::T2S;
+  static_assert(8 * N2 <= G::NTH && 8 * N1 <= G::NTH, "one column or row task per thread");
+  auto col_of = [&](int nh) { return nh < 4 ? 4 * half + nh : 8 + 4 * half + (nh - 4); };
+  // 1. columns: node nh, n2
+  if (tid < 8 * N2) {
+    const int nh = tid & 7, n2 = tid >> 3;
+    const float2* sp = A + col_of(nh) * NS;
+    cpx a[N1];
+    cfor<0, N1>([&](auto M1) {
+      constexpr int lo = N2 * decltype(M1)::value, hi = lo + N2 - 1;
+      if constexpr (hi <= L) {
+        const float2 v = sp[lo + n2];
+        a[decltype(M1)::value] = {v.x, v.y};
+      } else if constexpr (lo >= NF - L) {
+        const float2 v = sp[NS - NF + lo + n2];
+        a[decltype(M1)::value] = {v.x, v.y};
+      } else if constexpr (lo <= L) {
+        const int n = lo + n2;
+        const float2 v = sp[n <= L ? n : 0];
+        a[decltype(M1)::value] = n <= L ? cpx{v.x, v.y} : cpx{0.0f, 0.0f};
+      } else if constexpr (hi >= NF - L) {
+        const int n = lo + n2;
+        const float2 v = sp[n >= NF - L ? NS - NF + n : 0];
+        a[decltype(M1)::value] = n >= NF - L ? cpx{v.x, v.y} : cpx{0.0f, 0.0f};
+      } else {
+        a[decltype(M1)::value] = {0.0f, 0.0f};
+      }
+    });
+    fft_reg<N1, +1>(a);
+    cpx w[N1];
+    cpowers<N1>(tw_root<NF>(n2), w);
+    float2* tp = T + nh * TS + n2;
+    cfor<0, N1>([&](auto K1) {
+      constexpr int k1 = decltype(K1)::value;
+      const cpx v = k1 == 0 ? a[0] : cmul(a[k1], w[k1]);
+      tp[k1 * N2] = make_float2(v.re, v.im);
+    });
+  }
+  __syncthreads();
+  // 2. rows: node nh, k1 -> forward outputs m2 <= N2 / 2 in registers
+  cpx X2[H2];
+  const int rnh = tid & 7, rk1 = tid >> 3;
+  if (tid < 8 * N1) {
+    const float2* tp = T + rnh * TS + rk1 * N2;
+    cpx a[N2];
+    cfor<0, N2>([&](auto M2) {
+      const float2 v = tp[decltype(M2)::value];
+      a[decltype(M2)::value] = {v.x, v.y};
+    });
+    fft_reg<N2, +1>(a);
+    float gv[N2];
+    cfor<0, N2>([&](auto K2) { gv[decltype(K2)::value] = a[decltype(K2)::value].re * a[decltype(K2)::value].im; });
+    rfft2_fwd<N2>(gv, X2);
+    cpx w[H2];
+    cpowers<H2>(cconj(tw_root<NF>(rk1)), w);
+    cfor<1, H2>([&](auto M2) { X2[decltype(M2)::value] = cmul(X2[decltype(M2)::value], w[decltype(M2)::value]); });
+  }
+  __syncthreads();  // every row of T is read: T2 takes its place
+  if (tid < 8 * N1) {
+    float2* t2 = T + rnh * T2S + rk1;
+    cfor<0, H2>([&](auto M2) { t2[decltype(M2)::value * N1] = make_float2(X2[decltype(M2)::value].re,
+                                                                           X2[decltype(M2)::value].im); });
+  }
+  __syncthreads();
+  // 3. forward columns: pair j (node j, mirror 4 + j), m2; threads 4 * H2
+  if (tid < 4 * H2) {
+    const int j = tid & 3, m2 = tid >> 2;
+    const int pp = 4 * half + j;
+    constexpr float scale = float(G::NP) / (8.0f * float(NF));
+    cpx bn[N1], bm[N1];
+    const float2* t2n = T + j * T2S + m2 * N1;
+    const float2* t2m = T + (4 + j) * T2S + m2 * N1;
+    cfor<0, N1>([&](auto K1) {
+      constexpr int k1 = decltype(K1)::value;
+      const float2 u = t2n[k1], v = t2m[k1];
+      bn[k1] = {u.x, u.y};
+      bm[k1] = {v.x, v.y};
+    });
+    fft_reg<N1, -1>(bn);
+    fft_reg<N1, -1>(bm);
+    float* es = eo + pp * G::NMP2;        // sum of the mirror nodes
+    float* ed = eo + (8 + pp) * G::NMP2;  // difference
+    auto emit = [&](int m, cpx xn, cpx xm) {
+      es[2 * m] = (xn.re + xm.re) * scale;
+      ed[2 * m] = (xn.re - xm.re) * scale;
+      if (m > 0) {
+        es[2 * m + 1] = -(xn.im + xm.im) * scale;
+        ed[2 * m + 1] = -(xn.im - xm.im) * scale;
+      }
+    };
+    cfor<0, N1>([&](auto M1) {
+      constexpr int m1 = decltype(M1)::value;
+      if constexpr (N2 * m1 <= L) {
+        const int m = N2 * m1 + m2;
+        if (m <= L) emit(m, bn[m1], bm[m1]);
+      }
+    });
+    if (m2 != 0 && 2 * m2 != N2) {
+      cfor<1, N1>([&](auto AA) {
+        constexpr int aa = decltype(AA)::value;
+        if constexpr (N2 * aa - N2 / 2 < L + 1) {
+          const int m = N2 * aa - m2;
+          if (m <= L) emit(m, cconj(bn[N1 - aa]), cconj(bm[N1 - aa]));
+        }
+      });
+    }
+  }
+  __syncthreads();
+}
 
 // x into the LDS image (quads x1 cos, x1 sin, x2 cos, x2 sin) by the NTH
 // threads of the workgroup: every load is issued before the first wait
@@ -964,13 +1090,143 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   if constexpr (PAD) zero_tail<K>(y, P, ko, tid, NTH);
 }
 
+// L = 64 with the phi transforms by radix-2 FFT: four waves per product
+// working on one pass at a time -- wave v synthesises the m-parts of K-steps
+// v and 7 - v of the pass's 16 columns into the shared spectra, the 256
+// threads run the FFT stages in two half passes (phi_fft_half) and
+// accumulate the theta analysis of the pass's 8 mirror pairs in registers
+// (thread tid owns the rows tri(tid, 0) and q = tid + 256 it, as in
+// k_full_wave4).  LDS: the x image, one pass's moments, the spectra and one
+// half pass's transposes (76.6 KB: two products per CU).
+template <int L, typename T1, typename T2, bool WGT>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_full_wave4_fft(
+    const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, DevTables t,
+    DegWeights wt) {
+  using G = WGeo<L>;
+  using F = FGeo<L>;
+  static_assert(G::NW == 4 && G::NKS == 8, "four waves, two K-steps each");
+  constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
+                NIT = G::NIT, EOP = G::EOP, NTH = G::NTH;
+  __shared__ __align__(16) float lds[G::XQ * 4 + EOP + 2 * (16 * F::NS + 8 * F::TS)];
+  float* const xs = lds;
+  float* const eo = lds + G::XQ * 4;
+  float2* const fa = reinterpret_cast<float2*>(eo + EOP);
+  float2* const ft = fa + 16 * F::NS;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  if (int64_t(blockIdx.x) >= n) return;  // whole-workgroup exit (one product per workgroup)
+  const int64_t P = xcd_product(blockIdx.x, n);
+  stage_x<L, WGT>(xs, x1, x2, P, tid, t.XMAP, wt);
+  const __amdgpu_buffer_rsrc_t WPr = table_rsrc(t.WP, (NIT + 1) * NTH * L);
+  float a0 = 0.0f, ac[NIT], as[NIT];
+  int er[NIT];
+  cfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    ac[it] = as[it] = 0.0f;
+    er[it] = 0;
+    const int q = tid + NTH * it;
+    if (q < NROW) {
+      int l, m;
+      row_lm(q, l, m);
+      er[it] = ((l + m) & 1) * 8 * NMP2 + 2 * m;
+    }
+  });
+  for (int pass = 0; pass < PASSES; ++pass) {
+    const int pu = __builtin_amdgcn_readfirstlane(pass);
+    {
+      int lnp = lane;
+      asm volatile("" : "+v"(lnp));
+      const WaveCtx<L> w(lnp, reinterpret_cast<const float4*>(xs), t);
+      f4 o[G::NMR][4];
+      float zz;
+      // K-step s has L / 2 - 4 s u-steps: wave v takes K-steps v and 7 - v,
+      // the same work for every wave
+      if (wave == 0) {
+        w.template pass<true, 0, 1>(pu, o, zz, fa);
+        w.template pass<true, 7, 8>(pu, o, zz, fa);
+      } else if (wave == 1) {
+        w.template pass<true, 1, 2>(pu, o, zz, fa);
+        w.template pass<true, 6, 7>(pu, o, zz, fa);
+      } else if (wave == 2) {
+        w.template pass<true, 2, 3>(pu, o, zz, fa);
+        w.template pass<true, 5, 6>(pu, o, zz, fa);
+      } else {
+        w.template pass<true, 3, 4>(pu, o, zz, fa);
+        w.template pass<true, 4, 5>(pu, o, zz, fa);
+      }
+    }
+    __syncthreads();  // the 16 spectra are complete
+    phi_fft_half<L>(tid, 0, eo, fa, ft);
+    phi_fft_half<L>(tid, 1, eo, fa, ft);
+    // theta analysis over this pass's pairs 8 pu + 1 .. 8 pu + 8
+    if (tid <= L) {
+      const float4 w0 = tload4_s(WPr, tid * L * 4 + pu * 32, NIT * NTH * L * 4);
+      const float4 w1 = tload4_s(WPr, tid * L * 4 + pu * 32 + 16, NIT * NTH * L * 4);
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      cfor<0, 8>([&](auto JJ) {
+        constexpr int jj = decltype(JJ)::value;
+        a0 = fmaf(wv[jj], eo[(tid & 1) * 8 * NMP2 + jj * NMP2], a0);
+      });
+    }
+    cfor<0, NIT>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      if (tid + NTH * it < NROW) {
+        const float4 w0 = tload4_s(WPr, tid * L * 4 + pu * 32, it * NTH * L * 4);
+        const float4 w1 = tload4_s(WPr, tid * L * 4 + pu * 32 + 16, it * NTH * L * 4);
+        const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+        cfor<0, 8>([&](auto JJ) {
+          constexpr int jj = decltype(JJ)::value;
+          const f2 cs = *reinterpret_cast<const f2*>(eo + er[it] + jj * NMP2);
+          ac[it] = fmaf(wv[jj], cs.x, ac[it]);
+          as[it] = fmaf(wv[jj], cs.y, as[it]);
+        });
+      }
+    });
+    __syncthreads();  // the next pass rewrites the spectra and the moments
+  }
+  // poles (only the m = 0 parts are non-zero there) and the stores
+  float p1, p2;
+  {
+    const WaveCtx<L> w(lane, reinterpret_cast<const float4*>(xs), t);
+    float sv[G::NV0P];
+    w.m0_load(PASSES, sv);
+    w.m0_finish(sv, p1, p2);  // h = 0 lanes: north pole, h = 1 lanes: south pole
+  }
+  const float f = p1 * p2 * float(NP);
+  const float fN = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 0));
+  const float fS = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 8));
+  if (tid <= L) {
+    const int l = tid;
+    const __amdgpu_buffer_rsrc_t Wr = table_rsrc(t.WT, NJ * t.ntW);
+    a0 = fmaf(tload(Wr, (l * (l + 1) / 2) * 4), fN + ((l & 1) ? -fS : fS), a0);
+    if constexpr (WGT) {
+      if (wt.wo) a0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
+    }
+    y[P * K + l * l + l] = a0;
+  }
+  cfor<0, NIT>([&](auto IT) {
+    constexpr int it = decltype(IT)::value;
+    const int q = tid + NTH * it;
+    if (q < NROW) {
+      int l, m;
+      row_lm(q, l, m);
+      float wl = 1.0f;
+      if constexpr (WGT) {
+        if (wt.wo) wl = wt.wo[weight_row(wt, P) * (L + 1) + l];
+      }
+      y[P * K + l * l + l + m] = ac[it] * wl;
+      y[P * K + l * l + l - m] = as[it] * wl;
+    }
+  });
+}
+
 template <int L, typename T1, typename T2, bool WGT, bool PAD = false>
 hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y, const DevTables& t,
                              const DegWeights& wt, hipStream_t s, int k1 = WGeo<L>::K, int k2 = WGeo<L>::K,
                              int ko = WGeo<L>::K) {
   // the radix-FFT phi transforms where the plan asks for them and a
   // one-wave kernel exists (L = 16, 32)
-  const bool fft = t.phi_fft != 0 && WGeo<L>::NW == 1;
+  const bool fft = t.phi_fft != 0;
   using G = WGeo<L>;
   // at most 2^30 workgroups per launch
   for (int64_t p0 = 0; p0 < n; p0 += (int64_t(1) << 30)) {
@@ -987,6 +1243,9 @@ hipError_t launch_wave_typed(const void* x1, const void* x2, int64_t n, float* y
       else
         hipLaunchKernelGGL((k_full_wave<L, T1, T2, WGT, false, PAD>), dim3(unsigned(nn)), dim3(64), 0, s, a, b, yy, nn,
                            t, w, k1, k2, ko);
+    } else if (fft && !PAD) {
+      hipLaunchKernelGGL((k_full_wave4_fft<L, T1, T2, WGT>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t,
+                         w);
     } else {
       hipLaunchKernelGGL((k_full_wave4<L, T1, T2, WGT, PAD>), dim3(unsigned(nn)), dim3(G::NTH), 0, s, a, b, yy, nn, t,
                          w, k1, k2, ko);
