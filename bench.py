@@ -167,8 +167,28 @@ KERNEL_SOURCES = {
 }
 
 
-def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto"):
+# degree triples with a thread-per-product kernel of their own
+OWN_SMALL_TRIPLES = {(a, a, a) for a in range(1, 9)} | {(2, 2, 3), (3, 2, 3), (1, 2, 2), (2, 1, 3)}
+
+
+def padded_kernel(L1: int, L2: int, Lout: int):
+    """(kernel, roofline bound, source file) that runs a degree triple with no
+    kernel of its own: the dot product for Lout = 0, else the equal-degree
+    kernel of the padded degree A = max(L1, L2, min(Lout, L1 + L2))."""
+    if Lout == 0:
+        return "k_dot0", "hbm", "gtp_generic.hip"
+    A = max(1, L1, L2, min(Lout, L1 + L2))
+    if A <= 8:
+        return f"k_full_small_pad<{A}>", "alu", "gtp_small.hip"
+    W = 16 if A <= 16 else (32 if A <= 32 else 64)
+    return ("k_full_wave4" if W > 32 else "k_full_wave") + f" (padded to L = {W})", "mfma", "gtp_wave.hip"
+
+
+def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto", degrees=None):
     """(kernel, roofline bound, source file) of the kernel that dominates a workload."""
+    if degrees is not None and workload == "sweep" and conv == "auto" and tuple(degrees) not in OWN_SMALL_TRIPLES \
+            and not (degrees[0] == degrees[1] == degrees[2] and degrees[0] in (16, 32, 64)):
+        return padded_kernel(*degrees)
     if conv == "fft" and workload in ("sweep", "highdeg") and L in (16, 32, 64):
         return ("k_full_wave4_fft" if L > 32 else "k_full_wave (FFT)"), "alu", "gtp_wave.hip"
     if escn:
@@ -193,7 +213,9 @@ def kernel_sources_sha(kernel_source: str) -> str:
     return h.hexdigest()[:16]
 
 
-def traffic_key(workload: str, L: int) -> str:
+def traffic_key(workload: str, L: int, degrees=None) -> str:
+    if workload == "sweep" and degrees is not None and len(set(degrees)) > 1:
+        return "sweep_{}_{}_{}".format(*degrees)
     return f"sweep_L{L}" if workload == "sweep" else workload
 
 
@@ -580,11 +602,13 @@ def main():
     if alg_flops:
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
-        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn, args.conv)
+        degs = (desc["L1"], desc["L2"], desc["Lout"]) if "L2" in desc else None
+        kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn, args.conv,
+                                             degs)
         suffix = "_backward" if args.backward else ("_weighted" if args.weighted else ("_escn" if args.escn else ""))
         if args.conv != "auto":
             suffix += "_" + args.conv
-        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0)) + suffix, ksrc)
+        tb = load_traffic(traffic_key(args.workload, desc.get("L1", 0), degs) + suffix, ksrc)
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         comp = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "alg_flops_per_product": alg_flops,
