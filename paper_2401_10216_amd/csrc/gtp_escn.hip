@@ -223,6 +223,10 @@ __device__ __forceinline__ void load_drow(const float* Dl, float4 (&buf)[NQ]) {
 
 // register budget per lane: 3 waves per SIMD up to L = 6, 2 above
 constexpr int escn_waves(int L) { return L <= 6 ? 3 : 2; }
+// LDS stride of the x / y rows each lane reads or writes as its own: odd, so
+// that one column of the 64 rows lies in 64 distinct banks (K = (L + 1)^2 is
+// a multiple of 4 for odd L)
+constexpr int escn_stride(int k) { return k | 1; }
 
 template <int L, typename TIn>
 __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(L)))) void k_conv_escn(
@@ -232,7 +236,8 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   constexpr int K = ensh(L), H = L + 1, NPAIR = EG::NPAIR;
   static_assert(EscnConsts<L>::NPAIR == NPAIR && EscnConsts<L>::ERL == EG::ERL, "node-pair table layout");
   constexpr int DS = dofs(L + 1);
-  constexpr int XT = kEW * K;  // x / y tile
+  constexpr int S = escn_stride(K);
+  constexpr int XT = kEW * S;  // x / y tile
   // once the x rows are in registers the tile's space holds D (16-byte rows)
   static_assert(DS % 4 == 0 && DS <= XT, "LDS layout");
   constexpr int ND4 = DS / 4, RD = (ND4 + kEW - 1) / kEW;
@@ -258,8 +263,8 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   float v[K];
   bool staged = false;
   if constexpr (std::is_same<TIn, float>::value) {
-    if (dma && cnt == kEW && ((p0 * K) & 3) == 0) {
-      // the slab is laid out as the tile: coalesced 16-byte loads straight
+    if (S == K && dma && cnt == kEW && ((p0 * K) & 3) == 0) {
+      // (odd K) the slab is laid out as the tile: coalesced 16-byte loads straight
       // into LDS (lane q 64 + tid carries floats 4 (q 64 + tid) .. + 3); a
       // whole number of 16-byte runs (64 K floats) from a 16-byte aligned
       // start (base checked by the host, offset here)
@@ -306,11 +311,16 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   if (staged) {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the slab is in LDS
   } else {
-    cfor<0, K>([&](auto I) { tile[tid + decltype(I)::value * kEW] = v[decltype(I)::value]; });
+    cfor<0, K>([&](auto I) {
+      // slab element i is row i / K, column i % K of the tile
+      const int i = tid + decltype(I)::value * kEW;
+      const int r = i / K;
+      tile[r * S + (i - r * K)] = v[decltype(I)::value];
+    });
   }
   __syncthreads();
   float xr[K];
-  cfor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * K + decltype(I)::value]; });
+  cfor<0, K>([&](auto I) { xr[decltype(I)::value] = tile[tid * S + decltype(I)::value]; });
   __syncthreads();
   cfor<0, RD>([&](auto I) {
     constexpr int q = decltype(I)::value;
@@ -413,7 +423,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
 
   // ---- 6. store through the tile (coalesced)
   __syncthreads();  // every lane is done with D and the table
-  cfor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = yv[decltype(I)::value]; });
+  cfor<0, K>([&](auto I) { tile[tid * S + decltype(I)::value] = yv[decltype(I)::value]; });
   __syncthreads();
   // store indices from an opaque copy of the lane id: not kept alive from the
   // loads' index arithmetic
@@ -427,12 +437,22 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
     constexpr int N4 = kEW * K / 4, NQ = (N4 + kEW - 1) / kEW;
     cfor<0, NQ>([&](auto Q) {
       const int i4 = ln + decltype(Q)::value * kEW;
-      if (i4 < N4) reinterpret_cast<sv4*>(yb)[i4] = reinterpret_cast<const sv4*>(tile)[i4];
+      if (i4 < N4) {
+        if constexpr (S == K) {
+          reinterpret_cast<sv4*>(yb)[i4] = reinterpret_cast<const sv4*>(tile)[i4];
+        } else {
+          // padded rows; K is a multiple of 4, so no 16-byte run crosses a row
+          const int r = (4 * i4) / K;
+          const float* const t = tile + r * S + (4 * i4 - r * K);
+          reinterpret_cast<sv4*>(yb)[i4] = sv4{t[0], t[1], t[2], t[3]};
+        }
+      }
     });
   } else {
     cfor<0, K>([&](auto I) {
       const unsigned i = unsigned(ln + decltype(I)::value * kEW);
-      if (i < nx) yb[i] = tile[i];
+      const unsigned r = i / unsigned(K);
+      if (i < nx) yb[i] = tile[r * S + (i - r * K)];
     });
   }
 }

@@ -36,6 +36,11 @@ constexpr int cdeg(int i) {
 constexpr int csh(int L) { return (L + 1) * (L + 1); }
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
 constexpr int cmax(int a, int b) { return a > b ? a : b; }
+// LDS row stride of K-float rows that each lane reads or writes as its own
+// row: odd, so that one column of the 64 lanes' rows falls in 64 distinct
+// banks.  K = (L + 1)^2 is even (a multiple of 4) for odd L, where a stride
+// of K put every lane's element i in one bank.
+constexpr int lds_stride(int k) { return k | 1; }
 
 // Coefficient accessors of one lane's input vector: in registers, or a row of
 // the workgroup's LDS tile.  touch() makes the LDS row offset opaque so the
@@ -582,21 +587,36 @@ __device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0,
 template <int KO, int KE>
 __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, int cnt, float* tile,
                                            const float (&acc)[KE]) {
+  constexpr int SO = lds_stride(KO);
   const int tid = threadIdx.x;
   cfor<0, KO>([&](auto I) {
     constexpr int i = decltype(I)::value;
-    tile[tid * KO + i] = (i < KE) ? acc[i < KE ? i : 0] : 0.0f;
+    tile[tid * SO + i] = (i < KE) ? acc[i < KE ? i : 0] : 0.0f;
   });
   __syncthreads();
   float* out = y + p0 * KO;
+  typedef float sv4 __attribute__((ext_vector_type(4)));
   if (cnt == kTile && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
     // a full workgroup's rows are 64 KO floats, a whole number of 16-byte
-    // runs: 16-byte stores (the tile is 16-byte aligned)
-    typedef float sv4 __attribute__((ext_vector_type(4)));
+    // runs: 16-byte stores
     constexpr int N4 = kTile * KO / 4;
-    for (int i = tid; i < N4; i += kTile) reinterpret_cast<sv4*>(out)[i] = reinterpret_cast<const sv4*>(tile)[i];
+    if constexpr (SO == KO) {
+      // compact rows: the tile (16-byte aligned) is the output's layout
+      for (int i = tid; i < N4; i += kTile) reinterpret_cast<sv4*>(out)[i] = reinterpret_cast<const sv4*>(tile)[i];
+    } else {
+      // padded rows; KO is a multiple of 4, so no 16-byte run crosses a row
+      static_assert(KO % 4 == 0, "even row lengths are (2m)^2");
+      for (int i = tid; i < N4; i += kTile) {
+        const int r = (4 * i) / KO, c = 4 * i - r * KO;
+        const float* const t = tile + r * SO + c;
+        reinterpret_cast<sv4*>(out)[i] = sv4{t[0], t[1], t[2], t[3]};
+      }
+    }
   } else {
-    for (int i = tid; i < cnt * KO; i += kTile) out[i] = tile[i];
+    for (int i = tid; i < cnt * KO; i += kTile) {
+      const int r = i / KO;
+      out[i] = tile[r * SO + (i - r * KO)];
+    }
   }
 }
 
@@ -617,7 +637,8 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
                                                       PairIdx pi, int dma) {
   using G = Geo<L1, L2, LO, NU>;
   constexpr int K1 = csh(L1), K2 = NU == 0 ? csh(L2) : 1, KO = csh(LO);
-  constexpr int KT = cmax(cmax(K1, K2), KO);
+  constexpr int S2 = lds_stride(K2);
+  constexpr int KT = cmax(S2, lds_stride(KO));
   __shared__ __align__(16) float tile[kTile * KT];
   const int tid = threadIdx.x;
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
@@ -626,7 +647,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
   float acc[G::KE];
   if constexpr (NU == 0) {
     // each lane loads its own two rows, x1 into registers and x2 into its
-    // tile row (row-major, odd row length: conflict-free reads); a wave's
+    // tile row (row-major, odd row stride: conflict-free reads); a wave's
     // rows are contiguous, so every cache line still comes from HBM once.
     // Lanes past the end repeat the last product.  Outer-product indexing
     // (pair products of channel mixing) takes rows b C1 + c1 and b C2 + c2.
@@ -640,7 +661,8 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     // (measured: 2.4 % faster at L = 6; at L = 4 4 % and at L = 8 1 % slower
     // than the per-lane loads, so degrees 5..7 only.  Staging x1 the same way,
     // through the tile before x2, measured 1 % slower at L = 6.)
-    if constexpr (std::is_same<T2, float>::value && !OUT && L2 >= 5 && L2 <= 7) {
+    // (odd row lengths only: the slab's layout is the compact one)
+    if constexpr (std::is_same<T2, float>::value && !OUT && L2 >= 5 && L2 <= 7 && S2 == K2) {
       if (dma && cnt == kTile) {
         // a full workgroup's x2 rows are one contiguous slab laid out as the
         // tile: coalesced 16-byte loads straight into LDS (lane q 64 + tid
@@ -662,7 +684,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
       }
     }
     if (!staged)
-      cfor<0, K2>([&](auto I) { tile[tid * K2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+      cfor<0, K2>([&](auto I) { tile[tid * S2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
     if constexpr (WGT) {
       // each lane scales its own product: x1 in registers, x2 in its tile row
       const int64_t row = weight_row(wt, p0 + tid);
@@ -670,10 +692,10 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
         scale_by_degree<L1, K1>(wt.w1 + row * (L1 + 1), [&](auto I) -> float& { return xa[decltype(I)::value]; });
       if (wt.w2)
         scale_by_degree<L2, K2>(wt.w2 + row * (L2 + 1),
-                                [&](auto I) -> float& { return tile[tid * K2 + decltype(I)::value]; });
+                                [&](auto I) -> float& { return tile[tid * S2 + decltype(I)::value]; });
     }
     RegX<K1> A{xa};
-    LdsX B{tile, tid * K2};
+    LdsX B{tile, tid * S2};
     gtp_core<L1, L2, LO, NU>(A, B, acc, ST, ntS, WT, ntW);
     if constexpr (WGT) {
       // outputs above degree LE are zeros and stay zeros
@@ -705,8 +727,8 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
 template <int L, typename T1, typename T2>
 __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L, L, L)))) void k_full_small_pad(
     const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, int k1, int k2, int ko) {
-  constexpr int K = csh(L);
-  __shared__ __align__(16) float tile[kTile * K];
+  constexpr int K = csh(L), S = lds_stride(K);
+  __shared__ __align__(16) float tile[kTile * S];
   const int tid = threadIdx.x;
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
@@ -746,11 +768,11 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
       xb[i] = i < k2 ? v : 0.0f;
     });
     __syncthreads();
-    cfor<0, K>([&](auto I) { tile[tid * K + decltype(I)::value] = xb[decltype(I)::value]; });
+    cfor<0, K>([&](auto I) { tile[tid * S + decltype(I)::value] = xb[decltype(I)::value]; });
   }
   float acc[K];
   RegX<K> A{xa};
-  LdsX B{tile, tid * K};
+  LdsX B{tile, tid * S};
   gtp_core<L, L, L, 0>(A, B, acc, nullptr, 0, nullptr, 0);
   __syncthreads();
   if (ko <= K) {
@@ -775,7 +797,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   constexpr int K = csh(L), KO = csh(LO);
   using G1 = Geo<L, L, LO, 0>;
   using G2 = Geo<LO, L, LO, 0>;
-  constexpr int KT = cmax(K, KO);
+  constexpr int KT = lds_stride(KO);  // the output rows (store_rows)
   __shared__ __align__(16) float tile[kTile * KT];
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
@@ -884,8 +906,8 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
     int64_t C1, int64_t C2, int Co, int64_t P, const float* __restrict__ ST, int ntS, const float* __restrict__ WT,
     int ntW) {
   constexpr int Kd = csh(L);
-  constexpr int NKT = (Kd + 15) / 16, KTW = (NKT + 3) / 4, CoB = 16 * NCT;
-  __shared__ float tile[kMixThreads * Kd];
+  constexpr int NKT = (Kd + 15) / 16, KTW = (NKT + 3) / 4, CoB = 16 * NCT, KS = lds_stride(Kd);
+  __shared__ float tile[kMixThreads * KS];
   const int64_t b = blockIdx.x;
   const int64_t nround = (P + kMixThreads - 1) / kMixThreads;
   for (int64_t r = 0; r < nround; ++r) {
@@ -903,13 +925,13 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
       const TIn* const xr2 = x2 + (b * C2 + c2) * Kd;
       float xa[Kd], acc[Kd];
       cfor<0, Kd>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
-      cfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+      cfor<0, Kd>([&](auto I) { tile[tid * KS + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
       RegX<Kd> A{xa};
-      LdsX Bx{tile, tid * Kd};
+      LdsX Bx{tile, tid * KS};
       gtp_core<L, L, L, 0>(A, Bx, acc, ST, ntS, WT, ntW);
       // over the lane's own row (its x2 reads are done).  Slots past P hold
       // a copy of the last pair's product; their weight rows are zero.
-      cfor<0, Kd>([&](auto I) { tile[tid * Kd + decltype(I)::value] = acc[decltype(I)::value]; });
+      cfor<0, Kd>([&](auto I) { tile[tid * KS + decltype(I)::value] = acc[decltype(I)::value]; });
     }
     // this wave's partial sums of the previous rounds (output rows k0 + 4 g +
     // rr of channel 16 ct + i) and its first weight block, requested before
@@ -943,7 +965,7 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
           float a[4];
 #pragma unroll
           for (int sp = 0; sp < 4; ++sp) {
-            const float v = tile[(16 * q + 4 * sp + g) * Kd + ka];
+            const float v = tile[(16 * q + 4 * sp + g) * KS + ka];
             a[sp] = kok ? v : 0.0f;
           }
           const int qn = q + 1 < 16 ? q + 1 : q;
