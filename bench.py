@@ -1,6 +1,6 @@
 """Benchmark of the Gaunt tensor product hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload edge|tiny|manybody|sweep|highdeg|mix] [--L L]
+    python bench.py [--steps K] [--warmup W] [--workload edge|edge16|tiny|manybody|sweep|highdeg|mix] [--L L]
                     [--backward | --weighted] [--no-cpu-baseline] [--gpus 1]
 
 Default: the edge workload (B=65536 edges x C=128 channels, L1=L2=Lout=6,
@@ -164,6 +164,7 @@ KERNEL_SOURCES = {
     "gtp_small.hip": ["gen_small_consts.cpp"],
     "gtp_escn.hip": ["gen_small_consts.cpp", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
     "gtp_wave.hip": ["gtp_fft.hpp"],
+    "gtp_escn_wave.hip": ["gtp_escn.hip", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
 }
 
 
@@ -193,11 +194,13 @@ def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto
         return ("k_full_wave4_fft" if L > 32 else "k_full_wave (FFT)"), "alu", "gtp_wave.hip"
     if escn:
         # both kernels of the step (rotation matrices, then the product): one unit
+        if L == 16:
+            return "k_escn_rot+k_conv_escn_wave", "mfma", "gtp_escn_wave.hip"
         return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
     if workload == "mix":
         # pair products (thread per product) and the mix on the matrix cores in one kernel
         return "k_mix_fused", "alu", "gtp_small.hip"
-    if workload in ("sweep", "highdeg") and (L >= 16 or workload == "highdeg"):
+    if workload in ("sweep", "highdeg", "edge16") and (L >= 16 or workload == "highdeg"):
         return ("k_full_wave4" if L > 32 else "k_full_wave"), "mfma", "gtp_wave.hip"
     if workload == "manybody":
         return "k_self_stepwise_small", "alu", "gtp_small.hip"
@@ -285,9 +288,11 @@ def make_workload(args, torch, gtp, inputs):
     """Returns (step callable, products per step, description dict, alg flops, alg bytes, oracle sample fn)."""
     dev = torch.device("cuda:0")
     w = args.workload
-    if w == "edge":
-        B, C, L = 65536, 128, 6
-        x1, r, h = inputs.edge_inputs(B, C, L)
+    if w in ("edge", "edge16"):
+        # edge16: the edge shape at L = 16 with 8192 edges (1.2 GB per
+        # coefficient tensor)
+        B, C, L = (65536, 128, 6) if w == "edge" else (8192, 128, 16)
+        x1, r, h = inputs.edge_inputs(B, C, L, index=2 if w == "edge" else 7)
         t1 = torch.from_numpy(x1).to(dev)
         tr = torch.from_numpy(r.astype("float32")).to(dev)
         th = torch.from_numpy(h).to(dev)
@@ -295,7 +300,7 @@ def make_workload(args, torch, gtp, inputs):
         del th
         plan = gtp.Plan(L, L, L)
         y = torch.empty((B, C, nsh(L)), dtype=torch.float32, device=dev)
-        step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, 2)
+        step, result, oracle_of, _ = pair_step(args, torch, gtp, inputs, plan, t1, t2, y, 2 if w == "edge" else 7)
         if args.escn:
             # the same product from (x1, r, h) in the edge's rotated frame
             del t2
@@ -311,23 +316,23 @@ def make_workload(args, torch, gtp, inputs):
             bref = h[bi, ci][:, deg] * O.real_sh_xyz(L, r[bi])
             return oracle_of(O, idx, a, bref), result
 
-        desc = {"workload": "edge: B=65536 edges x C=128 channels, L1=L2=Lout=6, x1~N(0,1), "
+        desc = {"workload": f"{w}: B={B} edges x C={C} channels, L1=L2=Lout={L}, x1~N(0,1), "
                             "x2 = h[b,c,l] * Y_lm(r_b), r_b uniform on S^2, h~N(0,1)",
                 "B": B, "C": C, "L1": L, "L2": L, "Lout": L, "in_dtype": "f32"}
         if args.escn:
             desc["workload"] += "; gtp_conv_escn from (x1, r, h): rotated edge frame, m = 0 filter"
             # per product: rotation in (sum (2l+1)^2 FMA), zonal theta product, rotation out;
             # bytes: x1 and y, h, and the edge vector shared by C channels
-            return step, B * C, desc, (escn_flops(L, C), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
-                oracle_sample, 2
-        return step, B * C, desc, (kernel_flops(L, L, L), SURVEY_FLOPS[6]), 4 * (2 * nsh(L) + nsh(L)), \
-            oracle_sample, 2
+            return step, B * C, desc, (escn_flops(L, C), SURVEY_FLOPS[L]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
+                oracle_sample, 2 if w == "edge" else 7
+        return step, B * C, desc, (kernel_flops(L, L, L), SURVEY_FLOPS[L]), 4 * (2 * nsh(L) + nsh(L)), \
+            oracle_sample, 2 if w == "edge" else 7
     if (args.backward or args.weighted) and w not in ("edge", "tiny", "sweep", "highdeg"):
         raise SystemExit("--backward / --weighted apply to the pair workloads (edge, tiny, sweep, highdeg)")
     if args.backward and args.weighted:
         raise SystemExit("--backward and --weighted are separate benchmarks")
-    if args.escn and (w != "edge" or args.backward or args.weighted):
-        raise SystemExit("--escn applies to the edge workload's forward product")
+    if args.escn and (w not in ("edge", "edge16") or args.backward or args.weighted):
+        raise SystemExit("--escn applies to the edge workloads' forward product")
     if w in ("tiny", "sweep", "highdeg"):
         if w == "tiny":
             B, C, L, idx_cfg = 1024, 1, 2, 1

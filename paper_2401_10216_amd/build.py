@@ -20,7 +20,8 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgtp.so")
 
-HIP_SOURCES = ["gtp_api.hip", "gtp_small.hip", "gtp_wave.hip", "gtp_generic.hip", "gtp_escn.hip", "gtp_mix.hip",
+HIP_SOURCES = ["gtp_api.hip", "gtp_small.hip", "gtp_wave.hip", "gtp_generic.hip", "gtp_escn.hip", "gtp_escn_wave.hip",
+               "gtp_mix.hip",
                "gtp_probe.hip", "gtp_wgrad.hip"]
 CPP_SOURCES = ["gtp_tables.cpp", "gtp_escn_tables.cpp"]
 ARCH = "gfx950"

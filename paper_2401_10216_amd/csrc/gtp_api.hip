@@ -154,7 +154,7 @@ gtp_status upload(gtp_plan_* p, long fail_at) {
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
   d.phi_fft = p->conv == GTP_CONV_FFT ? 1 : 0;
-  p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0};
+  p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0, nullptr, nullptr};
   if (p->esc.NPAIR) {
     gtp::EscnDev& ed = p->escd;
     if ((s = up(&p->esc.J, nullptr, &ed.J)) != GTP_OK) return s;
@@ -162,6 +162,10 @@ gtp_status upload(gtp_plan_* p, long fail_at) {
     ed.LM = p->esc.LM;
     ed.NPAIR = p->esc.NPAIR;
     ed.ERL = p->esc.ERL;
+    if (!p->esc.A.empty()) {
+      if ((s = up(&p->esc.A, nullptr, &ed.A)) != GTP_OK) return s;
+      if ((s = up(&p->esc.Z, nullptr, &ed.Z)) != GTP_OK) return s;
+    }
   }
   if (t.waveL) {
     if ((s = up(&t.TWR, nullptr, &d.TWR)) != GTP_OK) return s;
@@ -224,8 +228,10 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
   try {
     if (fail_host) throw std::bad_alloc();
     p->tab = gtp::build_tables(L1, L2, Lout);
-    // the rotated-frame convolution kernel exists for equal degrees <= 8
-    if (L1 == L2 && L2 == Lout && L1 >= 1 && L1 <= 8) p->esc = gtp::build_escn_tables(p->tab);
+    // the rotated-frame convolution kernels exist for equal degrees <= 8
+    // and 16 (degrees 9..15 run on a 16-plan's tables)
+    if (L1 == L2 && L2 == Lout && ((L1 >= 1 && L1 <= 8) || L1 == gtp::kEscnWaveL))
+      p->esc = gtp::build_escn_tables(p->tab);
   } catch (const std::bad_alloc&) {
     return fail(GTP_ERR_ALLOC, "table allocation failed");
   } catch (const std::exception& e) {
@@ -954,7 +960,9 @@ gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
     }
     case 10: src = &p->esc.J; break;
     case 11: src = &p->esc.E; break;
-    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..11");
+    case 12: src = &p->esc.A; break;
+    case 13: src = &p->esc.Z; break;
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..13");
   }
   if (!buf) {
     *count = int64_t(src->size());

@@ -111,6 +111,41 @@ EscnHost build_escn_tables(const Tables& t) {
       off += pad4(L + 1 - m);
     }
   }
+
+  // ---- A, Z: operand images of the matrix-core kernel (layouts in the header)
+  if (L == kEscnWaveL && e.NPAIR == L + 1) {
+    auto S = [&](int l, int m, int j) { return l <= L ? t.S[size_t(tri(l, m)) * t.NJ + j] : 0.0; };
+    auto CW = [&](int l, int m, int j) {
+      return l <= L ? (m == 0 ? double(t.NP) : 0.5 * t.NP) * t.W[size_t(tri(l, m)) * t.NJ + j] : 0.0;
+    };
+    e.A.assign(size_t(escn_wave_moff(L, L + 1)), 0.0);
+    for (int m = 0; m <= L; ++m) {
+      const int n = L + 1 - m, ne = (n + 1) / 2, no = n / 2, ke = (ne + 3) / 4, ko = (no + 3) / 4;
+      const int nl = escn_wave_lane_floats(L, m);
+      for (int lane = 0; lane < 64; ++lane) {
+        const int k = lane / 16, i = lane % 16, pj = 4 * (i % 4) + i / 4 + 1;
+        double* v = e.A.data() + escn_wave_moff(L, m) + size_t(lane) * nl;
+        int q = 0;
+        for (int s = 0; s < ke; ++s) v[q++] = S(m + 2 * (4 * s + k), m, pj);
+        for (int s = 0; s < ko; ++s) v[q++] = S(m + 1 + 2 * (4 * s + k), m, pj);
+        for (int r = 0; r < 4; ++r) v[q++] = i < ne ? CW(m + 2 * i, m, 4 * r + k + 1) : 0.0;
+        if (no > 0)
+          for (int r = 0; r < 4; ++r) v[q++] = i < no ? CW(m + 1 + 2 * i, m, 4 * r + k + 1) : 0.0;
+      }
+    }
+    e.Z.assign(size_t(escn_wave_zfloats(L)), 0.0);
+    for (int g = 0; g < 4; ++g)
+      for (int r = 0; r < 4; ++r) {
+        const int j = 4 * r + g + 1;
+        for (int l = 0; l <= L; ++l) e.Z[size_t(4 * g + r) * (L + 1) + l] = e.E[size_t(j) * e.ERL + l];
+      }
+    double* zp = e.Z.data() + 16 * (L + 1);
+    for (int l = 0; l <= L; ++l) {
+      zp[l] = e.E[l];                // pole pair: the unit filter
+      zp[L + 1 + l] = S(l, 0, 0);    // Theta_l0(0)
+      zp[2 * (L + 1) + l] = CW(l, 0, 0);
+    }
+  }
   return e;
 }
 

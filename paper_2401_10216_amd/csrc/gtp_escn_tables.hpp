@@ -26,13 +26,44 @@ namespace gtp {
 //        function is NP a_0, NP / 2 a_m).  The mirror node NT - j takes the
 //        factor (-1)^(l + m) of both Theta and W.  Built for L1 = L2 = Lout
 //        only (NT = 2L + 1 is odd: no equator node).
+//   A, Z: the operand images of the matrix-core kernel (L = kEscnWaveL only;
+//        empty otherwise).  A holds, per order m = 0..L, escn_wave_steps(L, m)
+//        operands of the 16x16x4 contractions for each of the 64 lanes (lane
+//        16 k + i, a block of escn_wave_lane_floats(L, m) floats per lane,
+//        blocks at escn_wave_moff(L, m)):
+//          synthesis, even then odd set (l - m even / odd; K-steps of four
+//          degrees, lane row i = node pair 4 (i % 4) + i / 4 + 1, K index k =
+//          the degree m + par + 2 (4 s + k)): Theta_lm(t_j);
+//          analysis, even then odd set (4 K-steps each: row i = the degree
+//          m + par + 2 i, K index k = node pair 4 r + k + 1): c_m W[tri(l, m)][j];
+//        zero where the degree exceeds L.  Z holds the unit zonal filter
+//        Theta_l0(0) Theta_l0(t_j) at the node pairs 4 r + g + 1 of lane
+//        group g (Z[(g 4 + r)(L + 1) + l]), then three rows of L + 1 values
+//        at the pole pair: the filter, Theta_l0(0) and c_0 W[tri(l, 0)][0].
 struct EscnHost {
   int LM = 0, NPAIR = 0, ERL = 0;
-  std::vector<double> J, E;
+  std::vector<double> J, E, A, Z;
 };
 
+// Degree of the matrix-core rotated-frame kernel: 16 interior node pairs,
+// one per row of a 16 x 16 tile.
+constexpr int kEscnWaveL = 16;
+// K-steps of order m: synthesis over the even and odd degree sets, then 4
+// analysis steps per non-empty set.
+constexpr int escn_wave_steps(int L, int m) {
+  const int n = L + 1 - m, ne = (n + 1) / 2, no = n / 2;
+  return (ne + 3) / 4 + (no + 3) / 4 + 4 + (no > 0 ? 4 : 0);
+}
+constexpr int escn_wave_lane_floats(int L, int m) { return (escn_wave_steps(L, m) + 3) / 4 * 4; }
+constexpr int escn_wave_moff(int L, int m) {
+  int o = 0;
+  for (int k = 0; k < m; ++k) o += 64 * escn_wave_lane_floats(L, k);
+  return o;
+}
+constexpr int escn_wave_zfloats(int L) { return 16 * (L + 1) + 3 * (L + 1); }
+
 // Builds the tables from a plan's tables; empty (NPAIR = 0) unless
-// L1 = L2 = Lout.
+// L1 = L2 = Lout; A and Z only for L1 = kEscnWaveL.
 EscnHost build_escn_tables(const Tables& t);
 
 }  // namespace gtp

@@ -1,0 +1,181 @@
+"""Host replay of the degree-16 matrix-core rotated-frame convolution.
+
+The kernel's data flow, written out in numpy fp64 with the operand images the
+plan exports (tables 12 and 13 of gtp_plan_table) and the 16x16x4 contraction
+semantics of the matrix cores (A[i][k] from lane 16 k + i, B[k][j] from lane
+16 k + j, register r of lane 16 g + i = row 4 g + r, column i).  It checks the
+image layouts and the stage-to-stage register conventions against the oracle's
+rotated-frame convolution (Sec. 3.3, eq. sh2fs-escn) on the CPU, and the
+images themselves against the plan's theta tables (S, W).
+"""
+import numpy as np
+import pytest
+
+from oracle import gtp_oracle as O
+from paper_2401_10216_amd import gtp
+
+L = 16
+H = L + 1
+
+
+def tri(l, m):
+    return l * (l + 1) // 2 + m
+
+
+def steps(m):
+    n = L + 1 - m
+    ne, no = (n + 1) // 2, n // 2
+    return (ne + 3) // 4 + (no + 3) // 4 + 4 + (4 if no > 0 else 0)
+
+
+def lane_floats(m):
+    return (steps(m) + 3) // 4 * 4
+
+
+def moff(m):
+    return sum(64 * lane_floats(k) for k in range(m))
+
+
+@pytest.fixture(scope="module")
+def plan():
+    p = gtp.Plan(L, L, L, gtp.GTP_PLAN_HOST_ONLY)
+    info = p.info()
+    NJ = info["NT"] + 1
+    S = p.table(3).reshape(-1, NJ)
+    W = p.table(4).reshape(-1, NJ)
+    return p, info, S, W, p.table(12), p.table(13)
+
+
+def test_images_follow_theta_tables(plan):
+    """Every entry of the operand images is the theta table value its lane,
+    step and order name (layout of the header comment), zero past degree L."""
+    p, info, S, W, A, Z = plan
+    NP = info["NP"]
+    assert A.size == moff(L + 1) and Z.size == 16 * H + 3 * H
+
+    def s(l, m, j):
+        return S[tri(l, m), j] if l <= L else 0.0
+
+    def cw(l, m, j):
+        return (NP if m == 0 else 0.5 * NP) * W[tri(l, m), j] if l <= L else 0.0
+
+    for m in range(L + 1):
+        n = L + 1 - m
+        ne, no = (n + 1) // 2, n // 2
+        ke, ko = (ne + 3) // 4, (no + 3) // 4
+        for lane in range(64):
+            k, i = lane // 16, lane % 16
+            pj = 4 * (i % 4) + i // 4 + 1
+            v = A[moff(m) + lane * lane_floats(m):][:steps(m)]
+            want = [s(m + 2 * (4 * q + k), m, pj) for q in range(ke)]
+            want += [s(m + 1 + 2 * (4 * q + k), m, pj) for q in range(ko)]
+            want += [cw(m + 2 * i, m, 4 * r + k + 1) if i < ne else 0.0 for r in range(4)]
+            if no:
+                want += [cw(m + 1 + 2 * i, m, 4 * r + k + 1) if i < no else 0.0 for r in range(4)]
+            np.testing.assert_array_equal(v, np.array(want))
+    for g in range(4):
+        for r in range(4):
+            j = 4 * r + g + 1
+            np.testing.assert_allclose(Z[(4 * g + r) * H:][:H], [S[tri(l, 0), 0] * S[tri(l, 0), j] for l in range(H)],
+                                       rtol=1e-12, atol=1e-13)
+    zp = Z[16 * H:]
+    np.testing.assert_allclose(zp[:H], [S[tri(l, 0), 0] ** 2 for l in range(H)], rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(zp[H:2 * H], [S[tri(l, 0), 0] for l in range(H)])
+    np.testing.assert_array_equal(zp[2 * H:], [NP * W[tri(l, 0), 0] for l in range(H)])
+
+
+def mfma(a_lanes, b_lanes, c):
+    """c + A B for 64-lane operands (A[i][k] = a_lanes[16 k + i], B[k][j] = b_lanes[16 k + j])."""
+    A = a_lanes.reshape(4, 16).T
+    B = b_lanes.reshape(4, 16)
+    return c + A @ B
+
+
+def replay_tile(X, hm, D, A, Z):
+    """The kernel's stages on one 16-channel tile X[k][c] (fp64); hm[c][l]."""
+    X = X.copy()
+    lanes = np.arange(64)
+    g_of, i_of = lanes // 16, lanes % 16
+    # rotate in
+    for l in range(L + 1):
+        X[l * l:(l + 1) ** 2] = D[l] @ X[l * l:(l + 1) ** 2]
+    # filter at the lane's node pairs: FE[4 g + r][c], FO likewise (rows as the tile's)
+    FE = np.zeros((16, 16))
+    FO = np.zeros((16, 16))
+    for g in range(4):
+        for r in range(4):
+            z = Z[(4 * g + r) * H:][:H]
+            FE[4 * g + r] = (z[0::2] * hm[:, 0::2]).sum(axis=1)
+            FO[4 * g + r] = (z[1::2] * hm[:, 1::2]).sum(axis=1)
+    zp = Z[16 * H:]
+    fe0 = (zp[0:H:2] * hm[:, 0::2]).sum(axis=1)
+    fo0 = (zp[1:H:2] * hm[:, 1::2]).sum(axis=1)
+    for m in range(L + 1):
+        n = L + 1 - m
+        ne, no = (n + 1) // 2, n // 2
+        ke, ko = (ne + 3) // 4, (no + 3) // 4
+        nl = lane_floats(m)
+        av = A[moff(m):moff(m) + 64 * nl].reshape(64, nl)
+        for sg in ([0] if m == 0 else [0, 1]):
+            def row(l):
+                return l * l + l + (-m if sg else m)
+
+            def bx(l_of_lane):
+                return np.array([X[row(l), c] if l <= L else 0.0 for l, c in zip(l_of_lane, i_of)])
+
+            GE = np.zeros((16, 16))
+            GO = np.zeros((16, 16))
+            for q in range(ke):
+                GE = mfma(av[:, q], bx(m + 2 * (4 * q + g_of)), GE)
+            for q in range(ko):
+                GO = mfma(av[:, ke + q], bx(m + 1 + 2 * (4 * q + g_of)), GO)
+            pj = (FE + FO) * (GE + GO)
+            pm = (FE - FO) * (GE - GO)
+            PE, PO = pj + pm, pj - pm
+            YE = np.zeros((16, 16))
+            YO = np.zeros((16, 16))
+            for r in range(4):
+                # B for K-step r: register r of lane (g, c) = P[4 g + r][c]
+                YE = mfma(av[:, ke + ko + r], PE[4 * g_of + r, i_of], YE)
+                if no:
+                    YO = mfma(av[:, ke + ko + 4 + r], PO[4 * g_of + r, i_of], YO)
+            if m == 0:
+                xs = np.array([X[l * l + l] for l in range(H)])
+                ae = (zp[H:2 * H:2][:, None] * xs[0::2]).sum(axis=0)
+                ao = (zp[H + 1:2 * H:2][:, None] * xs[1::2]).sum(axis=0)
+                p0 = (fe0 + fo0) * (ae + ao)
+                q0 = (fe0 - fo0) * (ae - ao)
+                pe0, po0 = p0 + q0, p0 - q0
+            for ie in range(ne):
+                l = m + 2 * ie
+                v = YE[ie].copy()
+                if m == 0:
+                    v += zp[2 * H + l] * pe0
+                X[row(l)] = v
+            for io in range(no):
+                l = m + 1 + 2 * io
+                v = YO[io].copy()
+                if m == 0:
+                    v += zp[2 * H + l] * po0
+                X[row(l)] = v
+    for l in range(L + 1):
+        X[l * l:(l + 1) ** 2] = D[l].T @ X[l * l:(l + 1) ** 2]
+    return X
+
+
+def test_replay_matches_oracle(plan):
+    """The replay equals the oracle's rotated-frame convolution (fp64), with
+    the edge's rotation taken from the oracle's Wigner-D builder (any rotation
+    taking the edge to the pole gives the same product)."""
+    p, info, S, W, A, Z = plan
+    rng = np.random.default_rng(1616)
+    K = (L + 1) ** 2
+    for r in (np.array([0.3, -1.2, 0.7]), np.array([0.0, 0.0, 2.0]), np.array([1e-4, 2e-4, -1.0])):
+        x = rng.standard_normal((16, K))
+        hm = rng.standard_normal((16, H))
+        Dfull = O.wigner_d_real(L, O.edge_rotation(r))
+        D = [Dfull[l * l:(l + 1) ** 2, l * l:(l + 1) ** 2] for l in range(L + 1)]
+        y = replay_tile(x.T.copy(), hm, D, A, Z).T
+        ref = O.conv_escn(x[None], r[None], hm[None], L, L, L)[0]
+        err = O.max_rel_err(y, ref)
+        assert err < 1e-11, err

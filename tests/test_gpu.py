@@ -672,8 +672,11 @@ def _filter_ref(h, r, L2):
 
 # (full 64-channel workgroups read their x slab straight into LDS when it
 # starts 16-byte aligned: C = 65 and 70 mix aligned and unaligned slabs)
+# L = 16 runs on the matrix-core kernel (64-channel workgroups of four
+# 16-channel waves: C = 37 and 130 leave partial waves and empty ones)
 ESCN = [(1, 1, 1, 64), (2, 2, 2, 5), (3, 3, 3, 100), (4, 4, 4, 128), (5, 5, 5, 64), (6, 6, 6, 128), (6, 6, 6, 37),
-        (6, 6, 6, 65), (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3)]
+        (6, 6, 6, 65), (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3), (16, 16, 16, 64),
+        (16, 16, 16, 37), (16, 16, 16, 130), (16, 16, 16, 1)]
 
 
 @pytest.mark.parametrize("L1,L2,Lout,C", ESCN)
@@ -719,6 +722,27 @@ def test_conv_escn_bf16_direct_plan_and_empty():
     y = gtp.gtp_conv_escn(gtp.Plan(L, L, L), z, torch.empty((0, 3), device="cuda:0"),
                           torch.empty((0, C, L + 1), device="cuda:0"))
     assert y.shape == (0, C, O.nsh(L))
+
+
+def test_conv_escn_wave_bf16_and_rotated_route():
+    """L = 16 with bf16 x on the matrix-core kernel, against the oracle; the
+    plan reports the rotated-frame tables (operand images present)."""
+    L, B, C = 16, 6, 20
+    rng = np.random.default_rng(161)
+    bits, xv = inputs.round_to_bf16(rng.standard_normal((B, C, O.nsh(L))).astype(np.float32))
+    r = rng.standard_normal((B, 3)).astype(np.float32)
+    r[0] = 0.0
+    h = rng.standard_normal((B, C, L + 1)).astype(np.float32)
+    plan = gtp.Plan(L, L, L)
+    assert plan.table(12).size > 0 and plan.table(13).size > 0
+    _say("conv_escn L=16 bf16")
+    tx = torch.from_numpy(bits.view(np.int16)).cuda().view(torch.bfloat16)
+    y = gtp.gtp_conv_escn(plan, tx, dev(r), dev(h))
+    torch.cuda.synchronize()
+    ref = O.gtp_grid(xv.astype(np.float64).reshape(B * C, -1), _filter_ref(h, r, L).reshape(B * C, -1), L, L, L)
+    err = O.max_rel_err(y.view(B * C, -1).cpu().numpy(), ref)
+    _say(f"  err={err:.3e}")
+    assert err <= TOL, err
 
 
 def test_conv_escn_edge_workload_sampled():

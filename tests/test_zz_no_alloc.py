@@ -47,13 +47,15 @@ def _case(seed, B, C, L1, L2, bf16):
 
 # (degrees, flags, bf16, first call (B, C), second call (B, C)); scratch is
 # 64 MiB: 2240 B per edge at L = 6 (29959 edges per chunk), 4560 B at L = 8,
-# C * 121 * 4 B on the L = 10 filter route
+# 28560 B at L = 16 (2349 edges per chunk), C * 121 * 4 B on the L = 10
+# filter route
 CASES = [
     ((6, 6, 6), 0, False, (40000, 64), (1000, 96)),
     ((8, 8, 8), 0, True, (20000, 64), (300, 70)),
     ((10, 10, 10), 0, False, (5000, 64), (100, 3)),
     ((4, 4, 4), gtp.GTP_CONV_DIRECT, False, (3000, 64), (50, 5)),
     ((3, 5, 4), 0, False, (700, 200), (20, 1)),
+    ((16, 16, 16), 0, False, (3000, 64), (40, 17)),
 ]
 
 
