@@ -164,7 +164,7 @@ KERNEL_SOURCES = {
     "gtp_small.hip": ["gen_small_consts.cpp"],
     "gtp_escn.hip": ["gen_small_consts.cpp", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
     "gtp_wave.hip": ["gtp_fft.hpp"],
-    "gtp_escn_wave.hip": ["gtp_escn.hip", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
+    "gtp_escn_wave.hip": ["gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
 }
 
 
@@ -195,7 +195,8 @@ def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto
     if escn:
         # both kernels of the step (rotation matrices, then the product): one unit
         if L == 16:
-            return "k_escn_rot+k_conv_escn_wave", "mfma", "gtp_escn_wave.hip"
+            # one kernel: the rotations applied from the edge angles
+            return "k_conv_escn_wave", "mfma", "gtp_escn_wave.hip"
         return "k_escn_rot+k_conv_escn", "alu", "gtp_escn.hip"
     if workload == "mix":
         # pair products (thread per product) and the mix on the matrix cores in one kernel

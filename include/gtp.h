@@ -127,11 +127,12 @@ gtp_status gtp_channel_mix(gtp_plan p, const void *x1, const void *x2, gtp_dtype
  * x: [B, C, (L1+1)^2] (in_dtype); r: [B, 3] fp32 edge vectors (need not be
  * unit; a zero vector is taken as (0, 0, 1)); h: [B, C, L2+1] fp32 radial
  * weights; y: [B, C, (Lout+1)^2] fp32, not overlapping the inputs.  The
- * rotated-frame kernels cover L1 = L2 = Lout in 1..8 (one product per lane)
- * and 16 (the matrix cores, 16 channels per wave); both take one workgroup
- * per edge and 64 channels, so C >= 64 fills it, and the per-edge rotation
- * matrices go to a stream-ordered workspace (hipMallocAsync).  Other
- * degrees, and plans built with GTP_CONV_DIRECT, build the filter in such a
+ * rotated-frame kernels cover L1 = L2 = Lout in 1..8 (one product per lane;
+ * the per-edge rotation matrices go to a stream-ordered workspace,
+ * hipMallocAsync) and 16 (the matrix cores, 16 channels per wave, the
+ * rotation applied from the edge angles: no workspace); both take one
+ * workgroup per edge and 64 channels, so C >= 64 fills it.  Other degrees,
+ * and plans built with GTP_CONV_DIRECT, build the filter in a stream-ordered
  * workspace and take gtp_full. */
 gtp_status gtp_conv_escn(gtp_plan p, const void *x, gtp_dtype in_dtype, const float *r, const float *h, int64_t B,
                          int64_t C, float *y, void *stream);
@@ -140,8 +141,9 @@ gtp_status gtp_conv_escn(gtp_plan p, const void *x, gtp_dtype in_dtype, const fl
  * allocate: code under HIP graph capture, tight serving loops, harnesses that
  * forbid hipMalloc.  Same arguments, result and errors as gtp_conv_escn; no
  * hipMalloc / hipMallocAsync / hipFree / allocating library call is made.
- * The per-edge rotation matrices (or, for degrees without a rotated-frame
- * kernel, the filter rows) go to a static device scratch array of
+ * The per-edge rotation matrices of L = 1..8 (or, for degrees without a
+ * rotated-frame kernel, the filter rows; L = 16 needs none) go to a static
+ * device scratch array of
  * GTP_NOALLOC_SCRATCH_BYTES (64 MiB) per device, which exists from the
  * library's load on that device until the process ends; the edges are
  * processed in chunks that fit it.  Returns GTP_ERR_UNSUPPORTED (before any
@@ -292,9 +294,10 @@ gtp_status gtp_plan_info(gtp_plan p, int64_t *out8);
  *   which 11: E   [pair][row]               theta-node rows of the rotated-frame convolution
  *   which 12: A   [m][lane][step]           its matrix-core operand images (theta tables)
  *   which 13: Z   [group][pair][l] + poles  its zonal-filter table
+ *   which 14: JI  [l][tile][lane][step]     its operand images of J and J^T
  * with tri(l,m) = l(l+1)/2 + m, m >= 0.  Tables 5..9 exist only for
  * L1 = L2 = Lout = L in {16, 32, 64}, tables 10..11 for L1 = L2 = Lout in
- * 1..8 and 16, tables 12..13 for L1 = L2 = Lout = 16 (length 0 otherwise);
+ * 1..8 and 16, tables 12..14 for L1 = L2 = Lout = 16 (length 0 otherwise);
  * their layouts are internal to those kernels.  Pass buf = NULL to
  * get the length in *count; otherwise *count is the capacity in doubles. */
 gtp_status gtp_plan_table(gtp_plan p, int which, double *buf, int64_t *count);

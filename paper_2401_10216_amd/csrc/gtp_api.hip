@@ -154,7 +154,7 @@ gtp_status upload(gtp_plan_* p, long fail_at) {
   d.XMAP = nullptr;
   d.XQUADS = t.XQUADS;
   d.phi_fft = p->conv == GTP_CONV_FFT ? 1 : 0;
-  p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0, nullptr, nullptr};
+  p->escd = gtp::EscnDev{nullptr, nullptr, 0, 0, 0, nullptr, nullptr, nullptr};
   if (p->esc.NPAIR) {
     gtp::EscnDev& ed = p->escd;
     if ((s = up(&p->esc.J, nullptr, &ed.J)) != GTP_OK) return s;
@@ -165,6 +165,7 @@ gtp_status upload(gtp_plan_* p, long fail_at) {
     if (!p->esc.A.empty()) {
       if ((s = up(&p->esc.A, nullptr, &ed.A)) != GTP_OK) return s;
       if ((s = up(&p->esc.Z, nullptr, &ed.Z)) != GTP_OK) return s;
+      if ((s = up(&p->esc.JI, nullptr, &ed.JI)) != GTP_OK) return s;
     }
   }
   if (t.waveL) {
@@ -367,10 +368,11 @@ gtp_status escn_check(gtp_plan p, const void* x, gtp_dtype in_dtype, const float
 }
 
 // Whether the plan's rotated-frame convolution runs on its own kernels
-// (L1 = L2 = Lout in 1..8, convolution-theorem plan) rather than as filter +
-// plain product.
+// (L1 = L2 = Lout in 1..8 or 16, convolution-theorem plan) rather than as
+// filter + plain product.
 bool escn_rotated(gtp_plan p) {
-  return !p->force_generic && p->conv != GTP_CONV_DIRECT && p->esc.NPAIR > 0 && gtp::escn_rot_floats(p->L1) > 0;
+  return !p->force_generic && p->conv != GTP_CONV_DIRECT && p->esc.NPAIR > 0 &&
+         (gtp::escn_rot_floats(p->L1) > 0 || (p->L1 == gtp::kEscnWaveL && !p->esc.JI.empty()));
 }
 
 }  // namespace
@@ -532,15 +534,17 @@ gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const fl
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
   const int64_t rf = gtp::escn_rot_floats(p->L1);
   if (escn_rotated(p)) {
-    // per-edge rotation matrices in a stream-ordered workspace
+    // per-edge rotation matrices in a stream-ordered workspace (none when the
+    // kernel applies the rotations from the edge angles)
     float* dws = nullptr;
     int64_t nd = 0;
     if (!mul_ok(B, rf, &nd) || nd > INT64_MAX / 4) return fail(GTP_ERR_INVALID_ARG, "B too large");
-    hipError_t e = hipMallocAsync(reinterpret_cast<void**>(&dws), size_t(nd) * sizeof(float), st);
+    hipError_t e = nd > 0 ? hipMallocAsync(reinterpret_cast<void**>(&dws), size_t(nd) * sizeof(float), st)
+                          : hipSuccess;
     if (e != hipSuccess) return fail(GTP_ERR_ALLOC, std::string("hipMallocAsync: ") + hipGetErrorString(e));
     bool done = false;
     e = gtp::launch_conv_escn(p->escd, p->L1, p->L2, p->Lout, x, it, r, h, B, C, y, dws, st, &done);
-    const hipError_t e2 = hipFreeAsync(dws, st);
+    const hipError_t e2 = dws ? hipFreeAsync(dws, st) : hipSuccess;
     if (done) {
       if (e != hipSuccess) return hip_fail(e, "gtp_conv_escn launch");
       return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
@@ -583,7 +587,8 @@ gtp_status gtp_conv_escn_noalloc(gtp_plan p, const void* x, gtp_dtype in_dtype, 
   // stream-ordered after those of the previous one, so each chunk reuses the
   // whole array.  Every scratch entry a kernel reads was written earlier in
   // the same chunk: nothing needs clearing.
-  const int64_t chunk = cap / per_edge < B ? cap / per_edge : B;
+  // (the degree-16 rotated-frame kernel needs no scratch: one chunk)
+  const int64_t chunk = per_edge == 0 ? B : (cap / per_edge < B ? cap / per_edge : B);
   for (int64_t b0 = 0; b0 < B; b0 += chunk) {
     const int64_t nb = B - b0 < chunk ? B - b0 : chunk;
     const void* xc = static_cast<const char*>(x) + size_t(b0) * C * K1 * es;
@@ -962,7 +967,8 @@ gtp_status gtp_plan_table(gtp_plan p, int which, double* buf, int64_t* count) {
     case 11: src = &p->esc.E; break;
     case 12: src = &p->esc.A; break;
     case 13: src = &p->esc.Z; break;
-    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..13");
+    case 14: src = &p->esc.JI; break;
+    default: return fail(GTP_ERR_INVALID_ARG, "which must be 0..14");
   }
   if (!buf) {
     *count = int64_t(src->size());

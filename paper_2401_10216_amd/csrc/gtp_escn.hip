@@ -101,31 +101,26 @@ constexpr int first_pair_nz(int i) {
 }
 
 // ---------------------------------------------------------------------------
-// Per-edge rotation matrices: one wave per edge, four edges per workgroup
-// up to L = 8; above, four waves per edge (its matrices fill 29 KB of LDS).
+// Per-edge rotation matrices: one wave per edge, four edges per workgroup.
 // D_b = J^T Z(-beta) J Z(-alpha) for every degree l <= L, written in the
-// padded row layout the small-degree product kernel reads (block l at
-// dofs(l), rows of erow(l) floats, padding zero) up to L = 8, in compact rows
-// (block l at jofs(l), rows of 2l+1 floats) above.
-constexpr int rot_edges(int L) { return L <= 8 ? 4 : 1; }
-constexpr int rot_threads(int L) { return L <= 8 ? 64 : 256; }  // per edge
+// padded row layout the product kernel reads (block l at dofs(l), rows of
+// erow(l) floats, padding zero).
+constexpr int kRotEdges = 4;
 
 template <int L>
-__global__ __launch_bounds__(rot_threads(L) * rot_edges(L)) void k_escn_rot(const float* __restrict__ r, int64_t B,
-                                                                             float* __restrict__ Dout, EscnDev t) {
-  constexpr int kRotEdges = rot_edges(L), NTH = rot_threads(L);
-  constexpr bool kCompact = L > 8;
+__global__ __launch_bounds__(64 * kRotEdges) void k_escn_rot(const float* __restrict__ r, int64_t B,
+                                                             float* __restrict__ Dout, EscnDev t) {
   constexpr int H = L + 1, JS = jofs(L + 1), DS = dofs(L + 1);
   __shared__ float Jl[JS];
   __shared__ __align__(16) float Tw[kRotEdges][DS];  // T in D's padded row layout
   __shared__ float4 tw[kRotEdges][H];               // (cos m a, sin m a, cos m b, sin m b)
-  const int tid = threadIdx.x, w = tid / NTH, lane = tid % NTH;
+  const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int64_t b = int64_t(blockIdx.x) * kRotEdges + w;
   const bool valid = b < B;
   float* const Tl = Tw[w];
   float4* const trig = tw[w];
-  for (int e = tid; e < JS; e += NTH * kRotEdges) Jl[e] = t.J[e];
-  for (int e = lane; e < DS; e += NTH) Tl[e] = 0.0f;  // row padding stays zero
+  for (int e = tid; e < JS; e += 64 * kRotEdges) Jl[e] = t.J[e];
+  for (int e = lane; e < DS; e += 64) Tl[e] = 0.0f;  // row padding stays zero
   if (valid && lane <= L) {
     // the edge's angles (beta from the pole, alpha in the xy plane); a zero
     // vector takes the direction (0, 0, 1)
@@ -146,7 +141,7 @@ __global__ __launch_bounds__(rot_threads(L) * rot_edges(L)) void k_escn_rot(cons
   if (valid) {
     cfor<0, L + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), ew = erow(l);
-      for (int e = lane; e < (l + 1) * (l + 1); e += NTH) {
+      for (int e = lane; e < (l + 1) * (l + 1); e += 64) {
         const int p = e / (l + 1), q = e - p * (l + 1);
         const float4 tq = trig[q], tp = trig[p];
         const float* Jr = Jl + jo + (l + p) * d;  // row l + p
@@ -182,10 +177,10 @@ __global__ __launch_bounds__(rot_threads(L) * rot_edges(L)) void k_escn_rot(cons
   if (!valid) return;
   // D = J^T T: each item is four consecutive entries of one row (one J value
   // and one 16-byte quad of T per k), stored as one 16-byte write
-  float* const Db = Dout + b * (kCompact ? JS : DS);
+  float* const Db = Dout + b * DS;
   cfor<0, L + 1>([&](auto LL) {
     constexpr int l = decltype(LL)::value, d = 2 * l + 1, jo = jofs(l), nq = erow(l) / 4;
-    for (int e = lane; e < d * nq; e += NTH) {
+    for (int e = lane; e < d * nq; e += 64) {
       const int a = e / nq, q = e - a * nq;
       float4 s = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
       cfor<0, d>([&](auto KK) {
@@ -197,15 +192,7 @@ __global__ __launch_bounds__(rot_threads(L) * rot_edges(L)) void k_escn_rot(cons
         s.z = fmaf(jv, tv.z, s.z);
         s.w = fmaf(jv, tv.w, s.w);
       });
-      if constexpr (kCompact) {
-        float* const row = Db + jo + a * d + 4 * q;
-        row[0] = s.x;
-        if (4 * q + 1 < d) row[1] = s.y;
-        if (4 * q + 2 < d) row[2] = s.z;
-        if (4 * q + 3 < d) row[3] = s.w;
-      } else {
-        reinterpret_cast<float4*>(Db + dofs(l) + a * erow(l))[q] = s;
-      }
+      reinterpret_cast<float4*>(Db + dofs(l) + a * erow(l))[q] = s;
     }
   });
 }
@@ -476,7 +463,9 @@ hipError_t launch_l(const EscnDev& e, const void* x, int in_type, const float* r
   if (e.ERL != EGeo<L>::ERL) return hipErrorInvalidValue;  // table layout and kernel disagree
   const int64_t ncb = (C + kEW - 1) / kEW;
   if (B * ncb > 0x7fffffff) return hipErrorInvalidValue;
-  hipError_t err = launch_escn_rot(e, L, r, B, dws, s);
+  hipLaunchKernelGGL((k_escn_rot<L>), dim3(unsigned((B + kRotEdges - 1) / kRotEdges)), dim3(64 * kRotEdges), 0, s, r,
+                     B, dws, e);
+  hipError_t err = hipGetLastError();
   if (err != hipSuccess) return err;
   const dim3 grid(unsigned(B * ncb)), block(kEW);
   if (in_type == IN_BF16)
@@ -491,32 +480,7 @@ hipError_t launch_l(const EscnDev& e, const void* x, int in_type, const float* r
 }  // namespace
 
 int64_t escn_rot_floats(int L) {
-  if (L >= 1 && L <= 8) return dofs(L + 1);
-  return L == kEscnWaveL ? jofs(kEscnWaveL + 1) : 0;
-}
-
-hipError_t launch_escn_rot(const EscnDev& e, int L, const float* r, int64_t B, float* dws, hipStream_t s) {
-  if (B <= 0) return hipSuccess;
-  auto go = [&](auto LL) {
-    constexpr int l = decltype(LL)::value;
-    constexpr int ne = rot_edges(l);
-    if ((B + ne - 1) / ne > 0x7fffffff) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((k_escn_rot<l>), dim3(unsigned((B + ne - 1) / ne)), dim3(rot_threads(l) * ne), 0, s, r, B, dws,
-                       e);
-    return hipGetLastError();
-  };
-  switch (L) {
-    case 1: return go(std::integral_constant<int, 1>{});
-    case 2: return go(std::integral_constant<int, 2>{});
-    case 3: return go(std::integral_constant<int, 3>{});
-    case 4: return go(std::integral_constant<int, 4>{});
-    case 5: return go(std::integral_constant<int, 5>{});
-    case 6: return go(std::integral_constant<int, 6>{});
-    case 7: return go(std::integral_constant<int, 7>{});
-    case 8: return go(std::integral_constant<int, 8>{});
-    case kEscnWaveL: return go(std::integral_constant<int, kEscnWaveL>{});
-    default: return hipErrorInvalidValue;
-  }
+  return (L >= 1 && L <= 8) ? dofs(L + 1) : 0;
 }
 
 hipError_t launch_conv_escn(const EscnDev& e, int L1, int L2, int Lout, const void* x, int in_type, const float* r,
@@ -536,8 +500,8 @@ hipError_t launch_conv_escn(const EscnDev& e, int L1, int L2, int Lout, const vo
       default: break;
     }
   }
-  if (L1 == L2 && L2 == Lout && L1 == kEscnWaveL && e.A && e.LM == kEscnWaveL)
-    return launch_conv_escn_wave(e, x, in_type, r, h, B, C, y, dws, ensh(L1), L2 + 1, ensh(Lout), s);
+  if (L1 == L2 && L2 == Lout && L1 == kEscnWaveL && e.A && e.JI && e.LM == kEscnWaveL)
+    return launch_conv_escn_wave(e, x, in_type, r, h, B, C, y, ensh(L1), L2 + 1, ensh(Lout), s);
   *supported = false;
   return hipSuccess;
 }

@@ -20,10 +20,11 @@ struct EscnDev {
   int LM, NPAIR, ERL;
   const float* A;  // operand images of the matrix-core kernel (LM = kEscnWaveL)
   const float* Z;
+  const float* JI;
 };
 
 // Floats of one edge's rotation matrices in the workspace (0 when no
-// rotated-frame kernel exists for degree L).
+// rotated-frame kernel exists for degree L, or when its kernel needs none).
 int64_t escn_rot_floats(int L);
 
 // Launches the rotated-frame kernels for L1 = L2 = Lout = L in 1..8 (one
@@ -38,11 +39,9 @@ hipError_t launch_conv_escn(const EscnDev& e, int L1, int L2, int Lout, const vo
 // The matrix-core kernel of degree kEscnWaveL = 16 (tables of a 16-plan):
 // rows of k1 = (L1+1)^2 input coefficients, h rows of kh = L2 + 1 weights and
 // output rows of ko = (Lout+1)^2 floats, each at most that of degree 16 (rows
-// read zero-padded to degree 16, outputs truncated); dws holds the per-edge
-// rotation matrices written by the degree-16 rotation kernel first.
+// read zero-padded to degree 16, outputs truncated).  It applies each edge's
+// rotation factor by factor from its angles and needs no workspace.
 hipError_t launch_conv_escn_wave(const EscnDev& e, const void* x, int in_type, const float* r, const float* h,
-                                 int64_t B, int64_t C, float* y, float* dws, int k1, int kh, int ko, hipStream_t s);
-// The per-edge rotation matrices of degree L into dws (B * escn_rot_floats(L) floats).
-hipError_t launch_escn_rot(const EscnDev& e, int L, const float* r, int64_t B, float* dws, hipStream_t s);
+                                 int64_t B, int64_t C, float* y, int k1, int kh, int ko, hipStream_t s);
 
 }  // namespace gtp

@@ -145,6 +145,23 @@ EscnHost build_escn_tables(const Tables& t) {
       zp[L + 1 + l] = S(l, 0, 0);    // Theta_l0(0)
       zp[2 * (L + 1) + l] = CW(l, 0, 0);
     }
+    e.JI.assign(size_t(2 * escn_wave_jtoff()), 0.0);
+    size_t jo = 0;
+    for (int l = 0; l <= L; ++l) {
+      const int d = 2 * l + 1, nk4 = escn_wave_nk4(l);
+      for (int mt = 0; mt < escn_wave_nm(l); ++mt)
+        for (int lane = 0; lane < 64; ++lane) {
+          const int k = lane / 16, i = lane % 16, row = 16 * mt + i;
+          for (int s = 0; s < (d + 3) / 4; ++s) {
+            const int col = 4 * s + k;
+            if (row >= d || col >= d) continue;
+            const size_t at = size_t(escn_wave_joff(l, mt)) + size_t(lane) * nk4 + s;
+            e.JI[at] = e.J[jo + size_t(row) * d + col];                          // J[row][col]
+            e.JI[escn_wave_jtoff() + at] = e.J[jo + size_t(col) * d + row];      // J^T[row][col]
+          }
+        }
+      jo += size_t(d) * d;
+    }
   }
   return e;
 }

@@ -40,9 +40,16 @@ namespace gtp {
 //        Theta_l0(0) Theta_l0(t_j) at the node pairs 4 r + g + 1 of lane
 //        group g (Z[(g 4 + r)(L + 1) + l]), then three rows of L + 1 values
 //        at the pole pair: the filter, Theta_l0(0) and c_0 W[tri(l, 0)][0].
+//   JI : the A-operand images of J and J^T for that kernel's rotations
+//        (the edge's D_b = J^T Z(-beta) J Z(-alpha) applied factor by
+//        factor): per degree block l, 16-row tile mt and lane 16 k + i, the
+//        K-steps s = 0 .. NK(l) - 1 (NK = ceil((2l+1) / 4), padded to a
+//        multiple of 4) of J[16 mt + i][4 s + k] at escn_wave_joff(l, mt),
+//        then the same for J^T at escn_wave_jtoff() + escn_wave_joff(l, mt);
+//        zero outside the block.
 struct EscnHost {
   int LM = 0, NPAIR = 0, ERL = 0;
-  std::vector<double> J, E, A, Z;
+  std::vector<double> J, E, A, Z, JI;
 };
 
 // Degree of the matrix-core rotated-frame kernel: 16 interior node pairs,
@@ -61,6 +68,15 @@ constexpr int escn_wave_moff(int L, int m) {
   return o;
 }
 constexpr int escn_wave_zfloats(int L) { return 16 * (L + 1) + 3 * (L + 1); }
+// K-steps of degree block l (padded to 4 per lane) and the image offsets
+constexpr int escn_wave_nk4(int l) { return ((2 * l + 1 + 3) / 4 + 3) / 4 * 4; }
+constexpr int escn_wave_nm(int l) { return (2 * l + 1 + 15) / 16; }
+constexpr int escn_wave_joff(int l, int mt) {
+  int o = 0;
+  for (int k = 0; k < l; ++k) o += escn_wave_nm(k) * 64 * escn_wave_nk4(k);
+  return o + mt * 64 * escn_wave_nk4(l);
+}
+constexpr int escn_wave_jtoff() { return escn_wave_joff(kEscnWaveL + 1, 0); }
 
 // Builds the tables from a plan's tables; empty (NPAIR = 0) unless
 // L1 = L2 = Lout; A and Z only for L1 = kEscnWaveL.

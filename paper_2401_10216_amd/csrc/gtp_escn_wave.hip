@@ -4,12 +4,16 @@
 // Same computation as the small-degree kernel (y = D_b^T Z(D_b x, h), Z the
 // product with a zonal filter taken per order m at the theta nodes), but the
 // per-product state (289 coefficients) does not fit one lane's registers, so
-// the work is laid out across the channels of an edge, which share D_b and
-// every table: each stage is a small dense contraction with the 16 channels
-// of a wave as the N index of v_mfma_f32_16x16x4f32 (A[i][k] from lane 16 k +
-// i, B[k][j] from lane 16 k + j, register r of lane 16 g + i = row 4 g + r,
-// column i):
-//   rotate in    x'_l (rows 2l+1) = D_l x_l, per degree block, in place;
+// the work is laid out across the channels of an edge, which share the edge's
+// rotation and every table: each dense stage is a small contraction with the
+// 16 channels of a wave as the N index of v_mfma_f32_16x16x4f32 (A[i][k] from
+// lane 16 k + i, B[k][j] from lane 16 k + j, register r of lane 16 g + i = row
+// 4 g + r, column i).  The rotation D_b = J^T Z(-beta) J Z(-alpha) is applied
+// factor by factor: Z, a rotation about the pole, turns each (cos m, sin m)
+// coefficient pair by m times the edge angle (VALU), and J, the fixed real-SH
+// matrix of R_x(90 deg), is a per-degree-block contraction whose operands are
+// the same for every edge.  The stages, all in place on the wave's tile:
+//   rotate in    x' = J^T Z(-beta) J Z(-alpha) x;
 //   synthesis    per m-part (m, cos / sin) and degree parity (l - m even /
 //                odd): the partial sums at the 16 interior node pairs,
 //                G[pair][c] = sum_l Theta_lm(t_pair) x'[(l, m)][c] (row 4 g + r
@@ -20,13 +24,10 @@
 //                r takes register r of every lane (node pairs 4 r + g + 1, as
 //                the synthesis left them), so nothing moves between the two;
 //   poles        (only m = 0 is non-zero there) on the VALU;
-//   rotate out   y_l = D_l^T y'_l.
+//   rotate out   y = Z(alpha) J^T Z(beta) J y'.
 // One workgroup per (edge, 64 channels), one wave per 16 channels; LDS holds
-// the edge's D_b (compact rows of odd length 2l+1, as the rotation kernel
-// writes them above L = 8: conflict-free column and row reads) and each
-// wave's coefficient tile [k][16 channels], which the stages rewrite in place
-// (100 KB: one workgroup per CU, so the kernel keeps every load of a stage in
-// flight at once and prefetches the next order's operands).
+// each wave's coefficient tile [k][16 channels] (75 KB: two workgroups per CU)
+// and the edge's trig values.
 #include <type_traits>
 
 #include "gtp_ct.hpp"
@@ -49,16 +50,15 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f4 mfma(float a, float b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
 
-// compact D: block l at cofs(l), rows of 2l+1 floats
-constexpr int cofs(int l) {
-  int s = 0;
-  for (int k = 0; k < l; ++k) s += (2 * k + 1) * (2 * k + 1);
-  return s;
+
+// Pair p (0..135) of the rotations about the pole: degree l = 1..16 and
+// order m = 1..l, numbered l (l - 1) / 2 + m - 1.
+constexpr int pair_l(int p) {
+  int l = 1;
+  while (l * (l + 1) / 2 <= p) ++l;
+  return l;
 }
-constexpr int kDC = cofs(kWL + 1);  // 6545
-// D in LDS with room for the reads past its last block (row 47, column 35 of
-// the 33 x 33 block: values dropped)
-constexpr int kDCL = cofs(kWL) + 47 * (2 * kWL + 1) + 36;
+constexpr int pair_m(int p) { return p - pair_l(p) * (pair_l(p) - 1) / 2 + 1; }
 
 // The stages rewrite the tile in place: lanes read rows that other lanes then
 // overwrite, and read rows that other lanes wrote.  The wave issues its LDS
@@ -71,23 +71,23 @@ __device__ __forceinline__ float ldx(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ldx(const uint16_t* p, int64_t i) { return __uint_as_float(uint32_t(p[i]) << 16); }
 
 template <typename TIn>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_conv_escn_wave(
-    const TIn* __restrict__ x, const float* __restrict__ Dall, const float* __restrict__ h, float* __restrict__ y,
-    int64_t C, int ncb, const float* __restrict__ At, const float* __restrict__ Zt, int k1, int kh, int ko) {
-  __shared__ __align__(16) float Dl[kDCL];
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_conv_escn_wave(
+    const TIn* __restrict__ x, const float* __restrict__ rv, const float* __restrict__ h, float* __restrict__ y,
+    int64_t C, int ncb, const float* __restrict__ At, const float* __restrict__ Zt, const float* __restrict__ JI,
+    int k1, int kh, int ko) {
   __shared__ __align__(16) float tiles[kWaves * kTileF];
+  __shared__ float4 tw[kWH];  // (cos m alpha, sin m alpha, cos m beta, sin m beta)
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, i = lane & 15;
-  // XCD-aware: the ncb workgroups of an edge (which read its rotation
-  // matrices) run on one XCD
   const int64_t wg = xcd_product(blockIdx.x, gridDim.x);
   const int64_t b = wg / ncb;
   const int64_t c0 = (wg % ncb) * (16 * kWaves) + 16 * w;  // first channel of this wave
   const int cnt = C - c0 <= 0 ? 0 : (C - c0 < 16 ? int(C - c0) : 16);
-  float* const X = tiles + w * kTileF;  // rows 0..288; row 289 takes the writes of padding rows
+  float* const X = tiles + w * kTileF;  // rows 0..288, row 289 takes the writes of padding rows
 
   // ---- 1. every load in flight before the first use: the wave's x tile
-  // (lane (g, c) takes rows g, g + 4, ..: 16 B of each of 16 rows per load),
-  // its share of D_b, the radial weights of channel i, the operands of m = 0
+  // (lane (g, c) takes rows g, g + 4, ..), the radial weights of channel i,
+  // the operands of m = 0; the edge's angles (beta from the pole, alpha in
+  // the xy plane; a zero vector is taken as (0, 0, 1))
   constexpr int NXL = (kWK + 3) / 4;  // 73 rows per lane group
   float xv[NXL];
   {
@@ -96,21 +96,22 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 
     const int c = lane & 15;
     const int64_t ch = c0 + c < C ? c0 + c : C - 1;
     const TIn* const xr = x + (b * C + ch) * int64_t(k1);
-    cfor<0, NXL>([&](auto Q) {
-      constexpr int q = decltype(Q)::value;
-      const int k = g + 4 * q;
-      const float v = ldx(xr, k < k1 ? k : k1 - 1);
-      xv[q] = (c < cnt && k < k1) ? v : 0.0f;
-    });
-  }
-  constexpr int NDL = (kDC + 64 * kWaves - 1) / (64 * kWaves);  // 26 entries of D per thread
-  float dv[NDL];
-  {
-    const float* const Db = Dall + b * kDC;  // compact rows (the rotation kernel's layout above L = 8)
-    cfor<0, NDL>([&](auto Q) {
-      const int e = tid + decltype(Q)::value * 64 * kWaves;
-      dv[decltype(Q)::value] = Db[e < kDC ? e : 0];
-    });
+    if (k1 == kWK) {
+      // full rows: one base per lane, constant offsets
+      const TIn* const xg = xr + g;
+      cfor<0, NXL>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        const float v = ldx(xg, (4 * q + 3 < kWK) ? 4 * q : (g + 4 * q < kWK ? 4 * q : -g));
+        xv[q] = (c < cnt && g + 4 * q < kWK) ? v : 0.0f;
+      });
+    } else {
+      cfor<0, NXL>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        const int k = g + 4 * q;
+        const float v = ldx(xr, k < k1 ? k : k1 - 1);
+        xv[q] = (c < cnt && k < k1) ? v : 0.0f;
+      });
+    }
   }
   float hv[kWH];
   {
@@ -121,6 +122,16 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 
       const float v = hb[l < kh ? l : kh - 1];
       hv[l] = (i < cnt && l < kh) ? v : 0.0f;
     });
+  }
+  if (tid < kWH) {
+    const float rx = rv[3 * b], ry = rv[3 * b + 1], rz = rv[3 * b + 2];
+    const float rho = sqrtf(rx * rx + ry * ry);
+    const float al = rho > 0.0f ? atan2f(ry, rx) : 0.0f;
+    const float be = (rho > 0.0f || rz != 0.0f) ? atan2f(rho, rz) : 0.0f;
+    float sa, ca, sb, cb;
+    sincosf(float(tid) * al, &sa, &ca);
+    sincosf(float(tid) * be, &sb, &cb);
+    tw[tid] = make_float4(ca, sa, cb, sb);
   }
   f4 avq[2][4];  // the operands of order m (and m + 1, prefetched), four quads
   auto load_ops = [&](auto MM, f4(&dst)[4]) {
@@ -133,11 +144,6 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 
     constexpr int q = decltype(Q)::value;
     const int k = g + 4 * q;
     X[(k < kWK ? k : kWK) * 16 + i] = xv[q];
-  });
-  cfor<0, NDL>([&](auto Q) {
-    constexpr int q = decltype(Q)::value;
-    const int e = tid + q * 64 * kWaves;
-    if (q + 1 < NDL || e < kDC) Dl[e < kDC ? e : 0] = dv[q];
   });
   // the zonal filter at the lane's node pairs 4 r + g + 1 (even and odd
   // degrees apart) and at the poles
@@ -163,60 +169,103 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 
       else fo0 = fmaf(zp[l], hv[l], fo0);
     });
   }
-  __syncthreads();
+  __syncthreads();  // the trig values (and each wave's own tile)
 
-  // LDS reads are unconditional (clamped addresses; the value then selected),
-  // writes of padding rows go to the spare row kWK: no divergent branches.
+  // LDS reads of the tile are unconditional (past a degree block they stay
+  // inside the tile; the value is then selected), writes of padding rows go
+  // to the spare row kWK: no divergent branches.
   auto xrd = [&](int row, bool ok) {
     const float v = X[(ok ? row : 0) * 16 + i];
     return ok ? v : 0.0f;
   };
-  // the same for rows past a degree block, which stay inside the tile
   auto xrd_block = [&](int row, bool ok) {
     const float v = X[row * 16 + i];
     return ok ? v : 0.0f;
   };
-  // ---- 2. rotate in (M = rows of D_l, K = its columns), two degree blocks
-  // at a time: the MFMAs of both, then their writes (blocks touch disjoint
-  // rows; a block's reads precede its writes)
-  auto rot_in_mma = [&](auto LL, auto& acc) {
-    constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = (d + 15) / 16, NK = (d + 3) / 4, R0 = l * l;
-    cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
-    cfor<0, NK>([&](auto KS) {
-      constexpr int ks = decltype(KS)::value;
-      const int a = 4 * ks + g;
-      const float bv = xrd_block(R0 + a, a < d);
+
+  // ---- rotations about the pole: each (cos m, sin m) pair of the tile turned
+  // by m times the edge angle, AB = 0 alpha, 1 beta, SGN = -1 for Z(-angle):
+  //   c' = c cos + s sin, s' = -c sin + s cos   (Z(-angle); the transpose for +)
+  // the 136 pairs (l = 1..16, m = 1..l, numbered l (l - 1) / 2 + m - 1), lane
+  // group g taking the pairs numbered g mod 4
+  auto zrot = [&](auto AB, auto SGN) {
+    constexpr int ab = decltype(AB)::value, sgn = decltype(SGN)::value;
+    cfor<0, kWL * (kWL + 1) / 8>([&](auto Q) {
+      constexpr int q = decltype(Q)::value;
+      // the four candidates of pair 4 q + g, selected by the lane group
+      constexpr int l0 = pair_l(4 * q), l1 = pair_l(4 * q + 1), l2 = pair_l(4 * q + 2), l3 = pair_l(4 * q + 3);
+      const int l = g == 0 ? l0 : (g == 1 ? l1 : (g == 2 ? l2 : l3));
+      const int m = g == 0 ? pair_m(4 * q) : (g == 1 ? pair_m(4 * q + 1) : (g == 2 ? pair_m(4 * q + 2) : pair_m(4 * q + 3)));
+      const float4 t = tw[m];
+      const float cm = ab ? t.z : t.x, sm = ab ? t.w : t.y;
+      const int rc = l * l + l + m, rs = l * l + l - m;
+      const float c = X[rc * 16 + i], sv = X[rs * 16 + i];
+      if constexpr (sgn < 0) {
+        X[rc * 16 + i] = fmaf(c, cm, sv * sm);
+        X[rs * 16 + i] = fmaf(sv, cm, -c * sm);
+      } else {
+        X[rc * 16 + i] = fmaf(c, cm, -sv * sm);
+        X[rs * 16 + i] = fmaf(sv, cm, c * sm);
+      }
+    });
+    GTP_TILE_ORDER();
+  };
+  // ---- the fixed matrix J (TR = 0) or J^T (TR = 1) on every degree block
+  // (M = rows, K = columns), two blocks at a time: the MFMAs of both, then
+  // their writes (blocks touch disjoint rows; a block's reads precede its
+  // writes).  Operand images: lane-permuted, four K-steps per 16-byte load.
+  auto jpass = [&](auto TR) {
+    constexpr int tr = decltype(TR)::value;
+    const float* const img = JI + (tr ? escn_wave_jtoff() : 0);
+    auto mma = [&](auto LL, auto& acc) {
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), NK = (d + 3) / 4;
+      constexpr int NK4 = escn_wave_nk4(l), R0 = l * l;
+      f4 a[NM][NK4 / 4];
       cfor<0, NM>([&](auto M) {
         constexpr int mt = decltype(M)::value;
-        const int row = 16 * mt + i;
-        const bool ok = row < d && a < d;
-        const float t = Dl[cofs(l) + row * d + a];
-        acc[mt] = mfma(ok ? t : 0.0f, bv, acc[mt]);
+        const f4* const src = reinterpret_cast<const f4*>(img + escn_wave_joff(l, mt) + lane * NK4);
+        cfor<0, NK4 / 4>([&](auto Q) { a[mt][decltype(Q)::value] = src[decltype(Q)::value]; });
       });
-    });
-  };
-  auto rot_in_store = [&](auto LL, const auto& acc) {
-    constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = (d + 15) / 16, R0 = l * l;
-    cfor<0, NM>([&](auto M) {
-      constexpr int mt = decltype(M)::value;
-      cfor<0, 4>([&](auto RR) {
-        constexpr int r = decltype(RR)::value;
-        const int row = 16 * mt + 4 * g + r;
-        X[(row < d ? R0 + row : kWK) * 16 + i] = acc[mt][r];
+      cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
+      cfor<0, NK>([&](auto KS) {
+        constexpr int ks = decltype(KS)::value;
+        const int c = 4 * ks + g;
+        const float bv = xrd_block(R0 + c, c < d);
+        cfor<0, NM>([&](auto M) {
+          constexpr int mt = decltype(M)::value;
+          acc[mt] = mfma(a[mt][ks / 4][ks % 4], bv, acc[mt]);
+        });
       });
+    };
+    auto store = [&](auto LL, const auto& acc) {
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), R0 = l * l;
+      cfor<0, NM>([&](auto M) {
+        constexpr int mt = decltype(M)::value;
+        cfor<0, 4>([&](auto RR) {
+          constexpr int r = decltype(RR)::value;
+          const int row = 16 * mt + 4 * g + r;
+          X[(row < d ? R0 + row : kWK) * 16 + i] = acc[mt][r];
+        });
+      });
+    };
+    cfor<0, (kWL + 2) / 2>([&](auto PP) {
+      constexpr int l0 = 2 * decltype(PP)::value, l1 = l0 + 1 <= kWL ? l0 + 1 : l0;
+      f4 a0[escn_wave_nm(l0)], a1[escn_wave_nm(l1)];
+      mma(std::integral_constant<int, l0>{}, a0);
+      if constexpr (l1 != l0) mma(std::integral_constant<int, l1>{}, a1);
+      GTP_TILE_ORDER();
+      store(std::integral_constant<int, l0>{}, a0);
+      if constexpr (l1 != l0) store(std::integral_constant<int, l1>{}, a1);
     });
-  };
-  cfor<0, (kWL + 2) / 2>([&](auto PP) {
-    constexpr int l0 = 2 * decltype(PP)::value, l1 = l0 + 1 <= kWL ? l0 + 1 : l0;
-    constexpr int NM0 = (2 * l0 + 1 + 15) / 16, NM1 = (2 * l1 + 1 + 15) / 16;
-    f4 a0[NM0], a1[NM1];
-    rot_in_mma(std::integral_constant<int, l0>{}, a0);
-    if constexpr (l1 != l0) rot_in_mma(std::integral_constant<int, l1>{}, a1);
     GTP_TILE_ORDER();
-    rot_in_store(std::integral_constant<int, l0>{}, a0);
-    if constexpr (l1 != l0) rot_in_store(std::integral_constant<int, l1>{}, a1);
-  });
+  };
+
+  // ---- 2. rotate in: x' = J^T Z(-beta) J Z(-alpha) x
   GTP_TILE_ORDER();
+  zrot(std::integral_constant<int, 0>{}, std::integral_constant<int, -1>{});
+  jpass(std::integral_constant<int, 0>{});
+  zrot(std::integral_constant<int, 1>{}, std::integral_constant<int, -1>{});
+  jpass(std::integral_constant<int, 1>{});
 
   // ---- 3. the zonal product per order m, its cos and sin parts together
   // (m-parts touch disjoint rows)
@@ -303,79 +352,49 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(1, 
   });
   GTP_TILE_ORDER();
 
-  // ---- 4. rotate out (M = columns of D_l, K = its rows), two blocks at a
-  // time; blocks past Lout are skipped
-  auto rot_out_mma = [&](auto LL, auto& acc) {
-    constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = (d + 15) / 16, NK = (d + 3) / 4, R0 = l * l;
-    cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
-    cfor<0, NK>([&](auto KS) {
-      constexpr int ks = decltype(KS)::value;
-      const int rr = 4 * ks + g;
-      const float bv = xrd_block(R0 + rr, rr < d);
-      cfor<0, NM>([&](auto M) {
-        constexpr int mt = decltype(M)::value;
-        const int a = 16 * mt + i;
-        const bool ok = a < d && rr < d;
-        const float t = Dl[cofs(l) + rr * d + a];
-        acc[mt] = mfma(ok ? t : 0.0f, bv, acc[mt]);
-      });
-    });
-  };
-  auto rot_out_store = [&](auto LL, const auto& acc) {
-    constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = (d + 15) / 16, R0 = l * l;
-    cfor<0, NM>([&](auto M) {
-      constexpr int mt = decltype(M)::value;
-      cfor<0, 4>([&](auto RR) {
-        constexpr int r = decltype(RR)::value;
-        const int a = 16 * mt + 4 * g + r;
-        X[(a < d ? R0 + a : kWK) * 16 + i] = acc[mt][r];
-      });
-    });
-  };
-  cfor<0, (kWL + 2) / 2>([&](auto PP) {
-    constexpr int l0 = 2 * decltype(PP)::value, l1 = l0 + 1 <= kWL ? l0 + 1 : l0;
-    constexpr int NM0 = (2 * l0 + 1 + 15) / 16, NM1 = (2 * l1 + 1 + 15) / 16;
-    if (l0 * l0 < ko) {  // wave-uniform
-      f4 a0[NM0], a1[NM1];
-      rot_out_mma(std::integral_constant<int, l0>{}, a0);
-      if constexpr (l1 != l0) rot_out_mma(std::integral_constant<int, l1>{}, a1);
-      GTP_TILE_ORDER();
-      rot_out_store(std::integral_constant<int, l0>{}, a0);
-      if constexpr (l1 != l0) rot_out_store(std::integral_constant<int, l1>{}, a1);
-    }
-  });
-  GTP_TILE_ORDER();
+  // ---- 4. rotate out: y = Z(alpha) J^T Z(beta) J y'
+  jpass(std::integral_constant<int, 0>{});
+  zrot(std::integral_constant<int, 1>{}, std::integral_constant<int, 1>{});
+  jpass(std::integral_constant<int, 1>{});
+  zrot(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{});
 
   // ---- 5. store: rows of ko floats of the wave's channels
   {
     float* const yb = y + (b * C + c0) * int64_t(ko);
     const int c = lane & 15;
-    if (c < cnt)
-      cfor<0, NXL>([&](auto Q) {
-        const int k = g + 4 * decltype(Q)::value;
-        if (k < ko) yb[int64_t(c) * ko + k] = X[k * 16 + c];
-      });
+    if (c < cnt) {
+      if (ko == kWK) {
+        float* const yg = yb + int64_t(c) * ko + g;
+        cfor<0, NXL>([&](auto Q) {
+          constexpr int q = decltype(Q)::value;
+          if (4 * q + 3 < kWK || g + 4 * q < kWK) yg[4 * q] = X[(g + 4 * q) * 16 + c];
+        });
+      } else {
+        cfor<0, NXL>([&](auto Q) {
+          const int k = g + 4 * decltype(Q)::value;
+          if (k < ko) yb[int64_t(c) * ko + k] = X[k * 16 + c];
+        });
+      }
+    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_conv_escn_wave(const EscnDev& e, const void* x, int in_type, const float* r, const float* h,
-                                 int64_t B, int64_t C, float* y, float* dws, int k1, int kh, int ko, hipStream_t s) {
-  if (!e.A || !e.Z || e.LM != kWL || k1 > kWK || kh > kWH || ko > kWK || k1 < 1 || kh < 1 || ko < 1)
+                                 int64_t B, int64_t C, float* y, int k1, int kh, int ko, hipStream_t s) {
+  if (!e.A || !e.Z || !e.JI || e.LM != kWL || k1 > kWK || kh > kWH || ko > kWK || k1 < 1 || kh < 1 || ko < 1)
     return hipErrorInvalidValue;
   if (B <= 0 || C <= 0) return hipSuccess;
   const int64_t ncb = (C + 16 * kWaves - 1) / (16 * kWaves);
   if (B * ncb > 0x7fffffff) return hipErrorInvalidValue;
-  hipError_t err = launch_escn_rot(e, kWL, r, B, dws, s);
-  if (err != hipSuccess) return err;
   const dim3 grid(unsigned(B * ncb)), block(64 * kWaves);
   if (in_type == IN_BF16)
-    hipLaunchKernelGGL((k_conv_escn_wave<uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x), dws, h, y,
-                       C, int(ncb), e.A, e.Z, k1, kh, ko);
+    hipLaunchKernelGGL((k_conv_escn_wave<uint16_t>), grid, block, 0, s, static_cast<const uint16_t*>(x), r, h, y, C,
+                       int(ncb), e.A, e.Z, e.JI, k1, kh, ko);
   else
-    hipLaunchKernelGGL((k_conv_escn_wave<float>), grid, block, 0, s, static_cast<const float*>(x), dws, h, y, C,
-                       int(ncb), e.A, e.Z, k1, kh, ko);
+    hipLaunchKernelGGL((k_conv_escn_wave<float>), grid, block, 0, s, static_cast<const float*>(x), r, h, y, C,
+                       int(ncb), e.A, e.Z, e.JI, k1, kh, ko);
   return hipGetLastError();
 }
 

@@ -179,3 +179,76 @@ def test_replay_matches_oracle(plan):
         ref = O.conv_escn(x[None], r[None], hm[None], L, L, L)[0]
         err = O.max_rel_err(y, ref)
         assert err < 1e-11, err
+
+
+def nk4(l):
+    return (((2 * l + 1) + 3) // 4 + 3) // 4 * 4
+
+
+def nm(l):
+    return (2 * l + 1 + 15) // 16
+
+
+def joff(l, mt):
+    return sum(nm(k) * 64 * nk4(k) for k in range(l)) + mt * 64 * nk4(l)
+
+
+def j_blocks(p):
+    J = p.table(10)
+    out, o = [], 0
+    for l in range(L + 1):
+        d = 2 * l + 1
+        out.append(J[o:o + d * d].reshape(d, d))
+        o += d * d
+    return out
+
+
+def z_rot(l, angle, sign):
+    """Rotation about the pole on degree block l: each (cos m, sin m) pair
+    turned by m angle; sign = -1 for Z(-angle): c' = c cos + s sin, s' = -c sin + s cos."""
+    d = 2 * l + 1
+    Zm = np.eye(d)
+    for m in range(1, l + 1):
+        c, s = np.cos(m * angle), np.sin(m * angle)
+        ic, is_ = l + m, l - m
+        if sign < 0:
+            Zm[ic, ic], Zm[ic, is_], Zm[is_, ic], Zm[is_, is_] = c, s, -s, c
+        else:
+            Zm[ic, ic], Zm[ic, is_], Zm[is_, ic], Zm[is_, is_] = c, -s, s, c
+    return Zm
+
+
+def test_rotation_images_and_factorization(plan):
+    """Table 14 holds J and J^T in the lane-permuted K-step layout, and the
+    kernel's factor-by-factor rotation J^T Z(-beta) J Z(-alpha) (angles from
+    the edge vector as the kernel takes them) gives the oracle's product."""
+    p, info, S, W, A, Z = plan
+    JI = p.table(14)
+    Jb = j_blocks(p)
+    jt = joff(L + 1, 0)
+    assert JI.size == 2 * jt
+    for l in range(L + 1):
+        d = 2 * l + 1
+        for mt in range(nm(l)):
+            for lane in range(64):
+                k, i = lane // 16, lane % 16
+                row = 16 * mt + i
+                for s in range((d + 3) // 4):
+                    col = 4 * s + k
+                    at = joff(l, mt) + lane * nk4(l) + s
+                    want = Jb[l][row, col] if (row < d and col < d) else 0.0
+                    wantt = Jb[l][col, row] if (row < d and col < d) else 0.0
+                    assert JI[at] == want and JI[jt + at] == wantt
+    rng = np.random.default_rng(1717)
+    K = (L + 1) ** 2
+    for r in (np.array([0.3, -1.2, 0.7]), np.array([0.0, 0.0, -2.0]), np.array([0.0, 0.0, 0.0]),
+              np.array([-0.8, 0.1, 0.05])):
+        rho = np.hypot(r[0], r[1])
+        al = np.arctan2(r[1], r[0]) if rho > 0 else 0.0
+        be = np.arctan2(rho, r[2]) if (rho > 0 or r[2] != 0) else 0.0
+        D = [Jb[l].T @ z_rot(l, be, -1) @ Jb[l] @ z_rot(l, al, -1) for l in range(L + 1)]
+        x = rng.standard_normal((16, K))
+        hm = rng.standard_normal((16, H))
+        y = replay_tile(x.T.copy(), hm, D, A, Z).T
+        ref = O.conv_escn(x[None], r[None], hm[None], L, L, L)[0]
+        assert O.max_rel_err(y, ref) < 1e-11
