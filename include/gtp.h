@@ -79,7 +79,11 @@ typedef struct gtp_plan_ *gtp_plan;
 /* Create a plan (Sec. 3.2: the coefficients y^{l,m,*}_{u,v} of eq. sh-fs and
  * z^{l,m,*}_{u,v} of eq. fs-sh, plus the grids of the convolution).
  * out: receives the plan.  Returns GTP_ERR_NO_DEVICE without a device unless
- * GTP_PLAN_HOST_ONLY is set.  The plan owns its host and device tables. */
+ * GTP_PLAN_HOST_ONLY is set.  The plan owns its host and device tables.  A
+ * triple whose product or rotated-frame convolution runs on an equal-degree
+ * kernel of higher degree (16, 32 or 64; rows zero-padded) also gets that
+ * degree's plan here, kept by the library until the process ends, so that
+ * no later call needs to allocate. */
 gtp_status gtp_plan_create(gtp_plan *out, int L1, int L2, int Lout, unsigned flags);
 
 /* Destroy a plan and free its tables (NULL is a no-op).  Not stream-ordered:
@@ -130,10 +134,12 @@ gtp_status gtp_channel_mix(gtp_plan p, const void *x1, const void *x2, gtp_dtype
  * rotated-frame kernels cover L1 = L2 = Lout in 1..8 (one product per lane;
  * the per-edge rotation matrices go to a stream-ordered workspace,
  * hipMallocAsync) and 16 (the matrix cores, 16 channels per wave, the
- * rotation applied from the edge angles: no workspace); both take one
- * workgroup per edge and 64 channels, so C >= 64 fills it.  Other degrees,
- * and plans built with GTP_CONV_DIRECT, build the filter in a stream-ordered
- * workspace and take gtp_full. */
+ * rotation applied from the edge angles: no workspace), which also serves
+ * every other triple whose highest degree is 9..16 (rows read zero-padded
+ * to degree 16, outputs truncated: exact); both take one workgroup per edge
+ * and 64 channels, so C >= 64 fills it.  Other degrees, and plans built with
+ * GTP_CONV_DIRECT, build the filter in a stream-ordered workspace and take
+ * gtp_full. */
 gtp_status gtp_conv_escn(gtp_plan p, const void *x, gtp_dtype in_dtype, const float *r, const float *h, int64_t B,
                          int64_t C, float *y, void *stream);
 

@@ -34,6 +34,11 @@ struct gtp_plan_ {
   std::vector<float*> dbufs;
   gtp::DevTables dev{};
   gtp::EscnDev escd{};
+  // companion plans (process-lifetime cache entries), made with the plan so
+  // that no later call allocates: the equal-degree plan of the padded
+  // matrix-core product, and the degree-16 plan of the rotated-frame kernel
+  struct gtp_plan_* padw = nullptr;
+  struct gtp_plan_* esc16 = nullptr;
 };
 
 // Device scratch of the allocation-free entry point: one copy per device,
@@ -208,6 +213,23 @@ unsigned auto_conv(int L1, int L2, int Lout) {
   return GTP_CONV_DFT;
 }
 
+gtp_status cached_plan(int L1, int L2, int Lout, unsigned flags, gtp_plan* out);
+
+// Degree W of the equal-degree matrix-core kernel that runs a triple with no
+// kernel of its own (run_product's padding), 0 when none is needed.
+int pad_wave_degree(int L1, int L2, int Lout) {
+  const int A = std::max({1, L1, L2, std::min(Lout, L1 + L2)});
+  const bool own = L1 == L2 && L2 == Lout && (L1 == 16 || L1 == 32 || L1 == 64);
+  if (A <= 8 || A > kMaxL || own) return 0;
+  return A <= 16 ? 16 : (A <= 32 ? 32 : 64);
+}
+// Whether the degree-16 rotated-frame kernel serves a triple other than
+// (16, 16, 16) (rows zero-padded, outputs truncated): highest degree 9..16.
+bool escn_wave_padded(int L1, int L2, int Lout) {
+  const int M = std::max({L1, L2, Lout});
+  return M >= 9 && M <= gtp::kEscnWaveL && !(L1 == L2 && L2 == Lout && L1 == gtp::kEscnWaveL);
+}
+
 gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, int maxL) {
   if (!out) return fail(GTP_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
@@ -254,6 +276,18 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
       release(p.get());
       return s;
     }
+    if (!p->force_generic && p->conv != GTP_CONV_DIRECT) {
+      const int W = pad_wave_degree(L1, L2, Lout);
+      if (W && (s = cached_plan(W, W, W, GTP_CONV_DFT, &p->padw)) != GTP_OK) {
+        release(p.get());
+        return s;
+      }
+      if (escn_wave_padded(L1, L2, Lout) &&
+          (s = cached_plan(gtp::kEscnWaveL, gtp::kEscnWaveL, gtp::kEscnWaveL, GTP_CONV_DFT, &p->esc16)) != GTP_OK) {
+        release(p.get());
+        return s;
+      }
+    }
   }
   *out = p.release();
   return GTP_OK;
@@ -261,14 +295,14 @@ gtp_status make_plan(gtp_plan* out, int L1, int L2, int Lout, unsigned flags, in
 
 // Internal plan cache of the many-body and backward entry points, keyed by
 // device, degrees and plan flags.
-std::mutex g_cache_mu;
+std::recursive_mutex g_cache_mu;  // make_plan, called under it, takes companion plans
 std::map<std::tuple<int, int, int, int, unsigned>, gtp_plan> g_cache;
 
 gtp_status cached_plan(int L1, int L2, int Lout, unsigned flags, gtp_plan* out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  std::lock_guard<std::mutex> lk(g_cache_mu);
+  std::lock_guard<std::recursive_mutex> lk(g_cache_mu);
   auto key = std::make_tuple(dev, L1, L2, Lout, flags);
   auto it = g_cache.find(key);
   if (it != g_cache.end()) {
@@ -332,9 +366,11 @@ gtp_status run_product(gtp_plan p, const void* x1, int it1, const void* x2, int 
         if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
       } else if (A <= kMaxL) {
         const int W = A <= 16 ? 16 : (A <= 32 ? 32 : 64);
-        gtp_plan q = nullptr;
-        const gtp_status s = cached_plan(W, W, W, GTP_CONV_DFT, &q);
-        if (s != GTP_OK) return s;
+        gtp_plan q = p->padw;  // made with the plan
+        if (!q || q->L1 != W) {
+          const gtp_status s = cached_plan(W, W, W, GTP_CONV_DFT, &q);
+          if (s != GTP_OK) return s;
+        }
         e = gtp::launch_full_wave(q->dev, x1, it1, x2, it2, n, y, wt, st, &done, k1, k2, ko);
         if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, what);
       }
@@ -373,6 +409,19 @@ gtp_status escn_check(gtp_plan p, const void* x, gtp_dtype in_dtype, const float
 bool escn_rotated(gtp_plan p) {
   return !p->force_generic && p->conv != GTP_CONV_DIRECT && p->esc.NPAIR > 0 &&
          (gtp::escn_rot_floats(p->L1) > 0 || (p->L1 == gtp::kEscnWaveL && !p->esc.JI.empty()));
+}
+
+// Other triples with highest degree 9..16: the degree-16 rotated-frame kernel
+// on the companion plan's tables (rows zero-padded, outputs truncated; exact,
+// as for the padded product), without workspace.
+bool escn_wave16(gtp_plan p) {
+  return !p->force_generic && p->conv != GTP_CONV_DIRECT && !escn_rotated(p) && p->esc16 != nullptr;
+}
+gtp_status escn_wave16_run(gtp_plan p, const void* x, int it, const float* r, const float* h, int64_t B, int64_t C,
+                           float* y, hipStream_t st, const char* what) {
+  const hipError_t e = gtp::launch_conv_escn_wave(p->esc16->escd, x, it, r, h, B, C, y, gtp::nsh(p->L1), p->L2 + 1,
+                                                  gtp::nsh(p->Lout), st);
+  return e == hipSuccess ? GTP_OK : hip_fail(e, what);
 }
 
 }  // namespace
@@ -550,6 +599,7 @@ gtp_status gtp_conv_escn(gtp_plan p, const void* x, gtp_dtype in_dtype, const fl
       return e2 == hipSuccess ? GTP_OK : hip_fail(e2, "hipFreeAsync");
     }
   }
+  if (escn_wave16(p)) return escn_wave16_run(p, x, it, r, h, B, C, y, st, "gtp_conv_escn launch");
   // no rotated-frame kernel for these degrees: build the filter in a
   // stream-ordered workspace and take the plain product (same result)
   float* f = nullptr;
@@ -568,6 +618,12 @@ gtp_status gtp_conv_escn_noalloc(gtp_plan p, const void* x, gtp_dtype in_dtype, 
   int64_t n = 0;
   gtp_status s = escn_check(p, x, in_dtype, r, h, B, C, y, &n);
   if (s != GTP_OK || n == 0) return s;
+  if (escn_wave16(p)) {
+    // the degree-16 rotated-frame kernel needs no scratch
+    if ((s = device_ready(p)) != GTP_OK) return s;
+    return escn_wave16_run(p, x, in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32, r, h, B, C, y,
+                           static_cast<hipStream_t>(stream), "gtp_conv_escn_noalloc launch");
+  }
   // scratch floats one edge needs: its rotation matrices (rotated-frame
   // kernels) or its C filter rows (filter + plain product)
   const bool rot = escn_rotated(p);

@@ -673,10 +673,13 @@ def _filter_ref(h, r, L2):
 # (full 64-channel workgroups read their x slab straight into LDS when it
 # starts 16-byte aligned: C = 65 and 70 mix aligned and unaligned slabs)
 # L = 16 runs on the matrix-core kernel (64-channel workgroups of four
-# 16-channel waves: C = 37 and 130 leave partial waves and empty ones)
+# 16-channel waves: C = 37 and 130 leave partial waves and empty ones), and so
+# does every other triple whose highest degree is 9..16 (rows zero-padded to
+# degree 16, outputs truncated)
 ESCN = [(1, 1, 1, 64), (2, 2, 2, 5), (3, 3, 3, 100), (4, 4, 4, 128), (5, 5, 5, 64), (6, 6, 6, 128), (6, 6, 6, 37),
         (6, 6, 6, 65), (7, 7, 7, 64), (8, 8, 8, 70), (2, 2, 3, 16), (10, 10, 10, 3), (16, 16, 16, 64),
-        (16, 16, 16, 37), (16, 16, 16, 130), (16, 16, 16, 1)]
+        (16, 16, 16, 37), (16, 16, 16, 130), (16, 16, 16, 1), (12, 12, 12, 64), (9, 9, 9, 20), (16, 4, 12, 50),
+        (8, 8, 16, 30), (3, 12, 10, 17)]
 
 
 @pytest.mark.parametrize("L1,L2,Lout,C", ESCN)
