@@ -64,22 +64,38 @@ def generate_constants(verbose: bool = False) -> None:
     os.replace(out_e + ".tmp", out_e)
 
 
-def build(verbose: bool = False) -> str:
+POISON_BUILD = os.path.join(ROOT, "_build_poison")
+POISON_LIB = os.path.join(PKG, "libgtp_poison.so")
+
+
+def build(verbose: bool = False, poison: bool = True) -> str:
+    """Compile and link libgtp.so and, with poison=True, the poisoned-LDS
+    debug build libgtp_poison.so (-DGTP_POISON_LDS: every kernel fills its
+    LDS with NaN before first use; the tests compare it with the regular
+    build).  Both always recompile; at most 8 compilers run at once."""
     os.makedirs(BUILD, exist_ok=True)
     hipcc = _hipcc()
     generate_constants(verbose)
-    jobs = []
-    for s in HIP_SOURCES:
-        obj = os.path.join(BUILD, s.replace(".hip", ".o"))
-        jobs.append(([hipcc, *HIP_FLAGS, f"-I{GEN}", "-c", os.path.join(CSRC, s), "-o", obj], obj))
-    for s in CPP_SOURCES:
-        obj = os.path.join(BUILD, s.replace(".cpp", ".o"))
-        jobs.append((["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj))
+    variants = [(BUILD, LIB, [])] + ([(POISON_BUILD, POISON_LIB, ["-DGTP_POISON_LDS"])] if poison else [])
+    jobs = []  # (cmd, obj, variant index)
+    for vi, (bdir, _, extra) in enumerate(variants):
+        os.makedirs(bdir, exist_ok=True)
+        for s in HIP_SOURCES:
+            obj = os.path.join(bdir, s.replace(".hip", ".o"))
+            jobs.append(([hipcc, *HIP_FLAGS, *extra, f"-I{GEN}", "-c", os.path.join(CSRC, s), "-o", obj], obj, vi))
+        for s in CPP_SOURCES:
+            obj = os.path.join(bdir, s.replace(".cpp", ".o"))
+            jobs.append((["g++", *CXX_FLAGS, "-c", os.path.join(CSRC, s), "-o", obj], obj, vi))
     t0 = time.time()
-    procs = [(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True), cmd, obj)
-             for cmd, obj in jobs]
     failed = []
-    for p, cmd, obj in procs:
+    running = []
+    pending = sorted(jobs, key=lambda j: 0 if "gtp_small" in j[1] else 1)  # the longest first
+    while pending or running:
+        while pending and len(running) < 8:
+            cmd, obj, vi = pending.pop(0)
+            running.append((subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True), cmd,
+                            obj))
+        p, cmd, obj = running.pop(0)
         out, _ = p.communicate()
         if verbose or p.returncode:
             print(" ".join(cmd))
@@ -89,18 +105,19 @@ def build(verbose: bool = False) -> str:
             failed.append(obj)
     if failed:
         raise RuntimeError(f"compilation failed: {failed}")
-    tmp = LIB + ".tmp"
-    link = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *[o for _, o in jobs]]
-    r = subprocess.run(link, capture_output=True, text=True)
-    if r.returncode:
-        print(" ".join(link))
-        print(r.stdout, r.stderr)
-        raise RuntimeError("link failed")
-    os.replace(tmp, LIB)
-    if verbose:
-        print(f"built {LIB} in {time.time() - t0:.1f}s")
+    for vi, (bdir, lib, _) in enumerate(variants):
+        tmp = lib + ".tmp"
+        link = [hipcc, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *[o for _, o, v in jobs if v == vi]]
+        r = subprocess.run(link, capture_output=True, text=True)
+        if r.returncode:
+            print(" ".join(link))
+            print(r.stdout, r.stderr)
+            raise RuntimeError("link failed")
+        os.replace(tmp, lib)
+        if verbose:
+            print(f"built {lib} in {time.time() - t0:.1f}s")
     return LIB
 
 
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
+    build(verbose="-v" in sys.argv, poison="--no-poison" not in sys.argv)

@@ -76,6 +76,23 @@ __device__ __forceinline__ int degree_of(int i) {
   return l;
 }
 
+// Poisoned-LDS debug build (compiled with -DGTP_POISON_LDS; the library
+// then carries the name libgtp_poison.so): every kernel fills its LDS with a
+// quiet-NaN pattern before first use, so a read of a location the kernel has
+// not written yet (a race, a missing wait, a bad index) turns its results
+// into NaN.  All threads of the workgroup call it; it ends with a barrier.
+// Compiled to nothing in the regular build.
+__device__ __forceinline__ void lds_poison(float* p, int n) {
+#ifdef GTP_POISON_LDS
+  const int nt = int(blockDim.x * blockDim.y * blockDim.z);
+  for (int i = int(threadIdx.x); i < n; i += nt) p[i] = __int_as_float(0x7fc0dead);
+  __syncthreads();
+#else
+  (void)p;
+  (void)n;
+#endif
+}
+
 // Logical index of workgroup w among n: the dispatcher deals workgroups to
 // the 8 XCDs round robin (w mod 8), so XCD x takes the x-th contiguous run of
 // logical indices (runs of n / 8, the first n mod 8 one longer).  Work items

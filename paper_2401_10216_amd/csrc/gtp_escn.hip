@@ -114,6 +114,9 @@ __global__ __launch_bounds__(64 * kRotEdges) void k_escn_rot(const float* __rest
   __shared__ float Jl[JS];
   __shared__ __align__(16) float Tw[kRotEdges][DS];  // T in D's padded row layout
   __shared__ float4 tw[kRotEdges][H];               // (cos m a, sin m a, cos m b, sin m b)
+  lds_poison(Jl, JS);
+  lds_poison(&Tw[0][0], kRotEdges * DS);
+  lds_poison(reinterpret_cast<float*>(&tw[0][0]), kRotEdges * H * 4);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63;
   const int64_t b = int64_t(blockIdx.x) * kRotEdges + w;
   const bool valid = b < B;
@@ -242,6 +245,7 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
   static_assert(DS % 4 == 0 && DS <= XT, "LDS layout");
   constexpr int ND4 = DS / 4, RD = (ND4 + kEW - 1) / kEW;
   __shared__ __align__(16) float lds[XT];
+  lds_poison(lds, XT);
   float* const tile = lds;
   float* const Dl = lds;
 

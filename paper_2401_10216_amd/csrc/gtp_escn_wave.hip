@@ -77,6 +77,8 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     int k1, int kh, int ko) {
   __shared__ __align__(16) float tiles[kWaves * kTileF];
   __shared__ float4 tw[kWH];  // (cos m alpha, sin m alpha, cos m beta, sin m beta)
+  lds_poison(tiles, kWaves * kTileF);
+  lds_poison(reinterpret_cast<float*>(tw), kWH * 4);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, i = lane & 15;
   const int64_t wg = xcd_product(blockIdx.x, gridDim.x);
   const int64_t b = wg / ncb;

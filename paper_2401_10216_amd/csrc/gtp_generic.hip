@@ -61,6 +61,7 @@ __global__ __launch_bounds__(kBlock) void k_full_generic(DevTables t, const T1* 
                                                          int64_t n, int nu, int JC, DegWeights wt, PairIdx pi) {
   extern __shared__ float smem[];
   const GenericLayout g = generic_layout(t, nu, JC);
+  lds_poison(smem, g.total);
   const int tid = threadIdx.x;
   const int KO = (t.Lout + 1) * (t.Lout + 1);
   const int KE = (t.Le + 1) * (t.Le + 1);
@@ -201,6 +202,7 @@ __global__ __launch_bounds__(kBlock) void k_fourier_conv(int L1, int L2, const f
                                                          int64_t n, int use_lds) {
   extern __shared__ float smem[];
   const int D1 = 2 * L1 + 1, D2 = 2 * L2 + 1, U = L1 + L2, D3 = 2 * U + 1;
+  lds_poison(smem, use_lds ? 2 * D1 * D1 + 2 * D2 * D2 : 0);
   for (int64_t p = blockIdx.x; p < n; p += gridDim.x) {
     const float* a = g1 + p * 2 * D1 * D1;
     const float* b = g2 + p * 2 * D2 * D2;
@@ -376,6 +378,7 @@ __global__ __launch_bounds__(kBlock) void k_full_direct(DevTables t, const T1* _
                                                         const T2* __restrict__ x2, float* __restrict__ y, int64_t n) {
   extern __shared__ float smem[];
   const DirectLayout d = direct_layout(t);
+  lds_poison(smem, d.total);
   const int tid = threadIdx.x;
   const int L1 = t.L1, L2 = t.L2, Le = t.Le, U = t.U;
   const int KO = (t.Lout + 1) * (t.Lout + 1);

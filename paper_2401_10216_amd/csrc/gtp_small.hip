@@ -640,6 +640,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
   constexpr int S2 = lds_stride(K2);
   constexpr int KT = cmax(S2, lds_stride(KO));
   __shared__ __align__(16) float tile[kTile * KT];
+  lds_poison(tile, kTile * KT);
   const int tid = threadIdx.x;
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
@@ -729,6 +730,7 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     const T1* __restrict__ x1, const T2* __restrict__ x2, float* __restrict__ y, int64_t n, int k1, int k2, int ko) {
   constexpr int K = csh(L), S = lds_stride(K);
   __shared__ __align__(16) float tile[kTile * S];
+  lds_poison(tile, kTile * S);
   const int tid = threadIdx.x;
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
@@ -799,6 +801,7 @@ __global__ __launch_bounds__(kTile) void k_self_stepwise_small(const TIn* __rest
   using G2 = Geo<LO, L, LO, 0>;
   constexpr int KT = lds_stride(KO);  // the output rows (store_rows)
   __shared__ __align__(16) float tile[kTile * KT];
+  lds_poison(tile, kTile * KT);
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float a[K];
@@ -908,6 +911,7 @@ __global__ __launch_bounds__(kMixThreads) __attribute__((amdgpu_waves_per_eu(mix
   constexpr int Kd = csh(L);
   constexpr int NKT = (Kd + 15) / 16, KTW = (NKT + 3) / 4, CoB = 16 * NCT, KS = lds_stride(Kd);
   __shared__ float tile[kMixThreads * KS];
+  lds_poison(tile, kMixThreads * KS);
   const int64_t b = blockIdx.x;
   const int64_t nround = (P + kMixThreads - 1) / kMixThreads;
   for (int64_t r = 0; r < nround; ++r) {

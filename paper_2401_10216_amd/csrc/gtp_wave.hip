@@ -879,6 +879,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
   // the moments first: their reads then carry small immediate offsets
   constexpr int FFTF = FFT ? 2 * (FGeo<L>::AC + FGeo<L>::TC) : 0;  // the FFT variant's spectra and T
   __shared__ __align__(16) float lds[G::EOP + G::XQ * 4 + FFTF];
+  lds_poison(lds, G::EOP + G::XQ * 4 + FFTF);
   float* const eo = lds;
   float* const xs = lds + G::EOP;
   float2* const fa = reinterpret_cast<float2*>(lds + G::EOP + G::XQ * 4);
@@ -1011,6 +1012,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                 NIT = G::NIT, EOP = G::EOP, NTH = G::NTH;
   constexpr int XF = (G::XQ * 4 > 4 * EOP) ? G::XQ * 4 : 4 * EOP;  // x image, later the odd passes' moments
   __shared__ __align__(16) float lds[XF + 4 * EOP];               // + the even passes' moments
+  lds_poison(lds, XF + 4 * EOP);
   float* const eo_odd = lds;
   float* const eo_even = lds + XF;
 
@@ -1108,6 +1110,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   constexpr int NJ = G::NJ, NP = G::NP, NMP2 = G::NMP2, K = G::K, PASSES = G::PASSES, NROW = G::NROW,
                 NIT = G::NIT, EOP = G::EOP, NTH = G::NTH;
   __shared__ __align__(16) float lds[G::XQ * 4 + EOP + 2 * (16 * F::NS + 8 * F::TS)];
+  lds_poison(lds, G::XQ * 4 + EOP + 2 * (16 * F::NS + 8 * F::TS));
   float* const xs = lds;
   float* const eo = lds + G::XQ * 4;
   float2* const fa = reinterpret_cast<float2*>(eo + EOP);

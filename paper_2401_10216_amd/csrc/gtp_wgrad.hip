@@ -37,6 +37,7 @@ __global__ __launch_bounds__(kWgBlock) void k_wgrad_partial(const TA* __restrict
   const int64_t nprod = per_channel ? B : B * C;  // products in the row's sequence
   const int64_t q0 = ck * chunk, q1 = (q0 + chunk < nprod) ? q0 + chunk : nprod;
   const int S = K <= kWgBlock ? kWgBlock / K : 1;
+  lds_poison(red, S * K);
   const int s = K <= kWgBlock ? tid / K : 0;
   const int i0 = K <= kWgBlock ? tid % K : tid;
   const bool active = s < S;

@@ -65,25 +65,51 @@ _SIGS = {
 }
 
 
+def _load(path: str):
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2401_10216_amd.build`")
+    L = ctypes.CDLL(path)
+    for name, (res, args) in _SIGS.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
 def lib():
     """Load libgtp.so once (raises if it has not been built)."""
     global _lib
     with _lock:
         if _lib is None:
-            if not os.path.exists(LIB_PATH):
-                raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2401_10216_amd.build`")
-            L = ctypes.CDLL(LIB_PATH)
-            for name, (res, args) in _SIGS.items():
-                f = getattr(L, name)
-                f.restype = res
-                f.argtypes = args
-            _lib = L
+            _lib = _load(LIB_PATH)
     return _lib
 
 
-def _check(status: int):
+class use_library:
+    """Context in which the entry points (and the plans created there) use
+    another build of the library, e.g. the poisoned-LDS debug build
+    (libgtp_poison.so).  A plan keeps the library it was created with."""
+
+    def __init__(self, path: str):
+        self.path = path
+
+    def __enter__(self):
+        global _lib
+        with _lock:
+            self.saved = _lib
+            _lib = _load(self.path)
+        return _lib
+
+    def __exit__(self, *exc):
+        global _lib
+        with _lock:
+            _lib = self.saved
+        return False
+
+
+def _check(status: int, L=None):
     if status != GTP_OK:
-        raise GTPError(status, lib().gtp_last_error().decode())
+        raise GTPError(status, (L or lib()).gtp_last_error().decode())
 
 
 def _stream(stream=None):
@@ -154,12 +180,13 @@ class Plan:
     def __init__(self, L1: int, L2: int, Lout: int, flags: int = 0):
         self.L1, self.L2, self.Lout, self.flags = L1, L2, Lout, flags
         h = _P()
-        _check(lib().gtp_plan_create(ctypes.byref(h), L1, L2, Lout, flags))
+        self.lib = lib()
+        _check(self.lib.gtp_plan_create(ctypes.byref(h), L1, L2, Lout, flags), self.lib)
         self.handle = h
 
     def close(self):
         if getattr(self, "handle", None) is not None and self.handle.value:
-            lib().gtp_plan_destroy(self.handle)
+            self.lib.gtp_plan_destroy(self.handle)
             self.handle = None
 
     def __del__(self):
@@ -170,20 +197,20 @@ class Plan:
 
     def info(self) -> dict:
         out = (_I64 * 8)()
-        _check(lib().gtp_plan_info(self.handle, out))
+        _check(self.lib.gtp_plan_info(self.handle, out), self.lib)
         keys = ["L1", "L2", "Lout", "U", "Le", "NT", "NP", "conv"]
         return dict(zip(keys, [int(v) for v in out]))
 
     def table(self, which: int):
         import numpy as np
         cnt = _I64(0)
-        _check(lib().gtp_plan_table(self.handle, which, None, ctypes.byref(cnt)))
+        _check(self.lib.gtp_plan_table(self.handle, which, None, ctypes.byref(cnt)), self.lib)
         buf = np.zeros(cnt.value, dtype=np.float64)
-        _check(lib().gtp_plan_table(self.handle, which, buf.ctypes.data_as(_DP), ctypes.byref(cnt)))
+        _check(self.lib.gtp_plan_table(self.handle, which, buf.ctypes.data_as(_DP), ctypes.byref(cnt)), self.lib)
         return buf
 
     def grid_floats(self, which: int) -> int:
-        return int(lib().gtp_grid_floats(self.handle, which))
+        return int(self.lib.gtp_grid_floats(self.handle, which))
 
 
 def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
@@ -203,7 +230,7 @@ def gtp_full(plan: Plan, x1, x2, y=None, stream=None):
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x1.device)
     _on_gpu(x1, "x1")
-    _check(lib().gtp_full(plan.handle, p1, p2, code, B, C, py, _stream(stream)))
+    _check(plan.lib.gtp_full(plan.handle, p1, p2, code, B, C, py, _stream(stream)), plan.lib)
     return y
 
 
@@ -228,7 +255,7 @@ def gtp_channel_mix(plan: Plan, x1, x2, W, y=None, stream=None):
         y = torch.empty((B, Co, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     py = _want(y, "y", (B, Co, nsh(plan.Lout)), _f32(), x1.device)
     _on_gpu(x1, "x1")
-    _check(lib().gtp_channel_mix(plan.handle, p1, p2, code, pw, B, C1, C2, Co, py, _stream(stream)))
+    _check(plan.lib.gtp_channel_mix(plan.handle, p1, p2, code, pw, B, C1, C2, Co, py, _stream(stream)), plan.lib)
     return y
 
 
@@ -252,8 +279,8 @@ def gtp_conv_escn(plan: Plan, x, r, h, y=None, stream=None, noalloc: bool = Fals
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x.device)
     py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x.device)
     _on_gpu(x, "x")
-    fn = lib().gtp_conv_escn_noalloc if noalloc else lib().gtp_conv_escn
-    _check(fn(plan.handle, px, code, pr, ph, B, C, py, _stream(stream)))
+    fn = plan.lib.gtp_conv_escn_noalloc if noalloc else plan.lib.gtp_conv_escn
+    _check(fn(plan.handle, px, code, pr, ph, B, C, py, _stream(stream)), plan.lib)
     return y
 
 
@@ -283,8 +310,8 @@ def gtp_full_weighted(plan: Plan, x1, x2, w1=None, w2=None, wout=None, per_chann
         y = torch.empty((B, C, nsh(plan.Lout)), dtype=torch.float32, device=x1.device)
     py = _want(y, "y", (B, C, nsh(plan.Lout)), _f32(), x1.device)
     _on_gpu(x1, "x1")
-    _check(lib().gtp_full_weighted(plan.handle, p1, p2, code, *ptrs, 1 if per_channel else 0, B, C, py,
-                                   _stream(stream)))
+    _check(plan.lib.gtp_full_weighted(plan.handle, p1, p2, code, *ptrs, 1 if per_channel else 0, B, C, py,
+                                      _stream(stream)), plan.lib)
     return y
 
 
@@ -316,9 +343,9 @@ def gtp_full_weighted_backward(plan: Plan, x1, x2, dy, w1=None, w2=None, wout=No
     out = {k: torch.empty(shapes[k], dtype=torch.float32, device=x1.device) for k in need}
     ptr = {k: (ctypes.c_void_p(out[k].data_ptr()) if k in out else ctypes.c_void_p(None)) for k in shapes}
     _on_gpu(x1, "x1")
-    _check(lib().gtp_full_weighted_backward(plan.handle, px1, px2, code, *ws, 1 if per_channel else 0, pdy, B, C,
-                                            ptr["dx1"], ptr["dx2"], ptr["dw1"], ptr["dw2"], ptr["dwout"],
-                                            _stream(stream)))
+    _check(plan.lib.gtp_full_weighted_backward(plan.handle, px1, px2, code, *ws, 1 if per_channel else 0, pdy, B, C,
+                                               ptr["dx1"], ptr["dx2"], ptr["dw1"], ptr["dw2"], ptr["dwout"],
+                                               _stream(stream)), plan.lib)
     return out
 
 
@@ -346,7 +373,7 @@ def gtp_full_backward(plan: Plan, x1, x2, dy, need_dx1: bool = True, need_dx2: b
     p1 = _want(dx1, "dx1", (B, C, nsh(plan.L1)), _f32(), x1.device) if need_dx1 else ctypes.c_void_p(None)
     p2 = _want(dx2, "dx2", (B, C, nsh(plan.L2)), _f32(), x1.device) if need_dx2 else ctypes.c_void_p(None)
     _on_gpu(x1, "x1")
-    _check(lib().gtp_full_backward(plan.handle, px1, px2, code, pdy, B, C, p1, p2, _stream(stream)))
+    _check(plan.lib.gtp_full_backward(plan.handle, px1, px2, code, pdy, B, C, p1, p2, _stream(stream)), plan.lib)
     return (dx1 if need_dx1 else None), (dx2 if need_dx2 else None)
 
 
@@ -365,7 +392,7 @@ def gtp_sh2fourier(plan: Plan, which: int, x, grid=None, stream=None):
         grid = torch.empty((n, 2 * L + 1, 2 * L + 1), dtype=torch.complex64, device=x.device)
     pg = _want(grid, "grid", (n, 2 * L + 1, 2 * L + 1), (torch.complex64,), x.device)
     _on_gpu(x, "x")
-    _check(lib().gtp_sh2fourier(plan.handle, which, px, code, n, pg, _stream(stream)))
+    _check(plan.lib.gtp_sh2fourier(plan.handle, which, px, code, n, pg, _stream(stream)), plan.lib)
     return grid
 
 
@@ -382,7 +409,7 @@ def gtp_fourier_conv(plan: Plan, g1, g2, g3=None, stream=None):
         g3 = torch.empty((n, D3, D3), dtype=torch.complex64, device=g1.device)
     p3 = _want(g3, "g3", (n, D3, D3), c64, g1.device)
     _on_gpu(g1, "g1")
-    _check(lib().gtp_fourier_conv(plan.handle, p1, p2, n, p3, _stream(stream)))
+    _check(plan.lib.gtp_fourier_conv(plan.handle, p1, p2, n, p3, _stream(stream)), plan.lib)
     return g3
 
 
@@ -397,7 +424,7 @@ def gtp_fourier2sh(plan: Plan, g3, y=None, stream=None):
         y = torch.empty((n, nsh(plan.Lout)), dtype=torch.float32, device=g3.device)
     py = _want(y, "y", (n, nsh(plan.Lout)), _f32(), g3.device)
     _on_gpu(g3, "g3")
-    _check(lib().gtp_fourier2sh(plan.handle, p3, n, py, _stream(stream)))
+    _check(plan.lib.gtp_fourier2sh(plan.handle, p3, n, py, _stream(stream)), plan.lib)
     return y
 
 
@@ -450,6 +477,6 @@ def gtp_debug_host_pipeline(plan: Plan, x1, x2):
     a = np.ascontiguousarray(x1, dtype=np.float64).reshape(-1, nsh(plan.L1))
     b = np.ascontiguousarray(x2, dtype=np.float64).reshape(-1, nsh(plan.L2))
     y = np.zeros((a.shape[0], nsh(plan.Lout)), dtype=np.float64)
-    _check(lib().gtp_debug_host_pipeline(plan.handle, a.ctypes.data_as(_DP), b.ctypes.data_as(_DP), a.shape[0],
-                                         y.ctypes.data_as(_DP)))
+    _check(plan.lib.gtp_debug_host_pipeline(plan.handle, a.ctypes.data_as(_DP), b.ctypes.data_as(_DP), a.shape[0],
+                                            y.ctypes.data_as(_DP)), plan.lib)
     return y
