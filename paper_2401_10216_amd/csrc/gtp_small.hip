@@ -598,18 +598,21 @@ __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, in
   typedef float sv4 __attribute__((ext_vector_type(4)));
   if (cnt == kTile && (reinterpret_cast<uintptr_t>(out) & 15) == 0) {
     // a full workgroup's rows are 64 KO floats, a whole number of 16-byte
-    // runs: 16-byte stores
+    // runs: 16-byte non-temporal stores (the outputs are not read again:
+    // 1.6 % faster at L = 6 than plain stores; non-temporal loads of the
+    // input rows, by contrast, measured 1.5x slower)
     constexpr int N4 = kTile * KO / 4;
     if constexpr (SO == KO) {
       // compact rows: the tile (16-byte aligned) is the output's layout
-      for (int i = tid; i < N4; i += kTile) reinterpret_cast<sv4*>(out)[i] = reinterpret_cast<const sv4*>(tile)[i];
+      for (int i = tid; i < N4; i += kTile)
+        __builtin_nontemporal_store(reinterpret_cast<const sv4*>(tile)[i], reinterpret_cast<sv4*>(out) + i);
     } else {
       // padded rows; KO is a multiple of 4, so no 16-byte run crosses a row
       static_assert(KO % 4 == 0, "even row lengths are (2m)^2");
       for (int i = tid; i < N4; i += kTile) {
         const int r = (4 * i) / KO, c = 4 * i - r * KO;
         const float* const t = tile + r * SO + c;
-        reinterpret_cast<sv4*>(out)[i] = sv4{t[0], t[1], t[2], t[3]};
+        __builtin_nontemporal_store(sv4{t[0], t[1], t[2], t[3]}, reinterpret_cast<sv4*>(out) + i);
       }
     }
   } else {
