@@ -443,12 +443,12 @@ __global__ __launch_bounds__(kEW) __attribute__((amdgpu_waves_per_eu(escn_waves(
       const int i4 = ln + decltype(Q)::value * kEW;
       if (i4 < N4) {
         if constexpr (S == K) {
-          reinterpret_cast<sv4*>(yb)[i4] = reinterpret_cast<const sv4*>(tile)[i4];
+          __builtin_nontemporal_store(reinterpret_cast<const sv4*>(tile)[i4], reinterpret_cast<sv4*>(yb) + i4);
         } else {
           // padded rows; K is a multiple of 4, so no 16-byte run crosses a row
           const int r = (4 * i4) / K;
           const float* const t = tile + r * S + (4 * i4 - r * K);
-          reinterpret_cast<sv4*>(yb)[i4] = sv4{t[0], t[1], t[2], t[3]};
+          __builtin_nontemporal_store(sv4{t[0], t[1], t[2], t[3]}, reinterpret_cast<sv4*>(yb) + i4);
         }
       }
     });
