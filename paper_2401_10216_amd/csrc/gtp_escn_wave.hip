@@ -41,24 +41,26 @@ constexpr int kWL = kEscnWaveL;            // 16
 constexpr int kWK = (kWL + 1) * (kWL + 1);  // 289 coefficients
 constexpr int kWH = kWL + 1;                // 17 radial weights
 constexpr int kWaves = 4;                   // 16-channel tiles per workgroup
-// floats of one wave's tile: rows 0..288, row 289 takes the writes of
-// padding rows, rows up to 291 the reads past the last block (whose values
-// are then dropped)
-constexpr int kTileF = (kWK + 3) * 16;
+// One wave's tile, channel-major: coefficient k of channel c at c kTS + k,
+// the layout of the wave's 16 rows in memory (contiguous copies in and out).
+// Rows 0..288, row 289 takes the writes of padding rows, rows up to 291 the
+// reads past the last block (whose values are then dropped); the odd stride
+// puts one coefficient of the 16 channels in 16 banks.
+constexpr int kTS = kWK + 4;   // 293
+constexpr int kSpare = kWK;    // 289
+constexpr int kTileF = 16 * kTS;
 
-typedef float f4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f4 mfma(float a, float b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
-
-
-// Pair p (0..135) of the rotations about the pole: degree l = 1..16 and
-// order m = 1..l, numbered l (l - 1) / 2 + m - 1.
 constexpr int pair_l(int p) {
   int l = 1;
   while (l * (l + 1) / 2 <= p) ++l;
   return l;
 }
 constexpr int pair_m(int p) { return p - pair_l(p) * (pair_l(p) - 1) / 2 + 1; }
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 mfma(float a, float b, f4 c) { return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0); }
+
 
 // The stages rewrite the tile in place: lanes read rows that other lanes then
 // overwrite, and read rows that other lanes wrote.  The wave issues its LDS
@@ -90,30 +92,23 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // (lane (g, c) takes rows g, g + 4, ..), the radial weights of channel i,
   // the operands of m = 0; the edge's angles (beta from the pole, alpha in
   // the xy plane; a zero vector is taken as (0, 0, 1))
-  constexpr int NXL = (kWK + 3) / 4;  // 73 rows per lane group
+  // the wave's 16 rows as one block of 16 k1 floats: element e = lane + 64 q
+  // (64 consecutive floats per load), channel e / k1, coefficient e % k1
+  constexpr int NXL = (16 * kWK + 63) / 64;  // 73 loads per lane
   float xv[NXL];
-  {
-    // unconditional loads from clamped addresses (a valid row of the edge,
-    // a valid column), then the select: no divergent branches
-    const int c = lane & 15;
-    const int64_t ch = c0 + c < C ? c0 + c : C - 1;
-    const TIn* const xr = x + (b * C + ch) * int64_t(k1);
-    if (k1 == kWK) {
-      // full rows: one base per lane, constant offsets
-      const TIn* const xg = xr + g;
-      cfor<0, NXL>([&](auto Q) {
-        constexpr int q = decltype(Q)::value;
-        const float v = ldx(xg, (4 * q + 3 < kWK) ? 4 * q : (g + 4 * q < kWK ? 4 * q : -g));
-        xv[q] = (c < cnt && g + 4 * q < kWK) ? v : 0.0f;
-      });
-    } else {
-      cfor<0, NXL>([&](auto Q) {
-        constexpr int q = decltype(Q)::value;
-        const int k = g + 4 * q;
-        const float v = ldx(xr, k < k1 ? k : k1 - 1);
-        xv[q] = (c < cnt && k < k1) ? v : 0.0f;
-      });
-    }
+  const bool full = k1 == kWK && cnt == 16;  // wave-uniform
+  if (full) {
+    // one base per lane, constant offsets (the last load: lanes 0..15)
+    const TIn* const xl = x + (b * C + c0) * int64_t(kWK) + lane;
+    cfor<0, NXL>([&](auto Q) {
+      constexpr int q = decltype(Q)::value;
+      if constexpr (64 * q + 63 < 16 * kWK) {
+        xv[q] = ldx(xl, 64 * q);
+      } else {
+        const float v = ldx(xl, lane < 16 * kWK - 64 * q ? 64 * q : 0);
+        xv[q] = lane < 16 * kWK - 64 * q ? v : 0.0f;
+      }
+    });
   }
   float hv[kWH];
   {
@@ -142,11 +137,24 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     cfor<0, NL / 4>([&](auto Q) { dst[decltype(Q)::value] = src[decltype(Q)::value]; });
   };
   load_ops(std::integral_constant<int, 0>{}, avq[0]);
-  cfor<0, NXL>([&](auto Q) {
-    constexpr int q = decltype(Q)::value;
-    const int k = g + 4 * q;
-    X[(k < kWK ? k : kWK) * 16 + i] = xv[q];
-  });
+  if (full) {
+    cfor<0, NXL>([&](auto Q) {
+      const int e = lane + 64 * decltype(Q)::value;
+      const int c = e / kWK, k = e - c * kWK;
+      if (e < 16 * kWK) X[c * kTS + k] = xv[decltype(Q)::value];
+    });
+  } else {
+    // padded rows or a partial tile: zeros first, then the wave's cnt rows
+    // of k1 floats (a plain loop: the uncommon shapes)
+    for (int e = lane; e < kTileF; e += 64) X[e] = 0.0f;
+    GTP_TILE_ORDER();
+    const TIn* const xb = x + (b * C + c0) * int64_t(k1);
+    const int tot = cnt * k1;
+    for (int e = lane; e < tot; e += 64) {
+      const int c = e / k1, k = e - c * k1;
+      X[c * kTS + k] = ldx(xb, e);
+    }
+  }
   // the zonal filter at the lane's node pairs 4 r + g + 1 (even and odd
   // degrees apart) and at the poles
   f4 FE, FO;
@@ -177,11 +185,11 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // inside the tile; the value is then selected), writes of padding rows go
   // to the spare row kWK: no divergent branches.
   auto xrd = [&](int row, bool ok) {
-    const float v = X[(ok ? row : 0) * 16 + i];
+    const float v = X[i * kTS + (ok ? row : 0)];
     return ok ? v : 0.0f;
   };
   auto xrd_block = [&](int row, bool ok) {
-    const float v = X[row * 16 + i];
+    const float v = X[i * kTS + row];
     return ok ? v : 0.0f;
   };
 
@@ -194,20 +202,19 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     constexpr int ab = decltype(AB)::value, sgn = decltype(SGN)::value;
     cfor<0, kWL * (kWL + 1) / 8>([&](auto Q) {
       constexpr int q = decltype(Q)::value;
-      // the four candidates of pair 4 q + g, selected by the lane group
       constexpr int l0 = pair_l(4 * q), l1 = pair_l(4 * q + 1), l2 = pair_l(4 * q + 2), l3 = pair_l(4 * q + 3);
       const int l = g == 0 ? l0 : (g == 1 ? l1 : (g == 2 ? l2 : l3));
       const int m = g == 0 ? pair_m(4 * q) : (g == 1 ? pair_m(4 * q + 1) : (g == 2 ? pair_m(4 * q + 2) : pair_m(4 * q + 3)));
       const float4 t = tw[m];
       const float cm = ab ? t.z : t.x, sm = ab ? t.w : t.y;
       const int rc = l * l + l + m, rs = l * l + l - m;
-      const float c = X[rc * 16 + i], sv = X[rs * 16 + i];
+      const float c = X[i * kTS + rc], sv = X[i * kTS + rs];
       if constexpr (sgn < 0) {
-        X[rc * 16 + i] = fmaf(c, cm, sv * sm);
-        X[rs * 16 + i] = fmaf(sv, cm, -c * sm);
+        X[i * kTS + rc] = fmaf(c, cm, sv * sm);
+        X[i * kTS + rs] = fmaf(sv, cm, -c * sm);
       } else {
-        X[rc * 16 + i] = fmaf(c, cm, -sv * sm);
-        X[rs * 16 + i] = fmaf(sv, cm, c * sm);
+        X[i * kTS + rc] = fmaf(c, cm, -sv * sm);
+        X[i * kTS + rs] = fmaf(sv, cm, c * sm);
       }
     });
     GTP_TILE_ORDER();
@@ -246,7 +253,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
         cfor<0, 4>([&](auto RR) {
           constexpr int r = decltype(RR)::value;
           const int row = 16 * mt + 4 * g + r;
-          X[(row < d ? R0 + row : kWK) * 16 + i] = acc[mt][r];
+          X[i * kTS + (row < d ? R0 + row : kSpare)] = acc[mt][r];
         });
       });
     };
@@ -307,7 +314,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       float ae = 0.0f, ao = 0.0f;
       cfor<0, kWH>([&](auto LL) {
         constexpr int l = decltype(LL)::value;
-        const float v = zp[kWH + l] * X[(l * l + l) * 16 + i];
+        const float v = zp[kWH + l] * X[i * kTS + l * l + l];
         if constexpr (l % 2 == 0) ae += v;
         else ao += v;
       });
@@ -341,13 +348,13 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
           const int l = m + 2 * ie;
           float v = YE[sg][r];
           if constexpr (m == 0) v = fmaf(zp[2 * kWH + (ie < NE ? l : 0)], pe0, v);
-          X[(ie < NE ? row_of(l, sg) : kWK) * 16 + i] = v;
+          X[i * kTS + (ie < NE ? row_of(l, sg) : kSpare)] = v;
         }
         if constexpr (NO > 0) {
           const int l = m + 1 + 2 * ie;
           float v = YO[sg][r];
           if constexpr (m == 0) v = fmaf(zp[2 * kWH + (ie < NO ? l : 0)], po0, v);
-          X[(ie < NO ? row_of(l, sg) : kWK) * 16 + i] = v;
+          X[i * kTS + (ie < NO ? row_of(l, sg) : kSpare)] = v;
         }
       });
     });
@@ -360,22 +367,21 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   jpass(std::integral_constant<int, 1>{});
   zrot(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{});
 
-  // ---- 5. store: rows of ko floats of the wave's channels
+  // ---- 5. store: the wave's rows of ko floats as one block (64 consecutive
+  // floats per store, non-temporal)
   {
     float* const yb = y + (b * C + c0) * int64_t(ko);
-    const int c = lane & 15;
-    if (c < cnt) {
-      if (ko == kWK) {
-        float* const yg = yb + int64_t(c) * ko + g;
-        cfor<0, NXL>([&](auto Q) {
-          constexpr int q = decltype(Q)::value;
-          if (4 * q + 3 < kWK || g + 4 * q < kWK) yg[4 * q] = X[(g + 4 * q) * 16 + c];
-        });
-      } else {
-        cfor<0, NXL>([&](auto Q) {
-          const int k = g + 4 * decltype(Q)::value;
-          if (k < ko) yb[int64_t(c) * ko + k] = X[k * 16 + c];
-        });
+    const int tot = cnt * ko;
+    if (full && ko == kWK) {
+      cfor<0, NXL>([&](auto Q) {
+        const int e = lane + 64 * decltype(Q)::value;
+        const int c = e / kWK, k = e - c * kWK;
+        if (e < 16 * kWK) __builtin_nontemporal_store(X[c * kTS + k], yb + e);
+      });
+    } else {
+      for (int e = lane; e < tot; e += 64) {
+        const int c = e / ko, k = e - c * ko;
+        __builtin_nontemporal_store(X[c * kTS + k], yb + e);
       }
     }
   }
