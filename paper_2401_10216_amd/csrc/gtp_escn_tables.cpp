@@ -151,7 +151,7 @@ EscnHost build_escn_tables(const Tables& t) {
       const int d = 2 * l + 1, nk4 = escn_wave_nk4(l);
       for (int mt = 0; mt < escn_wave_nm(l); ++mt)
         for (int lane = 0; lane < 64; ++lane) {
-          const int k = lane / 16, i = lane % 16, row = 16 * mt + i;
+          const int k = lane / 16, i = lane % 16, row = 16 * mt + escn_wave_jrow(i);
           for (int s = 0; s < (d + 3) / 4; ++s) {
             const int col = 4 * s + k;
             if (row >= d || col >= d) continue;

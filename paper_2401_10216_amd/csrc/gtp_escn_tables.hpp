@@ -44,7 +44,8 @@ namespace gtp {
 //        (the edge's D_b = J^T Z(-beta) J Z(-alpha) applied factor by
 //        factor): per degree block l, 16-row tile mt and lane 16 k + i, the
 //        K-steps s = 0 .. NK(l) - 1 (NK = ceil((2l+1) / 4), padded to a
-//        multiple of 4) of J[16 mt + i][4 s + k] at escn_wave_joff(l, mt),
+//        multiple of 4) of J[16 mt + jrow(i)][4 s + k] at escn_wave_joff(l, mt)
+//        (jrow = escn_wave_jrow, the block row of tile row i),
 //        then the same for J^T at escn_wave_jtoff() + escn_wave_joff(l, mt);
 //        zero outside the block.
 struct EscnHost {
@@ -77,6 +78,10 @@ constexpr int escn_wave_joff(int l, int mt) {
   return o + mt * 64 * escn_wave_nk4(l);
 }
 constexpr int escn_wave_jtoff() { return escn_wave_joff(kEscnWaveL + 1, 0); }
+// The block row held by row rho = 4 g + r of a 16-row output tile (register
+// r of lane group g): 2 r + (g & 1) + 8 (g >> 1), so that lane groups 0 and
+// 1 (and 2 and 3), which share a half-wave's LDS access, write rows one apart.
+constexpr int escn_wave_jrow(int rho) { return 2 * (rho & 3) + ((rho >> 2) & 1) + 8 * (rho >> 3); }
 
 // Builds the tables from a plan's tables; empty (NPAIR = 0) unless
 // L1 = L2 = Lout; A and Z only for L1 = kEscnWaveL.

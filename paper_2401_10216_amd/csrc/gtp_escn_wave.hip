@@ -26,7 +26,7 @@
 //   poles        (only m = 0 is non-zero there) on the VALU;
 //   rotate out   y = Z(alpha) J^T Z(beta) J y'.
 // One workgroup per (edge, 64 channels), one wave per 16 channels; LDS holds
-// each wave's coefficient tile [k][16 channels] (75 KB: two workgroups per CU)
+// each wave's coefficient tile [k][16 channels] (74.5 KB: two workgroups per CU)
 // and the edge's trig values.
 #include <type_traits>
 
@@ -43,19 +43,18 @@ constexpr int kWH = kWL + 1;                // 17 radial weights
 constexpr int kWaves = 4;                   // 16-channel tiles per workgroup
 // One wave's tile, channel-major: coefficient k of channel c at c kTS + k,
 // the layout of the wave's 16 rows in memory (contiguous copies in and out).
-// Rows 0..288, row 289 takes the writes of padding rows, rows up to 291 the
-// reads past the last block (whose values are then dropped); the odd stride
-// puts one coefficient of the 16 channels in 16 banks.
-constexpr int kTS = kWK + 4;   // 293
+// Rows 0..288, row 289 takes the writes of padding rows; reads past the last
+// block reach rows 290 and 291, the next channel's first rows (past the last
+// tile: kTilePad), whose values are then dropped.  The LDS serves a wave's
+// access a half-wave (lane groups 0 and 1, or 2 and 3) at a time over 32
+// banks; with the stride = 2 (mod 32) the 16 channels of one row take the
+// even or the odd banks, so two lane groups whose rows are one apart (the
+// rotation stages' reads and writes) are conflict-free.
+constexpr int kTS = kWK + 1;   // 290
 constexpr int kSpare = kWK;    // 289
 constexpr int kTileF = 16 * kTS;
-
-constexpr int pair_l(int p) {
-  int l = 1;
-  while (l * (l + 1) / 2 <= p) ++l;
-  return l;
-}
-constexpr int pair_m(int p) { return p - pair_l(p) * (pair_l(p) - 1) / 2 + 1; }
+constexpr int kTilePad = 4;
+static_assert(kTS % 32 == 2, "bank layout");
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -69,6 +68,13 @@ __device__ __forceinline__ f4 mfma(float a, float b, f4 c) { return __builtin_am
 // it (it only sees the lane's own addresses).
 #define GTP_TILE_ORDER() asm volatile("" ::: "memory")
 
+// A copy of v the compiler cannot see through: addresses derived from it are
+// computed in the stage that uses them, not once and kept live across stages.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 __device__ __forceinline__ float ldx(const float* p, int64_t i) { return p[i]; }
 __device__ __forceinline__ float ldx(const uint16_t* p, int64_t i) { return __uint_as_float(uint32_t(p[i]) << 16); }
 
@@ -77,9 +83,9 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     const TIn* __restrict__ x, const float* __restrict__ rv, const float* __restrict__ h, float* __restrict__ y,
     int64_t C, int ncb, const float* __restrict__ At, const float* __restrict__ Zt, const float* __restrict__ JI,
     int k1, int kh, int ko) {
-  __shared__ __align__(16) float tiles[kWaves * kTileF];
+  __shared__ __align__(16) float tiles[kWaves * kTileF + kTilePad];
   __shared__ float4 tw[kWH];  // (cos m alpha, sin m alpha, cos m beta, sin m beta)
-  lds_poison(tiles, kWaves * kTileF);
+  lds_poison(tiles, kWaves * kTileF + kTilePad);
   lds_poison(reinterpret_cast<float*>(tw), kWH * 4);
   const int tid = threadIdx.x, w = tid >> 6, lane = tid & 63, g = lane >> 4, i = lane & 15;
   const int64_t wg = xcd_product(blockIdx.x, gridDim.x);
@@ -196,75 +202,137 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // ---- rotations about the pole: each (cos m, sin m) pair of the tile turned
   // by m times the edge angle, AB = 0 alpha, 1 beta, SGN = -1 for Z(-angle):
   //   c' = c cos + s sin, s' = -c sin + s cos   (Z(-angle); the transpose for +)
-  // the 136 pairs (l = 1..16, m = 1..l, numbered l (l - 1) / 2 + m - 1), lane
-  // group g taking the pairs numbered g mod 4
+  // Degree by degree, lane group g turning order m = 4 q + g + 1 in step q:
+  // rows l^2 + l + m and l^2 + l - m and the trig entry m are the lane
+  // group's base plus a constant (no per-lane select of addresses).  A lane
+  // past the degree (m > l, in the last step of a degree, l >= 2) turns by
+  // the identity (1, 0), writing back the values it read, of rows in blocks
+  // l + 1 and l - 1, which no other lane of that step touches.  Degree 1 (one
+  // pair) is turned by every lane group alike.
   auto zrot = [&](auto AB, auto SGN) {
     constexpr int ab = decltype(AB)::value, sgn = decltype(SGN)::value;
-    cfor<0, kWL * (kWL + 1) / 8>([&](auto Q) {
-      constexpr int q = decltype(Q)::value;
-      constexpr int l0 = pair_l(4 * q), l1 = pair_l(4 * q + 1), l2 = pair_l(4 * q + 2), l3 = pair_l(4 * q + 3);
-      const int l = g == 0 ? l0 : (g == 1 ? l1 : (g == 2 ? l2 : l3));
-      const int m = g == 0 ? pair_m(4 * q) : (g == 1 ? pair_m(4 * q + 1) : (g == 2 ? pair_m(4 * q + 2) : pair_m(4 * q + 3)));
-      const float4 t = tw[m];
-      const float cm = ab ? t.z : t.x, sm = ab ? t.w : t.y;
-      const int rc = l * l + l + m, rs = l * l + l - m;
-      const float c = X[i * kTS + rc], sv = X[i * kTS + rs];
+    const int gz = opaque(g);
+    float* const Xp = X + i * kTS + gz;      // rows r + g
+    float* const Xn = X + i * kTS + 3 - gz;  // rows r + 3 - g
+    auto turn = [&](float& c, float& sv, float cm, float sm) {
+      const float c0 = c, s0 = sv;
       if constexpr (sgn < 0) {
-        X[i * kTS + rc] = fmaf(c, cm, sv * sm);
-        X[i * kTS + rs] = fmaf(sv, cm, -c * sm);
+        c = fmaf(c0, cm, s0 * sm);
+        sv = fmaf(s0, cm, -c0 * sm);
       } else {
-        X[i * kTS + rc] = fmaf(c, cm, -sv * sm);
-        X[i * kTS + rs] = fmaf(sv, cm, c * sm);
+        c = fmaf(c0, cm, -s0 * sm);
+        sv = fmaf(s0, cm, c0 * sm);
       }
-    });
+    };
+    {
+      const float4 t = tw[1];
+      float c = X[i * kTS + 3], sv = X[i * kTS + 1];
+      turn(c, sv, ab ? t.z : t.x, ab ? t.w : t.y);
+      X[i * kTS + 3] = c;
+      X[i * kTS + 1] = sv;
+    }
     GTP_TILE_ORDER();
+    cfor<2, kWL + 1>([&](auto LL) {
+      constexpr int l = decltype(LL)::value;
+      cfor<0, (l + 3) / 4>([&](auto Q) {
+        constexpr int m0 = 4 * decltype(Q)::value + 1;
+        constexpr int rc = l * l + l + m0, rs = l * l + l - m0 - 3;  // rs >= l^2 - 3 + 3 - 3 >= 1
+        const float4 t = tw[m0 + gz];  // m0 + g <= 16
+        float cm = ab ? t.z : t.x, sm = ab ? t.w : t.y;
+        if constexpr (m0 + 3 > l) {  // the step's lane groups past the degree: identity
+          const bool ok = m0 + gz <= l;
+          cm = ok ? cm : 1.0f;
+          sm = ok ? sm : 0.0f;
+        }
+        float c = Xp[rc], sv = Xn[rs];
+        turn(c, sv, cm, sm);
+        Xp[rc] = c;
+        Xn[rs] = sv;
+      });
+      // a degree's identity writes precede the next degree's accesses of the
+      // same rows (by other lane groups, at other constant offsets)
+      GTP_TILE_ORDER();
+    });
   };
   // ---- the fixed matrix J (TR = 0) or J^T (TR = 1) on every degree block
   // (M = rows, K = columns), two blocks at a time: the MFMAs of both, then
   // their writes (blocks touch disjoint rows; a block's reads precede its
-  // writes).  Operand images: lane-permuted, four K-steps per 16-byte load.
+  // writes).  Operand images: lane-permuted, four K-steps per 16-byte load;
+  // row 4 g + r of a 16-row output tile holds block row escn_wave_jrow(4 g + r).
   auto jpass = [&](auto TR) {
     constexpr int tr = decltype(TR)::value;
+    const int gj = opaque(g);
     const float* const img = JI + (tr ? escn_wave_jtoff() : 0);
-    auto mma = [&](auto LL, auto& acc) {
+    constexpr int NPR = (kWL + 2) / 2;  // block pairs (2 p, 2 p + 1); the last holds degree 16 alone
+    // a block's operands (arrays sized for degree 16): the A images and the
+    // B values (column 4 ks + g of the block, channel i)
+    auto load = [&](auto LL, f4(&a)[3][3], float(&bv)[9]) {
       constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), NK = (d + 3) / 4;
       constexpr int NK4 = escn_wave_nk4(l), R0 = l * l;
-      f4 a[NM][NK4 / 4];
       cfor<0, NM>([&](auto M) {
         constexpr int mt = decltype(M)::value;
         const f4* const src = reinterpret_cast<const f4*>(img + escn_wave_joff(l, mt) + lane * NK4);
         cfor<0, NK4 / 4>([&](auto Q) { a[mt][decltype(Q)::value] = src[decltype(Q)::value]; });
       });
-      cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
       cfor<0, NK>([&](auto KS) {
         constexpr int ks = decltype(KS)::value;
         const int c = 4 * ks + g;
-        const float bv = xrd_block(R0 + c, c < d);
+        bv[ks] = xrd_block(R0 + c, c < d);
+      });
+    };
+    auto mma = [&](auto LL, const f4(&a)[3][3], const float(&bv)[9], f4(&acc)[3]) {
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), NK = (d + 3) / 4;
+      cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
+      cfor<0, NK>([&](auto KS) {
+        constexpr int ks = decltype(KS)::value;
         cfor<0, NM>([&](auto M) {
           constexpr int mt = decltype(M)::value;
-          acc[mt] = mfma(a[mt][ks / 4][ks % 4], bv, acc[mt]);
+          acc[mt] = mfma(a[mt][ks / 4][ks % 4], bv[ks], acc[mt]);
         });
       });
     };
-    auto store = [&](auto LL, const auto& acc) {
+    // Rows of a block's last tile past the block (A rows there are zero) are
+    // written unconditionally, into blocks l + 1 .. that the pass has read
+    // already and writes later (blocks up to l0 + 3 for the pair (l0, l1):
+    // checked for every l by the host replay), except for degree 1, whose
+    // padding reaches block 4, and degree 16, whose padding lies past the
+    // tile's rows: those go to the spare row.
+    const int jb = i * kTS + escn_wave_jrow(4 * gj);  // + 2 r + 16 mt + l^2
+    auto store = [&](auto LL, const f4(&acc)[3]) {
       constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), R0 = l * l;
       cfor<0, NM>([&](auto M) {
         constexpr int mt = decltype(M)::value;
         cfor<0, 4>([&](auto RR) {
           constexpr int r = decltype(RR)::value;
-          const int row = 16 * mt + 4 * g + r;
-          X[i * kTS + (row < d ? R0 + row : kSpare)] = acc[mt][r];
+          if constexpr ((l == 1 || l == kWL) && 16 * mt + 15 >= d) {
+            const int row = 16 * mt + escn_wave_jrow(4 * gj + r);
+            X[i * kTS + (row < d ? R0 + row : kSpare)] = acc[mt][r];
+          } else {
+            X[jb + R0 + 16 * mt + 2 * r] = acc[mt][r];
+          }
         });
       });
     };
-    cfor<0, (kWL + 2) / 2>([&](auto PP) {
-      constexpr int l0 = 2 * decltype(PP)::value, l1 = l0 + 1 <= kWL ? l0 + 1 : l0;
-      f4 a0[escn_wave_nm(l0)], a1[escn_wave_nm(l1)];
-      mma(std::integral_constant<int, l0>{}, a0);
-      if constexpr (l1 != l0) mma(std::integral_constant<int, l1>{}, a1);
+    // blocks touch disjoint rows and each is read before it is written: the
+    // operands of pair p + 1 are read before the writes of pair p
+    f4 a0[3][3], a1[3][3];
+    float b0[9], b1[9];
+    load(std::integral_constant<int, 0>{}, a0, b0);
+    load(std::integral_constant<int, 1>{}, a1, b1);
+    cfor<0, NPR>([&](auto PP) {
+      constexpr int p = decltype(PP)::value, l0 = 2 * p, l1 = l0 + 1 <= kWL ? l0 + 1 : l0;
+      f4 c0[3], c1[3];
+      mma(std::integral_constant<int, l0>{}, a0, b0, c0);
+      if constexpr (l1 != l0) mma(std::integral_constant<int, l1>{}, a1, b1, c1);
+      if constexpr (p + 1 < NPR) {
+        constexpr int n0 = l0 + 2, n1 = n0 + 1 <= kWL ? n0 + 1 : n0;
+        load(std::integral_constant<int, n0>{}, a0, b0);
+        if constexpr (n1 != n0) load(std::integral_constant<int, n1>{}, a1, b1);
+      }
       GTP_TILE_ORDER();
-      store(std::integral_constant<int, l0>{}, a0);
-      if constexpr (l1 != l0) store(std::integral_constant<int, l1>{}, a1);
+      store(std::integral_constant<int, l0>{}, c0);
+      GTP_TILE_ORDER();  // block l1's rows after block l0's padding rows
+      if constexpr (l1 != l0) store(std::integral_constant<int, l1>{}, c1);
     });
     GTP_TILE_ORDER();
   };

@@ -193,6 +193,12 @@ def joff(l, mt):
     return sum(nm(k) * 64 * nk4(k) for k in range(l)) + mt * 64 * nk4(l)
 
 
+def jrow(rho):
+    """Block row of output-tile row rho = 4 g + r: 2 r + (g & 1) + 8 (g >> 1)."""
+    g, r = rho // 4, rho % 4
+    return 2 * r + (g & 1) + 8 * (g >> 1)
+
+
 def j_blocks(p):
     J = p.table(10)
     out, o = [], 0
@@ -219,7 +225,8 @@ def z_rot(l, angle, sign):
 
 
 def test_rotation_images_and_factorization(plan):
-    """Table 14 holds J and J^T in the lane-permuted K-step layout, and the
+    """Table 14 holds J and J^T in the lane-permuted K-step layout (tile rows
+    permuted by jrow, a bijection of 0..15), and the
     kernel's factor-by-factor rotation J^T Z(-beta) J Z(-alpha) (angles from
     the edge vector as the kernel takes them) gives the oracle's product."""
     p, info, S, W, A, Z = plan
@@ -232,7 +239,7 @@ def test_rotation_images_and_factorization(plan):
         for mt in range(nm(l)):
             for lane in range(64):
                 k, i = lane // 16, lane % 16
-                row = 16 * mt + i
+                row = 16 * mt + jrow(i)
                 for s in range((d + 3) // 4):
                     col = 4 * s + k
                     at = joff(l, mt) + lane * nk4(l) + s
@@ -252,3 +259,69 @@ def test_rotation_images_and_factorization(plan):
         y = replay_tile(x.T.copy(), hm, D, A, Z).T
         ref = O.conv_escn(x[None], r[None], hm[None], L, L, L)[0]
         assert O.max_rel_err(y, ref) < 1e-11
+
+
+def jpass_replay(T, JI, tr):
+    """The degree-16 kernel's pass of J (tr = 0) or J^T (tr = 1) over a tile
+    T[row][channel], replayed in the kernel's program order: block pairs
+    (2p, 2p + 1) (degree 16 alone), the operands (B values) of pair p + 1
+    read before pair p's writes, the rows of a block's last tile past the
+    block written as they come (zero rows of the product), except for
+    degrees 1 and 16, whose padding goes to the spare row 289."""
+    img = JI[tr * joff(L + 1, 0):]
+    T = T.copy()
+    lanes = np.arange(64)
+    g_of, i_of = lanes // 16, lanes % 16
+
+    def load(l):
+        d, R0, nk = 2 * l + 1, l * l, nk4(l)
+        A = [img[joff(l, mt):joff(l, mt) + 64 * nk].reshape(64, nk) for mt in range(nm(l))]
+        B = []
+        for ks in range((d + 3) // 4):
+            c = 4 * ks + g_of
+            B.append(np.where(c < d, T[R0 + c, i_of], 0.0))
+        return A, B
+
+    def mma(l, A, B):
+        return [sum(mfma(A[mt][:, ks], B[ks], np.zeros((16, 16))) for ks in range(len(B))) for mt in range(nm(l))]
+
+    def store(l, acc):
+        d, R0 = 2 * l + 1, l * l
+        for mt in range(nm(l)):
+            for r in range(4):
+                row = 16 * mt + np.array([jrow(4 * g + r) for g in g_of])
+                v = acc[mt][4 * g_of + r, i_of]
+                if l in (1, L) and 16 * mt + 15 >= d:
+                    tgt = np.where(row < d, R0 + row, 289)
+                else:
+                    tgt = R0 + row
+                assert tgt.max() <= 289
+                T[tgt, i_of] = v
+
+    pairs = [(2 * p, 2 * p + 1) for p in range(L // 2)] + [(L,)]
+    ops = {l: load(l) for l in pairs[0]}
+    for p, pr in enumerate(pairs):
+        acc = {l: mma(l, *ops[l]) for l in pr}
+        if p + 1 < len(pairs):
+            ops = {l: load(l) for l in pairs[p + 1]}
+        for l in pr:
+            store(l, acc[l])
+    return T
+
+
+def test_jpass_replay_padded_writes(plan):
+    """The J and J^T passes as the kernel orders them equal the block-wise
+    products on every degree block (so no padded write lands on a row that is
+    read or kept afterwards), and rows 290, 291 (the next channel's) are
+    never written."""
+    p = plan[0]
+    JI = p.table(14)
+    Jb = j_blocks(p)
+    rng = np.random.default_rng(1818)
+    T0 = rng.standard_normal((292, 16))
+    for tr in (0, 1):
+        T = jpass_replay(T0, JI, tr)
+        for l in range(L + 1):
+            blk = Jb[l].T if tr else Jb[l]
+            np.testing.assert_allclose(T[l * l:(l + 1) ** 2], blk @ T0[l * l:(l + 1) ** 2], rtol=1e-12, atol=1e-12)
+        np.testing.assert_array_equal(T[290:], T0[290:])
