@@ -347,6 +347,23 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // ---- 3. the zonal product per order m, its cos and sin parts together
   // (m-parts touch disjoint rows)
   const float* const zp = Zt + 16 * kWH;
+  // the synthesis B values of order m, xz[sg][t]: degree m + 2 (4 t + g) for
+  // t < KE (even set), m + 1 + 2 (4 (t - KE) + g) after; order m + 1's are
+  // read before order m's writes (disjoint rows)
+  auto zrd = [&](auto MM, float(&xz)[2][5]) {
+    constexpr int m = decltype(MM)::value, n = kWL + 1 - m, NE = (n + 1) / 2, NO = n / 2;
+    constexpr int KE = (NE + 3) / 4, KO = (NO + 3) / 4, NSG = m == 0 ? 1 : 2;
+    cfor<0, NSG>([&](auto SG) {
+      constexpr int sg = decltype(SG)::value;
+      cfor<0, KE + KO>([&](auto T) {
+        constexpr int t = decltype(T)::value;
+        const int l = t < KE ? m + 2 * (4 * t + g) : m + 1 + 2 * (4 * (t - KE) + g);
+        xz[sg][t] = xrd(l * l + l + (sg ? -m : m), l <= kWL);
+      });
+    });
+  };
+  float xz[2][5];
+  zrd(std::integral_constant<int, 0>{}, xz);
   cfor<0, kWL + 1>([&](auto MM) {
     constexpr int m = decltype(MM)::value, n = kWL + 1 - m, NE = (n + 1) / 2, NO = n / 2;
     constexpr int KE = (NE + 3) / 4, KO = (NO + 3) / 4, NSG = m == 0 ? 1 : 2;
@@ -365,7 +382,7 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       const int l = m + 2 * (4 * ks + g);
       cfor<0, NSG>([&](auto SG) {
         constexpr int sg = decltype(SG)::value;
-        GE[sg] = mfma(av(ks), xrd(row_of(l, sg), l <= kWL), GE[sg]);
+        GE[sg] = mfma(av(ks), xz[sg][ks], GE[sg]);
       });
     });
     cfor<0, KO>([&](auto KS) {
@@ -373,9 +390,10 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       const int l = m + 1 + 2 * (4 * ks + g);
       cfor<0, NSG>([&](auto SG) {
         constexpr int sg = decltype(SG)::value;
-        GO[sg] = mfma(av(KE + ks), xrd(row_of(l, sg), l <= kWL), GO[sg]);
+        GO[sg] = mfma(av(KE + ks), xz[sg][KE + ks], GO[sg]);
       });
     });
+    if constexpr (m + 1 <= kWL) zrd(std::integral_constant<int, m + 1>{}, xz);
     // pole pair (m = 0 only): the lane's channel, every lane group alike
     float pe0 = 0.0f, po0 = 0.0f;
     if constexpr (m == 0) {
