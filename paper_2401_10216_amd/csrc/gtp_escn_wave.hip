@@ -204,10 +204,10 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   //   c' = c cos + s sin, s' = -c sin + s cos   (Z(-angle); the transpose for +)
   // Degree by degree, lane group g turning order m = 4 q + g + 1 in step q:
   // rows l^2 + l + m and l^2 + l - m and the trig entry m are the lane
-  // group's base plus a constant (no per-lane select of addresses).  A lane
-  // past the degree (m > l, in the last step of a degree, l >= 2) turns by
-  // the identity (1, 0), writing back the values it read, of rows in blocks
-  // l + 1 and l - 1, which no other lane of that step touches.  Degree 1 (one
+  // group's base plus a constant.  A lane past the degree (m > l, in the
+  // last step of a degree, l >= 2) reads rows of blocks l + 1 and l - 1 and
+  // writes the spare row, so every row of the tile is read and written by
+  // one step of one lane and the steps may run in any order.  Degree 1 (one
   // pair) is turned by every lane group alike.
   auto zrot = [&](auto AB, auto SGN) {
     constexpr int ab = decltype(AB)::value, sgn = decltype(SGN)::value;
@@ -231,28 +231,25 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
       X[i * kTS + 3] = c;
       X[i * kTS + 1] = sv;
     }
-    GTP_TILE_ORDER();
     cfor<2, kWL + 1>([&](auto LL) {
       constexpr int l = decltype(LL)::value;
       cfor<0, (l + 3) / 4>([&](auto Q) {
         constexpr int m0 = 4 * decltype(Q)::value + 1;
-        constexpr int rc = l * l + l + m0, rs = l * l + l - m0 - 3;  // rs >= l^2 - 3 + 3 - 3 >= 1
+        constexpr int rc = l * l + l + m0, rs = l * l + l - m0 - 3;  // rs >= 1 (l >= 2)
         const float4 t = tw[m0 + gz];  // m0 + g <= 16
-        float cm = ab ? t.z : t.x, sm = ab ? t.w : t.y;
-        if constexpr (m0 + 3 > l) {  // the step's lane groups past the degree: identity
-          const bool ok = m0 + gz <= l;
-          cm = ok ? cm : 1.0f;
-          sm = ok ? sm : 0.0f;
-        }
         float c = Xp[rc], sv = Xn[rs];
-        turn(c, sv, cm, sm);
-        Xp[rc] = c;
-        Xn[rs] = sv;
+        turn(c, sv, ab ? t.z : t.x, ab ? t.w : t.y);
+        if constexpr (m0 + 3 > l) {  // lane groups past the degree write the spare row
+          const bool ok = m0 + gz <= l;
+          X[i * kTS + (ok ? rc + gz : kSpare)] = c;
+          X[i * kTS + (ok ? rs + 3 - gz : kSpare)] = sv;
+        } else {
+          Xp[rc] = c;
+          Xn[rs] = sv;
+        }
       });
-      // a degree's identity writes precede the next degree's accesses of the
-      // same rows (by other lane groups, at other constant offsets)
-      GTP_TILE_ORDER();
     });
+    GTP_TILE_ORDER();
   };
   // ---- the fixed matrix J (TR = 0) or J^T (TR = 1) on every degree block
   // (M = rows, K = columns), two blocks at a time: the MFMAs of both, then
