@@ -148,18 +148,23 @@ EscnHost build_escn_tables(const Tables& t) {
     e.JI.assign(size_t(2 * escn_wave_jtoff()), 0.0);
     size_t jo = 0;
     for (int l = 0; l <= L; ++l) {
-      const int d = 2 * l + 1, nk4 = escn_wave_nk4(l);
-      for (int mt = 0; mt < escn_wave_nm(l); ++mt)
+      const int d = 2 * l + 1;
+      for (int t = 0; t < escn_wave_jtiles(l); ++t) {
+        const int nk4 = escn_wave_jnk4(l, t);
         for (int lane = 0; lane < 64; ++lane) {
-          const int k = lane / 16, i = lane % 16, row = 16 * mt + escn_wave_jrow(i);
-          for (int s = 0; s < (d + 3) / 4; ++s) {
-            const int col = 4 * s + k;
-            if (row >= d || col >= d) continue;
-            const size_t at = size_t(escn_wave_joff(l, mt)) + size_t(lane) * nk4 + s;
+          const int k = lane / 16, i = lane % 16, row = escn_wave_jtrow(l, t, i);
+          // class tiles: rows of one lane-group parity meet only the columns
+          // of the same parity (the other sub-blocks of J are zero)
+          const bool same = l < kEscnClassL || ((i / 4) & 1) == (k & 1);
+          for (int s = 0; s < escn_wave_jsteps(l, t); ++s) {
+            const int col = escn_wave_jtcol(l, t, s, k);
+            if (row < 0 || col < 0 || !same) continue;
+            const size_t at = size_t(escn_wave_joff(l, t)) + size_t(lane) * nk4 + s;
             e.JI[at] = e.J[jo + size_t(row) * d + col];                          // J[row][col]
             e.JI[escn_wave_jtoff() + at] = e.J[jo + size_t(col) * d + row];      // J^T[row][col]
           }
         }
+      }
       jo += size_t(d) * d;
     }
   }

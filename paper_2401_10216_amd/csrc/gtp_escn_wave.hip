@@ -252,68 +252,113 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
     GTP_TILE_ORDER();
   };
   // ---- the fixed matrix J (TR = 0) or J^T (TR = 1) on every degree block
-  // (M = rows, K = columns), two blocks at a time: the MFMAs of both, then
-  // their writes (blocks touch disjoint rows; a block's reads precede its
-  // writes).  Operand images: lane-permuted, four K-steps per 16-byte load;
-  // row 4 g + r of a 16-row output tile holds block row escn_wave_jrow(4 g + r).
+  // (M = rows, K = columns), in the output tiles of the operand images
+  // (escn_wave_jtile: below degree 8 the whole block; from degree 8 on the
+  // four class sub-blocks, two per tile), two blocks at a time: the MFMAs of
+  // both, then their writes (blocks touch disjoint rows; a block's reads
+  // precede its writes).  Operand images: lane-permuted, four K-steps per
+  // 16-byte load.
   auto jpass = [&](auto TR) {
     constexpr int tr = decltype(TR)::value;
     const int gj = opaque(g);
+    const int gp = gj & 1, gh = gj >> 1;  // lane-group parity and half
     const float* const img = JI + (tr ? escn_wave_jtoff() : 0);
     constexpr int NPR = (kWL + 2) / 2;  // block pairs (2 p, 2 p + 1); the last holds degree 16 alone
-    // a block's operands (arrays sized for degree 16): the A images and the
-    // B values (column 4 ks + g of the block, channel i)
-    auto load = [&](auto LL, f4(&a)[3][3], float(&bv)[9]) {
-      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), NK = (d + 3) / 4;
-      constexpr int NK4 = escn_wave_nk4(l), R0 = l * l;
-      cfor<0, NM>([&](auto M) {
-        constexpr int mt = decltype(M)::value;
-        const f4* const src = reinterpret_cast<const f4*>(img + escn_wave_joff(l, mt) + lane * NK4);
-        cfor<0, NK4 / 4>([&](auto Q) { a[mt][decltype(Q)::value] = src[decltype(Q)::value]; });
-      });
-      cfor<0, NK>([&](auto KS) {
-        constexpr int ks = decltype(KS)::value;
-        const int c = 4 * ks + g;
-        bv[ks] = xrd_block(R0 + c, c < d);
+    // class tiles: the block-local first index of a half's classes (rows and
+    // the columns they map to); a half without rows takes the other's
+    auto rstart = [](int l, int t, int par) {
+      const int c = escn_wave_jtcls(l, t, par) < 0 ? escn_wave_jtcls(l, t, 0) : escn_wave_jtcls(l, t, par);
+      return escn_cls_start(l, c) + 2 * escn_wave_jtfirst(t);
+    };
+    auto cstart = [](int l, int t, int par) {
+      const int c = escn_wave_jtcls(l, t, par) < 0 ? escn_wave_jtcls(l, t, 0) : escn_wave_jtcls(l, t, par);
+      return escn_cls_start(l, escn_cls_map(l, c));
+    };
+    const int ib2 = i * kTS + 2 * gh, ib8 = i * kTS + 8 * gh;
+    // a block's operands (arrays sized for the largest block): per tile the
+    // A images and the B values of its K-steps (channel i)
+    auto load = [&](auto LL, f4(&a)[3][2], float(&bv)[3][5]) {
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, R0 = l * l;
+      cfor<0, escn_wave_jtiles(l)>([&](auto TT) {
+        constexpr int t = decltype(TT)::value, NK4 = escn_wave_jnk4(l, t), NS = escn_wave_jsteps(l, t);
+        const f4* const src = reinterpret_cast<const f4*>(img + escn_wave_joff(l, t) + lane * NK4);
+        cfor<0, NK4 / 4>([&](auto Q) { a[t][decltype(Q)::value] = src[decltype(Q)::value]; });
+        if constexpr (l < kEscnClassL) {
+          cfor<0, NS>([&](auto KS) {
+            constexpr int ks = decltype(KS)::value;
+            const int c = 4 * ks + g;
+            bv[t][ks] = xrd_block(R0 + c, c < d);
+          });
+        } else {
+          // column element q = 2 ks + g / 2 of the half's class: block index
+          // first + 2 q (past the class: a value of the tile, dropped)
+          constexpr int C0 = escn_wave_jtcols(l, t, 0), C1 = escn_wave_jtcols(l, t, 1);
+          const int cb = ib2 + (gp ? cstart(l, t, 1) : cstart(l, t, 0));
+          cfor<0, NS>([&](auto KS) {
+            constexpr int ks = decltype(KS)::value;
+            const float v = X[cb + R0 + 4 * ks];
+            if constexpr (2 * ks + 1 < (C0 < C1 ? C0 : C1)) {
+              bv[t][ks] = v;
+            } else {
+              bv[t][ks] = 2 * ks + gh < (gp ? C1 : C0) ? v : 0.0f;
+            }
+          });
+        }
       });
     };
-    auto mma = [&](auto LL, const f4(&a)[3][3], const float(&bv)[9], f4(&acc)[3]) {
-      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), NK = (d + 3) / 4;
-      cfor<0, NM>([&](auto M) { acc[decltype(M)::value] = f4{0.0f, 0.0f, 0.0f, 0.0f}; });
-      cfor<0, NK>([&](auto KS) {
-        constexpr int ks = decltype(KS)::value;
-        cfor<0, NM>([&](auto M) {
-          constexpr int mt = decltype(M)::value;
-          acc[mt] = mfma(a[mt][ks / 4][ks % 4], bv[ks], acc[mt]);
+    auto mma = [&](auto LL, const f4(&a)[3][2], const float(&bv)[3][5], f4(&acc)[3]) {
+      constexpr int l = decltype(LL)::value;
+      cfor<0, escn_wave_jtiles(l)>([&](auto TT) {
+        constexpr int t = decltype(TT)::value;
+        acc[t] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        cfor<0, escn_wave_jsteps(l, t)>([&](auto KS) {
+          constexpr int ks = decltype(KS)::value;
+          acc[t] = mfma(a[t][ks / 4][ks % 4], bv[t][ks], acc[t]);
         });
       });
     };
-    // Rows of a block's last tile past the block (A rows there are zero) are
-    // written unconditionally, into blocks l + 1 .. that the pass has read
-    // already and writes later (blocks up to l0 + 3 for the pair (l0, l1):
-    // checked for every l by the host replay), except for degree 1, whose
-    // padding reaches block 4, and degree 16, whose padding lies past the
-    // tile's rows: those go to the spare row.
-    const int jb = i * kTS + escn_wave_jrow(4 * gj);  // + 2 r + 16 mt + l^2
+    // Whole-block tiles (degrees below 8): rows past the block (A rows there
+    // are zero) are written unconditionally, into blocks l + 1 .. that the
+    // pass has read already and writes later (blocks up to l0 + 3 for the
+    // pair (l0, l1): checked for every l by the host replay), except for
+    // degree 1, whose padding reaches block 4: it goes to the spare row, as
+    // do the padding rows of the class tiles.
+    const int jb = i * kTS + escn_wave_jrow(4 * gj);  // + 2 r + l^2
     auto store = [&](auto LL, const f4(&acc)[3]) {
-      constexpr int l = decltype(LL)::value, d = 2 * l + 1, NM = escn_wave_nm(l), R0 = l * l;
-      cfor<0, NM>([&](auto M) {
-        constexpr int mt = decltype(M)::value;
+      constexpr int l = decltype(LL)::value, d = 2 * l + 1, R0 = l * l;
+      if constexpr (l < kEscnClassL) {
         cfor<0, 4>([&](auto RR) {
           constexpr int r = decltype(RR)::value;
-          if constexpr ((l == 1 || l == kWL) && 16 * mt + 15 >= d) {
-            const int row = 16 * mt + escn_wave_jrow(4 * gj + r);
-            X[i * kTS + (row < d ? R0 + row : kSpare)] = acc[mt][r];
+          if constexpr (l == 1) {
+            const int row = escn_wave_jrow(4 * gj + r);
+            X[i * kTS + (row < d ? R0 + row : kSpare)] = acc[0][r];
           } else {
-            X[jb + R0 + 16 * mt + 2 * r] = acc[mt][r];
+            X[jb + R0 + 2 * r] = acc[0][r];
           }
         });
-      });
+      } else {
+        cfor<0, escn_wave_jtiles(l)>([&](auto TT) {
+          constexpr int t = decltype(TT)::value;
+          // row element p = 4 (g / 2) + r of the half's class: block index
+          // first + 2 p; past the class: the spare row
+          constexpr int N0 = escn_wave_jtrows(l, t, 0), N1 = escn_wave_jtrows(l, t, 1);
+          const int rb = ib8 + (gp ? rstart(l, t, 1) : rstart(l, t, 0));
+          cfor<0, 4>([&](auto RR) {
+            constexpr int r = decltype(RR)::value;
+            if constexpr (4 + r < (N0 < N1 ? N0 : N1)) {
+              X[rb + R0 + 2 * r] = acc[t][r];
+            } else {
+              const bool ok = 4 * gh + r < (gp ? N1 : N0);
+              X[ok ? rb + R0 + 2 * r : i * kTS + kSpare] = acc[t][r];
+            }
+          });
+        });
+      }
     };
     // blocks touch disjoint rows and each is read before it is written: the
     // operands of pair p + 1 are read before the writes of pair p
-    f4 a0[3][3], a1[3][3];
-    float b0[9], b1[9];
+    f4 a0[3][2], a1[3][2];
+    float b0[3][5], b1[3][5];
     load(std::integral_constant<int, 0>{}, a0, b0);
     load(std::integral_constant<int, 1>{}, a1, b1);
     cfor<0, NPR>([&](auto PP) {

@@ -181,22 +181,76 @@ def test_replay_matches_oracle(plan):
         assert err < 1e-11, err
 
 
-def nk4(l):
-    return (((2 * l + 1) + 3) // 4 + 3) // 4 * 4
+CLASS_L = 8
 
 
-def nm(l):
-    return (2 * l + 1 + 15) // 16
+def cls_n(l, c):
+    return l // 2 + 1 if c == 0 else (l // 2 if c == 2 else (l + 1) // 2)
 
 
-def joff(l, mt):
-    return sum(nm(k) * 64 * nk4(k) for k in range(l)) + mt * 64 * nk4(l)
+def cls_start(l, c):
+    return [l, l + 1, l & 1, 1 - (l & 1)][c]
+
+
+def cls_map(l, c):
+    return [3, 1, 2, 0][c] if l & 1 else [0, 2, 1, 3][c]
+
+
+def jtiles(l):
+    return 1 if l < CLASS_L else (3 if cls_n(l, 0) > 8 else 2)
+
+
+def jtcls(t, par):
+    return [[0, 3], [1, 2], [0, -1]][t][par]
+
+
+def jtfirst(t):
+    return 8 if t == 2 else 0
+
+
+def jtrows(l, t, par):
+    c = jtcls(t, par)
+    return 0 if c < 0 else min(cls_n(l, c) - jtfirst(t), 8)
+
+
+def jtcols(l, t, par):
+    c = jtcls(t, par)
+    return 0 if c < 0 else cls_n(l, cls_map(l, c))
+
+
+def jsteps(l, t):
+    return (2 * l + 1 + 3) // 4 if l < CLASS_L else (max(jtcols(l, t, 0), jtcols(l, t, 1)) + 1) // 2
+
+
+def jnk4(l, t):
+    return (jsteps(l, t) + 3) // 4 * 4
+
+
+def joff(l, t):
+    return sum(64 * jnk4(k, u) for k in range(l) for u in range(jtiles(k))) + sum(64 * jnk4(l, u) for u in range(t))
 
 
 def jrow(rho):
-    """Block row of output-tile row rho = 4 g + r: 2 r + (g & 1) + 8 (g >> 1)."""
+    """Block row of whole-block tile row rho = 4 g + r: 2 r + (g & 1) + 8 (g >> 1)."""
     g, r = rho // 4, rho % 4
     return 2 * r + (g & 1) + 8 * (g >> 1)
+
+
+def jtrow(l, t, i):
+    """Block-local row of tile row i (-1: padding)."""
+    if l < CLASS_L:
+        return jrow(i) if jrow(i) < 2 * l + 1 else -1
+    g, r = i // 4, i % 4
+    par, pp = g & 1, 4 * (g // 2) + r
+    return cls_start(l, jtcls(t, par)) + 2 * (jtfirst(t) + pp) if pp < jtrows(l, t, par) else -1
+
+
+def jtcol(l, t, s, k):
+    """Block-local column of tile column 4 s + k (-1: padding)."""
+    if l < CLASS_L:
+        return 4 * s + k if 4 * s + k < 2 * l + 1 else -1
+    par, q = k & 1, 2 * s + k // 2
+    return cls_start(l, cls_map(l, jtcls(t, par))) + 2 * q if q < jtcols(l, t, par) else -1
 
 
 def j_blocks(p):
@@ -225,27 +279,35 @@ def z_rot(l, angle, sign):
 
 
 def test_rotation_images_and_factorization(plan):
-    """Table 14 holds J and J^T in the lane-permuted K-step layout (tile rows
-    permuted by jrow, a bijection of 0..15), and the
-    kernel's factor-by-factor rotation J^T Z(-beta) J Z(-alpha) (angles from
-    the edge vector as the kernel takes them) gives the oracle's product."""
+    """Table 14 holds J and J^T in the lane-permuted K-step layout of the
+    output tiles (whole blocks below degree 8, class sub-blocks from 8 on;
+    every non-zero of J in exactly one entry), and the kernel's
+    factor-by-factor rotation J^T Z(-beta) J Z(-alpha) (angles from the edge
+    vector as the kernel takes them) gives the oracle's product."""
     p, info, S, W, A, Z = plan
     JI = p.table(14)
     Jb = j_blocks(p)
     jt = joff(L + 1, 0)
     assert JI.size == 2 * jt
     for l in range(L + 1):
-        d = 2 * l + 1
-        for mt in range(nm(l)):
+        covered = np.zeros((2 * l + 1, 2 * l + 1), dtype=int)
+        for t in range(jtiles(l)):
             for lane in range(64):
                 k, i = lane // 16, lane % 16
-                row = 16 * mt + jrow(i)
-                for s in range((d + 3) // 4):
-                    col = 4 * s + k
-                    at = joff(l, mt) + lane * nk4(l) + s
-                    want = Jb[l][row, col] if (row < d and col < d) else 0.0
-                    wantt = Jb[l][col, row] if (row < d and col < d) else 0.0
+                row = jtrow(l, t, i)
+                same = l < CLASS_L or ((i // 4) & 1) == (k & 1)
+                for s in range(jsteps(l, t)):
+                    col = jtcol(l, t, s, k)
+                    at = joff(l, t) + lane * jnk4(l, t) + s
+                    ok = row >= 0 and col >= 0 and same
+                    want = Jb[l][row, col] if ok else 0.0
+                    wantt = Jb[l][col, row] if ok else 0.0
                     assert JI[at] == want and JI[jt + at] == wantt
+                    if ok:
+                        covered[row, col] += 1
+        # every non-zero of J is in exactly one tile entry
+        assert np.all(covered[np.abs(Jb[l]) > 1e-12] == 1)
+        assert covered.max() <= 1
     rng = np.random.default_rng(1717)
     K = (L + 1) ** 2
     for r in (np.array([0.3, -1.2, 0.7]), np.array([0.0, 0.0, -2.0]), np.array([0.0, 0.0, 0.0]),
@@ -265,36 +327,55 @@ def jpass_replay(T, JI, tr):
     """The degree-16 kernel's pass of J (tr = 0) or J^T (tr = 1) over a tile
     T[row][channel], replayed in the kernel's program order: block pairs
     (2p, 2p + 1) (degree 16 alone), the operands (B values) of pair p + 1
-    read before pair p's writes, the rows of a block's last tile past the
-    block written as they come (zero rows of the product), except for
-    degrees 1 and 16, whose padding goes to the spare row 289."""
+    read before pair p's writes, the addresses the kernel forms.  Whole-block
+    tiles (degrees below 8) write the rows past the block as they come (zero
+    rows of the product), except degree 1, whose padding goes to the spare
+    row 289, as does the padding of the class tiles."""
     img = JI[tr * joff(L + 1, 0):]
     T = T.copy()
     lanes = np.arange(64)
     g_of, i_of = lanes // 16, lanes % 16
+    gp, gh = g_of & 1, g_of >> 1
+
+    def start(l, t, par, rows):
+        c = jtcls(t, par) if jtcls(t, par) >= 0 else jtcls(t, 0)
+        return cls_start(l, c) + 2 * jtfirst(t) if rows else cls_start(l, cls_map(l, c))
 
     def load(l):
-        d, R0, nk = 2 * l + 1, l * l, nk4(l)
-        A = [img[joff(l, mt):joff(l, mt) + 64 * nk].reshape(64, nk) for mt in range(nm(l))]
-        B = []
-        for ks in range((d + 3) // 4):
-            c = 4 * ks + g_of
-            B.append(np.where(c < d, T[R0 + c, i_of], 0.0))
+        d, R0 = 2 * l + 1, l * l
+        A, B = [], []
+        for t in range(jtiles(l)):
+            nk = jnk4(l, t)
+            A.append(img[joff(l, t):joff(l, t) + 64 * nk].reshape(64, nk))
+            Bt = []
+            for ks in range(jsteps(l, t)):
+                if l < CLASS_L:
+                    c = 4 * ks + g_of
+                    Bt.append(np.where(c < d, T[R0 + c, i_of], 0.0))
+                else:
+                    cb = 2 * gh + np.where(gp == 1, start(l, t, 1, False), start(l, t, 0, False))
+                    v = T[R0 + cb + 4 * ks, i_of]
+                    ok = 2 * ks + gh < np.where(gp == 1, jtcols(l, t, 1), jtcols(l, t, 0))
+                    Bt.append(np.where(ok, v, 0.0))
+            B.append(Bt)
         return A, B
 
     def mma(l, A, B):
-        return [sum(mfma(A[mt][:, ks], B[ks], np.zeros((16, 16))) for ks in range(len(B))) for mt in range(nm(l))]
+        return [sum(mfma(A[t][:, ks], B[t][ks], np.zeros((16, 16))) for ks in range(len(B[t])))
+                for t in range(jtiles(l))]
 
     def store(l, acc):
         d, R0 = 2 * l + 1, l * l
-        for mt in range(nm(l)):
+        for t in range(jtiles(l)):
             for r in range(4):
-                row = 16 * mt + np.array([jrow(4 * g + r) for g in g_of])
-                v = acc[mt][4 * g_of + r, i_of]
-                if l in (1, L) and 16 * mt + 15 >= d:
-                    tgt = np.where(row < d, R0 + row, 289)
+                v = acc[t][4 * g_of + r, i_of]
+                if l < CLASS_L:
+                    row = np.array([jrow(4 * g + r) for g in g_of])
+                    tgt = np.where(row < d, R0 + row, 289) if l == 1 else R0 + row
                 else:
-                    tgt = R0 + row
+                    rb = 8 * gh + np.where(gp == 1, start(l, t, 1, True), start(l, t, 0, True))
+                    ok = 4 * gh + r < np.where(gp == 1, jtrows(l, t, 1), jtrows(l, t, 0))
+                    tgt = np.where(ok, R0 + rb + 2 * r, 289)
                 assert tgt.max() <= 289
                 T[tgt, i_of] = v
 
