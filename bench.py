@@ -647,6 +647,10 @@ def main():
         metric = "Gaunt TP backward (dx1 and dx2) (b,c)-products/sec; % MFMA/ALU roofline per launch on 1 MI355X"
         desc["workload"] = "backward of " + desc["workload"] + "; dy ~ N(0,1)"
         desc["launches_per_step"] = 2
+    if "L1" in desc and args.workload != "mix":
+        # the degrees the workload runs at (the headline's L = 6 otherwise)
+        l1, l2, lo = desc["L1"], desc["L2"], desc["Lout"]
+        metric = metric.replace("at L=6", f"at L={l1}" if l1 == l2 == lo else f"at (L1,L2,Lout)=({l1},{l2},{lo})")
     line = {"metric": metric, "value": value, "unit": "products/s", "n_gpus": 1, "steps": args.steps,
             "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": desc,
