@@ -920,6 +920,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
       constexpr int it = decltype(IT)::value;
       er[it] = (lane + 64 * it < NROW) ? er_tab[64 * it + lane] : 0;
     });
+    // ---- 4. theta analysis over this pass's pairs (lane-permuted weights):
+    // the weights of the pole rows and of the first WQ row blocks are read
+    // before the moments are stored (the table is read-only), the later
+    // blocks WQ blocks ahead of their use (every lane reads: the table holds
+    // all 64 lanes of every block)
+    constexpr int WQ = 3;
+    const int wbase = pu * (NIT + 1) * 64 * 32;
+    float4 wq[WQ][2];
+    cfor<0, (WQ < NIT ? WQ : NIT)>([&](auto IT) {
+      constexpr int it = decltype(IT)::value;
+      wq[it][0] = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
+      wq[it][1] = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
+    });
+    const float4 wz0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
+    const float4 wz1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
     if constexpr (FFT) {
       __syncthreads();  // the spectra of all 16 column nodes are in LDS
       w.phi_fft(eo, fa, ft);
@@ -928,12 +943,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
     }
     __syncthreads();
 
-    // ---- 4. theta analysis over this pass's pairs (lane-permuted weights)
-    const int wbase = pu * (NIT + 1) * 64 * 32;
     if (lane <= L) {
-      const float4 w0 = tload4_s(WPr, lane * 32, wbase + NIT * 64 * 32);
-      const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + NIT * 64 * 32);
-      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+      const float wv[8] = {wz0.x, wz0.y, wz0.z, wz0.w, wz1.x, wz1.y, wz1.z, wz1.w};
       cfor<0, 8>([&](auto JJ) {
         constexpr int jj = decltype(JJ)::value;
         y0 = fmaf(wv[jj], eo[(lnp & 1) * 8 * NMP2 + jj * NMP2], y0);  // row tri(lane, 0)
@@ -941,9 +952,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
     }
     cfor<0, NIT>([&](auto IT) {
       constexpr int it = decltype(IT)::value;
+      const float4 w0 = wq[it % WQ][0], w1 = wq[it % WQ][1];
+      if constexpr (it + WQ < NIT) {
+        wq[it % WQ][0] = tload4_s(WPr, lane * 32, wbase + (it + WQ) * 64 * 32);
+        wq[it % WQ][1] = tload4_s(WPr, lane * 32 + 16, wbase + (it + WQ) * 64 * 32);
+      }
       if (lane + 64 * it < NROW) {
-        const float4 w0 = tload4_s(WPr, lane * 32, wbase + it * 64 * 32);
-        const float4 w1 = tload4_s(WPr, lane * 32 + 16, wbase + it * 64 * 32);
         const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
         cfor<0, 8>([&](auto JJ) {
           constexpr int jj = decltype(JJ)::value;
@@ -952,7 +966,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
           ys[it] = fmaf(wv[jj], cs.y, ys[it]);
         });
       }
-      if constexpr (it % 3 == 2) __builtin_amdgcn_sched_barrier(0);  // bound the loads in flight
+      __builtin_amdgcn_sched_barrier(0);  // keep the ring's distance
     });
     __syncthreads();  // eo is rewritten by the next pass
   }
