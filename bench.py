@@ -502,10 +502,12 @@ def cpu_baseline(O, inputs, oracle_sample, total, idx_cfg, budget_s=15.0):
 
 def stream_roofs(args, torch, gtp):
     """The HBM roof as the chip reaches it: 1 GiB read-only, write-only and
-    copy sweeps by the library's streaming probes (16-byte accesses,
-    non-temporal stores), and torch's device copy, each timed with HIP events
-    on the launch stream.  Also the calibration workload of the FETCH_SIZE /
-    WRITE_SIZE counters (k_probe_copy moves a known 1 GiB each way)."""
+    copy sweeps and a two-read-one-write sweep (the pair products' mix: 1 GiB
+    read, 0.5 GiB written) by the library's streaming probes (16-byte
+    accesses, non-temporal stores, one contiguous chunk per workgroup), and
+    torch's device copy, each timed with HIP events on the launch stream.
+    Also the calibration workload of the FETCH_SIZE / WRITE_SIZE counters
+    (k_probe_copy moves a known 1 GiB each way)."""
     nbytes = 1 << 30
     dev = torch.device("cuda:0")
     src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
@@ -516,6 +518,7 @@ def stream_roofs(args, torch, gtp):
     probes = [("read", lambda: gtp.gtp_stream_probe(0, src, sink), nbytes),
               ("write", lambda: gtp.gtp_stream_probe(1, None, dst), nbytes),
               ("copy", lambda: gtp.gtp_stream_probe(2, src, dst), 2 * nbytes),
+              ("read2_write1", lambda: gtp.gtp_stream_probe(3, src, dst), nbytes + nbytes // 2),
               ("torch_copy", lambda: dst.copy_(src), 2 * nbytes)]
     for name, fn, moved in probes:
         for _ in range(args.warmup):

@@ -269,10 +269,14 @@ gtp_status gtp_sh_filter(int L, const float *r, const float *h, int64_t B, int64
                          void *stream);
 
 /* HBM streaming probe (measurement aid: the roof the HBM-bound kernels are
- * read against).  mode 0: read nbytes of src (dst: a device float written
- * only if the data holds a NaN); 1: write nbytes to dst (non-temporal
- * stores); 2: copy nbytes from src to dst (non-overlapping).  Device
- * pointers 16-byte aligned, nbytes >= 0 a multiple of 16. */
+ * read against; each workgroup streams one contiguous chunk, the chunks
+ * dealt to the XCDs in contiguous runs).  mode 0: read nbytes of src (dst: a
+ * device float written only if the data holds a NaN); 1: write nbytes to dst
+ * (non-temporal stores); 2: copy nbytes from src to dst (non-overlapping);
+ * 3: dst = first half of src + second half (two read streams of nbytes / 2,
+ * one written stream of nbytes / 2: the read/write mix of the pair
+ * products; dst must not overlap src).  Device pointers 16-byte aligned,
+ * nbytes >= 0 a multiple of 16 (32 for mode 3). */
 gtp_status gtp_stream_probe(int mode, const void *src, void *dst, int64_t nbytes, void *stream);
 
 /* Number of floats of one per-product public grid: which = 1 or 2 gives the

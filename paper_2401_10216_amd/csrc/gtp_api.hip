@@ -970,12 +970,15 @@ gtp_status gtp_sh_filter(int L, const float* r, const float* h, int64_t B, int64
 }
 
 gtp_status gtp_stream_probe(int mode, const void* src, void* dst, int64_t nbytes, void* stream) {
-  if (mode < 0 || mode > 2) return fail(GTP_ERR_INVALID_ARG, "mode must be 0 (read), 1 (write) or 2 (copy)");
-  if (nbytes < 0 || nbytes % 16) return fail(GTP_ERR_INVALID_ARG, "nbytes must be a non-negative multiple of 16");
+  if (mode < 0 || mode > 3)
+    return fail(GTP_ERR_INVALID_ARG, "mode must be 0 (read), 1 (write), 2 (copy) or 3 (two reads, one write)");
+  if (nbytes < 0 || nbytes % (mode == 3 ? 32 : 16))
+    return fail(GTP_ERR_INVALID_ARG, "nbytes must be a non-negative multiple of 16 (32 for mode 3)");
   if (nbytes == 0) return GTP_OK;
   if (!dst || (mode != 1 && !src)) return fail(GTP_ERR_INVALID_ARG, "NULL data pointer");
   if (!aligned(16, src, dst)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
-  if (mode == 2 && ranges_overlap(src, size_t(nbytes), dst, size_t(nbytes)))
+  if ((mode == 2 || mode == 3) &&
+      ranges_overlap(src, size_t(nbytes), dst, size_t(mode == 3 ? nbytes / 2 : nbytes)))
     return fail(GTP_ERR_INVALID_ARG, "src and dst overlap");
   gtp_status s = check_device();
   if (s != GTP_OK) return s;

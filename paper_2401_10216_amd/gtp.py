@@ -463,10 +463,13 @@ def gtp_sh_filter(L: int, r, h=None, out=None, stream=None):
 
 
 def gtp_stream_probe(mode: int, src, dst, stream=None):
-    """HBM streaming probe: mode 0 reads src (dst: >= 1 float), 1 writes dst, 2 copies src to dst."""
+    """HBM streaming probe: mode 0 reads src (dst: >= 1 float), 1 writes dst, 2 copies src to dst,
+    3 writes the sum of src's two halves to dst (>= half of src)."""
     nbytes = (dst if mode == 1 else src).numel() * (dst if mode == 1 else src).element_size()
     if mode == 2 and dst.numel() * dst.element_size() < nbytes:
         raise ValueError("dst smaller than src")
+    if mode == 3 and dst.numel() * dst.element_size() < nbytes // 2:
+        raise ValueError("dst smaller than half of src")
     sp = ctypes.c_void_p(None) if mode == 1 else ctypes.c_void_p(src.data_ptr())
     _check(lib().gtp_stream_probe(mode, sp, ctypes.c_void_p(dst.data_ptr()), nbytes, _stream(stream)))
 

@@ -360,12 +360,14 @@ def test_stream_probe_validation(L):
     a, b = fake(0x100000), fake(0x200000)
     S = ctypes.c_void_p(0)
     INV = gtp.GTP_ERR_INVALID_ARG
-    assert L.gtp_stream_probe(3, a, b, 64, S) == INV
+    assert L.gtp_stream_probe(4, a, b, 64, S) == INV
+    assert L.gtp_stream_probe(3, a, b, 48, S) == INV  # mode 3: a multiple of 32
     assert L.gtp_stream_probe(0, a, b, 20, S) == INV  # not a multiple of 16
     assert L.gtp_stream_probe(0, a, b, -16, S) == INV
     assert L.gtp_stream_probe(0, None, b, 64, S) == INV
     assert L.gtp_stream_probe(1, None, None, 64, S) == INV
     assert L.gtp_stream_probe(2, a, fake(0x100000 + 32), 64, S) == INV  # overlap
+    assert L.gtp_stream_probe(3, a, fake(0x100000 + 32), 64, S) == INV  # dst inside src
     assert L.gtp_stream_probe(2, fake(0x100008), b, 64, S) == INV  # misaligned
     assert L.gtp_stream_probe(2, a, b, 0, S) == gtp.GTP_OK
 

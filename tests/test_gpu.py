@@ -1048,3 +1048,29 @@ def test_weighted_backward_subsets_and_empty():
     e = gtp.gtp_full_weighted_backward(plan, dev(z), dev(z), dev(z), need=("dw1", "dwout"), per_channel=True)
     torch.cuda.synchronize()
     assert e["dw1"].shape == (C, L + 1) and not e["dw1"].cpu().numpy().any() and not e["dwout"].cpu().numpy().any()
+
+
+@pytest.mark.parametrize("nfloats", [8, 1000, 4096 * 37 + 12, (1 << 22) + 8])
+def test_stream_probe_results(nfloats):
+    """The streaming probes move what they claim (ragged sizes: partial
+    chunks and chunks past the end): the copy is exact, the write fills the
+    pattern (1, 2, 3, 4), the two-stream read writes the sum of the halves,
+    and the read leaves its NaN-only sink untouched on finite data."""
+    _say(f"stream probe n={nfloats}")
+    n = nfloats - nfloats % 8
+    src = torch.arange(n, dtype=torch.float32, device="cuda") * 0.5 - 7.0
+    dst = torch.full((n,), -1.0, device="cuda")
+    gtp.gtp_stream_probe(2, src, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    gtp.gtp_stream_probe(1, None, dst)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, torch.tensor([1.0, 2.0, 3.0, 4.0], device="cuda").repeat(n // 4))
+    half = torch.full((n // 2,), -1.0, device="cuda")
+    gtp.gtp_stream_probe(3, src, half)
+    torch.cuda.synchronize()
+    assert torch.equal(half, src[: n // 2] + src[n // 2:])
+    sink = torch.zeros(1, device="cuda")
+    gtp.gtp_stream_probe(0, src, sink)
+    torch.cuda.synchronize()
+    assert sink.item() == 0.0
