@@ -26,8 +26,8 @@
 //   poles        (only m = 0 is non-zero there) on the VALU;
 //   rotate out   y = Z(alpha) J^T Z(beta) J y'.
 // One workgroup per (edge, 64 channels), one wave per 16 channels; LDS holds
-// each wave's coefficient tile [k][16 channels] (74.5 KB: two workgroups per CU)
-// and the edge's trig values.
+// each wave's coefficient tile (16 channels x 289 coefficients, channel-major:
+// 74.5 KB per workgroup, two workgroups per CU) and the edge's trig values.
 #include <type_traits>
 
 #include "gtp_ct.hpp"
@@ -206,9 +206,9 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 
   // rows l^2 + l + m and l^2 + l - m and the trig entry m are the lane
   // group's base plus a constant.  A lane past the degree (m > l, in the
   // last step of a degree, l >= 2) reads rows of blocks l + 1 and l - 1 and
-  // writes the spare row, so every row of the tile is read and written by
-  // one step of one lane and the steps may run in any order.  Degree 1 (one
-  // pair) is turned by every lane group alike.
+  // writes the spare row, so every row of the tile is written once, by the
+  // lane that read it in the same step, and the steps may run in any order.
+  // Degree 1 (one pair) is turned by every lane group alike.
   auto zrot = [&](auto AB, auto SGN) {
     constexpr int ab = decltype(AB)::value, sgn = decltype(SGN)::value;
     const int gz = opaque(g);
