@@ -505,7 +505,9 @@ def stream_roofs(args, torch, gtp):
     copy sweeps and a two-read-one-write sweep (the pair products' mix: 1 GiB
     read, 0.5 GiB written) by the library's streaming probes (16-byte
     accesses, non-temporal stores, one contiguous chunk per workgroup), and
-    torch's device copy, each timed with HIP events on the launch stream.
+    torch's device copy, each timed with HIP events on the launch stream;
+    then the fp32 rates the chip delivers under load (the library's compute
+    probes: VALU FMA chains and 16x16x4 MFMA chains, 8 waves per SIMD).
     Also the calibration workload of the FETCH_SIZE / WRITE_SIZE counters
     (k_probe_copy moves a known 1 GiB each way)."""
     nbytes = 1 << 30
@@ -520,7 +522,7 @@ def stream_roofs(args, torch, gtp):
               ("copy", lambda: gtp.gtp_stream_probe(2, src, dst), 2 * nbytes),
               ("read2_write1", lambda: gtp.gtp_stream_probe(3, src, dst), nbytes + nbytes // 2),
               ("torch_copy", lambda: dst.copy_(src), 2 * nbytes)]
-    for name, fn, moved in probes:
+    def timed(fn):
         for _ in range(args.warmup):
             fn()
         ev0 = torch.cuda.Event(enable_timing=True)
@@ -531,9 +533,18 @@ def stream_roofs(args, torch, gtp):
             fn()
         ev1.record(stream)
         torch.cuda.synchronize()
-        ms = ev0.elapsed_time(ev1) / args.steps
+        return ev0.elapsed_time(ev1) / args.steps
+
+    for name, fn, moved in probes:
+        ms = timed(fn)
         out[name] = {"ms": round(ms, 4), "GBps": round(moved / (ms * 1e-3) / 1e9, 1),
                      "frac_of_8TBps": round(moved / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
+    # the fp32 rates under load (VALU FMA chains, 16x16x4 MFMA chains)
+    for name, mode, iters in (("valu_fma_f32", 0, 1 << 14), ("mfma_f32", 1, 1 << 12)):
+        flops = gtp.gtp_compute_probe(mode, iters, sink)
+        ms = timed(lambda: gtp.gtp_compute_probe(mode, iters, sink))
+        out[name] = {"ms": round(ms, 4), "TFLOPs": round(flops / (ms * 1e-3) / 1e12, 2),
+                     "frac_of_157_3": round(flops / (ms * 1e-3) / 1e12 / PEAK_FP32_TFLOPS, 4)}
     print(json.dumps(out), flush=True)
 
 

@@ -279,6 +279,15 @@ gtp_status gtp_sh_filter(int L, const float *r, const float *h, int64_t B, int64
  * nbytes >= 0 a multiple of 16 (32 for mode 3). */
 gtp_status gtp_stream_probe(int mode, const void *src, void *dst, int64_t nbytes, void *stream);
 
+/* Compute probe (measurement aid: the fp32 rates the chip delivers under
+ * load, beside the published peak).  mode 0: fp32 VALU FMA chains (8
+ * independent chains per lane); 1: fp32 v_mfma_f32_16x16x4f32 chains (4
+ * independent accumulators per wave); 2048 workgroups of 256 lanes, iters
+ * steps (1..2^30).  sink: one device float (4-byte aligned), written only if
+ * a result is NaN; *flops (host) receives the flops the launch issues, for
+ * the caller to divide by its own timing of the launch on stream. */
+gtp_status gtp_compute_probe(int mode, int64_t iters, float *sink, double *flops, void *stream);
+
 /* Number of floats of one per-product public grid: which = 1 or 2 gives the
  * input grids (2 * (2L+1)^2), which = 3 the product grid (2 * (2U+1)^2).
  * Returns -1 on a bad argument. */

@@ -986,6 +986,17 @@ gtp_status gtp_stream_probe(int mode, const void* src, void* dst, int64_t nbytes
   return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_stream_probe launch");
 }
 
+gtp_status gtp_compute_probe(int mode, int64_t iters, float* sink, double* flops, void* stream) {
+  if (mode < 0 || mode > 1) return fail(GTP_ERR_INVALID_ARG, "mode must be 0 (VALU FMA) or 1 (MFMA)");
+  if (iters < 1 || iters > (int64_t(1) << 30)) return fail(GTP_ERR_INVALID_ARG, "iters must be in 1..2^30");
+  if (!sink || !flops) return fail(GTP_ERR_INVALID_ARG, "NULL pointer");
+  if (!aligned(4, sink)) return fail(GTP_ERR_INVALID_ARG, "misaligned pointer");
+  gtp_status s = check_device();
+  if (s != GTP_OK) return s;
+  const hipError_t e = gtp::launch_compute_probe(mode, iters, sink, flops, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_compute_probe launch");
+}
+
 int64_t gtp_grid_floats(gtp_plan p, int which) {
   if (!p || which < 1 || which > 3) return -1;
   const int64_t L = which == 1 ? p->L1 : (which == 2 ? p->L2 : p->L1 + p->L2);

@@ -1,5 +1,5 @@
-// Streaming probes of the HBM roof (measurement aids, not part of the
-// product): a read-only sweep, a write-only sweep, a copy and a two-stream
+// Streaming probes of the HBM roof and compute probes of the fp32 VALU and
+// matrix-core rates (measurement aids, not part of the product).  Streaming: a read-only sweep, a write-only sweep, a copy and a two-stream
 // read with one written stream (the read/write mix of the pair products),
 // moving 16 bytes per lane per access (global_load_dwordx4; non-temporal
 // global_store_dwordx4, which does not keep the written lines in the caches).
@@ -82,7 +82,66 @@ __global__ __launch_bounds__(kProbeBlock) void k_probe_copy(const v4f* __restric
   }
 }
 
+// Compute probes: the fp32 rates the chip delivers under load (the shader
+// clock under full load sits below the 2.4 GHz of the published peak).
+// VALU: every lane runs kFmaChains independent chains a = a b + c (plain
+// fp32 FMA, all operands in vector registers: an operand in a scalar
+// register halves the issue rate); MFMA: every wave runs kMfmaChains
+// independent accumulations of v_mfma_f32_16x16x4f32.  The results are
+// written to sink only if they are NaN (never, for the values used), so the
+// chains cannot be dropped.
+constexpr int kFmaChains = 8;
+constexpr int kMfmaChains = 4;
+typedef float f4p __attribute__((ext_vector_type(4)));
+
+__global__ __launch_bounds__(kProbeBlock) void k_probe_fma(float* __restrict__ sink, int64_t iters) {
+  float b = 0.999f, c = 0.001f;
+  asm volatile("" : "+v"(b), "+v"(c));  // vector operands
+  float a[kFmaChains];
+#pragma unroll
+  for (int k = 0; k < kFmaChains; ++k) a[k] = 1e-3f * float(threadIdx.x) + float(k);
+#pragma unroll 8
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < kFmaChains; ++k) a[k] = fmaf(a[k], b, c);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kFmaChains; ++k) s += a[k];
+  if (s != s) sink[0] = s;
+}
+
+__global__ __launch_bounds__(kProbeBlock) void k_probe_mfma(float* __restrict__ sink, int64_t iters) {
+  float a = 1e-3f * float(threadIdx.x & 63), b = 0.5f;
+  asm volatile("" : "+v"(a), "+v"(b));
+  f4p acc[kMfmaChains];
+#pragma unroll
+  for (int k = 0; k < kMfmaChains; ++k) acc[k] = f4p{0.0f, 0.0f, 0.0f, 0.0f};
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int k = 0; k < kMfmaChains; ++k) acc[k] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[k], 0, 0, 0);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int k = 0; k < kMfmaChains; ++k) s += (acc[k][0] + acc[k][1]) + (acc[k][2] + acc[k][3]);
+  if (s != s) sink[0] = s;
+}
+
 }  // namespace
+
+// 2048 workgroups of 256 lanes: 8 waves per SIMD.  Returns the flops issued.
+hipError_t launch_compute_probe(int mode, int64_t iters, float* sink, double* flops, hipStream_t s) {
+  constexpr unsigned kGroups = 2048;
+  const double waves = double(kGroups) * (kProbeBlock / 64);
+  if (mode == 0) {
+    *flops = waves * 64.0 * double(iters) * kFmaChains * 2.0;
+    hipLaunchKernelGGL(k_probe_fma, dim3(kGroups), dim3(kProbeBlock), 0, s, sink, iters);
+  } else {
+    *flops = waves * double(iters) * kMfmaChains * (16.0 * 16.0 * 4.0 * 2.0);
+    hipLaunchKernelGGL(k_probe_mfma, dim3(kGroups), dim3(kProbeBlock), 0, s, sink, iters);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_stream_probe(int mode, const void* src, void* dst, int64_t nbytes, hipStream_t s) {
   // mode 3 reads two streams of nbytes / 2 (the halves of src) and writes one

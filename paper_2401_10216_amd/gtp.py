@@ -56,6 +56,7 @@ _SIGS = {
     "gtp_selfproduct": (_I, [_I, _I, _I, _U, _P, _I, _I64, _I64, _P, _P]),
     "gtp_sh_filter": (_I, [_I, _P, _P, _I64, _I64, _P, _P]),
     "gtp_stream_probe": (_I, [_I, _P, _P, _I64, _P]),
+    "gtp_compute_probe": (_I, [_I, _I64, _P, _DP, _P]),
     "gtp_grid_floats": (_I64, [_P, _I]),
     "gtp_plan_info": (_I, [_P, ctypes.POINTER(_I64)]),
     "gtp_plan_table": (_I, [_P, _I, _DP, ctypes.POINTER(_I64)]),
@@ -472,6 +473,14 @@ def gtp_stream_probe(mode: int, src, dst, stream=None):
         raise ValueError("dst smaller than half of src")
     sp = ctypes.c_void_p(None) if mode == 1 else ctypes.c_void_p(src.data_ptr())
     _check(lib().gtp_stream_probe(mode, sp, ctypes.c_void_p(dst.data_ptr()), nbytes, _stream(stream)))
+
+
+def gtp_compute_probe(mode: int, iters: int, sink, stream=None) -> float:
+    """fp32 compute probe: mode 0 VALU FMA chains, 1 MFMA chains; returns the flops launched."""
+    ps = _want(sink, "sink", (1,), _f32())
+    fl = ctypes.c_double(0.0)
+    _check(lib().gtp_compute_probe(mode, iters, ps, ctypes.byref(fl), _stream(stream)))
+    return fl.value
 
 
 def gtp_debug_host_pipeline(plan: Plan, x1, x2):

@@ -356,6 +356,20 @@ def test_noalloc_escn_validation(L):
     assert f(q.handle, x, 0, r, h, 2, C - 1, y, S) == INV and b"HOST_ONLY" in L.gtp_last_error()
 
 
+def test_compute_probe_validation(L):
+    sink = fake(0x100000)
+    fl = ctypes.c_double(0.0)
+    INV = gtp.GTP_ERR_INVALID_ARG
+    S = ctypes.c_void_p(0)
+    assert L.gtp_compute_probe(2, 16, sink, ctypes.byref(fl), S) == INV
+    assert L.gtp_compute_probe(-1, 16, sink, ctypes.byref(fl), S) == INV
+    assert L.gtp_compute_probe(0, 0, sink, ctypes.byref(fl), S) == INV
+    assert L.gtp_compute_probe(0, (1 << 30) + 1, sink, ctypes.byref(fl), S) == INV
+    assert L.gtp_compute_probe(0, 16, None, ctypes.byref(fl), S) == INV
+    assert L.gtp_compute_probe(1, 16, sink, None, S) == INV
+    assert L.gtp_compute_probe(1, 16, fake(0x100002), ctypes.byref(fl), S) == INV  # misaligned
+
+
 def test_stream_probe_validation(L):
     a, b = fake(0x100000), fake(0x200000)
     S = ctypes.c_void_p(0)

@@ -1074,3 +1074,17 @@ def test_stream_probe_results(nfloats):
     gtp.gtp_stream_probe(0, src, sink)
     torch.cuda.synchronize()
     assert sink.item() == 0.0
+
+
+def test_compute_probe_runs():
+    """The compute probes launch, report the flops they issue (2048
+    workgroups of 256 lanes: 8 chains x 2 flops per lane step for the VALU,
+    4 x 2048 per wave step for the matrix cores) and leave the NaN-only sink
+    untouched."""
+    sink = torch.zeros(1, device="cuda")
+    f0 = gtp.gtp_compute_probe(0, 64, sink)
+    f1 = gtp.gtp_compute_probe(1, 64, sink)
+    torch.cuda.synchronize()
+    assert f0 == 2048 * 256 * 64 * 8 * 2
+    assert f1 == 2048 * 4 * 64 * 4 * 2048
+    assert sink.item() == 0.0
