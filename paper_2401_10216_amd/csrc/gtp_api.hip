@@ -19,6 +19,7 @@
 #include "../../include/gtp.h"
 #include "gtp_device.hpp"
 #include "gtp_escn.hpp"
+#include "gtp_probe.hpp"
 #include "gtp_tables.hpp"
 
 struct gtp_plan_ {

@@ -157,14 +157,6 @@ int64_t wgrad_nchunk(int64_t B, int64_t C, int per_channel);
 hipError_t launch_wgrad(const void* a, int a_type, const float* u, float* out, const float* w, int64_t B, int64_t C,
                         int L, int per_channel, float* partial, float* dw, hipStream_t s);
 
-// HBM streaming probes: mode 0 reads nbytes of src (dst receives at most one
-// float), 1 writes nbytes to dst, 2 copies src to dst, 3 writes the sum of
-// src's halves to dst; 16-byte accesses.
-hipError_t launch_stream_probe(int mode, const void* src, void* dst, int64_t nbytes, hipStream_t s);
-// Compute probes: mode 0 fp32 VALU FMA chains, 1 fp32 16x16x4 MFMA chains,
-// iters steps each; *flops receives the flops issued (sink: one device float,
-// written only on NaN).
-hipError_t launch_compute_probe(int mode, int64_t iters, float* sink, double* flops, hipStream_t s);
 // Fused channel mixing for equal degrees 1..8 and Co <= 128 (*supported =
 // false otherwise): pair products and the mix in one kernel, one workgroup
 // per batch entry.  WB: the weights in the blocked layout made by

@@ -10,6 +10,7 @@
 // the chip reaches for each access pattern, against which the HBM-bound
 // kernels are read.
 #include "gtp_device.hpp"
+#include "gtp_probe.hpp"
 
 namespace gtp {
 namespace {
