@@ -360,6 +360,30 @@ def test_edge_workload_full_size_sampled():
     assert err <= TOL
 
 
+def test_edge16_escn_full_size_sampled():
+    """The degree-16 edge workload through the rotated frame (gtp_conv_escn
+    from x1, r, h) at its full launch shape, 8192 edges x 128 channels, the
+    matrix-core rotated-frame kernel: a seeded sample including the last
+    rows, against the oracle's plain product with the SH filter (equal by
+    equivariance)."""
+    B, C, L = 8192, 128, 16
+    _say("edge16 workload: generating inputs")
+    x1, r, h = inputs.edge_inputs(B, C, L, index=7)
+    _say("edge16 workload: gtp_conv_escn B=8192 C=128 L=16")
+    y = gtp.gtp_conv_escn(gtp.Plan(L, L, L), dev(x1), dev(r.astype(np.float32)), dev(h))
+    torch.cuda.synchronize()
+    n = B * C
+    idx = np.unique(np.concatenate([inputs.sample_indices(7, n, 384), np.arange(n - 64, n)]))
+    yf = y.view(n, -1)[torch.from_numpy(idx).cuda()].cpu().numpy()
+    bi, ci = idx // C, idx % C
+    deg = inputs.degree_of_index(L)
+    bref = h[bi, ci][:, deg].astype(np.float64) * O.real_sh_xyz(L, r[bi])
+    ref = oracle_pair(x1[bi, ci].astype(np.float64), bref, L, L, L)
+    err = O.max_rel_err(yf, ref)
+    _say(f"edge16 workload sampled err={err:.3e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("mode", [gtp.GTP_SELF_STEPWISE, gtp.GTP_SELF_FUSED])
 def test_manybody_workload_full(mode):
     cfg = inputs.WORKLOADS["manybody"]
