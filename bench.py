@@ -548,6 +548,43 @@ def stream_roofs(args, torch, gtp):
     print(json.dumps(out), flush=True)
 
 
+def measure_roofs(torch, gtp):
+    """The roofs of this box, measured before the workload's warmup steps by
+    the library's probes (HIP events on the launch stream): the
+    two-reads-one-write stream (1 GiB read, 0.5 GiB written: the byte mix of
+    a product's two inputs and its output) and the fp32 rates under load (VALU
+    FMA chains, 16x16x4 MFMA chains).  About 0.35 s of GPU work; the stream
+    runs last, the load closest to the kernels' own."""
+    nbytes = 1 << 30
+    dev = torch.device("cuda:0")
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty(nbytes // 8, dtype=torch.float32, device=dev)
+    sink = torch.zeros(1, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, warm, reps):
+        for _ in range(warm):
+            fn()
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        ev0.record(stream)
+        for _ in range(reps):
+            fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return ev0.elapsed_time(ev1) / reps
+
+    out = {}
+    for name, mode, iters in (("mfma_f32_TFLOPs", 1, 1 << 12), ("valu_fma_f32_TFLOPs", 0, 1 << 14)):
+        flops = gtp.gtp_compute_probe(mode, iters, sink)
+        ms = timed(lambda: gtp.gtp_compute_probe(mode, iters, sink), 10, 60)
+        out[name] = round(flops / (ms * 1e-3) / 1e12, 2)
+    ms = timed(lambda: gtp.gtp_stream_probe(3, src, dst), 100, 400)
+    out["read2_write1_GBps"] = round((nbytes + nbytes // 2) / (ms * 1e-3) / 1e9, 1)
+    del src, dst
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -556,6 +593,8 @@ def main():
     ap.add_argument("--workload", default="edge")
     ap.add_argument("--L", type=int, default=32)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-roof-probe", action="store_true",
+                    help="skip the same-box roof measurement before the warmup steps")
     ap.add_argument("--conv", choices=["auto", "direct", "generic", "fft", "dft"], default="auto",
                     help="step-2 algorithm for the convolution crossover: auto (the measured fastest), direct "
                          "(fused direct real-form convolution), generic (workgroup-per-product convolution "
@@ -591,6 +630,7 @@ def main():
         return
     step, products, desc, alg_flops, alg_bytes, oracle_sample, idx_cfg = make_workload(args, torch, gtp, inputs)
 
+    measured = None if args.no_roof_probe else measure_roofs(torch, gtp)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -643,6 +683,9 @@ def main():
         else:
             roof = dict(comp, hbm=hbm)
         roof.update({"traffic": tb, "kernel": kname, "kernel_ms": round(kernel_ms, 5)})
+        if measured:
+            # the kernel's HBM rate against the stream of its byte mix on this machine
+            roof["measured"] = dict(measured, hbm_frac_of_measured=round(hbm_gbs / measured["read2_write1_GBps"], 4))
 
     cpu = None
     if not args.no_cpu_baseline:
