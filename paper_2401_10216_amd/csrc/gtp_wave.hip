@@ -34,6 +34,18 @@ __device__ __forceinline__ float ld_in_any(const float* p, int64_t i) { return p
 __device__ __forceinline__ float ld_in_any(const uint16_t* p, int64_t i) {
   return __uint_as_float(uint32_t(p[i]) << 16);
 }
+// Element i of a product's row that starts at the wave-uniform pointer r:
+// the byte offset stays a 32-bit unsigned value, so the access is a scalar
+// base plus one offset register (no 64-bit address arithmetic per lane).
+__device__ __forceinline__ float ld_row(const float* r, unsigned i) {
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(r) + i * 4u);
+}
+__device__ __forceinline__ float ld_row(const uint16_t* r, unsigned i) {
+  return __uint_as_float(uint32_t(*reinterpret_cast<const uint16_t*>(reinterpret_cast<const char*>(r) + i * 2u)) << 16);
+}
+__device__ __forceinline__ void st_row_bytes(float* r, unsigned byte_off, float v) {
+  *reinterpret_cast<float*>(reinterpret_cast<char*>(r) + byte_off) = v;
+}
 
 // One 64-lane wave per product, lane = 16 g + i, i = 8 h + pi.  The phi stage
 // at every theta node is a set of small dense contractions whose operands are
@@ -766,19 +778,21 @@ __device__ __forceinline__ void stage_x(float* xs, const T1* x1, const T2* x2, i
     slot[4 * k4 + 3] = v.w;
   });
   float v1[NXK], v2[NXK];
+  const T1* const r1 = x1 + P * (PAD ? k1 : K);  // this product's rows (wave-uniform)
+  const T2* const r2 = x2 + P * (PAD ? k2 : K);
   cfor<0, NXK>([&](auto KK) {
     constexpr int k = decltype(KK)::value;
     const int e = tid + NTH * k;
     if (NTH * k + NTH - 1 < K || e < K) {
       if constexpr (PAD) {
         // in-bounds index first, then the select: no load past a row's end
-        const float a = ld_in_any(x1, P * k1 + (e < k1 ? e : 0));
-        const float b = ld_in_any(x2, P * k2 + (e < k2 ? e : 0));
+        const float a = ld_row(r1, unsigned(e < k1 ? e : 0));
+        const float b = ld_row(r2, unsigned(e < k2 ? e : 0));
         v1[k] = e < k1 ? a : 0.0f;
         v2[k] = e < k2 ? b : 0.0f;
       } else {
-        v1[k] = ld_in_any(x1, P * K + e);
-        v2[k] = ld_in_any(x2, P * K + e);
+        v1[k] = ld_row(r1, unsigned(e));
+        v2[k] = ld_row(r2, unsigned(e));
       }
     }
   });
@@ -818,6 +832,16 @@ __device__ __forceinline__ void store_out(float* y, int64_t P, int ko, int i, fl
     if (i < ko) y[P * ko + i] = v;
   } else {
     y[P * K + i] = v;
+  }
+}
+// The same from the product's own output row yr (wave-uniform) and the
+// coefficient's byte offset in it.
+template <bool PAD>
+__device__ __forceinline__ void store_row(float* yr, int ko, unsigned byte_off, float v) {
+  if constexpr (PAD) {
+    if (byte_off < 4u * unsigned(ko)) st_row_bytes(yr, byte_off, v);
+  } else {
+    st_row_bytes(yr, byte_off, v);
   }
 }
 // A padded plan's outputs above degree L (when its Lout > L) are zeros.
@@ -860,6 +884,33 @@ __device__ __forceinline__ const int* row_er_table() {
     return kRowEr16.v;
   } else {
     return kRowEr32.v;
+  }
+}
+// Output byte offsets of the same rows: the (l, m) coefficient in the low
+// half, the (l, -m) one in the high half (4 (l^2 + l +- m) < 2^16 for
+// L <= 32); zero past the last row.
+template <int L>
+struct RowOutTab {
+  unsigned v[WGeo<L>::NIT * 64];
+};
+template <int L>
+constexpr RowOutTab<L> make_row_out() {
+  RowOutTab<L> t{};
+  int q = 0;
+  for (int l = 1; l <= L; ++l)
+    for (int m = 1; m <= l; ++m, ++q)
+      t.v[q] = unsigned(4 * (l * l + l + m)) | (unsigned(4 * (l * l + l - m)) << 16);
+  return t;
+}
+__device__ const RowOutTab<16> kRowOut16 = make_row_out<16>();
+__device__ const RowOutTab<32> kRowOut32 = make_row_out<32>();
+template <int L>
+__device__ __forceinline__ const unsigned* row_out_table() {
+  static_assert(4 * ((L + 1) * (L + 1)) <= 65536, "byte offsets must fit 16 bits");
+  if constexpr (L == 16) {
+    return kRowOut16.v;
+  } else {
+    return kRowOut32.v;
   }
 }
 
@@ -984,28 +1035,31 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(FFT ? 1 : 3)
   const float f = p1 * p2 * float(NP);
   const float fN = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 0));  // wave-uniform
   const float fS = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(f), 8));
+  float* const yr = y + P * (PAD ? ko : K);  // this product's output row (wave-uniform)
   if (lane <= L) {
     const int l = lane;
     y0 = fmaf(tload(Wr, wr0), fN + ((l & 1) ? -fS : fS), y0);
     if constexpr (WGT) {
       if (wt.wo) y0 *= wt.wo[weight_row(wt, P) * (L + 1) + l];
     }
-    store_out<PAD, K>(y, P, ko, l * l + l, y0);
+    store_row<PAD>(yr, ko, unsigned(4 * (l * l + l)), y0);
   }
   int ln = lane;
   asm volatile("" : "+v"(ln));
+  const unsigned* const ro_tab = row_out_table<L>();
   cfor<0, NIT>([&](auto IT) {
     constexpr int it = decltype(IT)::value;
     const int q = ln + 64 * it;
     if (q < NROW) {
-      int l, m;
-      row_lm(q, l, m);
+      const unsigned ro = ro_tab[q];
       float wl = 1.0f;
       if constexpr (WGT) {
+        int l, m;
+        row_lm(q, l, m);
         if (wt.wo) wl = wt.wo[weight_row(wt, P) * (L + 1) + l];
       }
-      store_out<PAD, K>(y, P, ko, l * l + l + m, yc[it] * wl);
-      store_out<PAD, K>(y, P, ko, l * l + l - m, ys[it] * wl);
+      store_row<PAD>(yr, ko, ro & 0xffffu, yc[it] * wl);
+      store_row<PAD>(yr, ko, ro >> 16, ys[it] * wl);
     }
   });
   if constexpr (PAD) zero_tail<K>(y, P, ko, lane, 64);
