@@ -161,7 +161,7 @@ def nsh(L):
 # kernel files (build-time constants, their tables)
 SHARED_SOURCES = ["gtp_ct.hpp", "gtp_device.hpp", "gtp_tables.cpp", "gtp_tables.hpp"]
 KERNEL_SOURCES = {
-    "gtp_small.hip": ["gen_small_consts.cpp"],
+    "gtp_small.hip": ["gen_small_consts.cpp", "gtp_small.hpp"],
     "gtp_escn.hip": ["gen_small_consts.cpp", "gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
     "gtp_wave.hip": ["gtp_fft.hpp"],
     "gtp_escn_wave.hip": ["gtp_escn.hpp", "gtp_escn_tables.cpp", "gtp_escn_tables.hpp"],
@@ -183,6 +183,13 @@ def padded_kernel(L1: int, L2: int, Lout: int):
         return f"k_full_small_pad<{A}>", "alu", "gtp_small.hip"
     W = 16 if A <= 16 else (32 if A <= 32 else 64)
     return ("k_full_wave4" if W > 32 else "k_full_wave") + f" (padded to L = {W})", "mfma", "gtp_wave.hip"
+
+
+def fused_backward(degrees, conv: str = "auto") -> bool:
+    """Whether gtp_full_backward computes both gradients in one launch
+    (k_bwd_small: equal degrees 1..7 on the thread-per-product kernel)."""
+    return (degrees is not None and degrees[0] == degrees[1] == degrees[2] and 1 <= degrees[0] <= 7
+            and conv not in ("generic", "direct"))
 
 
 def dominant_kernel(workload: str, L: int, escn: bool = False, conv: str = "auto", degrees=None):
@@ -645,16 +652,25 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    # average launch duration on the launch stream (a backward step is two
-    # launches of the same kernel, one per input gradient)
-    launches = 2 if args.backward else 1
+    # average launch duration on the launch stream (a backward step is one
+    # launch for both gradients at equal degrees up to 7, else two launches
+    # of the forward kernel, one per input gradient)
+    degs = (desc["L1"], desc["L2"], desc["Lout"]) if "L2" in desc else None
+    fused = args.backward and fused_backward(degs, args.conv)
+    launches = 2 if args.backward and not fused else 1
     if args.weighted and alg_flops:
         # one multiply per input and output coefficient on top of the product
         alg_flops = (alg_flops[0] + 3 * nsh(desc["L1"]), alg_flops[1])
     if args.backward and alg_flops:
-        # per launch: dy (fp32) and one input in, one gradient out (equal degrees)
+        # per launch (equal degrees): dy (fp32) and one input in, one gradient
+        # out; fused: dy and both inputs in, both gradients out, two products
         K = nsh(desc["L1"])
-        alg_bytes = (4 + (2 if desc.get("in_dtype") == "bf16" else 4) + 4) * K
+        es = 2 if desc.get("in_dtype") == "bf16" else 4
+        if fused:
+            alg_bytes = (4 + 2 * es + 2 * 4) * K
+            alg_flops = (2 * alg_flops[0], alg_flops[1] and 2 * alg_flops[1])
+        else:
+            alg_bytes = (4 + es + 4) * K
     kernel_ms = ev0.elapsed_time(ev1) / args.steps / launches
     value = products * args.steps / wall
 
@@ -662,9 +678,10 @@ def main():
     if alg_flops:
         alg_flops, survey_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
-        degs = (desc["L1"], desc["L2"], desc["Lout"]) if "L2" in desc else None
         kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn, args.conv,
                                              degs)
+        if fused:
+            kname = "k_bwd_small"
         suffix = "_backward" if args.backward else ("_weighted" if args.weighted else ("_escn" if args.escn else ""))
         if args.conv != "auto":
             suffix += "_" + args.conv
@@ -703,7 +720,7 @@ def main():
     if args.backward:
         metric = "Gaunt TP backward (dx1 and dx2) (b,c)-products/sec; % MFMA/ALU roofline per launch on 1 MI355X"
         desc["workload"] = "backward of " + desc["workload"] + "; dy ~ N(0,1)"
-        desc["launches_per_step"] = 2
+        desc["launches_per_step"] = launches
     if "L1" in desc and args.workload != "mix":
         # the degrees the workload runs at (the headline's L = 6 otherwise)
         l1, l2, lo = desc["L1"], desc["L2"], desc["Lout"]

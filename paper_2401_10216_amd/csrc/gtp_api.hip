@@ -20,6 +20,7 @@
 #include "gtp_device.hpp"
 #include "gtp_escn.hpp"
 #include "gtp_probe.hpp"
+#include "gtp_small.hpp"
 #include "gtp_tables.hpp"
 
 struct gtp_plan_ {
@@ -701,6 +702,13 @@ gtp_status gtp_full_backward(gtp_plan p, const void* x1, const void* x2, gtp_dty
   const unsigned conv = p->flags & 3u;  // the same request for the gradient plans
   const hipStream_t st = static_cast<hipStream_t>(stream);
   const int it = in_dtype == GTP_BF16 ? gtp::IN_BF16 : gtp::IN_F32;
+  if (dx1 && dx2 && p->L1 == p->L2 && p->L2 == p->Lout && !p->force_generic && p->conv != GTP_CONV_DIRECT) {
+    // equal degrees 1..8 (the thread-per-product kernel's): both gradients
+    // in one launch that reads dy once
+    bool done = false;
+    const hipError_t e = gtp::launch_bwd_small(p->L1, dy, x1, x2, it, n, dx1, dx2, st, &done);
+    if (done) return e == hipSuccess ? GTP_OK : hip_fail(e, "gtp_full_backward launch");
+  }
   if (dx1) {
     gtp_plan q = p;  // the plan's own tables when (Lout, L2, L1) = (L1, L2, Lout)
     if (p->Lout != p->L1 && (s = cached_plan(p->Lout, p->L2, p->L1, conv, &q)) != GTP_OK) return s;

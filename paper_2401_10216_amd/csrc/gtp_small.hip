@@ -17,6 +17,7 @@
 
 #include "gtp_ct.hpp"
 #include "gtp_device.hpp"
+#include "gtp_small.hpp"
 
 // Scheduling fence between the per-node stages: keeps the two mirror nodes
 // from being interleaved (which costs registers) and keeps the table
@@ -586,9 +587,8 @@ __device__ __forceinline__ void load_rows(const TIn* __restrict__ x, int64_t p0,
 
 template <int KO, int KE>
 __device__ __forceinline__ void store_rows(float* __restrict__ y, int64_t p0, int cnt, float* tile,
-                                           const float (&acc)[KE]) {
+                                           const float (&acc)[KE], int tid = threadIdx.x) {
   constexpr int SO = lds_stride(KO);
-  const int tid = threadIdx.x;
   cfor<0, KO>([&](auto I) {
     constexpr int i = decltype(I)::value;
     tile[tid * SO + i] = (i < KE) ? acc[i < KE ? i : 0] : 0.0f;
@@ -632,6 +632,40 @@ __device__ __forceinline__ void scale_by_degree(const float* __restrict__ wrow, 
   cfor<0, K>([&](auto I) { at(I) *= wl[cdeg(decltype(I)::value)]; });
 }
 
+// Row tid of a workgroup's products (xr: this lane's row, the last product's
+// for lanes past the end) into the LDS tile, row stride lds_stride(K); each
+// lane later reads only its own row.  fp32 rows of degree 5..7 with a compact
+// tile: when the workgroup is full and the slab is 16-byte aligned (dma), the
+// whole slab x + p0 K by coalesced 16-byte loads straight into LDS (lane
+// q 64 + tid carries floats 4 (q 64 + tid) .. + 3, no registers on the way;
+// the slab is a whole number of 16-byte runs, 64 K floats).  (Measured: 2.4 %
+// faster at L = 6; at L = 4 4 % and at L = 8 1 % slower than the per-lane
+// loads, so degrees 5..7 only.  Staging x1 the same way, through the tile
+// before x2, measured 1 % slower at L = 6.)
+template <int L, bool ALLOW_DMA, typename T>
+__device__ __forceinline__ void stage_tile_rows(float* tile, const T* __restrict__ x, const T* __restrict__ xr,
+                                                int64_t p0, int cnt, int tid, int dma) {
+  constexpr int K = csh(L), S = lds_stride(K);
+  bool staged = false;
+  if constexpr (std::is_same<T, float>::value && ALLOW_DMA && L >= 5 && L <= 7 && S == K) {
+    if (dma && cnt == kTile) {
+      typedef __attribute__((address_space(3))) void lds_void;
+      typedef const __attribute__((address_space(1))) void glb_void;
+      constexpr int NF = kTile * K, NQ = (NF + 255) / 256;
+      const float* const slab = x + p0 * K;
+      cfor<0, NQ>([&](auto Q) {
+        constexpr int q = decltype(Q)::value;
+        const int e = (q * 64 + tid) * 4;
+        if (q + 1 < NQ || e < NF)
+          __builtin_amdgcn_global_load_lds((glb_void*)(slab + e), (lds_void*)(tile + q * 256), 16, 0, 0);
+      });
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the whole wave's rows are in LDS
+      staged = true;
+    }
+  }
+  if (!staged) cfor<0, K>([&](auto I) { tile[tid * S + decltype(I)::value] = ld_in(xr, decltype(I)::value); });
+}
+
 template <int L1, int L2, int LO, int NU, typename T1, typename T2, bool WGT, bool OUT>
 __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L1, L2, LO)))) void k_full_small(const T1* __restrict__ x1, const T2* __restrict__ x2,
                                                       float* __restrict__ y, int64_t n,
@@ -661,34 +695,8 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     const T1* const xr1 = x1 + r1 * K1;
     const T2* const xr2 = x2 + r2 * K2;
     cfor<0, K1>([&](auto I) { xa[decltype(I)::value] = ld_in(xr1, decltype(I)::value); });
-    bool staged = false;
-    // (measured: 2.4 % faster at L = 6; at L = 4 4 % and at L = 8 1 % slower
-    // than the per-lane loads, so degrees 5..7 only.  Staging x1 the same way,
-    // through the tile before x2, measured 1 % slower at L = 6.)
-    // (odd row lengths only: the slab's layout is the compact one)
-    if constexpr (std::is_same<T2, float>::value && !OUT && L2 >= 5 && L2 <= 7 && S2 == K2) {
-      if (dma && cnt == kTile) {
-        // a full workgroup's x2 rows are one contiguous slab laid out as the
-        // tile: coalesced 16-byte loads straight into LDS (lane q 64 + tid
-        // carries floats 4 (q 64 + tid) .. + 3), no registers on the way;
-        // the slab is a whole number of 16-byte runs (64 K2 floats) and the
-        // base is 16-byte aligned (the host checks x2)
-        typedef __attribute__((address_space(3))) void lds_void;
-        typedef const __attribute__((address_space(1))) void glb_void;
-        constexpr int NF = kTile * K2, NQ = (NF + 255) / 256;
-        const float* const slab = x2 + p0 * K2;
-        cfor<0, NQ>([&](auto Q) {
-          constexpr int q = decltype(Q)::value;
-          const int e = (q * 64 + tid) * 4;
-          if (q + 1 < NQ || e < NF)
-            __builtin_amdgcn_global_load_lds((glb_void*)(slab + e), (lds_void*)(tile + q * 256), 16, 0, 0);
-        });
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the whole wave's rows are in LDS
-        staged = true;
-      }
-    }
-    if (!staged)
-      cfor<0, K2>([&](auto I) { tile[tid * S2 + decltype(I)::value] = ld_in(xr2, decltype(I)::value); });
+    // x2 into its tile rows (the pair products' rows are not one slab)
+    stage_tile_rows<L2, !OUT>(tile, x2, xr2, p0, cnt, tid, dma);
     if constexpr (WGT) {
       // each lane scales its own product: x1 in registers, x2 in its tile row
       const int64_t row = weight_row(wt, p0 + tid);
@@ -718,6 +726,47 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
     gtp_core<L1, L2, LO, NU>(A, A, acc, ST, ntS, WT, ntW);
   }
   store_rows<KO, G::KE>(y, p0, cnt, tile, acc);
+}
+
+// Both input gradients of an equal-degree product (the backward of Sec. 3.1's
+// product, L1 = L2 = Lout = L <= 8): dx1 = P_L(GTP(dy, x2)) and then
+// dx2 = P_L(GTP(dy, x1)), each the forward product on the compile-time
+// tables of (L, L, L).  Each lane's dy row is read once and stays in
+// registers for both products; x2, then x1, pass through the one LDS tile,
+// and each gradient leaves through it as the forward's output does.  Against
+// two forward launches this saves dy's second read: five rows move per
+// product instead of six.  The two products run as a loop that is not
+// unrolled, so the core's code is not duplicated.
+template <int L, typename TX>
+__global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_waves(L, L, L)))) void k_bwd_small(
+    const float* __restrict__ dy, const TX* __restrict__ x1, const TX* __restrict__ x2, float* __restrict__ dx1,
+    float* __restrict__ dx2, int64_t n, int dma) {
+  constexpr int K = csh(L), S = lds_stride(K);
+  __shared__ __align__(16) float tile[kTile * S];
+  lds_poison(tile, kTile * S);
+  const int64_t p0 = int64_t(blockIdx.x) * kTile;
+  const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
+  float xd[K], acc[K];
+#pragma unroll 1
+  for (int g = 0; g < 2; ++g) {
+    // The lane's row addresses from an opaque copy of the lane id, rebuilt
+    // in each product rather than held across it, and dy's row read again
+    // for the second product (from L2): neither the reads nor dy's node
+    // syntheses, the same in both products, are hoisted out of the loop and
+    // held across it (that would take more registers than the core has).
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int64_t p = p0 + (tid < cnt ? tid : cnt - 1);
+    const float* const dr = dy + p * K;
+    cfor<0, K>([&](auto I) { xd[decltype(I)::value] = dr[decltype(I)::value]; });
+    const TX* const x = g == 0 ? x2 : x1;  // dx1 pairs dy with x2, dx2 with x1
+    float* const out = g == 0 ? dx1 : dx2;
+    stage_tile_rows<L, true>(tile, x, x + p * K, p0, cnt, tid, dma);
+    gtp_core_lit<L>(RegX<K>{xd}, LdsX{tile, tid * S}, acc);
+    __syncthreads();
+    store_rows<K, K>(out, p0, cnt, tile, acc, tid);
+    __syncthreads();  // the stores' tile reads are done before the next rows land there
+  }
 }
 
 // Degree-padded product: a plan of degrees (a, b, c) whose padded degree
@@ -1095,6 +1144,42 @@ hipError_t launch_pad_one(const void* x1, int it1, const void* x2, int it2, int6
     return hipSuccess;
   }
   return hipGetLastError();
+}
+
+template <int L>
+hipError_t launch_bwd_one(const float* dy, const void* x1, const void* x2, int it, int64_t n, float* dx1, float* dx2,
+                          hipStream_t s, bool* supported) {
+  const dim3 grid(unsigned((n + kTile - 1) / kTile)), block(kTile);
+  // 16-byte runs straight into LDS when both input slabs are aligned
+  const int dma = ((reinterpret_cast<uintptr_t>(x1) | reinterpret_cast<uintptr_t>(x2)) % 16) == 0;
+  if (it == IN_F32)
+    hipLaunchKernelGGL((k_bwd_small<L, float>), grid, block, 0, s, dy, static_cast<const float*>(x1),
+                       static_cast<const float*>(x2), dx1, dx2, n, dma);
+  else if (it == IN_BF16)
+    hipLaunchKernelGGL((k_bwd_small<L, uint16_t>), grid, block, 0, s, dy, static_cast<const uint16_t*>(x1),
+                       static_cast<const uint16_t*>(x2), dx1, dx2, n, dma);
+  else {
+    *supported = false;
+    return hipSuccess;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_small(int L, const float* dy, const void* x1, const void* x2, int it, int64_t n, float* dx1,
+                            float* dx2, hipStream_t s, bool* supported) {
+  *supported = true;
+  switch (L) {
+    case 1: return launch_bwd_one<1>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 2: return launch_bwd_one<2>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 3: return launch_bwd_one<3>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 4: return launch_bwd_one<4>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 5: return launch_bwd_one<5>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 6: return launch_bwd_one<6>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    case 7: return launch_bwd_one<7>(dy, x1, x2, it, n, dx1, dx2, s, supported);
+    default: break;  // L = 8: the forward's registers are already all in use; two launches
+  }
+  *supported = false;
+  return hipSuccess;
 }
 
 hipError_t launch_full_small_padded(int L, const void* x1, int it1, int k1, const void* x2, int it2, int k2,

@@ -544,6 +544,40 @@ def test_backward_bf16_inputs(L1, L2, Lout):
     assert e1 <= TOL and e2 <= TOL, (e1, e2)
 
 
+@pytest.mark.parametrize("L,dt", [(1, "f32"), (2, "f32"), (3, "bf16"), (4, "f32"), (5, "f32"), (6, "f32"),
+                                  (6, "bf16"), (7, "f32"), (8, "f32")])
+def test_backward_fused_matches_single_gradients(L, dt):
+    """Both gradients of an equal-degree product (one launch for L <= 7: dy read
+    once) against each gradient asked for alone (one forward launch each on
+    the gradient plan, the same arithmetic): equal bit for bit, and within
+    the tolerance of the oracle on a sample.  Full workgroups (the 16-byte
+    LDS staging of fp32 rows at L = 5..7) and a ragged last one."""
+    n = 64 * 5 + 23
+    rng = np.random.default_rng(400 + L)
+    a, b = (rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32) for _ in range(2))
+    d = rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32)
+    if dt == "bf16":
+        bits1, a = inputs.round_to_bf16(a)
+        bits2, b = inputs.round_to_bf16(b)
+        t1 = torch.from_numpy(bits1.view(np.int16)).cuda().view(torch.bfloat16)
+        t2 = torch.from_numpy(bits2.view(np.int16)).cuda().view(torch.bfloat16)
+    else:
+        t1, t2 = dev(a), dev(b)
+    plan = gtp.Plan(L, L, L)
+    _say(f"backward fused L={L} {dt} n={n}")
+    dx1, dx2 = gtp.gtp_full_backward(plan, t1, t2, dev(d))
+    s1, _ = gtp.gtp_full_backward(plan, t1, t2, dev(d), need_dx2=False)
+    _, s2 = gtp.gtp_full_backward(plan, t1, t2, dev(d), need_dx1=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dx1, s1) and torch.equal(dx2, s2)
+    idx = np.arange(0, n, 5)
+    r1, r2 = oracle_vjp(a[idx], b[idx], d[idx], L, L, L)
+    e1 = O.max_rel_err(dx1.cpu().numpy()[idx], r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy()[idx], r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
 def test_backward_options_and_paths():
     """One gradient at a time, the generic and direct plans, and an empty batch."""
     L = 4
