@@ -747,18 +747,23 @@ __global__ __launch_bounds__(kTile) __attribute__((amdgpu_waves_per_eu(small_wav
   const int64_t p0 = int64_t(blockIdx.x) * kTile;
   const int cnt = int((n - p0) < kTile ? (n - p0) : kTile);
   float xd[K], acc[K];
+  {
+    const int tid = threadIdx.x;
+    const float* const dr = dy + (p0 + (tid < cnt ? tid : cnt - 1)) * K;
+    cfor<0, K>([&](auto I) { xd[decltype(I)::value] = dr[decltype(I)::value]; });
+  }
 #pragma unroll 1
   for (int g = 0; g < 2; ++g) {
-    // The lane's row addresses from an opaque copy of the lane id, rebuilt
-    // in each product rather than held across it, and dy's row read again
-    // for the second product (from L2): neither the reads nor dy's node
-    // syntheses, the same in both products, are hoisted out of the loop and
-    // held across it (that would take more registers than the core has).
+    // dy's values opaque to the compiler in each product (its node
+    // syntheses, the same in both, are not hoisted out of the loop and held:
+    // that would take more registers than the core has), and the lane's row
+    // addresses rebuilt from an opaque copy of the lane id in each product
+    // rather than held across it
+#pragma unroll
+    for (int i = 0; i < K; ++i) asm volatile("" : "+v"(xd[i]));
     int tid = threadIdx.x;
     asm volatile("" : "+v"(tid));
     const int64_t p = p0 + (tid < cnt ? tid : cnt - 1);
-    const float* const dr = dy + p * K;
-    cfor<0, K>([&](auto I) { xd[decltype(I)::value] = dr[decltype(I)::value]; });
     const TX* const x = g == 0 ? x2 : x1;  // dx1 pairs dy with x2, dx2 with x1
     float* const out = g == 0 ? dx1 : dx2;
     stage_tile_rows<L, true>(tile, x, x + p * K, p0, cnt, tid, dma);
