@@ -219,7 +219,10 @@ gtp_status gtp_full_weighted_backward(gtp_plan p, const void *x1, const void *x2
  * are written, not accumulated.  Neither may overlap an input or the other.
  * B*C == 0, or dx1 == dx2 == NULL, is a successful no-op.  Tables for
  * (Lout, L2, L1) and (Lout, L1, L2) are built on first use and cached per
- * device (that first call is synchronous); equal degrees reuse the plan's. */
+ * device (that first call is synchronous); equal degrees reuse the plan's.
+ * With L1 = L2 = Lout <= 7 and both gradients asked for, both come from one
+ * launch that reads dy once (results equal bit for bit to asking for each
+ * gradient alone). */
 gtp_status gtp_full_backward(gtp_plan p, const void *x1, const void *x2, gtp_dtype in_dtype, const float *dy,
                              int64_t B, int64_t C, float *dx1, float *dx2, void *stream);
 
