@@ -58,3 +58,15 @@ def test_formulation_flops_values():
     # never above the FFT-based counts the targets were set with
     for L in (4, 6, 8, 16, 32, 64):
         assert bench.formulation_flops(L, L, L) < bench.SURVEY_FLOPS[L]
+
+
+def test_fused_backward_bookkeeping():
+    """The backward step is one launch exactly where gtp_full_backward takes the
+    one-launch kernel: equal degrees 1..7 on the thread-per-product path."""
+    for L in range(1, 8):
+        assert bench.fused_backward((L, L, L))
+        assert bench.fused_backward((L, L, L), "fft") and bench.fused_backward((L, L, L), "dft")
+        assert not bench.fused_backward((L, L, L), "generic") and not bench.fused_backward((L, L, L), "direct")
+    for degs in ((8, 8, 8), (16, 16, 16), (0, 0, 0), (6, 6, 2), (4, 6, 5), (2, 2, 3)):
+        assert not bench.fused_backward(degs)
+    assert not bench.fused_backward(None)
