@@ -10,7 +10,11 @@ gtp_full over the whole batch.  Prints one JSON line with the throughput in
 with HIP events on the stream it runs on; reported against whichever roof,
 fp32 compute or HBM, the kernel comes closer to, with the other alongside)
 and the fp64 oracle timed on the
-host cores on a bounded sample of the same workload.  --backward times
+host cores on a bounded sample of the same workload.  Before the warmup
+steps the box's roofs are measured with the library's probes (MFMA and VALU
+fp32 rates, the two-reads-one-write HBM stream; --no-roof-probe skips them);
+after the edge workload, the L = 32 degree sweep is timed the same way and
+reported as l32_sweep (--no-l32 skips it).  --backward times
 gtp_full_backward (both input gradients) on the same inputs instead,
 --weighted gtp_full_weighted with per-degree weights.
 """
@@ -592,6 +596,39 @@ def measure_roofs(torch, gtp):
     return out
 
 
+def l32_sweep(args, torch, gtp, inputs):
+    """The degree-32 product measured in the same run as the edge workload:
+    the L = 32 degree sweep (B = 2048 x C = 128 products, iid N(0,1), fp32,
+    the matrix-core kernel k_full_wave<32>), with the same warmup and step
+    counts, after the edge workload's timed region: its kernel time on the
+    launch stream, its fraction of the fp32 peak at the kernel's flop count
+    and its HBM traffic when the committed counters match the sources (its
+    parity with the oracle is the GPU tests')."""
+    sa = argparse.Namespace(**vars(args))
+    sa.workload, sa.L, sa.degrees, sa.products, sa.conv = "sweep", 32, "", 0, "auto"
+    sa.backward = sa.weighted = sa.escn = False
+    step, products, desc, alg_flops, alg_bytes, oracle_sample, idx_cfg = make_workload(sa, torch, gtp, inputs)
+    for _ in range(args.warmup):
+        step()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    kernel_ms = ev0.elapsed_time(ev1) / args.steps
+    achieved = alg_flops[0] * products / (kernel_ms * 1e-3) / 1e12
+    return {"workload": desc["workload"], "kernel": "k_full_wave", "kernel_ms": round(kernel_ms, 5),
+            "products_per_s": products / (kernel_ms * 1e-3),
+            "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "alg_flops_per_product": alg_flops[0],
+                         "traffic": load_traffic("sweep_L32", "gtp_wave.hip"),
+                         "alg_bytes_per_launch": alg_bytes * products}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -602,6 +639,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roof-probe", action="store_true",
                     help="skip the same-box roof measurement before the warmup steps")
+    ap.add_argument("--no-l32", action="store_true",
+                    help="with the edge workload: skip the L = 32 degree sweep measured after it")
     ap.add_argument("--conv", choices=["auto", "direct", "generic", "fft", "dft"], default="auto",
                     help="step-2 algorithm for the convolution crossover: auto (the measured fastest), direct "
                          "(fused direct real-form convolution), generic (workgroup-per-product convolution "
@@ -708,6 +747,9 @@ def main():
     if not args.no_cpu_baseline:
         from oracle import gtp_oracle as O
         cpu = cpu_baseline(O, inputs, oracle_sample, products, idx_cfg)
+    l32 = None
+    if args.workload == "edge" and not (args.backward or args.weighted or args.escn or args.no_l32):
+        l32 = l32_sweep(args, torch, gtp, inputs)
 
     metric = METRIC
     if args.workload == "mix":
@@ -729,6 +771,8 @@ def main():
             "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True,
             "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": desc,
             "roofline": roof, "cpu_baseline": cpu}
+    if l32 is not None:
+        line["l32_sweep"] = l32
     print(json.dumps(line), flush=True)
 
 
