@@ -41,8 +41,8 @@ PEAK_HBM_GBS = 8000.0     # MI355X HBM3E
 # convolution, projection to Lout): the figures the 50 % targets were set
 # with, reported as context only (the kernels run a formulation with fewer
 # flops, whose own count sets the roofline).
-SURVEY_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
-SURVEY_FLOPS_MANYBODY = 2200
+FFT_FORMULATION_FLOPS = {2: 745, 4: 6403, 6: 25785, 8: 71349, 16: 346034, 32: 1549020, 64: 7442286}
+FFT_FORMULATION_FLOPS_MANYBODY = 2200
 
 # Flops per product of the thread-per-product kernel at equal degrees
 # L1 = L2 = Lout = L (fp32 inputs) as it runs: 2 FMA + MUL + ADD per lane (one
@@ -335,9 +335,9 @@ def make_workload(args, torch, gtp, inputs):
             desc["workload"] += "; gtp_conv_escn from (x1, r, h): rotated edge frame, m = 0 filter"
             # per product: rotation in (sum (2l+1)^2 FMA), zonal theta product, rotation out;
             # bytes: x1 and y, h, and the edge vector shared by C channels
-            return step, B * C, desc, (escn_flops(L, C), SURVEY_FLOPS[L]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
+            return step, B * C, desc, (escn_flops(L, C), FFT_FORMULATION_FLOPS[L]), 4 * (2 * nsh(L) + L + 1) + 12.0 / C, \
                 oracle_sample, 2 if w == "edge" else 7
-        return step, B * C, desc, (kernel_flops(L, L, L), SURVEY_FLOPS[L]), 4 * (2 * nsh(L) + nsh(L)), \
+        return step, B * C, desc, (kernel_flops(L, L, L), FFT_FORMULATION_FLOPS[L]), 4 * (2 * nsh(L) + nsh(L)), \
             oracle_sample, 2 if w == "edge" else 7
     if (args.backward or args.weighted) and w not in ("edge", "tiny", "sweep", "highdeg"):
         raise SystemExit("--backward / --weighted apply to the pair workloads (edge, tiny, sweep, highdeg)")
@@ -400,7 +400,7 @@ def make_workload(args, torch, gtp, inputs):
         fl = kernel_flops(L1, L2, Lo)
         if args.conv == "fft" and L1 == L2 == Lo and L in (16, 32, 64):
             fl = fft_variant_flops(L)
-        return step, B * C, desc, (fl, SURVEY_FLOPS.get(L) if (L1, L2, Lo) == (L, L, L) else None), \
+        return step, B * C, desc, (fl, FFT_FORMULATION_FLOPS.get(L) if (L1, L2, Lo) == (L, L, L) else None), \
             in_bytes * (nsh(L1) + nsh(L2)) + 4 * nsh(Lo), oracle_sample, idx_cfg
     if w == "manybody":
         N, C, L, nu, Lout = 1728, 256, 2, 3, 3
@@ -418,7 +418,7 @@ def make_workload(args, torch, gtp, inputs):
 
         desc = {"workload": "manybody: 64 molecules x 27 atoms = 1728 nodes, C=256, L=2, nu=3 stepwise, Lout=3, "
                             "x~N(0,1)/sqrt(2l+1)", "B": N, "C": C, "L": L, "nu": nu, "Lout": Lout, "in_dtype": "f32"}
-        return step, N * C, desc, (STEPWISE_FLOPS_L2_NU3_LOUT3, SURVEY_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), \
+        return step, N * C, desc, (STEPWISE_FLOPS_L2_NU3_LOUT3, FFT_FORMULATION_FLOPS_MANYBODY), 4 * (nsh(L) + nsh(Lout)), \
             oracle_sample, 3
     if w == "mix":
         cfg = inputs.WORKLOADS["mix"]
@@ -662,7 +662,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the Gaunt tensor product shards over (b,c) with no exchange, "
-              "and this build runs on a single MI355X (--gpus 1).", file=sys.stderr)
+              "and the benchmark runs on a single MI355X (--gpus 1).", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -715,7 +715,7 @@ def main():
 
     roof = None
     if alg_flops:
-        alg_flops, survey_flops = alg_flops
+        alg_flops, fft_flops = alg_flops
         achieved = alg_flops * products / (kernel_ms * 1e-3) / 1e12
         kname, bound, ksrc = dominant_kernel(args.workload, desc.get("L1", desc.get("L", 0)), args.escn, args.conv,
                                              degs)
@@ -728,7 +728,7 @@ def main():
         # fp32 peak: packed VALU and dense fp32 MFMA are both 157.3 TFLOP/s on MI355X
         comp = {"bound": bound, "achieved": round(achieved, 3), "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / PEAK_FP32_TFLOPS, 4), "alg_flops_per_product": alg_flops,
-                "survey_flops_per_product": survey_flops}
+                "fft_formulation_flops_per_product": fft_flops}
         hbm_gbs = alg_bytes * products / (kernel_ms * 1e-3) / 1e9
         hbm = {"bound": "hbm", "achieved": round(hbm_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                "frac": round(hbm_gbs / PEAK_HBM_GBS, 4), "alg_bytes_per_product": alg_bytes}

@@ -57,7 +57,7 @@ def test_formulation_flops_values():
         [852, 3996, 9660, 20940, 130572, 910860, 6779916]
     # never above the FFT-based counts the targets were set with
     for L in (4, 6, 8, 16, 32, 64):
-        assert bench.formulation_flops(L, L, L) < bench.SURVEY_FLOPS[L]
+        assert bench.formulation_flops(L, L, L) < bench.FFT_FORMULATION_FLOPS[L]
 
 
 def test_fused_backward_bookkeeping():
