@@ -578,6 +578,42 @@ def test_backward_fused_matches_single_gradients(L, dt):
     assert e1 <= TOL and e2 <= TOL, (e1, e2)
 
 
+@pytest.mark.parametrize("L", [5, 6, 7])
+@pytest.mark.parametrize("off", ["none", "x1", "x2"])
+def test_backward_fused_slab_offsets(L, off):
+    """The one-launch backward stages x2, then x1, as 16-byte slabs straight
+    into LDS only when both are 16-byte aligned; one of them a float off that
+    alignment sends every workgroup to per-lane loads.  Either way the
+    gradients equal the single-gradient launches bit for bit and match the
+    oracle.  4 full workgroups + 37 products."""
+    n = 4 * 64 + 37
+    K = O.nsh(L)
+    rng = np.random.default_rng(500 + 10 * L + len(off))
+    a, b, d = (rng.standard_normal((n, 1, K)).astype(np.float32) for _ in range(3))
+
+    def placed(v, shift):
+        store = torch.zeros(n * K + 4, device="cuda:0")
+        t = store[shift:shift + n * K].view(n, 1, K)
+        t.copy_(dev(v))
+        assert (t.data_ptr() % 16 == 0) == (shift == 0)
+        return t
+
+    t1 = placed(a, 1 if off == "x1" else 0)
+    t2 = placed(b, 1 if off == "x2" else 0)
+    plan = gtp.Plan(L, L, L)
+    _say(f"backward fused slabs L={L} offset={off}")
+    dx1, dx2 = gtp.gtp_full_backward(plan, t1, t2, dev(d))
+    s1, _ = gtp.gtp_full_backward(plan, t1, t2, dev(d), need_dx2=False)
+    _, s2 = gtp.gtp_full_backward(plan, t1, t2, dev(d), need_dx1=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dx1, s1) and torch.equal(dx2, s2)
+    r1, r2 = oracle_vjp(a, b, d, L, L, L)
+    e1 = O.max_rel_err(dx1.cpu().numpy(), r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy(), r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
 def test_backward_options_and_paths():
     """One gradient at a time, the generic and direct plans, and an empty batch."""
     L = 4
