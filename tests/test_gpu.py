@@ -578,6 +578,27 @@ def test_backward_fused_matches_single_gradients(L, dt):
     assert e1 <= TOL and e2 <= TOL, (e1, e2)
 
 
+@pytest.mark.parametrize("n", [1, 63, 64, 65])
+def test_backward_fused_tiny_batches(n):
+    """The one-launch backward on one partial workgroup, exactly one, and one
+    product past it (L = 6: the LDS slab path only for full workgroups)."""
+    L = 6
+    rng = np.random.default_rng(600 + n)
+    a, b, d = (rng.standard_normal((n, 1, O.nsh(L))).astype(np.float32) for _ in range(3))
+    plan = gtp.Plan(L, L, L)
+    _say(f"backward fused tiny n={n}")
+    dx1, dx2 = gtp.gtp_full_backward(plan, dev(a), dev(b), dev(d))
+    s1, _ = gtp.gtp_full_backward(plan, dev(a), dev(b), dev(d), need_dx2=False)
+    _, s2 = gtp.gtp_full_backward(plan, dev(a), dev(b), dev(d), need_dx1=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dx1, s1) and torch.equal(dx2, s2)
+    r1, r2 = oracle_vjp(a, b, d, L, L, L)
+    e1 = O.max_rel_err(dx1.cpu().numpy(), r1)
+    e2 = O.max_rel_err(dx2.cpu().numpy(), r2)
+    _say(f"  err dx1={e1:.3e} dx2={e2:.3e}")
+    assert e1 <= TOL and e2 <= TOL, (e1, e2)
+
+
 @pytest.mark.parametrize("L", [5, 6, 7])
 @pytest.mark.parametrize("off", ["none", "x1", "x2"])
 def test_backward_fused_slab_offsets(L, off):
